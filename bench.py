@@ -1,0 +1,235 @@
+#!/usr/bin/env python3
+"""Benchmark of the per-layer OJBKQ quantisation path on one MI355X.
+
+One step = the whole path for one layer: Gram and cross term over every
+calibration token, damping, Cholesky, the two triangular solves, centres,
+Klein temperatures, the batched Babai + K Klein decode of every column and
+the selection, with the synthetic inputs already resident in HBM.
+
+Default workload: the Llama-7B-shaped attention projection, W 4096 x 4096
+(n = 4096 output channels, m = 4096 input features), X_ref / X_q 4096 x
+262144 calibration tokens with heavy-tailed per-channel scales, 4-bit,
+group 128, K = 16 Klein samples, alpha (the JTA knob) = 0.5.
+
+Prints one JSON line.  value = n (K + 1) / layer time, i.e. candidate paths
+(columns x samples) decoded per second, end to end.  The roofline object is
+for the dominant kernel, the fused Gram + cross-term contraction, timed with
+HIP events on the stream it is launched on.  The CPU baseline times the oracle
+on a bounded sample of the same workload on this host and extrapolates.
+"""
+
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "layer quantize time (s) and columns×samples decoded/sec; % MFMA/HBM peak"
+PEAK_F64_MFMA_TFLOPS = 78.6     # MI355X dense fp64 matrix peak
+PEAK_HBM_GBS = 8000.0
+
+
+def log(msg):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def parse():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=5)
+    ap.add_argument("--warmup", type=int, default=1)
+    ap.add_argument("--config", default="c2", help="workload key (c1..c5)")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-tokens", type=int, default=16384,
+                    help="tokens of the oracle's timed Gram/cross sample")
+    ap.add_argument("--cpu-columns", type=int, default=24,
+                    help="columns of the oracle's timed solve/decode sample")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="also run one plain 1 GiB device copy (for scaling HBM counters)")
+    return ap.parse_args()
+
+
+def workload_desc(cfg):
+    return {
+        "workload": f"{cfg.key}: {cfg.title}",
+        "n_out": cfg.n, "m_in": cfg.m, "tokens": cfg.T, "bits": cfg.bits, "group": cfg.group,
+        "K": cfg.K, "alpha": cfg.mu, "lambda_rel": cfg.lambda_rel, "token_chunks": cfg.chunks,
+    }
+
+
+def cpu_baseline(cfg, W, Xr, Xq, tokens, columns):
+    """The oracle as it stands, timed stage by stage on a bounded sample, extrapolated."""
+    import numpy as np
+    from oracle import ojbkq as orc
+    try:
+        from threadpoolctl import threadpool_info
+        blas_threads = max([int(i.get("num_threads", 1)) for i in threadpool_info()] or [1])
+    except Exception:
+        blas_threads = len(os.sched_getaffinity(0))
+    Ts = min(tokens, cfg.T)
+    ns = min(columns, cfg.n)
+    Wn = W[:ns].cpu().numpy()
+    Xrn = Xr[:, :Ts].cpu().numpy()
+    Xqn = Xq[:, :Ts].cpu().numpy()
+    t = {}
+    t0 = time.perf_counter()
+    S, Z = orc.scales_zeros(Wn, cfg.bits, cfg.group)
+    t["scales"] = time.perf_counter() - t0
+    t0 = time.perf_counter()
+    G = orc.gram(Xqn)
+    t["gram"] = time.perf_counter() - t0
+    lam2 = orc.damping(G, cfg.lambda_rel)
+    t0 = time.perf_counter()
+    R = orc.cholesky_upper(G + lam2 * np.eye(cfg.m))
+    t["cholesky"] = time.perf_counter() - t0
+    t0 = time.perf_counter()
+    V = orc.relaxed_solution(Wn, Xrn, Xqn, cfg.mu, lam2, R)
+    t["relaxed"] = time.perf_counter() - t0
+    qb = orc.centres(V, S, Z, cfg.group)
+    t0 = time.perf_counter()
+    orc.decode(R, qb, S, cfg.bits, cfg.group, cfg.K, cfg.klein_seed)
+    t["decode"] = time.perf_counter() - t0
+    sample_s = sum(t.values())
+    tok_x, col_x = cfg.T / Ts, cfg.n / ns
+    # the oracle's relaxed solution forms X~^T y* per column over the tokens
+    layer_s = (t["gram"] * tok_x + t["cholesky"] + t["relaxed"] * tok_x * col_x
+               + (t["decode"] + t["scales"]) * col_x)
+    return {
+        "value": cfg.n * (cfg.K + 1) / layer_s,
+        "unit": "columns*samples/s",
+        "cores": blas_threads,
+        "kind": "oracle",
+        "layer_s_extrapolated": layer_s,
+        "sample_s": sample_s,
+        "stage_s": {k: round(v, 4) for k, v in t.items()},
+        "sample": (f"fp64 numpy oracle on this host: Gram on {Ts} of {cfg.T} tokens "
+                   f"(x{tok_x:g}), damped Cholesky of the full {cfg.m}x{cfg.m} Gram, relaxed "
+                   f"solution over {Ts} tokens for {ns} of {cfg.n} columns (x{tok_x * col_x:g}), "
+                   f"decode of all {cfg.K + 1} candidates of {ns} columns (x{col_x:g}); "
+                   f"layer time extrapolated linearly"),
+    }
+
+
+def main():
+    args = parse()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print(f"bench.py measures one GPU only (asked for --gpus {args.gpus}, WORLD_SIZE {world}): "
+              "the path runs on a single GPU; sharding over columns is described in DESIGN.md",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import paper_2602_08376_amd as ok
+    from synth import CONFIGS
+    from synth.workloads import activation_chunks, make_weights
+
+    cfg = CONFIGS[args.config]
+    dev = torch.device("cuda", 0)
+    torch.cuda.set_device(dev)
+    ok.library()
+    log(f"workload {cfg.key}: {cfg.title}")
+    t0 = time.perf_counter()
+    W = make_weights(cfg, device=dev)
+    chunks = list(activation_chunks(cfg, device=dev))
+    torch.cuda.synchronize()
+    log(f"inputs generated on the GPU in {time.perf_counter() - t0:.1f} s "
+        f"({sum(x.numel() * 8 for x, _ in chunks) / 2**30:.1f} GiB of activations)")
+
+    need = ok.workspace_bytes(cfg.m, cfg.n, cfg.bits, cfg.group, cfg.K, cfg.mu, cfg.lambda_rel,
+                              cfg.klein_seed)
+    ws = torch.empty(need, dtype=torch.uint8, device=dev)
+    stream = torch.cuda.current_stream(dev)
+    log(f"workspace {need / 2**30:.2f} GiB")
+
+    def step(record):
+        s = ok.LayerSolver(cfg.m, cfg.n, cfg.bits, cfg.group, cfg.K, cfg.klein_seed,
+                           cfg.lambda_rel, device=dev, workspace=ws)
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(2 * len(chunks) + 1)]
+        for i, (Xr, Xq) in enumerate(chunks):
+            ev[2 * i].record(stream)
+            s.accumulate(Xr, Xq)              # one gram_cross launch per chunk
+            ev[2 * i + 1].record(stream)
+        out = s.solve(W, cfg.mu)
+        ev[-1].record(stream)
+        s.close()
+        if record is not None:
+            record.append((ev, out))
+        return out
+
+    for w in range(args.warmup):
+        step(None)
+        log(f"warmup step {w + 1}/{args.warmup} done")
+    torch.cuda.synchronize()
+    recs = []
+    t0 = time.perf_counter()
+    for k in range(args.steps):
+        step(recs)
+        log(f"timed step {k + 1}/{args.steps} done")
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ms_step = wall * 1e3 / args.steps
+
+    gc_ms, solve_ms = [], []
+    for ev, _ in recs:
+        for i in range(len(chunks)):
+            gc_ms.append(ev[2 * i].elapsed_time(ev[2 * i + 1]))
+        solve_ms.append(ev[2 * len(chunks) - 1].elapsed_time(ev[-1]))
+    gc_avg = sum(gc_ms) / len(gc_ms)
+    m, T = cfg.m, cfg.T
+    Tc = T // cfg.chunks
+    flops = 3.0 * m * m * Tc          # syrk m^2 Tc (lower half) + cross 2 m^2 Tc per launch
+    achieved = flops / (gc_avg * 1e-3) / 1e12
+    paths = cfg.n * (cfg.K + 1)
+    out = recs[-1][1]
+    result = {
+        "metric": METRIC,
+        "value": paths / (ms_step * 1e-3),
+        "unit": "columns*samples/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_step,
+        "layer_time_s": ms_step * 1e-3,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f64",
+        "data": "synthetic (seeded, generated on the GPU; inputs resident in HBM)",
+        "config": workload_desc(cfg),
+        "stages_ms": {"gram_cross_per_launch": gc_avg,
+                      "rest_of_path": sum(solve_ms) / len(solve_ms)},
+        "roofline": {
+            "bound": "mfma",
+            "kernel": "gram_cross_kernel",
+            "achieved": achieved,
+            "peak": PEAK_F64_MFMA_TFLOPS,
+            "unit": "TFLOP/s",
+            "frac": achieved / PEAK_F64_MFMA_TFLOPS,
+            "traffic": None,
+            "algorithmic_flops_per_launch": flops,
+        },
+        "checks": {"codes_max": int(out.codes.max()),
+                   "mean_winner_is_klein": float((out.winner > 0).float().mean())},
+    }
+    if args.copy_calibration:
+        a = torch.empty(1 << 28, dtype=torch.float32, device=dev)
+        b = torch.empty_like(a)
+        b.copy_(a)
+        torch.cuda.synchronize()
+        result["copy_calibration_bytes"] = a.numel() * 4
+    if not args.no_cpu_baseline:
+        log("timing the CPU oracle on a bounded sample")
+        Xr0, Xq0 = chunks[0]
+        result["cpu_baseline"] = cpu_baseline(cfg, W, Xr0, Xq0, args.cpu_tokens, args.cpu_columns)
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

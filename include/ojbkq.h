@@ -1,0 +1,164 @@
+/*
+ * ojbkq.h -- C ABI of the MI355X (gfx950) library for OJBKQ's per-layer
+ * quantisation path: the multiple-right-hand-side box-constrained integer
+ * least-squares (BILS) solve of one linear layer.
+ *
+ * Paper: "Objective-Joint Babai-Klein Quantization" (arXiv 2602.08376).
+ * The operation, end to end (Sec. 3.1-3.2, Alg. 1, Eq. klein_prob, Alg. 3,
+ * Alg. 4):
+ *
+ *   scales/zeros  S, Z per (output channel, group of `group` input rows),
+ *                 asymmetric min-max over the group, range widened to hold 0,
+ *                 fixed before the decode (Alg. 1 step 1; Sec. 3.2 data model).
+ *   Gram          H = X~^T X~ + lambda^2 I = R^T R, R upper (Alg. 1 step 2),
+ *                 lambda^2 = lambda_rel * mean(diag(X~^T X~)).
+ *   target        Y*(mu) = (1 - mu) X W + mu X~ W (Eq. jta_target); the real
+ *                 least-squares solution v_j of the stacked problem
+ *                 (Eq. new_obj) is w_j + (1 - mu) H^-1 X~^T (X - X~) w_j,
+ *                 found with two triangular solves (Alg. 1 step 3), and the
+ *                 real centre is qbar_j = v_j / s_j + z_j (Alg. 1 step 4).
+ *   decode        per column j, K + 1 candidate code vectors against the
+ *                 shared factor: candidate 0 is the box-clamped Babai
+ *                 nearest-plane point (Alg. 1 steps 6-10), candidates 1..K
+ *                 are Klein draws with Pr(q_i = v) proportional to
+ *                 exp(-alpha_j Rbar_ii^2 (c_i - v)^2), v in the box
+ *                 (Eq. klein_prob, Alg. 3), alpha_j = ln(rho) / min_i Rbar_ii^2
+ *                 with K = (e rho)^(2m/rho) (the temperature rule stated after
+ *                 Eq. klein_prob), Rbar_j = R diag(s_j).
+ *   selection     the candidate with the smallest reduced residual
+ *                 ||Rbar_j (q - qbar_j)||^2 (the JTA score of Eq. jta_score
+ *                 minus the column's least-squares floor); first strict
+ *                 minimum wins, so the Babai point wins ties (Alg. 4).
+ *
+ * Conventions shared by every entry point
+ *   - Layouts (row-major, the PyTorch nn.Linear convention):
+ *       W      [n, m] float32  (row j = the paper's column w_j)
+ *       X_ref  [m, T] float32  (the paper's X^T: full-precision activations)
+ *       X_q    [m, T] float32  (the paper's X~^T: runtime activations)
+ *       codes  [n, m] uint8    (values 0 .. 2^bits - 1)
+ *       scales [n, G] float32, zeros [n, G] float32 (integer-valued),
+ *              G = ceil(m / g), g = group (<= 0 or >= m: g = m)
+ *       residuals [n] float64, winner [n] int32 (0 = Babai candidate)
+ *   - Every array pointer is a DEVICE pointer owned by the caller; the library
+ *     never allocates device memory.  All scratch comes from the caller's
+ *     `workspace` (device memory, at least the size reported by the matching
+ *     *_workspace_bytes call, any alignment of 256 bytes or more).
+ *   - `stream` is a hipStream_t (NULL = the default stream).  Work is enqueued
+ *     on it; every compute entry point synchronises that stream before it
+ *     returns, because it reports a non-positive-definite Gram (a device-side
+ *     condition) through its return code.
+ *   - Argument errors return OJBKQ_EINVAL before anything is enqueued.
+ *     Failures carry a message readable with ojbkq_last_error() (per thread).
+ *   - Random draws: Klein draw for row i, column j, candidate k uses
+ *     Philox4x32-10 (Salmon et al., SC'11) with counter (i, j, k, 0) and key
+ *     (seed mod 2^32, seed div 2^32); the uniform in [0, 1) is
+ *     ((x0 >> 5) * 2^26 + (x1 >> 6)) * 2^-53.  Results depend only on the
+ *     inputs and the seed, never on the launch geometry.
+ *   - Calls that share a workspace or a context must not overlap.
+ */
+#ifndef OJBKQ_H
+#define OJBKQ_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  OJBKQ_OK = 0,
+  OJBKQ_EINVAL = -1,   /* bad argument (nothing was enqueued)                 */
+  OJBKQ_ENOSPACE = -2, /* workspace smaller than the *_workspace_bytes figure */
+  OJBKQ_ENOTPD = -3,   /* damped Gram not positive definite (Alg. 1 step 2);
+                          outputs are undefined, ojbkq_last_error() names the
+                          first failing pivot                                 */
+  OJBKQ_EHIP = -4,     /* HIP runtime error                                   */
+  OJBKQ_ESTATE = -5    /* staged call out of order                            */
+} ojbkq_status;
+
+typedef struct {
+  int64_t m;           /* input features = lattice dimension (>= 1)           */
+  int64_t n;           /* output channels = independent problems (>= 1)       */
+  int32_t bits;        /* box {0 .. 2^bits - 1}, 1 <= bits <= 8               */
+  int32_t group;       /* rows per scale group; <= 0 or >= m: one group       */
+  int32_t K;           /* Klein samples (>= 0); K + 1 candidates per column   */
+  int32_t reserved;    /* must be 0                                           */
+  double alpha;        /* the JTA knob mu of Eq. jta_target, 0 <= alpha <= 1  */
+  double lambda_rel;   /* lambda^2 = lambda_rel * mean(diag(X~^T X~)), >= 0   */
+  uint64_t seed;       /* Philox key for the Klein draws                      */
+} ojbkq_params;
+
+typedef struct ojbkq_ctx ojbkq_ctx;   /* opaque staged-solve state (host)     */
+
+/* Workspace bytes needed by ojbkq_quantize_layer and the staged calls for
+ * these parameters (independent of the token count).  0 on invalid params. */
+size_t ojbkq_workspace_bytes(const ojbkq_params* p);
+
+/* One-shot layer quantisation (the whole path above, Alg. 1 + Alg. 3 + Alg. 4).
+ *   X_ref, X_q: [m, T] with row stride ldx >= T (elements).  X_ref may be NULL
+ *     or equal to X_q, and is not read when alpha == 1: the cross term
+ *     X~^T (X - X~) then vanishes (Eq. jta_target with X = X~ or mu = 1).
+ *   Outputs: codes, scales, zeros, residuals (required); winner (nullable).
+ * Returns OJBKQ_OK, OJBKQ_EINVAL, OJBKQ_ENOSPACE, OJBKQ_ENOTPD or OJBKQ_EHIP. */
+int ojbkq_quantize_layer(const ojbkq_params* p, const float* W, const float* X_ref,
+                         const float* X_q, int64_t T, int64_t ldx, void* workspace,
+                         size_t workspace_bytes, void* stream, uint8_t* codes, float* scales,
+                         float* zeros, double* residuals, int32_t* winner);
+
+/* Staged form of the same path, for calibration sets streamed in token chunks
+ * (the Gram and cross term are sums over tokens, Alg. 1 step 2-3) and for
+ * several JTA knobs on one Gram (R does not depend on mu).
+ *   create:     binds params, workspace (>= ojbkq_workspace_bytes) and stream;
+ *               *out receives a host-side handle.  Sums start at zero.
+ *   accumulate: adds X_q_c X_q_c^T and X_q_c (X_ref_c - X_q_c)^T of one chunk
+ *               ([m, T_c], row stride ldx).  X_ref_c NULL or == X_q_c adds no
+ *               cross term.  Not allowed after the first solve (ESTATE).
+ *   solve:      damps and factors the accumulated Gram on first use, then runs
+ *               the rest of the path for W [n, m] and knob `alpha` (overrides
+ *               p->alpha).  Output arguments as in ojbkq_quantize_layer.
+ *   destroy:    frees the handle (not the workspace).                       */
+int ojbkq_create(const ojbkq_params* p, void* workspace, size_t workspace_bytes, void* stream,
+                 ojbkq_ctx** out);
+int ojbkq_accumulate(ojbkq_ctx* ctx, const float* X_ref_c, const float* X_q_c, int64_t T_c,
+                     int64_t ldx);
+int ojbkq_solve(ojbkq_ctx* ctx, const float* W, double alpha, uint8_t* codes, float* scales,
+                float* zeros, double* residuals, int32_t* winner);
+int ojbkq_destroy(ojbkq_ctx* ctx);
+
+/* Read-only view of an intermediate of the last staged solve (device pointer
+ * into the workspace, valid until the next call on ctx):
+ *   which = 0: L = R^T, lower triangle of [m, m] float64, strict upper zero
+ *           1: qbar [n, m] float64 (Alg. 1 step 4)
+ *           2: alpha_j [n] float64 (Klein temperature per column)
+ *           3: lambda^2 [1] float64
+ *           4: per-candidate residuals [n, K + 1] float64
+ * Returns EINVAL for an unknown `which`, ESTATE before the first solve.    */
+int ojbkq_inspect(ojbkq_ctx* ctx, int which, const void** ptr);
+
+/* Decode and selection alone (Alg. 1 steps 5-10, Eq. klein_prob, Alg. 4) on a
+ * given factor, for testing the decoder in isolation:
+ *   R [m, m] float64, upper triangular (row-major; the strict lower part is
+ *   ignored), positive diagonal; qbar [n, m] float64; scales [n, G] float32.
+ *   codes/residuals required, winner/path_codes/path_resid nullable:
+ *   path_codes [n, K + 1, m] uint8 and path_resid [n, K + 1] float64 receive
+ *   every candidate.  p->alpha, p->lambda_rel are not used.              */
+size_t ojbkq_decode_workspace_bytes(const ojbkq_params* p);
+int ojbkq_decode_stage(const ojbkq_params* p, const double* R, const double* qbar,
+                       const float* scales, void* workspace, size_t workspace_bytes, void* stream,
+                       uint8_t* codes, double* residuals, int32_t* winner, uint8_t* path_codes,
+                       double* path_resid);
+
+/* ln(rho) where rho > 1 solves K = (e rho)^(2m / rho) (the Klein temperature
+ * rule after Eq. klein_prob).  Host-only, no GPU needed.  K <= 1: +infinity
+ * (greedy rounding); ln K >= 2m: 0 (flat sampling); m < 1: NaN.           */
+double ojbkq_klein_log_rho(int64_t m, int64_t K);
+
+/* Message of the last failure on this thread ("" if none). */
+const char* ojbkq_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* OJBKQ_H */

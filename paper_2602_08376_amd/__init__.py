@@ -1,0 +1,305 @@
+"""MI355X (gfx950) implementation of OJBKQ's per-layer quantisation path.
+
+A thin Python binding over the C ABI of ``include/ojbkq.h`` (``libojbkq.so``
+in this directory).  Only argument marshalling happens here: torch supplies
+device memory and the current stream, every step of the path runs in the HIP
+kernels of the library.  There is no fallback: without the built library
+every call raises.
+"""
+
+from __future__ import annotations
+
+import ctypes
+import math
+import os
+from dataclasses import dataclass
+from typing import Optional
+
+import torch
+
+__all__ = [
+    "OjbkqError", "Params", "library", "library_path", "quantize_layer", "LayerSolver",
+    "decode_stage", "klein_log_rho", "workspace_bytes", "decode_workspace_bytes",
+    "ABI_FUNCTIONS", "QuantResult",
+]
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+library_path = os.path.join(_PKG, "libojbkq.so")
+
+# every entry point of include/ojbkq.h
+ABI_FUNCTIONS = (
+    "ojbkq_workspace_bytes", "ojbkq_quantize_layer", "ojbkq_create", "ojbkq_accumulate",
+    "ojbkq_solve", "ojbkq_destroy", "ojbkq_inspect", "ojbkq_decode_workspace_bytes",
+    "ojbkq_decode_stage", "ojbkq_klein_log_rho", "ojbkq_last_error",
+)
+
+_STATUS = {0: "OK", -1: "EINVAL", -2: "ENOSPACE", -3: "ENOTPD", -4: "EHIP", -5: "ESTATE"}
+
+
+class OjbkqError(RuntimeError):
+    """A library call returned a non-zero status."""
+
+    def __init__(self, status: int, message: str):
+        super().__init__(f"ojbkq {_STATUS.get(status, status)}: {message}")
+        self.status = status
+        self.code = _STATUS.get(status, str(status))
+
+
+class Params(ctypes.Structure):
+    _fields_ = [
+        ("m", ctypes.c_int64), ("n", ctypes.c_int64), ("bits", ctypes.c_int32),
+        ("group", ctypes.c_int32), ("K", ctypes.c_int32), ("reserved", ctypes.c_int32),
+        ("alpha", ctypes.c_double), ("lambda_rel", ctypes.c_double), ("seed", ctypes.c_uint64),
+    ]
+
+
+_lib = None
+
+
+def library() -> ctypes.CDLL:
+    """The loaded HIP library; raises if it has not been built."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(library_path):
+        raise RuntimeError(f"HIP library {library_path} is not built; run "
+                           "`python -m paper_2602_08376_amd.build` (no CPU fallback exists)")
+    lib = ctypes.CDLL(library_path)
+    P, vp, i64, dp = ctypes.POINTER(Params), ctypes.c_void_p, ctypes.c_int64, ctypes.c_double
+    sig = {
+        "ojbkq_workspace_bytes": (ctypes.c_size_t, [P]),
+        "ojbkq_decode_workspace_bytes": (ctypes.c_size_t, [P]),
+        "ojbkq_quantize_layer": (ctypes.c_int, [P, vp, vp, vp, i64, i64, vp, ctypes.c_size_t, vp,
+                                                vp, vp, vp, vp, vp]),
+        "ojbkq_create": (ctypes.c_int, [P, vp, ctypes.c_size_t, vp, ctypes.POINTER(vp)]),
+        "ojbkq_accumulate": (ctypes.c_int, [vp, vp, vp, i64, i64]),
+        "ojbkq_solve": (ctypes.c_int, [vp, vp, dp, vp, vp, vp, vp, vp]),
+        "ojbkq_destroy": (ctypes.c_int, [vp]),
+        "ojbkq_inspect": (ctypes.c_int, [vp, ctypes.c_int, ctypes.POINTER(vp)]),
+        "ojbkq_decode_stage": (ctypes.c_int, [P, vp, vp, vp, vp, ctypes.c_size_t, vp, vp, vp, vp,
+                                              vp, vp]),
+        "ojbkq_klein_log_rho": (ctypes.c_double, [i64, i64]),
+        "ojbkq_last_error": (ctypes.c_char_p, []),
+    }
+    for name, (res, args) in sig.items():
+        fn = getattr(lib, name)
+        fn.restype = res
+        fn.argtypes = args
+    _lib = lib
+    return lib
+
+
+def _check(rc: int):
+    if rc != 0:
+        msg = library().ojbkq_last_error().decode(errors="replace")
+        raise OjbkqError(rc, msg)
+
+
+def _params(m, n, bits, group, K, alpha, lambda_rel, seed) -> Params:
+    return Params(int(m), int(n), int(bits), int(group), int(K), 0, float(alpha),
+                  float(lambda_rel), int(seed) & 0xFFFFFFFFFFFFFFFF)
+
+
+def _ptr(t: Optional[torch.Tensor]):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(device: torch.device):
+    return ctypes.c_void_p(torch.cuda.current_stream(device).cuda_stream)
+
+
+def _need(t: torch.Tensor, name: str, dtype, shape=None, device=None):
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch.Tensor")
+    if t.device.type != "cuda":
+        raise ValueError(f"{name} must be on the GPU (got {t.device})")
+    if t.dtype != dtype:
+        raise ValueError(f"{name} must be {dtype} (got {t.dtype})")
+    if shape is not None and tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name} must have shape {tuple(shape)} (got {tuple(t.shape)})")
+    if device is not None and t.device != device:
+        raise ValueError(f"{name} is on {t.device}, expected {device}")
+
+
+def _rows_view(X: torch.Tensor, name: str, m: int):
+    """(T, row stride) of an [m, T] float32 tensor whose rows are contiguous."""
+    if X.dim() != 2 or X.shape[0] != m:
+        raise ValueError(f"{name} must be [m={m}, T] (got {tuple(X.shape)})")
+    if X.stride(1) != 1:
+        raise ValueError(f"{name} rows must be contiguous")
+    T = X.shape[1]
+    ld = X.stride(0) if X.shape[0] > 1 else T
+    return T, max(ld, T)
+
+
+def num_groups(m: int, group: int) -> int:
+    g = m if (group <= 0 or group >= m) else group
+    return (m + g - 1) // g
+
+
+def workspace_bytes(m, n, bits, group, K, alpha=0.5, lambda_rel=0.01, seed=0) -> int:
+    p = _params(m, n, bits, group, K, alpha, lambda_rel, seed)
+    nb = library().ojbkq_workspace_bytes(ctypes.byref(p))
+    if nb == 0:
+        _check(-1)
+    return int(nb)
+
+
+def decode_workspace_bytes(m, n, bits, group, K, seed=0) -> int:
+    p = _params(m, n, bits, group, K, 0.5, 0.0, seed)
+    nb = library().ojbkq_decode_workspace_bytes(ctypes.byref(p))
+    if nb == 0:
+        _check(-1)
+    return int(nb)
+
+
+def _workspace(nbytes: int, device) -> torch.Tensor:
+    # torch's allocator returns 512-byte aligned blocks
+    return torch.empty(max(nbytes, 1), dtype=torch.uint8, device=device)
+
+
+@dataclass
+class QuantResult:
+    codes: torch.Tensor       # [n, m] uint8
+    scales: torch.Tensor      # [n, G] float32
+    zeros: torch.Tensor       # [n, G] float32
+    residuals: torch.Tensor   # [n] float64
+    winner: torch.Tensor      # [n] int32
+
+
+def _outputs(n, m, G, device):
+    return QuantResult(
+        codes=torch.empty(n, m, dtype=torch.uint8, device=device),
+        scales=torch.empty(n, G, dtype=torch.float32, device=device),
+        zeros=torch.empty(n, G, dtype=torch.float32, device=device),
+        residuals=torch.empty(n, dtype=torch.float64, device=device),
+        winner=torch.empty(n, dtype=torch.int32, device=device),
+    )
+
+
+def quantize_layer(W, X_ref, X_q, alpha, bits, group, K, seed, lambda_rel=0.01,
+                   workspace: Optional[torch.Tensor] = None) -> QuantResult:
+    """One-shot ``ojbkq_quantize_layer`` on device tensors.
+
+    W [n, m] float32; X_ref, X_q [m, T] float32 (X_ref may be None or X_q).
+    """
+    n, m = W.shape
+    dev = W.device
+    _need(W, "W", torch.float32, device=dev)
+    if not W.is_contiguous():
+        raise ValueError("W must be contiguous")
+    _need(X_q, "X_q", torch.float32, device=dev)
+    T, ld = _rows_view(X_q, "X_q", m)
+    if X_ref is not None and X_ref is not X_q:
+        _need(X_ref, "X_ref", torch.float32, device=dev)
+        if tuple(X_ref.shape) != tuple(X_q.shape) or X_ref.stride() != X_q.stride():
+            raise ValueError("X_ref must have the shape and strides of X_q")
+    p = _params(m, n, bits, group, K, alpha, lambda_rel, seed)
+    lib = library()
+    need = lib.ojbkq_workspace_bytes(ctypes.byref(p))
+    if need == 0:
+        _check(-1)
+    ws = workspace if workspace is not None else _workspace(need, dev)
+    out = _outputs(n, m, num_groups(m, group), dev)
+    rc = lib.ojbkq_quantize_layer(ctypes.byref(p), _ptr(W), _ptr(X_ref), _ptr(X_q), T, ld,
+                                  _ptr(ws), ws.numel(), _stream(dev), _ptr(out.codes),
+                                  _ptr(out.scales), _ptr(out.zeros), _ptr(out.residuals),
+                                  _ptr(out.winner))
+    _check(rc)
+    return out
+
+
+class LayerSolver:
+    """Staged form: accumulate token chunks, then solve for one or more knobs."""
+
+    def __init__(self, m, n, bits, group, K, seed, lambda_rel=0.01, device="cuda",
+                 workspace: Optional[torch.Tensor] = None):
+        self.m, self.n, self.bits, self.group, self.K = int(m), int(n), bits, group, K
+        self.device = torch.device(device)
+        if self.device.index is None:
+            self.device = torch.device("cuda", torch.cuda.current_device())
+        self.p = _params(m, n, bits, group, K, 0.5, lambda_rel, seed)
+        lib = library()
+        need = lib.ojbkq_workspace_bytes(ctypes.byref(self.p))
+        if need == 0:
+            _check(-1)
+        self.ws = workspace if workspace is not None else _workspace(need, self.device)
+        h = ctypes.c_void_p()
+        _check(lib.ojbkq_create(ctypes.byref(self.p), _ptr(self.ws), self.ws.numel(),
+                                _stream(self.device), ctypes.byref(h)))
+        self.h = h
+
+    def accumulate(self, X_ref_c, X_q_c):
+        _need(X_q_c, "X_q_c", torch.float32, device=self.device)
+        T, ld = _rows_view(X_q_c, "X_q_c", self.m)
+        if X_ref_c is not None and X_ref_c is not X_q_c:
+            _need(X_ref_c, "X_ref_c", torch.float32, device=self.device)
+            if tuple(X_ref_c.shape) != tuple(X_q_c.shape) or X_ref_c.stride() != X_q_c.stride():
+                raise ValueError("X_ref_c must have the shape and strides of X_q_c")
+        _check(library().ojbkq_accumulate(self.h, _ptr(X_ref_c), _ptr(X_q_c), T, ld))
+
+    def solve(self, W, alpha) -> QuantResult:
+        _need(W, "W", torch.float32, (self.n, self.m), self.device)
+        if not W.is_contiguous():
+            raise ValueError("W must be contiguous")
+        out = _outputs(self.n, self.m, num_groups(self.m, self.group), self.device)
+        _check(library().ojbkq_solve(self.h, _ptr(W), float(alpha), _ptr(out.codes),
+                                     _ptr(out.scales), _ptr(out.zeros), _ptr(out.residuals),
+                                     _ptr(out.winner)))
+        return out
+
+    def inspect(self, which: str) -> torch.Tensor:
+        """A copy of an intermediate of the last solve: 'L', 'qbar', 'alpha', 'lam2', 'path_resid'."""
+        idx = {"L": 0, "qbar": 1, "alpha": 2, "lam2": 3, "path_resid": 4}[which]
+        ptr = ctypes.c_void_p()
+        _check(library().ojbkq_inspect(self.h, idx, ctypes.byref(ptr)))
+        shape = {"L": (self.m, self.m), "qbar": (self.n, self.m), "alpha": (self.n,),
+                 "lam2": (1,), "path_resid": (self.n, self.K + 1)}[which]
+        off = ptr.value - self.ws.data_ptr()
+        count = int(math.prod(shape))
+        flat = self.ws[off:off + 8 * count].view(torch.float64)
+        return flat.reshape(shape).clone()
+
+    def close(self):
+        if getattr(self, "h", None) is not None and self.h.value:
+            library().ojbkq_destroy(self.h)
+            self.h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+def decode_stage(R, qbar, scales, bits, group, K, seed, want_paths=False):
+    """``ojbkq_decode_stage``: decode + select on a given upper factor R (float64)."""
+    m = R.shape[0]
+    n = qbar.shape[0]
+    dev = R.device
+    _need(R, "R", torch.float64, (m, m), dev)
+    _need(qbar, "qbar", torch.float64, (n, m), dev)
+    _need(scales, "scales", torch.float32, (n, num_groups(m, group)), dev)
+    for t, nm in ((R, "R"), (qbar, "qbar"), (scales, "scales")):
+        if not t.is_contiguous():
+            raise ValueError(f"{nm} must be contiguous")
+    p = _params(m, n, bits, group, K, 0.5, 0.0, seed)
+    lib = library()
+    need = lib.ojbkq_decode_workspace_bytes(ctypes.byref(p))
+    if need == 0:
+        _check(-1)
+    ws = _workspace(need, dev)
+    codes = torch.empty(n, m, dtype=torch.uint8, device=dev)
+    resid = torch.empty(n, dtype=torch.float64, device=dev)
+    winner = torch.empty(n, dtype=torch.int32, device=dev)
+    pc = torch.empty(n, K + 1, m, dtype=torch.uint8, device=dev) if want_paths else None
+    pr = torch.empty(n, K + 1, dtype=torch.float64, device=dev) if want_paths else None
+    _check(lib.ojbkq_decode_stage(ctypes.byref(p), _ptr(R), _ptr(qbar), _ptr(scales), _ptr(ws),
+                                  ws.numel(), _stream(dev), _ptr(codes), _ptr(resid), _ptr(winner),
+                                  _ptr(pc), _ptr(pr)))
+    return codes, resid, winner, pc, pr
+
+
+def klein_log_rho(m: int, K: int) -> float:
+    """Host-side ``ojbkq_klein_log_rho`` (no GPU needed)."""
+    return float(library().ojbkq_klein_log_rho(int(m), int(K)))

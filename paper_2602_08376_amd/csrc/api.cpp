@@ -1,0 +1,410 @@
+// C ABI of the library (declared in include/ojbkq.h): argument checks,
+// workspace carving and the order of the stages on the caller's stream.
+#include "ojbkq.h"
+
+#include <hip/hip_runtime.h>
+
+#include <climits>
+#include <cmath>
+#include <cstdio>
+#include <cstring>
+#include <new>
+#include <string>
+
+#include "kernels.h"
+
+namespace {
+
+thread_local std::string g_error;
+
+int fail(int code, const std::string& msg) {
+  g_error = msg;
+  return code;
+}
+
+int hip_fail(hipError_t e, const char* where) {
+  return fail(OJBKQ_EHIP, std::string(where) + ": " + hipGetErrorString(e));
+}
+
+#define OJBKQ_HIP(call, where)                     \
+  do {                                             \
+    hipError_t e_ = (call);                        \
+    if (e_ != hipSuccess) return hip_fail(e_, where); \
+  } while (0)
+
+constexpr size_t kAlign = 256;
+constexpr int kStatusClear = 0x7f7f7f7f;   // byte-fill value meaning "no bad pivot"
+
+size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+
+struct Shape {
+  int64_t m, n, g, G, K, paths, nwg;
+  int qmax;
+};
+
+Shape shape_of(const ojbkq_params& p) {
+  Shape s;
+  s.m = p.m;
+  s.n = p.n;
+  s.g = (p.group <= 0 || p.group >= p.m) ? p.m : p.group;
+  s.G = (s.m + s.g - 1) / s.g;
+  s.K = p.K;
+  s.paths = p.n * (int64_t)(p.K + 1);
+  s.nwg = ojbkq::decode_workgroups(p.n, p.K);
+  s.qmax = (1 << p.bits) - 1;
+  return s;
+}
+
+// Offsets of every buffer carved from the workspace.
+struct Layout {
+  size_t status = 0, lam2 = 0, G = 0, E = 0, U = 0, qbar = 0, gq = 0, alpha = 0, pcodes = 0,
+         presid = 0, total = 0;
+};
+
+Layout layout_full(const Shape& s) {
+  Layout L;
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    const size_t at = off;
+    off += align_up(bytes);
+    return at;
+  };
+  const size_t mm = (size_t)s.m * (size_t)s.m * sizeof(double);
+  const size_t nm = (size_t)s.n * (size_t)s.m * sizeof(double);
+  L.status = take(sizeof(int));
+  L.lam2 = take(sizeof(double));
+  L.G = take(mm);
+  L.E = take(mm);
+  L.U = take(nm);
+  L.qbar = take(nm);
+  L.gq = take(nm);
+  L.alpha = take((size_t)s.n * sizeof(double));
+  L.pcodes = take((size_t)s.nwg * ojbkq::kDecodeThreads * (size_t)s.m);
+  L.presid = take((size_t)s.nwg * ojbkq::kDecodeThreads * sizeof(double));
+  L.total = off;
+  return L;
+}
+
+Layout layout_decode(const Shape& s) {
+  Layout L;
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    const size_t at = off;
+    off += align_up(bytes);
+    return at;
+  };
+  const size_t mm = (size_t)s.m * (size_t)s.m * sizeof(double);
+  const size_t nm = (size_t)s.n * (size_t)s.m * sizeof(double);
+  L.G = take(mm);   // holds L = R^T
+  L.U = take(nm);
+  L.gq = take(nm);
+  L.alpha = take((size_t)s.n * sizeof(double));
+  L.pcodes = take((size_t)s.nwg * ojbkq::kDecodeThreads * (size_t)s.m);
+  L.presid = take((size_t)s.nwg * ojbkq::kDecodeThreads * sizeof(double));
+  L.total = off;
+  return L;
+}
+
+int check_params(const ojbkq_params* p) {
+  if (!p) return fail(OJBKQ_EINVAL, "params is NULL");
+  if (p->m < 1 || p->m > (int64_t)1 << 20) return fail(OJBKQ_EINVAL, "m must be in [1, 2^20]");
+  if (p->n < 1 || p->n > (int64_t)1 << 24) return fail(OJBKQ_EINVAL, "n must be in [1, 2^24]");
+  if (p->bits < 1 || p->bits > 8) return fail(OJBKQ_EINVAL, "bits must be in [1, 8]");
+  if (p->K < 0 || p->K > (1 << 20)) return fail(OJBKQ_EINVAL, "K must be in [0, 2^20]");
+  if (p->reserved != 0) return fail(OJBKQ_EINVAL, "reserved must be 0");
+  if (!(p->alpha >= 0.0 && p->alpha <= 1.0)) return fail(OJBKQ_EINVAL, "alpha must be in [0, 1]");
+  if (!(p->lambda_rel >= 0.0) || !std::isfinite(p->lambda_rel))
+    return fail(OJBKQ_EINVAL, "lambda_rel must be finite and >= 0");
+  if (p->n * (int64_t)(p->K + 1) > (int64_t)INT_MAX)
+    return fail(OJBKQ_EINVAL, "n * (K + 1) must fit in 31 bits");
+  if (p->m > (int64_t)INT_MAX / 2) return fail(OJBKQ_EINVAL, "m too large");
+  return OJBKQ_OK;
+}
+
+double log_rho(int64_t m, int64_t K) {
+  // ln K = (2m / rho)(1 + ln rho).  In x = ln rho the right side
+  // h(x) = 2m (1 + x) e^-x falls strictly for x > 0 from 2m to 0, so a root
+  // x > 0 exists and is unique iff 0 < ln K < 2m.  Bracket, then bisect to
+  // the last representable midpoint.
+  if (m < 1) return NAN;
+  if (K <= 1) return INFINITY;
+  const double target = std::log((double)K);
+  const double two_m = 2.0 * (double)m;
+  if (target >= two_m) return 0.0;
+  auto h = [&](double x) { return two_m * (1.0 + x) * std::exp(-x); };
+  double lo = 0.0, hi = 1.0;
+  while (h(hi) > target) {
+    lo = hi;
+    hi *= 2.0;
+  }
+  for (int it = 0; it < 2000; ++it) {
+    const double mid = 0.5 * (lo + hi);
+    if (!(mid > lo && mid < hi)) break;
+    if (h(mid) > target)
+      lo = mid;
+    else
+      hi = mid;
+  }
+  return 0.5 * (lo + hi);
+}
+
+}  // namespace
+
+struct ojbkq_ctx {
+  ojbkq_params p;
+  Shape s;
+  Layout L;
+  char* ws = nullptr;
+  hipStream_t stream = nullptr;
+  bool any_chunk = false;
+  bool cross_seen = false;
+  bool factored = false;
+  bool solved = false;
+
+  template <typename T>
+  T* at(size_t off) const {
+    return reinterpret_cast<T*>(ws + off);
+  }
+};
+
+namespace {
+
+int ctx_init(ojbkq_ctx* c, const ojbkq_params* p, void* ws, size_t bytes, void* stream) {
+  int rc = check_params(p);
+  if (rc) return rc;
+  if (!ws) return fail(OJBKQ_EINVAL, "workspace is NULL");
+  if (reinterpret_cast<uintptr_t>(ws) % kAlign)
+    return fail(OJBKQ_EINVAL, "workspace must be 256-byte aligned");
+  c->p = *p;
+  c->s = shape_of(*p);
+  c->L = layout_full(c->s);
+  if (bytes < c->L.total)
+    return fail(OJBKQ_ENOSPACE, "workspace has " + std::to_string(bytes) + " bytes, needs " +
+                                    std::to_string(c->L.total));
+  c->ws = static_cast<char*>(ws);
+  c->stream = static_cast<hipStream_t>(stream);
+  OJBKQ_HIP(hipMemsetAsync(c->at<int>(c->L.status), 0x7f, sizeof(int), c->stream), "status clear");
+  return OJBKQ_OK;
+}
+
+int ctx_accumulate(ojbkq_ctx* c, const float* Xr, const float* Xq, int64_t T, int64_t ldx) {
+  if (c->factored) return fail(OJBKQ_ESTATE, "accumulate after the Gram was factored");
+  if (!Xq) return fail(OJBKQ_EINVAL, "X_q is NULL");
+  if (T < 1) return fail(OJBKQ_EINVAL, "token count must be >= 1");
+  if (ldx < T) return fail(OJBKQ_EINVAL, "ldx must be >= T");
+  const bool cross = Xr != nullptr && Xr != Xq;
+  OJBKQ_HIP(ojbkq::gram_cross(Xq, cross ? Xr : nullptr, c->s.m, T, ldx, c->at<double>(c->L.G),
+                              c->at<double>(c->L.E), c->any_chunk, c->cross_seen, c->stream),
+            "gram and cross term");
+  if (cross) c->cross_seen = true;
+  c->any_chunk = true;
+  return OJBKQ_OK;
+}
+
+int finish(ojbkq_ctx* c) {
+  int st = kStatusClear;
+  OJBKQ_HIP(hipMemcpyAsync(&st, c->at<int>(c->L.status), sizeof(int), hipMemcpyDeviceToHost,
+                           c->stream),
+            "status read");
+  OJBKQ_HIP(hipStreamSynchronize(c->stream), "stream sync");
+  if (st != kStatusClear)
+    return fail(OJBKQ_ENOTPD, "damped Gram is not positive definite (pivot " + std::to_string(st) +
+                                  ")");
+  return OJBKQ_OK;
+}
+
+int ctx_solve(ojbkq_ctx* c, const float* W, double alpha, uint8_t* codes, float* scales,
+              float* zeros, double* residuals, int32_t* winner) {
+  if (!c->any_chunk) return fail(OJBKQ_ESTATE, "solve before any accumulate");
+  if (!W || !codes || !scales || !zeros || !residuals)
+    return fail(OJBKQ_EINVAL, "W, codes, scales, zeros and residuals are required");
+  if (!(alpha >= 0.0 && alpha <= 1.0)) return fail(OJBKQ_EINVAL, "alpha must be in [0, 1]");
+  const Shape& s = c->s;
+  hipStream_t st = c->stream;
+  double* Lf = c->at<double>(c->L.G);
+  if (!c->factored) {
+    OJBKQ_HIP(ojbkq::launch_damp(Lf, s.m, c->p.lambda_rel, c->at<double>(c->L.lam2), st), "damp");
+    OJBKQ_HIP(ojbkq::cholesky_lower(Lf, s.m, c->at<int>(c->L.status), st), "cholesky");
+    c->factored = true;
+  }
+  OJBKQ_HIP(ojbkq::launch_scale_zero(W, s.n, s.m, s.g, s.G, s.qmax, scales, zeros, st),
+            "scales");
+  double* U = c->at<double>(c->L.U);
+  const bool cross = c->cross_seen && alpha != 1.0;
+  if (cross) {
+    ojbkq::GemmDesc g;   // U = W E^T: row j is X~^T (X - X~) w_j
+    g.M = s.n; g.N = s.m; g.Kd = s.m;
+    g.A = W; g.lda = s.m; g.ta = ojbkq::Elt::F32;
+    g.B = c->at<double>(c->L.E); g.ldb = s.m; g.tb = ojbkq::Elt::F64;
+    g.C = U; g.ldc = s.m;
+    OJBKQ_HIP(ojbkq::gemm_f64(g, st), "target projection");
+    OJBKQ_HIP(ojbkq::solve_llt(Lf, U, s.n, s.m, st), "solves");
+  }
+  double* qbar = c->at<double>(c->L.qbar);
+  OJBKQ_HIP(ojbkq::launch_centres(W, cross ? U : nullptr, 1.0 - alpha, scales, zeros, s.n, s.m,
+                                  s.g, s.G, qbar, U, st),
+            "centres");
+  double* gq = c->at<double>(c->L.gq);
+  {
+    ojbkq::GemmDesc g;   // gq_j = Rbar_j qbar_j: gq[j][i] = sum_l Y[j][l] L[l][i]
+    g.M = s.n; g.N = s.m; g.Kd = s.m;
+    g.A = U; g.lda = s.m; g.ta = ojbkq::Elt::F64;
+    g.B = Lf; g.ldb = s.m; g.tb = ojbkq::Elt::F64; g.b_kmajor = true;
+    g.C = gq; g.ldc = s.m;
+    OJBKQ_HIP(ojbkq::gemm_f64(g, st), "Rbar qbar");
+  }
+  double* al = c->at<double>(c->L.alpha);
+  OJBKQ_HIP(ojbkq::launch_klein_alpha(Lf, scales, s.n, s.m, s.g, s.G, log_rho(s.m, s.K), al, st),
+            "klein alpha");
+  ojbkq::DecodeDesc d;
+  d.L = Lf; d.gq = gq; d.S = scales; d.alpha = al;
+  d.m = s.m; d.n = s.n; d.g = s.g; d.G = s.G; d.K = (int)s.K; d.bits = c->p.bits;
+  d.seed = c->p.seed;
+  d.pcodes = c->at<uint8_t>(c->L.pcodes);
+  d.presid = c->at<double>(c->L.presid);
+  OJBKQ_HIP(ojbkq::launch_decode(d, st), "decode");
+  OJBKQ_HIP(ojbkq::launch_select(d.pcodes, d.presid, s.n, s.m, (int)s.K, codes, residuals, winner,
+                                 nullptr, nullptr, st),
+            "select");
+  c->solved = true;
+  return finish(c);
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t ojbkq_workspace_bytes(const ojbkq_params* p) {
+  if (check_params(p)) return 0;
+  return layout_full(shape_of(*p)).total;
+}
+
+int ojbkq_quantize_layer(const ojbkq_params* p, const float* W, const float* X_ref,
+                         const float* X_q, int64_t T, int64_t ldx, void* workspace,
+                         size_t workspace_bytes, void* stream, uint8_t* codes, float* scales,
+                         float* zeros, double* residuals, int32_t* winner) {
+  g_error.clear();
+  int rc = check_params(p);
+  if (rc) return rc;
+  if (!W || !X_q || !codes || !scales || !zeros || !residuals)
+    return fail(OJBKQ_EINVAL, "W, X_q, codes, scales, zeros and residuals are required");
+  if (T < 1) return fail(OJBKQ_EINVAL, "token count must be >= 1");
+  if (ldx < T) return fail(OJBKQ_EINVAL, "ldx must be >= T");
+  ojbkq_ctx c;
+  if ((rc = ctx_init(&c, p, workspace, workspace_bytes, stream))) return rc;
+  const float* Xr = (p->alpha == 1.0) ? nullptr : X_ref;
+  if ((rc = ctx_accumulate(&c, Xr, X_q, T, ldx))) return rc;
+  return ctx_solve(&c, W, p->alpha, codes, scales, zeros, residuals, winner);
+}
+
+int ojbkq_create(const ojbkq_params* p, void* workspace, size_t workspace_bytes, void* stream,
+                 ojbkq_ctx** out) {
+  g_error.clear();
+  if (!out) return fail(OJBKQ_EINVAL, "out is NULL");
+  *out = nullptr;
+  ojbkq_ctx* c = new (std::nothrow) ojbkq_ctx();
+  if (!c) return fail(OJBKQ_EINVAL, "out of host memory");
+  int rc = ctx_init(c, p, workspace, workspace_bytes, stream);
+  if (rc) {
+    delete c;
+    return rc;
+  }
+  *out = c;
+  return OJBKQ_OK;
+}
+
+int ojbkq_accumulate(ojbkq_ctx* ctx, const float* X_ref_c, const float* X_q_c, int64_t T_c,
+                     int64_t ldx) {
+  g_error.clear();
+  if (!ctx) return fail(OJBKQ_EINVAL, "ctx is NULL");
+  return ctx_accumulate(ctx, X_ref_c, X_q_c, T_c, ldx);
+}
+
+int ojbkq_solve(ojbkq_ctx* ctx, const float* W, double alpha, uint8_t* codes, float* scales,
+                float* zeros, double* residuals, int32_t* winner) {
+  g_error.clear();
+  if (!ctx) return fail(OJBKQ_EINVAL, "ctx is NULL");
+  return ctx_solve(ctx, W, alpha, codes, scales, zeros, residuals, winner);
+}
+
+int ojbkq_destroy(ojbkq_ctx* ctx) {
+  g_error.clear();
+  delete ctx;
+  return OJBKQ_OK;
+}
+
+int ojbkq_inspect(ojbkq_ctx* ctx, int which, const void** ptr) {
+  g_error.clear();
+  if (!ctx || !ptr) return fail(OJBKQ_EINVAL, "ctx and ptr are required");
+  if (!ctx->solved) return fail(OJBKQ_ESTATE, "inspect before the first solve");
+  switch (which) {
+    case 0: *ptr = ctx->at<void>(ctx->L.G); break;
+    case 1: *ptr = ctx->at<void>(ctx->L.qbar); break;
+    case 2: *ptr = ctx->at<void>(ctx->L.alpha); break;
+    case 3: *ptr = ctx->at<void>(ctx->L.lam2); break;
+    case 4: *ptr = ctx->at<void>(ctx->L.presid); break;
+    default: return fail(OJBKQ_EINVAL, "unknown intermediate");
+  }
+  return OJBKQ_OK;
+}
+
+size_t ojbkq_decode_workspace_bytes(const ojbkq_params* p) {
+  if (check_params(p)) return 0;
+  return layout_decode(shape_of(*p)).total;
+}
+
+int ojbkq_decode_stage(const ojbkq_params* p, const double* R, const double* qbar,
+                       const float* scales, void* workspace, size_t workspace_bytes, void* stream,
+                       uint8_t* codes, double* residuals, int32_t* winner, uint8_t* path_codes,
+                       double* path_resid) {
+  g_error.clear();
+  int rc = check_params(p);
+  if (rc) return rc;
+  if (!R || !qbar || !scales || !codes || !residuals)
+    return fail(OJBKQ_EINVAL, "R, qbar, scales, codes and residuals are required");
+  if (!workspace) return fail(OJBKQ_EINVAL, "workspace is NULL");
+  if (reinterpret_cast<uintptr_t>(workspace) % kAlign)
+    return fail(OJBKQ_EINVAL, "workspace must be 256-byte aligned");
+  const Shape s = shape_of(*p);
+  const Layout L = layout_decode(s);
+  if (workspace_bytes < L.total)
+    return fail(OJBKQ_ENOSPACE, "workspace has " + std::to_string(workspace_bytes) +
+                                    " bytes, needs " + std::to_string(L.total));
+  char* ws = static_cast<char*>(workspace);
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  double* Lf = reinterpret_cast<double*>(ws + L.G);
+  double* Y = reinterpret_cast<double*>(ws + L.U);
+  double* gq = reinterpret_cast<double*>(ws + L.gq);
+  double* al = reinterpret_cast<double*>(ws + L.alpha);
+  OJBKQ_HIP(ojbkq::launch_upper_to_lower(R, Lf, s.m, st), "transpose");
+  OJBKQ_HIP(ojbkq::launch_centres(nullptr, nullptr, 0.0, scales, nullptr, s.n, s.m, s.g, s.G,
+                                  const_cast<double*>(qbar), Y, st),
+            "scaled centres");
+  {
+    ojbkq::GemmDesc g;
+    g.M = s.n; g.N = s.m; g.Kd = s.m;
+    g.A = Y; g.lda = s.m; g.ta = ojbkq::Elt::F64;
+    g.B = Lf; g.ldb = s.m; g.tb = ojbkq::Elt::F64; g.b_kmajor = true;
+    g.C = gq; g.ldc = s.m;
+    OJBKQ_HIP(ojbkq::gemm_f64(g, st), "Rbar qbar");
+  }
+  OJBKQ_HIP(ojbkq::launch_klein_alpha(Lf, scales, s.n, s.m, s.g, s.G, log_rho(s.m, s.K), al, st),
+            "klein alpha");
+  ojbkq::DecodeDesc d;
+  d.L = Lf; d.gq = gq; d.S = scales; d.alpha = al;
+  d.m = s.m; d.n = s.n; d.g = s.g; d.G = s.G; d.K = (int)s.K; d.bits = p->bits; d.seed = p->seed;
+  d.pcodes = reinterpret_cast<uint8_t*>(ws + L.pcodes);
+  d.presid = reinterpret_cast<double*>(ws + L.presid);
+  OJBKQ_HIP(ojbkq::launch_decode(d, st), "decode");
+  OJBKQ_HIP(ojbkq::launch_select(d.pcodes, d.presid, s.n, s.m, (int)s.K, codes, residuals, winner,
+                                 path_codes, path_resid, st),
+            "select");
+  OJBKQ_HIP(hipStreamSynchronize(st), "stream sync");
+  return OJBKQ_OK;
+}
+
+double ojbkq_klein_log_rho(int64_t m, int64_t K) { return log_rho(m, K); }
+
+const char* ojbkq_last_error(void) { return g_error.c_str(); }
+
+}  // extern "C"

@@ -1,0 +1,60 @@
+// Device-side helpers shared by the gfx950 kernels: the fp64 MFMA tile type
+// and the counter-based Philox4x32-10 generator used for Klein's draws.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace ojbkq {
+
+// Accumulator of one v_mfma_f64_16x16x4_f64: a 16x16 fp64 tile spread over a
+// wave, four values per lane.  Lane l supplies A[l % 16][l / 16] and
+// B[l / 16][l % 16] of the 16x4 and 4x16 operands and holds
+// D[l / 16 + 4 r][l % 16], r = 0..3 (measured on gfx950).
+typedef double d4 __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ d4 mfma_f64(double a, double b, d4 c) {
+  return __builtin_amdgcn_mfma_f64_16x16x4f64(a, b, c, 0, 0, 0);
+}
+
+// Philox4x32-10 (Salmon, Moraes, Dror, Shaw, SC'11): ten rounds of two
+// 32x32->64-bit products on a 128-bit counter, key bumped by the two Weyl
+// constants between rounds.
+struct Philox4 {
+  uint32_t x0, x1, x2, x3;
+};
+
+__device__ __forceinline__ Philox4 philox4x32_10(uint32_t c0, uint32_t c1, uint32_t c2,
+                                                 uint32_t c3, uint32_t k0, uint32_t k1) {
+  constexpr uint32_t kM0 = 0xD2511F53u, kM1 = 0xCD9E8D57u;
+  constexpr uint32_t kW0 = 0x9E3779B9u, kW1 = 0xBB67AE85u;
+#pragma unroll
+  for (int round = 0; round < 10; ++round) {
+    if (round) {
+      k0 += kW0;
+      k1 += kW1;
+    }
+    const uint32_t lo0 = kM0 * c0, hi0 = __umulhi(kM0, c0);
+    const uint32_t lo1 = kM1 * c2, hi1 = __umulhi(kM1, c2);
+    const uint32_t n0 = hi1 ^ c1 ^ k0;
+    const uint32_t n2 = hi0 ^ c3 ^ k1;
+    c0 = n0;
+    c1 = lo1;
+    c2 = n2;
+    c3 = lo0;
+  }
+  return Philox4{c0, c1, c2, c3};
+}
+
+// Uniform double in [0, 1) for the Klein draw of (row i, column j, candidate
+// k): counter (i, j, k, 0), key (seed lo, seed hi), 53 bits from the first
+// two words (27 high bits of x0, 26 high bits of x1).
+__device__ __forceinline__ double klein_uniform(uint64_t seed, uint32_t i, uint32_t j,
+                                                uint32_t k) {
+  const Philox4 r = philox4x32_10(i, j, k, 0u, (uint32_t)seed, (uint32_t)(seed >> 32));
+  const double hi = (double)(r.x0 >> 5);
+  const double lo = (double)(r.x1 >> 6);
+  return (hi * 67108864.0 + lo) * (1.0 / 9007199254740992.0);
+}
+
+}  // namespace ojbkq

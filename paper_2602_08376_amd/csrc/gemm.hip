@@ -1,0 +1,299 @@
+// fp64 MFMA GEMM for gfx950: C = beta C + alpha op(A) op(B)^T.
+//
+// Serves every dense contraction of the path: the Gram X~^T X~ (Alg. 1
+// step 2), the cross term X~^T (X - X~) and its product with W (the target
+// projection behind Eq. jta_target / Alg. 1 step 3), the Cholesky trailing
+// updates, the blocked triangular-solve updates and Rbar qbar for the decoder.
+//
+// Design: 128x128 output tile per 256-thread workgroup, four waves in a 2x2
+// grid, each wave a 64x64 block of 4x4 v_mfma_f64_16x16x4_f64 tiles
+// (64 fp64 accumulators per lane).  Operands are staged through LDS in
+// 16-deep k-chunks, widened to fp64 on the way in (fp32 x fp32 products are
+// exact in fp64), with the next chunk prefetched into registers while the
+// current one feeds the matrix cores.  Tiles are numbered so that each XCD
+// (eight per MI355X, one L2 each) receives a contiguous, row-grouped run of
+// tiles that share A and B panels.
+#include "kernels.h"
+#include "device.h"
+
+namespace ojbkq {
+namespace {
+
+constexpr int kTile = 128;
+constexpr int kKC = 16;
+constexpr int kLdsLd = kTile + 2;  // padded LDS row (doubles)
+constexpr int kGroupRows = 8;      // tile rows per raster group
+
+struct GemmArgs {
+  int64_t M, N, Kd;
+  const void* A;
+  int64_t lda;
+  const void* B;
+  const void* B2;
+  int64_t ldb;
+  double* C;
+  int64_t ldc;
+  double alpha, beta;
+  int64_t tiles_m, tiles_n;
+  int lower;
+  int vec_a, vec_b;
+};
+
+// Eight consecutive elements starting at p, the first `valid` of them real
+// (the rest read as 0), widened to fp64.
+template <typename T>
+__device__ __forceinline__ void load8(const T* __restrict__ p, int valid, bool vec,
+                                      double out[8]) {
+  if (valid >= 8 && vec) {
+    if constexpr (sizeof(T) == 4) {
+      const float4 a = *reinterpret_cast<const float4*>(p);
+      const float4 b = *reinterpret_cast<const float4*>(p + 4);
+      out[0] = a.x; out[1] = a.y; out[2] = a.z; out[3] = a.w;
+      out[4] = b.x; out[5] = b.y; out[6] = b.z; out[7] = b.w;
+    } else {
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const double2 v = *reinterpret_cast<const double2*>(p + 2 * q);
+        out[2 * q] = v.x;
+        out[2 * q + 1] = v.y;
+      }
+    }
+  } else {
+#pragma unroll
+    for (int q = 0; q < 8; ++q) out[q] = (q < valid) ? (double)p[q] : 0.0;
+  }
+}
+
+// Loads this thread's share (8 elements) of a 128 x 16 operand chunk.
+// Non-k-major: thread -> (row tid/2, k offset 8*(tid%2)); k-major: thread ->
+// (k row tid/16, row offset 8*(tid%16)).
+template <typename T, bool KMAJOR>
+__device__ __forceinline__ void load_chunk(const T* __restrict__ X, int64_t ld, int64_t rows,
+                                           int64_t Kd, int64_t r0, int64_t k0, int tid, bool vec,
+                                           double out[8]) {
+  if constexpr (!KMAJOR) {
+    const int64_t r = r0 + (tid >> 1);
+    const int64_t k = k0 + (tid & 1) * 8;
+    const int64_t left = Kd - k;
+    const int valid = (r < rows && left > 0) ? (int)(left < 8 ? left : 8) : 0;
+    const T* p = valid > 0 ? X + r * ld + k : X;
+    load8<T>(p, valid, vec, out);
+  } else {
+    const int64_t k = k0 + (tid >> 4);
+    const int64_t r = r0 + (tid & 15) * 8;
+    const int64_t left = rows - r;
+    const int valid = (k < Kd && left > 0) ? (int)(left < 8 ? left : 8) : 0;
+    const T* p = valid > 0 ? X + k * ld + r : X;
+    load8<T>(p, valid, vec, out);
+  }
+}
+
+template <bool KMAJOR>
+__device__ __forceinline__ void store_chunk(double (*s)[kLdsLd], int tid, const double v[8]) {
+  if constexpr (!KMAJOR) {
+    const int r = tid >> 1, k = (tid & 1) * 8;
+#pragma unroll
+    for (int q = 0; q < 8; ++q) s[k + q][r] = v[q];
+  } else {
+    const int k = tid >> 4, r = (tid & 15) * 8;
+#pragma unroll
+    for (int q = 0; q < 8; ++q) s[k][r + q] = v[q];
+  }
+}
+
+// Tile numbering shared by the kernels below.  Lower-triangle tiles of a
+// square grid are numbered row by row; full grids in groups of kGroupRows
+// tile rows so that neighbouring workgroups share A and B panels.
+__device__ __forceinline__ void lower_tile(int64_t t, int64_t& ti, int64_t& tj) {
+  ti = (int64_t)((sqrt(8.0 * (double)t + 1.0) - 1.0) * 0.5);
+  while (ti * (ti + 1) / 2 > t) --ti;
+  while ((ti + 1) * (ti + 2) / 2 <= t) ++ti;
+  tj = t - ti * (ti + 1) / 2;
+}
+
+__device__ __forceinline__ void raster_tile(int64_t t, int64_t tiles_m, int64_t tiles_n,
+                                            int64_t& ti, int64_t& tj) {
+  const int64_t per = (int64_t)kGroupRows * tiles_n;
+  const int64_t first = (t / per) * kGroupRows;
+  const int64_t rows = (tiles_m - first) < kGroupRows ? (tiles_m - first) : kGroupRows;
+  const int64_t r = t % per;
+  ti = first + r % rows;
+  tj = r / rows;
+}
+
+// Consecutive tile numbers go to the same XCD (workgroups are dealt to the
+// eight XCDs round-robin by blockIdx).
+__device__ __forceinline__ int64_t xcd_tile_number() {
+  int64_t t = blockIdx.x;
+  const int64_t nb = gridDim.x;
+  if ((nb & 7) == 0) t = (t & 7) * (nb >> 3) + (t >> 3);
+  return t;
+}
+
+// One 128x128 output tile (ti, tj) of C = beta C + alpha op(A) op(B)^T.
+template <typename TA, typename TB, bool AK, bool BK, bool BDIFF>
+__device__ __forceinline__ void gemm_tile(const GemmArgs& g, int64_t ti, int64_t tj,
+                                          double (*sA)[kLdsLd], double (*sB)[kLdsLd]) {
+  const int64_t I0 = ti * kTile, J0 = tj * kTile;
+  const int tid = threadIdx.x;
+  const int lane = tid & 63, wave = tid >> 6;
+  const int wr = wave >> 1, wc = wave & 1;
+  const TA* A = static_cast<const TA*>(g.A);
+  const TB* B = static_cast<const TB*>(g.B);
+  const TB* B2 = static_cast<const TB*>(g.B2);
+
+  d4 acc[4][4];
+#pragma unroll
+  for (int x = 0; x < 4; ++x)
+#pragma unroll
+    for (int y = 0; y < 4; ++y) acc[x][y] = d4{0.0, 0.0, 0.0, 0.0};
+
+  double ra[8], rb[8];
+  auto fetch = [&](int64_t k0) {
+    load_chunk<TA, AK>(A, g.lda, g.M, g.Kd, I0, k0, tid, g.vec_a, ra);
+    load_chunk<TB, BK>(B, g.ldb, g.N, g.Kd, J0, k0, tid, g.vec_b, rb);
+    if constexpr (BDIFF) {
+      double r2[8];
+      load_chunk<TB, BK>(B2, g.ldb, g.N, g.Kd, J0, k0, tid, g.vec_b, r2);
+#pragma unroll
+      for (int q = 0; q < 8; ++q) rb[q] -= r2[q];
+    }
+  };
+
+  if (g.Kd > 0) fetch(0);
+  for (int64_t k0 = 0; k0 < g.Kd; k0 += kKC) {
+    __syncthreads();
+    store_chunk<AK>(sA, tid, ra);
+    store_chunk<BK>(sB, tid, rb);
+    __syncthreads();
+    if (k0 + kKC < g.Kd) fetch(k0 + kKC);
+#pragma unroll
+    for (int kk = 0; kk < kKC / 4; ++kk) {
+      const int kr = kk * 4 + (lane >> 4);
+      double a[4], b[4];
+#pragma unroll
+      for (int x = 0; x < 4; ++x) a[x] = sA[kr][wr * 64 + x * 16 + (lane & 15)];
+#pragma unroll
+      for (int y = 0; y < 4; ++y) b[y] = sB[kr][wc * 64 + y * 16 + (lane & 15)];
+#pragma unroll
+      for (int x = 0; x < 4; ++x)
+#pragma unroll
+        for (int y = 0; y < 4; ++y) acc[x][y] = mfma_f64(a[x], b[y], acc[x][y]);
+    }
+  }
+
+#pragma unroll
+  for (int x = 0; x < 4; ++x)
+#pragma unroll
+    for (int y = 0; y < 4; ++y)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int64_t i = I0 + wr * 64 + x * 16 + (lane >> 4) + 4 * r;
+        const int64_t j = J0 + wc * 64 + y * 16 + (lane & 15);
+        if (i < g.M && j < g.N) {
+          double v = g.alpha * acc[x][y][r];
+          if (g.beta != 0.0) v += g.beta * g.C[i * g.ldc + j];
+          g.C[i * g.ldc + j] = v;
+        }
+      }
+}
+
+template <typename TA, typename TB, bool AK, bool BK, bool BDIFF>
+__global__ __launch_bounds__(256, 2) void gemm_f64_kernel(GemmArgs g) {
+  __shared__ double sA[kKC][kLdsLd];
+  __shared__ double sB[kKC][kLdsLd];
+  const int64_t t = xcd_tile_number();
+  int64_t ti, tj;
+  if (g.lower)
+    lower_tile(t, ti, tj);
+  else
+    raster_tile(t, g.tiles_m, g.tiles_n, ti, tj);
+  gemm_tile<TA, TB, AK, BK, BDIFF>(g, ti, tj, sA, sB);
+}
+
+// The calibration-set contractions of one token chunk in one launch: the
+// first n_gram workgroups take the lower-triangle tiles of G += X_q X_q^T,
+// the rest every tile of E += X_q (X_ref - X_q)^T.
+__global__ __launch_bounds__(256, 2) void gram_cross_kernel(GemmArgs gG, GemmArgs gE,
+                                                            int64_t n_gram) {
+  __shared__ double sA[kKC][kLdsLd];
+  __shared__ double sB[kKC][kLdsLd];
+  const int64_t t = xcd_tile_number();
+  int64_t ti, tj;
+  if (t < n_gram) {
+    lower_tile(t, ti, tj);
+    gemm_tile<float, float, false, false, false>(gG, ti, tj, sA, sB);
+  } else {
+    raster_tile(t - n_gram, gE.tiles_m, gE.tiles_n, ti, tj);
+    gemm_tile<float, float, false, false, true>(gE, ti, tj, sA, sB);
+  }
+}
+
+template <typename TA, typename TB, bool AK, bool BK, bool BDIFF>
+hipError_t launch(const GemmArgs& g, int64_t ntiles, hipStream_t s) {
+  gemm_f64_kernel<TA, TB, AK, BK, BDIFF><<<dim3((unsigned)ntiles), dim3(256), 0, s>>>(g);
+  return hipGetLastError();
+}
+
+bool vec_ok(const void* p, int64_t ld, Elt e) {
+  const int64_t per16 = (e == Elt::F32) ? 4 : 2;
+  return p != nullptr && (reinterpret_cast<uintptr_t>(p) % 16) == 0 && (ld % per16) == 0;
+}
+
+}  // namespace
+
+hipError_t gemm_f64(const GemmDesc& d, hipStream_t stream) {
+  if (d.M <= 0 || d.N <= 0) return hipSuccess;
+  GemmArgs g;
+  g.M = d.M; g.N = d.N; g.Kd = d.Kd < 0 ? 0 : d.Kd;
+  g.A = d.A; g.lda = d.lda; g.B = d.B; g.B2 = d.B2; g.ldb = d.ldb;
+  g.C = d.C; g.ldc = d.ldc; g.alpha = d.alpha; g.beta = d.beta;
+  g.tiles_m = (d.M + kTile - 1) / kTile;
+  g.tiles_n = (d.N + kTile - 1) / kTile;
+  g.lower = d.lower_tiles ? 1 : 0;
+  g.vec_a = vec_ok(d.A, d.lda, d.ta) ? 1 : 0;
+  g.vec_b = (vec_ok(d.B, d.ldb, d.tb) && (d.B2 == nullptr || vec_ok(d.B2, d.ldb, d.tb))) ? 1 : 0;
+  if (d.lower_tiles && g.tiles_m != g.tiles_n) return hipErrorInvalidValue;
+  const int64_t ntiles = d.lower_tiles ? g.tiles_m * (g.tiles_m + 1) / 2 : g.tiles_m * g.tiles_n;
+  if (ntiles > 0x7fffffff) return hipErrorInvalidValue;
+
+  const bool diff = d.B2 != nullptr;
+  if (d.ta == Elt::F32 && d.tb == Elt::F32 && !d.a_kmajor && !d.b_kmajor)
+    return diff ? launch<float, float, false, false, true>(g, ntiles, stream)
+                : launch<float, float, false, false, false>(g, ntiles, stream);
+  if (diff) return hipErrorInvalidValue;
+  if (d.ta == Elt::F64 && d.tb == Elt::F64 && !d.a_kmajor && !d.b_kmajor)
+    return launch<double, double, false, false, false>(g, ntiles, stream);
+  if (d.ta == Elt::F64 && d.tb == Elt::F64 && !d.a_kmajor && d.b_kmajor)
+    return launch<double, double, false, true, false>(g, ntiles, stream);
+  if (d.ta == Elt::F32 && d.tb == Elt::F64 && !d.a_kmajor && !d.b_kmajor)
+    return launch<float, double, false, false, false>(g, ntiles, stream);
+  return hipErrorInvalidValue;
+}
+
+hipError_t gram_cross(const float* Xq, const float* Xr, int64_t m, int64_t T, int64_t ldx,
+                      double* G, double* E, bool accumulate_g, bool accumulate_e,
+                      hipStream_t stream) {
+  if (m <= 0) return hipSuccess;
+  GemmArgs gG;
+  gG.M = m; gG.N = m; gG.Kd = T < 0 ? 0 : T;
+  gG.A = Xq; gG.lda = ldx; gG.B = Xq; gG.B2 = nullptr; gG.ldb = ldx;
+  gG.C = G; gG.ldc = m; gG.alpha = 1.0; gG.beta = accumulate_g ? 1.0 : 0.0;
+  gG.tiles_m = gG.tiles_n = (m + kTile - 1) / kTile;
+  gG.lower = 1;
+  gG.vec_a = gG.vec_b = vec_ok(Xq, ldx, Elt::F32) ? 1 : 0;
+  const int64_t n_gram = gG.tiles_m * (gG.tiles_m + 1) / 2;
+  int64_t n_cross = 0;
+  GemmArgs gE = gG;
+  if (Xr != nullptr) {
+    gE.B = Xr; gE.B2 = Xq; gE.C = E; gE.beta = accumulate_e ? 1.0 : 0.0; gE.lower = 0;
+    gE.vec_b = (vec_ok(Xr, ldx, Elt::F32) && vec_ok(Xq, ldx, Elt::F32)) ? 1 : 0;
+    n_cross = gE.tiles_m * gE.tiles_n;
+  }
+  const int64_t total = n_gram + n_cross;
+  if (total > 0x7fffffff) return hipErrorInvalidValue;
+  gram_cross_kernel<<<dim3((unsigned)total), dim3(256), 0, stream>>>(gG, gE, n_gram);
+  return hipGetLastError();
+}
+
+}  // namespace ojbkq

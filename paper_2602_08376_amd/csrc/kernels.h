@@ -1,0 +1,102 @@
+// Host-side launchers of the gfx950 kernels (internal to the library).  Each
+// enqueues work on `stream` and returns the launch status; none allocates.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace ojbkq {
+
+// ---- fp64 MFMA GEMM -------------------------------------------------------
+// C[M, N] = beta * C + alpha * sum_k opA(i, k) * opB(j, k), accumulated in
+// fp64 on v_mfma_f64_16x16x4_f64 (fp32 inputs are widened exactly).
+//   opA(i, k) = a_kmajor ? A[k * lda + i] : A[i * lda + k]
+//   opB(j, k) = b_kmajor ? B[k * ldb + j] : B[j * ldb + k]
+//   with B2 != nullptr, opB = B - B2 (same layout), formed in fp64.
+//   lower_tiles: only 128x128 output tiles with tile_row >= tile_col are
+//   computed (a symmetric product whose lower triangle is wanted).
+enum class Elt { F32, F64 };
+
+struct GemmDesc {
+  int64_t M = 0, N = 0, Kd = 0;
+  const void* A = nullptr;
+  int64_t lda = 0;
+  Elt ta = Elt::F64;
+  bool a_kmajor = false;
+  const void* B = nullptr;
+  const void* B2 = nullptr;
+  int64_t ldb = 0;
+  Elt tb = Elt::F64;
+  bool b_kmajor = false;
+  double* C = nullptr;
+  int64_t ldc = 0;
+  double alpha = 1.0, beta = 0.0;
+  bool lower_tiles = false;
+};
+
+hipError_t gemm_f64(const GemmDesc& d, hipStream_t stream);
+
+// One token chunk of the calibration sums in a single launch:
+//   G (lower triangle by 128-tiles) = [G +] X_q X_q^T
+//   E (all of it, only if Xr != nullptr) = [E +] X_q (X_ref - X_q)^T
+// X_q, X_ref: [m, T] float32 with row stride ldx; G, E: [m, m] float64.
+hipError_t gram_cross(const float* Xq, const float* Xr, int64_t m, int64_t T, int64_t ldx,
+                      double* G, double* E, bool accumulate_g, bool accumulate_e,
+                      hipStream_t stream);
+
+// ---- scales and zero points (Alg. 1 step 1) --------------------------------
+hipError_t launch_scale_zero(const float* W, int64_t n, int64_t m, int64_t g, int64_t G, int qmax,
+                             float* S, float* Z, hipStream_t stream);
+
+// ---- damping and factorisation (Alg. 1 step 2) -----------------------------
+// H (lower triangle, row-major, ld = m) += lambda_rel * mean(diag(H)) * I;
+// lam2_out receives lambda^2.
+hipError_t launch_damp(double* H, int64_t m, double lambda_rel, double* lam2_out,
+                       hipStream_t stream);
+// In-place blocked Cholesky H = L L^T (lower, row-major); zeroes the strict
+// upper triangle.  *status (device int, initialised to INT32_MAX) receives the
+// smallest index of a non-positive pivot.
+hipError_t cholesky_lower(double* H, int64_t m, int* status, hipStream_t stream);
+// L = R^T for an upper-triangular R (row-major); strict upper part of L = 0.
+hipError_t launch_upper_to_lower(const double* R, double* L, int64_t m, hipStream_t stream);
+// In-place solves for n right-hand sides stored as rows of U [n, m]:
+// forward L y = u, then backward L^T x = y (x = H^-1 u).
+hipError_t solve_llt(const double* L, double* U, int64_t n, int64_t m, hipStream_t stream);
+
+// ---- relaxed solution -> centres (Alg. 1 steps 3-5) ------------------------
+// qbar = (w + c * delta) / s + z (delta may be null), Y = s * qbar.
+hipError_t launch_centres(const float* W, const double* delta, double c, const float* S,
+                          const float* Z, int64_t n, int64_t m, int64_t g, int64_t G,
+                          double* qbar, double* Y, hipStream_t stream);
+// alpha_j = log_rho / min_i (L_ii s_j(i))^2.
+hipError_t launch_klein_alpha(const double* L, const float* S, int64_t n, int64_t m, int64_t g,
+                              int64_t G, double log_rho, double* alpha, hipStream_t stream);
+
+// ---- batched Babai / Klein decode and selection (Alg. 1, 3, 4) -------------
+constexpr int kDecodeThreads = 256;   // candidate paths per workgroup
+
+struct DecodeDesc {
+  const double* L = nullptr;   // [m, m] lower factor (L = R^T)
+  const double* gq = nullptr;  // [n, m]: gq_j = Rbar_j qbar_j
+  const float* S = nullptr;    // [n, G]
+  const double* alpha = nullptr;  // [n]
+  int64_t m = 0, n = 0, g = 0, G = 0;
+  int K = 0, bits = 0;
+  uint64_t seed = 0;
+  uint8_t* pcodes = nullptr;   // [nwg, m, 256] candidate codes
+  double* presid = nullptr;    // [nwg * 256] candidate residuals
+};
+
+inline int64_t decode_workgroups(int64_t n, int K) {
+  return (n * (int64_t)(K + 1) + kDecodeThreads - 1) / kDecodeThreads;
+}
+
+hipError_t launch_decode(const DecodeDesc& d, hipStream_t stream);
+
+// First strict minimum over the K + 1 candidates of each column; gathers the
+// winner's codes.  path_codes / path_resid / winner may be null.
+hipError_t launch_select(const uint8_t* pcodes, const double* presid, int64_t n, int64_t m, int K,
+                         uint8_t* codes, double* resid, int32_t* winner, uint8_t* path_codes,
+                         double* path_resid, hipStream_t stream);
+
+}  // namespace ojbkq

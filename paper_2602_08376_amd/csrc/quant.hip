@@ -1,0 +1,130 @@
+// Per-group scales and zero points (Alg. 1 step 1; the Q, S, Z data model of
+// Sec. 3.2), the real centres qbar (Alg. 1 steps 3-4) and the per-column
+// Klein temperature (the alpha rule stated after Eq. klein_prob).
+#include "kernels.h"
+#include "device.h"
+
+namespace ojbkq {
+namespace {
+
+// One wave per (column j, group t).  Asymmetric min-max over the group with
+// the range widened to contain 0 (so the grid represents 0 exactly); an
+// all-zero group uses [-1, 1].  The scale is rounded to float32 once and the
+// zero point is taken against that stored value: z = rint(-xmin / s).
+__global__ __launch_bounds__(256) void scale_zero_kernel(const float* __restrict__ W, int64_t n,
+                                                         int64_t m, int64_t g, int64_t G, int qmax,
+                                                         float* __restrict__ S,
+                                                         float* __restrict__ Z) {
+  const int lane = threadIdx.x & 63;
+  const int64_t gid = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (gid >= n * G) return;
+  const int64_t j = gid / G, t = gid % G;
+  const int64_t a = t * g, b = (a + g < m) ? a + g : m;
+  float mn = INFINITY, mx = -INFINITY;
+  for (int64_t l = a + lane; l < b; l += 64) {
+    const float w = W[j * m + l];
+    mn = fminf(mn, w);
+    mx = fmaxf(mx, w);
+  }
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) {
+    mn = fminf(mn, __shfl_xor(mn, off, 64));
+    mx = fmaxf(mx, __shfl_xor(mx, off, 64));
+  }
+  if (lane == 0) {
+    double xmin = (double)mn < 0.0 ? (double)mn : 0.0;
+    double xmax = (double)mx > 0.0 ? (double)mx : 0.0;
+    if (xmax == xmin) {
+      xmin = -1.0;
+      xmax = 1.0;
+    }
+    const float s = (float)((xmax - xmin) / (double)qmax);
+    S[gid] = s;
+    Z[gid] = (float)rint(-xmin / (double)s);
+  }
+}
+
+// qbar = (w + c * delta) / s + z and Y = s * qbar, elementwise over [n, m].
+__global__ __launch_bounds__(256) void centres_kernel(const float* __restrict__ W,
+                                                      const double* delta, double c,
+                                                      const float* __restrict__ S,
+                                                      const float* __restrict__ Z, int64_t n,
+                                                      int64_t m, int64_t g, int64_t G,
+                                                      double* __restrict__ qbar, double* Y) {
+  const int64_t total = n * m;
+  for (int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x; idx < total;
+       idx += (int64_t)gridDim.x * 256) {
+    const int64_t j = idx / m, l = idx % m;
+    const int64_t sg = j * G + l / g;
+    const double s = (double)S[sg];
+    double v = (double)W[idx];
+    if (delta) v += c * delta[idx];
+    const double qb = v / s + (double)Z[sg];
+    qbar[idx] = qb;
+    Y[idx] = s * qb;
+  }
+}
+
+// Y = s * qbar for a given qbar (decode-only entry).
+__global__ __launch_bounds__(256) void scale_centres_kernel(const double* __restrict__ qbar,
+                                                            const float* __restrict__ S, int64_t n,
+                                                            int64_t m, int64_t g, int64_t G,
+                                                            double* __restrict__ Y) {
+  const int64_t total = n * m;
+  for (int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x; idx < total;
+       idx += (int64_t)gridDim.x * 256) {
+    const int64_t j = idx / m, l = idx % m;
+    Y[idx] = (double)S[j * G + l / g] * qbar[idx];
+  }
+}
+
+// alpha_j = log_rho / min_i (R_ii s_j(i))^2 over the scaled basis Rbar_j.
+__global__ __launch_bounds__(256) void klein_alpha_kernel(const double* __restrict__ L,
+                                                          const float* __restrict__ S, int64_t n,
+                                                          int64_t m, int64_t g, int64_t G,
+                                                          double log_rho,
+                                                          double* __restrict__ alpha) {
+  const int64_t j = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (j >= n) return;
+  double mn = INFINITY;
+  for (int64_t i = 0; i < m; ++i) {
+    const double rb = L[i * m + i] * (double)S[j * G + i / g];
+    const double r2 = rb * rb;
+    mn = r2 < mn ? r2 : mn;
+  }
+  alpha[j] = log_rho / mn;
+}
+
+unsigned grid_for(int64_t total) {
+  const int64_t b = (total + 255) / 256;
+  return (unsigned)(b < 65536 ? (b > 0 ? b : 1) : 65536);
+}
+
+}  // namespace
+
+hipError_t launch_scale_zero(const float* W, int64_t n, int64_t m, int64_t g, int64_t G, int qmax,
+                             float* S, float* Z, hipStream_t stream) {
+  const int64_t groups = n * G;
+  scale_zero_kernel<<<(unsigned)((groups + 3) / 4), 256, 0, stream>>>(W, n, m, g, G, qmax, S, Z);
+  return hipGetLastError();
+}
+
+hipError_t launch_centres(const float* W, const double* delta, double c, const float* S,
+                          const float* Z, int64_t n, int64_t m, int64_t g, int64_t G,
+                          double* qbar, double* Y, hipStream_t stream) {
+  if (W == nullptr) {
+    scale_centres_kernel<<<grid_for(n * m), 256, 0, stream>>>(qbar, S, n, m, g, G, Y);
+  } else {
+    centres_kernel<<<grid_for(n * m), 256, 0, stream>>>(W, delta, c, S, Z, n, m, g, G, qbar, Y);
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_klein_alpha(const double* L, const float* S, int64_t n, int64_t m, int64_t g,
+                              int64_t G, double log_rho, double* alpha, hipStream_t stream) {
+  klein_alpha_kernel<<<(unsigned)((n + 255) / 256), 256, 0, stream>>>(L, S, n, m, g, G, log_rho,
+                                                                        alpha);
+  return hipGetLastError();
+}
+
+}  // namespace ojbkq

@@ -1,0 +1,277 @@
+"""GPU parity: the HIP path (through the C ABI) against the CPU fp64 oracle.
+
+Every input is seeded and synthetic; the oracle receives host copies of the
+very arrays the GPU consumed.  Sizes are chosen so that the oracle finishes in
+seconds while the GPU kernels still span several GEMM tiles (128), Cholesky
+panels (64), decoder blocks (32) and decoder workgroups (256 paths), with
+ragged tails everywhere.
+"""
+
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import paper_2602_08376_amd as ok
+from oracle import ojbkq as orc
+from parity import (SCALE_RTOL, check_paths, check_residuals, np64)
+from synth import CONFIGS, LayerConfig, make_layer, make_triangular_problem
+
+pytestmark = pytest.mark.gpu
+
+DEV = "cuda"
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    ok.library()          # fails loudly if the HIP library is missing
+    torch.cuda.init()
+
+
+def small_cfg(m, n, T, bits, group, K, seed, kind="heavy", sparsity=0.0, mu=0.5):
+    return LayerConfig(key=f"t{m}x{n}", title="test", n=n, m=m, T=T, bits=bits, group=group, K=K,
+                       mus=(mu,), w_std=0.02, kind=kind, data_seed=seed, klein_seed=seed + 7,
+                       outliers=2, outlier_gain=20.0, noise=0.05 if kind == "tiny" else 0.02,
+                       sparsity=sparsity)
+
+
+def run_pair(cfg, mu=None, lambda_rel=None):
+    mu = cfg.mu if mu is None else mu
+    lam = cfg.lambda_rel if lambda_rel is None else lambda_rel
+    W, Xr, Xq = make_layer(cfg, device=DEV)
+    g = ok.quantize_layer(W, Xr, Xq, mu, cfg.bits, cfg.group, cfg.K, cfg.klein_seed, lam)
+    torch.cuda.synchronize()
+    o = orc.quantize_layer(np64(W), np64(Xr), np64(Xq), mu, cfg.bits, cfg.group, cfg.K,
+                           cfg.klein_seed, lambda_rel=lam)
+    return (W, Xr, Xq), g, o
+
+
+def check_layer(cfg, g, o, mu):
+    S, Z = np64(g.scales), np64(g.zeros)
+    assert np.array_equal(S, o.scales), "scales differ"
+    assert np.array_equal(Z, o.zeros), "zero points differ"
+    assert np.all(np.abs(S - o.scales) <= SCALE_RTOL * np.abs(o.scales))
+    codes = np64(g.codes)
+    assert codes.max() <= (1 << cfg.bits) - 1
+    win = np64(g.winner)
+    res = np64(g.residuals)
+    frac = float((codes == o.codes).mean())
+    worst, nwin = check_residuals(res, win, o.residuals, o.winner)
+    print(f"[{cfg.key} mu={mu}] code agreement {frac:.6f}, winner mismatches {nwin}, "
+          f"worst residual rel err {worst:.2e}")
+    return frac
+
+
+# ---------------------------------------------------------------------------
+# hand-worked example (the 3x3 layer worked out by hand in tests/golden)
+# ---------------------------------------------------------------------------
+
+def test_hand_worked_layer(golden):
+    gd = golden("hand_worked_3x3.txt")
+    W = torch.tensor([gd["layer_W"]], dtype=torch.float32, device=DEV)
+    Xq = torch.tensor(gd["layer_Xq"], dtype=torch.float32, device=DEV).reshape(3, 3)
+    g = ok.quantize_layer(W, Xq, Xq, 1.0, 2, 128, 0, 0, lambda_rel=0.0)
+    assert np64(g.codes)[0].tolist() == [int(v) for v in gd["layer_codes"]]
+    assert abs(float(g.residuals[0]) - gd["layer_residual"][0]) < 5e-7
+    assert int(g.winner[0]) == 0
+
+
+def test_hand_worked_decode(golden):
+    gd = golden("hand_worked_3x3.txt")
+    R = torch.tensor(gd["decode_R"], dtype=torch.float64, device=DEV).reshape(3, 3)
+    qbar = torch.tensor([gd["decode_qbar"]], dtype=torch.float64, device=DEV)
+    S = torch.ones(1, 1, dtype=torch.float32, device=DEV)
+    codes, res, win, _, _ = ok.decode_stage(R, qbar, S, 2, 128, 0, 0)
+    assert np64(codes)[0].tolist() == [int(v) for v in gd["decode_babai"]]
+    assert abs(float(res[0]) - gd["decode_babai_residual"][0]) < 1e-12
+
+
+# ---------------------------------------------------------------------------
+# the decoder alone, on the oracle's own factor and centres
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("m,n,bits,group,K,seed", [
+    (7, 5, 2, 128, 6, 1),          # tiny, one partial block
+    (100, 23, 3, 40, 9, 2),        # ragged groups and blocks, several workgroups
+    (257, 40, 4, 128, 16, 3),      # > 256 paths, 9 blocks, 3 groups (ragged)
+    (64, 300, 4, 0, 0, 4),         # Babai only, 2 workgroups
+    (96, 11, 8, 32, 3, 5),         # 8-bit box (256 values)
+])
+def test_decode_stage_matches_oracle(m, n, bits, group, K, seed):
+    R, qbar, S = make_triangular_problem(m, n, orc.num_groups(m, group), seed)
+    if bits == 8:
+        qbar = qbar * 16.0
+    Rn, qn, Sn = R.numpy(), qbar.numpy(), S.numpy()
+    codes, res, win, pc, pr = ok.decode_stage(R.to(DEV), qbar.to(DEV), S.to(DEV), bits, group, K,
+                                              seed, want_paths=True)
+    dec = orc.decode(Rn, qn, Sn, bits, group, K, seed)
+    frac, ties = check_paths(Rn, qn, Sn, group, bits, K, seed, dec.alpha, np64(pc),
+                             dec.path_codes)
+    rel = np.abs(np64(pr) - dec.path_resid) / np.abs(dec.path_resid)
+    print(f"[decode m={m} n={n} b={bits} K={K}] agreement {frac:.6f} ties {ties} "
+          f"max path resid rel err {rel.max():.2e}")
+    assert rel.max() <= 1e-9
+    assert np.array_equal(np64(win), dec.winner)
+    assert np.array_equal(np64(codes), dec.codes)
+    assert np.all(np64(res) == np64(pr)[np.arange(n), np64(win)])
+
+
+def test_decode_brute_force_small():
+    """m = 6, b = 2: nothing beats the exact optimum, the choice never loses to Babai, and the
+    GPU reaches the optimum on exactly the instances where the oracle's own draws do."""
+    import itertools
+    hits = orc_hits = 0
+    pts = np.array(list(itertools.product(range(4), repeat=6)), dtype=np.float64)
+    for trial in range(6):
+        R, qbar, S = make_triangular_problem(6, 4, 1, 100 + trial, coupling=1.0, qbar_lo=-0.5,
+                                             qbar_hi=3.5)
+        S = torch.ones_like(S)
+        codes, res, win, pc, pr = ok.decode_stage(R.to(DEV), qbar.to(DEV), S.to(DEV), 2, 128, 300,
+                                                  trial, want_paths=True)
+        Rn, qn = R.numpy(), qbar.numpy()
+        dec = orc.decode(Rn, qn, S.numpy(), 2, 128, 300, trial)
+        for j in range(4):
+            r_opt = np.sum(((pts - qn[j][None, :]) @ Rn.T) ** 2, axis=1).min()
+            assert float(res[j]) >= r_opt - 1e-9
+            assert float(res[j]) <= float(pr[j, 0]) + 1e-15          # never worse than Babai
+            hits += int(abs(float(res[j]) - r_opt) <= 1e-9 * max(1.0, r_opt))
+            orc_hits += int(abs(dec.residuals[j] - r_opt) <= 1e-9 * max(1.0, r_opt))
+    print(f"[brute force] optimum reached on {hits}/24 columns (oracle {orc_hits}/24)")
+    assert hits == orc_hits
+    assert hits >= 12
+
+
+# ---------------------------------------------------------------------------
+# whole layer through the one-shot entry point
+# ---------------------------------------------------------------------------
+
+def test_tiny_config_c1():
+    cfg = CONFIGS["c1"]
+    _, g, o = run_pair(cfg)
+    frac = check_layer(cfg, g, o, cfg.mu)
+    assert frac == 1.0
+
+
+@pytest.mark.parametrize("m,n,T,bits,group,K,seed,mu", [
+    (200, 37, 300, 3, 128, 3, 11, 0.5),     # ragged group (72), ragged tiles
+    (130, 5, 257, 4, 0, 0, 12, 0.0),        # one group per column, Babai only, mu = 0
+    (300, 150, 700, 4, 128, 8, 13, 1.0),    # several tiles / panels / blocks, mu = 1
+    (1, 3, 5, 2, 128, 2, 14, 0.5),          # single input feature
+    (33, 2, 40, 8, 16, 5, 15, 0.25),        # 8-bit box
+])
+def test_layer_matches_oracle(m, n, T, bits, group, K, seed, mu):
+    cfg = small_cfg(m, n, T, bits, group, K, seed)
+    _, g, o = run_pair(cfg, mu=mu)
+    frac = check_layer(cfg, g, o, mu)
+    assert frac >= 0.999
+
+
+def test_heavy_tailed_layer_m1024():
+    """A slice of the 4096x4096 attention workload: heavy-tailed channels, 1% outliers x50."""
+    cfg = small_cfg(1024, 48, 4096, 4, 128, 16, 21)
+    _, g, o = run_pair(cfg)
+    frac = check_layer(cfg, g, o, cfg.mu)
+    assert frac >= 0.999
+
+
+def test_sparse_mlp_layer_3bit():
+    """Post-SiLU-like activations (60% near-zero), 3-bit box, as the down_proj workload."""
+    cfg = small_cfg(640, 40, 2048, 3, 128, 16, 22, sparsity=0.6)
+    _, g, o = run_pair(cfg)
+    frac = check_layer(cfg, g, o, cfg.mu)
+    assert frac >= 0.999
+
+
+# ---------------------------------------------------------------------------
+# intermediates of the staged entry points
+# ---------------------------------------------------------------------------
+
+def test_staged_intermediates_and_chunks():
+    cfg = small_cfg(300, 60, 1200, 4, 128, 8, 31)
+    W, Xr, Xq = make_layer(cfg, device=DEV)
+    s = ok.LayerSolver(cfg.m, cfg.n, cfg.bits, cfg.group, cfg.K, cfg.klein_seed, device=DEV)
+    for c0 in range(0, cfg.T, 400):          # three token chunks (views with row stride T)
+        s.accumulate(Xr[:, c0:c0 + 400], Xq[:, c0:c0 + 400])
+    g = s.solve(W, 0.5)
+    o = orc.quantize_layer(np64(W), np64(Xr), np64(Xq), 0.5, cfg.bits, cfg.group, cfg.K,
+                           cfg.klein_seed)
+    L = np64(s.inspect("L"))
+    colnorm = np.sqrt(np.sum(o.R ** 2, axis=0))          # sqrt(H_ll)
+    errR = np.max(np.abs(L.T - o.R) / colnorm[None, :])
+    assert errR < 1e-10, errR
+    lam2 = float(s.inspect("lam2")[0])
+    assert abs(lam2 - o.lam2) <= 1e-12 * o.lam2
+    qb = np64(s.inspect("qbar"))
+    errq = np.max(np.abs(qb - o.qbar))
+    assert errq < 1e-7, errq
+    al = np64(s.inspect("alpha"))
+    assert np.allclose(al, o.decode.alpha, rtol=1e-12)
+    pr = np64(s.inspect("path_resid"))
+    assert np.allclose(pr, o.decode.path_resid, rtol=1e-9)
+    print(f"[staged] R err {errR:.2e}, qbar err {errq:.2e}")
+    check_layer(cfg, g, o, 0.5)
+    # the one-shot call on the whole token set gives the same codes
+    one = ok.quantize_layer(W, Xr, Xq, 0.5, cfg.bits, cfg.group, cfg.K, cfg.klein_seed)
+    assert torch.equal(one.codes, g.codes)
+    assert np.allclose(np64(one.residuals), np64(g.residuals), rtol=1e-10)
+    s.close()
+
+
+def test_alpha_sweep_reuses_factor():
+    cfg = small_cfg(160, 20, 600, 3, 32, 5, 41)
+    W, Xr, Xq = make_layer(cfg, device=DEV)
+    s = ok.LayerSolver(cfg.m, cfg.n, cfg.bits, cfg.group, cfg.K, cfg.klein_seed, device=DEV)
+    s.accumulate(Xr, Xq)
+    for mu in (0.0, 0.5, 1.0):
+        g = s.solve(W, mu)
+        one = ok.quantize_layer(W, Xr, Xq, mu, cfg.bits, cfg.group, cfg.K, cfg.klein_seed)
+        assert torch.equal(one.codes, g.codes)
+        o = orc.quantize_layer(np64(W), np64(Xr), np64(Xq), mu, cfg.bits, cfg.group, cfg.K,
+                               cfg.klein_seed)
+        check_layer(cfg, g, o, mu)
+    with pytest.raises(ok.OjbkqError) as ei:
+        s.accumulate(Xr, Xq)
+    assert ei.value.code == "ESTATE"
+    s.close()
+
+
+def test_same_activations_make_mu_irrelevant():
+    cfg = small_cfg(96, 12, 300, 4, 32, 4, 51)
+    W, _, Xq = make_layer(cfg, device=DEV)
+    a = ok.quantize_layer(W, Xq, Xq, 0.0, cfg.bits, cfg.group, cfg.K, 3)
+    b = ok.quantize_layer(W, None, Xq, 1.0, cfg.bits, cfg.group, cfg.K, 3)
+    assert torch.equal(a.codes, b.codes)
+    assert torch.equal(a.residuals, b.residuals)
+
+
+# ---------------------------------------------------------------------------
+# invariants, determinism, failure path
+# ---------------------------------------------------------------------------
+
+def test_invariants_and_determinism():
+    cfg = small_cfg(256, 64, 1024, 4, 128, 12, 61)
+    W, Xr, Xq = make_layer(cfg, device=DEV)
+    a = ok.quantize_layer(W, Xr, Xq, 0.5, 4, 128, 12, 9)
+    b = ok.quantize_layer(W, Xr, Xq, 0.5, 4, 128, 12, 9)
+    assert torch.equal(a.codes, b.codes) and torch.equal(a.residuals, b.residuals)
+    z = ok.quantize_layer(W, Xr, Xq, 0.5, 4, 128, 0, 9)           # K = 0: Babai only
+    assert torch.all(z.winner == 0)
+    assert torch.all(a.residuals <= z.residuals)                   # chosen <= Babai
+    one = ok.quantize_layer(W, Xr, Xq, 0.5, 4, 128, 1, 9)          # K = 1: alpha = inf
+    assert torch.equal(one.codes, z.codes) and torch.all(one.winner == 0)
+    c = ok.quantize_layer(W, Xr, Xq, 0.5, 4, 128, 12, 10)          # another seed, other draws
+    assert not torch.equal(a.codes, c.codes)
+
+
+def test_not_positive_definite_reported():
+    cfg = small_cfg(40, 4, 100, 4, 128, 2, 71)
+    W, Xr, Xq = make_layer(cfg, device=DEV)
+    Xq = Xq.clone()
+    Xq[17] = 0.0
+    with pytest.raises(ok.OjbkqError) as ei:
+        ok.quantize_layer(W, Xr, Xq, 0.5, 4, 128, 2, 0, lambda_rel=0.0)
+    assert ei.value.code == "ENOTPD" and "17" in str(ei.value)
+    ok.quantize_layer(W, Xr, Xq, 0.5, 4, 128, 2, 0, lambda_rel=0.01)   # damping repairs it
