@@ -55,6 +55,34 @@ def parse():
     return ap.parse_args()
 
 
+KERNEL_SOURCES = ("paper_2602_08376_amd/csrc/gemm.hip", "paper_2602_08376_amd/csrc/device.h")
+
+
+def measured_traffic(kernel, workload):
+    """HBM bytes per launch from the committed rocprofv3 FETCH_SIZE / WRITE_SIZE passes.
+
+    Returns None when no summary covers (kernel, workload) or when the kernel's
+    sources changed since the counters were taken (hash recorded in the summary).
+    """
+    import glob
+    import hashlib
+    h = hashlib.sha256()
+    for rel in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, rel), "rb") as f:
+            h.update(f.read())
+    digest = h.hexdigest()[:16]
+    for path in sorted(glob.glob(os.path.join(ROOT, "profiles", "*.md"))):
+        with open(path) as f:
+            for line in f:
+                if not line.startswith("traffic "):
+                    continue
+                kv = dict(t.split("=", 1) for t in line.split()[1:])
+                if (kv.get("kernel") == kernel and kv.get("workload") == workload
+                        and kv.get("source_sha256_16") == digest):
+                    return float(kv["bytes_per_launch"])
+    return None
+
+
 def workload_desc(cfg):
     return {
         "workload": f"{cfg.key}: {cfg.title}",
@@ -212,8 +240,9 @@ def main():
             "peak": PEAK_F64_MFMA_TFLOPS,
             "unit": "TFLOP/s",
             "frac": achieved / PEAK_F64_MFMA_TFLOPS,
-            "traffic": None,
+            "traffic": measured_traffic("gram_cross_kernel", cfg.key),
             "algorithmic_flops_per_launch": flops,
+            "algorithmic_bytes_per_launch": 8.0 * m * Tc + 16.0 * m * m,
         },
         "checks": {"codes_max": int(out.codes.max()),
                    "mean_winner_is_klein": float((out.winner > 0).float().mean())},
