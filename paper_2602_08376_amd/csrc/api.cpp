@@ -58,7 +58,7 @@ Shape shape_of(const ojbkq_params& p) {
 // Offsets of every buffer carved from the workspace.
 struct Layout {
   size_t status = 0, lam2 = 0, G = 0, E = 0, U = 0, qbar = 0, gq = 0, alpha = 0, pcodes = 0,
-         presid = 0, total = 0;
+         presid = 0, gc_scratch = 0, total = 0;
 };
 
 Layout layout_full(const Shape& s) {
@@ -81,8 +81,19 @@ Layout layout_full(const Shape& s) {
   L.alpha = take((size_t)s.n * sizeof(double));
   L.pcodes = take((size_t)s.nwg * ojbkq::kDecodeThreads * (size_t)s.m);
   L.presid = take((size_t)s.nwg * ojbkq::kDecodeThreads * sizeof(double));
+  L.gc_scratch = take(ojbkq::gram_cross_scratch_bytes());
   L.total = off;
   return L;
+}
+
+// Resident workgroups of the Gram kernel on the current device: two per CU.
+int gram_shares() {
+  int dev = 0, cus = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return ojbkq::kGramCrossMaxShares;
+  if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+      cus <= 0)
+    return ojbkq::kGramCrossMaxShares;
+  return 2 * cus;
 }
 
 Layout layout_decode(const Shape& s) {
@@ -194,7 +205,8 @@ int ctx_accumulate(ojbkq_ctx* c, const float* Xr, const float* Xq, int64_t T, in
   if (ldx < T) return fail(OJBKQ_EINVAL, "ldx must be >= T");
   const bool cross = Xr != nullptr && Xr != Xq;
   OJBKQ_HIP(ojbkq::gram_cross(Xq, cross ? Xr : nullptr, c->s.m, T, ldx, c->at<double>(c->L.G),
-                              c->at<double>(c->L.E), c->any_chunk, c->cross_seen, c->stream),
+                              c->at<double>(c->L.E), c->any_chunk, c->cross_seen,
+                              c->at<void>(c->L.gc_scratch), gram_shares(), c->stream),
             "gram and cross term");
   if (cross) c->cross_seen = true;
   c->any_chunk = true;
@@ -223,6 +235,8 @@ int ctx_solve(ojbkq_ctx* c, const float* W, double alpha, uint8_t* codes, float*
   hipStream_t st = c->stream;
   double* Lf = c->at<double>(c->L.G);
   if (!c->factored) {
+    if (c->cross_seen)   // mixed product -> cross term, while G is still the Gram
+      OJBKQ_HIP(ojbkq::cross_from_mixed(c->at<double>(c->L.E), Lf, s.m, st), "cross term");
     OJBKQ_HIP(ojbkq::launch_damp(Lf, s.m, c->p.lambda_rel, c->at<double>(c->L.lam2), st), "damp");
     OJBKQ_HIP(ojbkq::cholesky_lower(Lf, s.m, c->at<int>(c->L.status), st), "cholesky");
     c->factored = true;

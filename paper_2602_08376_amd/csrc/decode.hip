@@ -41,21 +41,30 @@ __device__ __forceinline__ int babai_round(double c, int qmax) {
 // normalised by the largest weight (the nearest box point): the smallest v
 // whose running weight sum exceeds u times the total; if rounding leaves
 // none, the largest v with a non-zero weight.  kappa = inf: nearest point.
+// Only the window of v whose exponent is >= -750 is evaluated: outside it
+// exp() is exactly 0 in double precision, so the sums are unchanged.
 __device__ __noinline__ int klein_pick(double c, double kappa, double u, int qmax) {
   if (!(kappa < INFINITY)) return babai_round(c, qmax);
   const double nk = -kappa;
   const double vs = fmin(fmax(rint(c), 0.0), (double)qmax);
   const double ts = c - vs;
   const double top = nk * (ts * ts);   // the largest exponent
+  int lo = 0, hi = qmax;
+  if (kappa > 0.0) {
+    const double rad = sqrt(750.0 / kappa + ts * ts) + 1.0;
+    const double a = ceil(c - rad), b = floor(c + rad);
+    if (a > 0.0) lo = a > (double)qmax ? qmax : (int)a;
+    if (b < (double)qmax) hi = b < 0.0 ? 0 : (int)b;
+  }
   double total = 0.0;
-  for (int v = 0; v <= qmax; ++v) {
+  for (int v = lo; v <= hi; ++v) {
     const double t = c - (double)v;
     total += exp(nk * (t * t) - top);
   }
   const double thr = u * total;
   double cum = 0.0;
   int last = -1;
-  for (int v = 0; v <= qmax; ++v) {
+  for (int v = lo; v <= hi; ++v) {
     const double t = c - (double)v;
     const double w = exp(nk * (t * t) - top);
     cum += w;
@@ -65,9 +74,21 @@ __device__ __noinline__ int klein_pick(double c, double kappa, double u, int qma
   return last < 0 ? (int)vs : last;
 }
 
+constexpr int kFC = 32;          // decided rows per staged chunk of the lazy update
+constexpr int kQRow = 320;       // bytes per staged code row (256 paths + bank padding)
+constexpr int kAccBytes = kBS * kDecodeThreads * (int)sizeof(double);
+constexpr int kRBytes = 2 * kFC * kBS * (int)sizeof(double);
+constexpr int kQBytes = 2 * kFC * kQRow;
+static_assert(kRBytes + kQBytes <= kAccBytes, "staging buffers must fit in the update buffer");
+
 __global__ __launch_bounds__(256, 2) void decode_kernel(DecodeDesc d) {
-  __shared__ double sAcc[kBS][kDecodeThreads];   // lazy-update result, [row][path]
+  // The staged R / code chunks of the lazy update and its [row][path] result
+  // are never live together, so they share one buffer.
+  __shared__ __align__(16) unsigned char smem[kAccBytes];
   __shared__ double sT[kBS][kBS + 1];            // sT[r][c] = R[i0 + c][i0 + r], c <= r
+  double (*sAcc)[kDecodeThreads] = reinterpret_cast<double (*)[kDecodeThreads]>(smem);
+  double (*sR)[kFC][kBS] = reinterpret_cast<double (*)[kFC][kBS]>(smem);
+  unsigned char (*sQ)[kFC][kQRow] = reinterpret_cast<unsigned char (*)[kFC][kQRow]>(smem + kRBytes);
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int64_t m = d.m, g = d.g, G = d.G;
@@ -94,6 +115,8 @@ __global__ __launch_bounds__(256, 2) void decode_kernel(DecodeDesc d) {
     bval[t] = pb < P;
     bcol[t] = bval[t] ? pb / kp1 : 0;
   }
+  // cooperative staging: thread -> (chunk row tid / 8, 4 R values / 32 code bytes)
+  const int sff = tid >> 3, spart = tid & 7;
 
   double resid = 0.0;
   const int64_t nblk = (m + kBS - 1) / kBS;
@@ -115,33 +138,69 @@ __global__ __launch_bounds__(256, 2) void decode_kernel(DecodeDesc d) {
 #pragma unroll
       for (int t = 0; t < 4; ++t) acc[a][t] = d4{0.0, 0.0, 0.0, 0.0};
     if (i1 < m) {
-      int64_t f = i1 + (lane >> 4);
+      const int64_t nch = (m - i1 + kFC - 1) / kFC;
+      // prefetch registers of the next chunk (kept as scalars so that they stay in VGPRs)
+      double rr0, rr1, rr2, rr3;
+      uint4 rq0, rq1;
+#define OJBKQ_DECODE_FETCH(F0)                                                             \
+  {                                                                                        \
+    const int64_t f_ = (F0) + sff;                                                         \
+    const bool fin_ = f_ < m;                                                              \
+    const int64_t col_ = i0 + spart * 4;                                                   \
+    const double* lp_ = d.L + (fin_ ? f_ * m : 0) + col_;                                  \
+    rr0 = (fin_ && col_ + 0 < i1) ? lp_[0] : 0.0;                                          \
+    rr1 = (fin_ && col_ + 1 < i1) ? lp_[1] : 0.0;                                          \
+    rr2 = (fin_ && col_ + 2 < i1) ? lp_[2] : 0.0;                                          \
+    rr3 = (fin_ && col_ + 3 < i1) ? lp_[3] : 0.0;                                          \
+    if (fin_) {                                                                            \
+      const uint4* src_ = reinterpret_cast<const uint4*>(cw + f_ * kDecodeThreads + spart * 32); \
+      rq0 = src_[0];                                                                       \
+      rq1 = src_[1];                                                                       \
+    } else {                                                                               \
+      rq0 = make_uint4(0u, 0u, 0u, 0u);                                                    \
+      rq1 = rq0;                                                                           \
+    }                                                                                      \
+  }
+      OJBKQ_DECODE_FETCH(i1)
+      int64_t f = i1 + (lane >> 4);   // this lane's row of operand B
       int64_t gnext = -1;
       double sb[4] = {0.0, 0.0, 0.0, 0.0};
-      const uint8_t* crow = cw + wave * 64 + 4 * (lane & 15);
-      for (int64_t f0 = i1; f0 < m; f0 += 4, f += 4) {
-        const bool fin = f < m;
-        if (fin && f >= gnext) {
-          const int64_t grp = f / g;
-          gnext = (grp + 1) * g;
+      for (int64_t ch = 0; ch < nch; ++ch) {
+        const int buf = (int)(ch & 1);
+        sR[buf][sff][spart * 4 + 0] = rr0;
+        sR[buf][sff][spart * 4 + 1] = rr1;
+        sR[buf][sff][spart * 4 + 2] = rr2;
+        sR[buf][sff][spart * 4 + 3] = rr3;
+        uint4* qd = reinterpret_cast<uint4*>(&sQ[buf][sff][spart * 32]);
+        qd[0] = rq0;
+        qd[1] = rq1;
+        __syncthreads();
+        if (ch + 1 < nch) OJBKQ_DECODE_FETCH(i1 + (ch + 1) * kFC)
 #pragma unroll
-          for (int t = 0; t < 4; ++t) sb[t] = bval[t] ? (double)d.S[bcol[t] * G + grp] : 0.0;
+        for (int s4 = 0; s4 < kFC / 4; ++s4, f += 4) {
+          const int ff = s4 * 4 + (lane >> 4);
+          if (f < m && f >= gnext) {
+            const int64_t grp = f / g;
+            gnext = (grp + 1) * g;
+#pragma unroll
+            for (int t = 0; t < 4; ++t) sb[t] = bval[t] ? (double)d.S[bcol[t] * G + grp] : 0.0;
+          }
+          double av[2];
+#pragma unroll
+          for (int a = 0; a < 2; ++a) av[a] = sR[buf][ff][16 * a + (lane & 15)];
+          const uint32_t c4 =
+              *reinterpret_cast<const uint32_t*>(&sQ[buf][ff][wave * 64 + 4 * (lane & 15)]);
+          double bv[4];
+#pragma unroll
+          for (int t = 0; t < 4; ++t) bv[t] = (double)((c4 >> (8 * t)) & 255u) * sb[t];
+#pragma unroll
+          for (int a = 0; a < 2; ++a)
+#pragma unroll
+            for (int t = 0; t < 4; ++t) acc[a][t] = mfma_f64(av[a], bv[t], acc[a][t]);
         }
-        double av[2];
-#pragma unroll
-        for (int a = 0; a < 2; ++a) {
-          const int64_t row = i0 + 16 * a + (lane & 15);
-          av[a] = (fin && row < i1) ? d.L[f * m + row] : 0.0;
-        }
-        const uint32_t c4 = fin ? *reinterpret_cast<const uint32_t*>(crow + f * kDecodeThreads) : 0u;
-        double bv[4];
-#pragma unroll
-        for (int t = 0; t < 4; ++t) bv[t] = (double)((c4 >> (8 * t)) & 255u) * sb[t];
-#pragma unroll
-        for (int a = 0; a < 2; ++a)
-#pragma unroll
-          for (int t = 0; t < 4; ++t) acc[a][t] = mfma_f64(av[a], bv[t], acc[a][t]);
       }
+      __syncthreads();   // every wave is done with the staged chunks (aliased below)
+#undef OJBKQ_DECODE_FETCH
     }
 #pragma unroll
     for (int a = 0; a < 2; ++a)

@@ -211,24 +211,6 @@ __global__ __launch_bounds__(256, 2) void gemm_f64_kernel(GemmArgs g) {
   gemm_tile<TA, TB, AK, BK, BDIFF>(g, ti, tj, sA, sB);
 }
 
-// The calibration-set contractions of one token chunk in one launch: the
-// first n_gram workgroups take the lower-triangle tiles of G += X_q X_q^T,
-// the rest every tile of E += X_q (X_ref - X_q)^T.
-__global__ __launch_bounds__(256, 2) void gram_cross_kernel(GemmArgs gG, GemmArgs gE,
-                                                            int64_t n_gram) {
-  __shared__ double sA[kKC][kLdsLd];
-  __shared__ double sB[kKC][kLdsLd];
-  const int64_t t = xcd_tile_number();
-  int64_t ti, tj;
-  if (t < n_gram) {
-    lower_tile(t, ti, tj);
-    gemm_tile<float, float, false, false, false>(gG, ti, tj, sA, sB);
-  } else {
-    raster_tile(t - n_gram, gE.tiles_m, gE.tiles_n, ti, tj);
-    gemm_tile<float, float, false, false, true>(gE, ti, tj, sA, sB);
-  }
-}
-
 template <typename TA, typename TB, bool AK, bool BK, bool BDIFF>
 hipError_t launch(const GemmArgs& g, int64_t ntiles, hipStream_t s) {
   gemm_f64_kernel<TA, TB, AK, BK, BDIFF><<<dim3((unsigned)ntiles), dim3(256), 0, s>>>(g);
@@ -269,31 +251,6 @@ hipError_t gemm_f64(const GemmDesc& d, hipStream_t stream) {
   if (d.ta == Elt::F32 && d.tb == Elt::F64 && !d.a_kmajor && !d.b_kmajor)
     return launch<float, double, false, false, false>(g, ntiles, stream);
   return hipErrorInvalidValue;
-}
-
-hipError_t gram_cross(const float* Xq, const float* Xr, int64_t m, int64_t T, int64_t ldx,
-                      double* G, double* E, bool accumulate_g, bool accumulate_e,
-                      hipStream_t stream) {
-  if (m <= 0) return hipSuccess;
-  GemmArgs gG;
-  gG.M = m; gG.N = m; gG.Kd = T < 0 ? 0 : T;
-  gG.A = Xq; gG.lda = ldx; gG.B = Xq; gG.B2 = nullptr; gG.ldb = ldx;
-  gG.C = G; gG.ldc = m; gG.alpha = 1.0; gG.beta = accumulate_g ? 1.0 : 0.0;
-  gG.tiles_m = gG.tiles_n = (m + kTile - 1) / kTile;
-  gG.lower = 1;
-  gG.vec_a = gG.vec_b = vec_ok(Xq, ldx, Elt::F32) ? 1 : 0;
-  const int64_t n_gram = gG.tiles_m * (gG.tiles_m + 1) / 2;
-  int64_t n_cross = 0;
-  GemmArgs gE = gG;
-  if (Xr != nullptr) {
-    gE.B = Xr; gE.B2 = Xq; gE.C = E; gE.beta = accumulate_e ? 1.0 : 0.0; gE.lower = 0;
-    gE.vec_b = (vec_ok(Xr, ldx, Elt::F32) && vec_ok(Xq, ldx, Elt::F32)) ? 1 : 0;
-    n_cross = gE.tiles_m * gE.tiles_n;
-  }
-  const int64_t total = n_gram + n_cross;
-  if (total > 0x7fffffff) return hipErrorInvalidValue;
-  gram_cross_kernel<<<dim3((unsigned)total), dim3(256), 0, stream>>>(gG, gE, n_gram);
-  return hipGetLastError();
 }
 
 }  // namespace ojbkq

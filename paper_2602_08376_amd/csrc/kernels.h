@@ -36,13 +36,22 @@ struct GemmDesc {
 
 hipError_t gemm_f64(const GemmDesc& d, hipStream_t stream);
 
-// One token chunk of the calibration sums in a single launch:
+// One token chunk of the calibration sums in a single persistent launch
+// (plus a small fix-up launch):
 //   G (lower triangle by 128-tiles) = [G +] X_q X_q^T
-//   E (all of it, only if Xr != nullptr) = [E +] X_q (X_ref - X_q)^T
+//   E (all of it, only if Xr != nullptr) = [E +] X_q X_ref^T   (mixed product)
 // X_q, X_ref: [m, T] float32 with row stride ldx; G, E: [m, m] float64.
+// scratch: gram_cross_scratch_bytes() of device memory for partial tiles;
+// max_shares: workgroups to use (two per CU is the resident maximum).
+constexpr int kGramCrossMaxShares = 512;
+size_t gram_cross_scratch_bytes();
 hipError_t gram_cross(const float* Xq, const float* Xr, int64_t m, int64_t T, int64_t ldx,
-                      double* G, double* E, bool accumulate_g, bool accumulate_e,
-                      hipStream_t stream);
+                      double* G, double* E, bool accumulate_g, bool accumulate_e, void* scratch,
+                      int max_shares, hipStream_t stream);
+// E <- E - G (G read through symmetry): turns the accumulated mixed product
+// X_q X_ref^T into the cross term X_q (X_ref - X_q)^T.  Call before G is
+// factored.
+hipError_t cross_from_mixed(double* E, const double* G, int64_t m, hipStream_t stream);
 
 // ---- scales and zero points (Alg. 1 step 1) --------------------------------
 hipError_t launch_scale_zero(const float* W, int64_t n, int64_t m, int64_t g, int64_t G, int qmax,
