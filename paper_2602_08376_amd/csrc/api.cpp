@@ -38,7 +38,8 @@ constexpr int kStatusClear = 0x7f7f7f7f;   // byte-fill value meaning "no bad pi
 size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 
 struct Shape {
-  int64_t m, n, g, G, K, paths, nwg;
+  int64_t m, n, g, G, K, paths;
+  ojbkq::DecodeGeom geo;
   int qmax;
 };
 
@@ -50,7 +51,7 @@ Shape shape_of(const ojbkq_params& p) {
   s.G = (s.m + s.g - 1) / s.g;
   s.K = p.K;
   s.paths = p.n * (int64_t)(p.K + 1);
-  s.nwg = ojbkq::decode_workgroups(p.n, p.K);
+  s.geo = ojbkq::decode_geometry(p.n, p.K);
   s.qmax = (1 << p.bits) - 1;
   return s;
 }
@@ -79,8 +80,8 @@ Layout layout_full(const Shape& s) {
   L.qbar = take(nm);
   L.gq = take(nm);
   L.alpha = take((size_t)s.n * sizeof(double));
-  L.pcodes = take((size_t)s.nwg * ojbkq::kDecodeThreads * (size_t)s.m);
-  L.presid = take((size_t)s.nwg * ojbkq::kDecodeThreads * sizeof(double));
+  L.pcodes = take((size_t)s.geo.nwg * (size_t)s.geo.threads * (size_t)s.m);
+  L.presid = take((size_t)s.paths * sizeof(double));
   L.gc_scratch = take(ojbkq::gram_cross_scratch_bytes());
   L.total = off;
   return L;
@@ -110,8 +111,8 @@ Layout layout_decode(const Shape& s) {
   L.U = take(nm);
   L.gq = take(nm);
   L.alpha = take((size_t)s.n * sizeof(double));
-  L.pcodes = take((size_t)s.nwg * ojbkq::kDecodeThreads * (size_t)s.m);
-  L.presid = take((size_t)s.nwg * ojbkq::kDecodeThreads * sizeof(double));
+  L.pcodes = take((size_t)s.geo.nwg * (size_t)s.geo.threads * (size_t)s.m);
+  L.presid = take((size_t)s.paths * sizeof(double));
   L.total = off;
   return L;
 }
@@ -274,11 +275,12 @@ int ctx_solve(ojbkq_ctx* c, const float* W, double alpha, uint8_t* codes, float*
   d.L = Lf; d.gq = gq; d.S = scales; d.alpha = al;
   d.m = s.m; d.n = s.n; d.g = s.g; d.G = s.G; d.K = (int)s.K; d.bits = c->p.bits;
   d.seed = c->p.seed;
+  d.wg_paths = s.geo.wg_paths; d.threads = s.geo.threads;
   d.pcodes = c->at<uint8_t>(c->L.pcodes);
   d.presid = c->at<double>(c->L.presid);
   OJBKQ_HIP(ojbkq::launch_decode(d, st), "decode");
-  OJBKQ_HIP(ojbkq::launch_select(d.pcodes, d.presid, s.n, s.m, (int)s.K, codes, residuals, winner,
-                                 nullptr, nullptr, st),
+  OJBKQ_HIP(ojbkq::launch_select(d.pcodes, d.presid, s.n, s.m, (int)s.K, s.geo, codes, residuals,
+                                 winner, nullptr, nullptr, st),
             "select");
   c->solved = true;
   return finish(c);
@@ -407,11 +409,12 @@ int ojbkq_decode_stage(const ojbkq_params* p, const double* R, const double* qba
   ojbkq::DecodeDesc d;
   d.L = Lf; d.gq = gq; d.S = scales; d.alpha = al;
   d.m = s.m; d.n = s.n; d.g = s.g; d.G = s.G; d.K = (int)s.K; d.bits = p->bits; d.seed = p->seed;
+  d.wg_paths = s.geo.wg_paths; d.threads = s.geo.threads;
   d.pcodes = reinterpret_cast<uint8_t*>(ws + L.pcodes);
   d.presid = reinterpret_cast<double*>(ws + L.presid);
   OJBKQ_HIP(ojbkq::launch_decode(d, st), "decode");
-  OJBKQ_HIP(ojbkq::launch_select(d.pcodes, d.presid, s.n, s.m, (int)s.K, codes, residuals, winner,
-                                 path_codes, path_resid, st),
+  OJBKQ_HIP(ojbkq::launch_select(d.pcodes, d.presid, s.n, s.m, (int)s.K, s.geo, codes, residuals,
+                                 winner, path_codes, path_resid, st),
             "select");
   OJBKQ_HIP(hipStreamSynchronize(st), "stream sync");
   return OJBKQ_OK;

@@ -8,13 +8,15 @@
 // the one shared factor R: path 0 rounds each centre to the nearest box point,
 // paths 1..K draw each code from Pr(v) ~ exp(-alpha_j Rbar_ii^2 (c_i - v)^2).
 //
-// Layout.  A workgroup owns 256 consecutive paths (path p = j (K + 1) + k),
-// one per lane, and walks the rows i = m-1 .. 0 in blocks of kBS rows.  With
+// Layout.  A workgroup owns wg_paths consecutive paths (path p = j (K + 1) +
+// k), one per lane; wg_paths is chosen so that all workgroups of a round fit
+// one per CU.  It walks the rows i = m-1 .. 0 in blocks of kBS rows.  With
 // e_l = s_j(l) q_l the centre of row i is
 //     c_i = z_i / Rbar_ii,  z_i = (Rbar_j qbar_j)_i - sum_{l > i} R_il e_l,
 // where (Rbar_j qbar_j) is precomputed for every column by one GEMM.  The
 // sum splits into
-//   * rows l of earlier blocks: one 32 x |F| by |F| x 64 product per wave,
+//   * rows l of earlier blocks: one 32 x |F| by |F| x 64 product per wave
+//     (16-path tiles that hold no path are skipped),
 //     R (shared by every path, streamed from L2 as rows of L = R^T) against
 //     the codes already decided (bytes, scaled by s on the fly), on
 //     v_mfma_f64_16x16x4_f64 -- the lazy batched update;
@@ -22,8 +24,8 @@
 //     with the 32x32 diagonal block of R broadcast from LDS.
 // The MFMA result is transposed through LDS so that each lane then holds
 // the 32 partial centres of its own path for the serial in-block steps.
-// Decided codes go to a per-workgroup [m][256] byte buffer that is both the
-// operand of later updates and the source of the selection gather.
+// Decided codes go to a per-workgroup [m][threads] byte buffer that is both
+// the operand of later updates and the source of the selection gather.
 #include "kernels.h"
 #include "device.h"
 
@@ -74,49 +76,57 @@ __device__ __noinline__ int klein_pick(double c, double kappa, double u, int qma
   return last < 0 ? (int)vs : last;
 }
 
-constexpr int kFC = 32;          // decided rows per staged chunk of the lazy update
-constexpr int kQRow = 320;       // bytes per staged code row (256 paths + bank padding)
-constexpr int kAccBytes = kBS * kDecodeThreads * (int)sizeof(double);
+constexpr int kFC = 64;          // decided rows per staged chunk of the lazy update
+constexpr int kMaxT = kDecodeMaxThreads;
+constexpr int kQPad = 16;        // bank padding of a staged code row (bytes)
+constexpr int kAccBytes = kBS * kMaxT * (int)sizeof(double);
 constexpr int kRBytes = 2 * kFC * kBS * (int)sizeof(double);
-constexpr int kQBytes = 2 * kFC * kQRow;
-static_assert(kRBytes + kQBytes <= kAccBytes, "staging buffers must fit in the update buffer");
+constexpr int kQBytesMax = 2 * kFC * (kMaxT + kQPad);
+constexpr int kMinT = 256;                       // workgroups have 256 .. 512 lanes
+constexpr int kRPer = (kFC * kBS + kMinT - 1) / kMinT;   // R values staged per thread, at most
+constexpr int kQPer = kFC / 16;                  // 16-byte code packets per thread
+static_assert(kRBytes + kQBytesMax <= kAccBytes, "staging buffers must fit in the update buffer");
 
-__global__ __launch_bounds__(256, 2) void decode_kernel(DecodeDesc d) {
+__global__ __launch_bounds__(kMaxT, 2) void decode_kernel(DecodeDesc d) {
   // The staged R / code chunks of the lazy update and its [row][path] result
   // are never live together, so they share one buffer.
   __shared__ __align__(16) unsigned char smem[kAccBytes];
   __shared__ double sT[kBS][kBS + 1];            // sT[r][c] = R[i0 + c][i0 + r], c <= r
-  double (*sAcc)[kDecodeThreads] = reinterpret_cast<double (*)[kDecodeThreads]>(smem);
-  double (*sR)[kFC][kBS] = reinterpret_cast<double (*)[kFC][kBS]>(smem);
-  unsigned char (*sQ)[kFC][kQRow] = reinterpret_cast<unsigned char (*)[kFC][kQRow]>(smem + kRBytes);
+  const int T = d.threads;                       // lanes (= code-row bytes) per workgroup
+  const int qrow = T + kQPad;
+  double* const sAcc = reinterpret_cast<double*>(smem);                  // [kBS][T]
+  double (*sR)[kFC][kBS] = reinterpret_cast<double (*)[kFC][kBS]>(smem);  // [2][kFC][kBS]
+  unsigned char* const sQ = smem + kRBytes;                              // [2][kFC][qrow]
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int64_t m = d.m, g = d.g, G = d.G;
   const int64_t kp1 = (int64_t)d.K + 1;
   const int64_t P = d.n * kp1;
   const int64_t wg = blockIdx.x;
-  const int64_t p = wg * kDecodeThreads + tid;
-  const bool valid = p < P;
+  const int64_t base = wg * d.wg_paths;           // first path of this workgroup
+  const int64_t npaths = (P - base) < d.wg_paths ? (P - base) : d.wg_paths;
+  const int64_t p = base + tid;
+  const bool valid = tid < npaths;
   const int64_t j = valid ? p / kp1 : 0;
   const uint32_t kk = valid ? (uint32_t)(p % kp1) : 0u;
   const int qmax = (1 << d.bits) - 1;
   const double alpha_j = valid ? d.alpha[j] : 0.0;
-  uint8_t* const cw = d.pcodes + wg * m * kDecodeThreads;
+  uint8_t* const cw = d.pcodes + wg * m * T;
   const double* const gq = d.gq + j * m;
   const float* const Sj = d.S + j * G;
 
-  // MFMA operand B: this lane feeds wave-local paths 4 (lane % 16) + t of
-  // tile t, so its four codes for one row are four adjacent bytes.
+  // MFMA operand B: tile t of this wave covers its paths 16 t .. 16 t + 15;
+  // this lane feeds path 16 t + (lane % 16) of each.
   int64_t bcol[4];
   bool bval[4];
+  int ntile = 0;   // tiles of this wave holding at least one path
 #pragma unroll
   for (int t = 0; t < 4; ++t) {
-    const int64_t pb = wg * kDecodeThreads + wave * 64 + 4 * (lane & 15) + t;
-    bval[t] = pb < P;
-    bcol[t] = bval[t] ? pb / kp1 : 0;
+    const int64_t local = wave * 64 + 16 * t + (lane & 15);
+    bval[t] = local < npaths;
+    bcol[t] = bval[t] ? (base + local) / kp1 : 0;
+    if (wave * 64 + 16 * t < npaths) ntile = t + 1;
   }
-  // cooperative staging: thread -> (chunk row tid / 8, 4 R values / 32 code bytes)
-  const int sff = tid >> 3, spart = tid & 7;
 
   double resid = 0.0;
   const int64_t nblk = (m + kBS - 1) / kBS;
@@ -126,7 +136,7 @@ __global__ __launch_bounds__(256, 2) void decode_kernel(DecodeDesc d) {
     const int bl = (int)(i1 - i0);
 
     __syncthreads();   // the previous block is done with sT / sAcc / codes
-    for (int e = tid; e < kBS * kBS; e += kDecodeThreads) {
+    for (int e = tid; e < kBS * kBS; e += T) {
       const int r = e / kBS, c = e % kBS;
       sT[r][c] = (r < bl && c <= r) ? d.L[(i0 + r) * m + i0 + c] : 0.0;
     }
@@ -139,27 +149,26 @@ __global__ __launch_bounds__(256, 2) void decode_kernel(DecodeDesc d) {
       for (int t = 0; t < 4; ++t) acc[a][t] = d4{0.0, 0.0, 0.0, 0.0};
     if (i1 < m) {
       const int64_t nch = (m - i1 + kFC - 1) / kFC;
-      // prefetch registers of the next chunk (kept as scalars so that they stay in VGPRs)
-      double rr0, rr1, rr2, rr3;
-      uint4 rq0, rq1;
-#define OJBKQ_DECODE_FETCH(F0)                                                             \
-  {                                                                                        \
-    const int64_t f_ = (F0) + sff;                                                         \
-    const bool fin_ = f_ < m;                                                              \
-    const int64_t col_ = i0 + spart * 4;                                                   \
-    const double* lp_ = d.L + (fin_ ? f_ * m : 0) + col_;                                  \
-    rr0 = (fin_ && col_ + 0 < i1) ? lp_[0] : 0.0;                                          \
-    rr1 = (fin_ && col_ + 1 < i1) ? lp_[1] : 0.0;                                          \
-    rr2 = (fin_ && col_ + 2 < i1) ? lp_[2] : 0.0;                                          \
-    rr3 = (fin_ && col_ + 3 < i1) ? lp_[3] : 0.0;                                          \
-    if (fin_) {                                                                            \
-      const uint4* src_ = reinterpret_cast<const uint4*>(cw + f_ * kDecodeThreads + spart * 32); \
-      rq0 = src_[0];                                                                       \
-      rq1 = src_[1];                                                                       \
-    } else {                                                                               \
-      rq0 = make_uint4(0u, 0u, 0u, 0u);                                                    \
-      rq1 = rq0;                                                                           \
-    }                                                                                      \
+      const int qpk = T / 16;            // 16-byte packets per code row
+      double rr[kRPer];
+      uint4 rq[kQPer];
+      // stage rows f0 .. f0 + kFC of R (columns i0 .. i1) and of the codes
+#define OJBKQ_DECODE_FETCH(F0)                                                          \
+  {                                                                                     \
+    _Pragma("unroll") for (int q_ = 0; q_ < kRPer; ++q_) {                              \
+      const int e_ = tid + q_ * T;                                                      \
+      const int ff_ = e_ / kBS, cc_ = e_ % kBS;                                         \
+      const int64_t f_ = (F0) + ff_;                                                    \
+      rr[q_] = (e_ < kFC * kBS && f_ < m && i0 + cc_ < i1) ? d.L[f_ * m + i0 + cc_] : 0.0; \
+    }                                                                                   \
+    _Pragma("unroll") for (int q_ = 0; q_ < kQPer; ++q_) {                              \
+      const int e_ = tid + q_ * T;                                                      \
+      const int ff_ = e_ / qpk, cc_ = e_ % qpk;                                         \
+      const int64_t f_ = (F0) + ff_;                                                    \
+      rq[q_] = (ff_ < kFC && f_ < m)                                                    \
+                   ? *reinterpret_cast<const uint4*>(cw + f_ * T + cc_ * 16)            \
+                   : make_uint4(0u, 0u, 0u, 0u);                                        \
+    }                                                                                   \
   }
       OJBKQ_DECODE_FETCH(i1)
       int64_t f = i1 + (lane >> 4);   // this lane's row of operand B
@@ -167,16 +176,21 @@ __global__ __launch_bounds__(256, 2) void decode_kernel(DecodeDesc d) {
       double sb[4] = {0.0, 0.0, 0.0, 0.0};
       for (int64_t ch = 0; ch < nch; ++ch) {
         const int buf = (int)(ch & 1);
-        sR[buf][sff][spart * 4 + 0] = rr0;
-        sR[buf][sff][spart * 4 + 1] = rr1;
-        sR[buf][sff][spart * 4 + 2] = rr2;
-        sR[buf][sff][spart * 4 + 3] = rr3;
-        uint4* qd = reinterpret_cast<uint4*>(&sQ[buf][sff][spart * 32]);
-        qd[0] = rq0;
-        qd[1] = rq1;
+#pragma unroll
+        for (int q = 0; q < kRPer; ++q) {
+          const int e = tid + q * T;
+          if (e < kFC * kBS) sR[buf][e / kBS][e % kBS] = rr[q];
+        }
+#pragma unroll
+        for (int q = 0; q < kQPer; ++q) {
+          const int e = tid + q * T;
+          if (e / qpk < kFC)
+            *reinterpret_cast<uint4*>(sQ + (buf * kFC + e / qpk) * qrow + (e % qpk) * 16) = rq[q];
+        }
         __syncthreads();
         if (ch + 1 < nch) OJBKQ_DECODE_FETCH(i1 + (ch + 1) * kFC)
-#pragma unroll
+        const unsigned char* qb = sQ + buf * kFC * qrow + wave * 64 + (lane & 15);
+#pragma unroll 4
         for (int s4 = 0; s4 < kFC / 4; ++s4, f += 4) {
           const int ff = s4 * 4 + (lane >> 4);
           if (f < m && f >= gnext) {
@@ -188,15 +202,14 @@ __global__ __launch_bounds__(256, 2) void decode_kernel(DecodeDesc d) {
           double av[2];
 #pragma unroll
           for (int a = 0; a < 2; ++a) av[a] = sR[buf][ff][16 * a + (lane & 15)];
-          const uint32_t c4 =
-              *reinterpret_cast<const uint32_t*>(&sQ[buf][ff][wave * 64 + 4 * (lane & 15)]);
-          double bv[4];
 #pragma unroll
-          for (int t = 0; t < 4; ++t) bv[t] = (double)((c4 >> (8 * t)) & 255u) * sb[t];
+          for (int t = 0; t < 4; ++t) {
+            if (t < ntile) {
+              const double bv = (double)qb[ff * qrow + 16 * t] * sb[t];
 #pragma unroll
-          for (int a = 0; a < 2; ++a)
-#pragma unroll
-            for (int t = 0; t < 4; ++t) acc[a][t] = mfma_f64(av[a], bv[t], acc[a][t]);
+              for (int a = 0; a < 2; ++a) acc[a][t] = mfma_f64(av[a], bv, acc[a][t]);
+            }
+          }
         }
       }
       __syncthreads();   // every wave is done with the staged chunks (aliased below)
@@ -208,14 +221,14 @@ __global__ __launch_bounds__(256, 2) void decode_kernel(DecodeDesc d) {
       for (int t = 0; t < 4; ++t)
 #pragma unroll
         for (int r = 0; r < 4; ++r)
-          sAcc[16 * a + (lane >> 4) + 4 * r][wave * 64 + 4 * (lane & 15) + t] = acc[a][t][r];
+          sAcc[(16 * a + (lane >> 4) + 4 * r) * T + wave * 64 + 16 * t + (lane & 15)] = acc[a][t][r];
     __syncthreads();
 
     // ---- serial in-block steps, one path per lane ----
     if (valid) {
       double z[kBS];
 #pragma unroll
-      for (int r = 0; r < kBS; ++r) z[r] = (r < bl) ? gq[i0 + r] - sAcc[r][tid] : 0.0;
+      for (int r = 0; r < kBS; ++r) z[r] = (r < bl) ? gq[i0 + r] - sAcc[r * T + tid] : 0.0;
 #pragma unroll
       for (int r = kBS - 1; r >= 0; --r) {
         if (r < bl) {
@@ -235,11 +248,11 @@ __global__ __launch_bounds__(256, 2) void decode_kernel(DecodeDesc d) {
           const double e = s * (double)q;
 #pragma unroll
           for (int r2 = 0; r2 < r; ++r2) z[r2] -= sT[r][r2] * e;
-          cw[i * kDecodeThreads + tid] = (uint8_t)q;
+          cw[i * T + tid] = (uint8_t)q;
         }
       }
     } else {
-      for (int r = 0; r < bl; ++r) cw[(i0 + r) * kDecodeThreads + tid] = 0;
+      for (int r = 0; r < bl; ++r) cw[(i0 + r) * T + tid] = 0;
     }
   }
   if (valid) d.presid[p] = resid;
@@ -247,7 +260,8 @@ __global__ __launch_bounds__(256, 2) void decode_kernel(DecodeDesc d) {
 
 __global__ __launch_bounds__(256) void select_kernel(const uint8_t* __restrict__ pcodes,
                                                      const double* __restrict__ presid, int64_t n,
-                                                     int64_t m, int K, uint8_t* __restrict__ codes,
+                                                     int64_t m, int K, int64_t wg_paths,
+                                                     int threads, uint8_t* __restrict__ codes,
                                                      double* __restrict__ resid,
                                                      int32_t* __restrict__ winner,
                                                      uint8_t* __restrict__ path_codes,
@@ -273,17 +287,16 @@ __global__ __launch_bounds__(256) void select_kernel(const uint8_t* __restrict__
   __syncthreads();
   {
     const int64_t ps = j * kp1 + kstar;
-    const uint8_t* src = pcodes + (ps / kDecodeThreads) * m * kDecodeThreads + (ps % kDecodeThreads);
-    for (int64_t i = tid; i < m; i += 256) codes[j * m + i] = src[i * kDecodeThreads];
+    const uint8_t* src = pcodes + (ps / wg_paths) * m * threads + (ps % wg_paths);
+    for (int64_t i = tid; i < m; i += 256) codes[j * m + i] = src[i * threads];
   }
   if (path_resid)
     for (int64_t k = tid; k < kp1; k += 256) path_resid[j * kp1 + k] = presid[j * kp1 + k];
   if (path_codes) {
     for (int64_t k = 0; k < kp1; ++k) {
       const int64_t ps = j * kp1 + k;
-      const uint8_t* src =
-          pcodes + (ps / kDecodeThreads) * m * kDecodeThreads + (ps % kDecodeThreads);
-      for (int64_t i = tid; i < m; i += 256) path_codes[ps * m + i] = src[i * kDecodeThreads];
+      const uint8_t* src = pcodes + (ps / wg_paths) * m * threads + (ps % wg_paths);
+      for (int64_t i = tid; i < m; i += 256) path_codes[ps * m + i] = src[i * threads];
     }
   }
 }
@@ -291,18 +304,20 @@ __global__ __launch_bounds__(256) void select_kernel(const uint8_t* __restrict__
 }  // namespace
 
 hipError_t launch_decode(const DecodeDesc& d, hipStream_t stream) {
-  const int64_t nwg = decode_workgroups(d.n, d.K);
-  if (nwg <= 0) return hipSuccess;
-  if (nwg > 0x7fffffff) return hipErrorInvalidValue;
-  decode_kernel<<<dim3((unsigned)nwg), dim3(kDecodeThreads), 0, stream>>>(d);
+  const DecodeGeom geo = decode_geometry(d.n, d.K);
+  if (geo.nwg <= 0) return hipSuccess;
+  if (geo.nwg > 0x7fffffff || d.threads != geo.threads || d.wg_paths != geo.wg_paths)
+    return hipErrorInvalidValue;
+  decode_kernel<<<dim3((unsigned)geo.nwg), dim3(geo.threads), 0, stream>>>(d);
   return hipGetLastError();
 }
 
 hipError_t launch_select(const uint8_t* pcodes, const double* presid, int64_t n, int64_t m, int K,
-                         uint8_t* codes, double* resid, int32_t* winner, uint8_t* path_codes,
-                         double* path_resid, hipStream_t stream) {
-  select_kernel<<<dim3((unsigned)n), dim3(256), 0, stream>>>(pcodes, presid, n, m, K, codes, resid,
-                                                              winner, path_codes, path_resid);
+                         const DecodeGeom& geom, uint8_t* codes, double* resid, int32_t* winner,
+                         uint8_t* path_codes, double* path_resid, hipStream_t stream) {
+  select_kernel<<<dim3((unsigned)n), dim3(256), 0, stream>>>(
+      pcodes, presid, n, m, K, geom.wg_paths, geom.threads, codes, resid, winner, path_codes,
+      path_resid);
   return hipGetLastError();
 }
 

@@ -82,7 +82,35 @@ hipError_t launch_klein_alpha(const double* L, const float* S, int64_t n, int64_
                               int64_t G, double log_rho, double* alpha, hipStream_t stream);
 
 // ---- batched Babai / Klein decode and selection (Alg. 1, 3, 4) -------------
-constexpr int kDecodeThreads = 256;   // candidate paths per workgroup
+// Each decode workgroup walks all m rows for its set of paths, so one
+// workgroup's latency is the kernel's floor: the paths are spread so that
+// every one of the device's CUs gets at most one workgroup per round.
+constexpr int kDecodeCUs = 256;         // compute units of an MI355X
+constexpr int kDecodeMaxThreads = 512;  // paths (one per lane) per workgroup, at most
+
+struct DecodeGeom {
+  int64_t wg_paths = 0;   // paths per workgroup (a multiple of 16)
+  int threads = 0;        // lanes per workgroup (wg_paths rounded up to 64, >= 256)
+  int64_t nwg = 0;        // workgroups
+};
+
+inline DecodeGeom decode_geometry(int64_t n, int K) {
+  const int64_t P = n * (int64_t)(K + 1);
+  int64_t per = 16;
+  for (int64_t rounds = 1;; ++rounds) {
+    const int64_t slots = (int64_t)kDecodeCUs * rounds;
+    per = (P + slots - 1) / slots;
+    per = (per + 15) / 16 * 16;
+    if (per <= kDecodeMaxThreads) break;
+  }
+  if (per < 16) per = 16;
+  DecodeGeom g;
+  g.wg_paths = per;
+  g.threads = (int)((per + 63) / 64 * 64);
+  if (g.threads < 256) g.threads = 256;   // at least four waves (staging assumes it)
+  g.nwg = (P + per - 1) / per;
+  return g;
+}
 
 struct DecodeDesc {
   const double* L = nullptr;   // [m, m] lower factor (L = R^T)
@@ -92,20 +120,18 @@ struct DecodeDesc {
   int64_t m = 0, n = 0, g = 0, G = 0;
   int K = 0, bits = 0;
   uint64_t seed = 0;
-  uint8_t* pcodes = nullptr;   // [nwg, m, 256] candidate codes
-  double* presid = nullptr;    // [nwg * 256] candidate residuals
+  int64_t wg_paths = 0;        // from decode_geometry
+  int threads = 0;
+  uint8_t* pcodes = nullptr;   // [nwg, m, threads] candidate codes
+  double* presid = nullptr;    // [n (K + 1)] candidate residuals
 };
-
-inline int64_t decode_workgroups(int64_t n, int K) {
-  return (n * (int64_t)(K + 1) + kDecodeThreads - 1) / kDecodeThreads;
-}
 
 hipError_t launch_decode(const DecodeDesc& d, hipStream_t stream);
 
 // First strict minimum over the K + 1 candidates of each column; gathers the
 // winner's codes.  path_codes / path_resid / winner may be null.
 hipError_t launch_select(const uint8_t* pcodes, const double* presid, int64_t n, int64_t m, int K,
-                         uint8_t* codes, double* resid, int32_t* winner, uint8_t* path_codes,
-                         double* path_resid, hipStream_t stream);
+                         const DecodeGeom& geom, uint8_t* codes, double* resid, int32_t* winner,
+                         uint8_t* path_codes, double* path_resid, hipStream_t stream);
 
 }  // namespace ojbkq
