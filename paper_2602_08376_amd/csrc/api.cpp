@@ -264,7 +264,7 @@ int ctx_solve(ojbkq_ctx* c, const float* W, double alpha, uint8_t* codes, float*
     ojbkq::GemmDesc g;   // gq_j = Rbar_j qbar_j: gq[j][i] = sum_l Y[j][l] L[l][i]
     g.M = s.n; g.N = s.m; g.Kd = s.m;
     g.A = U; g.lda = s.m; g.ta = ojbkq::Elt::F64;
-    g.B = Lf; g.ldb = s.m; g.tb = ojbkq::Elt::F64; g.b_kmajor = true;
+    g.B = Lf; g.ldb = s.m; g.tb = ojbkq::Elt::F64; g.b_kmajor = true; g.b_zero_below_col = true;
     g.C = gq; g.ldc = s.m;
     OJBKQ_HIP(ojbkq::gemm_f64(g, st), "Rbar qbar");
   }
@@ -400,7 +400,7 @@ int ojbkq_decode_stage(const ojbkq_params* p, const double* R, const double* qba
     ojbkq::GemmDesc g;
     g.M = s.n; g.N = s.m; g.Kd = s.m;
     g.A = Y; g.lda = s.m; g.ta = ojbkq::Elt::F64;
-    g.B = Lf; g.ldb = s.m; g.tb = ojbkq::Elt::F64; g.b_kmajor = true;
+    g.B = Lf; g.ldb = s.m; g.tb = ojbkq::Elt::F64; g.b_kmajor = true; g.b_zero_below_col = true;
     g.C = gq; g.ldc = s.m;
     OJBKQ_HIP(ojbkq::gemm_f64(g, st), "Rbar qbar");
   }

@@ -31,35 +31,40 @@ __global__ __launch_bounds__(256) void damp_kernel(double* H, int64_t m, double 
   for (int64_t i = tid; i < m; i += 256) H[i * m + i] += lam2;
 }
 
-// Unblocked Cholesky of the nbk x nbk diagonal block starting at (k0, k0).
-__global__ __launch_bounds__(256) void potrf_diag_kernel(double* H, int64_t m, int64_t k0, int nbk,
-                                                         int* status) {
-  __shared__ double a[kNB][kNB + 1];
-  const int tid = threadIdx.x;
-  for (int e = tid; e < kNB * kNB; e += 256) {
-    const int r = e / kNB, c = e % kNB;
-    a[r][c] = (r < nbk && c <= r) ? H[(k0 + r) * m + k0 + c] : 0.0;
-  }
-  __syncthreads();
-  for (int c = 0; c < nbk; ++c) {
-    const double d = a[c][c];
-    if (tid == 0 && !(d > 0.0)) atomicMin(status, (int)(k0 + c));
-    const double piv = sqrt(d);
-    __syncthreads();
-    if (tid == 0) a[c][c] = piv;
-    for (int r = c + 1 + tid; r < nbk; r += 256) a[r][c] /= piv;
-    __syncthreads();
-    const int w = nbk - c - 1;
-    for (int e = tid; e < w * w; e += 256) {
-      const int rr = c + 1 + e / w, cc = c + 1 + e % w;
-      if (cc <= rr) a[rr][cc] -= a[rr][c] * a[cc][c];
+__device__ __forceinline__ double lane_value(double v, int lane) {
+  const int lo = __builtin_amdgcn_readlane(__double2loint(v), lane);
+  const int hi = __builtin_amdgcn_readlane(__double2hiint(v), lane);
+  return __hiloint2double(hi, lo);
+}
+
+// Unblocked Cholesky of the nbk x nbk diagonal block starting at (k0, k0),
+// by one wave: lane r keeps row r in registers and column c is broadcast
+// lane by lane, so the 64 dependent column steps touch no memory.
+__global__ __launch_bounds__(64) void potrf_diag_kernel(double* H, int64_t m, int64_t k0, int nbk,
+                                                        int* status) {
+  const int r = threadIdx.x;   // row of the block held by this lane
+  double a[kNB];
+#pragma unroll
+  for (int c = 0; c < kNB; ++c) a[c] = (r < nbk && c <= r) ? H[(k0 + r) * m + k0 + c] : 0.0;
+#pragma unroll
+  for (int c = 0; c < kNB; ++c) {
+    if (c < nbk) {
+      const double d = lane_value(a[c], c);   // pivot: row c, column c
+      if (r == 0 && !(d > 0.0)) atomicMin(status, (int)(k0 + c));
+      const double piv = sqrt(d);
+      const double lrc = (r > c) ? a[c] / piv : 0.0;   // L[r][c]
+      if (r == c) a[c] = piv;
+      if (r > c) a[c] = lrc;
+#pragma unroll
+      for (int c2 = c + 1; c2 < kNB; ++c2) {
+        const double l2 = lane_value(lrc, c2);   // L[c2][c]
+        if (c2 <= r) a[c2] -= lrc * l2;
+      }
     }
-    __syncthreads();
   }
-  for (int e = tid; e < kNB * kNB; e += 256) {
-    const int r = e / kNB, c = e % kNB;
-    if (r < nbk && c <= r) H[(k0 + r) * m + k0 + c] = a[r][c];
-  }
+#pragma unroll
+  for (int c = 0; c < kNB; ++c)
+    if (r < nbk && c <= r) H[(k0 + r) * m + k0 + c] = a[c];
 }
 
 // Rows i >= k0 + nbk of the panel: H[i][K] <- H[i][K] L_KK^-T.
@@ -81,10 +86,10 @@ __global__ __launch_bounds__(256) void trsm_panel_kernel(double* H, int64_t m, i
 #pragma unroll
   for (int c = 0; c < kNB; ++c) {
     if (c < nbk) {
-      double s = x[c];
+      double p[4] = {0.0, 0.0, 0.0, 0.0};   // four partial sums break the FMA chain
 #pragma unroll
-      for (int c2 = 0; c2 < c; ++c2) s -= x[c2] * Lk[c][c2];
-      x[c] = s / Lk[c][c];
+      for (int c2 = 0; c2 < c; ++c2) p[c2 & 3] += x[c2] * Lk[c][c2];
+      x[c] = (x[c] - ((p[0] + p[1]) + (p[2] + p[3]))) / Lk[c][c];
     }
   }
 #pragma unroll
@@ -135,10 +140,10 @@ __global__ __launch_bounds__(256) void trsv_fwd_kernel(const double* L, double* 
 #pragma unroll
   for (int c = 0; c < kNB; ++c) {
     if (c < nbk) {
-      double s = x[c];
+      double p[4] = {0.0, 0.0, 0.0, 0.0};   // four partial sums break the FMA chain
 #pragma unroll
-      for (int c2 = 0; c2 < c; ++c2) s -= Lk[c][c2] * x[c2];
-      x[c] = s / Lk[c][c];
+      for (int c2 = 0; c2 < c; ++c2) p[c2 & 3] += Lk[c][c2] * x[c2];
+      x[c] = (x[c] - ((p[0] + p[1]) + (p[2] + p[3]))) / Lk[c][c];
     }
   }
 #pragma unroll
@@ -165,10 +170,10 @@ __global__ __launch_bounds__(256) void trsv_bwd_kernel(const double* L, double* 
 #pragma unroll
   for (int c = kNB - 1; c >= 0; --c) {
     if (c < nbk) {
-      double s = x[c];
+      double p[4] = {0.0, 0.0, 0.0, 0.0};   // four partial sums; zero beyond nbk
 #pragma unroll
-      for (int c2 = c + 1; c2 < kNB; ++c2) s -= Lk[c2][c] * x[c2];   // zero beyond nbk
-      x[c] = s / Lk[c][c];
+      for (int c2 = c + 1; c2 < kNB; ++c2) p[c2 & 3] += Lk[c2][c] * x[c2];
+      x[c] = (x[c] - ((p[0] + p[1]) + (p[2] + p[3]))) / Lk[c][c];
     }
   }
 #pragma unroll
@@ -189,7 +194,7 @@ hipError_t launch_damp(double* H, int64_t m, double lambda_rel, double* lam2_out
 hipError_t cholesky_lower(double* H, int64_t m, int* status, hipStream_t stream) {
   for (int64_t k0 = 0; k0 < m; k0 += kNB) {
     const int nbk = (int)((m - k0) < kNB ? (m - k0) : kNB);
-    potrf_diag_kernel<<<1, 256, 0, stream>>>(H, m, k0, nbk, status);
+    potrf_diag_kernel<<<1, 64, 0, stream>>>(H, m, k0, nbk, status);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     const int64_t rest = m - k0 - nbk;

@@ -37,6 +37,7 @@ struct GemmArgs {
   int64_t tiles_m, tiles_n;
   int lower;
   int vec_a, vec_b;
+  int b_tri;
 };
 
 // Eight consecutive elements starting at p, the first `valid` of them real
@@ -160,8 +161,9 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& g, int64_t ti, int64_t
     }
   };
 
-  if (g.Kd > 0) fetch(0);
-  for (int64_t k0 = 0; k0 < g.Kd; k0 += kKC) {
+  const int64_t kbeg = g.b_tri ? (J0 < g.Kd ? J0 : g.Kd) : 0;   // J0 is a multiple of kKC
+  if (kbeg < g.Kd) fetch(kbeg);
+  for (int64_t k0 = kbeg; k0 < g.Kd; k0 += kKC) {
     __syncthreads();
     store_chunk<AK>(sA, tid, ra);
     store_chunk<BK>(sB, tid, rb);
@@ -233,6 +235,7 @@ hipError_t gemm_f64(const GemmDesc& d, hipStream_t stream) {
   g.tiles_m = (d.M + kTile - 1) / kTile;
   g.tiles_n = (d.N + kTile - 1) / kTile;
   g.lower = d.lower_tiles ? 1 : 0;
+  g.b_tri = d.b_zero_below_col ? 1 : 0;
   g.vec_a = vec_ok(d.A, d.lda, d.ta) ? 1 : 0;
   g.vec_b = (vec_ok(d.B, d.ldb, d.tb) && (d.B2 == nullptr || vec_ok(d.B2, d.ldb, d.tb))) ? 1 : 0;
   if (d.lower_tiles && g.tiles_m != g.tiles_n) return hipErrorInvalidValue;

@@ -32,6 +32,9 @@ struct GemmDesc {
   int64_t ldc = 0;
   double alpha = 1.0, beta = 0.0;
   bool lower_tiles = false;
+  // opB(j, k) == 0 whenever k < j (B is the lower factor read k-major): the
+  // k loop of an output tile starts at its first column.
+  bool b_zero_below_col = false;
 };
 
 hipError_t gemm_f64(const GemmDesc& d, hipStream_t stream);

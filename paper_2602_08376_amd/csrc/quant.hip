@@ -79,20 +79,27 @@ __global__ __launch_bounds__(256) void scale_centres_kernel(const double* __rest
 }
 
 // alpha_j = log_rho / min_i (R_ii s_j(i))^2 over the scaled basis Rbar_j.
+// One wave per column: lanes stride over the rows, then a min-reduction.
 __global__ __launch_bounds__(256) void klein_alpha_kernel(const double* __restrict__ L,
                                                           const float* __restrict__ S, int64_t n,
                                                           int64_t m, int64_t g, int64_t G,
                                                           double log_rho,
                                                           double* __restrict__ alpha) {
-  const int64_t j = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  const int lane = threadIdx.x & 63;
+  const int64_t j = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
   if (j >= n) return;
   double mn = INFINITY;
-  for (int64_t i = 0; i < m; ++i) {
+  for (int64_t i = lane; i < m; i += 64) {
     const double rb = L[i * m + i] * (double)S[j * G + i / g];
     const double r2 = rb * rb;
     mn = r2 < mn ? r2 : mn;
   }
-  alpha[j] = log_rho / mn;
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) {
+    const double o = __shfl_xor(mn, off, 64);
+    mn = o < mn ? o : mn;
+  }
+  if (lane == 0) alpha[j] = log_rho / mn;
 }
 
 unsigned grid_for(int64_t total) {
@@ -122,8 +129,8 @@ hipError_t launch_centres(const float* W, const double* delta, double c, const f
 
 hipError_t launch_klein_alpha(const double* L, const float* S, int64_t n, int64_t m, int64_t g,
                               int64_t G, double log_rho, double* alpha, hipStream_t stream) {
-  klein_alpha_kernel<<<(unsigned)((n + 255) / 256), 256, 0, stream>>>(L, S, n, m, g, G, log_rho,
-                                                                        alpha);
+  klein_alpha_kernel<<<(unsigned)((n + 3) / 4), 256, 0, stream>>>(L, S, n, m, g, G, log_rho,
+                                                                    alpha);
   return hipGetLastError();
 }
 
