@@ -12,7 +12,8 @@ Default workload: the Llama-7B-shaped attention projection, W 4096 x 4096
 group 128, K = 16 Klein samples, alpha (the JTA knob) = 0.5.
 
 Prints one JSON line.  value = n (K + 1) / layer time, i.e. candidate paths
-(columns x samples) decoded per second, end to end.  The roofline object is
+(columns x samples) decoded per second, end to end (times the number of JTA
+knobs when a workload sweeps several on one factor).  The roofline object is
 for the dominant kernel, the fused Gram + cross-term contraction, timed with
 HIP events on the stream it is launched on.  The CPU baseline times the oracle
 on a bounded sample of the same workload on this host and extrapolates.
@@ -87,7 +88,8 @@ def workload_desc(cfg):
     return {
         "workload": f"{cfg.key}: {cfg.title}",
         "n_out": cfg.n, "m_in": cfg.m, "tokens": cfg.T, "bits": cfg.bits, "group": cfg.group,
-        "K": cfg.K, "alpha": cfg.mu, "lambda_rel": cfg.lambda_rel, "token_chunks": cfg.chunks,
+        "K": cfg.K, "alpha": list(cfg.mus) if len(cfg.mus) > 1 else cfg.mu,
+        "lambda_rel": cfg.lambda_rel, "token_chunks": cfg.chunks,
     }
 
 
@@ -184,7 +186,8 @@ def main():
             ev[2 * i].record(stream)
             s.accumulate(Xr, Xq)              # one gram_cross launch per chunk
             ev[2 * i + 1].record(stream)
-        out = s.solve(W, cfg.mu)
+        for mu in cfg.mus:                    # one factor serves every JTA knob
+            out = s.solve(W, mu)
         ev[-1].record(stream)
         s.close()
         if record is not None:
@@ -214,7 +217,7 @@ def main():
     Tc = T // cfg.chunks
     flops = 3.0 * m * m * Tc          # syrk m^2 Tc (lower half) + cross 2 m^2 Tc per launch
     achieved = flops / (gc_avg * 1e-3) / 1e12
-    paths = cfg.n * (cfg.K + 1)
+    paths = cfg.n * (cfg.K + 1) * len(cfg.mus)
     out = recs[-1][1]
     result = {
         "metric": METRIC,
