@@ -56,7 +56,7 @@ def parse():
     return ap.parse_args()
 
 
-KERNEL_SOURCES = ("paper_2602_08376_amd/csrc/gemm.hip", "paper_2602_08376_amd/csrc/device.h")
+KERNEL_SOURCES = ("paper_2602_08376_amd/csrc/gram.hip", "paper_2602_08376_amd/csrc/device.h")
 
 
 def measured_traffic(kernel, workload):

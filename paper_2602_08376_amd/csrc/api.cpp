@@ -10,6 +10,7 @@
 #include <cstring>
 #include <new>
 #include <string>
+#include <vector>
 
 #include "kernels.h"
 
@@ -59,7 +60,7 @@ Shape shape_of(const ojbkq_params& p) {
 // Offsets of every buffer carved from the workspace.
 struct Layout {
   size_t status = 0, lam2 = 0, G = 0, E = 0, U = 0, qbar = 0, gq = 0, alpha = 0, pcodes = 0,
-         presid = 0, gc_scratch = 0, total = 0;
+         presid = 0, gc_scratch = 0, gc_tiles = 0, total = 0;
 };
 
 Layout layout_full(const Shape& s) {
@@ -83,6 +84,7 @@ Layout layout_full(const Shape& s) {
   L.pcodes = take((size_t)s.geo.nwg * (size_t)s.geo.threads * (size_t)s.m);
   L.presid = take((size_t)s.paths * sizeof(double));
   L.gc_scratch = take(ojbkq::gram_cross_scratch_bytes());
+  L.gc_tiles = take((size_t)ojbkq::gram_tile_count(s.m) * sizeof(uint32_t));
   L.total = off;
   return L;
 }
@@ -196,6 +198,15 @@ int ctx_init(ojbkq_ctx* c, const ojbkq_params* p, void* ws, size_t bytes, void* 
   c->ws = static_cast<char*>(ws);
   c->stream = static_cast<hipStream_t>(stream);
   OJBKQ_HIP(hipMemsetAsync(c->at<int>(c->L.status), 0x7f, sizeof(int), c->stream), "status clear");
+  {
+    // tile order of the Gram launch, built once per context
+    std::vector<uint32_t> tiles((size_t)ojbkq::gram_tile_count(c->s.m));
+    ojbkq::gram_tile_list(c->s.m, tiles.data());
+    OJBKQ_HIP(hipMemcpyAsync(c->at<uint32_t>(c->L.gc_tiles), tiles.data(),
+                             tiles.size() * sizeof(uint32_t), hipMemcpyHostToDevice, c->stream),
+              "tile list");
+    OJBKQ_HIP(hipStreamSynchronize(c->stream), "tile list");
+  }
   return OJBKQ_OK;
 }
 
@@ -207,7 +218,8 @@ int ctx_accumulate(ojbkq_ctx* c, const float* Xr, const float* Xq, int64_t T, in
   const bool cross = Xr != nullptr && Xr != Xq;
   OJBKQ_HIP(ojbkq::gram_cross(Xq, cross ? Xr : nullptr, c->s.m, T, ldx, c->at<double>(c->L.G),
                               c->at<double>(c->L.E), c->any_chunk, c->cross_seen,
-                              c->at<void>(c->L.gc_scratch), gram_shares(), c->stream),
+                              c->at<uint32_t>(c->L.gc_tiles), c->at<void>(c->L.gc_scratch),
+                              gram_shares(), c->stream),
             "gram and cross term");
   if (cross) c->cross_seen = true;
   c->any_chunk = true;

@@ -4,14 +4,16 @@
 // in one persistent launch on fp64 MFMA.  The cross term X~^T (X - X~) is
 // C - G, formed once after the last chunk (cross_from_mixed).
 //
-// Work is the list of (tile, 32-token chunk) pairs, Gram tiles first.  The
-// grid is exactly the number of resident workgroups (two per CU) and each
-// workgroup takes one contiguous, equal share of that list ("stream-K"), so
-// there is no tail of partly filled waves.  A share starts and ends inside a
-// tile at most once each: those two partial tiles go to per-workgroup slots of
-// a scratch buffer and a second kernel adds them up in workgroup order, so the
-// result does not depend on timing.  Shares are dealt so that one XCD holds a
-// contiguous run of tiles and its L2 sees their shared operand panels.
+// The grid is exactly the number of resident workgroups P (two per CU).
+// Tiles are listed Gram first, each part in 8x8 blocks of tiles (a tile list
+// built on the host).  The first floor(ntiles / P) * P tiles go in whole-tile
+// rounds: in a round all workgroups walk the tokens together and the 64 on one
+// XCD hold one 8x8 block, so their L2 serves each operand panel to eight
+// tiles.  The remaining tiles' (tile, 32-token chunk) pairs are split into P
+// equal contiguous shares ("stream-K"), so no round is left partly filled.  A
+// share starts and ends inside a tile at most once each: those partial tiles
+// go to per-workgroup slots of a scratch buffer and a second kernel adds them
+// up in workgroup order, so the result does not depend on timing.
 //
 // Operands stay fp32 in LDS and are widened to fp64 when a fragment is read
 // (every product of two fp32 values is exact in fp64).
@@ -35,36 +37,29 @@ struct GcArgs {
   double* E;
   double beta_g, beta_e;
   int64_t tiles;      // tiles per side
-  int64_t n_gram, ntiles, nchunks, work;
-  int nshare;
+  int64_t n_gram, ntiles, nchunks;
+  int64_t n_dp;       // whole-tile rounds
+  int64_t tile0;      // first stream-K tile (n_dp * nshare)
+  int64_t work;       // stream-K work: (ntiles - tile0) * nchunks
+  const uint32_t* tile_list;   // [ntiles]: cross flag << 31 | tile row << 16 | tile col
+  int nshare;         // workgroups
+  int nsk;            // stream-K shares (<= nshare, each non-empty)
   double* part;       // [nshare][2][128*128]
   int* part_tile;     // [nshare][2]
   int vec;
 };
 
+// First stream-K work item of share r (r <= nsk).
 __device__ __forceinline__ int64_t share_begin(int64_t r, const GcArgs& a) {
-  return (r * a.work) / a.nshare;
+  return (r * a.work) / a.nsk;
 }
 
 __device__ __forceinline__ void tile_coords(int64_t tile, const GcArgs& a, int64_t& ti,
                                             int64_t& tj, bool& cross) {
-  if (tile < a.n_gram) {
-    cross = false;
-    ti = (int64_t)((sqrt(8.0 * (double)tile + 1.0) - 1.0) * 0.5);
-    while (ti * (ti + 1) / 2 > tile) --ti;
-    while ((ti + 1) * (ti + 2) / 2 <= tile) ++ti;
-    tj = tile - ti * (ti + 1) / 2;
-  } else {
-    cross = true;
-    const int64_t t = tile - a.n_gram;
-    constexpr int64_t kGroup = 8;   // tile rows per raster group
-    const int64_t per = kGroup * a.tiles;
-    const int64_t first = (t / per) * kGroup;
-    const int64_t rows = (a.tiles - first) < kGroup ? (a.tiles - first) : kGroup;
-    const int64_t r = t % per;
-    ti = first + r % rows;
-    tj = r / rows;
-  }
+  const uint32_t e = a.tile_list[tile];
+  cross = (e >> 31) != 0;
+  ti = (e >> 16) & 0x7fff;
+  tj = e & 0xffff;
 }
 
 // kPer consecutive floats of row `row` from token k (zero past the ends).
@@ -88,94 +83,102 @@ __device__ __forceinline__ void load_run(const float* __restrict__ X, int64_t ld
   }
 }
 
+// Chunks [c0, c1) of one tile.  A whole tile is written to G / E directly;
+// a part goes to partial slot `slot` of share r.
+__device__ __forceinline__ void gram_segment(const GcArgs& a, int64_t tile, int64_t c0, int64_t c1,
+                                             int64_t r, int& slot, float (*sA)[kLd],
+                                             float (*sB)[kLd]) {
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wr = wave >> 1, wc = wave & 1;   // 64x64 block of the tile
+  constexpr int kPartsPerRow = kKC / kPer;
+  const int lrow = tid / kPartsPerRow, lk = (tid % kPartsPerRow) * kPer;
+  int64_t ti, tj;
+  bool cross;
+  tile_coords(tile, a, ti, tj, cross);
+  const int64_t I0 = ti * kTile, J0 = tj * kTile;
+  const float* Bsrc = cross ? a.Xr : a.Xq;
+
+  d4 acc[4][4];
+#pragma unroll
+  for (int x = 0; x < 4; ++x)
+#pragma unroll
+    for (int y = 0; y < 4; ++y) acc[x][y] = d4{0.0, 0.0, 0.0, 0.0};
+
+  float ra[kPer], rb[kPer];
+  load_run(a.Xq, a.ldx, a.m, a.T, I0 + lrow, c0 * kKC + lk, a.vec, ra);
+  load_run(Bsrc, a.ldx, a.m, a.T, J0 + lrow, c0 * kKC + lk, a.vec, rb);
+  for (int64_t c = c0; c < c1; ++c) {
+    __syncthreads();
+#pragma unroll
+    for (int q = 0; q < kPer; ++q) {
+      sA[lk + q][lrow] = ra[q];
+      sB[lk + q][lrow] = rb[q];
+    }
+    __syncthreads();
+    if (c + 1 < c1) {
+      load_run(a.Xq, a.ldx, a.m, a.T, I0 + lrow, (c + 1) * kKC + lk, a.vec, ra);
+      load_run(Bsrc, a.ldx, a.m, a.T, J0 + lrow, (c + 1) * kKC + lk, a.vec, rb);
+    }
+#pragma unroll
+    for (int kk = 0; kk < kKC / 4; ++kk) {
+      const int kr = kk * 4 + (lane >> 4);
+      double fa[4], fb[4];
+#pragma unroll
+      for (int x = 0; x < 4; ++x) fa[x] = (double)sA[kr][wr * 64 + x * 16 + (lane & 15)];
+#pragma unroll
+      for (int y = 0; y < 4; ++y) fb[y] = (double)sB[kr][wc * 64 + y * 16 + (lane & 15)];
+#pragma unroll
+      for (int x = 0; x < 4; ++x)
+#pragma unroll
+        for (int y = 0; y < 4; ++y) acc[x][y] = mfma_f64(fa[x], fb[y], acc[x][y]);
+    }
+  }
+
+  const bool whole = (c0 == 0 && c1 == a.nchunks);
+  double* C = cross ? a.E : a.G;
+  const double beta = cross ? a.beta_e : a.beta_g;
+  double* P = a.part + (r * 2 + slot) * kSlotElems;
+#pragma unroll
+  for (int x = 0; x < 4; ++x)
+#pragma unroll
+    for (int y = 0; y < 4; ++y)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int li = wr * 64 + x * 16 + (lane >> 4) + 4 * q;
+        const int lj = wc * 64 + y * 16 + (lane & 15);
+        if (whole) {
+          const int64_t i = I0 + li, j = J0 + lj;
+          if (i < a.m && j < a.m) {
+            double v = acc[x][y][q];
+            if (beta != 0.0) v += beta * C[i * a.m + j];
+            C[i * a.m + j] = v;
+          }
+        } else {
+          P[li * kTile + lj] = acc[x][y][q];
+        }
+      }
+  if (!whole) {
+    if (tid == 0) a.part_tile[r * 2 + slot] = (int)tile;
+    ++slot;
+  }
+}
+
 __global__ __launch_bounds__(kThreads, 2) void gram_cross_kernel(GcArgs a) {
   __shared__ float sA[kKC][kLd];   // X_q rows of the A panel
   __shared__ float sB[kKC][kLd];   // X_q (Gram tile) or X_ref (mixed tile) rows of the B panel
-
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wr = wave >> 1, wc = wave & 1;   // 64x64 block of the tile
   // share index: consecutive shares on one XCD
   int64_t r = blockIdx.x;
   if ((a.nshare & 7) == 0) r = (r & 7) * (a.nshare >> 3) + (r >> 3);
-  const int64_t w_end = share_begin(r + 1, a);
-  int64_t w = share_begin(r, a);
   int slot = 0;
-  constexpr int kPartsPerRow = kKC / kPer;
-  const int lrow = tid / kPartsPerRow, lk = (tid % kPartsPerRow) * kPer;
-
-  while (w < w_end) {
-    const int64_t tile = w / a.nchunks;
+  for (int64_t round = 0; round < a.n_dp; ++round)
+    gram_segment(a, round * a.nshare + r, 0, a.nchunks, r, slot, sA, sB);
+  if (r >= a.nsk) return;
+  const int64_t w_end = share_begin(r + 1, a);
+  for (int64_t w = share_begin(r, a); w < w_end;) {
+    const int64_t tile = a.tile0 + w / a.nchunks;
     const int64_t c0 = w % a.nchunks;
     const int64_t c1 = (a.nchunks - c0) < (w_end - w) ? a.nchunks : c0 + (w_end - w);
-    int64_t ti, tj;
-    bool cross;
-    tile_coords(tile, a, ti, tj, cross);
-    const int64_t I0 = ti * kTile, J0 = tj * kTile;
-    const float* Bsrc = cross ? a.Xr : a.Xq;
-
-    d4 acc[4][4];
-#pragma unroll
-    for (int x = 0; x < 4; ++x)
-#pragma unroll
-      for (int y = 0; y < 4; ++y) acc[x][y] = d4{0.0, 0.0, 0.0, 0.0};
-
-    float ra[kPer], rb[kPer];
-    load_run(a.Xq, a.ldx, a.m, a.T, I0 + lrow, c0 * kKC + lk, a.vec, ra);
-    load_run(Bsrc, a.ldx, a.m, a.T, J0 + lrow, c0 * kKC + lk, a.vec, rb);
-    for (int64_t c = c0; c < c1; ++c) {
-      __syncthreads();
-#pragma unroll
-      for (int q = 0; q < kPer; ++q) {
-        sA[lk + q][lrow] = ra[q];
-        sB[lk + q][lrow] = rb[q];
-      }
-      __syncthreads();
-      if (c + 1 < c1) {
-        load_run(a.Xq, a.ldx, a.m, a.T, I0 + lrow, (c + 1) * kKC + lk, a.vec, ra);
-        load_run(Bsrc, a.ldx, a.m, a.T, J0 + lrow, (c + 1) * kKC + lk, a.vec, rb);
-      }
-#pragma unroll
-      for (int kk = 0; kk < kKC / 4; ++kk) {
-        const int kr = kk * 4 + (lane >> 4);
-        double fa[4], fb[4];
-#pragma unroll
-        for (int x = 0; x < 4; ++x) fa[x] = (double)sA[kr][wr * 64 + x * 16 + (lane & 15)];
-#pragma unroll
-        for (int y = 0; y < 4; ++y) fb[y] = (double)sB[kr][wc * 64 + y * 16 + (lane & 15)];
-#pragma unroll
-        for (int x = 0; x < 4; ++x)
-#pragma unroll
-          for (int y = 0; y < 4; ++y) acc[x][y] = mfma_f64(fa[x], fb[y], acc[x][y]);
-      }
-    }
-
-    const bool whole = (c0 == 0 && c1 == a.nchunks);
-    double* C = cross ? a.E : a.G;
-    const double beta = cross ? a.beta_e : a.beta_g;
-    double* P = a.part + ((int64_t)r * 2 + slot) * kSlotElems;
-#pragma unroll
-    for (int x = 0; x < 4; ++x)
-#pragma unroll
-      for (int y = 0; y < 4; ++y)
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          const int li = wr * 64 + x * 16 + (lane >> 4) + 4 * q;
-          const int lj = wc * 64 + y * 16 + (lane & 15);
-          if (whole) {
-            const int64_t i = I0 + li, j = J0 + lj;
-            if (i < a.m && j < a.m) {
-              double v = acc[x][y][q];
-              if (beta != 0.0) v += beta * C[i * a.m + j];
-              C[i * a.m + j] = v;
-            }
-          } else {
-            P[li * kTile + lj] = acc[x][y][q];
-          }
-        }
-    if (!whole) {
-      if (tid == 0) a.part_tile[r * 2 + slot] = (int)tile;
-      ++slot;
-    }
+    gram_segment(a, tile, c0, c1, r, slot, sA, sB);
     w += c1 - c0;
   }
 }
@@ -187,9 +190,9 @@ __global__ __launch_bounds__(256) void gram_cross_fixup_kernel(GcArgs a) {
   const int64_t rb = (int64_t)blockIdx.x + 1;
   const int64_t wb = share_begin(rb, a);
   if (wb >= a.work || wb % a.nchunks == 0) return;
-  const int64_t tile = wb / a.nchunks;
-  const int64_t tstart = tile * a.nchunks, tend = tstart + a.nchunks;
+  const int64_t tstart = (wb / a.nchunks) * a.nchunks, tend = tstart + a.nchunks;
   if (share_begin(rb - 1, a) > tstart) return;   // an earlier boundary in this tile does it
+  const int64_t tile = a.tile0 + wb / a.nchunks;
   int64_t ti, tj;
   bool cross;
   tile_coords(tile, a, ti, tj, cross);
@@ -197,7 +200,7 @@ __global__ __launch_bounds__(256) void gram_cross_fixup_kernel(GcArgs a) {
   const double beta = cross ? a.beta_e : a.beta_g;
   // contributing shares: rb - 1 .. the share holding tend - 1
   int64_t rlast = rb;
-  while (rlast + 1 < a.nshare && share_begin(rlast + 1, a) < tend) ++rlast;
+  while (rlast + 1 < a.nsk && share_begin(rlast + 1, a) < tend) ++rlast;
   for (int e = threadIdx.x; e < kSlotElems; e += 256) {
     const int li = e / kTile, lj = e % kTile;
     const int64_t i = ti * kTile + li, j = tj * kTile + lj;
@@ -241,9 +244,32 @@ size_t gram_cross_scratch_bytes() {
          (size_t)kGramCrossMaxShares * 2 * sizeof(int);
 }
 
+int64_t gram_tile_count(int64_t m) {
+  const int64_t t = (m + kTile - 1) / kTile;
+  return t * (t + 1) / 2 + t * t;
+}
+
+void gram_tile_list(int64_t m, uint32_t* out) {
+  // Gram tiles (lower triangle) then cross tiles, each walked in 8x8 blocks of tiles.
+  const int64_t t = (m + kTile - 1) / kTile;
+  const int64_t nb = (t + 7) / 8;
+  int64_t k = 0;
+  for (int pass = 0; pass < 2; ++pass)
+    for (int64_t bi = 0; bi < nb; ++bi)
+      for (int64_t bj = 0; bj < nb; ++bj) {
+        if (pass == 0 && bj > bi) continue;
+        for (int64_t i = bi * 8; i < bi * 8 + 8 && i < t; ++i)
+          for (int64_t j = bj * 8; j < bj * 8 + 8 && j < t; ++j) {
+            if (pass == 0 && j > i) continue;
+            out[k++] = ((uint32_t)pass << 31) | ((uint32_t)i << 16) | (uint32_t)j;
+          }
+      }
+}
+
 hipError_t gram_cross(const float* Xq, const float* Xr, int64_t m, int64_t T, int64_t ldx,
-                      double* G, double* E, bool accumulate_g, bool accumulate_e, void* scratch,
-                      int max_shares, hipStream_t stream) {
+                      double* G, double* E, bool accumulate_g, bool accumulate_e,
+                      const uint32_t* tile_list, void* scratch, int max_shares,
+                      hipStream_t stream) {
   if (m <= 0 || T <= 0) return hipSuccess;
   GcArgs a;
   a.Xq = Xq;
@@ -259,14 +285,18 @@ hipError_t gram_cross(const float* Xq, const float* Xr, int64_t m, int64_t T, in
   a.n_gram = a.tiles * (a.tiles + 1) / 2;
   a.ntiles = a.n_gram + (Xr ? a.tiles * a.tiles : 0);
   a.nchunks = (T + kKC - 1) / kKC;
-  a.work = a.ntiles * a.nchunks;
-  // at least 64 chunks per share, at most max_shares shares, a multiple of 8
-  int64_t shares = (a.work + 63) / 64;
+  a.tile_list = tile_list;
+  // at least 64 chunks per workgroup, at most max_shares workgroups, a multiple of 8
+  int64_t shares = (a.ntiles * a.nchunks + 63) / 64;
   if (shares > max_shares) shares = max_shares;
   if (shares > kGramCrossMaxShares) shares = kGramCrossMaxShares;
   if (shares >= 8) shares &= ~(int64_t)7;
   if (shares < 1) shares = 1;
   a.nshare = (int)shares;
+  a.n_dp = a.ntiles / shares;
+  a.tile0 = a.n_dp * shares;
+  a.work = (a.ntiles - a.tile0) * a.nchunks;
+  a.nsk = (int)(a.work < shares ? a.work : shares);
   a.part = static_cast<double*>(scratch);
   a.part_tile = reinterpret_cast<int*>(static_cast<char*>(scratch) +
                                        (size_t)kGramCrossMaxShares * 2 * kSlotElems * sizeof(double));
@@ -275,8 +305,8 @@ hipError_t gram_cross(const float* Xq, const float* Xr, int64_t m, int64_t T, in
   a.vec = vec ? 1 : 0;
   gram_cross_kernel<<<dim3((unsigned)a.nshare), dim3(kThreads), 0, stream>>>(a);
   hipError_t e = hipGetLastError();
-  if (e != hipSuccess || a.nshare < 2) return e;
-  gram_cross_fixup_kernel<<<dim3((unsigned)(a.nshare - 1)), dim3(256), 0, stream>>>(a);
+  if (e != hipSuccess || a.nsk < 2) return e;
+  gram_cross_fixup_kernel<<<dim3((unsigned)(a.nsk - 1)), dim3(256), 0, stream>>>(a);
   return hipGetLastError();
 }
 

@@ -48,9 +48,13 @@ hipError_t gemm_f64(const GemmDesc& d, hipStream_t stream);
 // max_shares: workgroups to use (two per CU is the resident maximum).
 constexpr int kGramCrossMaxShares = 512;
 size_t gram_cross_scratch_bytes();
+// tile_list: device copy of gram_tile_list(m) (gram_tile_count(m) entries).
+int64_t gram_tile_count(int64_t m);
+void gram_tile_list(int64_t m, uint32_t* out);   // host-side
 hipError_t gram_cross(const float* Xq, const float* Xr, int64_t m, int64_t T, int64_t ldx,
-                      double* G, double* E, bool accumulate_g, bool accumulate_e, void* scratch,
-                      int max_shares, hipStream_t stream);
+                      double* G, double* E, bool accumulate_g, bool accumulate_e,
+                      const uint32_t* tile_list, void* scratch, int max_shares,
+                      hipStream_t stream);
 // E <- E - G (G read through symmetry): turns the accumulated mixed product
 // X_q X_ref^T into the cross term X_q (X_ref - X_q)^T.  Call before G is
 // factored.
