@@ -181,6 +181,7 @@ def main():
     def step(record):
         s = ok.LayerSolver(cfg.m, cfg.n, cfg.bits, cfg.group, cfg.K, cfg.klein_seed,
                            cfg.lambda_rel, device=dev, workspace=ws)
+        s.set_timing(True)                        # per-stage HIP events inside the library
         ev = [torch.cuda.Event(enable_timing=True) for _ in range(2 * len(chunks) + 1)]
         for i, (Xr, Xq) in enumerate(chunks):
             ev[2 * i].record(stream)
@@ -189,9 +190,10 @@ def main():
         for mu in cfg.mus:                    # one factor serves every JTA knob
             out = s.solve(W, mu)
         ev[-1].record(stream)
+        stages = s.stage_times()
         s.close()
         if record is not None:
-            record.append((ev, out))
+            record.append((ev, out, stages))
         return out
 
     for w in range(args.warmup):
@@ -208,7 +210,8 @@ def main():
     ms_step = wall * 1e3 / args.steps
 
     gc_ms, solve_ms = [], []
-    for ev, _ in recs:
+    stage_ms = {k: sum(r[2][k] for r in recs) / len(recs) for k in ok.STAGES}
+    for ev, _, _ in recs:
         for i in range(len(chunks)):
             gc_ms.append(ev[2 * i].elapsed_time(ev[2 * i + 1]))
         solve_ms.append(ev[2 * len(chunks) - 1].elapsed_time(ev[-1]))
@@ -218,6 +221,7 @@ def main():
     flops = 3.0 * m * m * Tc          # syrk m^2 Tc (lower half) + cross 2 m^2 Tc per launch
     achieved = flops / (gc_avg * 1e-3) / 1e12
     paths = cfg.n * (cfg.K + 1) * len(cfg.mus)
+    dec_flops = float(m) * m * paths     # m^2 per candidate path (the strict triangle, 2 FLOP/MAC)
     out = recs[-1][1]
     result = {
         "metric": METRIC,
@@ -235,7 +239,8 @@ def main():
         "data": "synthetic (seeded, generated on the GPU; inputs resident in HBM)",
         "config": workload_desc(cfg),
         "stages_ms": {"gram_cross_per_launch": gc_avg,
-                      "rest_of_path": sum(solve_ms) / len(solve_ms)},
+                      "rest_of_path": sum(solve_ms) / len(solve_ms),
+                      **{f"library_{k}": v for k, v in stage_ms.items()}},
         "roofline": {
             "bound": "mfma",
             "kernel": "gram_cross_kernel",
@@ -246,6 +251,16 @@ def main():
             "traffic": measured_traffic("gram_cross_kernel", cfg.key),
             "algorithmic_flops_per_launch": flops,
             "algorithmic_bytes_per_launch": 8.0 * m * Tc + 16.0 * m * m,
+        },
+        "decode_roofline": {
+            "bound": "mfma",
+            "kernel": "decode_kernel",
+            "achieved": dec_flops / (stage_ms["decode"] * 1e-3) / 1e12,
+            "peak": PEAK_F64_MFMA_TFLOPS,
+            "unit": "TFLOP/s",
+            "frac": dec_flops / (stage_ms["decode"] * 1e-3) / 1e12 / PEAK_F64_MFMA_TFLOPS,
+            "algorithmic_flops_per_step": dec_flops,
+            "paths_per_s": paths / (stage_ms["decode"] * 1e-3),
         },
         "checks": {"codes_max": int(out.codes.max()),
                    "mean_winner_is_klein": float((out.winner > 0).float().mean())},

@@ -136,6 +136,30 @@ int ojbkq_destroy(ojbkq_ctx* ctx);
  * Returns EINVAL for an unknown `which`, ESTATE before the first solve.    */
 int ojbkq_inspect(ojbkq_ctx* ctx, int which, const void** ptr);
 
+/* Stage timing of a staged context, for tracing.  With timing enabled, the
+ * accumulate and solve calls record HIP events on the context's stream around
+ * each stage; ojbkq_stage_times() then returns the device milliseconds spent
+ * in each stage since timing was enabled, summed over calls, into
+ * ms_out[OJBKQ_NUM_STAGES] (host memory).  Events are host-side objects; no
+ * device memory is allocated.  Stages:
+ *   GRAM     Gram and mixed-product launches (every accumulate)
+ *   FACTOR   cross term from the mixed product, damping, blocked Cholesky
+ *   SOLVE    scales and zero points, W E^T, the two triangular solves
+ *   CENTRES  centres qbar, Rbar qbar, Klein temperatures
+ *   DECODE   the batched Babai / Klein decode kernel
+ *   SELECT   candidate selection and gather                              */
+enum {
+  OJBKQ_STAGE_GRAM = 0,
+  OJBKQ_STAGE_FACTOR = 1,
+  OJBKQ_STAGE_SOLVE = 2,
+  OJBKQ_STAGE_CENTRES = 3,
+  OJBKQ_STAGE_DECODE = 4,
+  OJBKQ_STAGE_SELECT = 5,
+  OJBKQ_NUM_STAGES = 6
+};
+int ojbkq_set_timing(ojbkq_ctx* ctx, int enable);
+int ojbkq_stage_times(ojbkq_ctx* ctx, double* ms_out);
+
 /* Decode and selection alone (Alg. 1 steps 5-10, Eq. klein_prob, Alg. 4) on a
  * given factor, for testing the decoder in isolation:
  *   R [m, m] float64, upper triangular (row-major; the strict lower part is

@@ -20,7 +20,7 @@ import torch
 __all__ = [
     "OjbkqError", "Params", "library", "library_path", "quantize_layer", "LayerSolver",
     "decode_stage", "klein_log_rho", "workspace_bytes", "decode_workspace_bytes",
-    "ABI_FUNCTIONS", "QuantResult",
+    "ABI_FUNCTIONS", "QuantResult", "STAGES",
 ]
 
 _PKG = os.path.dirname(os.path.abspath(__file__))
@@ -30,8 +30,11 @@ library_path = os.path.join(_PKG, "libojbkq.so")
 ABI_FUNCTIONS = (
     "ojbkq_workspace_bytes", "ojbkq_quantize_layer", "ojbkq_create", "ojbkq_accumulate",
     "ojbkq_solve", "ojbkq_destroy", "ojbkq_inspect", "ojbkq_decode_workspace_bytes",
-    "ojbkq_decode_stage", "ojbkq_klein_log_rho", "ojbkq_last_error",
+    "ojbkq_decode_stage", "ojbkq_klein_log_rho", "ojbkq_last_error", "ojbkq_set_timing",
+    "ojbkq_stage_times",
 )
+
+STAGES = ("gram", "factor", "solve", "centres", "decode", "select")
 
 _STATUS = {0: "OK", -1: "EINVAL", -2: "ENOSPACE", -3: "ENOTPD", -4: "EHIP", -5: "ESTATE"}
 
@@ -79,6 +82,8 @@ def library() -> ctypes.CDLL:
         "ojbkq_decode_stage": (ctypes.c_int, [P, vp, vp, vp, vp, ctypes.c_size_t, vp, vp, vp, vp,
                                               vp, vp]),
         "ojbkq_klein_log_rho": (ctypes.c_double, [i64, i64]),
+        "ojbkq_set_timing": (ctypes.c_int, [vp, ctypes.c_int]),
+        "ojbkq_stage_times": (ctypes.c_int, [vp, ctypes.POINTER(ctypes.c_double)]),
         "ojbkq_last_error": (ctypes.c_char_p, []),
     }
     for name, (res, args) in sig.items():
@@ -259,6 +264,16 @@ class LayerSolver:
         count = int(math.prod(shape))
         flat = self.ws[off:off + 8 * count].view(torch.float64)
         return flat.reshape(shape).clone()
+
+    def set_timing(self, enable: bool = True):
+        """Record per-stage device times from now on (see ojbkq_stage_times)."""
+        _check(library().ojbkq_set_timing(self.h, 1 if enable else 0))
+
+    def stage_times(self) -> dict:
+        """Device milliseconds per stage since timing was enabled."""
+        arr = (ctypes.c_double * len(STAGES))()
+        _check(library().ojbkq_stage_times(self.h, arr))
+        return {name: float(arr[i]) for i, name in enumerate(STAGES)}
 
     def close(self):
         if getattr(self, "h", None) is not None and self.h.value:

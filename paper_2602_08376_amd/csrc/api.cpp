@@ -10,6 +10,7 @@
 #include <cstring>
 #include <new>
 #include <string>
+#include <utility>
 #include <vector>
 
 #include "kernels.h"
@@ -174,6 +175,11 @@ struct ojbkq_ctx {
   bool cross_seen = false;
   bool factored = false;
   bool solved = false;
+  // stage timing: event pairs recorded per stage, folded into ms[] at sync points
+  bool timing = false;
+  std::vector<std::pair<int, std::pair<hipEvent_t, hipEvent_t>>> pending;
+  std::vector<hipEvent_t> pool;
+  double ms[OJBKQ_NUM_STAGES] = {0, 0, 0, 0, 0, 0};
 
   template <typename T>
   T* at(size_t off) const {
@@ -182,6 +188,55 @@ struct ojbkq_ctx {
 };
 
 namespace {
+
+hipEvent_t take_event(ojbkq_ctx* c) {
+  if (!c->pool.empty()) {
+    hipEvent_t e = c->pool.back();
+    c->pool.pop_back();
+    return e;
+  }
+  hipEvent_t e = nullptr;
+  if (hipEventCreate(&e) != hipSuccess) return nullptr;
+  return e;
+}
+
+// Opens a timed stage: returns the start event (null when timing is off).
+hipEvent_t stage_begin(ojbkq_ctx* c) {
+  if (!c->timing) return nullptr;
+  hipEvent_t e = take_event(c);
+  if (e) (void)hipEventRecord(e, c->stream);
+  return e;
+}
+
+void stage_end(ojbkq_ctx* c, int stage, hipEvent_t start) {
+  if (!c->timing || !start) return;
+  hipEvent_t e = take_event(c);
+  if (!e) return;
+  (void)hipEventRecord(e, c->stream);
+  c->pending.push_back({stage, {start, e}});
+}
+
+// After a stream sync: fold the recorded pairs into the per-stage sums.
+void fold_times(ojbkq_ctx* c) {
+  for (auto& pe : c->pending) {
+    float ms = 0.0f;
+    if (hipEventElapsedTime(&ms, pe.second.first, pe.second.second) == hipSuccess)
+      c->ms[pe.first] += ms;
+    c->pool.push_back(pe.second.first);
+    c->pool.push_back(pe.second.second);
+  }
+  c->pending.clear();
+}
+
+void release_events(ojbkq_ctx* c) {
+  for (auto& pe : c->pending) {
+    (void)hipEventDestroy(pe.second.first);
+    (void)hipEventDestroy(pe.second.second);
+  }
+  for (hipEvent_t e : c->pool) (void)hipEventDestroy(e);
+  c->pending.clear();
+  c->pool.clear();
+}
 
 int ctx_init(ojbkq_ctx* c, const ojbkq_params* p, void* ws, size_t bytes, void* stream) {
   int rc = check_params(p);
@@ -216,11 +271,13 @@ int ctx_accumulate(ojbkq_ctx* c, const float* Xr, const float* Xq, int64_t T, in
   if (T < 1) return fail(OJBKQ_EINVAL, "token count must be >= 1");
   if (ldx < T) return fail(OJBKQ_EINVAL, "ldx must be >= T");
   const bool cross = Xr != nullptr && Xr != Xq;
+  hipEvent_t t0 = stage_begin(c);
   OJBKQ_HIP(ojbkq::gram_cross(Xq, cross ? Xr : nullptr, c->s.m, T, ldx, c->at<double>(c->L.G),
                               c->at<double>(c->L.E), c->any_chunk, c->cross_seen,
                               c->at<uint32_t>(c->L.gc_tiles), c->at<void>(c->L.gc_scratch),
                               gram_shares(), c->stream),
             "gram and cross term");
+  stage_end(c, OJBKQ_STAGE_GRAM, t0);
   if (cross) c->cross_seen = true;
   c->any_chunk = true;
   return OJBKQ_OK;
@@ -232,6 +289,7 @@ int finish(ojbkq_ctx* c) {
                            c->stream),
             "status read");
   OJBKQ_HIP(hipStreamSynchronize(c->stream), "stream sync");
+  fold_times(c);
   if (st != kStatusClear)
     return fail(OJBKQ_ENOTPD, "damped Gram is not positive definite (pivot " + std::to_string(st) +
                                   ")");
@@ -247,12 +305,15 @@ int ctx_solve(ojbkq_ctx* c, const float* W, double alpha, uint8_t* codes, float*
   const Shape& s = c->s;
   hipStream_t st = c->stream;
   double* Lf = c->at<double>(c->L.G);
+  hipEvent_t t0 = stage_begin(c);
   if (!c->factored) {
     if (c->cross_seen)   // mixed product -> cross term, while G is still the Gram
       OJBKQ_HIP(ojbkq::cross_from_mixed(c->at<double>(c->L.E), Lf, s.m, st), "cross term");
     OJBKQ_HIP(ojbkq::launch_damp(Lf, s.m, c->p.lambda_rel, c->at<double>(c->L.lam2), st), "damp");
     OJBKQ_HIP(ojbkq::cholesky_lower(Lf, s.m, c->at<int>(c->L.status), st), "cholesky");
     c->factored = true;
+    stage_end(c, OJBKQ_STAGE_FACTOR, t0);
+    t0 = stage_begin(c);
   }
   OJBKQ_HIP(ojbkq::launch_scale_zero(W, s.n, s.m, s.g, s.G, s.qmax, scales, zeros, st),
             "scales");
@@ -267,6 +328,8 @@ int ctx_solve(ojbkq_ctx* c, const float* W, double alpha, uint8_t* codes, float*
     OJBKQ_HIP(ojbkq::gemm_f64(g, st), "target projection");
     OJBKQ_HIP(ojbkq::solve_llt(Lf, U, s.n, s.m, st), "solves");
   }
+  stage_end(c, OJBKQ_STAGE_SOLVE, t0);
+  t0 = stage_begin(c);
   double* qbar = c->at<double>(c->L.qbar);
   OJBKQ_HIP(ojbkq::launch_centres(W, cross ? U : nullptr, 1.0 - alpha, scales, zeros, s.n, s.m,
                                   s.g, s.G, qbar, U, st),
@@ -283,6 +346,7 @@ int ctx_solve(ojbkq_ctx* c, const float* W, double alpha, uint8_t* codes, float*
   double* al = c->at<double>(c->L.alpha);
   OJBKQ_HIP(ojbkq::launch_klein_alpha(Lf, scales, s.n, s.m, s.g, s.G, log_rho(s.m, s.K), al, st),
             "klein alpha");
+  stage_end(c, OJBKQ_STAGE_CENTRES, t0);
   ojbkq::DecodeDesc d;
   d.L = Lf; d.gq = gq; d.S = scales; d.alpha = al;
   d.m = s.m; d.n = s.n; d.g = s.g; d.G = s.G; d.K = (int)s.K; d.bits = c->p.bits;
@@ -290,10 +354,14 @@ int ctx_solve(ojbkq_ctx* c, const float* W, double alpha, uint8_t* codes, float*
   d.wg_paths = s.geo.wg_paths; d.threads = s.geo.threads;
   d.pcodes = c->at<uint8_t>(c->L.pcodes);
   d.presid = c->at<double>(c->L.presid);
+  t0 = stage_begin(c);
   OJBKQ_HIP(ojbkq::launch_decode(d, st), "decode");
+  stage_end(c, OJBKQ_STAGE_DECODE, t0);
+  t0 = stage_begin(c);
   OJBKQ_HIP(ojbkq::launch_select(d.pcodes, d.presid, s.n, s.m, (int)s.K, s.geo, codes, residuals,
                                  winner, nullptr, nullptr, st),
             "select");
+  stage_end(c, OJBKQ_STAGE_SELECT, t0);
   c->solved = true;
   return finish(c);
 }
@@ -357,7 +425,27 @@ int ojbkq_solve(ojbkq_ctx* ctx, const float* W, double alpha, uint8_t* codes, fl
 
 int ojbkq_destroy(ojbkq_ctx* ctx) {
   g_error.clear();
+  if (ctx) release_events(ctx);
   delete ctx;
+  return OJBKQ_OK;
+}
+
+int ojbkq_set_timing(ojbkq_ctx* ctx, int enable) {
+  g_error.clear();
+  if (!ctx) return fail(OJBKQ_EINVAL, "ctx is NULL");
+  ctx->timing = enable != 0;
+  for (double& v : ctx->ms) v = 0.0;
+  return OJBKQ_OK;
+}
+
+int ojbkq_stage_times(ojbkq_ctx* ctx, double* ms_out) {
+  g_error.clear();
+  if (!ctx || !ms_out) return fail(OJBKQ_EINVAL, "ctx and ms_out are required");
+  if (!ctx->pending.empty()) {
+    OJBKQ_HIP(hipStreamSynchronize(ctx->stream), "stream sync");
+    fold_times(ctx);
+  }
+  for (int i = 0; i < OJBKQ_NUM_STAGES; ++i) ms_out[i] = ctx->ms[i];
   return OJBKQ_OK;
 }
 

@@ -275,3 +275,23 @@ def test_not_positive_definite_reported():
         ok.quantize_layer(W, Xr, Xq, 0.5, 4, 128, 2, 0, lambda_rel=0.0)
     assert ei.value.code == "ENOTPD" and "17" in str(ei.value)
     ok.quantize_layer(W, Xr, Xq, 0.5, 4, 128, 2, 0, lambda_rel=0.01)   # damping repairs it
+
+
+def test_stage_timing():
+    cfg = small_cfg(256, 64, 1024, 4, 128, 8, 81)
+    W, Xr, Xq = make_layer(cfg, device=DEV)
+    s = ok.LayerSolver(cfg.m, cfg.n, cfg.bits, cfg.group, cfg.K, cfg.klein_seed, device=DEV)
+    s.set_timing(True)
+    s.accumulate(Xr, Xq)
+    g1 = s.solve(W, 0.5)
+    t1 = s.stage_times()
+    assert set(t1) == set(ok.STAGES)
+    assert all(v > 0.0 for v in t1.values()), t1
+    g2 = s.solve(W, 0.0)             # the factor is reused: no second factor stage
+    t2 = s.stage_times()
+    assert t2["factor"] == t1["factor"] and t2["decode"] > t1["decode"]
+    s.set_timing(False)
+    assert all(v == 0.0 for v in s.stage_times().values())
+    one = ok.quantize_layer(W, Xr, Xq, 0.5, cfg.bits, cfg.group, cfg.K, cfg.klein_seed)
+    assert torch.equal(one.codes, g1.codes)     # timing changes nothing
+    s.close()
