@@ -86,6 +86,7 @@ constexpr int kMinT = 256;                       // workgroups have 256 .. 512 l
 constexpr int kRPer = (kFC * kBS + kMinT - 1) / kMinT;   // R values staged per thread, at most
 constexpr int kQPer = kFC / 16;                  // 16-byte code packets per thread
 static_assert(kRBytes + kQBytesMax <= kAccBytes, "staging buffers must fit in the update buffer");
+static_assert(kBS == kDecodePanel, "decoder blocks are the panels of the factor copy");
 
 __global__ __launch_bounds__(kMaxT, 2) void decode_kernel(DecodeDesc d) {
   // The staged R / code chunks of the lazy update and its [row][path] result
@@ -134,11 +135,12 @@ __global__ __launch_bounds__(kMaxT, 2) void decode_kernel(DecodeDesc d) {
     const int64_t i0 = b * kBS;
     const int64_t i1 = (i0 + kBS < m) ? i0 + kBS : m;
     const int bl = (int)(i1 - i0);
+    const double* const Lpan = d.Lp + b * m * kBS;   // this block's 32 columns, rows contiguous
 
     __syncthreads();   // the previous block is done with sT / sAcc / codes
     for (int e = tid; e < kBS * kBS; e += T) {
       const int r = e / kBS, c = e % kBS;
-      sT[r][c] = (r < bl && c <= r) ? d.L[(i0 + r) * m + i0 + c] : 0.0;
+      sT[r][c] = (r < bl && c <= r) ? Lpan[(i0 + r) * kBS + c] : 0.0;
     }
 
     // ---- lazy update from every decided row f >= i1 (MFMA) ----
@@ -159,7 +161,7 @@ __global__ __launch_bounds__(kMaxT, 2) void decode_kernel(DecodeDesc d) {
       const int e_ = tid + q_ * T;                                                      \
       const int ff_ = e_ / kBS, cc_ = e_ % kBS;                                         \
       const int64_t f_ = (F0) + ff_;                                                    \
-      rr[q_] = (e_ < kFC * kBS && f_ < m && i0 + cc_ < i1) ? d.L[f_ * m + i0 + cc_] : 0.0; \
+      rr[q_] = (e_ < kFC * kBS && f_ < m && i0 + cc_ < i1) ? Lpan[f_ * kBS + cc_] : 0.0;   \
     }                                                                                   \
     _Pragma("unroll") for (int q_ = 0; q_ < kQPer; ++q_) {                              \
       const int e_ = tid + q_ * T;                                                      \
@@ -301,7 +303,27 @@ __global__ __launch_bounds__(256) void select_kernel(const uint8_t* __restrict__
   }
 }
 
+// Lp[b][f][c] = L[f][32 b + c], zero past column m.
+__global__ __launch_bounds__(256) void panel_copy_kernel(const double* __restrict__ L, int64_t m,
+                                                         double* __restrict__ Lp) {
+  const int64_t total = decode_panel_elems(m);
+  for (int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x; e < total;
+       e += (int64_t)gridDim.x * 256) {
+    const int64_t b = e / (m * kDecodePanel);
+    const int64_t rem = e % (m * kDecodePanel);
+    const int64_t f = rem / kDecodePanel, c = b * kDecodePanel + rem % kDecodePanel;
+    Lp[e] = (c < m) ? L[f * m + c] : 0.0;
+  }
+}
+
 }  // namespace
+
+hipError_t launch_panel_copy(const double* L, int64_t m, double* Lp, hipStream_t stream) {
+  const int64_t blocks = (decode_panel_elems(m) + 255) / 256;
+  panel_copy_kernel<<<dim3((unsigned)(blocks < 65536 ? blocks : 65536)), dim3(256), 0, stream>>>(
+      L, m, Lp);
+  return hipGetLastError();
+}
 
 hipError_t launch_decode(const DecodeDesc& d, hipStream_t stream) {
   const DecodeGeom geo = decode_geometry(d.n, d.K);

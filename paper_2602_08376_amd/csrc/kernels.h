@@ -119,8 +119,16 @@ inline DecodeGeom decode_geometry(int64_t n, int K) {
   return g;
 }
 
+// Panel-major copy of the factor for the decoder: Lp[b][f][c] = L[f][32 b + c]
+// (zero beyond m), so the rows f of one 32-column panel are contiguous.
+constexpr int kDecodePanel = 32;
+__host__ __device__ inline int64_t decode_panel_elems(int64_t m) {
+  return ((m + kDecodePanel - 1) / kDecodePanel) * m * kDecodePanel;
+}
+hipError_t launch_panel_copy(const double* L, int64_t m, double* Lp, hipStream_t stream);
+
 struct DecodeDesc {
-  const double* L = nullptr;   // [m, m] lower factor (L = R^T)
+  const double* Lp = nullptr;  // panel-major factor (decode_panel_elems(m) doubles)
   const double* gq = nullptr;  // [n, m]: gq_j = Rbar_j qbar_j
   const float* S = nullptr;    // [n, G]
   const double* alpha = nullptr;  // [n]
