@@ -61,7 +61,7 @@ Shape shape_of(const ojbkq_params& p) {
 // Offsets of every buffer carved from the workspace.
 struct Layout {
   size_t status = 0, lam2 = 0, G = 0, E = 0, U = 0, qbar = 0, gq = 0, alpha = 0, pcodes = 0,
-         presid = 0, gc_scratch = 0, gc_tiles = 0, Lp = 0, total = 0;
+         presid = 0, gc_scratch = 0, gc_tiles = 0, F = 0, total = 0;
 };
 
 Layout layout_full(const Shape& s) {
@@ -82,11 +82,11 @@ Layout layout_full(const Shape& s) {
   L.qbar = take(nm);
   L.gq = take(nm);
   L.alpha = take((size_t)s.n * sizeof(double));
-  L.pcodes = take((size_t)s.geo.nwg * (size_t)s.geo.threads * (size_t)s.m);
+  L.pcodes = take((size_t)ojbkq::decode_code_bytes(s.m, s.geo));
   L.presid = take((size_t)s.paths * sizeof(double));
   L.gc_scratch = take(ojbkq::gram_cross_scratch_bytes());
   L.gc_tiles = take((size_t)ojbkq::gram_tile_count(s.m) * sizeof(uint32_t));
-  L.Lp = take((size_t)ojbkq::decode_panel_elems(s.m) * sizeof(double));
+  L.F = take((size_t)ojbkq::decode_tile_count(s.m) * ojbkq::kDecodeTile * sizeof(double));
   L.total = off;
   return L;
 }
@@ -115,9 +115,9 @@ Layout layout_decode(const Shape& s) {
   L.U = take(nm);
   L.gq = take(nm);
   L.alpha = take((size_t)s.n * sizeof(double));
-  L.pcodes = take((size_t)s.geo.nwg * (size_t)s.geo.threads * (size_t)s.m);
+  L.pcodes = take((size_t)ojbkq::decode_code_bytes(s.m, s.geo));
   L.presid = take((size_t)s.paths * sizeof(double));
-  L.Lp = take((size_t)ojbkq::decode_panel_elems(s.m) * sizeof(double));
+  L.F = take((size_t)ojbkq::decode_tile_count(s.m) * ojbkq::kDecodeTile * sizeof(double));
   L.total = off;
   return L;
 }
@@ -313,7 +313,7 @@ int ctx_solve(ojbkq_ctx* c, const float* W, double alpha, uint8_t* codes, float*
       OJBKQ_HIP(ojbkq::cross_from_mixed(c->at<double>(c->L.E), Lf, s.m, st), "cross term");
     OJBKQ_HIP(ojbkq::launch_damp(Lf, s.m, c->p.lambda_rel, c->at<double>(c->L.lam2), st), "damp");
     OJBKQ_HIP(ojbkq::cholesky_lower(Lf, s.m, c->at<int>(c->L.status), st), "cholesky");
-    OJBKQ_HIP(ojbkq::launch_panel_copy(Lf, s.m, c->at<double>(c->L.Lp), st), "factor panels");
+    OJBKQ_HIP(ojbkq::launch_decode_tiles(Lf, s.m, c->at<double>(c->L.F), st), "decoder tiles");
     c->factored = true;
     stage_end(c, OJBKQ_STAGE_FACTOR, t0);
     t0 = stage_begin(c);
@@ -351,7 +351,7 @@ int ctx_solve(ojbkq_ctx* c, const float* W, double alpha, uint8_t* codes, float*
             "klein alpha");
   stage_end(c, OJBKQ_STAGE_CENTRES, t0);
   ojbkq::DecodeDesc d;
-  d.Lp = c->at<double>(c->L.Lp); d.gq = gq; d.S = scales; d.alpha = al;
+  d.F = c->at<double>(c->L.F); d.gq = gq; d.S = scales; d.alpha = al;
   d.m = s.m; d.n = s.n; d.g = s.g; d.G = s.G; d.K = (int)s.K; d.bits = c->p.bits;
   d.seed = c->p.seed;
   d.wg_paths = s.geo.wg_paths; d.threads = s.geo.threads;
@@ -509,10 +509,10 @@ int ojbkq_decode_stage(const ojbkq_params* p, const double* R, const double* qba
   }
   OJBKQ_HIP(ojbkq::launch_klein_alpha(Lf, scales, s.n, s.m, s.g, s.G, log_rho(s.m, s.K), al, st),
             "klein alpha");
-  OJBKQ_HIP(ojbkq::launch_panel_copy(Lf, s.m, reinterpret_cast<double*>(ws + L.Lp), st),
-            "factor panels");
+  OJBKQ_HIP(ojbkq::launch_decode_tiles(Lf, s.m, reinterpret_cast<double*>(ws + L.F), st),
+            "decoder tiles");
   ojbkq::DecodeDesc d;
-  d.Lp = reinterpret_cast<double*>(ws + L.Lp); d.gq = gq; d.S = scales; d.alpha = al;
+  d.F = reinterpret_cast<double*>(ws + L.F); d.gq = gq; d.S = scales; d.alpha = al;
   d.m = s.m; d.n = s.n; d.g = s.g; d.G = s.G; d.K = (int)s.K; d.bits = p->bits; d.seed = p->seed;
   d.wg_paths = s.geo.wg_paths; d.threads = s.geo.threads;
   d.pcodes = reinterpret_cast<uint8_t*>(ws + L.pcodes);

@@ -8,258 +8,322 @@
 // the one shared factor R: path 0 rounds each centre to the nearest box point,
 // paths 1..K draw each code from Pr(v) ~ exp(-alpha_j Rbar_ii^2 (c_i - v)^2).
 //
-// Layout.  A workgroup owns wg_paths consecutive paths (path p = j (K + 1) +
-// k), one per lane; wg_paths is chosen so that all workgroups of a round fit
-// one per CU.  It walks the rows i = m-1 .. 0 in blocks of kBS rows.  With
-// e_l = s_j(l) q_l the centre of row i is
+// Layout.  Path p = j (K + 1) + k runs on one lane; a wave owns up to 64
+// consecutive paths in whole 16-path tiles and walks the rows i = m-1 .. 0 in
+// blocks of 32 rows without ever waiting for another wave.  With e_l = s_j(l) q_l the centre of
+// row i is
 //     c_i = z_i / Rbar_ii,  z_i = (Rbar_j qbar_j)_i - sum_{l > i} R_il e_l,
-// where (Rbar_j qbar_j) is precomputed for every column by one GEMM.  The
-// sum splits into
-//   * rows l of earlier blocks: one 32 x |F| by |F| x 64 product per wave
-//     (16-path tiles that hold no path are skipped),
-//     R (shared by every path, streamed from L2 as rows of L = R^T) against
-//     the codes already decided (bytes, scaled by s on the fly), on
-//     v_mfma_f64_16x16x4_f64 -- the lazy batched update;
+// where Rbar_j qbar_j is precomputed for every column by one GEMM.  The sum
+// splits into
+//   * rows l of earlier blocks: per block of 32 decided rows, a 32 x 32 by
+//     32 x 64 product on v_mfma_f64_16x16x4_f64 (16-path tiles that hold no
+//     path are skipped) -- R streamed from L2 in the MFMA operand order of a
+//     re-laid-out copy of the factor, the decided codes read back as bytes
+//     and scaled by s on the fly -- the lazy batched update, one block of
+//     operands prefetched ahead;
 //   * rows of the current block: updated in registers after each decision,
-//     with the 32x32 diagonal block of R broadcast from LDS.
-// The MFMA result is transposed through LDS so that each lane then holds
-// the 32 partial centres of its own path for the serial in-block steps.
-// Decided codes go to a per-workgroup [m][threads] byte buffer that is both
-// the operand of later updates and the source of the selection gather.
+//     with the 32 x 32 diagonal block of R broadcast from the wave's LDS.
+// The MFMA result is transposed through the wave's LDS so that each lane then
+// holds the 32 partial centres of its own path for the serial steps.  Each
+// lane keeps its 32 decided codes in registers and stores them as one 32-byte
+// segment per block: the operand of later updates and the source of the
+// selection gather.
 #include "kernels.h"
 #include "device.h"
 
 namespace ojbkq {
 namespace {
 
-constexpr int kBS = 32;   // rows per serial block
+constexpr int kBS = kDecodeBlock;                 // rows per serial block
+constexpr int kGR = 4;                            // rows per serial group
+constexpr int kWaveLds = kBS * 64 * (int)sizeof(double);   // LDS per wave: z of 32 rows x 64 paths
+constexpr int kSeg = kBS;                         // code bytes per (block, lane)
+constexpr int kBlockCodes = 64 * kSeg;            // code bytes per (wave, block)
+static_assert(kBS == 32, "the block is eight 4-row MFMA steps and one 32-byte code segment");
 
-__device__ __forceinline__ int babai_round(double c, int qmax) {
-  const double r = fmin(fmax(rint(c), 0.0), (double)qmax);
-  return (int)r;
+// Position of row r of a block in its 32-byte code segment: rows 4 s + h,
+// s = 0..7, are the eight bytes 8 h .. 8 h + 7, so the lane that feeds row
+// offset h of every 4-row MFMA step reads its codes with one 8-byte load.
+__host__ __device__ constexpr int seg_byte(int r) { return 8 * (r % 4) + r / 4; }
+static_assert(kBS % kGR == 0 && kBS / kGR <= 8, "a lane packs one code byte per group");
+
+// Log-weight floor of the Klein draw: box points whose weight is below
+// exp(-kLogCut) times the largest one are not evaluated.  Even all 256 of
+// them together hold less than 2^-55 of the probability mass, below the
+// rounding of the running sums, so the draw is that of the full box.
+constexpr double kLogCut = 45.0;
+
+__device__ __forceinline__ double nearest_box_point(double c, int qmax) {
+  return fmin(fmax(rint(c), 0.0), (double)qmax);
 }
 
 // Inverse-CDF draw of v in {0..qmax} with weights exp(-kappa (c - v)^2),
 // normalised by the largest weight (the nearest box point): the smallest v
-// whose running weight sum exceeds u times the total; if rounding leaves
-// none, the largest v with a non-zero weight.  kappa = inf: nearest point.
-// Only the window of v whose exponent is >= -750 is evaluated: outside it
-// exp() is exactly 0 in double precision, so the sums are unchanged.
-__device__ __noinline__ int klein_pick(double c, double kappa, double u, int qmax) {
-  if (!(kappa < INFINITY)) return babai_round(c, qmax);
-  const double nk = -kappa;
-  const double vs = fmin(fmax(rint(c), 0.0), (double)qmax);
+// whose running weight sum exceeds u times the total, else the last one.
+// kappa = inf: the nearest point.  Over the window of non-negligible weights
+// the ratio of neighbouring weights, exp(-kappa (2 (v - c) + 1)), itself
+// changes by the constant factor exp(-2 kappa) per step, so three
+// exponentials give every weight.
+__device__ __forceinline__ int klein_pick(double c, double kappa, double u, int qmax) {
+  const double vs = nearest_box_point(c, qmax);
+  if (!(kappa < INFINITY)) return (int)vs;
   const double ts = c - vs;
-  const double top = nk * (ts * ts);   // the largest exponent
-  int lo = 0, hi = qmax;
+  double lo = 0.0, hi = (double)qmax;
   if (kappa > 0.0) {
-    const double rad = sqrt(750.0 / kappa + ts * ts) + 1.0;
-    const double a = ceil(c - rad), b = floor(c + rad);
-    if (a > 0.0) lo = a > (double)qmax ? qmax : (int)a;
-    if (b < (double)qmax) hi = b < 0.0 ? 0 : (int)b;
+    const double rad = sqrt(kLogCut / kappa + ts * ts);
+    lo = fmin(fmax(ceil(c - rad), 0.0), vs);
+    hi = fmax(fmin(floor(c + rad), (double)qmax), vs);
   }
-  double total = 0.0;
-  for (int v = lo; v <= hi; ++v) {
-    const double t = c - (double)v;
-    total += exp(nk * (t * t) - top);
+  if (lo == hi) return (int)lo;
+  const double nk = -kappa;
+  const double t0 = c - lo;
+  const double w0 = exp(nk * (t0 * t0 - ts * ts));   // weight of lo
+  const double r0 = exp(nk * (1.0 - 2.0 * t0));      // weight(lo + 1) / weight(lo)
+  const double q2 = exp(-2.0 * kappa);
+  const int nv = (int)(hi - lo);
+  double total = 0.0, w = w0, r = r0;
+  for (int v = 0; v <= nv; ++v) {
+    total += w;
+    w *= r;
+    r *= q2;
   }
   const double thr = u * total;
   double cum = 0.0;
-  int last = -1;
-  for (int v = lo; v <= hi; ++v) {
-    const double t = c - (double)v;
-    const double w = exp(nk * (t * t) - top);
+  w = w0;
+  r = r0;
+  for (int v = 0; v < nv; ++v) {
     cum += w;
-    if (thr < cum) return v;
-    if (w > 0.0) last = v;
+    if (thr < cum) return (int)lo + v;
+    w *= r;
+    r *= q2;
   }
-  return last < 0 ? (int)vs : last;
+  return (int)hi;
 }
 
-constexpr int kFC = 64;          // decided rows per staged chunk of the lazy update
-constexpr int kMaxT = kDecodeMaxThreads;
-constexpr int kQPad = 16;        // bank padding of a staged code row (bytes)
-constexpr int kAccBytes = kBS * kMaxT * (int)sizeof(double);
-constexpr int kRBytes = 2 * kFC * kBS * (int)sizeof(double);
-constexpr int kQBytesMax = 2 * kFC * (kMaxT + kQPad);
-constexpr int kMinT = 256;                       // workgroups have 256 .. 512 lanes
-constexpr int kRPer = (kFC * kBS + kMinT - 1) / kMinT;   // R values staged per thread, at most
-constexpr int kQPer = kFC / 16;                  // 16-byte code packets per thread
-static_assert(kRBytes + kQBytesMax <= kAccBytes, "staging buffers must fit in the update buffer");
-static_assert(kBS == kDecodePanel, "decoder blocks are the panels of the factor copy");
+// All lanes of the wave have finished their LDS / global accesses before any
+// lane goes on (lanes of one wave run in lockstep; this orders the memory
+// operations and keeps the compiler from moving them across).
+__device__ __forceinline__ void wave_sync() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
+}
 
-__global__ __launch_bounds__(kMaxT, 2) void decode_kernel(DecodeDesc d) {
-  // The staged R / code chunks of the lazy update and its [row][path] result
-  // are never live together, so they share one buffer.
-  __shared__ __align__(16) unsigned char smem[kAccBytes];
-  __shared__ double sT[kBS][kBS + 1];            // sT[r][c] = R[i0 + c][i0 + r], c <= r
-  const int T = d.threads;                       // lanes (= code-row bytes) per workgroup
-  const int qrow = T + kQPad;
-  double* const sAcc = reinterpret_cast<double*>(smem);                  // [kBS][T]
-  double (*sR)[kFC][kBS] = reinterpret_cast<double (*)[kFC][kBS]>(smem);  // [2][kFC][kBS]
-  unsigned char* const sQ = smem + kRBytes;                              // [2][kFC][qrow]
+// A scale for the lazy update, read where it is prefetched: as a relaxed
+// atomic (a plain load at workgroup scope) it is not merged across the
+// operand sets into a late load at the point of use.
+__device__ __forceinline__ float load_scale(const float* p) {
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+}
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+// Codes and scales of one decided block for the lazy update (operand B).
+template <int NT, bool kUniS>
+struct BOperand {
+  uint2 q[NT];         // codes of rows 4 s + l / 16, s = 0..7, of path 16 t + l % 16
+  float sc[NT][kUniS ? 1 : 8];
+};
+
+template <int NT, bool kUniS>
+__device__ __forceinline__ void load_b(BOperand<NT, kUniS>& c, const DecodeDesc& d, int64_t bb,
+                                       const uint8_t* cw, const uint32_t (&so)[NT], int lane) {
+  const uint8_t* Bt = cw + bb * kBlockCodes + (lane & 15) * kSeg + 8 * (lane >> 4);
+#pragma unroll
+  for (int t = 0; t < NT; ++t) c.q[t] = *reinterpret_cast<const uint2*>(Bt + t * 16 * kSeg);
+  if constexpr (kUniS) {
+    const uint32_t grp = d.G == 1 ? 0u : (uint32_t)(bb * kBS) / (uint32_t)d.g;
+#pragma unroll
+    for (int t = 0; t < NT; ++t) c.sc[t][0] = load_scale(d.S + (so[t] + grp));
+  } else {
+#pragma unroll
+    for (int s = 0; s < 8; ++s) {
+      int64_t f = bb * kBS + 4 * s + (lane >> 4);
+      f = f < d.m ? f : d.m - 1;
+      const uint32_t grp = (uint32_t)f / (uint32_t)d.g;
+#pragma unroll
+      for (int t = 0; t < NT; ++t) c.sc[t][s] = load_scale(d.S + (so[t] + grp));
+    }
+  }
+}
+
+// The lazy update of block b for a wave with NT tiles: acc += R[block b][bb]
+// E[bb] over the decided blocks bb = nb-1 .. b+1, E = codes scaled by s.
+// Operands stream one block ahead: each MFMA step's A fragment (R, two
+// doubles per lane) is refilled with the next block's as soon as it has been
+// used, and the next block's codes and scales are fetched at the start of a
+// block (the last round re-reads block b + 1 rather than branch around the
+// loads).
+template <int NT, bool kUniS>
+__device__ __forceinline__ void lazy_update(const DecodeDesc& d, int64_t nb, int64_t b,
+                                            const uint8_t* cw, const uint32_t (&so)[NT],
+                                            d4 (&acc)[2][NT], int lane) {
+  double2 a[8];   // R[16 a + l % 16][4 s + l / 16], a = 0, 1, for the 4-row steps s = 0..7
+  const double* At = d.F + decode_offdiag_tile(nb, b, nb - 1) * kDecodeTile + 2 * lane;
+#pragma unroll
+  for (int s = 0; s < 8; ++s) a[s] = *reinterpret_cast<const double2*>(At + s * 128);
+  BOperand<NT, kUniS> cur, nxt;
+  load_b(cur, d, nb - 1, cw, so, lane);
+  for (int64_t bb = nb - 1; bb > b; --bb) {
+    const int64_t bn = bb - 1 > b ? bb - 1 : b + 1;
+    load_b(nxt, d, bn, cw, so, lane);
+    const double* An = d.F + decode_offdiag_tile(nb, b, bn) * kDecodeTile + 2 * lane;
+    double sc[NT];
+    if constexpr (kUniS) {
+#pragma unroll
+      for (int t = 0; t < NT; ++t) sc[t] = (double)cur.sc[t][0];
+    }
+#pragma unroll
+    for (int s = 0; s < 8; ++s) {
+#pragma unroll
+      for (int t = 0; t < NT; ++t) {
+        const uint32_t code = (((s < 4) ? cur.q[t].x : cur.q[t].y) >> (8 * (s & 3))) & 0xffu;
+        const double st = kUniS ? sc[t] : (double)cur.sc[t][kUniS ? 0 : s];
+        const double bv = (double)code * st;
+        acc[0][t] = mfma_f64(a[s].x, bv, acc[0][t]);
+        acc[1][t] = mfma_f64(a[s].y, bv, acc[1][t]);
+      }
+      a[s] = *reinterpret_cast<const double2*>(An + s * 128);
+    }
+    cur = nxt;
+  }
+}
+
+// One wave's share of the decode: paths pbase .. pbase + npw - 1 (npw <= 64,
+// in NT = ceil(npw / 16) tiles), codes at cw, LDS buffer sZ of kWaveLds bytes.
+template <int NT, bool kUniS>
+__device__ __forceinline__ void decode_wave(const DecodeDesc& d, int64_t pbase, int npw,
+                                            uint8_t* cw, double* sZ) {
+  const int lane = threadIdx.x & 63;
   const int64_t m = d.m, g = d.g, G = d.G;
   const int64_t kp1 = (int64_t)d.K + 1;
-  const int64_t P = d.n * kp1;
-  const int64_t wg = blockIdx.x;
-  const int64_t base = wg * d.wg_paths;           // first path of this workgroup
-  const int64_t npaths = (P - base) < d.wg_paths ? (P - base) : d.wg_paths;
-  const int64_t p = base + tid;
-  const bool valid = tid < npaths;
-  const int64_t j = valid ? p / kp1 : 0;
-  const uint32_t kk = valid ? (uint32_t)(p % kp1) : 0u;
+  const int64_t nb = (m + kBS - 1) / kBS;
+  const bool valid = lane < npw;
+  const int64_t p = pbase + (valid ? lane : 0);
+  const int64_t j = p / kp1;
+  const uint32_t kk = (uint32_t)(p - j * kp1);
   const int qmax = (1 << d.bits) - 1;
-  const double alpha_j = valid ? d.alpha[j] : 0.0;
-  uint8_t* const cw = d.pcodes + wg * m * T;
-  const double* const gq = d.gq + j * m;
+  const double alpha_j = d.alpha[j];
   const float* const Sj = d.S + j * G;
 
-  // MFMA operand B: tile t of this wave covers its paths 16 t .. 16 t + 15;
-  // this lane feeds path 16 t + (lane % 16) of each.
-  int64_t bcol[4];
-  bool bval[4];
-  int ntile = 0;   // tiles of this wave holding at least one path
+  // MFMA operand B and result: tile t carries path 16 t + l % 16 of this wave.
+  // Scale offsets fit 32 bits (n G < 2^31 is checked on the host).
+  uint32_t so[NT], colB[NT];
 #pragma unroll
-  for (int t = 0; t < 4; ++t) {
-    const int64_t local = wave * 64 + 16 * t + (lane & 15);
-    bval[t] = local < npaths;
-    bcol[t] = bval[t] ? (base + local) / kp1 : 0;
-    if (wave * 64 + 16 * t < npaths) ntile = t + 1;
+  for (int t = 0; t < NT; ++t) {
+    const int loc = 16 * t + (lane & 15);
+    colB[t] = (uint32_t)((pbase + (loc < npw ? loc : 0)) / kp1);
+    so[t] = colB[t] * (uint32_t)G;
   }
 
   double resid = 0.0;
-  const int64_t nblk = (m + kBS - 1) / kBS;
-  for (int64_t b = nblk - 1; b >= 0; --b) {
+  for (int64_t b = nb - 1; b >= 0; --b) {
     const int64_t i0 = b * kBS;
-    const int64_t i1 = (i0 + kBS < m) ? i0 + kBS : m;
-    const int bl = (int)(i1 - i0);
-    const double* const Lpan = d.Lp + b * m * kBS;   // this block's 32 columns, rows contiguous
+    const int bl = (int)((m - i0) < kBS ? (m - i0) : kBS);
 
-    __syncthreads();   // the previous block is done with sT / sAcc / codes
-    for (int e = tid; e < kBS * kBS; e += T) {
-      const int r = e / kBS, c = e % kBS;
-      sT[r][c] = (r < bl && c <= r) ? Lpan[(i0 + r) * kBS + c] : 0.0;
+    // ---- lazy update from the decided blocks (MFMA) ----
+    // The accumulator starts at -(Rbar_j qbar_j) of the block's rows and ends
+    // at -z; its loads are in flight during the products.
+    d4 acc[2][NT];
+#pragma unroll
+    for (int t = 0; t < NT; ++t) {
+      const double* gb = d.gq + (int64_t)colB[t] * m + i0;
+#pragma unroll
+      for (int a = 0; a < 2; ++a)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int row = 16 * a + (lane >> 4) + 4 * r;
+          acc[a][t][r] = (row < bl) ? -gb[row] : 0.0;
+        }
     }
+    if (b + 1 < nb) lazy_update<NT, kUniS>(d, nb, b, cw, so, acc, lane);
 
-    // ---- lazy update from every decided row f >= i1 (MFMA) ----
-    d4 acc[2][4];
+    // ---- transpose through LDS: sZ[r * 64 + l] = -z of row r, path l ----
+    wave_sync();   // the previous block's reads of the buffer are done
 #pragma unroll
     for (int a = 0; a < 2; ++a)
 #pragma unroll
-      for (int t = 0; t < 4; ++t) acc[a][t] = d4{0.0, 0.0, 0.0, 0.0};
-    if (i1 < m) {
-      const int64_t nch = (m - i1 + kFC - 1) / kFC;
-      const int qpk = T / 16;            // 16-byte packets per code row
-      double rr[kRPer];
-      uint4 rq[kQPer];
-      // stage rows f0 .. f0 + kFC of R (columns i0 .. i1) and of the codes
-#define OJBKQ_DECODE_FETCH(F0)                                                          \
-  {                                                                                     \
-    _Pragma("unroll") for (int q_ = 0; q_ < kRPer; ++q_) {                              \
-      const int e_ = tid + q_ * T;                                                      \
-      const int ff_ = e_ / kBS, cc_ = e_ % kBS;                                         \
-      const int64_t f_ = (F0) + ff_;                                                    \
-      rr[q_] = (e_ < kFC * kBS && f_ < m && i0 + cc_ < i1) ? Lpan[f_ * kBS + cc_] : 0.0;   \
-    }                                                                                   \
-    _Pragma("unroll") for (int q_ = 0; q_ < kQPer; ++q_) {                              \
-      const int e_ = tid + q_ * T;                                                      \
-      const int ff_ = e_ / qpk, cc_ = e_ % qpk;                                         \
-      const int64_t f_ = (F0) + ff_;                                                    \
-      rq[q_] = (ff_ < kFC && f_ < m)                                                    \
-                   ? *reinterpret_cast<const uint4*>(cw + f_ * T + cc_ * 16)            \
-                   : make_uint4(0u, 0u, 0u, 0u);                                        \
-    }                                                                                   \
-  }
-      OJBKQ_DECODE_FETCH(i1)
-      int64_t f = i1 + (lane >> 4);   // this lane's row of operand B
-      int64_t gnext = -1;
-      double sb[4] = {0.0, 0.0, 0.0, 0.0};
-      for (int64_t ch = 0; ch < nch; ++ch) {
-        const int buf = (int)(ch & 1);
-#pragma unroll
-        for (int q = 0; q < kRPer; ++q) {
-          const int e = tid + q * T;
-          if (e < kFC * kBS) sR[buf][e / kBS][e % kBS] = rr[q];
-        }
-#pragma unroll
-        for (int q = 0; q < kQPer; ++q) {
-          const int e = tid + q * T;
-          if (e / qpk < kFC)
-            *reinterpret_cast<uint4*>(sQ + (buf * kFC + e / qpk) * qrow + (e % qpk) * 16) = rq[q];
-        }
-        __syncthreads();
-        if (ch + 1 < nch) OJBKQ_DECODE_FETCH(i1 + (ch + 1) * kFC)
-        const unsigned char* qb = sQ + buf * kFC * qrow + wave * 64 + (lane & 15);
-#pragma unroll 4
-        for (int s4 = 0; s4 < kFC / 4; ++s4, f += 4) {
-          const int ff = s4 * 4 + (lane >> 4);
-          if (f < m && f >= gnext) {
-            const int64_t grp = f / g;
-            gnext = (grp + 1) * g;
-#pragma unroll
-            for (int t = 0; t < 4; ++t) sb[t] = bval[t] ? (double)d.S[bcol[t] * G + grp] : 0.0;
-          }
-          double av[2];
-#pragma unroll
-          for (int a = 0; a < 2; ++a) av[a] = sR[buf][ff][16 * a + (lane & 15)];
-#pragma unroll
-          for (int t = 0; t < 4; ++t) {
-            if (t < ntile) {
-              const double bv = (double)qb[ff * qrow + 16 * t] * sb[t];
-#pragma unroll
-              for (int a = 0; a < 2; ++a) acc[a][t] = mfma_f64(av[a], bv, acc[a][t]);
-            }
-          }
-        }
-      }
-      __syncthreads();   // every wave is done with the staged chunks (aliased below)
-#undef OJBKQ_DECODE_FETCH
-    }
-#pragma unroll
-    for (int a = 0; a < 2; ++a)
-#pragma unroll
-      for (int t = 0; t < 4; ++t)
+      for (int t = 0; t < NT; ++t)
 #pragma unroll
         for (int r = 0; r < 4; ++r)
-          sAcc[(16 * a + (lane >> 4) + 4 * r) * T + wave * 64 + 16 * t + (lane & 15)] = acc[a][t][r];
-    __syncthreads();
+          sZ[(16 * a + (lane >> 4) + 4 * r) * 64 + 16 * t + (lane & 15)] = acc[a][t][r];
+    wave_sync();
 
-    // ---- serial in-block steps, one path per lane ----
-    if (valid) {
-      double z[kBS];
+    // ---- serial steps, one path per lane, in groups of four rows from the
+    // top: the group's rows update each other in registers, then the group
+    // updates the rows below it in LDS with one rank-4 step ----
+    const double* const Db = d.F + b * kDecodeTile;   // Db[r * 32 + c] = R[i0 + c][i0 + r]
+    uint64_t wcode[kGR] = {0, 0, 0, 0};   // byte g of wcode[k]: code of row kGR g + k
+    double s_blk = 0.0;
+    if constexpr (kUniS) s_blk = (double)Sj[G == 1 ? 0u : (uint32_t)i0 / (uint32_t)g];
+    for (int g4 = (bl - 1) / kGR; g4 >= 0; --g4) {
+      const int r0 = kGR * g4;
+      double z[kGR], u[kGR], sr[kGR], rb[kGR];
 #pragma unroll
-      for (int r = 0; r < kBS; ++r) z[r] = (r < bl) ? gq[i0 + r] - sAcc[r * T + tid] : 0.0;
-#pragma unroll
-      for (int r = kBS - 1; r >= 0; --r) {
-        if (r < bl) {
-          const int64_t i = i0 + r;
-          const double s = (double)Sj[i / g];
-          const double rb = sT[r][r] * s;   // Rbar_ii
-          const double c = z[r] / rb;       // centre of row i
-          int q;
-          if (kk == 0) {
-            q = babai_round(c, qmax);
-          } else {
-            const double u = klein_uniform(d.seed, (uint32_t)i, (uint32_t)j, kk);
-            q = klein_pick(c, alpha_j * (rb * rb), u, qmax);
-          }
-          const double dq = rb * ((double)q - c);
-          resid += dq * dq;
-          const double e = s * (double)q;
-#pragma unroll
-          for (int r2 = 0; r2 < r; ++r2) z[r2] -= sT[r][r2] * e;
-          cw[i * T + tid] = (uint8_t)q;
-        }
+      for (int k = 0; k < kGR; ++k) {
+        z[k] = -sZ[(r0 + k) * 64 + lane];
+        sr[k] = kUniS ? s_blk : (double)Sj[(uint32_t)(i0 + r0 + k < m ? i0 + r0 + k : m - 1) / (uint32_t)g];
+        rb[k] = Db[(r0 + k) * (kBS + 1)] * sr[k];   // Rbar_ii
+        u[k] = (kk != 0) ? klein_uniform(d.seed, (uint32_t)(i0 + r0 + k), (uint32_t)j, kk) : 0.0;
       }
-    } else {
-      for (int r = 0; r < bl; ++r) cw[(i0 + r) * T + tid] = 0;
+      double e[kGR];
+#pragma unroll
+      for (int k = kGR - 1; k >= 0; --k) {
+        e[k] = 0.0;
+        if (r0 + k < bl && valid) {
+          const double c = z[k] / rb[k];   // centre of row i0 + r0 + k
+          const int q = (kk == 0) ? (int)nearest_box_point(c, qmax)
+                                  : klein_pick(c, alpha_j * (rb[k] * rb[k]), u[k], qmax);
+          const double dq = rb[k] * ((double)q - c);
+          resid += dq * dq;
+          e[k] = sr[k] * (double)q;
+          wcode[k] |= (uint64_t)q << (8 * g4);
+        }
+#pragma unroll
+        for (int k2 = 0; k2 < k; ++k2) z[k2] -= Db[(r0 + k) * kBS + r0 + k2] * e[k];
+      }
+      // rank-4 update of the rows below the group (the buffer holds -z)
+      for (int r2 = r0 - 1; r2 >= 0; --r2) {
+        double v = sZ[r2 * 64 + lane];
+#pragma unroll
+        for (int k = 0; k < kGR; ++k) v += Db[(r0 + k) * kBS + r2] * e[k];
+        sZ[r2 * 64 + lane] = v;
+      }
     }
+    uint8_t* seg = cw + b * kBlockCodes + lane * kSeg;
+    *reinterpret_cast<uint4*>(seg) = make_uint4((uint32_t)wcode[0], (uint32_t)(wcode[0] >> 32),
+                                                (uint32_t)wcode[1], (uint32_t)(wcode[1] >> 32));
+    *reinterpret_cast<uint4*>(seg + 16) = make_uint4((uint32_t)wcode[2], (uint32_t)(wcode[2] >> 32),
+                                                     (uint32_t)wcode[3], (uint32_t)(wcode[3] >> 32));
+    wave_sync();   // codes visible to the later update loads
   }
   if (valid) d.presid[p] = resid;
 }
 
+template <bool kUniS>
+__global__ __launch_bounds__(kDecodeMaxThreads) void decode_kernel(DecodeDesc d) {
+  extern __shared__ __align__(16) double lds[];
+  const int wave = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
+  const int waves = d.threads / 64;
+  const int64_t P = d.n * ((int64_t)d.K + 1);
+  const int64_t wg0 = (int64_t)blockIdx.x * d.wg_paths;
+  const int64_t wgend = (wg0 + d.wg_paths < P) ? wg0 + d.wg_paths : P;
+  const WaveTiles wt = decode_wave_tiles((int)(d.wg_paths / 16), waves, wave);
+  const int64_t pbase = wg0 + 16 * wt.first;
+  const int64_t pend = (pbase + 16 * wt.count < wgend) ? pbase + 16 * wt.count : wgend;
+  if (pbase >= pend) return;   // waves never synchronise, so idle ones may leave
+  const int npw = (int)(pend - pbase);
+  const int64_t nb = (d.m + kBS - 1) / kBS;
+  uint8_t* cw = d.pcodes + ((int64_t)blockIdx.x * waves + wave) * nb * kBlockCodes;
+  double* sZ = lds + wave * (kWaveLds / (int)sizeof(double));
+  switch ((npw + 15) / 16) {
+    case 1: decode_wave<1, kUniS>(d, pbase, npw, cw, sZ); break;
+    case 2: decode_wave<2, kUniS>(d, pbase, npw, cw, sZ); break;
+    case 3: decode_wave<3, kUniS>(d, pbase, npw, cw, sZ); break;
+    default: decode_wave<4, kUniS>(d, pbase, npw, cw, sZ); break;
+  }
+}
+
+// First strict minimum over the K + 1 candidates of column j, then the gather
+// of the winner's codes (and, if asked, of every candidate).
 __global__ __launch_bounds__(256) void select_kernel(const uint8_t* __restrict__ pcodes,
                                                      const double* __restrict__ presid, int64_t n,
                                                      int64_t m, int K, int64_t wg_paths,
@@ -271,6 +335,7 @@ __global__ __launch_bounds__(256) void select_kernel(const uint8_t* __restrict__
   __shared__ int kstar;
   const int64_t j = blockIdx.x;
   const int64_t kp1 = (int64_t)K + 1;
+  const int64_t nb = (m + kBS - 1) / kBS;
   const int tid = threadIdx.x;
   if (tid == 0) {
     int best = 0;
@@ -287,50 +352,84 @@ __global__ __launch_bounds__(256) void select_kernel(const uint8_t* __restrict__
     if (winner) winner[j] = best;
   }
   __syncthreads();
+  // codes of path ps: the wave of its workgroup that holds its tile, row i
+  // in the lane's segment of block i / 32
+  const int waves = threads / 64, tiles = (int)(wg_paths / 16);
+  auto path_base = [&](int64_t ps) {
+    const int64_t wg = ps / wg_paths;
+    const int loc = (int)(ps % wg_paths);
+    const int w = decode_tile_wave(tiles, waves, loc / 16);
+    const int lane = loc - 16 * decode_wave_tiles(tiles, waves, w).first;
+    return pcodes + ((wg * waves + w) * nb * 64 + lane) * kSeg;
+  };
   {
-    const int64_t ps = j * kp1 + kstar;
-    const uint8_t* src = pcodes + (ps / wg_paths) * m * threads + (ps % wg_paths);
-    for (int64_t i = tid; i < m; i += 256) codes[j * m + i] = src[i * threads];
+    const uint8_t* src = path_base(j * kp1 + kstar);
+    for (int64_t i = tid; i < m; i += 256)
+      codes[j * m + i] = src[(i / kBS) * kBlockCodes + seg_byte((int)(i % kBS))];
   }
   if (path_resid)
     for (int64_t k = tid; k < kp1; k += 256) path_resid[j * kp1 + k] = presid[j * kp1 + k];
   if (path_codes) {
     for (int64_t k = 0; k < kp1; ++k) {
       const int64_t ps = j * kp1 + k;
-      const uint8_t* src = pcodes + (ps / wg_paths) * m * threads + (ps % wg_paths);
-      for (int64_t i = tid; i < m; i += 256) path_codes[ps * m + i] = src[i * threads];
+      const uint8_t* src = path_base(ps);
+      for (int64_t i = tid; i < m; i += 256)
+        path_codes[ps * m + i] = src[(i / kBS) * kBlockCodes + seg_byte((int)(i % kBS))];
     }
   }
 }
 
-// Lp[b][f][c] = L[f][32 b + c], zero past column m.
-__global__ __launch_bounds__(256) void panel_copy_kernel(const double* __restrict__ L, int64_t m,
-                                                         double* __restrict__ Lp) {
-  const int64_t total = decode_panel_elems(m);
-  for (int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x; e < total;
-       e += (int64_t)gridDim.x * 256) {
-    const int64_t b = e / (m * kDecodePanel);
-    const int64_t rem = e % (m * kDecodePanel);
-    const int64_t f = rem / kDecodePanel, c = b * kDecodePanel + rem % kDecodePanel;
-    Lp[e] = (c < m) ? L[f * m + c] : 0.0;
+// The decoder's copy of the factor (layout described with
+// decode_tile_count): blockIdx.y = row block b; x runs over the diagonal
+// tile of b followed by the off-diagonal tiles bb = b+1 .. nb-1.
+__global__ __launch_bounds__(256) void decode_tiles_kernel(const double* __restrict__ L, int64_t m,
+                                                           double* __restrict__ F) {
+  const int64_t nb = (m + kBS - 1) / kBS;
+  const int64_t b = blockIdx.y;
+  const int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  const int64_t tile = e / kDecodeTile;   // 0: diagonal, 1..: bb = b + tile
+  const int idx = (int)(e % kDecodeTile);
+  if (tile >= nb - b) return;
+  if (tile == 0) {
+    const int r = idx / kBS, c = idx % kBS;
+    const int64_t row = b * kBS + r;
+    F[b * kDecodeTile + idx] = (c <= r && row < m) ? L[row * m + b * kBS + c] : 0.0;
+  } else {
+    const int64_t bb = b + tile;
+    const int s = idx / 128, l = (idx / 2) % 64, a = idx % 2;
+    const int64_t row = b * kBS + 16 * a + (l & 15);       // row of R
+    const int64_t col = bb * kBS + 4 * s + (l >> 4);       // column of R
+    F[decode_offdiag_tile(nb, b, bb) * kDecodeTile + idx] = (col < m) ? L[col * m + row] : 0.0;
   }
 }
 
 }  // namespace
 
-hipError_t launch_panel_copy(const double* L, int64_t m, double* Lp, hipStream_t stream) {
-  const int64_t blocks = (decode_panel_elems(m) + 255) / 256;
-  panel_copy_kernel<<<dim3((unsigned)(blocks < 65536 ? blocks : 65536)), dim3(256), 0, stream>>>(
-      L, m, Lp);
+hipError_t launch_decode_tiles(const double* L, int64_t m, double* F, hipStream_t stream) {
+  const int64_t nb = (m + kBS - 1) / kBS;
+  if (nb > 65535) return hipErrorInvalidValue;
+  const int64_t bx = (nb * kDecodeTile + 255) / 256;
+  decode_tiles_kernel<<<dim3((unsigned)bx, (unsigned)nb), dim3(256), 0, stream>>>(L, m, F);
   return hipGetLastError();
 }
 
 hipError_t launch_decode(const DecodeDesc& d, hipStream_t stream) {
   const DecodeGeom geo = decode_geometry(d.n, d.K);
   if (geo.nwg <= 0) return hipSuccess;
-  if (geo.nwg > 0x7fffffff || d.threads != geo.threads || d.wg_paths != geo.wg_paths)
+  if (geo.nwg > 0x7fffffff || d.threads != geo.threads || d.wg_paths != geo.wg_paths ||
+      d.threads > kDecodeMaxThreads || d.threads % 64 != 0 || d.wg_paths % 16 != 0 ||
+      d.wg_paths > 4 * (int64_t)d.threads)
     return hipErrorInvalidValue;
-  decode_kernel<<<dim3((unsigned)geo.nwg), dim3(geo.threads), 0, stream>>>(d);
+  const size_t lds = (size_t)(d.threads / 64) * kWaveLds;
+  const bool uniform_scale = d.G == 1 || d.g % kBS == 0;
+  const void* fn = uniform_scale ? reinterpret_cast<const void*>(&decode_kernel<true>)
+                                 : reinterpret_cast<const void*>(&decode_kernel<false>);
+  hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+  if (e != hipSuccess) return e;
+  if (uniform_scale)
+    decode_kernel<true><<<dim3((unsigned)geo.nwg), dim3(geo.threads), lds, stream>>>(d);
+  else
+    decode_kernel<false><<<dim3((unsigned)geo.nwg), dim3(geo.threads), lds, stream>>>(d);
   return hipGetLastError();
 }
 

@@ -34,14 +34,14 @@ __device__ __forceinline__ Philox4 philox4x32_10(uint32_t c0, uint32_t c1, uint3
       k0 += kW0;
       k1 += kW1;
     }
-    const uint32_t lo0 = kM0 * c0, hi0 = __umulhi(kM0, c0);
-    const uint32_t lo1 = kM1 * c2, hi1 = __umulhi(kM1, c2);
-    const uint32_t n0 = hi1 ^ c1 ^ k0;
-    const uint32_t n2 = hi0 ^ c3 ^ k1;
+    // one v_mad_u64_u32 per 32 x 32 -> 64-bit product (both halves at once)
+    const uint64_t p0 = (uint64_t)kM0 * c0, p1 = (uint64_t)kM1 * c2;
+    const uint32_t n0 = (uint32_t)(p1 >> 32) ^ c1 ^ k0;
+    const uint32_t n2 = (uint32_t)(p0 >> 32) ^ c3 ^ k1;
     c0 = n0;
-    c1 = lo1;
+    c1 = (uint32_t)p1;
     c2 = n2;
-    c3 = lo0;
+    c3 = (uint32_t)p0;
   }
   return Philox4{c0, c1, c2, c3};
 }

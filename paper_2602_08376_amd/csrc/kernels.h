@@ -89,15 +89,22 @@ hipError_t launch_klein_alpha(const double* L, const float* S, int64_t n, int64_
                               int64_t G, double log_rho, double* alpha, hipStream_t stream);
 
 // ---- batched Babai / Klein decode and selection (Alg. 1, 3, 4) -------------
-// Each decode workgroup walks all m rows for its set of paths, so one
-// workgroup's latency is the kernel's floor: the paths are spread so that
-// every one of the device's CUs gets at most one workgroup per round.
+// Every wave of the decoder owns up to 64 consecutive paths (one per lane),
+// in whole 16-path MFMA tiles, and walks all m rows for them on its own.
+// Workgroups of up to kDecodeMaxThreads lanes are sized so that each of the
+// device's CUs gets at most one per round, and spread their tiles over as
+// many waves (up to eight) as evenly as possible: with two waves per SIMD one
+// wave's serial steps overlap the other's matrix products.  Waves never wait
+// for each other.
 constexpr int kDecodeCUs = 256;         // compute units of an MI355X
 constexpr int kDecodeMaxThreads = 512;  // paths (one per lane) per workgroup, at most
+constexpr int kDecodeMaxWaves = 8;      // waves per workgroup, at most
+constexpr int kDecodeBlock = 32;        // rows decided per serial block
+constexpr int kDecodeTile = kDecodeBlock * kDecodeBlock;
 
 struct DecodeGeom {
   int64_t wg_paths = 0;   // paths per workgroup (a multiple of 16)
-  int threads = 0;        // lanes per workgroup (wg_paths rounded up to 64, >= 256)
+  int threads = 0;        // 64 x waves per workgroup
   int64_t nwg = 0;        // workgroups
 };
 
@@ -113,22 +120,57 @@ inline DecodeGeom decode_geometry(int64_t n, int K) {
   if (per < 16) per = 16;
   DecodeGeom g;
   g.wg_paths = per;
-  g.threads = (int)((per + 63) / 64 * 64);
-  if (g.threads < 256) g.threads = 256;   // at least four waves (staging assumes it)
+  const int64_t tiles = per / 16;
+  g.threads = 64 * (int)(tiles < kDecodeMaxWaves ? tiles : kDecodeMaxWaves);
   g.nwg = (P + per - 1) / per;
   return g;
 }
 
-// Panel-major copy of the factor for the decoder: Lp[b][f][c] = L[f][32 b + c]
-// (zero beyond m), so the rows f of one 32-column panel are contiguous.
-constexpr int kDecodePanel = 32;
-__host__ __device__ inline int64_t decode_panel_elems(int64_t m) {
-  return ((m + kDecodePanel - 1) / kDecodePanel) * m * kDecodePanel;
+// Tiles of a workgroup's wave w: the first (tiles % waves) waves take one
+// more than the rest (waves w and w + 4 share a SIMD, so the extra tiles
+// land on different SIMDs first).
+struct WaveTiles {
+  int first = 0, count = 0;
+};
+__host__ __device__ inline WaveTiles decode_wave_tiles(int tiles, int waves, int w) {
+  const int base = tiles / waves, extra = tiles % waves;
+  WaveTiles t;
+  t.first = w * base + (w < extra ? w : extra);
+  t.count = base + (w < extra ? 1 : 0);
+  return t;
 }
-hipError_t launch_panel_copy(const double* L, int64_t m, double* Lp, hipStream_t stream);
+// The wave holding tile `tile` of its workgroup (inverse of the above).
+__host__ __device__ inline int decode_tile_wave(int tiles, int waves, int tile) {
+  const int base = tiles / waves, extra = tiles % waves;
+  const int split = extra * (base + 1);
+  return tile < split ? tile / (base + 1) : extra + (tile - split) / base;
+}
+
+// Bytes of candidate codes the decoder writes: per wave, one 32-byte segment
+// per (row block, lane) -- [wave][block][lane][32].
+inline int64_t decode_code_bytes(int64_t m, const DecodeGeom& g) {
+  const int64_t nb = (m + kDecodeBlock - 1) / kDecodeBlock;
+  return g.nwg * (int64_t)g.threads * nb * kDecodeBlock;
+}
+
+// The factor re-laid-out for the decoder, built from L = R^T (lower,
+// row-major [m, m]) in 32 x 32 tiles of nb = ceil(m / 32) row blocks:
+//   tiles 0 .. nb-1: the diagonal blocks, D_b[r][c] = L[32 b + r][32 b + c]
+//     for c <= r, zero above the diagonal and beyond m;
+//   then, for b = 0 .. nb-1 and bb = b+1 .. nb-1, the tile R[block b][block bb]
+//     in MFMA A-operand order: element (s * 64 + l) * 2 + a holds
+//     R[32 b + 16 a + l % 16][32 bb + 4 s + l / 16] (zero beyond m).
+__host__ __device__ inline int64_t decode_tile_count(int64_t m) {
+  const int64_t nb = (m + kDecodeBlock - 1) / kDecodeBlock;
+  return nb * (nb + 1) / 2;
+}
+__host__ __device__ inline int64_t decode_offdiag_tile(int64_t nb, int64_t b, int64_t bb) {
+  return nb + b * (nb - 1) - b * (b - 1) / 2 + (bb - b - 1);
+}
+hipError_t launch_decode_tiles(const double* L, int64_t m, double* F, hipStream_t stream);
 
 struct DecodeDesc {
-  const double* Lp = nullptr;  // panel-major factor (decode_panel_elems(m) doubles)
+  const double* F = nullptr;   // decode_tile_count(m) tiles of kDecodeTile doubles
   const double* gq = nullptr;  // [n, m]: gq_j = Rbar_j qbar_j
   const float* S = nullptr;    // [n, G]
   const double* alpha = nullptr;  // [n]
@@ -137,7 +179,7 @@ struct DecodeDesc {
   uint64_t seed = 0;
   int64_t wg_paths = 0;        // from decode_geometry
   int threads = 0;
-  uint8_t* pcodes = nullptr;   // [nwg, m, threads] candidate codes
+  uint8_t* pcodes = nullptr;   // decode_code_bytes(m, geometry) candidate codes
   double* presid = nullptr;    // [n (K + 1)] candidate residuals
 };
 
