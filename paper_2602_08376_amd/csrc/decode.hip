@@ -53,6 +53,9 @@ static_assert(kBS % kGR == 0 && kBS / kGR <= 8, "a lane packs one code byte per 
 // rounding of the running sums, so the draw is that of the full box.
 constexpr double kLogCut = 45.0;
 
+constexpr double kTwo52 = 4503599627370496.0;   // 2^52
+constexpr int kTwo52Hi = 0x43300000;            // high word of 2^52 + x, 0 <= x < 2^32
+
 __device__ __forceinline__ double nearest_box_point(double c, int qmax) {
   return fmin(fmax(rint(c), 0.0), (double)qmax);
 }
@@ -166,10 +169,16 @@ __device__ __forceinline__ void lazy_update(const DecodeDesc& d, int64_t nb, int
     const int64_t bn = bb - 1 > b ? bb - 1 : b + 1;
     load_b(nxt, d, bn, cw, so, lane);
     const double* An = d.F + decode_offdiag_tile(nb, b, bn) * kDecodeTile + 2 * lane;
-    double sc[NT];
+    // B = code * s, formed exactly as fma(2^52 + code, s, -2^52 s): the first
+    // factor is assembled from the code's bits, and code * s needs at most 32
+    // significant bits, so no rounding occurs anywhere.
+    double sc[NT], sb[NT];
     if constexpr (kUniS) {
 #pragma unroll
-      for (int t = 0; t < NT; ++t) sc[t] = (double)cur.sc[t][0];
+      for (int t = 0; t < NT; ++t) {
+        sc[t] = (double)cur.sc[t][0];
+        sb[t] = -kTwo52 * sc[t];
+      }
     }
 #pragma unroll
     for (int s = 0; s < 8; ++s) {
@@ -177,7 +186,8 @@ __device__ __forceinline__ void lazy_update(const DecodeDesc& d, int64_t nb, int
       for (int t = 0; t < NT; ++t) {
         const uint32_t code = (((s < 4) ? cur.q[t].x : cur.q[t].y) >> (8 * (s & 3))) & 0xffu;
         const double st = kUniS ? sc[t] : (double)cur.sc[t][kUniS ? 0 : s];
-        const double bv = (double)code * st;
+        const double bias = kUniS ? sb[t] : -kTwo52 * st;
+        const double bv = __builtin_fma(__hiloint2double(kTwo52Hi, (int)code), st, bias);
         acc[0][t] = mfma_f64(a[s].x, bv, acc[0][t]);
         acc[1][t] = mfma_f64(a[s].y, bv, acc[1][t]);
       }
