@@ -35,8 +35,9 @@ namespace ojbkq {
 namespace {
 
 constexpr int kBS = kDecodeBlock;                 // rows per serial block
-constexpr int kGR = 4;                            // rows per serial group
-constexpr int kWaveLds = kBS * 64 * (int)sizeof(double);   // LDS per wave: z of 32 rows x 64 paths
+constexpr int kGR = 4;                            // rows per serial group (one MFMA k-step)
+constexpr int kGBuf = kGR * 64;                   // group exchange buffer: 4 rows x 64 paths
+constexpr int kWaveLds = (kGBuf + kDecodeTile) * (int)sizeof(double);   // LDS bytes per wave
 constexpr int kSeg = kBS;                         // code bytes per (block, lane)
 constexpr int kBlockCodes = 64 * kSeg;            // code bytes per (wave, block)
 static_assert(kBS == 32, "the block is eight 4-row MFMA steps and one 32-byte code segment");
@@ -224,10 +225,23 @@ __device__ __forceinline__ void decode_wave(const DecodeDesc& d, int64_t pbase, 
     so[t] = colB[t] * (uint32_t)G;
   }
 
+  double* const sG = sZ;            // [4][64]: a group's z or e values by (row, path)
+  double* const sD = sZ + kGBuf;    // sD[r * 32 + c] = R[i0 + c][i0 + r], c <= r
+
   double resid = 0.0;
   for (int64_t b = nb - 1; b >= 0; --b) {
     const int64_t i0 = b * kBS;
     const int bl = (int)((m - i0) < kBS ? (m - i0) : kBS);
+
+    // ---- the block's diagonal tile to LDS (the previous block's reads
+    // ended at its last wave_sync) ----
+    {
+      const double* Dt = d.F + b * kDecodeTile + 2 * lane;
+#pragma unroll
+      for (int q = 0; q < kDecodeTile / 128; ++q)
+        *reinterpret_cast<double2*>(sD + q * 128 + 2 * lane) =
+            *reinterpret_cast<const double2*>(Dt + q * 128);
+    }
 
     // ---- lazy update from the decided blocks (MFMA) ----
     // The accumulator starts at -(Rbar_j qbar_j) of the block's rows and ends
@@ -245,33 +259,35 @@ __device__ __forceinline__ void decode_wave(const DecodeDesc& d, int64_t pbase, 
         }
     }
     if (b + 1 < nb) lazy_update<NT, kUniS>(d, nb, b, cw, so, acc, lane);
-
-    // ---- transpose through LDS: sZ[r * 64 + l] = -z of row r, path l ----
-    wave_sync();   // the previous block's reads of the buffer are done
-#pragma unroll
-    for (int a = 0; a < 2; ++a)
-#pragma unroll
-      for (int t = 0; t < NT; ++t)
-#pragma unroll
-        for (int r = 0; r < 4; ++r)
-          sZ[(16 * a + (lane >> 4) + 4 * r) * 64 + 16 * t + (lane & 15)] = acc[a][t][r];
-    wave_sync();
+    wave_sync();   // the diagonal tile is in LDS
 
     // ---- serial steps, one path per lane, in groups of four rows from the
-    // top: the group's rows update each other in registers, then the group
-    // updates the rows below it in LDS with one rank-4 step ----
-    const double* const Db = d.F + b * kDecodeTile;   // Db[r * 32 + c] = R[i0 + c][i0 + r]
+    // top.  A group's rows sit in one slot (a, r) of the accumulator (rows
+    // 16 a + 4 r + l / 16); they reach their lanes through LDS, update each
+    // other in registers, and update the rows below with one MFMA step
+    // (K = 4) on the accumulator: R[., group] E[group] ----
     uint64_t wcode[kGR] = {0, 0, 0, 0};   // byte g of wcode[k]: code of row kGR g + k
     double s_blk = 0.0;
     if constexpr (kUniS) s_blk = (double)Sj[G == 1 ? 0u : (uint32_t)i0 / (uint32_t)g];
     for (int g4 = (bl - 1) / kGR; g4 >= 0; --g4) {
       const int r0 = kGR * g4;
+      double* const gslot = sG + (lane >> 4) * 64 + (lane & 15);
+      switch (g4) {
+#define OJBKQ_PUT_GROUP(G4)                                               \
+  case G4:                                                                \
+    _Pragma("unroll") for (int t = 0; t < NT; ++t) gslot[16 * t] = acc[(G4) / 4][t][(G4) % 4]; \
+    break;
+        OJBKQ_PUT_GROUP(0) OJBKQ_PUT_GROUP(1) OJBKQ_PUT_GROUP(2) OJBKQ_PUT_GROUP(3)
+        OJBKQ_PUT_GROUP(4) OJBKQ_PUT_GROUP(5) OJBKQ_PUT_GROUP(6) OJBKQ_PUT_GROUP(7)
+#undef OJBKQ_PUT_GROUP
+      }
+      wave_sync();
       double z[kGR], u[kGR], sr[kGR], rb[kGR];
 #pragma unroll
       for (int k = 0; k < kGR; ++k) {
-        z[k] = -sZ[(r0 + k) * 64 + lane];
+        z[k] = -sG[k * 64 + lane];
         sr[k] = kUniS ? s_blk : (double)Sj[(uint32_t)(i0 + r0 + k < m ? i0 + r0 + k : m - 1) / (uint32_t)g];
-        rb[k] = Db[(r0 + k) * (kBS + 1)] * sr[k];   // Rbar_ii
+        rb[k] = sD[(r0 + k) * (kBS + 1)] * sr[k];   // Rbar_ii
         u[k] = (kk != 0) ? klein_uniform(d.seed, (uint32_t)(i0 + r0 + k), (uint32_t)j, kk) : 0.0;
       }
       double e[kGR];
@@ -288,22 +304,32 @@ __device__ __forceinline__ void decode_wave(const DecodeDesc& d, int64_t pbase, 
           wcode[k] |= (uint64_t)q << (8 * g4);
         }
 #pragma unroll
-        for (int k2 = 0; k2 < k; ++k2) z[k2] -= Db[(r0 + k) * kBS + r0 + k2] * e[k];
+        for (int k2 = 0; k2 < k; ++k2) z[k2] -= sD[(r0 + k) * kBS + r0 + k2] * e[k];
       }
-      // rank-4 update of the rows below the group (the buffer holds -z)
-      for (int r2 = r0 - 1; r2 >= 0; --r2) {
-        double v = sZ[r2 * 64 + lane];
+      if (g4 == 0) break;   // no rows below
+      // rows below: acc += R[rows][group] E[group] (the accumulator holds -z);
+      // rows at or above the group meet zeros of the diagonal tile
+      wave_sync();   // the group's z reads are done
 #pragma unroll
-        for (int k = 0; k < kGR; ++k) v += Db[(r0 + k) * kBS + r2] * e[k];
-        sZ[r2 * 64 + lane] = v;
+      for (int k = 0; k < kGR; ++k) sG[k * 64 + lane] = e[k];
+      wave_sync();
+      double bq[NT];
+#pragma unroll
+      for (int t = 0; t < NT; ++t) bq[t] = gslot[16 * t];   // E[r0 + l / 16][path 16 t + l % 16]
+#pragma unroll
+      for (int a = 0; a < 2; ++a) {
+        const double aq = sD[(r0 + (lane >> 4)) * kBS + 16 * a + (lane & 15)];   // R[16 a + l % 16][r0 + l / 16]
+#pragma unroll
+        for (int t = 0; t < NT; ++t) acc[a][t] = mfma_f64(aq, bq[t], acc[a][t]);
       }
+      wave_sync();   // the e reads are done before the next group's writes
     }
     uint8_t* seg = cw + b * kBlockCodes + lane * kSeg;
     *reinterpret_cast<uint4*>(seg) = make_uint4((uint32_t)wcode[0], (uint32_t)(wcode[0] >> 32),
                                                 (uint32_t)wcode[1], (uint32_t)(wcode[1] >> 32));
     *reinterpret_cast<uint4*>(seg + 16) = make_uint4((uint32_t)wcode[2], (uint32_t)(wcode[2] >> 32),
                                                      (uint32_t)wcode[3], (uint32_t)(wcode[3] >> 32));
-    wave_sync();   // codes visible to the later update loads
+    wave_sync();   // codes visible to the later update loads; LDS reads done
   }
   if (valid) d.presid[p] = resid;
 }
