@@ -61,7 +61,7 @@ Shape shape_of(const ojbkq_params& p) {
 // Offsets of every buffer carved from the workspace.
 struct Layout {
   size_t status = 0, lam2 = 0, G = 0, E = 0, U = 0, qbar = 0, gq = 0, alpha = 0, pcodes = 0,
-         presid = 0, gc_scratch = 0, gc_tiles = 0, F = 0, total = 0;
+         presid = 0, gc_scratch = 0, gc_tiles = 0, F = 0, Linv = 0, total = 0;
 };
 
 Layout layout_full(const Shape& s) {
@@ -87,6 +87,7 @@ Layout layout_full(const Shape& s) {
   L.gc_scratch = take(ojbkq::gram_cross_scratch_bytes());
   L.gc_tiles = take((size_t)ojbkq::gram_tile_count(s.m) * sizeof(uint32_t));
   L.F = take((size_t)ojbkq::decode_tile_count(s.m) * ojbkq::kDecodeTile * sizeof(double));
+  L.Linv = take(mm);
   L.total = off;
   return L;
 }
@@ -313,6 +314,10 @@ int ctx_solve(ojbkq_ctx* c, const float* W, double alpha, uint8_t* codes, float*
       OJBKQ_HIP(ojbkq::cross_from_mixed(c->at<double>(c->L.E), Lf, s.m, st), "cross term");
     OJBKQ_HIP(ojbkq::launch_damp(Lf, s.m, c->p.lambda_rel, c->at<double>(c->L.lam2), st), "damp");
     OJBKQ_HIP(ojbkq::cholesky_lower(Lf, s.m, c->at<int>(c->L.status), st), "cholesky");
+    // L^-1 for the solves; the decoder tiles' buffer is free scratch until
+    // they are written
+    OJBKQ_HIP(ojbkq::invert_lower(Lf, s.m, c->at<double>(c->L.Linv), c->at<double>(c->L.F), st),
+              "factor inverse");
     OJBKQ_HIP(ojbkq::launch_decode_tiles(Lf, s.m, c->at<double>(c->L.F), st), "decoder tiles");
     c->factored = true;
     stage_end(c, OJBKQ_STAGE_FACTOR, t0);
@@ -329,7 +334,9 @@ int ctx_solve(ojbkq_ctx* c, const float* W, double alpha, uint8_t* codes, float*
     g.B = c->at<double>(c->L.E); g.ldb = s.m; g.tb = ojbkq::Elt::F64;
     g.C = U; g.ldc = s.m;
     OJBKQ_HIP(ojbkq::gemm_f64(g, st), "target projection");
-    OJBKQ_HIP(ojbkq::solve_llt(Lf, U, s.n, s.m, st), "solves");
+    OJBKQ_HIP(ojbkq::solve_llt(c->at<double>(c->L.Linv), U, c->at<double>(c->L.gq), s.n, s.m,
+                               st),
+              "solves");
   }
   stage_end(c, OJBKQ_STAGE_SOLVE, t0);
   t0 = stage_begin(c);

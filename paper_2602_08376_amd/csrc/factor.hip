@@ -4,8 +4,10 @@
 // The factor is kept as L = R^T, lower triangular, row-major: row f of L is
 // column f of R, so the decoder's reads of R[i][f] over a block of rows i are
 // contiguous.  Right-looking blocked algorithms with 64-wide panels: the
-// panel work (a 64x64 diagonal block in LDS, a row-parallel triangular solve)
-// is small; every trailing update is a call of the fp64 MFMA GEMM.
+// Cholesky's panel work (a 64x64 diagonal block in one wave, a row-parallel
+// triangular solve) is small and every trailing update is a call of the fp64
+// MFMA GEMM.  The solves use L^-1, formed once per factor by doubling from
+// inverted 64x64 diagonal blocks, so each is one triangular GEMM.
 #include "kernels.h"
 #include "device.h"
 
@@ -121,64 +123,40 @@ __global__ __launch_bounds__(256) void upper_to_lower_kernel(const double* R, do
   }
 }
 
-// Forward block solve of L_KK y = u for every right-hand side (row of U).
-__global__ __launch_bounds__(256) void trsv_fwd_kernel(const double* L, double* U, int64_t n,
-                                                       int64_t m, int64_t k0, int nbk) {
+// Inverses of the 64x64 diagonal blocks of L (one workgroup per block),
+// written to the same positions of the m x m matrix Linv: lane c forms
+// column c of L_KK^-1 by forward substitution on e_c, with the block
+// broadcast from LDS.
+__global__ __launch_bounds__(64) void trtri_blocks_kernel(const double* __restrict__ L, int64_t m,
+                                                          double* __restrict__ Linv) {
   __shared__ double Lk[kNB][kNB + 1];
-  const int tid = threadIdx.x;
-  for (int e = tid; e < kNB * kNB; e += 256) {
-    const int r = e / kNB, c = e % kNB;
-    Lk[r][c] = (r < nbk && c < nbk && c <= r) ? L[(k0 + r) * m + k0 + c] : 0.0;
+  const int c = threadIdx.x;
+  const int64_t k0 = (int64_t)blockIdx.x * kNB;
+  const int nbk = (int)((m - k0) < kNB ? (m - k0) : kNB);
+  for (int e = c; e < kNB * kNB; e += kNB) {
+    const int r = e / kNB, cc = e % kNB;
+    Lk[r][cc] = (r < nbk && cc <= r) ? L[(k0 + r) * m + k0 + cc] : (r == cc ? 1.0 : 0.0);
   }
   __syncthreads();
-  const int64_t j = (int64_t)blockIdx.x * 256 + tid;
-  if (j >= n) return;
-  double* row = U + j * m + k0;
   double x[kNB];
 #pragma unroll
-  for (int c = 0; c < kNB; ++c) x[c] = (c < nbk) ? row[c] : 0.0;
+  for (int r = 0; r < kNB; ++r) {
+    double p[4] = {0.0, 0.0, 0.0, 0.0};   // four partial sums break the FMA chain
 #pragma unroll
-  for (int c = 0; c < kNB; ++c) {
-    if (c < nbk) {
-      double p[4] = {0.0, 0.0, 0.0, 0.0};   // four partial sums break the FMA chain
-#pragma unroll
-      for (int c2 = 0; c2 < c; ++c2) p[c2 & 3] += Lk[c][c2] * x[c2];
-      x[c] = (x[c] - ((p[0] + p[1]) + (p[2] + p[3]))) / Lk[c][c];
-    }
+    for (int k = 0; k < r; ++k) p[k & 3] += Lk[r][k] * x[k];
+    const double v = ((r == c) ? 1.0 : 0.0) - ((p[0] + p[1]) + (p[2] + p[3]));
+    x[r] = (r >= c) ? v / Lk[r][r] : 0.0;
   }
+  double* out = Linv + k0 * m + k0;
 #pragma unroll
-  for (int c = 0; c < kNB; ++c)
-    if (c < nbk) row[c] = x[c];
+  for (int r = 0; r < kNB; ++r)
+    if (r < nbk && c < nbk) out[r * m + c] = x[r];
 }
 
-// Backward block solve of L_KK^T x = y for every right-hand side.
-__global__ __launch_bounds__(256) void trsv_bwd_kernel(const double* L, double* U, int64_t n,
-                                                       int64_t m, int64_t k0, int nbk) {
-  __shared__ double Lk[kNB][kNB + 1];
-  const int tid = threadIdx.x;
-  for (int e = tid; e < kNB * kNB; e += 256) {
-    const int r = e / kNB, c = e % kNB;
-    Lk[r][c] = (r < nbk && c < nbk && c <= r) ? L[(k0 + r) * m + k0 + c] : 0.0;
-  }
-  __syncthreads();
-  const int64_t j = (int64_t)blockIdx.x * 256 + tid;
-  if (j >= n) return;
-  double* row = U + j * m + k0;
-  double x[kNB];
-#pragma unroll
-  for (int c = 0; c < kNB; ++c) x[c] = (c < nbk) ? row[c] : 0.0;
-#pragma unroll
-  for (int c = kNB - 1; c >= 0; --c) {
-    if (c < nbk) {
-      double p[4] = {0.0, 0.0, 0.0, 0.0};   // four partial sums; zero beyond nbk
-#pragma unroll
-      for (int c2 = c + 1; c2 < kNB; ++c2) p[c2 & 3] += Lk[c2][c] * x[c2];
-      x[c] = (x[c] - ((p[0] + p[1]) + (p[2] + p[3]))) / Lk[c][c];
-    }
-  }
-#pragma unroll
-  for (int c = 0; c < kNB; ++c)
-    if (c < nbk) row[c] = x[c];
+__global__ __launch_bounds__(256) void fill_zero_kernel(double* __restrict__ p, int64_t count) {
+  for (int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x; e < count;
+       e += (int64_t)gridDim.x * 256)
+    p[e] = 0.0;
 }
 
 unsigned blocks_for(int64_t count, int per) { return (unsigned)((count + per - 1) / per); }
@@ -221,36 +199,69 @@ hipError_t launch_upper_to_lower(const double* R, double* L, int64_t m, hipStrea
   return hipGetLastError();
 }
 
-hipError_t solve_llt(const double* L, double* U, int64_t n, int64_t m, hipStream_t stream) {
-  hipError_t e;
-  for (int64_t k0 = 0; k0 < m; k0 += kNB) {
-    const int nbk = (int)((m - k0) < kNB ? (m - k0) : kNB);
-    trsv_fwd_kernel<<<blocks_for(n, 256), 256, 0, stream>>>(L, U, n, m, k0, nbk);
-    if ((e = hipGetLastError()) != hipSuccess) return e;
-    const int64_t rest = m - k0 - nbk;
-    if (rest <= 0) continue;
-    GemmDesc g;   // U[:, k1:] -= Y[:, K] L[k1:, K]^T
-    g.M = n; g.N = rest; g.Kd = nbk;
-    g.A = U + k0; g.lda = m; g.ta = Elt::F64;
-    g.B = L + (k0 + nbk) * m + k0; g.ldb = m; g.tb = Elt::F64;
-    g.C = U + k0 + nbk; g.ldc = m; g.alpha = -1.0; g.beta = 1.0;
-    if ((e = gemm_f64(g, stream)) != hipSuccess) return e;
-  }
-  const int64_t nblk = (m + kNB - 1) / kNB;
-  for (int64_t b = nblk - 1; b >= 0; --b) {
-    const int64_t k0 = b * kNB;
-    const int nbk = (int)((m - k0) < kNB ? (m - k0) : kNB);
-    trsv_bwd_kernel<<<blocks_for(n, 256), 256, 0, stream>>>(L, U, n, m, k0, nbk);
-    if ((e = hipGetLastError()) != hipSuccess) return e;
-    if (k0 == 0) continue;
-    GemmDesc g;   // U[:, :k0] -= X[:, K] L[K, :k0]
-    g.M = n; g.N = k0; g.Kd = nbk;
-    g.A = U + k0; g.lda = m; g.ta = Elt::F64;
-    g.B = L + k0 * m; g.ldb = m; g.tb = Elt::F64; g.b_kmajor = true;
-    g.C = U; g.ldc = m; g.alpha = -1.0; g.beta = 1.0;
-    if ((e = gemm_f64(g, stream)) != hipSuccess) return e;
+// L^-1 by doubling: the 64x64 diagonal blocks are inverted directly, then
+// pairs of inverted blocks of size s merge into blocks of size 2 s with
+//   [A 0; C D]^-1 = [A^-1 0; -D^-1 C A^-1  D^-1],
+// one batched GEMM for T = C A^-1 and one for -D^-1 T per level (plus one
+// pair of calls for a ragged last pair).  scratch holds m^2 / 4 doubles.
+hipError_t invert_lower(const double* L, int64_t m, double* Linv, double* scratch,
+                        hipStream_t stream) {
+  const int64_t count = m * m;
+  const int64_t zb = (count + 255) / 256;
+  fill_zero_kernel<<<dim3((unsigned)(zb < 65536 ? zb : 65536)), dim3(256), 0, stream>>>(Linv, count);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  trtri_blocks_kernel<<<dim3((unsigned)((m + kNB - 1) / kNB)), dim3(kNB), 0, stream>>>(L, m, Linv);
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  for (int64_t s = kNB; s < m; s *= 2) {
+    const int64_t pitch = 2 * s * m + 2 * s;   // from one pair to the next
+    auto merge = [&](int64_t p0, int64_t pairs, int64_t dsize) -> hipError_t {
+      const int64_t a0 = 2 * s * p0;           // first row / column of the pair
+      GemmDesc t;   // T = C A^-1 (A^-1 lower: its k-major rows start at the column)
+      t.M = dsize; t.N = s; t.Kd = s;
+      t.A = L + (a0 + s) * m + a0; t.lda = m; t.ta = Elt::F64;
+      t.B = Linv + a0 * m + a0; t.ldb = m; t.tb = Elt::F64; t.b_kmajor = true;
+      t.b_zero_below_col = true;
+      t.C = scratch; t.ldc = s; t.alpha = 1.0; t.beta = 0.0;
+      t.batch = pairs; t.stride_a = pitch; t.stride_b = pitch; t.stride_c = s * s;
+      hipError_t e2 = gemm_f64(t, stream);
+      if (e2 != hipSuccess) return e2;
+      GemmDesc x;   // X_21 = -D^-1 T
+      x.M = dsize; x.N = s; x.Kd = dsize;
+      x.A = Linv + (a0 + s) * m + (a0 + s); x.lda = m; x.ta = Elt::F64;
+      x.B = scratch; x.ldb = s; x.tb = Elt::F64; x.b_kmajor = true;
+      x.C = Linv + (a0 + s) * m + a0; x.ldc = m; x.alpha = -1.0; x.beta = 0.0;
+      x.batch = pairs; x.stride_a = pitch; x.stride_b = s * s; x.stride_c = pitch;
+      return gemm_f64(x, stream);
+    };
+    const int64_t full = m / (2 * s);
+    for (int64_t p0 = 0; p0 < full; p0 += 65535) {
+      const int64_t pairs = (full - p0) < 65535 ? (full - p0) : 65535;
+      if ((e = merge(p0, pairs, s)) != hipSuccess) return e;
+    }
+    const int64_t a0 = 2 * s * full;
+    if (a0 + s < m && (e = merge(full, 1, m - a0 - s)) != hipSuccess) return e;
   }
   return hipSuccess;
+}
+
+// The two solves as two triangular GEMMs with L^-1 (row form, every row of
+// U a right-hand side): Y = U L^-T into T, then X = Y L^-1 into U.
+hipError_t solve_llt(const double* Linv, double* U, double* T, int64_t n, int64_t m,
+                     hipStream_t stream) {
+  GemmDesc y;   // Y[i][c] = sum_k U[i][k] Linv[c][k], Linv[c][k] = 0 for k > c
+  y.M = n; y.N = m; y.Kd = m;
+  y.A = U; y.lda = m; y.ta = Elt::F64;
+  y.B = Linv; y.ldb = m; y.tb = Elt::F64; y.b_zero_above_col = true;
+  y.C = T; y.ldc = m; y.alpha = 1.0; y.beta = 0.0;
+  hipError_t e = gemm_f64(y, stream);
+  if (e != hipSuccess) return e;
+  GemmDesc x;   // X[i][c] = sum_k Y[i][k] Linv[k][c], Linv[k][c] = 0 for k < c
+  x.M = n; x.N = m; x.Kd = m;
+  x.A = T; x.lda = m; x.ta = Elt::F64;
+  x.B = Linv; x.ldb = m; x.tb = Elt::F64; x.b_kmajor = true; x.b_zero_below_col = true;
+  x.C = U; x.ldc = m; x.alpha = 1.0; x.beta = 0.0;
+  return gemm_f64(x, stream);
 }
 
 }  // namespace ojbkq

@@ -38,6 +38,9 @@ struct GemmArgs {
   int lower;
   int vec_a, vec_b;
   int b_tri;
+  int b_tri_up;
+  int64_t sa, sb, sc;   // element strides between batch entries (blockIdx.y)
+  int64_t batch;
 };
 
 // Eight consecutive elements starting at p, the first `valid` of them real
@@ -162,13 +165,14 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& g, int64_t ti, int64_t
   };
 
   const int64_t kbeg = g.b_tri ? (J0 < g.Kd ? J0 : g.Kd) : 0;   // J0 is a multiple of kKC
-  if (kbeg < g.Kd) fetch(kbeg);
-  for (int64_t k0 = kbeg; k0 < g.Kd; k0 += kKC) {
+  const int64_t kend = g.b_tri_up ? (J0 + kTile < g.Kd ? J0 + kTile : g.Kd) : g.Kd;
+  if (kbeg < kend) fetch(kbeg);
+  for (int64_t k0 = kbeg; k0 < kend; k0 += kKC) {
     __syncthreads();
     store_chunk<AK>(sA, tid, ra);
     store_chunk<BK>(sB, tid, rb);
     __syncthreads();
-    if (k0 + kKC < g.Kd) fetch(k0 + kKC);
+    if (k0 + kKC < kend) fetch(k0 + kKC);
 #pragma unroll
     for (int kk = 0; kk < kKC / 4; ++kk) {
       const int kr = kk * 4 + (lane >> 4);
@@ -204,6 +208,11 @@ template <typename TA, typename TB, bool AK, bool BK, bool BDIFF>
 __global__ __launch_bounds__(256, 2) void gemm_f64_kernel(GemmArgs g) {
   __shared__ double sA[kKC][kLdsLd];
   __shared__ double sB[kKC][kLdsLd];
+  if (blockIdx.y) {   // batch entry
+    g.A = static_cast<const TA*>(g.A) + blockIdx.y * g.sa;
+    g.B = static_cast<const TB*>(g.B) + blockIdx.y * g.sb;
+    g.C += blockIdx.y * g.sc;
+  }
   const int64_t t = xcd_tile_number();
   int64_t ti, tj;
   if (g.lower)
@@ -215,7 +224,8 @@ __global__ __launch_bounds__(256, 2) void gemm_f64_kernel(GemmArgs g) {
 
 template <typename TA, typename TB, bool AK, bool BK, bool BDIFF>
 hipError_t launch(const GemmArgs& g, int64_t ntiles, hipStream_t s) {
-  gemm_f64_kernel<TA, TB, AK, BK, BDIFF><<<dim3((unsigned)ntiles), dim3(256), 0, s>>>(g);
+  gemm_f64_kernel<TA, TB, AK, BK, BDIFF><<<dim3((unsigned)ntiles, (unsigned)g.batch), dim3(256), 0,
+                                           s>>>(g);
   return hipGetLastError();
 }
 
@@ -236,6 +246,10 @@ hipError_t gemm_f64(const GemmDesc& d, hipStream_t stream) {
   g.tiles_n = (d.N + kTile - 1) / kTile;
   g.lower = d.lower_tiles ? 1 : 0;
   g.b_tri = d.b_zero_below_col ? 1 : 0;
+  g.b_tri_up = d.b_zero_above_col ? 1 : 0;
+  g.sa = d.stride_a; g.sb = d.stride_b; g.sc = d.stride_c;
+  g.batch = d.batch;
+  if (d.batch < 1 || d.batch > 65535 || (d.batch > 1 && d.B2 != nullptr)) return hipErrorInvalidValue;
   g.vec_a = vec_ok(d.A, d.lda, d.ta) ? 1 : 0;
   g.vec_b = (vec_ok(d.B, d.ldb, d.tb) && (d.B2 == nullptr || vec_ok(d.B2, d.ldb, d.tb))) ? 1 : 0;
   if (d.lower_tiles && g.tiles_m != g.tiles_n) return hipErrorInvalidValue;

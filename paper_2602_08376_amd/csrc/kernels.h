@@ -35,6 +35,12 @@ struct GemmDesc {
   // opB(j, k) == 0 whenever k < j (B is the lower factor read k-major): the
   // k loop of an output tile starts at its first column.
   bool b_zero_below_col = false;
+  // opB(j, k) == 0 whenever k > j (B is a lower triangle read row-major): the
+  // k loop of an output tile ends after its last column.
+  bool b_zero_above_col = false;
+  // Batched form: `batch` independent products, entry b at A + b stride_a,
+  // B + b stride_b, C + b stride_c (in elements).
+  int64_t batch = 1, stride_a = 0, stride_b = 0, stride_c = 0;
 };
 
 hipError_t gemm_f64(const GemmDesc& d, hipStream_t stream);
@@ -75,9 +81,14 @@ hipError_t launch_damp(double* H, int64_t m, double lambda_rel, double* lam2_out
 hipError_t cholesky_lower(double* H, int64_t m, int* status, hipStream_t stream);
 // L = R^T for an upper-triangular R (row-major); strict upper part of L = 0.
 hipError_t launch_upper_to_lower(const double* R, double* L, int64_t m, hipStream_t stream);
-// In-place solves for n right-hand sides stored as rows of U [n, m]:
-// forward L y = u, then backward L^T x = y (x = H^-1 u).
-hipError_t solve_llt(const double* L, double* U, int64_t n, int64_t m, hipStream_t stream);
+// Linv = L^-1 [m, m] (lower, strict upper part zero) for the lower factor L;
+// scratch holds at least m^2 / 4 doubles.
+hipError_t invert_lower(const double* L, int64_t m, double* Linv, double* scratch,
+                        hipStream_t stream);
+// Solves for n right-hand sides stored as rows of U [n, m] with Linv = L^-1:
+// y = L^-1 u, then x = L^-T y = H^-1 u, written to U; T [n, m] is scratch.
+hipError_t solve_llt(const double* Linv, double* U, double* T, int64_t n, int64_t m,
+                     hipStream_t stream);
 
 // ---- relaxed solution -> centres (Alg. 1 steps 3-5) ------------------------
 // qbar = (w + c * delta) / s + z (delta may be null), Y = s * qbar.
