@@ -313,7 +313,8 @@ int ctx_solve(ojbkq_ctx* c, const float* W, double alpha, uint8_t* codes, float*
     if (c->cross_seen)   // mixed product -> cross term, while G is still the Gram
       OJBKQ_HIP(ojbkq::cross_from_mixed(c->at<double>(c->L.E), Lf, s.m, st), "cross term");
     OJBKQ_HIP(ojbkq::launch_damp(Lf, s.m, c->p.lambda_rel, c->at<double>(c->L.lam2), st), "damp");
-    OJBKQ_HIP(ojbkq::cholesky_lower(Lf, s.m, c->at<int>(c->L.status), st), "cholesky");
+    OJBKQ_HIP(ojbkq::cholesky_lower(Lf, s.m, c->at<int>(c->L.status), c->at<double>(c->L.Linv), st),
+              "cholesky");
     // L^-1 for the solves; the decoder tiles' buffer is free scratch until
     // they are written
     OJBKQ_HIP(ojbkq::invert_lower(Lf, s.m, c->at<double>(c->L.Linv), c->at<double>(c->L.F), st),

@@ -3,11 +3,11 @@
 //
 // The factor is kept as L = R^T, lower triangular, row-major: row f of L is
 // column f of R, so the decoder's reads of R[i][f] over a block of rows i are
-// contiguous.  Right-looking blocked algorithms with 64-wide panels: the
-// Cholesky's panel work (a 64x64 diagonal block in one wave, a row-parallel
-// triangular solve) is small and every trailing update is a call of the fp64
+// contiguous.  Right-looking blocked Cholesky with 64-wide panels: one wave
+// factors and inverts each 64x64 diagonal block, the panel below it is one
+// GEMM with that inverse, and every trailing update is a call of the fp64
 // MFMA GEMM.  The solves use L^-1, formed once per factor by doubling from
-// inverted 64x64 diagonal blocks, so each is one triangular GEMM.
+// the inverted diagonal blocks, so each is one triangular GEMM.
 #include "kernels.h"
 #include "device.h"
 
@@ -33,6 +33,26 @@ __global__ __launch_bounds__(256) void damp_kernel(double* H, int64_t m, double 
   for (int64_t i = tid; i < m; i += 256) H[i * m + i] += lam2;
 }
 
+// All lanes of the wave have finished their LDS accesses before any lane
+// goes on (one wave: lockstep; this orders the memory operations).
+__device__ __forceinline__ void wave_sync() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
+}
+
+// 1 / sqrt(d): hardware estimate, then two Newton steps y += y (1 - d y^2) / 2
+// (the estimate's error of about 2^-22 relative squares away each step).
+__device__ __forceinline__ double rsqrt_f64(double d) {
+  double y = __builtin_amdgcn_rsq(d);
+#pragma unroll
+  for (int it = 0; it < 2; ++it) {
+    const double e = fma(-d * y, y, 1.0);
+    y = fma(0.5 * y, e, y);
+  }
+  return y;
+}
+
 __device__ __forceinline__ double lane_value(double v, int lane) {
   const int lo = __builtin_amdgcn_readlane(__double2loint(v), lane);
   const int hi = __builtin_amdgcn_readlane(__double2hiint(v), lane);
@@ -40,63 +60,104 @@ __device__ __forceinline__ double lane_value(double v, int lane) {
 }
 
 // Unblocked Cholesky of the nbk x nbk diagonal block starting at (k0, k0),
-// by one wave: lane r keeps row r in registers and column c is broadcast
-// lane by lane, so the 64 dependent column steps touch no memory.
-__global__ __launch_bounds__(64) void potrf_diag_kernel(double* H, int64_t m, int64_t k0, int nbk,
-                                                        int* status) {
-  const int r = threadIdx.x;   // row of the block held by this lane
-  double a[kNB];
+// by one wave, followed by the inverse of the factored block, written to
+// Linv at (k0, k0).  The block lives in LDS column-major (padded to 64 x 64
+// with the identity) and both phases walk it in chunks of eight columns, so
+// the code is a few short loops that stay in the instruction cache.
+//  - Factor: lane r owns row r.  A chunk's eight entries of the row sit in
+//    registers; within the chunk each new column reaches the other lanes by
+//    readlane, then the chunk is stored and the rows below take its rank-8
+//    update, eight columns per pass, from broadcast LDS reads.
+//  - Inverse: lane c forms column c of L_KK^-1 by forward substitution, eight
+//    rows at a time; earlier rows of the column come back from LDS.
+// Loads and LDS reads are unconditional (addresses clamped into the block),
+// so they issue back to back instead of waiting one by one.
+__global__ __launch_bounds__(64) void potrf_trtri_kernel(double* H, int64_t m, int64_t k0, int nbk,
+                                                         int* status, double* Linv) {
+  constexpr int kP = kNB + 2;   // column pitch of the block in LDS (doubles; 16-byte rows)
+  constexpr int kCh = 8;        // columns per chunk
+  __shared__ __align__(16) double Lt[kNB * kP];   // Lt[c * kP + r] = L[r][c]
+  __shared__ double X[kNB * kNB];                 // X[r * kNB + c] = (L_KK^-1)[r][c]
+  __shared__ double rdiag[kNB];                   // 1 / L[i][i]
+  const int r = threadIdx.x;
+  double* blk = H + k0 * m + k0;
+  {
+    const int rc = r < nbk ? r : nbk - 1;
+    double v[kNB];   // all row loads in flight at once
 #pragma unroll
-  for (int c = 0; c < kNB; ++c) a[c] = (r < nbk && c <= r) ? H[(k0 + r) * m + k0 + c] : 0.0;
+    for (int i = 0; i < kNB; ++i) {
+      const int ic = i < nbk ? i : nbk - 1;
+      v[i] = blk[ic * m + (rc < ic ? rc : ic)];
+    }
 #pragma unroll
-  for (int c = 0; c < kNB; ++c) {
-    if (c < nbk) {
-      const double d = lane_value(a[c], c);   // pivot: row c, column c
-      if (r == 0 && !(d > 0.0)) atomicMin(status, (int)(k0 + c));
-      const double piv = sqrt(d);
-      const double lrc = (r > c) ? a[c] / piv : 0.0;   // L[r][c]
-      if (r == c) a[c] = piv;
-      if (r > c) a[c] = lrc;
+    for (int i = 0; i < kNB; ++i) Lt[r * kP + i] = (i < nbk && r <= i) ? v[i] : (r == i ? 1.0 : 0.0);
+  }
+  wave_sync();
+  for (int j = 0; j < kNB; j += kCh) {
+    double cur[kCh];
 #pragma unroll
-      for (int c2 = c + 1; c2 < kNB; ++c2) {
-        const double l2 = lane_value(lrc, c2);   // L[c2][c]
-        if (c2 <= r) a[c2] -= lrc * l2;
+    for (int c = 0; c < kCh; ++c) cur[c] = Lt[(j + c) * kP + r];
+#pragma unroll
+    for (int c = 0; c < kCh; ++c) {
+      const int cc = j + c;
+      const double d = lane_value(cur[c], cc);   // pivot: row cc, column cc
+      if (r == 0 && cc < nbk && !(d > 0.0)) atomicMin(status, (int)(k0 + cc));
+      const double rs = rsqrt_f64(d);              // 1 / L[cc][cc]
+      const double l = (r > cc) ? cur[c] * rs : 0.0;   // L[r][cc]
+      cur[c] = (r == cc) ? sqrt(d) : l;
+      if (r == 0) rdiag[cc] = rs;
+#pragma unroll
+      for (int c2 = c + 1; c2 < kCh; ++c2) cur[c2] -= l * lane_value(l, j + c2);
+    }
+#pragma unroll
+    for (int c = 0; c < kCh; ++c) Lt[(j + c) * kP + r] = (j + c <= r) ? cur[c] : 0.0;
+    wave_sync();
+    // rank-8 update of the columns right of the chunk (row r, columns <= r)
+    for (int c0 = j + kCh; c0 < kNB; c0 += kCh) {
+      double t[kCh];
+#pragma unroll
+      for (int q = 0; q < kCh; ++q) t[q] = Lt[(c0 + q) * kP + r];
+#pragma unroll
+      for (int c = 0; c < kCh; ++c)
+#pragma unroll
+        for (int q = 0; q < kCh; ++q) t[q] -= cur[c] * Lt[(j + c) * kP + c0 + q];
+#pragma unroll
+      for (int q = 0; q < kCh; ++q)
+        if (c0 + q <= r) Lt[(c0 + q) * kP + r] = t[q];
+    }
+    wave_sync();
+  }
+  for (int i = 0; i < nbk; ++i)
+    if (r <= i) blk[i * m + r] = Lt[r * kP + i];
+  double* out = Linv + k0 * m + k0;
+  for (int J = 0; J < kNB; J += kCh) {
+    double acc[kCh];
+#pragma unroll
+    for (int i = 0; i < kCh; ++i) acc[i] = (J + i == r) ? 1.0 : 0.0;
+    for (int k = 0; k < J; k += kCh) {
+#pragma unroll
+      for (int kk = 0; kk < kCh; ++kk) {
+        const double xk = X[(k + kk) * kNB + r];
+        const double* lrow = &Lt[(k + kk) * kP + J];   // L[J .. J+7][k+kk]
+#pragma unroll
+        for (int i = 0; i < kCh; i += 2) {
+          const double2 l2 = *reinterpret_cast<const double2*>(lrow + i);
+          acc[i] -= l2.x * xk;
+          acc[i + 1] -= l2.y * xk;
+        }
       }
     }
-  }
+    double x[kCh];
 #pragma unroll
-  for (int c = 0; c < kNB; ++c)
-    if (r < nbk && c <= r) H[(k0 + r) * m + k0 + c] = a[c];
-}
-
-// Rows i >= k0 + nbk of the panel: H[i][K] <- H[i][K] L_KK^-T.
-__global__ __launch_bounds__(256) void trsm_panel_kernel(double* H, int64_t m, int64_t k0,
-                                                         int nbk) {
-  __shared__ double Lk[kNB][kNB + 1];
-  const int tid = threadIdx.x;
-  for (int e = tid; e < kNB * kNB; e += 256) {
-    const int r = e / kNB, c = e % kNB;
-    Lk[r][c] = (r < nbk && c <= r) ? H[(k0 + r) * m + k0 + c] : 0.0;
-  }
-  __syncthreads();
-  const int64_t i = k0 + nbk + (int64_t)blockIdx.x * 256 + tid;
-  if (i >= m) return;
-  double* row = H + i * m + k0;
-  double x[kNB];
+    for (int i = 0; i < kCh; ++i) {
+      double v = acc[i];   // the newest x enters last: the serial chain is two operations per row
 #pragma unroll
-  for (int c = 0; c < kNB; ++c) x[c] = (c < nbk) ? row[c] : 0.0;
-#pragma unroll
-  for (int c = 0; c < kNB; ++c) {
-    if (c < nbk) {
-      double p[4] = {0.0, 0.0, 0.0, 0.0};   // four partial sums break the FMA chain
-#pragma unroll
-      for (int c2 = 0; c2 < c; ++c2) p[c2 & 3] += x[c2] * Lk[c][c2];
-      x[c] = (x[c] - ((p[0] + p[1]) + (p[2] + p[3]))) / Lk[c][c];
+      for (int i2 = 0; i2 < i; ++i2) v -= Lt[(J + i2) * kP + J + i] * x[i2];
+      x[i] = v * rdiag[J + i];
+      X[(J + i) * kNB + r] = x[i];
+      if (J + i < nbk && r < nbk) out[(J + i) * m + r] = x[i];
     }
   }
-#pragma unroll
-  for (int c = 0; c < kNB; ++c)
-    if (c < nbk) row[c] = x[c];
 }
 
 __global__ void zero_upper_kernel(double* H, int64_t m) {
@@ -123,36 +184,6 @@ __global__ __launch_bounds__(256) void upper_to_lower_kernel(const double* R, do
   }
 }
 
-// Inverses of the 64x64 diagonal blocks of L (one workgroup per block),
-// written to the same positions of the m x m matrix Linv: lane c forms
-// column c of L_KK^-1 by forward substitution on e_c, with the block
-// broadcast from LDS.
-__global__ __launch_bounds__(64) void trtri_blocks_kernel(const double* __restrict__ L, int64_t m,
-                                                          double* __restrict__ Linv) {
-  __shared__ double Lk[kNB][kNB + 1];
-  const int c = threadIdx.x;
-  const int64_t k0 = (int64_t)blockIdx.x * kNB;
-  const int nbk = (int)((m - k0) < kNB ? (m - k0) : kNB);
-  for (int e = c; e < kNB * kNB; e += kNB) {
-    const int r = e / kNB, cc = e % kNB;
-    Lk[r][cc] = (r < nbk && cc <= r) ? L[(k0 + r) * m + k0 + cc] : (r == cc ? 1.0 : 0.0);
-  }
-  __syncthreads();
-  double x[kNB];
-#pragma unroll
-  for (int r = 0; r < kNB; ++r) {
-    double p[4] = {0.0, 0.0, 0.0, 0.0};   // four partial sums break the FMA chain
-#pragma unroll
-    for (int k = 0; k < r; ++k) p[k & 3] += Lk[r][k] * x[k];
-    const double v = ((r == c) ? 1.0 : 0.0) - ((p[0] + p[1]) + (p[2] + p[3]));
-    x[r] = (r >= c) ? v / Lk[r][r] : 0.0;
-  }
-  double* out = Linv + k0 * m + k0;
-#pragma unroll
-  for (int r = 0; r < kNB; ++r)
-    if (r < nbk && c < nbk) out[r * m + c] = x[r];
-}
-
 __global__ __launch_bounds__(256) void fill_zero_kernel(double* __restrict__ p, int64_t count) {
   for (int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x; e < count;
        e += (int64_t)gridDim.x * 256)
@@ -169,17 +200,25 @@ hipError_t launch_damp(double* H, int64_t m, double lambda_rel, double* lam2_out
   return hipGetLastError();
 }
 
-hipError_t cholesky_lower(double* H, int64_t m, int* status, hipStream_t stream) {
+hipError_t cholesky_lower(double* H, int64_t m, int* status, double* Linv, hipStream_t stream) {
+  const int64_t count = m * m;
+  const int64_t zb = (count + 255) / 256;
+  fill_zero_kernel<<<dim3((unsigned)(zb < 65536 ? zb : 65536)), dim3(256), 0, stream>>>(Linv, count);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
   for (int64_t k0 = 0; k0 < m; k0 += kNB) {
     const int nbk = (int)((m - k0) < kNB ? (m - k0) : kNB);
-    potrf_diag_kernel<<<1, 64, 0, stream>>>(H, m, k0, nbk, status);
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
+    potrf_trtri_kernel<<<1, 64, 0, stream>>>(H, m, k0, nbk, status, Linv);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
     const int64_t rest = m - k0 - nbk;
     if (rest <= 0) continue;
-    trsm_panel_kernel<<<blocks_for(rest, 256), 256, 0, stream>>>(H, m, k0, nbk);
-    if ((e = hipGetLastError()) != hipSuccess) return e;
-    GemmDesc g;
+    GemmDesc p;   // panel, in place: H[k1:, K] <- H[k1:, K] L_KK^-T (each row block read, then written)
+    p.M = rest; p.N = nbk; p.Kd = nbk;
+    p.A = H + (k0 + nbk) * m + k0; p.lda = m; p.ta = Elt::F64;
+    p.B = Linv + k0 * m + k0; p.ldb = m; p.tb = Elt::F64; p.b_zero_above_col = true;
+    p.C = H + (k0 + nbk) * m + k0; p.ldc = m; p.alpha = 1.0; p.beta = 0.0;
+    if ((e = gemm_f64(p, stream)) != hipSuccess) return e;
+    GemmDesc g;   // trailing update of the lower tiles
     g.M = rest; g.N = rest; g.Kd = nbk;
     g.A = H + (k0 + nbk) * m + k0; g.lda = m; g.ta = Elt::F64;
     g.B = H + (k0 + nbk) * m + k0; g.ldb = m; g.tb = Elt::F64;
@@ -199,20 +238,15 @@ hipError_t launch_upper_to_lower(const double* R, double* L, int64_t m, hipStrea
   return hipGetLastError();
 }
 
-// L^-1 by doubling: the 64x64 diagonal blocks are inverted directly, then
-// pairs of inverted blocks of size s merge into blocks of size 2 s with
+// L^-1 by doubling from the inverted 64x64 diagonal blocks that
+// cholesky_lower leaves in Linv: pairs of inverted blocks of size s merge
+// into blocks of size 2 s with
 //   [A 0; C D]^-1 = [A^-1 0; -D^-1 C A^-1  D^-1],
 // one batched GEMM for T = C A^-1 and one for -D^-1 T per level (plus one
 // pair of calls for a ragged last pair).  scratch holds m^2 / 4 doubles.
 hipError_t invert_lower(const double* L, int64_t m, double* Linv, double* scratch,
                         hipStream_t stream) {
-  const int64_t count = m * m;
-  const int64_t zb = (count + 255) / 256;
-  fill_zero_kernel<<<dim3((unsigned)(zb < 65536 ? zb : 65536)), dim3(256), 0, stream>>>(Linv, count);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
-  trtri_blocks_kernel<<<dim3((unsigned)((m + kNB - 1) / kNB)), dim3(kNB), 0, stream>>>(L, m, Linv);
-  if ((e = hipGetLastError()) != hipSuccess) return e;
+  hipError_t e;
   for (int64_t s = kNB; s < m; s *= 2) {
     const int64_t pitch = 2 * s * m + 2 * s;   // from one pair to the next
     auto merge = [&](int64_t p0, int64_t pairs, int64_t dsize) -> hipError_t {

@@ -125,6 +125,17 @@ __device__ __forceinline__ void raster_tile(int64_t t, int64_t tiles_m, int64_t 
   tj = r / rows;
 }
 
+// Triangular B (the k range grows or shrinks with the tile column): columns
+// in order of decreasing work, tile rows inner, one tile per blockIdx.  The
+// eight XCDs, dealt workgroups round-robin, then receive equal mixes of long
+// and short tiles, and each XCD starts its longest tiles first.
+__device__ __forceinline__ void tri_tile(int64_t t, int64_t tiles_m, int64_t tiles_n, bool grows,
+                                         int64_t& ti, int64_t& tj) {
+  ti = t % tiles_m;
+  const int64_t p = t / tiles_m;
+  tj = grows ? tiles_n - 1 - p : p;
+}
+
 // Consecutive tile numbers go to the same XCD (workgroups are dealt to the
 // eight XCDs round-robin by blockIdx).
 __device__ __forceinline__ int64_t xcd_tile_number() {
@@ -164,15 +175,19 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& g, int64_t ti, int64_t
     }
   };
 
+  // k range of the tile; with B zero below the diagonal the chunks run from
+  // the end down, so all tiles of a tile row start on the same A chunk.
   const int64_t kbeg = g.b_tri ? (J0 < g.Kd ? J0 : g.Kd) : 0;   // J0 is a multiple of kKC
   const int64_t kend = g.b_tri_up ? (J0 + kTile < g.Kd ? J0 + kTile : g.Kd) : g.Kd;
-  if (kbeg < kend) fetch(kbeg);
-  for (int64_t k0 = kbeg; k0 < kend; k0 += kKC) {
+  const int64_t nck = (kend - kbeg + kKC - 1) / kKC;
+  auto chunk_k = [&](int64_t c) { return kbeg + (g.b_tri ? nck - 1 - c : c) * kKC; };
+  if (nck > 0) fetch(chunk_k(0));
+  for (int64_t c = 0; c < nck; ++c) {
     __syncthreads();
     store_chunk<AK>(sA, tid, ra);
     store_chunk<BK>(sB, tid, rb);
     __syncthreads();
-    if (k0 + kKC < kend) fetch(k0 + kKC);
+    if (c + 1 < nck) fetch(chunk_k(c + 1));
 #pragma unroll
     for (int kk = 0; kk < kKC / 4; ++kk) {
       const int kr = kk * 4 + (lane >> 4);
@@ -188,20 +203,35 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& g, int64_t ti, int64_t
     }
   }
 
+  // Epilogue.  With beta != 0, the 16 C values of a row of wave tiles are
+  // loaded together (indices clamped into C, so the loads are unconditional
+  // and go out back to back) before any of them is overwritten.
 #pragma unroll
-  for (int x = 0; x < 4; ++x)
+  for (int x = 0; x < 4; ++x) {
+    const int64_t ib = I0 + wr * 64 + x * 16 + (lane >> 4);
+    const int64_t jb = J0 + wc * 64 + (lane & 15);
+    double cv[4][4];
+    if (g.beta != 0.0) {
+#pragma unroll
+      for (int y = 0; y < 4; ++y)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int64_t i = ib + 4 * r, j = jb + y * 16;
+          cv[y][r] = g.C[(i < g.M ? i : g.M - 1) * g.ldc + (j < g.N ? j : g.N - 1)];
+        }
+    }
 #pragma unroll
     for (int y = 0; y < 4; ++y)
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
-        const int64_t i = I0 + wr * 64 + x * 16 + (lane >> 4) + 4 * r;
-        const int64_t j = J0 + wc * 64 + y * 16 + (lane & 15);
+        const int64_t i = ib + 4 * r, j = jb + y * 16;
         if (i < g.M && j < g.N) {
           double v = g.alpha * acc[x][y][r];
-          if (g.beta != 0.0) v += g.beta * g.C[i * g.ldc + j];
+          if (g.beta != 0.0) v += g.beta * cv[y][r];
           g.C[i * g.ldc + j] = v;
         }
       }
+  }
 }
 
 template <typename TA, typename TB, bool AK, bool BK, bool BDIFF>
@@ -213,12 +243,13 @@ __global__ __launch_bounds__(256, 2) void gemm_f64_kernel(GemmArgs g) {
     g.B = static_cast<const TB*>(g.B) + blockIdx.y * g.sb;
     g.C += blockIdx.y * g.sc;
   }
-  const int64_t t = xcd_tile_number();
   int64_t ti, tj;
   if (g.lower)
-    lower_tile(t, ti, tj);
+    lower_tile(xcd_tile_number(), ti, tj);
+  else if (g.b_tri || g.b_tri_up)
+    tri_tile(blockIdx.x, g.tiles_m, g.tiles_n, g.b_tri_up != 0, ti, tj);
   else
-    raster_tile(t, g.tiles_m, g.tiles_n, ti, tj);
+    raster_tile(xcd_tile_number(), g.tiles_m, g.tiles_n, ti, tj);
   gemm_tile<TA, TB, AK, BK, BDIFF>(g, ti, tj, sA, sB);
 }
 

@@ -77,12 +77,14 @@ hipError_t launch_damp(double* H, int64_t m, double lambda_rel, double* lam2_out
                        hipStream_t stream);
 // In-place blocked Cholesky H = L L^T (lower, row-major); zeroes the strict
 // upper triangle.  *status (device int, initialised to INT32_MAX) receives the
-// smallest index of a non-positive pivot.
-hipError_t cholesky_lower(double* H, int64_t m, int* status, hipStream_t stream);
+// smallest index of a non-positive pivot.  Linv [m, m] is zeroed and receives
+// the inverses of the 64x64 diagonal blocks of L (the start of invert_lower).
+hipError_t cholesky_lower(double* H, int64_t m, int* status, double* Linv, hipStream_t stream);
 // L = R^T for an upper-triangular R (row-major); strict upper part of L = 0.
 hipError_t launch_upper_to_lower(const double* R, double* L, int64_t m, hipStream_t stream);
-// Linv = L^-1 [m, m] (lower, strict upper part zero) for the lower factor L;
-// scratch holds at least m^2 / 4 doubles.
+// Linv = L^-1 [m, m] (lower, strict upper part zero) for the lower factor L,
+// given Linv as cholesky_lower leaves it; scratch holds at least m^2 / 4
+// doubles.
 hipError_t invert_lower(const double* L, int64_t m, double* Linv, double* scratch,
                         hipStream_t stream);
 // Solves for n right-hand sides stored as rows of U [n, m] with Linv = L^-1:
