@@ -96,7 +96,7 @@ typedef struct ojbkq_ctx ojbkq_ctx;   /* opaque staged-solve state (host)     */
 size_t ojbkq_workspace_bytes(const ojbkq_params* p);
 
 /* One-shot layer quantisation (the whole path above, Alg. 1 + Alg. 3 + Alg. 4).
- *   X_ref, X_q: [m, T] with row stride ldx >= T (elements).  X_ref may be NULL
+ *   X_ref, X_q: [m, T] with row stride T <= ldx <= 2^27 (elements).  X_ref may be NULL
  *     or equal to X_q, and is not read when alpha == 1: the cross term
  *     X~^T (X - X~) then vanishes (Eq. jta_target with X = X~ or mu = 1).
  *   Outputs: codes, scales, zeros, residuals (required); winner (nullable).
@@ -112,7 +112,7 @@ int ojbkq_quantize_layer(const ojbkq_params* p, const float* W, const float* X_r
  *   create:     binds params, workspace (>= ojbkq_workspace_bytes) and stream;
  *               *out receives a host-side handle.  Sums start at zero.
  *   accumulate: adds X_q_c X_q_c^T and X_q_c (X_ref_c - X_q_c)^T of one chunk
- *               ([m, T_c], row stride ldx).  X_ref_c NULL or == X_q_c adds no
+ *               ([m, T_c], row stride T_c <= ldx <= 2^27).  X_ref_c NULL or == X_q_c adds no
  *               cross term.  Not allowed after the first solve (ESTATE).
  *   solve:      damps and factors the accumulated Gram on first use, then runs
  *               the rest of the path for W [n, m] and knob `alpha` (overrides

@@ -268,11 +268,16 @@ int ctx_init(ojbkq_ctx* c, const ojbkq_params* p, void* ws, size_t bytes, void* 
   return OJBKQ_OK;
 }
 
+// Row stride limit of the activation panels: the Gram kernel addresses a
+// lane's tokens by 32-bit byte offsets of up to 8 rows from a row pointer.
+constexpr int64_t kMaxLdx = int64_t(1) << 27;
+
 int ctx_accumulate(ojbkq_ctx* c, const float* Xr, const float* Xq, int64_t T, int64_t ldx) {
   if (c->factored) return fail(OJBKQ_ESTATE, "accumulate after the Gram was factored");
   if (!Xq) return fail(OJBKQ_EINVAL, "X_q is NULL");
   if (T < 1) return fail(OJBKQ_EINVAL, "token count must be >= 1");
   if (ldx < T) return fail(OJBKQ_EINVAL, "ldx must be >= T");
+  if (ldx > kMaxLdx) return fail(OJBKQ_EINVAL, "ldx must be <= 2^27");
   const bool cross = Xr != nullptr && Xr != Xq;
   hipEvent_t t0 = stage_begin(c);
   OJBKQ_HIP(ojbkq::gram_cross(Xq, cross ? Xr : nullptr, c->s.m, T, ldx, c->at<double>(c->L.G),
@@ -397,6 +402,7 @@ int ojbkq_quantize_layer(const ojbkq_params* p, const float* W, const float* X_r
     return fail(OJBKQ_EINVAL, "W, X_q, codes, scales, zeros and residuals are required");
   if (T < 1) return fail(OJBKQ_EINVAL, "token count must be >= 1");
   if (ldx < T) return fail(OJBKQ_EINVAL, "ldx must be >= T");
+  if (ldx > kMaxLdx) return fail(OJBKQ_EINVAL, "ldx must be <= 2^27");
   ojbkq_ctx c;
   if ((rc = ctx_init(&c, p, workspace, workspace_bytes, stream))) return rc;
   const float* Xr = (p->alpha == 1.0) ? nullptr : X_ref;

@@ -26,7 +26,6 @@ namespace {
 constexpr int kTile = 128;
 constexpr int kKC = 32;             // tokens per chunk
 constexpr int kThreads = 256;       // 4 waves: 2 x 2 blocks of 64x64
-constexpr int kLd = kTile + 16;     // padded LDS row (floats)
 constexpr int kSlotElems = kTile * kTile;
 
 struct GcArgs {
@@ -62,36 +61,77 @@ __device__ __forceinline__ void tile_coords(int64_t tile, const GcArgs& a, int64
   tj = e & 0xffff;
 }
 
-// kPer consecutive floats of row `row` from token k (zero past the ends).
-constexpr int kPer = kKC * kTile / kThreads;   // floats per thread per operand
-__device__ __forceinline__ void load_run(const float* __restrict__ X, int64_t ld, int64_t rows,
-                                         int64_t T, int64_t row, int64_t k, bool vec,
-                                         float v[kPer]) {
-  const int64_t left = T - k;
-  const int valid = (row < rows && left > 0) ? (int)(left < kPer ? left : kPer) : 0;
-  if (valid == kPer && vec) {
-    const float4* p = reinterpret_cast<const float4*>(X + row * ld + k);
+// LDS image of one operand chunk: 128 tile rows x 32 tokens of fp32, row r
+// at r * 32 floats, its eight 4-token groups permuted within the row (group
+// g in slot g ^ ((r >> 1) & 7)).  A fragment read (16 rows x 4 tokens of
+// one group) then touches 64 distinct banks, and 8 consecutive rows form a
+// contiguous 1 KB block that one direct-to-LDS load instruction fills from
+// 8 whole 128-byte lines.
+constexpr int kChunkFloats = kTile * kKC;
+typedef __attribute__((address_space(3))) void lds_void;
+typedef __attribute__((address_space(1))) void gbl_void;
+
+__device__ __forceinline__ int group_slot(int row, int g) { return g ^ ((row >> 1) & 7); }
+
+// This wave's share of the direct-to-LDS loads of one operand panel (tile
+// rows R0 .. R0+127): load instruction j fills the 1 KB (or, with 4-byte
+// loads, 256-byte) LDS block `inst`, i.e. tile rows inst * kRowsPerInst ...
+// Each instruction addresses a wave-uniform row pointer plus a 32-bit lane
+// offset, so a chunk's loads cost no vector arithmetic: only the uniform
+// pointers move by 32 tokens per chunk.  Rows past the matrix read its last
+// row (their products land only in unused outputs).  kBytes = 16 needs
+// 16-byte aligned rows and T % 4 == 0; kBytes = 4 has no requirement.
+template <int kBytes>
+struct PanelLoader {
+  static constexpr int kLanesPerRow = kKC * 4 / kBytes;   // lanes covering one row
+  static constexpr int kRowsPerInst = 64 / kLanesPerRow;
+  static constexpr int kInst = kTile / kRowsPerInst / 4;   // per wave
+  const float* rowp[kInst];   // first row of block inst (wave-uniform)
+  uint32_t off[kInst];        // this lane's byte offset from rowp[j] at token k0
+
+  // tmax: the last token a lane may start at past k0 (kKC - 1 but for a
+  // ragged chunk, where tokens past T are read from T - 1 and zeroed later)
+  __device__ __forceinline__ void setup(const float* X, int64_t ld, int64_t rows, int64_t R0,
+                                        int wave, int lane, int64_t tmax) {
 #pragma unroll
-    for (int q = 0; q < kPer / 4; ++q) {
-      const float4 f = p[q];
-      v[4 * q] = f.x; v[4 * q + 1] = f.y; v[4 * q + 2] = f.z; v[4 * q + 3] = f.w;
+    for (int j = 0; j < kInst; ++j) {
+      const int inst = wave * kInst + j;
+      int64_t r0 = R0 + inst * kRowsPerInst;
+      r0 = r0 < rows ? r0 : rows - 1;
+      rowp[j] = X + r0 * ld;
+      const int rl = inst * kRowsPerInst + lane / kLanesPerRow;   // tile row (LDS)
+      int64_t dr = lane / kLanesPerRow;                           // rows past r0 (clamped)
+      dr = r0 + dr < rows ? dr : rows - 1 - r0;
+      const int pos = (lane % kLanesPerRow) * (kBytes / 4);       // float position in the row
+      int64_t t = 4 * group_slot(rl, pos >> 2) + (pos & 3);       // the slot's token
+      t = t < tmax ? t : tmax;
+      off[j] = (uint32_t)((dr * ld + t) * 4);
     }
-  } else {
-    const float* p = valid > 0 ? X + row * ld + k : X;
-#pragma unroll
-    for (int q = 0; q < kPer; ++q) v[q] = (q < valid) ? p[q] : 0.0f;
   }
-}
+  __device__ __forceinline__ void issue(int64_t k0, float* dst, int wave) const {
+#pragma unroll
+    for (int j = 0; j < kInst; ++j) {
+      gbl_void* src = (gbl_void*)(reinterpret_cast<const char*>(rowp[j] + k0) + off[j]);
+      lds_void* to = (lds_void*)(dst + (wave * kInst + j) * 16 * kBytes);
+      if constexpr (kBytes == 16)
+        __builtin_amdgcn_global_load_lds(src, to, 16, 0, 0);
+      else
+        __builtin_amdgcn_global_load_lds(src, to, 4, 0, 0);
+    }
+  }
+};
+
+// vmcnt(0): this wave's direct-to-LDS loads have landed.
+__device__ __forceinline__ void wait_loads() { __builtin_amdgcn_s_waitcnt(0x0f70); }
 
 // Chunks [c0, c1) of one tile.  A whole tile is written to G / E directly;
-// a part goes to partial slot `slot` of share r.
+// a part goes to partial slot `slot` of share r.  Two LDS stages: the loads
+// of chunk c + 1 fly while chunk c feeds the matrix cores.
+template <int kBytes>
 __device__ __forceinline__ void gram_segment(const GcArgs& a, int64_t tile, int64_t c0, int64_t c1,
-                                             int64_t r, int& slot, float (*sA)[kLd],
-                                             float (*sB)[kLd]) {
+                                             int64_t r, int& slot, float* sbuf) {
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wr = wave >> 1, wc = wave & 1;   // 64x64 block of the tile
-  constexpr int kPartsPerRow = kKC / kPer;
-  const int lrow = tid / kPartsPerRow, lk = (tid % kPartsPerRow) * kPer;
   int64_t ti, tj;
   bool cross;
   tile_coords(tile, a, ti, tj, cross);
@@ -104,29 +144,51 @@ __device__ __forceinline__ void gram_segment(const GcArgs& a, int64_t tile, int6
 #pragma unroll
     for (int y = 0; y < 4; ++y) acc[x][y] = d4{0.0, 0.0, 0.0, 0.0};
 
-  float ra[kPer], rb[kPer];
-  load_run(a.Xq, a.ldx, a.m, a.T, I0 + lrow, c0 * kKC + lk, a.vec, ra);
-  load_run(Bsrc, a.ldx, a.m, a.T, J0 + lrow, c0 * kKC + lk, a.vec, rb);
+  const int sw = (lane & 15) >> 1, kt = lane >> 4;   // this lane's slot permutation and token
+  const int uwave = __builtin_amdgcn_readfirstlane(wave);
+  // the last chunk may be ragged: its loads start no later than token T - kBytes / 4
+  const int64_t klast = (a.nchunks - 1) * kKC;
+  const int64_t tlast = a.T - kBytes / 4 - klast;
+  PanelLoader<kBytes> la, lb;
+  la.setup(a.Xq, a.ldx, a.m, I0, uwave, lane, kKC);
+  lb.setup(Bsrc, a.ldx, a.m, J0, uwave, lane, kKC);
+  __syncthreads();   // the previous segment's reads of both stages are done
+  auto issue = [&](int64_t c, float* dst) {
+    if (c * kKC == klast && tlast < kKC - 1) {   // ragged last chunk: clamp the token offsets
+      PanelLoader<kBytes> ra, rb;
+      ra.setup(a.Xq, a.ldx, a.m, I0, uwave, lane, tlast);
+      rb.setup(Bsrc, a.ldx, a.m, J0, uwave, lane, tlast);
+      ra.issue(klast, dst, uwave);
+      rb.issue(klast, dst + kChunkFloats, uwave);
+    } else {
+      la.issue(c * kKC, dst, uwave);
+      lb.issue(c * kKC, dst + kChunkFloats, uwave);
+    }
+  };
+  issue(c0, sbuf);
   for (int64_t c = c0; c < c1; ++c) {
-    __syncthreads();
-#pragma unroll
-    for (int q = 0; q < kPer; ++q) {
-      sA[lk + q][lrow] = ra[q];
-      sB[lk + q][lrow] = rb[q];
+    float* cur = sbuf + ((c - c0) & 1) * 2 * kChunkFloats;
+    wait_loads();
+    __syncthreads();   // chunk c is in LDS; every wave is done with chunk c - 1
+    const int64_t k0 = c * kKC;
+    if (k0 + kKC > a.T) {   // ragged last chunk: zero the tokens past T
+      const int rl = tid & (kTile - 1);
+      float* row = cur + (tid >> 7) * kChunkFloats + rl * kKC;
+      for (int q = 0; q < kKC; ++q)
+        if (k0 + q >= a.T) row[4 * group_slot(rl, q >> 2) + (q & 3)] = 0.0f;
+      __syncthreads();
     }
-    __syncthreads();
-    if (c + 1 < c1) {
-      load_run(a.Xq, a.ldx, a.m, a.T, I0 + lrow, (c + 1) * kKC + lk, a.vec, ra);
-      load_run(Bsrc, a.ldx, a.m, a.T, J0 + lrow, (c + 1) * kKC + lk, a.vec, rb);
-    }
+    if (c + 1 < c1) issue(c + 1, sbuf + ((c + 1 - c0) & 1) * 2 * kChunkFloats);
+    const float* sA = cur + (wr * 64 + (lane & 15)) * kKC + kt;
+    const float* sB = cur + kChunkFloats + (wc * 64 + (lane & 15)) * kKC + kt;
 #pragma unroll
     for (int kk = 0; kk < kKC / 4; ++kk) {
-      const int kr = kk * 4 + (lane >> 4);
+      const int off = 4 * (kk ^ sw);
       double fa[4], fb[4];
 #pragma unroll
-      for (int x = 0; x < 4; ++x) fa[x] = (double)sA[kr][wr * 64 + x * 16 + (lane & 15)];
+      for (int x = 0; x < 4; ++x) fa[x] = (double)sA[x * 16 * kKC + off];
 #pragma unroll
-      for (int y = 0; y < 4; ++y) fb[y] = (double)sB[kr][wc * 64 + y * 16 + (lane & 15)];
+      for (int y = 0; y < 4; ++y) fb[y] = (double)sB[y * 16 * kKC + off];
 #pragma unroll
       for (int x = 0; x < 4; ++x)
 #pragma unroll
@@ -163,30 +225,37 @@ __device__ __forceinline__ void gram_segment(const GcArgs& a, int64_t tile, int6
   }
 }
 
+template <int kBytes>
 __global__ __launch_bounds__(kThreads, 2) void gram_cross_kernel(GcArgs a) {
-  __shared__ float sA[kKC][kLd];   // X_q rows of the A panel
-  __shared__ float sB[kKC][kLd];   // X_q (Gram tile) or X_ref (mixed tile) rows of the B panel
+  // two stages x (A panel: X_q rows; B panel: X_q rows of a Gram tile or
+  // X_ref rows of a mixed tile), 64 KB
+  __shared__ __align__(16) float sbuf[2 * 2 * kChunkFloats];
   // share index: consecutive shares on one XCD
   int64_t r = blockIdx.x;
   if ((a.nshare & 7) == 0) r = (r & 7) * (a.nshare >> 3) + (r >> 3);
   int slot = 0;
   for (int64_t round = 0; round < a.n_dp; ++round)
-    gram_segment(a, round * a.nshare + r, 0, a.nchunks, r, slot, sA, sB);
+    gram_segment<kBytes>(a, round * a.nshare + r, 0, a.nchunks, r, slot, sbuf);
   if (r >= a.nsk) return;
   const int64_t w_end = share_begin(r + 1, a);
   for (int64_t w = share_begin(r, a); w < w_end;) {
     const int64_t tile = a.tile0 + w / a.nchunks;
     const int64_t c0 = w % a.nchunks;
     const int64_t c1 = (a.nchunks - c0) < (w_end - w) ? a.nchunks : c0 + (w_end - w);
-    gram_segment(a, tile, c0, c1, r, slot, sA, sB);
+    gram_segment<kBytes>(a, tile, c0, c1, r, slot, sbuf);
     w += c1 - c0;
   }
 }
 
 // Sum the partial tiles of every tile that straddles share boundaries, in
-// share order.  Workgroup b handles the tile holding the start of share b + 1
-// when b + 1 is the first share boundary inside that tile.
+// share order.  Workgroup (b, y) handles element block y of the tile holding
+// the start of share b + 1 when b + 1 is the first share boundary inside that
+// tile.  The contributing shares' slot numbers are staged in LDS 256 at a
+// time; each thread then streams its kFixElems elements of every partial.
+constexpr int kFixSplit = 16;                                // element blocks per tile
+constexpr int kFixElems = kSlotElems / kFixSplit / 256;      // elements per thread
 __global__ __launch_bounds__(256) void gram_cross_fixup_kernel(GcArgs a) {
+  __shared__ int slot_of[256];
   const int64_t rb = (int64_t)blockIdx.x + 1;
   const int64_t wb = share_begin(rb, a);
   if (wb >= a.work || wb % a.nchunks == 0) return;
@@ -201,18 +270,31 @@ __global__ __launch_bounds__(256) void gram_cross_fixup_kernel(GcArgs a) {
   // contributing shares: rb - 1 .. the share holding tend - 1
   int64_t rlast = rb;
   while (rlast + 1 < a.nsk && share_begin(rlast + 1, a) < tend) ++rlast;
-  for (int e = threadIdx.x; e < kSlotElems; e += 256) {
-    const int li = e / kTile, lj = e % kTile;
-    const int64_t i = ti * kTile + li, j = tj * kTile + lj;
-    if (i >= a.m || j >= a.m) continue;
-    double s = 0.0;
-    for (int64_t q = rb - 1; q <= rlast; ++q) {
-      const int sl = (a.part_tile[q * 2] == (int)tile) ? 0 : 1;
-      s += a.part[(q * 2 + sl) * kSlotElems + e];
+  const int e0 = blockIdx.y * (kSlotElems / kFixSplit) + threadIdx.x;
+  double s[kFixElems];
+#pragma unroll
+  for (int k = 0; k < kFixElems; ++k) s[k] = 0.0;
+  for (int64_t qb = rb - 1; qb <= rlast; qb += 256) {
+    const int nq = (int)((rlast + 1 - qb) < 256 ? (rlast + 1 - qb) : 256);
+    __syncthreads();
+    if ((int)threadIdx.x < nq)
+      slot_of[threadIdx.x] = (a.part_tile[(qb + threadIdx.x) * 2] == (int)tile) ? 0 : 1;
+    __syncthreads();
+    for (int u = 0; u < nq; ++u) {
+      const double* P = a.part + ((qb + u) * 2 + slot_of[u]) * kSlotElems + e0;
+#pragma unroll
+      for (int k = 0; k < kFixElems; ++k) s[k] += P[k * 256];
     }
-    double v = s;
-    if (beta != 0.0) v += beta * C[i * a.m + j];
-    C[i * a.m + j] = v;
+  }
+#pragma unroll
+  for (int k = 0; k < kFixElems; ++k) {
+    const int e = e0 + k * 256;
+    const int64_t i = ti * kTile + e / kTile, j = tj * kTile + e % kTile;
+    if (i < a.m && j < a.m) {
+      double v = s[k];
+      if (beta != 0.0) v += beta * C[i * a.m + j];
+      C[i * a.m + j] = v;
+    }
   }
 }
 
@@ -301,12 +383,15 @@ hipError_t gram_cross(const float* Xq, const float* Xr, int64_t m, int64_t T, in
   a.part_tile = reinterpret_cast<int*>(static_cast<char*>(scratch) +
                                        (size_t)kGramCrossMaxShares * 2 * kSlotElems * sizeof(double));
   const bool vec = (reinterpret_cast<uintptr_t>(Xq) % 16 == 0) && (ldx % 4 == 0) &&
-                   (Xr == nullptr || reinterpret_cast<uintptr_t>(Xr) % 16 == 0);
+                   (T % 4 == 0) && (Xr == nullptr || reinterpret_cast<uintptr_t>(Xr) % 16 == 0);
   a.vec = vec ? 1 : 0;
-  gram_cross_kernel<<<dim3((unsigned)a.nshare), dim3(kThreads), 0, stream>>>(a);
+  if (vec)
+    gram_cross_kernel<16><<<dim3((unsigned)a.nshare), dim3(kThreads), 0, stream>>>(a);
+  else
+    gram_cross_kernel<4><<<dim3((unsigned)a.nshare), dim3(kThreads), 0, stream>>>(a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || a.nsk < 2) return e;
-  gram_cross_fixup_kernel<<<dim3((unsigned)(a.nsk - 1)), dim3(256), 0, stream>>>(a);
+  gram_cross_fixup_kernel<<<dim3((unsigned)(a.nsk - 1), kFixSplit), dim3(256), 0, stream>>>(a);
   return hipGetLastError();
 }
 

@@ -78,6 +78,9 @@ def test_null_and_shape_errors_before_any_launch():
                                     None) == -1
     assert lib.ojbkq_quantize_layer(ctypes.byref(p), 1, None, 1, 10, 9, 256, ws, None, 1, 1, 1, 1,
                                     None) == -1
+    assert lib.ojbkq_quantize_layer(ctypes.byref(p), 1, None, 1, 10, (1 << 27) + 1, 256, ws, None,
+                                    1, 1, 1, 1, None) == -1
+    assert "2^27" in lib.ojbkq_last_error().decode()
     # misaligned or missing workspace
     assert lib.ojbkq_quantize_layer(ctypes.byref(p), 1, None, 1, 10, 10, 0, ws, None, 1, 1, 1, 1,
                                     None) == -1

@@ -220,6 +220,36 @@ def test_staged_intermediates_and_chunks():
     s.close()
 
 
+def test_gram_load_paths_agree():
+    """The Gram/cross contraction reads 16-byte runs of tokens when rows are
+    16-byte aligned and T % 4 == 0, else single tokens; both paths stage the
+    same LDS image, so the factor they lead to is bit-identical, and it matches
+    the oracle's."""
+    cfg = small_cfg(200, 24, 1200, 4, 128, 4, 33)
+    W, Xr, Xq = make_layer(cfg, device=DEV)
+
+    def factor(xr, xq):
+        s = ok.LayerSolver(cfg.m, cfg.n, cfg.bits, cfg.group, cfg.K, cfg.klein_seed, device=DEV)
+        s.accumulate(xr, xq)
+        s.solve(W, 0.5)
+        L = s.inspect("L")
+        s.close()
+        return L
+
+    L16 = factor(Xr, Xq)
+    # the same tokens as views at a 4-byte offset with an odd row stride
+    br = torch.zeros(cfg.m, cfg.T + 5, dtype=torch.float32, device=DEV)
+    bq = torch.zeros_like(br)
+    br[:, 1:cfg.T + 1] = Xr
+    bq[:, 1:cfg.T + 1] = Xq
+    L4 = factor(br[:, 1:cfg.T + 1], bq[:, 1:cfg.T + 1])
+    assert torch.equal(L16, L4)
+    o = orc.quantize_layer(np64(W), np64(Xr), np64(Xq), 0.5, cfg.bits, cfg.group, cfg.K,
+                           cfg.klein_seed)
+    colnorm = np.sqrt(np.sum(o.R ** 2, axis=0))
+    assert np.max(np.abs(np64(L16).T - o.R) / colnorm[None, :]) < 1e-10
+
+
 def test_alpha_sweep_reuses_factor():
     cfg = small_cfg(160, 20, 600, 3, 32, 5, 41)
     W, Xr, Xq = make_layer(cfg, device=DEV)
