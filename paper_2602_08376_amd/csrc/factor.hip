@@ -59,23 +59,23 @@ __device__ __forceinline__ double lane_value(double v, int lane) {
   return __hiloint2double(hi, lo);
 }
 
-// Unblocked Cholesky of the nbk x nbk diagonal block starting at (k0, k0),
-// by one wave, followed by the inverse of the factored block, written to
-// Linv at (k0, k0).  The block lives in LDS column-major (padded to 64 x 64
-// with the identity) and both phases walk it in chunks of eight columns, so
-// the code is a few short loops that stay in the instruction cache.
-//  - Factor: lane r owns row r.  A chunk's eight entries of the row sit in
-//    registers; within the chunk each new column reaches the other lanes by
-//    readlane, then the chunk is stored and the rows below take its rank-8
-//    update, eight columns per pass, from broadcast LDS reads.
-//  - Inverse: lane c forms column c of L_KK^-1 by forward substitution, eight
-//    rows at a time; earlier rows of the column come back from LDS.
-// Loads and LDS reads are unconditional (addresses clamped into the block),
-// so they issue back to back instead of waiting one by one.
+// Cholesky of the nbk x nbk diagonal block starting at (k0, k0), by one
+// wave, followed by the inverse of the factored block, written to Linv at
+// (k0, k0).  The block lives in LDS column-major (padded to 64 x 64 with the
+// identity).
+//  - Factor, eight columns per chunk: every lane factors the chunk's 8 x 8
+//    diagonal block in registers (the same values on all lanes, so no
+//    cross-lane traffic on the serial chain), then lane r solves its row's
+//    eight entries against it, and the columns right of the chunk take the
+//    rank-8 update C -= P P^T of the 64 x 8 chunk panel P on fp64 MFMA.
+//  - Inverse, sixteen rows per chunk: the product of the chunk's rows of L
+//    with the rows of L_KK^-1 already known runs on MFMA; then lane c solves
+//    its column's sixteen entries by forward substitution.
 __global__ __launch_bounds__(64) void potrf_trtri_kernel(double* H, int64_t m, int64_t k0, int nbk,
                                                          int* status, double* Linv) {
-  constexpr int kP = kNB + 2;   // column pitch of the block in LDS (doubles; 16-byte rows)
-  constexpr int kCh = 8;        // columns per chunk
+  constexpr int kP = kNB + 2;   // column pitch of the block in LDS (doubles; 16-byte columns)
+  constexpr int kCh = 8;        // factor chunk (columns)
+  constexpr int kIh = 16;       // inverse chunk (rows)
   __shared__ __align__(16) double Lt[kNB * kP];   // Lt[c * kP + r] = L[r][c]
   __shared__ double X[kNB * kNB];                 // X[r * kNB + c] = (L_KK^-1)[r][c]
   __shared__ double rdiag[kNB];                   // 1 / L[i][i]
@@ -93,70 +93,103 @@ __global__ __launch_bounds__(64) void potrf_trtri_kernel(double* H, int64_t m, i
     for (int i = 0; i < kNB; ++i) Lt[r * kP + i] = (i < nbk && r <= i) ? v[i] : (r == i ? 1.0 : 0.0);
   }
   wave_sync();
+  const int l16 = r & 15, lk = r >> 4;   // MFMA operand coordinates of this lane
   for (int j = 0; j < kNB; j += kCh) {
-    double cur[kCh];
+    // the chunk's diagonal block D (lower), factored redundantly on every lane
+    double D[kCh][kCh], rs[kCh];
 #pragma unroll
-    for (int c = 0; c < kCh; ++c) cur[c] = Lt[(j + c) * kP + r];
+    for (int b = 0; b < kCh; ++b)
+#pragma unroll
+      for (int a = 0; a < kCh; a += 2) {
+        const double2 v2 = *reinterpret_cast<const double2*>(&Lt[(j + b) * kP + j + a]);
+        D[a][b] = v2.x;
+        D[a + 1][b] = v2.y;
+      }
+#pragma unroll
+    for (int a = 0; a < kCh; ++a) {
+      const double d = D[a][a];
+      if (r == 0 && j + a < nbk && !(d > 0.0)) atomicMin(status, (int)(k0 + j + a));
+      rs[a] = rsqrt_f64(d);
+#pragma unroll
+      for (int b = a + 1; b < kCh; ++b) D[b][a] *= rs[a];
+#pragma unroll
+      for (int b = a + 1; b < kCh; ++b)
+#pragma unroll
+        for (int c = a + 1; c <= b; ++c) D[b][c] -= D[b][a] * D[c][a];
+    }
+    if (r == 0) {
+#pragma unroll
+      for (int a = 0; a < kCh; ++a) rdiag[j + a] = rs[a];
+    }
+    // row r's entries of the chunk: L[r][j+c] = (H[r][j+c] - sum_{c'<c} L[r][j+c'] L[j+c][j+c']) / L[j+c][j+c]
+    double x[kCh];
 #pragma unroll
     for (int c = 0; c < kCh; ++c) {
-      const int cc = j + c;
-      const double d = lane_value(cur[c], cc);   // pivot: row cc, column cc
-      if (r == 0 && cc < nbk && !(d > 0.0)) atomicMin(status, (int)(k0 + cc));
-      const double rs = rsqrt_f64(d);              // 1 / L[cc][cc]
-      const double l = (r > cc) ? cur[c] * rs : 0.0;   // L[r][cc]
-      cur[c] = (r == cc) ? sqrt(d) : l;
-      if (r == 0) rdiag[cc] = rs;
+      double v = Lt[(j + c) * kP + r];
 #pragma unroll
-      for (int c2 = c + 1; c2 < kCh; ++c2) cur[c2] -= l * lane_value(l, j + c2);
+      for (int c2 = 0; c2 < c; ++c2) v -= x[c2] * D[c][c2];
+      x[c] = v * rs[c];
     }
 #pragma unroll
-    for (int c = 0; c < kCh; ++c) Lt[(j + c) * kP + r] = (j + c <= r) ? cur[c] : 0.0;
+    for (int c = 0; c < kCh; ++c) Lt[(j + c) * kP + r] = (j + c <= r) ? x[c] : 0.0;
     wave_sync();
-    // rank-8 update of the columns right of the chunk (row r, columns <= r)
-    for (int c0 = j + kCh; c0 < kNB; c0 += kCh) {
-      double t[kCh];
+    // C[row][col] -= sum_c P[row][c] P[col][c] for col >= j + 8, row >= col
+    // (16 x 16 MFMA tiles; lane l holds rows 16 R + l/16 + 4 q of column 16 Cb + l%16)
+    for (int Cb = (j + kCh) >> 4; Cb < kNB / 16; ++Cb) {
+      double bo[2];
 #pragma unroll
-      for (int q = 0; q < kCh; ++q) t[q] = Lt[(c0 + q) * kP + r];
+      for (int s2 = 0; s2 < 2; ++s2) bo[s2] = Lt[(j + 4 * s2 + lk) * kP + 16 * Cb + l16];
+      const int col = 16 * Cb + l16;
+      for (int R = Cb; R < kNB / 16; ++R) {
+        d4 acc;
 #pragma unroll
-      for (int c = 0; c < kCh; ++c)
+        for (int q = 0; q < 4; ++q) acc[q] = Lt[col * kP + 16 * R + lk + 4 * q];
 #pragma unroll
-        for (int q = 0; q < kCh; ++q) t[q] -= cur[c] * Lt[(j + c) * kP + c0 + q];
+        for (int s2 = 0; s2 < 2; ++s2)
+          acc = mfma_f64(-Lt[(j + 4 * s2 + lk) * kP + 16 * R + l16], bo[s2], acc);
 #pragma unroll
-      for (int q = 0; q < kCh; ++q)
-        if (c0 + q <= r) Lt[(c0 + q) * kP + r] = t[q];
+        for (int q = 0; q < 4; ++q) {
+          const int row = 16 * R + lk + 4 * q;
+          if (col >= j + kCh && row >= col) Lt[col * kP + row] = acc[q];
+        }
+      }
     }
     wave_sync();
   }
   for (int i = 0; i < nbk; ++i)
     if (r <= i) blk[i * m + r] = Lt[r * kP + i];
   double* out = Linv + k0 * m + k0;
-  for (int J = 0; J < kNB; J += kCh) {
-    double acc[kCh];
+  for (int J = 0; J < kNB; J += kIh) {
+    // V[J+i][col] = delta - sum_{k<J} L[J+i][k] X[k][col] on MFMA, staged in X's rows J..J+15
+    d4 acc[kNB / 16];
 #pragma unroll
-    for (int i = 0; i < kCh; ++i) acc[i] = (J + i == r) ? 1.0 : 0.0;
-    for (int k = 0; k < J; k += kCh) {
+    for (int Cb = 0; Cb < kNB / 16; ++Cb)
 #pragma unroll
-      for (int kk = 0; kk < kCh; ++kk) {
-        const double xk = X[(k + kk) * kNB + r];
-        const double* lrow = &Lt[(k + kk) * kP + J];   // L[J .. J+7][k+kk]
+      for (int q = 0; q < 4; ++q) acc[Cb][q] = (J + lk + 4 * q == 16 * Cb + l16) ? 1.0 : 0.0;
+#pragma unroll 4
+    for (int k = 0; k < J; k += 4) {
+      const double a = -Lt[(k + lk) * kP + J + l16];
 #pragma unroll
-        for (int i = 0; i < kCh; i += 2) {
-          const double2 l2 = *reinterpret_cast<const double2*>(lrow + i);
-          acc[i] -= l2.x * xk;
-          acc[i + 1] -= l2.y * xk;
-        }
-      }
+      for (int Cb = 0; Cb < kNB / 16; ++Cb)
+        acc[Cb] = mfma_f64(a, X[(k + lk) * kNB + 16 * Cb + l16], acc[Cb]);
     }
-    double x[kCh];
 #pragma unroll
-    for (int i = 0; i < kCh; ++i) {
-      double v = acc[i];   // the newest x enters last: the serial chain is two operations per row
+    for (int Cb = 0; Cb < kNB / 16; ++Cb)
 #pragma unroll
-      for (int i2 = 0; i2 < i; ++i2) v -= Lt[(J + i2) * kP + J + i] * x[i2];
-      x[i] = v * rdiag[J + i];
-      X[(J + i) * kNB + r] = x[i];
-      if (J + i < nbk && r < nbk) out[(J + i) * m + r] = x[i];
+      for (int q = 0; q < 4; ++q) X[(J + lk + 4 * q) * kNB + 16 * Cb + l16] = acc[Cb][q];
+    wave_sync();
+    // lane r = column: forward substitution through the chunk's 16 rows
+    double xs[kIh];
+#pragma unroll
+    for (int i = 0; i < kIh; ++i) {
+      double v = X[(J + i) * kNB + r];
+#pragma unroll
+      for (int i2 = 0; i2 < i; ++i2) v -= Lt[(J + i2) * kP + J + i] * xs[i2];
+      xs[i] = v * rdiag[J + i];
+      X[(J + i) * kNB + r] = xs[i];
+      if (J + i < nbk && r < nbk) out[(J + i) * m + r] = xs[i];
     }
+    wave_sync();
   }
 }
 
