@@ -129,7 +129,8 @@ int ojbkq_destroy(ojbkq_ctx* ctx);
 /* Read-only view of an intermediate of the last staged solve (device pointer
  * into the workspace, valid until the next call on ctx):
  *   which = 0: L = R^T, lower triangle of [m, m] float64, strict upper zero
- *           1: qbar [n, m] float64 (Alg. 1 step 4)
+ *           1: Rbar qbar [n, m] float64: row j is R diag(s_j) qbar_j, the
+ *              decoder's input (qbar itself, Alg. 1 step 4, is never formed)
  *           2: alpha_j [n] float64 (Klein temperature per column)
  *           3: lambda^2 [1] float64
  *           4: per-candidate residuals [n, K + 1] float64
@@ -144,8 +145,8 @@ int ojbkq_inspect(ojbkq_ctx* ctx, int which, const void** ptr);
  * device memory is allocated.  Stages:
  *   GRAM     Gram and mixed-product launches (every accumulate)
  *   FACTOR   cross term from the mixed product, damping, blocked Cholesky
- *   SOLVE    scales and zero points, W E^T, the two triangular solves
- *   CENTRES  centres qbar, Rbar qbar, Klein temperatures
+ *   SOLVE    scales and zero points, W E^T, its product with L^-T
+ *   CENTRES  shifted weights W + s z, Rbar qbar, Klein temperatures
  *   DECODE   the batched Babai / Klein decode kernel
  *   SELECT   candidate selection and gather                              */
 enum {

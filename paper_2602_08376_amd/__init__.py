@@ -254,11 +254,12 @@ class LayerSolver:
         return out
 
     def inspect(self, which: str) -> torch.Tensor:
-        """A copy of an intermediate of the last solve: 'L', 'qbar', 'alpha', 'lam2', 'path_resid'."""
-        idx = {"L": 0, "qbar": 1, "alpha": 2, "lam2": 3, "path_resid": 4}[which]
+        """A copy of an intermediate of the last solve: 'L', 'gq' (rows Rbar_j qbar_j),
+        'alpha', 'lam2', 'path_resid'."""
+        idx = {"L": 0, "gq": 1, "alpha": 2, "lam2": 3, "path_resid": 4}[which]
         ptr = ctypes.c_void_p()
         _check(library().ojbkq_inspect(self.h, idx, ctypes.byref(ptr)))
-        shape = {"L": (self.m, self.m), "qbar": (self.n, self.m), "alpha": (self.n,),
+        shape = {"L": (self.m, self.m), "gq": (self.n, self.m), "alpha": (self.n,),
                  "lam2": (1,), "path_resid": (self.n, self.K + 1)}[which]
         off = ptr.value - self.ws.data_ptr()
         count = int(math.prod(shape))

@@ -60,7 +60,7 @@ Shape shape_of(const ojbkq_params& p) {
 
 // Offsets of every buffer carved from the workspace.
 struct Layout {
-  size_t status = 0, lam2 = 0, G = 0, E = 0, U = 0, qbar = 0, gq = 0, alpha = 0, pcodes = 0,
+  size_t status = 0, lam2 = 0, G = 0, E = 0, U = 0, gq = 0, alpha = 0, pcodes = 0,
          presid = 0, gc_scratch = 0, gc_tiles = 0, F = 0, Linv = 0, total = 0;
 };
 
@@ -79,7 +79,6 @@ Layout layout_full(const Shape& s) {
   L.G = take(mm);
   L.E = take(mm);
   L.U = take(nm);
-  L.qbar = take(nm);
   L.gq = take(nm);
   L.alpha = take((size_t)s.n * sizeof(double));
   L.pcodes = take((size_t)ojbkq::decode_code_bytes(s.m, s.geo));
@@ -332,6 +331,7 @@ int ctx_solve(ojbkq_ctx* c, const float* W, double alpha, uint8_t* codes, float*
   OJBKQ_HIP(ojbkq::launch_scale_zero(W, s.n, s.m, s.g, s.G, s.qmax, scales, zeros, st),
             "scales");
   double* U = c->at<double>(c->L.U);
+  double* gq = c->at<double>(c->L.gq);
   const bool cross = c->cross_seen && alpha != 1.0;
   if (cross) {
     ojbkq::GemmDesc g;   // U = W E^T: row j is X~^T (X - X~) w_j
@@ -340,23 +340,21 @@ int ctx_solve(ojbkq_ctx* c, const float* W, double alpha, uint8_t* codes, float*
     g.B = c->at<double>(c->L.E); g.ldb = s.m; g.tb = ojbkq::Elt::F64;
     g.C = U; g.ldc = s.m;
     OJBKQ_HIP(ojbkq::gemm_f64(g, st), "target projection");
-    OJBKQ_HIP(ojbkq::solve_llt(c->at<double>(c->L.Linv), U, c->at<double>(c->L.gq), s.n, s.m,
-                               st),
-              "solves");
+    // gq <- U L^-T: row j is L^-1 u_j = R delta_j (delta_j = H^-1 u_j)
+    OJBKQ_HIP(ojbkq::apply_linv(c->at<double>(c->L.Linv), U, gq, s.n, s.m, st), "solve");
   }
   stage_end(c, OJBKQ_STAGE_SOLVE, t0);
   t0 = stage_begin(c);
-  double* qbar = c->at<double>(c->L.qbar);
-  OJBKQ_HIP(ojbkq::launch_centres(W, cross ? U : nullptr, 1.0 - alpha, scales, zeros, s.n, s.m,
-                                  s.g, s.G, qbar, U, st),
-            "centres");
-  double* gq = c->at<double>(c->L.gq);
+  // Rbar_j qbar_j = R (s_j qbar_j) = R (w_j + s_j z_j) + (1 - mu) R delta_j:
+  // as rows, gq = (W + S Z) L + (1 - mu) gq
+  OJBKQ_HIP(ojbkq::launch_shifted_weights(W, scales, zeros, s.n, s.m, s.g, s.G, U, st),
+            "shifted weights");
   {
-    ojbkq::GemmDesc g;   // gq_j = Rbar_j qbar_j: gq[j][i] = sum_l Y[j][l] L[l][i]
+    ojbkq::GemmDesc g;   // gq[j][i] = sum_l A[j][l] L[l][i] + beta gq[j][i]
     g.M = s.n; g.N = s.m; g.Kd = s.m;
     g.A = U; g.lda = s.m; g.ta = ojbkq::Elt::F64;
     g.B = Lf; g.ldb = s.m; g.tb = ojbkq::Elt::F64; g.b_kmajor = true; g.b_zero_below_col = true;
-    g.C = gq; g.ldc = s.m;
+    g.C = gq; g.ldc = s.m; g.beta = cross ? 1.0 - alpha : 0.0;
     OJBKQ_HIP(ojbkq::gemm_f64(g, st), "Rbar qbar");
   }
   double* al = c->at<double>(c->L.alpha);
@@ -472,7 +470,7 @@ int ojbkq_inspect(ojbkq_ctx* ctx, int which, const void** ptr) {
   if (!ctx->solved) return fail(OJBKQ_ESTATE, "inspect before the first solve");
   switch (which) {
     case 0: *ptr = ctx->at<void>(ctx->L.G); break;
-    case 1: *ptr = ctx->at<void>(ctx->L.qbar); break;
+    case 1: *ptr = ctx->at<void>(ctx->L.gq); break;
     case 2: *ptr = ctx->at<void>(ctx->L.alpha); break;
     case 3: *ptr = ctx->at<void>(ctx->L.lam2); break;
     case 4: *ptr = ctx->at<void>(ctx->L.presid); break;
@@ -510,8 +508,7 @@ int ojbkq_decode_stage(const ojbkq_params* p, const double* R, const double* qba
   double* gq = reinterpret_cast<double*>(ws + L.gq);
   double* al = reinterpret_cast<double*>(ws + L.alpha);
   OJBKQ_HIP(ojbkq::launch_upper_to_lower(R, Lf, s.m, st), "transpose");
-  OJBKQ_HIP(ojbkq::launch_centres(nullptr, nullptr, 0.0, scales, nullptr, s.n, s.m, s.g, s.G,
-                                  const_cast<double*>(qbar), Y, st),
+  OJBKQ_HIP(ojbkq::launch_scale_centres(qbar, scales, s.n, s.m, s.g, s.G, Y, st),
             "scaled centres");
   {
     ojbkq::GemmDesc g;

@@ -7,7 +7,8 @@
 // factors and inverts each 64x64 diagonal block, the panel below it is one
 // GEMM with that inverse, and every trailing update is a call of the fp64
 // MFMA GEMM.  The solves use L^-1, formed once per factor by doubling from
-// the inverted diagonal blocks, so each is one triangular GEMM.
+// the inverted diagonal blocks, so the one substitution the path needs is a
+// triangular GEMM.
 #include "kernels.h"
 #include "device.h"
 
@@ -314,21 +315,14 @@ hipError_t invert_lower(const double* L, int64_t m, double* Linv, double* scratc
 
 // The two solves as two triangular GEMMs with L^-1 (row form, every row of
 // U a right-hand side): Y = U L^-T into T, then X = Y L^-1 into U.
-hipError_t solve_llt(const double* Linv, double* U, double* T, int64_t n, int64_t m,
-                     hipStream_t stream) {
+hipError_t apply_linv(const double* Linv, const double* U, double* Y, int64_t n, int64_t m,
+                      hipStream_t stream) {
   GemmDesc y;   // Y[i][c] = sum_k U[i][k] Linv[c][k], Linv[c][k] = 0 for k > c
   y.M = n; y.N = m; y.Kd = m;
   y.A = U; y.lda = m; y.ta = Elt::F64;
   y.B = Linv; y.ldb = m; y.tb = Elt::F64; y.b_zero_above_col = true;
-  y.C = T; y.ldc = m; y.alpha = 1.0; y.beta = 0.0;
-  hipError_t e = gemm_f64(y, stream);
-  if (e != hipSuccess) return e;
-  GemmDesc x;   // X[i][c] = sum_k Y[i][k] Linv[k][c], Linv[k][c] = 0 for k < c
-  x.M = n; x.N = m; x.Kd = m;
-  x.A = T; x.lda = m; x.ta = Elt::F64;
-  x.B = Linv; x.ldb = m; x.tb = Elt::F64; x.b_kmajor = true; x.b_zero_below_col = true;
-  x.C = U; x.ldc = m; x.alpha = 1.0; x.beta = 0.0;
-  return gemm_f64(x, stream);
+  y.C = Y; y.ldc = m; y.alpha = 1.0; y.beta = 0.0;
+  return gemm_f64(y, stream);
 }
 
 }  // namespace ojbkq

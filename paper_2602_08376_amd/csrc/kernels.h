@@ -87,16 +87,23 @@ hipError_t launch_upper_to_lower(const double* R, double* L, int64_t m, hipStrea
 // doubles.
 hipError_t invert_lower(const double* L, int64_t m, double* Linv, double* scratch,
                         hipStream_t stream);
-// Solves for n right-hand sides stored as rows of U [n, m] with Linv = L^-1:
-// y = L^-1 u, then x = L^-T y = H^-1 u, written to U; T [n, m] is scratch.
-hipError_t solve_llt(const double* Linv, double* U, double* T, int64_t n, int64_t m,
-                     hipStream_t stream);
+// The forward half of the solves for n right-hand sides stored as rows of
+// U [n, m], with Linv = L^-1: row j of Y [n, m] is L^-1 u_j, i.e. Y = U L^-T
+// (one triangular GEMM).
+hipError_t apply_linv(const double* Linv, const double* U, double* Y, int64_t n, int64_t m,
+                      hipStream_t stream);
 
 // ---- relaxed solution -> centres (Alg. 1 steps 3-5) ------------------------
-// qbar = (w + c * delta) / s + z (delta may be null), Y = s * qbar.
-hipError_t launch_centres(const float* W, const double* delta, double c, const float* S,
-                          const float* Z, int64_t n, int64_t m, int64_t g, int64_t G,
-                          double* qbar, double* Y, hipStream_t stream);
+// A = W + s * z in fp64 (s, z of each element's group): with Y = U L^-T, the
+// decoder's input Rbar_j qbar_j = R (s_j qbar_j) = R (w_j + (1 - mu) delta_j
+// + s_j z_j) is, as rows, A L + (1 - mu) Y, because R delta_j = R H^-1 u_j
+// = L^-1 u_j.  So the centres are never formed and the back substitution
+// L^-T (L^-1 u_j) is not needed.
+hipError_t launch_shifted_weights(const float* W, const float* S, const float* Z, int64_t n,
+                                  int64_t m, int64_t g, int64_t G, double* A, hipStream_t stream);
+// Y = s * qbar for given centres (the decoder-only entry point).
+hipError_t launch_scale_centres(const double* qbar, const float* S, int64_t n, int64_t m,
+                                int64_t g, int64_t G, double* Y, hipStream_t stream);
 // alpha_j = log_rho / min_i (L_ii s_j(i))^2.
 hipError_t launch_klein_alpha(const double* L, const float* S, int64_t n, int64_t m, int64_t g,
                               int64_t G, double log_rho, double* alpha, hipStream_t stream);

@@ -1,6 +1,7 @@
 // Per-group scales and zero points (Alg. 1 step 1; the Q, S, Z data model of
-// Sec. 3.2), the real centres qbar (Alg. 1 steps 3-4) and the per-column
-// Klein temperature (the alpha rule stated after Eq. klein_prob).
+// Sec. 3.2), the shifted weights w + s z that carry the real centres qbar of
+// Alg. 1 steps 3-4 into the decoder's Rbar qbar, and the per-column Klein
+// temperature (the alpha rule stated after Eq. klein_prob).
 #include "kernels.h"
 #include "device.h"
 
@@ -45,27 +46,19 @@ __global__ __launch_bounds__(256) void scale_zero_kernel(const float* __restrict
 }
 
 // qbar = (w + c * delta) / s + z and Y = s * qbar, elementwise over [n, m].
-__global__ __launch_bounds__(256) void centres_kernel(const float* __restrict__ W,
-                                                      const double* delta, double c,
-                                                      const float* __restrict__ S,
-                                                      const float* __restrict__ Z, int64_t n,
-                                                      int64_t m, int64_t g, int64_t G,
-                                                      double* __restrict__ qbar, double* Y) {
+__global__ __launch_bounds__(256) void shifted_weights_kernel(const float* __restrict__ W,
+                                                              const float* __restrict__ S,
+                                                              const float* __restrict__ Z,
+                                                              int64_t n, int64_t m, int64_t g,
+                                                              int64_t G, double* __restrict__ A) {
   const int64_t total = n * m;
   for (int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x; idx < total;
        idx += (int64_t)gridDim.x * 256) {
     const int64_t j = idx / m, l = idx % m;
     const int64_t sg = j * G + l / g;
-    const double s = (double)S[sg];
-    double v = (double)W[idx];
-    if (delta) v += c * delta[idx];
-    const double qb = v / s + (double)Z[sg];
-    qbar[idx] = qb;
-    Y[idx] = s * qb;
+    A[idx] = (double)W[idx] + (double)S[sg] * (double)Z[sg];   // s * z is exact in fp64
   }
 }
-
-// Y = s * qbar for a given qbar (decode-only entry).
 __global__ __launch_bounds__(256) void scale_centres_kernel(const double* __restrict__ qbar,
                                                             const float* __restrict__ S, int64_t n,
                                                             int64_t m, int64_t g, int64_t G,
@@ -116,14 +109,15 @@ hipError_t launch_scale_zero(const float* W, int64_t n, int64_t m, int64_t g, in
   return hipGetLastError();
 }
 
-hipError_t launch_centres(const float* W, const double* delta, double c, const float* S,
-                          const float* Z, int64_t n, int64_t m, int64_t g, int64_t G,
-                          double* qbar, double* Y, hipStream_t stream) {
-  if (W == nullptr) {
-    scale_centres_kernel<<<grid_for(n * m), 256, 0, stream>>>(qbar, S, n, m, g, G, Y);
-  } else {
-    centres_kernel<<<grid_for(n * m), 256, 0, stream>>>(W, delta, c, S, Z, n, m, g, G, qbar, Y);
-  }
+hipError_t launch_shifted_weights(const float* W, const float* S, const float* Z, int64_t n,
+                                  int64_t m, int64_t g, int64_t G, double* A, hipStream_t stream) {
+  shifted_weights_kernel<<<grid_for(n * m), 256, 0, stream>>>(W, S, Z, n, m, g, G, A);
+  return hipGetLastError();
+}
+
+hipError_t launch_scale_centres(const double* qbar, const float* S, int64_t n, int64_t m,
+                                int64_t g, int64_t G, double* Y, hipStream_t stream) {
+  scale_centres_kernel<<<grid_for(n * m), 256, 0, stream>>>(qbar, S, n, m, g, G, Y);
   return hipGetLastError();
 }
 

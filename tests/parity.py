@@ -31,6 +31,20 @@ def np64(t):
     return t.detach().cpu().numpy()
 
 
+def centres_from_gq(L, gq_rows, S_rows, group):
+    """The real centres behind the decoder's input rows.
+
+    Row j of gq is Rbar_j qbar_j = R (s_j qbar_j) written as a row,
+    (s_j qbar_j)^T L with L = R^T; so s_j qbar_j = L^-T gq_j (one host
+    triangular solve per row) and qbar_j follows by dividing by the scales.
+    """
+    import scipy.linalg
+    m = L.shape[0]
+    v = scipy.linalg.solve_triangular(L, np.asarray(gq_rows, dtype=np.float64).T, lower=True,
+                                      trans="T", check_finite=False).T
+    return v / orc.expand_groups(S_rows, m, group)
+
+
 def _pick_range(c, kappa, u, qmax):
     """Set of codes reachable by moving c within the tie band or u within U_BAND."""
     picks = set()

@@ -19,7 +19,7 @@ import torch
 
 import paper_2602_08376_amd as ok
 from oracle import ojbkq as orc
-from parity import check_residuals, first_divergence_is_tie, np64
+from parity import centres_from_gq, check_residuals, first_divergence_is_tie, np64
 from synth import CONFIGS
 from synth.workloads import activation_chunks, make_weights
 
@@ -45,7 +45,7 @@ def test_attention_projection_full_size():
     s.accumulate(Xr, Xq)
     g = s.solve(W, cfg.mu)
     L = np64(s.inspect("L"))
-    qbar_g = np64(s.inspect("qbar"))
+    gq_g = np64(s.inspect("gq"))
     alpha_g = np64(s.inspect("alpha"))
     lam2_g = float(s.inspect("lam2")[0])
     pres_g = np64(s.inspect("path_resid"))
@@ -80,7 +80,8 @@ def test_attention_projection_full_size():
     errR = float(np.max(np.abs(L.T - R) / colnorm[None, :]))
     assert errR < 1e-9, errR
     # centres and temperatures of the sample
-    errq = float(np.max(np.abs(qbar_g[cols] - qb)))
+    qbar_g = centres_from_gq(L, gq_g[cols], np64(g.scales)[cols], cfg.group)
+    errq = float(np.max(np.abs(qbar_g - qb)))
     assert errq < 1e-6, errq
     assert np.allclose(alpha_g[cols], dec.alpha, rtol=1e-9)
     # codes: the winners' code vectors; a differing one must start at a near-tie
@@ -114,7 +115,7 @@ def test_attention_projection_full_size():
 #   * the factor: sampled entries of L L^T - lambda^2 I against the oracle's
 #     Gram of the two rows (exact fp64 dot products over all tokens);
 #   * the centres: for sampled columns the relaxed solution v (recovered from
-#     qbar, s, z) satisfies the normal equations of the stacked problem
+#     the decoder's input Rbar qbar, s, z) satisfies the normal equations of the stacked problem
 #     (Eq. new_obj): (X~^T X~ + lambda^2 I) v = X~^T y*(mu) + lambda^2 w,
 #     both sides formed on the host chunk by chunk;
 #   * the decode: for sampled columns the oracle decodes every candidate
@@ -167,11 +168,15 @@ def test_full_size_sampled(key):
             scale = np.sqrt(diag[i] * diag[j])
             assert abs(h - gpairs[p]) <= 1e-11 * scale, (key, i, j, h, gpairs[p])
         # centres: normal equations of the stacked problem for sampled columns
-        qbar_g = s.inspect("qbar")
+        gq_g = s.inspect("gq")
+        R = np64(Lg).T.copy()
+        del Lg
         cols = np.sort(rng.choice(cfg.n, n_cent, replace=False))
         Sx = orc.expand_groups(S[cols], cfg.m, cfg.group)
         Zx = orc.expand_groups(Z[cols], cfg.m, cfg.group)
-        V = ((np64(qbar_g[torch.as_tensor(cols, device=dev)]) - Zx) * Sx).T   # [m, c]
+        qbar_c = centres_from_gq(R.T, np64(gq_g[torch.as_tensor(cols, device=dev)]), S[cols],
+                                 cfg.group)
+        V = ((qbar_c - Zx) * Sx).T   # [m, c]
         Wc = Wn[cols].astype(np.float64).T
         lhs = lam2_g * V
         rhs = lam2_g * Wc
@@ -185,8 +190,6 @@ def test_full_size_sampled(key):
               f"{[f'{x:.2e}' for x in rel]}", flush=True)
         assert float(rel.max()) < 1e-9, (key, mu, rel)
         # decode: oracle candidates on the GPU's R and qbar for sampled columns
-        R = np64(Lg).T.copy()
-        del Lg
         alpha_g = np64(s.inspect("alpha"))
         pres_g = np64(s.inspect("path_resid"))
         codes_g, win_g = np64(g.codes), np64(g.winner)
@@ -194,7 +197,8 @@ def test_full_size_sampled(key):
         dcols = np.sort(rng.choice(cfg.n, n_dec, replace=False))
         for jcol in dcols:
             sx = orc.expand_groups(S[jcol:jcol + 1], cfg.m, cfg.group)[0]
-            qb = np64(qbar_g[int(jcol)])
+            qb = centres_from_gq(R.T, np64(gq_g[int(jcol):int(jcol) + 1]), S[jcol:jcol + 1],
+                                 cfg.group)[0]
             alpha_o = lr / float(np.min((np.diag(R) * sx) ** 2))
             assert abs(alpha_g[jcol] - alpha_o) <= 1e-12 * alpha_o
             Q = orc.decode_column(R, qb, sx, cfg.bits, cfg.K, alpha_o, cfg.klein_seed, int(jcol))

@@ -15,7 +15,7 @@ import torch
 
 import paper_2602_08376_amd as ok
 from oracle import ojbkq as orc
-from parity import (SCALE_RTOL, check_paths, check_residuals, np64)
+from parity import (SCALE_RTOL, centres_from_gq, check_paths, check_residuals, np64)
 from synth import CONFIGS, LayerConfig, make_layer, make_triangular_problem
 
 pytestmark = pytest.mark.gpu
@@ -204,7 +204,15 @@ def test_staged_intermediates_and_chunks():
     assert errR < 1e-10, errR
     lam2 = float(s.inspect("lam2")[0])
     assert abs(lam2 - o.lam2) <= 1e-12 * o.lam2
-    qb = np64(s.inspect("qbar"))
+    # the decoder's input rows Rbar_j qbar_j against the oracle's centres and
+    # factor, and the centres recovered from them
+    gq = np64(s.inspect("gq"))
+    Sx = orc.expand_groups(o.scales, cfg.m, cfg.group)
+    gq_o = (Sx * o.qbar) @ o.R.T
+    gq_scale = np.abs(Sx * o.qbar) @ np.abs(o.R.T)
+    errg = np.max(np.abs(gq - gq_o) / gq_scale)
+    assert errg < 1e-10, errg
+    qb = centres_from_gq(L, gq, o.scales, cfg.group)
     errq = np.max(np.abs(qb - o.qbar))
     assert errq < 1e-7, errq
     al = np64(s.inspect("alpha"))
