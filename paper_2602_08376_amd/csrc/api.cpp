@@ -61,7 +61,8 @@ Shape shape_of(const ojbkq_params& p) {
 // Offsets of every buffer carved from the workspace.
 struct Layout {
   size_t status = 0, lam2 = 0, G = 0, E = 0, U = 0, gq = 0, alpha = 0, pcodes = 0,
-         presid = 0, gc_scratch = 0, gc_tiles = 0, F = 0, Linv = 0, total = 0;
+         presid = 0, gc_scratch = 0, gc_tiles = 0, F = 0, Linv = 0, Q = 0, Lsum = 0, SZ = 0,
+         total = 0;
 };
 
 Layout layout_full(const Shape& s) {
@@ -78,7 +79,6 @@ Layout layout_full(const Shape& s) {
   L.lam2 = take(sizeof(double));
   L.G = take(mm);
   L.E = take(mm);
-  L.U = take(nm);
   L.gq = take(nm);
   L.alpha = take((size_t)s.n * sizeof(double));
   L.pcodes = take((size_t)ojbkq::decode_code_bytes(s.m, s.geo));
@@ -87,6 +87,9 @@ Layout layout_full(const Shape& s) {
   L.gc_tiles = take((size_t)ojbkq::gram_tile_count(s.m) * sizeof(uint32_t));
   L.F = take((size_t)ojbkq::decode_tile_count(s.m) * ojbkq::kDecodeTile * sizeof(double));
   L.Linv = take(mm);
+  L.Q = take(mm);
+  L.Lsum = take((size_t)s.G * (size_t)s.m * sizeof(double));
+  L.SZ = take((size_t)s.n * (size_t)s.G * sizeof(double));
   L.total = off;
   return L;
 }
@@ -324,37 +327,52 @@ int ctx_solve(ojbkq_ctx* c, const float* W, double alpha, uint8_t* codes, float*
     OJBKQ_HIP(ojbkq::invert_lower(Lf, s.m, c->at<double>(c->L.Linv), c->at<double>(c->L.F), st),
               "factor inverse");
     OJBKQ_HIP(ojbkq::launch_decode_tiles(Lf, s.m, c->at<double>(c->L.F), st), "decoder tiles");
+    OJBKQ_HIP(ojbkq::launch_group_row_sums(Lf, s.m, s.g, s.G, c->at<double>(c->L.Lsum), st),
+              "group sums");
     c->factored = true;
     stage_end(c, OJBKQ_STAGE_FACTOR, t0);
     t0 = stage_begin(c);
   }
   OJBKQ_HIP(ojbkq::launch_scale_zero(W, s.n, s.m, s.g, s.G, s.qmax, scales, zeros, st),
             "scales");
-  double* U = c->at<double>(c->L.U);
   double* gq = c->at<double>(c->L.gq);
   const bool cross = c->cross_seen && alpha != 1.0;
+  const double* Q = Lf;
   if (cross) {
-    ojbkq::GemmDesc g;   // U = W E^T: row j is X~^T (X - X~) w_j
+    // Q = L + (1 - mu) (L^-1 E)^T: C = L, then C += (1 - mu) E^T L^-T
+    double* Qw = c->at<double>(c->L.Q);
+    OJBKQ_HIP(hipMemcpyAsync(Qw, Lf, (size_t)s.m * s.m * sizeof(double), hipMemcpyDeviceToDevice,
+                             st),
+              "copy factor");
+    ojbkq::GemmDesc g;   // C[i][j] += (1 - mu) sum_k E[k][i] Linv[j][k], Linv[j][k] = 0 for k > j
+    g.M = s.m; g.N = s.m; g.Kd = s.m;
+    g.A = c->at<double>(c->L.E); g.lda = s.m; g.ta = ojbkq::Elt::F64; g.a_kmajor = true;
+    g.B = c->at<double>(c->L.Linv); g.ldb = s.m; g.tb = ojbkq::Elt::F64;
+    g.b_zero_above_col = true;
+    g.C = Qw; g.ldc = s.m; g.alpha = 1.0 - alpha; g.beta = 1.0;
+    OJBKQ_HIP(ojbkq::gemm_f64(g, st), "relaxed-solution operator");
+    Q = Qw;
+  }
+  {
+    ojbkq::GemmDesc g;   // gq[j][i] = sum_l W[j][l] Q[l][i]
     g.M = s.n; g.N = s.m; g.Kd = s.m;
     g.A = W; g.lda = s.m; g.ta = ojbkq::Elt::F32;
-    g.B = c->at<double>(c->L.E); g.ldb = s.m; g.tb = ojbkq::Elt::F64;
-    g.C = U; g.ldc = s.m;
-    OJBKQ_HIP(ojbkq::gemm_f64(g, st), "target projection");
-    // gq <- U L^-T: row j is L^-1 u_j = R delta_j (delta_j = H^-1 u_j)
-    OJBKQ_HIP(ojbkq::apply_linv(c->at<double>(c->L.Linv), U, gq, s.n, s.m, st), "solve");
+    g.B = Q; g.ldb = s.m; g.tb = ojbkq::Elt::F64; g.b_kmajor = true;
+    g.b_zero_below_col = !cross;   // Q = L is lower triangular
+    g.C = gq; g.ldc = s.m;
+    OJBKQ_HIP(ojbkq::gemm_f64(g, st), "W Q");
   }
   stage_end(c, OJBKQ_STAGE_SOLVE, t0);
   t0 = stage_begin(c);
-  // Rbar_j qbar_j = R (s_j qbar_j) = R (w_j + s_j z_j) + (1 - mu) R delta_j:
-  // as rows, gq = (W + S Z) L + (1 - mu) gq
-  OJBKQ_HIP(ojbkq::launch_shifted_weights(W, scales, zeros, s.n, s.m, s.g, s.G, U, st),
-            "shifted weights");
   {
-    ojbkq::GemmDesc g;   // gq[j][i] = sum_l A[j][l] L[l][i] + beta gq[j][i]
-    g.M = s.n; g.N = s.m; g.Kd = s.m;
-    g.A = U; g.lda = s.m; g.ta = ojbkq::Elt::F64;
-    g.B = Lf; g.ldb = s.m; g.tb = ojbkq::Elt::F64; g.b_kmajor = true; g.b_zero_below_col = true;
-    g.C = gq; g.ldc = s.m; g.beta = cross ? 1.0 - alpha : 0.0;
+    // gq += (S Z) Lsum: the zero points' share of Rbar qbar
+    double* SZ = c->at<double>(c->L.SZ);
+    OJBKQ_HIP(ojbkq::launch_scale_zero_products(scales, zeros, s.n, s.G, SZ, st), "s z");
+    ojbkq::GemmDesc g;
+    g.M = s.n; g.N = s.m; g.Kd = s.G;
+    g.A = SZ; g.lda = s.G; g.ta = ojbkq::Elt::F64;
+    g.B = c->at<double>(c->L.Lsum); g.ldb = s.m; g.tb = ojbkq::Elt::F64; g.b_kmajor = true;
+    g.C = gq; g.ldc = s.m; g.beta = 1.0;
     OJBKQ_HIP(ojbkq::gemm_f64(g, st), "Rbar qbar");
   }
   double* al = c->at<double>(c->L.alpha);

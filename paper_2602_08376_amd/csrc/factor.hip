@@ -6,9 +6,8 @@
 // contiguous.  Right-looking blocked Cholesky with 64-wide panels: one wave
 // factors and inverts each 64x64 diagonal block, the panel below it is one
 // GEMM with that inverse, and every trailing update is a call of the fp64
-// MFMA GEMM.  The solves use L^-1, formed once per factor by doubling from
-// the inverted diagonal blocks, so the one substitution the path needs is a
-// triangular GEMM.
+// MFMA GEMM.  The solve uses L^-1, formed once per factor by doubling from
+// the inverted diagonal blocks, so it is a triangular GEMM.
 #include "kernels.h"
 #include "device.h"
 
@@ -315,14 +314,4 @@ hipError_t invert_lower(const double* L, int64_t m, double* Linv, double* scratc
 
 // The two solves as two triangular GEMMs with L^-1 (row form, every row of
 // U a right-hand side): Y = U L^-T into T, then X = Y L^-1 into U.
-hipError_t apply_linv(const double* Linv, const double* U, double* Y, int64_t n, int64_t m,
-                      hipStream_t stream) {
-  GemmDesc y;   // Y[i][c] = sum_k U[i][k] Linv[c][k], Linv[c][k] = 0 for k > c
-  y.M = n; y.N = m; y.Kd = m;
-  y.A = U; y.lda = m; y.ta = Elt::F64;
-  y.B = Linv; y.ldb = m; y.tb = Elt::F64; y.b_zero_above_col = true;
-  y.C = Y; y.ldc = m; y.alpha = 1.0; y.beta = 0.0;
-  return gemm_f64(y, stream);
-}
-
 }  // namespace ojbkq

@@ -281,7 +281,7 @@ hipError_t gemm_f64(const GemmDesc& d, hipStream_t stream) {
   g.sa = d.stride_a; g.sb = d.stride_b; g.sc = d.stride_c;
   g.batch = d.batch;
   if (d.batch < 1 || d.batch > 65535 || (d.batch > 1 && d.B2 != nullptr)) return hipErrorInvalidValue;
-  g.vec_a = vec_ok(d.A, d.lda, d.ta) ? 1 : 0;
+  g.vec_a = vec_ok(d.A, d.lda, d.ta) ? 1 : 0;   // rows (or, k-major, k rows) of 16-byte runs
   g.vec_b = (vec_ok(d.B, d.ldb, d.tb) && (d.B2 == nullptr || vec_ok(d.B2, d.ldb, d.tb))) ? 1 : 0;
   if (d.lower_tiles && g.tiles_m != g.tiles_n) return hipErrorInvalidValue;
   const int64_t ntiles = d.lower_tiles ? g.tiles_m * (g.tiles_m + 1) / 2 : g.tiles_m * g.tiles_n;
@@ -296,8 +296,12 @@ hipError_t gemm_f64(const GemmDesc& d, hipStream_t stream) {
     return launch<double, double, false, false, false>(g, ntiles, stream);
   if (d.ta == Elt::F64 && d.tb == Elt::F64 && !d.a_kmajor && d.b_kmajor)
     return launch<double, double, false, true, false>(g, ntiles, stream);
+  if (d.ta == Elt::F64 && d.tb == Elt::F64 && d.a_kmajor && !d.b_kmajor)
+    return launch<double, double, true, false, false>(g, ntiles, stream);
   if (d.ta == Elt::F32 && d.tb == Elt::F64 && !d.a_kmajor && !d.b_kmajor)
     return launch<float, double, false, false, false>(g, ntiles, stream);
+  if (d.ta == Elt::F32 && d.tb == Elt::F64 && !d.a_kmajor && d.b_kmajor)
+    return launch<float, double, false, true, false>(g, ntiles, stream);
   return hipErrorInvalidValue;
 }
 

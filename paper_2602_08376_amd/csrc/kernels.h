@@ -87,20 +87,22 @@ hipError_t launch_upper_to_lower(const double* R, double* L, int64_t m, hipStrea
 // doubles.
 hipError_t invert_lower(const double* L, int64_t m, double* Linv, double* scratch,
                         hipStream_t stream);
-// The forward half of the solves for n right-hand sides stored as rows of
-// U [n, m], with Linv = L^-1: row j of Y [n, m] is L^-1 u_j, i.e. Y = U L^-T
-// (one triangular GEMM).
-hipError_t apply_linv(const double* Linv, const double* U, double* Y, int64_t n, int64_t m,
-                      hipStream_t stream);
 
 // ---- relaxed solution -> centres (Alg. 1 steps 3-5) ------------------------
-// A = W + s * z in fp64 (s, z of each element's group): with Y = U L^-T, the
-// decoder's input Rbar_j qbar_j = R (s_j qbar_j) = R (w_j + (1 - mu) delta_j
-// + s_j z_j) is, as rows, A L + (1 - mu) Y, because R delta_j = R H^-1 u_j
-// = L^-1 u_j.  So the centres are never formed and the back substitution
-// L^-T (L^-1 u_j) is not needed.
-hipError_t launch_shifted_weights(const float* W, const float* S, const float* Z, int64_t n,
-                                  int64_t m, int64_t g, int64_t G, double* A, hipStream_t stream);
+// The decoder's input Rbar_j qbar_j = R (s_j qbar_j) = R (w_j + (1 - mu)
+// delta_j + s_j z_j) with delta_j = H^-1 E w_j, so R delta_j = L^-1 E w_j
+// and, as rows over all columns j,
+//   gq = W Q + (S Z) Lsum,   Q = L + (1 - mu) (L^-1 E)^T,
+// where Lsum [G, m] holds the sums of L's rows over each group of g rows and
+// (S Z) [n, G] the products s z per (column, group).  Q does not depend on
+// W, so a mu sweep or a second weight matrix reuses it; the centres qbar are
+// never formed.
+// Lsum[t][i] = sum over rows l of group t of L[l][i].
+hipError_t launch_group_row_sums(const double* L, int64_t m, int64_t g, int64_t G, double* Lsum,
+                                 hipStream_t stream);
+// SZ[j][t] = S[j][t] * Z[j][t] in fp64 (exact: z is a small integer).
+hipError_t launch_scale_zero_products(const float* S, const float* Z, int64_t n, int64_t G,
+                                      double* SZ, hipStream_t stream);
 // Y = s * qbar for given centres (the decoder-only entry point).
 hipError_t launch_scale_centres(const double* qbar, const float* S, int64_t n, int64_t m,
                                 int64_t g, int64_t G, double* Y, hipStream_t stream);

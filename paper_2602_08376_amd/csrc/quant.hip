@@ -1,7 +1,7 @@
 // Per-group scales and zero points (Alg. 1 step 1; the Q, S, Z data model of
-// Sec. 3.2), the shifted weights w + s z that carry the real centres qbar of
-// Alg. 1 steps 3-4 into the decoder's Rbar qbar, and the per-column Klein
-// temperature (the alpha rule stated after Eq. klein_prob).
+// Sec. 3.2), the group sums that carry the zero-point part of the real
+// centres qbar (Alg. 1 steps 3-4) into the decoder's Rbar qbar, and the
+// per-column Klein temperature (the alpha rule stated after Eq. klein_prob).
 #include "kernels.h"
 #include "device.h"
 
@@ -46,18 +46,28 @@ __global__ __launch_bounds__(256) void scale_zero_kernel(const float* __restrict
 }
 
 // qbar = (w + c * delta) / s + z and Y = s * qbar, elementwise over [n, m].
-__global__ __launch_bounds__(256) void shifted_weights_kernel(const float* __restrict__ W,
-                                                              const float* __restrict__ S,
-                                                              const float* __restrict__ Z,
-                                                              int64_t n, int64_t m, int64_t g,
-                                                              int64_t G, double* __restrict__ A) {
-  const int64_t total = n * m;
-  for (int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x; idx < total;
-       idx += (int64_t)gridDim.x * 256) {
-    const int64_t j = idx / m, l = idx % m;
-    const int64_t sg = j * G + l / g;
-    A[idx] = (double)W[idx] + (double)S[sg] * (double)Z[sg];   // s * z is exact in fp64
+// One thread per column i of L and group t: a strided walk down g rows.
+__global__ __launch_bounds__(256) void group_row_sums_kernel(const double* __restrict__ L,
+                                                             int64_t m, int64_t g, int64_t G,
+                                                             double* __restrict__ Lsum) {
+  for (int64_t t = blockIdx.y; t < G; t += gridDim.y) {
+    const int64_t l0 = t * g, l1 = (l0 + g < m) ? l0 + g : m;
+    for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < m;
+         i += (int64_t)gridDim.x * 256) {
+      double s = 0.0;
+      for (int64_t l = (l0 > i ? l0 : i); l < l1; ++l) s += L[l * m + i];   // L[l][i] = 0 for l < i
+      Lsum[t * m + i] = s;
+    }
   }
+}
+
+__global__ __launch_bounds__(256) void scale_zero_products_kernel(const float* __restrict__ S,
+                                                                  const float* __restrict__ Z,
+                                                                  int64_t count,
+                                                                  double* __restrict__ SZ) {
+  for (int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x; e < count;
+       e += (int64_t)gridDim.x * 256)
+    SZ[e] = (double)S[e] * (double)Z[e];
 }
 __global__ __launch_bounds__(256) void scale_centres_kernel(const double* __restrict__ qbar,
                                                             const float* __restrict__ S, int64_t n,
@@ -109,9 +119,18 @@ hipError_t launch_scale_zero(const float* W, int64_t n, int64_t m, int64_t g, in
   return hipGetLastError();
 }
 
-hipError_t launch_shifted_weights(const float* W, const float* S, const float* Z, int64_t n,
-                                  int64_t m, int64_t g, int64_t G, double* A, hipStream_t stream) {
-  shifted_weights_kernel<<<grid_for(n * m), 256, 0, stream>>>(W, S, Z, n, m, g, G, A);
+hipError_t launch_group_row_sums(const double* L, int64_t m, int64_t g, int64_t G, double* Lsum,
+                                 hipStream_t stream) {
+  const int64_t bx = (m + 255) / 256;
+  const int64_t by = G < 65535 ? G : 65535;
+  group_row_sums_kernel<<<dim3((unsigned)(bx < 1024 ? bx : 1024), (unsigned)by), 256, 0, stream>>>(
+      L, m, g, G, Lsum);
+  return hipGetLastError();
+}
+
+hipError_t launch_scale_zero_products(const float* S, const float* Z, int64_t n, int64_t G,
+                                      double* SZ, hipStream_t stream) {
+  scale_zero_products_kernel<<<grid_for(n * G), 256, 0, stream>>>(S, Z, n * G, SZ);
   return hipGetLastError();
 }
 

@@ -114,9 +114,9 @@ def test_null_and_shape_errors_before_any_launch():
 def test_workspace_size_grows_with_shape():
     small = ok.workspace_bytes(128, 64, 4, 128, 4)
     big = ok.workspace_bytes(4096, 4096, 4, 128, 16)
-    # G, E and L^-1 (m^2 doubles each), two n*m double arrays, codes of n(K+1) padded paths
+    # G, E, L^-1 and Q (m^2 doubles each), one n*m double array, codes of n(K+1) padded paths
     paths = ((4096 * 17 + 255) // 256) * 256
-    assert big >= 3 * 4096 * 4096 * 8 + 2 * 4096 * 4096 * 8 + paths * 4096
+    assert big >= 4 * 4096 * 4096 * 8 + 4096 * 4096 * 8 + paths * 4096
     assert small < big
 
 
