@@ -2,8 +2,8 @@
 """Benchmark of the per-layer OJBKQ quantisation path on one MI355X.
 
 One step = the whole path for one layer: Gram and cross term over every
-calibration token, damping, Cholesky, the two triangular solves, centres,
-Klein temperatures, the batched Babai + K Klein decode of every column and
+calibration token, damping, Cholesky and L^-1, the relaxed solution folded
+into the decoder's input Rbar qbar, Klein temperatures, the batched Babai + K Klein decode of every column and
 the selection, with the synthetic inputs already resident in HBM.
 
 Default workload: the Llama-7B-shaped attention projection, W 4096 x 4096

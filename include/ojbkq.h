@@ -15,8 +15,11 @@
  *   target        Y*(mu) = (1 - mu) X W + mu X~ W (Eq. jta_target); the real
  *                 least-squares solution v_j of the stacked problem
  *                 (Eq. new_obj) is w_j + (1 - mu) H^-1 X~^T (X - X~) w_j,
- *                 found with two triangular solves (Alg. 1 step 3), and the
- *                 real centre is qbar_j = v_j / s_j + z_j (Alg. 1 step 4).
+ *                 (Alg. 1 step 3), and the real centre is
+ *                 qbar_j = v_j / s_j + z_j (Alg. 1 step 4).  The library
+ *                 reaches the same decode without forming either: the
+ *                 decoder needs only Rbar_j qbar_j = R (w_j + s_j z_j) +
+ *                 (1 - mu) L^-1 X~^T (X - X~) w_j, with L = R^T.
  *   decode        per column j, K + 1 candidate code vectors against the
  *                 shared factor: candidate 0 is the box-clamped Babai
  *                 nearest-plane point (Alg. 1 steps 6-10), candidates 1..K

@@ -312,6 +312,4 @@ hipError_t invert_lower(const double* L, int64_t m, double* Linv, double* scratc
   return hipSuccess;
 }
 
-// The two solves as two triangular GEMMs with L^-1 (row form, every row of
-// U a right-hand side): Y = U L^-T into T, then X = Y L^-1 into U.
 }  // namespace ojbkq
