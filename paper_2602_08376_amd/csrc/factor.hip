@@ -53,12 +53,6 @@ __device__ __forceinline__ double rsqrt_f64(double d) {
   return y;
 }
 
-__device__ __forceinline__ double lane_value(double v, int lane) {
-  const int lo = __builtin_amdgcn_readlane(__double2loint(v), lane);
-  const int hi = __builtin_amdgcn_readlane(__double2hiint(v), lane);
-  return __hiloint2double(hi, lo);
-}
-
 // Cholesky of the nbk x nbk diagonal block starting at (k0, k0), by one
 // wave, followed by the inverse of the factored block, written to Linv at
 // (k0, k0).  The block lives in LDS column-major (padded to 64 x 64 with the
