@@ -1,13 +1,14 @@
-// Damping, blocked Cholesky and blocked triangular solves in fp64 (Alg. 1
-// steps 2-3: H = X~^T X~ + lambda^2 I = R^T R, then R^T u = A^T t, R v = u).
+// Damping, blocked Cholesky and the explicit inverse of the factor in fp64
+// (Alg. 1 step 2, H = X~^T X~ + lambda^2 I = R^T R; the solves of step 3 are
+// products with L^-1, R^-1 = L^-T).
 //
 // The factor is kept as L = R^T, lower triangular, row-major: row f of L is
 // column f of R, so the decoder's reads of R[i][f] over a block of rows i are
 // contiguous.  Right-looking blocked Cholesky with 64-wide panels: one wave
 // factors and inverts each 64x64 diagonal block, the panel below it is one
 // GEMM with that inverse, and every trailing update is a call of the fp64
-// MFMA GEMM.  The solve uses L^-1, formed once per factor by doubling from
-// the inverted diagonal blocks, so it is a triangular GEMM.
+// MFMA GEMM.  L^-1 is formed once per factor by doubling from the inverted
+// diagonal blocks.
 #include "kernels.h"
 #include "device.h"
 
