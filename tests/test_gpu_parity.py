@@ -276,6 +276,30 @@ def test_alpha_sweep_reuses_factor():
     s.close()
 
 
+def test_degenerate_groups_and_channels():
+    """Weight groups that are all zero, all positive or all negative, two equal
+    columns, and a dead input channel (zero Gram row: only the damping keeps
+    H positive definite)."""
+    cfg = small_cfg(160, 24, 600, 4, 32, 6, 71)
+    W, Xr, Xq = make_layer(cfg, device=DEV)
+    W[0, :32] = 0.0
+    W[1, 32:64] = W[1, 32:64].abs()
+    W[2] = -W[2].abs()
+    W[4] = W[3]
+    Xr[5] = 0.0
+    Xq[5] = 0.0
+    g = ok.quantize_layer(W, Xr, Xq, 0.5, cfg.bits, cfg.group, cfg.K, cfg.klein_seed)
+    torch.cuda.synchronize()
+    o = orc.quantize_layer(np64(W), np64(Xr), np64(Xq), 0.5, cfg.bits, cfg.group, cfg.K,
+                           cfg.klein_seed)
+    assert check_layer(cfg, g, o, 0.5) >= 0.999
+    # the degenerate group's grid is [-1, 1]: zero point in the middle of the box
+    assert float(g.scales[0, 0]) == float(o.scales[0, 0]) == float(np.float32(2.0 / 15.0))
+    assert float(g.zeros[0, 0]) == float(o.zeros[0, 0])
+    # equal columns share scales and zero points
+    assert torch.equal(g.scales[3], g.scales[4]) and torch.equal(g.zeros[3], g.zeros[4])
+
+
 def test_same_activations_make_mu_irrelevant():
     cfg = small_cfg(96, 12, 300, 4, 32, 4, 51)
     W, _, Xq = make_layer(cfg, device=DEV)
