@@ -58,6 +58,12 @@ Shape shape_of(const ojbkq_params& p) {
   return s;
 }
 
+// Rbar qbar = W Q + (S Z) Lsum with Q = L + (1 - mu) (L^-1 E)^T costs m^3/2
+// + n m^2 multiply-adds; the direct route W L + (1 - mu) (W E^T) L^-T +
+// (S Z) Lsum costs 2 n m^2.  The first is cheaper once n > m / 2 (and for a
+// mu sweep, which repeats only the n m^2 part).
+inline bool route_q(const Shape& s) { return 2 * s.n > s.m; }
+
 // Offsets of every buffer carved from the workspace.
 struct Layout {
   size_t status = 0, lam2 = 0, G = 0, E = 0, U = 0, gq = 0, alpha = 0, pcodes = 0,
@@ -87,7 +93,10 @@ Layout layout_full(const Shape& s) {
   L.gc_tiles = take((size_t)ojbkq::gram_tile_count(s.m) * sizeof(uint32_t));
   L.F = take((size_t)ojbkq::decode_tile_count(s.m) * ojbkq::kDecodeTile * sizeof(double));
   L.Linv = take(mm);
-  L.Q = take(mm);
+  if (route_q(s))
+    L.Q = take(mm);
+  else
+    L.U = take(nm);
   L.Lsum = take((size_t)s.G * (size_t)s.m * sizeof(double));
   L.SZ = take((size_t)s.n * (size_t)s.G * sizeof(double));
   L.total = off;
@@ -337,23 +346,23 @@ int ctx_solve(ojbkq_ctx* c, const float* W, double alpha, uint8_t* codes, float*
             "scales");
   double* gq = c->at<double>(c->L.gq);
   const bool cross = c->cross_seen && alpha != 1.0;
-  const double* Q = Lf;
-  if (cross) {
-    // Q = L + (1 - mu) (L^-1 E)^T: C = L, then C += (1 - mu) E^T L^-T
-    double* Qw = c->at<double>(c->L.Q);
-    OJBKQ_HIP(hipMemcpyAsync(Qw, Lf, (size_t)s.m * s.m * sizeof(double), hipMemcpyDeviceToDevice,
-                             st),
-              "copy factor");
-    ojbkq::GemmDesc g;   // C[i][j] += (1 - mu) sum_k E[k][i] Linv[j][k], Linv[j][k] = 0 for k > j
-    g.M = s.m; g.N = s.m; g.Kd = s.m;
-    g.A = c->at<double>(c->L.E); g.lda = s.m; g.ta = ojbkq::Elt::F64; g.a_kmajor = true;
-    g.B = c->at<double>(c->L.Linv); g.ldb = s.m; g.tb = ojbkq::Elt::F64;
-    g.b_zero_above_col = true;
-    g.C = Qw; g.ldc = s.m; g.alpha = 1.0 - alpha; g.beta = 1.0;
-    OJBKQ_HIP(ojbkq::gemm_f64(g, st), "relaxed-solution operator");
-    Q = Qw;
-  }
-  {
+  if (route_q(s)) {
+    const double* Q = Lf;
+    if (cross) {
+      // Q = L + (1 - mu) (L^-1 E)^T: C = L, then C += (1 - mu) E^T L^-T
+      double* Qw = c->at<double>(c->L.Q);
+      OJBKQ_HIP(hipMemcpyAsync(Qw, Lf, (size_t)s.m * s.m * sizeof(double),
+                               hipMemcpyDeviceToDevice, st),
+                "copy factor");
+      ojbkq::GemmDesc g;   // C[i][j] += (1 - mu) sum_k E[k][i] Linv[j][k], Linv[j][k] = 0 for k > j
+      g.M = s.m; g.N = s.m; g.Kd = s.m;
+      g.A = c->at<double>(c->L.E); g.lda = s.m; g.ta = ojbkq::Elt::F64; g.a_kmajor = true;
+      g.B = c->at<double>(c->L.Linv); g.ldb = s.m; g.tb = ojbkq::Elt::F64;
+      g.b_zero_above_col = true;
+      g.C = Qw; g.ldc = s.m; g.alpha = 1.0 - alpha; g.beta = 1.0;
+      OJBKQ_HIP(ojbkq::gemm_f64(g, st), "relaxed-solution operator");
+      Q = Qw;
+    }
     ojbkq::GemmDesc g;   // gq[j][i] = sum_l W[j][l] Q[l][i]
     g.M = s.n; g.N = s.m; g.Kd = s.m;
     g.A = W; g.lda = s.m; g.ta = ojbkq::Elt::F32;
@@ -361,6 +370,29 @@ int ctx_solve(ojbkq_ctx* c, const float* W, double alpha, uint8_t* codes, float*
     g.b_zero_below_col = !cross;   // Q = L is lower triangular
     g.C = gq; g.ldc = s.m;
     OJBKQ_HIP(ojbkq::gemm_f64(g, st), "W Q");
+  } else {
+    if (cross) {
+      double* U = c->at<double>(c->L.U);
+      ojbkq::GemmDesc u;   // U = W E^T: row j is X~^T (X - X~) w_j
+      u.M = s.n; u.N = s.m; u.Kd = s.m;
+      u.A = W; u.lda = s.m; u.ta = ojbkq::Elt::F32;
+      u.B = c->at<double>(c->L.E); u.ldb = s.m; u.tb = ojbkq::Elt::F64;
+      u.C = U; u.ldc = s.m;
+      OJBKQ_HIP(ojbkq::gemm_f64(u, st), "target projection");
+      ojbkq::GemmDesc y;   // gq = (1 - mu) U L^-T: row j is (1 - mu) L^-1 u_j
+      y.M = s.n; y.N = s.m; y.Kd = s.m;
+      y.A = U; y.lda = s.m; y.ta = ojbkq::Elt::F64;
+      y.B = c->at<double>(c->L.Linv); y.ldb = s.m; y.tb = ojbkq::Elt::F64;
+      y.b_zero_above_col = true;   // Linv[i][k] = 0 for k > i
+      y.C = gq; y.ldc = s.m; y.alpha = 1.0 - alpha;
+      OJBKQ_HIP(ojbkq::gemm_f64(y, st), "solve");
+    }
+    ojbkq::GemmDesc g;   // gq[j][i] (+)= sum_l W[j][l] L[l][i]
+    g.M = s.n; g.N = s.m; g.Kd = s.m;
+    g.A = W; g.lda = s.m; g.ta = ojbkq::Elt::F32;
+    g.B = Lf; g.ldb = s.m; g.tb = ojbkq::Elt::F64; g.b_kmajor = true; g.b_zero_below_col = true;
+    g.C = gq; g.ldc = s.m; g.beta = cross ? 1.0 : 0.0;
+    OJBKQ_HIP(ojbkq::gemm_f64(g, st), "W L");
   }
   stage_end(c, OJBKQ_STAGE_SOLVE, t0);
   t0 = stage_begin(c);

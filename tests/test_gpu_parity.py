@@ -161,6 +161,8 @@ def test_tiny_config_c1():
     (300, 150, 700, 4, 128, 8, 13, 1.0),    # several tiles / panels / blocks, mu = 1
     (1, 3, 5, 2, 128, 2, 14, 0.5),          # single input feature
     (33, 2, 40, 8, 16, 5, 15, 0.25),        # 8-bit box
+    (96, 80, 400, 4, 32, 6, 16, 0.5),       # n > m / 2: Rbar qbar through Q = L + (1 - mu) (L^-1 E)^T
+    (150, 40, 500, 3, 64, 4, 17, 0.0),      # n < m / 2: Rbar qbar through W E^T and L^-T, mu = 0
 ])
 def test_layer_matches_oracle(m, n, T, bits, group, K, seed, mu):
     cfg = small_cfg(m, n, T, bits, group, K, seed)
