@@ -1,9 +1,10 @@
 // fp64 MFMA GEMM for gfx950: C = beta C + alpha op(A) op(B)^T.
 //
-// Serves every dense contraction of the path: the Gram X~^T X~ (Alg. 1
-// step 2), the cross term X~^T (X - X~) and its product with W (the target
-// projection behind Eq. jta_target / Alg. 1 step 3), the Cholesky trailing
-// updates, the blocked triangular-solve updates and Rbar qbar for the decoder.
+// Serves the dense contractions after the Gram (which has its own kernel):
+// the Cholesky panels and trailing updates and the doubling steps of L^-1
+// (Alg. 1 step 2), and the products that carry the target projection of
+// Eq. jta_target through the solve into the decoder's Rbar qbar (Alg. 1
+// steps 3-4): (L^-1 E)^T, W Q, or W E^T, its product with L^-T and W L.
 //
 // Design: 128x128 output tile per 256-thread workgroup, four waves in a 2x2
 // grid, each wave a 64x64 block of 4x4 v_mfma_f64_16x16x4_f64 tiles
@@ -12,7 +13,8 @@
 // exact in fp64), with the next chunk prefetched into registers while the
 // current one feeds the matrix cores.  Tiles are numbered so that each XCD
 // (eight per MI355X, one L2 each) receives a contiguous, row-grouped run of
-// tiles that share A and B panels.
+// tiles that share A and B panels; with a triangular B, in order of
+// decreasing work instead.
 #include "kernels.h"
 #include "device.h"
 
