@@ -4,10 +4,10 @@
 //
 // The factor is kept as L = R^T, lower triangular, row-major: row f of L is
 // column f of R, so the decoder's reads of R[i][f] over a block of rows i are
-// contiguous.  Right-looking blocked Cholesky with 64-wide panels: one wave
-// factors and inverts each 64x64 diagonal block, the panel below it is one
-// GEMM with that inverse, and every trailing update is a call of the fp64
-// MFMA GEMM.  L^-1 is formed once per factor by doubling from the inverted
+// contiguous.  Right-looking blocked Cholesky with 64-wide steps (grouped
+// into 256-wide outer panels when m is large): one wave factors and inverts
+// each 64x64 diagonal block, the panel below it is one GEMM with that
+// inverse, and every trailing update is a call of the fp64 MFMA GEMM.  L^-1 is formed once per factor by doubling from the inverted
 // diagonal blocks.
 #include "kernels.h"
 #include "device.h"
@@ -15,7 +15,9 @@
 namespace ojbkq {
 namespace {
 
-constexpr int kNB = 64;   // panel width
+constexpr int kNB = 64;      // diagonal block / inner panel width
+constexpr int kOuter = 256;  // outer panel width for large m (a multiple of kNB)
+constexpr int64_t kOuterFromM = 6144;
 
 __global__ __launch_bounds__(256) void damp_kernel(double* H, int64_t m, double lambda_rel,
                                                    double* lam2_out) {
@@ -234,23 +236,44 @@ hipError_t cholesky_lower(double* H, int64_t m, int* status, double* Linv, hipSt
   fill_zero_kernel<<<dim3((unsigned)(zb < 65536 ? zb : 65536)), dim3(256), 0, stream>>>(Linv, count);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  for (int64_t k0 = 0; k0 < m; k0 += kNB) {
-    const int nbk = (int)((m - k0) < kNB ? (m - k0) : kNB);
-    potrf_trtri_kernel<<<1, 64, 0, stream>>>(H, m, k0, nbk, status, Linv);
-    if ((e = hipGetLastError()) != hipSuccess) return e;
-    const int64_t rest = m - k0 - nbk;
+  // Two levels for large m: 256-wide outer panels, factored 64 columns at a
+  // time with updates confined to the outer panel's columns; the trailing
+  // matrix right of an outer panel takes one rank-256 update, a quarter of
+  // the passes over it (each a read and a write of the whole trailing
+  // triangle) that 64-wide steps would make.  Below kOuterFromM the extra
+  // launches cost more than the traffic saved, and the outer panel is the
+  // 64-wide step itself.
+  const int64_t outer = m >= kOuterFromM ? kOuter : kNB;
+  for (int64_t K0 = 0; K0 < m; K0 += outer) {
+    const int64_t K1 = (m - K0) < outer ? m : K0 + outer;
+    for (int64_t k0 = K0; k0 < K1; k0 += kNB) {
+      const int nbk = (int)((m - k0) < kNB ? (m - k0) : kNB);
+      potrf_trtri_kernel<<<1, 64, 0, stream>>>(H, m, k0, nbk, status, Linv);
+      if ((e = hipGetLastError()) != hipSuccess) return e;
+      const int64_t k1 = k0 + nbk, rest = m - k1;
+      if (rest <= 0) continue;
+      GemmDesc p;   // panel, in place: H[k1:, K] <- H[k1:, K] L_KK^-T (each row block read, then written)
+      p.M = rest; p.N = nbk; p.Kd = nbk;
+      p.A = H + k1 * m + k0; p.lda = m; p.ta = Elt::F64;
+      p.B = Linv + k0 * m + k0; p.ldb = m; p.tb = Elt::F64; p.b_zero_above_col = true;
+      p.C = H + k1 * m + k0; p.ldc = m; p.alpha = 1.0; p.beta = 0.0;
+      if ((e = gemm_f64(p, stream)) != hipSuccess) return e;
+      if (k1 >= K1) continue;
+      GemmDesc u;   // the outer panel's remaining columns: H[k1:, k1:K1] -= P P[0:K1-k1]^T
+      u.M = rest; u.N = K1 - k1; u.Kd = nbk;
+      u.A = H + k1 * m + k0; u.lda = m; u.ta = Elt::F64;
+      u.B = H + k1 * m + k0; u.ldb = m; u.tb = Elt::F64;
+      u.C = H + k1 * m + k1; u.ldc = m;
+      u.alpha = -1.0; u.beta = 1.0;
+      if ((e = gemm_f64(u, stream)) != hipSuccess) return e;
+    }
+    const int64_t rest = m - K1;
     if (rest <= 0) continue;
-    GemmDesc p;   // panel, in place: H[k1:, K] <- H[k1:, K] L_KK^-T (each row block read, then written)
-    p.M = rest; p.N = nbk; p.Kd = nbk;
-    p.A = H + (k0 + nbk) * m + k0; p.lda = m; p.ta = Elt::F64;
-    p.B = Linv + k0 * m + k0; p.ldb = m; p.tb = Elt::F64; p.b_zero_above_col = true;
-    p.C = H + (k0 + nbk) * m + k0; p.ldc = m; p.alpha = 1.0; p.beta = 0.0;
-    if ((e = gemm_f64(p, stream)) != hipSuccess) return e;
-    GemmDesc g;   // trailing update of the lower tiles
-    g.M = rest; g.N = rest; g.Kd = nbk;
-    g.A = H + (k0 + nbk) * m + k0; g.lda = m; g.ta = Elt::F64;
-    g.B = H + (k0 + nbk) * m + k0; g.ldb = m; g.tb = Elt::F64;
-    g.C = H + (k0 + nbk) * m + (k0 + nbk); g.ldc = m;
+    GemmDesc g;   // trailing update of the lower tiles by the whole outer panel
+    g.M = rest; g.N = rest; g.Kd = K1 - K0;
+    g.A = H + K1 * m + K0; g.lda = m; g.ta = Elt::F64;
+    g.B = H + K1 * m + K0; g.ldb = m; g.tb = Elt::F64;
+    g.C = H + K1 * m + K1; g.ldc = m;
     g.alpha = -1.0; g.beta = 1.0; g.lower_tiles = true;
     if ((e = gemm_f64(g, stream)) != hipSuccess) return e;
   }

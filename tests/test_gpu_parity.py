@@ -179,6 +179,25 @@ def test_heavy_tailed_layer_m1024():
     assert frac >= 0.999
 
 
+def test_wide_layer_two_level_factor():
+    """m = 6200: the factor runs in 256-wide outer panels (m >= 6144), with a
+    ragged last outer panel (56 columns) and a ragged last 64-wide step."""
+    cfg = small_cfg(6200, 6, 8192, 4, 128, 2, 23)
+    W, Xr, Xq = make_layer(cfg, device=DEV)
+    s = ok.LayerSolver(cfg.m, cfg.n, cfg.bits, cfg.group, cfg.K, cfg.klein_seed, device=DEV)
+    s.accumulate(Xr, Xq)
+    g = s.solve(W, cfg.mu)
+    L = np64(s.inspect("L"))
+    s.close()
+    o = orc.quantize_layer(np64(W), np64(Xr), np64(Xq), cfg.mu, cfg.bits, cfg.group, cfg.K,
+                           cfg.klein_seed)
+    colnorm = np.sqrt(np.sum(o.R ** 2, axis=0))
+    errR = float(np.max(np.abs(L.T - o.R) / colnorm[None, :]))
+    print(f"[t6200] R err {errR:.2e}")
+    assert errR < 1e-9, errR
+    assert check_layer(cfg, g, o, cfg.mu) >= 0.999
+
+
 def test_sparse_mlp_layer_3bit():
     """Post-SiLU-like activations (60% near-zero), 3-bit box, as the down_proj workload."""
     cfg = small_cfg(640, 40, 2048, 3, 128, 16, 22, sparsity=0.6)
