@@ -15,7 +15,9 @@ Prints one JSON line.  value = n (K + 1) / layer time, i.e. candidate paths
 (columns x samples) decoded per second, end to end (times the number of JTA
 knobs when a workload sweeps several on one factor).  The roofline object is
 for the dominant kernel, the fused Gram + cross-term contraction, timed with
-HIP events on the stream it is launched on.  The CPU baseline times the oracle
+HIP events on the stream it is launched on (for layers with n <= 0.4 m,
+whose cross term is accumulated already multiplied by W, the accumulate call
+as a whole: the Gram kernel and the two projection GEMMs).  The CPU baseline times the oracle
 on a bounded sample of the same workload on this host and extrapolates.
 """
 
@@ -182,6 +184,7 @@ def main():
         s = ok.LayerSolver(cfg.m, cfg.n, cfg.bits, cfg.group, cfg.K, cfg.klein_seed,
                            cfg.lambda_rel, device=dev, workspace=ws)
         s.set_timing(True)                        # per-stage HIP events inside the library
+        s.set_weights(W)                          # lets thin layers skip the m x m cross term
         ev = [torch.cuda.Event(enable_timing=True) for _ in range(2 * len(chunks) + 1)]
         for i, (Xr, Xq) in enumerate(chunks):
             ev[2 * i].record(stream)
@@ -218,7 +221,11 @@ def main():
     gc_avg = sum(gc_ms) / len(gc_ms)
     m, T = cfg.m, cfg.T
     Tc = T // cfg.chunks
-    flops = 3.0 * m * m * Tc          # syrk m^2 Tc (lower half) + cross 2 m^2 Tc per launch
+    projected = ok.projects_cross_term(m, cfg.n)
+    # per accumulate call: the Gram's lower half m^2 Tc, plus the cross term:
+    # the mixed product 2 m^2 Tc, or (thin layers, weights bound) W (X - X~)
+    # and its product with X~^T, 4 n m Tc
+    flops = m * m * Tc + (4.0 * cfg.n * m * Tc if projected else 2.0 * m * m * Tc)
     achieved = flops / (gc_avg * 1e-3) / 1e12
     paths = cfg.n * (cfg.K + 1) * len(cfg.mus)
     dec_flops = float(m) * m * paths     # m^2 per candidate path (the strict triangle, 2 FLOP/MAC)
@@ -243,14 +250,17 @@ def main():
                       **{f"library_{k}": v for k, v in stage_ms.items()}},
         "roofline": {
             "bound": "mfma",
-            "kernel": "gram_cross_kernel",
+            "kernel": ("gram_cross_kernel + projection GEMMs (accumulate call)" if projected
+                       else "gram_cross_kernel"),
             "achieved": achieved,
             "peak": PEAK_F64_MFMA_TFLOPS,
             "unit": "TFLOP/s",
             "frac": achieved / PEAK_F64_MFMA_TFLOPS,
-            "traffic": measured_traffic("gram_cross_kernel", cfg.key),
+            "traffic": None if projected else measured_traffic("gram_cross_kernel", cfg.key),
             "algorithmic_flops_per_launch": flops,
-            "algorithmic_bytes_per_launch": 8.0 * m * Tc + 16.0 * m * m,
+            # activations read once; G (and E) written, or W read and U updated
+            "algorithmic_bytes_per_launch": 8.0 * m * Tc + (
+                8.0 * m * m + 20.0 * cfg.n * m if projected else 16.0 * m * m),
         },
         "decode_roofline": {
             "bound": "mfma",

@@ -114,15 +114,26 @@ int ojbkq_quantize_layer(const ojbkq_params* p, const float* W, const float* X_r
  * several JTA knobs on one Gram (R does not depend on mu).
  *   create:     binds params, workspace (>= ojbkq_workspace_bytes) and stream;
  *               *out receives a host-side handle.  Sums start at zero.
+ *   set_weights (optional, before the first accumulate, else ESTATE): binds
+ *               W [n, m] float32 (device, caller-owned, unchanged until the
+ *               last solve; NULL: EINVAL).  The cross term enters the path
+ *               only as X~^T (X - X~) w_j (Eq. jta_target); when 5 n <= 2 m
+ *               the library then accumulates those products chunk by chunk
+ *               and never forms the [m, m] cross term, which costs 4 n m
+ *               instead of 2 m^2 multiply-adds per token.  Results are the
+ *               same either way up to rounding.  Every solve must then pass
+ *               this same W pointer (EINVAL otherwise).
  *   accumulate: adds X_q_c X_q_c^T and X_q_c (X_ref_c - X_q_c)^T of one chunk
  *               ([m, T_c], row stride T_c <= ldx <= 2^27).  X_ref_c NULL or == X_q_c adds no
- *               cross term.  Not allowed after the first solve (ESTATE).
+ *               cross term (that chunk has X_ref = X_q); chunks with and
+ *               without one may be mixed.  Not allowed after the first solve (ESTATE).
  *   solve:      damps and factors the accumulated Gram on first use, then runs
  *               the rest of the path for W [n, m] and knob `alpha` (overrides
  *               p->alpha).  Output arguments as in ojbkq_quantize_layer.
  *   destroy:    frees the handle (not the workspace).                       */
 int ojbkq_create(const ojbkq_params* p, void* workspace, size_t workspace_bytes, void* stream,
                  ojbkq_ctx** out);
+int ojbkq_set_weights(ojbkq_ctx* ctx, const float* W);
 int ojbkq_accumulate(ojbkq_ctx* ctx, const float* X_ref_c, const float* X_q_c, int64_t T_c,
                      int64_t ldx);
 int ojbkq_solve(ojbkq_ctx* ctx, const float* W, double alpha, uint8_t* codes, float* scales,

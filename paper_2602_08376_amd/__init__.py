@@ -31,7 +31,7 @@ ABI_FUNCTIONS = (
     "ojbkq_workspace_bytes", "ojbkq_quantize_layer", "ojbkq_create", "ojbkq_accumulate",
     "ojbkq_solve", "ojbkq_destroy", "ojbkq_inspect", "ojbkq_decode_workspace_bytes",
     "ojbkq_decode_stage", "ojbkq_klein_log_rho", "ojbkq_last_error", "ojbkq_set_timing",
-    "ojbkq_stage_times",
+    "ojbkq_stage_times", "ojbkq_set_weights",
 )
 
 STAGES = ("gram", "factor", "solve", "centres", "decode", "select")
@@ -75,6 +75,7 @@ def library() -> ctypes.CDLL:
         "ojbkq_quantize_layer": (ctypes.c_int, [P, vp, vp, vp, i64, i64, vp, ctypes.c_size_t, vp,
                                                 vp, vp, vp, vp, vp]),
         "ojbkq_create": (ctypes.c_int, [P, vp, ctypes.c_size_t, vp, ctypes.POINTER(vp)]),
+        "ojbkq_set_weights": (ctypes.c_int, [vp, vp]),
         "ojbkq_accumulate": (ctypes.c_int, [vp, vp, vp, i64, i64]),
         "ojbkq_solve": (ctypes.c_int, [vp, vp, dp, vp, vp, vp, vp, vp]),
         "ojbkq_destroy": (ctypes.c_int, [vp]),
@@ -135,6 +136,12 @@ def _rows_view(X: torch.Tensor, name: str, m: int):
     T = X.shape[1]
     ld = X.stride(0) if X.shape[0] > 1 else T
     return T, max(ld, T)
+
+
+def projects_cross_term(m: int, n: int) -> bool:
+    """Whether a context with bound weights accumulates the cross term as
+    W E^T instead of forming E (the rule stated at ojbkq_set_weights)."""
+    return 5 * n <= 2 * m
 
 
 def num_groups(m: int, group: int) -> int:
@@ -233,6 +240,15 @@ class LayerSolver:
         _check(lib.ojbkq_create(ctypes.byref(self.p), _ptr(self.ws), self.ws.numel(),
                                 _stream(self.device), ctypes.byref(h)))
         self.h = h
+
+    def set_weights(self, W):
+        """Bind W before the first chunk (see ojbkq_set_weights); every solve
+        must then be given this same tensor, which is kept alive here."""
+        _need(W, "W", torch.float32, (self.n, self.m), self.device)
+        if not W.is_contiguous():
+            raise ValueError("W must be contiguous")
+        _check(library().ojbkq_set_weights(self.h, _ptr(W)))
+        self.W = W
 
     def accumulate(self, X_ref_c, X_q_c):
         _need(X_q_c, "X_q_c", torch.float32, device=self.device)

@@ -64,6 +64,23 @@ Shape shape_of(const ojbkq_params& p) {
 // mu sweep, which repeats only the n m^2 part).
 inline bool route_q(const Shape& s) { return 2 * s.n > s.m; }
 
+// With W known while the activations stream in, the direct route needs the
+// cross term only through U = W E^T = sum over chunks of (W D_c) X~_c^T,
+// D_c = X_c - X~_c: 4 n m multiply-adds per token instead of the mixed
+// product's 2 m^2 (and no W E^T at solve time).  That pays once n is below
+// about 0.4 m (the general GEMM reaches about 0.75 of the MFMA peak, the
+// Gram kernel about 0.89).
+inline bool route_p(const Shape& s) { return 5 * s.n <= 2 * s.m; }
+
+// Tokens per projection step: W D_c for this many tokens at a time sits in
+// the cross-term buffer, which the projected route leaves unused (n t <= m^2).
+int64_t proj_tokens(const Shape& s) {
+  int64_t t = (s.m * s.m) / s.n;
+  t = t < 16384 ? t : 16384;
+  t = t >= 16 ? t / 16 * 16 : t;
+  return t < 1 ? 1 : t;
+}
+
 // Offsets of every buffer carved from the workspace.
 struct Layout {
   size_t status = 0, lam2 = 0, G = 0, E = 0, U = 0, gq = 0, alpha = 0, pcodes = 0,
@@ -187,6 +204,10 @@ struct ojbkq_ctx {
   hipStream_t stream = nullptr;
   bool any_chunk = false;
   bool cross_seen = false;
+  // W bound by ojbkq_set_weights (or the one-shot call): with route_p the
+  // cross term is accumulated projected, as U = W E^T, and E is never formed
+  const float* W = nullptr;
+  bool projected = false;
   bool factored = false;
   bool solved = false;
   // stage timing: event pairs recorded per stage, folded into ms[] at sync points
@@ -290,15 +311,59 @@ int ctx_accumulate(ojbkq_ctx* c, const float* Xr, const float* Xq, int64_t T, in
   if (ldx < T) return fail(OJBKQ_EINVAL, "ldx must be >= T");
   if (ldx > kMaxLdx) return fail(OJBKQ_EINVAL, "ldx must be <= 2^27");
   const bool cross = Xr != nullptr && Xr != Xq;
+  const Shape& s = c->s;
+  double* G = c->at<double>(c->L.G);
+  double* E = c->at<double>(c->L.E);
   hipEvent_t t0 = stage_begin(c);
-  OJBKQ_HIP(ojbkq::gram_cross(Xq, cross ? Xr : nullptr, c->s.m, T, ldx, c->at<double>(c->L.G),
-                              c->at<double>(c->L.E), c->any_chunk, c->cross_seen,
-                              c->at<uint32_t>(c->L.gc_tiles), c->at<void>(c->L.gc_scratch),
-                              gram_shares(), c->stream),
-            "gram and cross term");
+  if (c->projected) {
+    OJBKQ_HIP(ojbkq::gram_cross(Xq, nullptr, s.m, T, ldx, G, E, c->any_chunk, false,
+                                c->at<uint32_t>(c->L.gc_tiles), c->at<void>(c->L.gc_scratch),
+                                gram_shares(), c->stream),
+              "gram");
+    if (cross) {
+      // U (+)= (W D) X~^T over this chunk, tp tokens at a time; W D in E's buffer
+      double* P = E;
+      double* U = c->at<double>(c->L.U);
+      const int64_t tp = proj_tokens(s);
+      for (int64_t t0k = 0; t0k < T; t0k += tp) {
+        const int64_t tk = (T - t0k) < tp ? (T - t0k) : tp;
+        ojbkq::GemmDesc p;   // P[j][t] = sum_f W[j][f] (X[f][t] - X~[f][t])
+        p.M = s.n; p.N = tk; p.Kd = s.m;
+        p.A = c->W; p.lda = s.m; p.ta = ojbkq::Elt::F32;
+        p.B = Xr + t0k; p.B2 = Xq + t0k; p.ldb = ldx; p.tb = ojbkq::Elt::F32; p.b_kmajor = true;
+        p.C = P; p.ldc = tp;
+        OJBKQ_HIP(ojbkq::gemm_f64(p, c->stream), "projected activations");
+        ojbkq::GemmDesc u;   // U[j][f] (+)= sum_t P[j][t] X~[f][t]
+        u.M = s.n; u.N = s.m; u.Kd = tk;
+        u.A = P; u.lda = tp; u.ta = ojbkq::Elt::F64;
+        u.B = Xq + t0k; u.ldb = ldx; u.tb = ojbkq::Elt::F32;
+        u.C = U; u.ldc = s.m; u.beta = (c->cross_seen || t0k > 0) ? 1.0 : 0.0;
+        OJBKQ_HIP(ojbkq::gemm_f64(u, c->stream), "projected cross term");
+      }
+    }
+  } else {
+    // E holds the mixed product X~ X^T of every chunk; a chunk without a cross
+    // term contributes X~ X~^T to it, so that E - G stays the cross term
+    const bool mixed = cross || c->cross_seen;
+    if (cross && !c->cross_seen && c->any_chunk)
+      OJBKQ_HIP(ojbkq::mixed_from_gram(E, G, s.m, c->stream), "mixed product of earlier chunks");
+    OJBKQ_HIP(ojbkq::gram_cross(Xq, mixed ? (cross ? Xr : Xq) : nullptr, s.m, T, ldx, G, E,
+                                c->any_chunk, c->cross_seen || (cross && c->any_chunk),
+                                c->at<uint32_t>(c->L.gc_tiles), c->at<void>(c->L.gc_scratch),
+                                gram_shares(), c->stream),
+              "gram and cross term");
+  }
   stage_end(c, OJBKQ_STAGE_GRAM, t0);
   if (cross) c->cross_seen = true;
   c->any_chunk = true;
+  return OJBKQ_OK;
+}
+
+int ctx_set_weights(ojbkq_ctx* c, const float* W) {
+  if (!W) return fail(OJBKQ_EINVAL, "W is NULL");
+  if (c->any_chunk) return fail(OJBKQ_ESTATE, "weights must be bound before the first accumulate");
+  c->W = W;
+  c->projected = !route_q(c->s) && route_p(c->s);
   return OJBKQ_OK;
 }
 
@@ -321,12 +386,13 @@ int ctx_solve(ojbkq_ctx* c, const float* W, double alpha, uint8_t* codes, float*
   if (!W || !codes || !scales || !zeros || !residuals)
     return fail(OJBKQ_EINVAL, "W, codes, scales, zeros and residuals are required");
   if (!(alpha >= 0.0 && alpha <= 1.0)) return fail(OJBKQ_EINVAL, "alpha must be in [0, 1]");
+  if (c->W && W != c->W) return fail(OJBKQ_EINVAL, "W differs from the weights bound to ctx");
   const Shape& s = c->s;
   hipStream_t st = c->stream;
   double* Lf = c->at<double>(c->L.G);
   hipEvent_t t0 = stage_begin(c);
   if (!c->factored) {
-    if (c->cross_seen)   // mixed product -> cross term, while G is still the Gram
+    if (c->cross_seen && !c->projected)   // mixed product -> cross term, while G is the Gram
       OJBKQ_HIP(ojbkq::cross_from_mixed(c->at<double>(c->L.E), Lf, s.m, st), "cross term");
     OJBKQ_HIP(ojbkq::launch_damp(Lf, s.m, c->p.lambda_rel, c->at<double>(c->L.lam2), st), "damp");
     OJBKQ_HIP(ojbkq::cholesky_lower(Lf, s.m, c->at<int>(c->L.status), c->at<double>(c->L.Linv), st),
@@ -373,12 +439,14 @@ int ctx_solve(ojbkq_ctx* c, const float* W, double alpha, uint8_t* codes, float*
   } else {
     if (cross) {
       double* U = c->at<double>(c->L.U);
-      ojbkq::GemmDesc u;   // U = W E^T: row j is X~^T (X - X~) w_j
-      u.M = s.n; u.N = s.m; u.Kd = s.m;
-      u.A = W; u.lda = s.m; u.ta = ojbkq::Elt::F32;
-      u.B = c->at<double>(c->L.E); u.ldb = s.m; u.tb = ojbkq::Elt::F64;
-      u.C = U; u.ldc = s.m;
-      OJBKQ_HIP(ojbkq::gemm_f64(u, st), "target projection");
+      if (!c->projected) {
+        ojbkq::GemmDesc u;   // U = W E^T: row j is X~^T (X - X~) w_j
+        u.M = s.n; u.N = s.m; u.Kd = s.m;
+        u.A = W; u.lda = s.m; u.ta = ojbkq::Elt::F32;
+        u.B = c->at<double>(c->L.E); u.ldb = s.m; u.tb = ojbkq::Elt::F64;
+        u.C = U; u.ldc = s.m;
+        OJBKQ_HIP(ojbkq::gemm_f64(u, st), "target projection");
+      }
       ojbkq::GemmDesc y;   // gq = (1 - mu) U L^-T: row j is (1 - mu) L^-1 u_j
       y.M = s.n; y.N = s.m; y.Kd = s.m;
       y.A = U; y.lda = s.m; y.ta = ojbkq::Elt::F64;
@@ -453,6 +521,7 @@ int ojbkq_quantize_layer(const ojbkq_params* p, const float* W, const float* X_r
   if (ldx > kMaxLdx) return fail(OJBKQ_EINVAL, "ldx must be <= 2^27");
   ojbkq_ctx c;
   if ((rc = ctx_init(&c, p, workspace, workspace_bytes, stream))) return rc;
+  if ((rc = ctx_set_weights(&c, W))) return rc;
   const float* Xr = (p->alpha == 1.0) ? nullptr : X_ref;
   if ((rc = ctx_accumulate(&c, Xr, X_q, T, ldx))) return rc;
   return ctx_solve(&c, W, p->alpha, codes, scales, zeros, residuals, winner);
@@ -472,6 +541,12 @@ int ojbkq_create(const ojbkq_params* p, void* workspace, size_t workspace_bytes,
   }
   *out = c;
   return OJBKQ_OK;
+}
+
+int ojbkq_set_weights(ojbkq_ctx* ctx, const float* W) {
+  g_error.clear();
+  if (!ctx) return fail(OJBKQ_EINVAL, "ctx is NULL");
+  return ctx_set_weights(ctx, W);
 }
 
 int ojbkq_accumulate(ojbkq_ctx* ctx, const float* X_ref_c, const float* X_q_c, int64_t T_c,

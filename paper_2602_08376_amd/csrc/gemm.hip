@@ -4,7 +4,9 @@
 // the Cholesky panels and trailing updates and the doubling steps of L^-1
 // (Alg. 1 step 2), and the products that carry the target projection of
 // Eq. jta_target through the solve into the decoder's Rbar qbar (Alg. 1
-// steps 3-4): (L^-1 E)^T, W Q, or W E^T, its product with L^-T and W L.
+// steps 3-4): (L^-1 E)^T, W Q, or W E^T, its product with L^-T and W L;
+// and, for layers with few output channels, the target projection taken
+// straight from the activations, W (X - X~) followed by its product with X~^T.
 //
 // Design: 128x128 output tile per 256-thread workgroup, four waves in a 2x2
 // grid, each wave a 64x64 block of 4x4 v_mfma_f64_16x16x4_f64 tiles
@@ -290,10 +292,11 @@ hipError_t gemm_f64(const GemmDesc& d, hipStream_t stream) {
   if (ntiles > 0x7fffffff) return hipErrorInvalidValue;
 
   const bool diff = d.B2 != nullptr;
-  if (d.ta == Elt::F32 && d.tb == Elt::F32 && !d.a_kmajor && !d.b_kmajor)
-    return diff ? launch<float, float, false, false, true>(g, ntiles, stream)
-                : launch<float, float, false, false, false>(g, ntiles, stream);
+  if (d.ta == Elt::F32 && d.tb == Elt::F32 && !d.a_kmajor && d.b_kmajor && diff)
+    return launch<float, float, false, true, true>(g, ntiles, stream);
   if (diff) return hipErrorInvalidValue;
+  if (d.ta == Elt::F64 && d.tb == Elt::F32 && !d.a_kmajor && !d.b_kmajor)
+    return launch<double, float, false, false, false>(g, ntiles, stream);
   if (d.ta == Elt::F64 && d.tb == Elt::F64 && !d.a_kmajor && !d.b_kmajor)
     return launch<double, double, false, false, false>(g, ntiles, stream);
   if (d.ta == Elt::F64 && d.tb == Elt::F64 && !d.a_kmajor && d.b_kmajor)

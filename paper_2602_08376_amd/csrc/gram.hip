@@ -312,7 +312,25 @@ __global__ __launch_bounds__(256) void cross_from_mixed_kernel(double* E, const 
   }
 }
 
+// E = G read through symmetry, for every element.
+__global__ __launch_bounds__(256) void mixed_from_gram_kernel(double* E, const double* G,
+                                                              int64_t m) {
+  const int64_t total = m * m;
+  for (int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x; e < total;
+       e += (int64_t)gridDim.x * 256) {
+    const int64_t i = e / m, j = e % m;
+    E[e] = (i >= j) ? G[i * m + j] : G[j * m + i];
+  }
+}
+
 }  // namespace
+
+hipError_t mixed_from_gram(double* E, const double* G, int64_t m, hipStream_t stream) {
+  const int64_t blocks = (m * m + 255) / 256;
+  mixed_from_gram_kernel<<<dim3((unsigned)(blocks < 65536 ? blocks : 65536)), dim3(256), 0,
+                           stream>>>(E, G, m);
+  return hipGetLastError();
+}
 
 hipError_t cross_from_mixed(double* E, const double* G, int64_t m, hipStream_t stream) {
   const int64_t blocks = (m * m + 255) / 256;

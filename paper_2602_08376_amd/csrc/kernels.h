@@ -12,7 +12,8 @@ namespace ojbkq {
 // fp64 on v_mfma_f64_16x16x4_f64 (fp32 inputs are widened exactly).
 //   opA(i, k) = a_kmajor ? A[k * lda + i] : A[i * lda + k]
 //   opB(j, k) = b_kmajor ? B[k * ldb + j] : B[j * ldb + k]
-//   with B2 != nullptr, opB = B - B2 (same layout), formed in fp64.
+//   with B2 != nullptr, opB = B - B2 (same layout), formed in fp64 (fp32 A
+//   and B, B k-major only).
 //   lower_tiles: only 128x128 output tiles with tile_row >= tile_col are
 //   computed (a symmetric product whose lower triangle is wanted).
 enum class Elt { F32, F64 };
@@ -65,6 +66,9 @@ hipError_t gram_cross(const float* Xq, const float* Xr, int64_t m, int64_t T, in
 // X_q X_ref^T into the cross term X_q (X_ref - X_q)^T.  Call before G is
 // factored.
 hipError_t cross_from_mixed(double* E, const double* G, int64_t m, hipStream_t stream);
+// E = G over the whole square (G's lower triangle of 128-tiles valid): the
+// mixed product of chunks that were accumulated without a cross term.
+hipError_t mixed_from_gram(double* E, const double* G, int64_t m, hipStream_t stream);
 
 // ---- scales and zero points (Alg. 1 step 1) --------------------------------
 hipError_t launch_scale_zero(const float* W, int64_t n, int64_t m, int64_t g, int64_t G, int qmax,

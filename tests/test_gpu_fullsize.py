@@ -42,6 +42,7 @@ def test_attention_projection_full_size():
     (Xr, Xq), = list(activation_chunks(cfg, device=dev))
     s = ok.LayerSolver(cfg.m, cfg.n, cfg.bits, cfg.group, cfg.K, cfg.klein_seed, cfg.lambda_rel,
                        device=dev)
+    s.set_weights(W)
     s.accumulate(Xr, Xq)
     g = s.solve(W, cfg.mu)
     L = np64(s.inspect("L"))
@@ -136,6 +137,7 @@ def test_full_size_sampled(key):
     Wn = np64(W)
     s = ok.LayerSolver(cfg.m, cfg.n, cfg.bits, cfg.group, cfg.K, cfg.klein_seed, cfg.lambda_rel,
                        device=dev)
+    s.set_weights(W)          # as bench.py: c3 and c5 take the projected cross term
     diag = np.zeros(cfg.m)
     pairs = np.sort(rng.choice(cfg.m, size=(n_pairs, 2)), axis=1)[:, ::-1]   # i >= j
     gpairs = np.zeros(n_pairs)

@@ -249,6 +249,60 @@ def test_staged_intermediates_and_chunks():
     s.close()
 
 
+def _chunked_reference(Xr, Xq, bounds, cross):
+    """X_ref as the oracle sees it: chunks accumulated without a cross term
+    have X_ref = X_q."""
+    xr = Xr.clone()
+    for (a, b), c in zip(bounds, cross):
+        if not c:
+            xr[:, a:b] = Xq[:, a:b]
+    return xr
+
+
+@pytest.mark.parametrize("m,n,bind", [
+    (300, 40, True),    # 5 n <= 2 m with W bound: cross term accumulated as W E^T
+    (300, 40, False),   # same layer, mixed product route
+    (120, 100, True),   # n > m / 2: W only bound, mixed product route
+])
+def test_mixed_chunks_and_bound_weights(m, n, bind):
+    """Chunks with and without a cross term in any order, and the projected
+    route, whose token steps (2240 tokens at m = 300, n = 40) split the
+    second chunk with a ragged tail."""
+    cfg = small_cfg(m, n, 3600, 4, 128, 6, 35)
+    W, Xr, Xq = make_layer(cfg, device=DEV)
+    bounds = [(0, 400), (400, 2600), (2600, 3000), (3000, 3600)]
+    cross = [False, True, False, True]
+    s = ok.LayerSolver(cfg.m, cfg.n, cfg.bits, cfg.group, cfg.K, cfg.klein_seed, device=DEV)
+    if bind:
+        s.set_weights(W)
+    for (a, b), c in zip(bounds, cross):
+        s.accumulate(Xr[:, a:b] if c else None, Xq[:, a:b])
+    xr_o = np64(_chunked_reference(Xr, Xq, bounds, cross))
+    for mu in (0.5, 0.0):
+        g = s.solve(W, mu)
+        torch.cuda.synchronize()
+        o = orc.quantize_layer(np64(W), xr_o, np64(Xq), mu, cfg.bits, cfg.group, cfg.K,
+                               cfg.klein_seed)
+        gq = np64(s.inspect("gq"))
+        Sx = orc.expand_groups(o.scales, cfg.m, cfg.group)
+        gq_o = (Sx * o.qbar) @ o.R.T
+        errg = np.max(np.abs(gq - gq_o) / (np.abs(Sx * o.qbar) @ np.abs(o.R.T)))
+        print(f"[mixed m={m} n={n} bind={bind} mu={mu}] Rbar qbar rel err {errg:.2e}")
+        assert errg < 1e-10, errg
+        assert check_layer(cfg, g, o, mu) >= 0.999
+    if bind:
+        with pytest.raises(ok.OjbkqError) as ei:
+            s.solve(W.clone(), 0.5)          # another buffer than the bound one
+        assert ei.value.code == "EINVAL"
+    s.close()
+    s = ok.LayerSolver(cfg.m, cfg.n, cfg.bits, cfg.group, cfg.K, cfg.klein_seed, device=DEV)
+    s.accumulate(Xr, Xq)
+    with pytest.raises(ok.OjbkqError) as ei:
+        s.set_weights(W)                     # only before the first chunk
+    assert ei.value.code == "ESTATE"
+    s.close()
+
+
 def test_gram_load_paths_agree():
     """The Gram/cross contraction reads 16-byte runs of tokens when rows are
     16-byte aligned and T % 4 == 0, else single tokens; both paths stage the
