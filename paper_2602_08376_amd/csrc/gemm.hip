@@ -24,7 +24,8 @@ namespace ojbkq {
 namespace {
 
 constexpr int kTile = 128;
-constexpr int kKC = 16;
+constexpr int kKC = 32;            // k per LDS stage
+constexpr int kKH = 16;            // k per load / store step (two per stage)
 constexpr int kLdsLd = kTile + 2;  // padded LDS row (doubles)
 constexpr int kGroupRows = 8;      // tile rows per raster group
 
@@ -47,53 +48,72 @@ struct GemmArgs {
   int64_t batch;
 };
 
-// Eight consecutive elements starting at p, the first `valid` of them real
-// (the rest read as 0), widened to fp64.
-template <typename T>
-__device__ __forceinline__ void load8(const T* __restrict__ p, int valid, bool vec,
-                                      double out[8]) {
-  if (valid >= 8 && vec) {
+// This thread's share of a 128 x 16 operand step: 8 consecutive elements
+// from `p`, of which the first `valid` are real.  Non-k-major: thread -> (row
+// tid/2, k offset 8*(tid%2)); k-major: thread -> (k row tid/16, row offset
+// 8*(tid%16)).
+template <typename T, bool KMAJOR>
+__device__ __forceinline__ const T* step_ptr(const T* X, int64_t ld, int64_t rows, int64_t Kd,
+                                             int64_t r0, int64_t k0, int tid, int& valid) {
+  int64_t r, k, left;
+  if constexpr (!KMAJOR) {
+    r = r0 + (tid >> 1);
+    k = k0 + (tid & 1) * 8;
+    left = r < rows ? Kd - k : 0;
+  } else {
+    k = k0 + (tid >> 4);
+    r = r0 + (tid & 15) * 8;
+    left = k < Kd ? rows - r : 0;
+  }
+  valid = left > 0 ? (int)(left < 8 ? left : 8) : 0;
+  return KMAJOR ? X + k * ld + r : X + r * ld + k;
+}
+
+// The step's elements as stored, with no arithmetic on them, so the loads
+// stay in flight until the values are staged into LDS.  VEC (16-byte aligned
+// rows): two 16-byte loads per lane, from the operand's base for a lane with
+// fewer than 8 real elements (fix_step reloads those lanes).  Otherwise one
+// load per real element.
+template <typename T, bool VEC>
+__device__ __forceinline__ void load_step(const T* X, const T* p, int valid, T out[8]) {
+  if constexpr (VEC) {
+    const T* q0 = valid == 8 ? p : X;
     if constexpr (sizeof(T) == 4) {
-      const float4 a = *reinterpret_cast<const float4*>(p);
-      const float4 b = *reinterpret_cast<const float4*>(p + 4);
+      const float4 a = *reinterpret_cast<const float4*>(q0);
+      const float4 b = *reinterpret_cast<const float4*>(q0 + 4);
       out[0] = a.x; out[1] = a.y; out[2] = a.z; out[3] = a.w;
       out[4] = b.x; out[5] = b.y; out[6] = b.z; out[7] = b.w;
     } else {
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
-        const double2 v = *reinterpret_cast<const double2*>(p + 2 * q);
+        const double2 v = *reinterpret_cast<const double2*>(q0 + 2 * q);
         out[2 * q] = v.x;
         out[2 * q + 1] = v.y;
       }
     }
   } else {
 #pragma unroll
-    for (int q = 0; q < 8; ++q) out[q] = (q < valid) ? (double)p[q] : 0.0;
+    for (int q = 0; q < 8; ++q) out[q] = (q < valid) ? p[q] : T(0);
   }
 }
 
-// Loads this thread's share (8 elements) of a 128 x 16 operand chunk.
-// Non-k-major: thread -> (row tid/2, k offset 8*(tid%2)); k-major: thread ->
-// (k row tid/16, row offset 8*(tid%16)).
-template <typename T, bool KMAJOR>
-__device__ __forceinline__ void load_chunk(const T* __restrict__ X, int64_t ld, int64_t rows,
-                                           int64_t Kd, int64_t r0, int64_t k0, int tid, bool vec,
-                                           double out[8]) {
-  if constexpr (!KMAJOR) {
-    const int64_t r = r0 + (tid >> 1);
-    const int64_t k = k0 + (tid & 1) * 8;
-    const int64_t left = Kd - k;
-    const int valid = (r < rows && left > 0) ? (int)(left < 8 ? left : 8) : 0;
-    const T* p = valid > 0 ? X + r * ld + k : X;
-    load8<T>(p, valid, vec, out);
-  } else {
-    const int64_t k = k0 + (tid >> 4);
-    const int64_t r = r0 + (tid & 15) * 8;
-    const int64_t left = rows - r;
-    const int valid = (k < Kd && left > 0) ? (int)(left < 8 ? left : 8) : 0;
-    const T* p = valid > 0 ? X + k * ld + r : X;
-    load8<T>(p, valid, vec, out);
+// VEC path, at staging time: the real elements of a lane with 0 < valid < 8.
+template <typename T, bool VEC>
+__device__ __forceinline__ void fix_step(const T* p, int valid, T out[8]) {
+  if constexpr (VEC) {
+    if (valid > 0 && valid < 8) {
+#pragma unroll
+      for (int q = 0; q < 7; ++q)
+        if (q < valid) out[q] = p[q];
+    }
   }
+}
+
+// The raw elements widened to fp64, zero past `valid`.
+template <typename T>
+__device__ __forceinline__ void widen8(const T raw[8], int valid, double out[8]) {
+#pragma unroll
+  for (int q = 0; q < 8; ++q) out[q] = (q < valid) ? (double)raw[q] : 0.0;
 }
 
 template <bool KMAJOR>
@@ -150,7 +170,7 @@ __device__ __forceinline__ int64_t xcd_tile_number() {
 }
 
 // One 128x128 output tile (ti, tj) of C = beta C + alpha op(A) op(B)^T.
-template <typename TA, typename TB, bool AK, bool BK, bool BDIFF>
+template <typename TA, typename TB, bool AK, bool BK, bool BDIFF, bool VEC>
 __device__ __forceinline__ void gemm_tile(const GemmArgs& g, int64_t ti, int64_t tj,
                                           double (*sA)[kLdsLd], double (*sB)[kLdsLd]) {
   const int64_t I0 = ti * kTile, J0 = tj * kTile;
@@ -167,15 +187,36 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& g, int64_t ti, int64_t
 #pragma unroll
     for (int y = 0; y < 4; ++y) acc[x][y] = d4{0.0, 0.0, 0.0, 0.0};
 
-  double ra[8], rb[8];
+  // the next stage's operands, as stored in memory, and how many are real
+  TA ra[2][8];
+  TB rb[2][8], r2[BDIFF ? 2 : 1][8];
+  int va[2], vb[2];
+  int64_t kf = 0;   // first k of the stage in flight
   auto fetch = [&](int64_t k0) {
-    load_chunk<TA, AK>(A, g.lda, g.M, g.Kd, I0, k0, tid, g.vec_a, ra);
-    load_chunk<TB, BK>(B, g.ldb, g.N, g.Kd, J0, k0, tid, g.vec_b, rb);
-    if constexpr (BDIFF) {
-      double r2[8];
-      load_chunk<TB, BK>(B2, g.ldb, g.N, g.Kd, J0, k0, tid, g.vec_b, r2);
+    kf = k0;
 #pragma unroll
-      for (int q = 0; q < 8; ++q) rb[q] -= r2[q];
+    for (int h = 0; h < 2; ++h) {
+      const TA* pa = step_ptr<TA, AK>(A, g.lda, g.M, g.Kd, I0, k0 + h * kKH, tid, va[h]);
+      const TB* pb = step_ptr<TB, BK>(B, g.ldb, g.N, g.Kd, J0, k0 + h * kKH, tid, vb[h]);
+      load_step<TA, VEC>(A, pa, va[h], ra[h]);
+      load_step<TB, VEC>(B, pb, vb[h], rb[h]);
+      if constexpr (BDIFF) load_step<TB, VEC>(B2, B2 + (pb - B), vb[h], r2[h]);
+    }
+  };
+  // VEC: lanes with a ragged step exist only where the tile or the stage
+  // crosses the operand's edge (the same for every lane)
+  const bool rows_in = I0 + kTile <= g.M && J0 + kTile <= g.N;
+  auto fix = [&]() {
+    if (VEC && !(rows_in && kf + kKC <= g.Kd)) {
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        int v;
+        fix_step<TA, VEC>(step_ptr<TA, AK>(A, g.lda, g.M, g.Kd, I0, kf + h * kKH, tid, v), v,
+                          ra[h]);
+        const TB* pb = step_ptr<TB, BK>(B, g.ldb, g.N, g.Kd, J0, kf + h * kKH, tid, v);
+        fix_step<TB, VEC>(pb, v, rb[h]);
+        if constexpr (BDIFF) fix_step<TB, VEC>(B2 + (pb - B), v, r2[h]);
+      }
     }
   };
 
@@ -188,8 +229,21 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& g, int64_t ti, int64_t
   if (nck > 0) fetch(chunk_k(0));
   for (int64_t c = 0; c < nck; ++c) {
     __syncthreads();
-    store_chunk<AK>(sA, tid, ra);
-    store_chunk<BK>(sB, tid, rb);
+    fix();
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      double wa[8], wb[8];
+      widen8<TA>(ra[h], va[h], wa);
+      widen8<TB>(rb[h], vb[h], wb);
+      if constexpr (BDIFF) {   // B - B2, exact in fp64 for fp32 inputs
+        double w2[8];
+        widen8<TB>(r2[h], vb[h], w2);
+#pragma unroll
+        for (int q = 0; q < 8; ++q) wb[q] -= w2[q];
+      }
+      store_chunk<AK>(sA + h * kKH, tid, wa);
+      store_chunk<BK>(sB + h * kKH, tid, wb);
+    }
     __syncthreads();
     if (c + 1 < nck) fetch(chunk_k(c + 1));
 #pragma unroll
@@ -238,7 +292,7 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& g, int64_t ti, int64_t
   }
 }
 
-template <typename TA, typename TB, bool AK, bool BK, bool BDIFF>
+template <typename TA, typename TB, bool AK, bool BK, bool BDIFF, bool VEC>
 __global__ __launch_bounds__(256, 2) void gemm_f64_kernel(GemmArgs g) {
   __shared__ double sA[kKC][kLdsLd];
   __shared__ double sB[kKC][kLdsLd];
@@ -254,13 +308,16 @@ __global__ __launch_bounds__(256, 2) void gemm_f64_kernel(GemmArgs g) {
     tri_tile(blockIdx.x, g.tiles_m, g.tiles_n, g.b_tri_up != 0, ti, tj);
   else
     raster_tile(xcd_tile_number(), g.tiles_m, g.tiles_n, ti, tj);
-  gemm_tile<TA, TB, AK, BK, BDIFF>(g, ti, tj, sA, sB);
+  gemm_tile<TA, TB, AK, BK, BDIFF, VEC>(g, ti, tj, sA, sB);
 }
 
 template <typename TA, typename TB, bool AK, bool BK, bool BDIFF>
 hipError_t launch(const GemmArgs& g, int64_t ntiles, hipStream_t s) {
-  gemm_f64_kernel<TA, TB, AK, BK, BDIFF><<<dim3((unsigned)ntiles, (unsigned)g.batch), dim3(256), 0,
-                                           s>>>(g);
+  const dim3 grid((unsigned)ntiles, (unsigned)g.batch);
+  if (g.vec_a && g.vec_b)
+    gemm_f64_kernel<TA, TB, AK, BK, BDIFF, true><<<grid, dim3(256), 0, s>>>(g);
+  else
+    gemm_f64_kernel<TA, TB, AK, BK, BDIFF, false><<<grid, dim3(256), 0, s>>>(g);
   return hipGetLastError();
 }
 
@@ -285,8 +342,14 @@ hipError_t gemm_f64(const GemmDesc& d, hipStream_t stream) {
   g.sa = d.stride_a; g.sb = d.stride_b; g.sc = d.stride_c;
   g.batch = d.batch;
   if (d.batch < 1 || d.batch > 65535 || (d.batch > 1 && d.B2 != nullptr)) return hipErrorInvalidValue;
-  g.vec_a = vec_ok(d.A, d.lda, d.ta) ? 1 : 0;   // rows (or, k-major, k rows) of 16-byte runs
-  g.vec_b = (vec_ok(d.B, d.ldb, d.tb) && (d.B2 == nullptr || vec_ok(d.B2, d.ldb, d.tb))) ? 1 : 0;
+  // 16-byte loads: rows (or, k-major, k rows) start 16-byte aligned in every
+  // batch entry, and the first 8 elements of the operand exist (a lane whose
+  // step is ragged reads those and discards them)
+  const int64_t per16a = d.ta == Elt::F32 ? 4 : 2, per16b = d.tb == Elt::F32 ? 4 : 2;
+  g.vec_a = (vec_ok(d.A, d.lda, d.ta) && d.stride_a % per16a == 0 &&
+             (d.a_kmajor ? d.M : g.Kd) >= 8) ? 1 : 0;
+  g.vec_b = (vec_ok(d.B, d.ldb, d.tb) && (d.B2 == nullptr || vec_ok(d.B2, d.ldb, d.tb)) &&
+             d.stride_b % per16b == 0 && (d.b_kmajor ? d.N : g.Kd) >= 8) ? 1 : 0;
   if (d.lower_tiles && g.tiles_m != g.tiles_n) return hipErrorInvalidValue;
   const int64_t ntiles = d.lower_tiles ? g.tiles_m * (g.tiles_m + 1) / 2 : g.tiles_m * g.tiles_n;
   if (ntiles > 0x7fffffff) return hipErrorInvalidValue;
