@@ -97,23 +97,23 @@ __device__ __forceinline__ void load_step(const T* X, const T* p, int valid, T o
   }
 }
 
-// VEC path, at staging time: the real elements of a lane with 0 < valid < 8.
+// VEC path, at staging time: a lane with fewer than 8 real elements reads
+// them one by one and zeroes the rest.
 template <typename T, bool VEC>
 __device__ __forceinline__ void fix_step(const T* p, int valid, T out[8]) {
   if constexpr (VEC) {
-    if (valid > 0 && valid < 8) {
+    if (valid < 8) {
 #pragma unroll
-      for (int q = 0; q < 7; ++q)
-        if (q < valid) out[q] = p[q];
+      for (int q = 0; q < 8; ++q) out[q] = (q < valid) ? p[q] : T(0);
     }
   }
 }
 
-// The raw elements widened to fp64, zero past `valid`.
+// The raw elements widened to fp64 (elements past the real ones are zero).
 template <typename T>
-__device__ __forceinline__ void widen8(const T raw[8], int valid, double out[8]) {
+__device__ __forceinline__ void widen8(const T raw[8], double out[8]) {
 #pragma unroll
-  for (int q = 0; q < 8; ++q) out[q] = (q < valid) ? (double)raw[q] : 0.0;
+  for (int q = 0; q < 8; ++q) out[q] = (double)raw[q];
 }
 
 template <bool KMAJOR>
@@ -187,27 +187,48 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& g, int64_t ti, int64_t
 #pragma unroll
     for (int y = 0; y < 4; ++y) acc[x][y] = d4{0.0, 0.0, 0.0, 0.0};
 
-  // the next stage's operands, as stored in memory, and how many are real
+  // the next stage's operands, as stored in memory
   TA ra[2][8];
   TB rb[2][8], r2[BDIFF ? 2 : 1][8];
-  int va[2], vb[2];
-  int64_t kf = 0;   // first k of the stage in flight
+  int64_t kf = 0;      // first k of the stage in flight
+  bool full = false;   // that stage lies wholly inside the operands (wave-uniform)
+  // A stage is full when the tile's rows and its 32 k values lie inside the
+  // operands.  Its lanes then load from per-lane pointers set up once per
+  // tile and moved by one 64-bit add per stage; other stages take each lane's
+  // position and real-element count from step_ptr.
+  const bool rows_in = VEC && I0 + kTile <= g.M && J0 + kTile <= g.N;
+  const int64_t a_ks = AK ? g.lda : 1, b_ks = BK ? g.ldb : 1;
+  int unused;
+  const TA* a0 = step_ptr<TA, AK>(A, g.lda, g.M, g.Kd, I0, 0, tid, unused);
+  const TB* b0 = step_ptr<TB, BK>(B, g.ldb, g.N, g.Kd, J0, 0, tid, unused);
+  const int64_t d2 = BDIFF ? B2 - B : 0;   // B2 read at B's positions
   auto fetch = [&](int64_t k0) {
     kf = k0;
+    full = rows_in && k0 + kKC <= g.Kd;
+    if (full) {
 #pragma unroll
-    for (int h = 0; h < 2; ++h) {
-      const TA* pa = step_ptr<TA, AK>(A, g.lda, g.M, g.Kd, I0, k0 + h * kKH, tid, va[h]);
-      const TB* pb = step_ptr<TB, BK>(B, g.ldb, g.N, g.Kd, J0, k0 + h * kKH, tid, vb[h]);
-      load_step<TA, VEC>(A, pa, va[h], ra[h]);
-      load_step<TB, VEC>(B, pb, vb[h], rb[h]);
-      if constexpr (BDIFF) load_step<TB, VEC>(B2, B2 + (pb - B), vb[h], r2[h]);
+      for (int h = 0; h < 2; ++h) {
+        const TA* pa = a0 + (k0 + h * kKH) * a_ks;
+        const TB* pb = b0 + (k0 + h * kKH) * b_ks;
+        load_step<TA, true>(A, pa, 8, ra[h]);
+        load_step<TB, true>(B, pb, 8, rb[h]);
+        if constexpr (BDIFF) load_step<TB, true>(B2, pb + d2, 8, r2[h]);
+      }
+    } else {
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        int va, vb;
+        const TA* pa = step_ptr<TA, AK>(A, g.lda, g.M, g.Kd, I0, k0 + h * kKH, tid, va);
+        const TB* pb = step_ptr<TB, BK>(B, g.ldb, g.N, g.Kd, J0, k0 + h * kKH, tid, vb);
+        load_step<TA, VEC>(A, pa, va, ra[h]);
+        load_step<TB, VEC>(B, pb, vb, rb[h]);
+        if constexpr (BDIFF) load_step<TB, VEC>(B2, B2 + (pb - B), vb, r2[h]);
+      }
     }
   };
-  // VEC: lanes with a ragged step exist only where the tile or the stage
-  // crosses the operand's edge (the same for every lane)
-  const bool rows_in = I0 + kTile <= g.M && J0 + kTile <= g.N;
+  // VEC, stage not full: the real elements of lanes whose step is ragged
   auto fix = [&]() {
-    if (VEC && !(rows_in && kf + kKC <= g.Kd)) {
+    if (VEC && !full) {
 #pragma unroll
       for (int h = 0; h < 2; ++h) {
         int v;
@@ -230,14 +251,15 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& g, int64_t ti, int64_t
   for (int64_t c = 0; c < nck; ++c) {
     __syncthreads();
     fix();
+    // widen (B - B2: exact in fp64 for fp32 inputs) and stage into LDS
 #pragma unroll
     for (int h = 0; h < 2; ++h) {
       double wa[8], wb[8];
-      widen8<TA>(ra[h], va[h], wa);
-      widen8<TB>(rb[h], vb[h], wb);
-      if constexpr (BDIFF) {   // B - B2, exact in fp64 for fp32 inputs
+      widen8<TA>(ra[h], wa);
+      widen8<TB>(rb[h], wb);
+      if constexpr (BDIFF) {
         double w2[8];
-        widen8<TB>(r2[h], vb[h], w2);
+        widen8<TB>(r2[h], w2);
 #pragma unroll
         for (int q = 0; q < 8; ++q) wb[q] -= w2[q];
       }
