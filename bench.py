@@ -55,7 +55,74 @@ def parse():
                     help="columns of the oracle's timed solve/decode sample")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run one plain 1 GiB device copy (for scaling HBM counters)")
+    ap.add_argument("--sweep-k", metavar="SHAPES", default=None,
+                    help="instead of the benchmark line: one JSON line per (layer, K) with the "
+                         "layer time and the mean JTA residual, on the Llama-3-8B-shaped layers "
+                         "given as a comma list of l3_* keys or 'all'")
+    ap.add_argument("--k-values", default="0,1,5,10,25,50", help="K values of --sweep-k")
     return ap.parse_args()
+
+
+def sweep_k(args):
+    """Layer time and selected residual against K (the paper's ablation over
+    K and its figure of the per-layer time increase with K), one fresh layer
+    per K: Gram, factor, solves, decode and selection all rerun."""
+    import torch
+    import paper_2602_08376_amd as ok
+    from synth import LLAMA3_8B
+    from synth.workloads import activation_chunks, make_weights
+
+    keys = list(LLAMA3_8B) if args.sweep_k == "all" else args.sweep_k.split(",")
+    ks = [int(k) for k in args.k_values.split(",")]
+    dev = torch.device("cuda", 0)
+    torch.cuda.set_device(dev)
+    ok.library()
+    for key in keys:
+        cfg = LLAMA3_8B[key]
+        W = make_weights(cfg, device=dev)
+        chunks = list(activation_chunks(cfg, device=dev))
+        torch.cuda.synchronize()
+        log(f"sweep {key}: inputs generated")
+
+        def layer(K):
+            s = ok.LayerSolver(cfg.m, cfg.n, cfg.bits, cfg.group, K, cfg.klein_seed,
+                               cfg.lambda_rel, device=dev)
+            s.set_timing(True)
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+            s.set_weights(W)
+            for Xr, Xq in chunks:
+                s.accumulate(Xr, Xq)
+            out = s.solve(W, cfg.mu)
+            torch.cuda.synchronize()
+            t = time.perf_counter() - t0
+            stages = s.stage_times()
+            s.close()
+            return t, out, stages
+
+        layer(ks[0])   # warm-up: first launches of every kernel
+        base = None
+        for K in ks:
+            t, out, stages = layer(K)
+            res = out.residuals.double()
+            mean_r = float(res.mean())
+            if base is None:
+                base = (t, mean_r, res)
+            line = {
+                "sweep": "K", "workload": f"{key}: {cfg.title}", "K": K,
+                "n_out": cfg.n, "m_in": cfg.m, "tokens": cfg.T, "bits": cfg.bits,
+                "group": cfg.group, "alpha": cfg.mu,
+                "layer_time_s": t, "time_ratio_vs_first": t / base[0],
+                "decode_ms": stages["decode"],
+                "decode_paths_per_s": cfg.n * (K + 1) / (stages["decode"] * 1e-3),
+                "mean_residual": mean_r, "residual_ratio_vs_first": mean_r / base[1],
+                "columns_improved_vs_first": float((res < base[2]).double().mean()),
+                "klein_wins": float((out.winner > 0).double().mean()),
+            }
+            print(json.dumps(line), flush=True)
+            log(f"sweep {key} K={K}: {t * 1e3:.1f} ms, mean residual {mean_r:.6e}")
+        del W, chunks
+        torch.cuda.empty_cache()
 
 
 KERNEL_SOURCES = ("paper_2602_08376_amd/csrc/gram.hip", "paper_2602_08376_amd/csrc/device.h")
@@ -156,6 +223,9 @@ def main():
               "the path runs on a single GPU; sharding over columns is described in DESIGN.md",
               file=sys.stderr)
         sys.exit(2)
+    if args.sweep_k:
+        sweep_k(args)
+        return
 
     import torch
     import paper_2602_08376_amd as ok

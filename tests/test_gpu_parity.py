@@ -303,6 +303,31 @@ def test_mixed_chunks_and_bound_weights(m, n, bind):
     s.close()
 
 
+def test_large_k_and_k_sweep_invariants():
+    """K = 25 and 50, the top of the paper's K ablation, against the oracle;
+    and across the sweep: K = 1 draws greedily (alpha = inf), so it returns
+    the Babai point, and no K selects a worse candidate than that path."""
+    cfg = small_cfg(512, 12, 2048, 4, 128, 0, 51, mu=0.6)
+    W, Xr, Xq = make_layer(cfg, device=DEV)
+    runs = {}
+    for K in (0, 1, 25, 50):
+        g = ok.quantize_layer(W, Xr, Xq, 0.6, cfg.bits, cfg.group, K, cfg.klein_seed)
+        torch.cuda.synchronize()
+        runs[K] = g
+        if K >= 25:
+            o = orc.quantize_layer(np64(W), np64(Xr), np64(Xq), 0.6, cfg.bits, cfg.group, K,
+                                   cfg.klein_seed)
+            assert check_layer(cfg, g, o, 0.6) >= 0.999
+    r0 = np64(runs[0].residuals)
+    assert np.array_equal(np64(runs[1].codes), np64(runs[0].codes))
+    assert np.allclose(np64(runs[1].residuals), r0, rtol=1e-13, atol=0)
+    assert np.all(np64(runs[1].winner) == 0)
+    for K in (25, 50):
+        assert np.all(np64(runs[K].residuals) <= r0 * (1 + 1e-13)), K
+    print(f"[k sweep] mean residual K=0 {r0.mean():.4e}, K=25 {np64(runs[25].residuals).mean():.4e}, "
+          f"K=50 {np64(runs[50].residuals).mean():.4e}")
+
+
 def test_gram_load_paths_agree():
     """The Gram/cross contraction reads 16-byte runs of tokens when rows are
     16-byte aligned and T % 4 == 0, else single tokens; both paths stage the

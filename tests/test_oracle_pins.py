@@ -338,6 +338,25 @@ def test_invariants_layer():
     assert np.array_equal(a.codes, b.codes) and np.allclose(a.residuals, b.residuals, rtol=1e-9)
 
 
+def test_k_sweep_invariants():
+    """Across the K values of the paper's ablation: path 0 is the same Babai
+    point for every K, K = 1 is greedy (alpha = inf) and so repeats it, and
+    no K selects a candidate worse than that path (residuals compared to a
+    relative 1e-12: the oracle sums a path's residual in an order that
+    depends on how many paths it evaluates together)."""
+    W, Xr, Xq = small_layer(6, m=40, n=6, T=120)
+    runs = {K: o.quantize_layer(W, Xr, Xq, 0.6, 4, 16, K, 3) for K in (0, 1, 5, 25)}
+    babai = runs[0].codes
+    r0 = runs[0].residuals
+    for K, r in runs.items():
+        assert np.array_equal(r.decode.path_codes[:, 0], babai), K
+        assert np.all(r.residuals <= r0 * (1 + 1e-12)), K
+    assert np.array_equal(runs[1].codes, babai)
+    assert np.allclose(runs[1].residuals, r0, rtol=1e-12, atol=0)
+    assert np.all(runs[1].winner == 0)
+    assert runs[25].residuals.sum() < runs[0].residuals.sum()
+
+
 def test_scale_invariance():
     """X -> 2X scales the residuals by 4 with the same codes; W -> 2W scales s exactly."""
     W, Xr, Xq = small_layer(4, m=16, n=5, T=50)
