@@ -60,6 +60,8 @@ def parse():
                          "layer time and the mean JTA residual, on the Llama-3-8B-shaped layers "
                          "given as a comma list of l3_* keys or 'all'")
     ap.add_argument("--k-values", default="0,1,5,10,25,50", help="K values of --sweep-k")
+    ap.add_argument("--scheme", default="asym", choices=("asym", "sym"),
+                    help="scales and zero points: asymmetric min-max or symmetric Absmax")
     return ap.parse_args()
 
 
@@ -86,7 +88,7 @@ def sweep_k(args):
 
         def layer(K):
             s = ok.LayerSolver(cfg.m, cfg.n, cfg.bits, cfg.group, K, cfg.klein_seed,
-                               cfg.lambda_rel, device=dev)
+                               cfg.lambda_rel, device=dev, scheme=args.scheme)
             s.set_timing(True)
             torch.cuda.synchronize()
             t0 = time.perf_counter()
@@ -111,7 +113,7 @@ def sweep_k(args):
             line = {
                 "sweep": "K", "workload": f"{key}: {cfg.title}", "K": K,
                 "n_out": cfg.n, "m_in": cfg.m, "tokens": cfg.T, "bits": cfg.bits,
-                "group": cfg.group, "alpha": cfg.mu,
+                "group": cfg.group, "alpha": cfg.mu, "scheme": args.scheme,
                 "layer_time_s": t, "time_ratio_vs_first": t / base[0],
                 "decode_ms": stages["decode"],
                 "decode_paths_per_s": cfg.n * (K + 1) / (stages["decode"] * 1e-3),
@@ -162,7 +164,7 @@ def workload_desc(cfg):
     }
 
 
-def cpu_baseline(cfg, W, Xr, Xq, tokens, columns):
+def cpu_baseline(cfg, W, Xr, Xq, tokens, columns, scheme="asym"):
     """The oracle as it stands, timed stage by stage on a bounded sample, extrapolated."""
     import numpy as np
     from oracle import ojbkq as orc
@@ -178,7 +180,7 @@ def cpu_baseline(cfg, W, Xr, Xq, tokens, columns):
     Xqn = Xq[:, :Ts].cpu().numpy()
     t = {}
     t0 = time.perf_counter()
-    S, Z = orc.scales_zeros(Wn, cfg.bits, cfg.group)
+    S, Z = orc.scales_zeros(Wn, cfg.bits, cfg.group, scheme)
     t["scales"] = time.perf_counter() - t0
     t0 = time.perf_counter()
     G = orc.gram(Xqn)
@@ -252,7 +254,7 @@ def main():
 
     def step(record):
         s = ok.LayerSolver(cfg.m, cfg.n, cfg.bits, cfg.group, cfg.K, cfg.klein_seed,
-                           cfg.lambda_rel, device=dev, workspace=ws)
+                           cfg.lambda_rel, device=dev, workspace=ws, scheme=args.scheme)
         s.set_timing(True)                        # per-stage HIP events inside the library
         s.set_weights(W)                          # lets thin layers skip the m x m cross term
         ev = [torch.cuda.Event(enable_timing=True) for _ in range(2 * len(chunks) + 1)]
@@ -314,7 +316,7 @@ def main():
         "vs_baseline": None,
         "dtype": "f64",
         "data": "synthetic (seeded, generated on the GPU; inputs resident in HBM)",
-        "config": workload_desc(cfg),
+        "config": {**workload_desc(cfg), **({"scheme": "sym"} if args.scheme == "sym" else {})},
         "stages_ms": {"gram_cross_per_launch": gc_avg,
                       "rest_of_path": sum(solve_ms) / len(solve_ms),
                       **{f"library_{k}": v for k, v in stage_ms.items()}},
@@ -354,7 +356,8 @@ def main():
     if not args.no_cpu_baseline:
         log("timing the CPU oracle on a bounded sample")
         Xr0, Xq0 = chunks[0]
-        result["cpu_baseline"] = cpu_baseline(cfg, W, Xr0, Xq0, args.cpu_tokens, args.cpu_columns)
+        result["cpu_baseline"] = cpu_baseline(cfg, W, Xr0, Xq0, args.cpu_tokens, args.cpu_columns,
+                                              args.scheme)
     print(json.dumps(result), flush=True)
 
 

@@ -86,7 +86,15 @@ typedef struct {
   int32_t bits;        /* box {0 .. 2^bits - 1}, 1 <= bits <= 8               */
   int32_t group;       /* rows per scale group; <= 0 or >= m: one group       */
   int32_t K;           /* Klein samples (>= 0); K + 1 candidates per column   */
-  int32_t reserved;    /* must be 0                                           */
+  int32_t scheme;      /* scales and zero points (Sec. 3.2; the paper names
+                          Absmax calibration as an example), per group:
+                          0: asymmetric min-max, range widened to hold 0,
+                             s = (max(w,0) - min(w,0)) / (2^bits - 1),
+                             z = rint(-min(w,0) / s);
+                          1: symmetric Absmax, z = 2^(bits-1),
+                             s = max|w| / (2^(bits-1) - 1), bits >= 2;
+                          s is rounded to float32 once; an all-zero group
+                          uses [-1, 1] (0) or max|w| = 1 (1)                */
   double alpha;        /* the JTA knob mu of Eq. jta_target, 0 <= alpha <= 1  */
   double lambda_rel;   /* lambda^2 = lambda_rel * mean(diag(X~^T X~)), >= 0   */
   uint64_t seed;       /* Philox key for the Klein draws                      */

@@ -24,6 +24,10 @@ W is [n, m] (row j = the paper's column w_j), X_ref and X_q are [m, T]
   * scale/zero: asymmetric min-max over each group with the range widened to
     contain 0; an all-zero group uses [-1, 1]; the scale is stored in float32
     and that stored value is the one the decode uses; z = rint(-xmin / s).
+    The symmetric Absmax variant (the calibration the paper names as an
+    example): z = 2^(bits-1) and s = max|w| / (2^(bits-1) - 1) in float32,
+    so that the grid s (q - z) holds +max|w| and -max|w| (all-zero group:
+    max|w| = 1); it needs bits >= 2.
   * lambda^2 = lambda_rel * mean(diag(X~^T X~)) on the unnormalised Gram.
   * A^T y of Alg. 1 step 3 is A^T t_j = X~^T y*_j + lambda^2 w_j.
   * qbar = v / s + z (Alg. 1 step 4; the derivation text drops the +z).
@@ -66,16 +70,20 @@ def num_groups(m: int, group: int) -> int:
     return (m + g - 1) // g
 
 
-def scales_zeros(W: np.ndarray, bits: int, group: int):
+def scales_zeros(W: np.ndarray, bits: int, group: int, scheme: str = "asym"):
     """Per (column, group) scale s and zero point z from the float32 weights.
 
-    W_hat = S * (Q - Z) must be able to represent 0 and the group's extreme
-    values, so the range is [min(w, 0), max(w, 0)] spread over the
-    2^bits - 1 steps of the box.  Returns (S, Z) as float32 [n, groups].
+    "asym": W_hat = S * (Q - Z) must be able to represent 0 and the group's
+    extreme values, so the range is [min(w, 0), max(w, 0)] spread over the
+    2^bits - 1 steps of the box.  "sym" (Absmax): the zero point is the middle
+    of the box, 2^(bits-1), and the scale maps max|w| to the 2^(bits-1) - 1
+    steps above it.  Returns (S, Z) as float32 [n, groups].
     """
     W = np.asarray(W)
     n, m = W.shape
     qmax = (1 << bits) - 1
+    if scheme not in ("asym", "sym") or (scheme == "sym" and bits < 2):
+        raise ValueError("scheme must be 'asym', or 'sym' with bits >= 2")
     g = group_size(m, group)
     G = num_groups(m, group)
     S = np.empty((n, G), dtype=np.float32)
@@ -83,6 +91,14 @@ def scales_zeros(W: np.ndarray, bits: int, group: int):
     for j in range(n):
         for t in range(G):
             w = W[j, t * g:min(m, (t + 1) * g)].astype(np.float64)
+            if scheme == "sym":
+                a = float(np.abs(w).max())
+                if a == 0.0:
+                    a = 1.0
+                half = 1 << (bits - 1)
+                S[j, t] = np.float32(a / (half - 1))
+                Z[j, t] = half
+                continue
             xmin = min(float(w.min()), 0.0)
             xmax = max(float(w.max()), 0.0)
             if xmax == xmin:
@@ -339,15 +355,17 @@ class LayerResult:
 
 
 def quantize_layer(W, X_ref, X_q, mu: float, bits: int, group: int, K: int, seed: int,
-                   lambda_rel: float = 0.01, columns=None, G: Optional[np.ndarray] = None) -> LayerResult:
+                   lambda_rel: float = 0.01, columns=None, G: Optional[np.ndarray] = None,
+                   scheme: str = "asym") -> LayerResult:
     """The per-layer path end to end.
 
     ``columns`` restricts the decode (not the scales, Gram or factor) to a
     subset of output channels; ``G`` may pass a Gram the caller already
-    formed with :func:`gram` on the same X_q.
+    formed with :func:`gram` on the same X_q; ``scheme`` picks the scale and
+    zero-point rule (see :func:`scales_zeros`).
     """
     W = np.asarray(W)
-    S, Z = scales_zeros(W, bits, group)
+    S, Z = scales_zeros(W, bits, group, scheme)
     Gm = gram(X_q) if G is None else G
     lam2 = damping(Gm, lambda_rel)
     H = Gm + lam2 * np.eye(Gm.shape[0])

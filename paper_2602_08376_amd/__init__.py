@@ -51,7 +51,7 @@ class OjbkqError(RuntimeError):
 class Params(ctypes.Structure):
     _fields_ = [
         ("m", ctypes.c_int64), ("n", ctypes.c_int64), ("bits", ctypes.c_int32),
-        ("group", ctypes.c_int32), ("K", ctypes.c_int32), ("reserved", ctypes.c_int32),
+        ("group", ctypes.c_int32), ("K", ctypes.c_int32), ("scheme", ctypes.c_int32),
         ("alpha", ctypes.c_double), ("lambda_rel", ctypes.c_double), ("seed", ctypes.c_uint64),
     ]
 
@@ -101,8 +101,13 @@ def _check(rc: int):
         raise OjbkqError(rc, msg)
 
 
-def _params(m, n, bits, group, K, alpha, lambda_rel, seed) -> Params:
-    return Params(int(m), int(n), int(bits), int(group), int(K), 0, float(alpha),
+SCHEMES = {"asym": 0, "sym": 1}   # scale / zero-point rule (ojbkq_params.scheme)
+
+
+def _params(m, n, bits, group, K, alpha, lambda_rel, seed, scheme="asym") -> Params:
+    if scheme not in SCHEMES:
+        raise ValueError(f"scheme must be one of {sorted(SCHEMES)}")
+    return Params(int(m), int(n), int(bits), int(group), int(K), SCHEMES[scheme], float(alpha),
                   float(lambda_rel), int(seed) & 0xFFFFFFFFFFFFFFFF)
 
 
@@ -190,10 +195,11 @@ def _outputs(n, m, G, device):
 
 
 def quantize_layer(W, X_ref, X_q, alpha, bits, group, K, seed, lambda_rel=0.01,
-                   workspace: Optional[torch.Tensor] = None) -> QuantResult:
+                   workspace: Optional[torch.Tensor] = None, scheme="asym") -> QuantResult:
     """One-shot ``ojbkq_quantize_layer`` on device tensors.
 
-    W [n, m] float32; X_ref, X_q [m, T] float32 (X_ref may be None or X_q).
+    W [n, m] float32; X_ref, X_q [m, T] float32 (X_ref may be None or X_q);
+    scheme: "asym" (min-max) or "sym" (Absmax) scales and zero points.
     """
     n, m = W.shape
     dev = W.device
@@ -206,7 +212,7 @@ def quantize_layer(W, X_ref, X_q, alpha, bits, group, K, seed, lambda_rel=0.01,
         _need(X_ref, "X_ref", torch.float32, device=dev)
         if tuple(X_ref.shape) != tuple(X_q.shape) or X_ref.stride() != X_q.stride():
             raise ValueError("X_ref must have the shape and strides of X_q")
-    p = _params(m, n, bits, group, K, alpha, lambda_rel, seed)
+    p = _params(m, n, bits, group, K, alpha, lambda_rel, seed, scheme)
     lib = library()
     need = lib.ojbkq_workspace_bytes(ctypes.byref(p))
     if need == 0:
@@ -225,12 +231,12 @@ class LayerSolver:
     """Staged form: accumulate token chunks, then solve for one or more knobs."""
 
     def __init__(self, m, n, bits, group, K, seed, lambda_rel=0.01, device="cuda",
-                 workspace: Optional[torch.Tensor] = None):
+                 workspace: Optional[torch.Tensor] = None, scheme="asym"):
         self.m, self.n, self.bits, self.group, self.K = int(m), int(n), bits, group, K
         self.device = torch.device(device)
         if self.device.index is None:
             self.device = torch.device("cuda", torch.cuda.current_device())
-        self.p = _params(m, n, bits, group, K, 0.5, lambda_rel, seed)
+        self.p = _params(m, n, bits, group, K, 0.5, lambda_rel, seed, scheme)
         lib = library()
         need = lib.ojbkq_workspace_bytes(ctypes.byref(self.p))
         if need == 0:

@@ -157,7 +157,8 @@ int check_params(const ojbkq_params* p) {
   if (p->n < 1 || p->n > (int64_t)1 << 24) return fail(OJBKQ_EINVAL, "n must be in [1, 2^24]");
   if (p->bits < 1 || p->bits > 8) return fail(OJBKQ_EINVAL, "bits must be in [1, 8]");
   if (p->K < 0 || p->K > (1 << 20)) return fail(OJBKQ_EINVAL, "K must be in [0, 2^20]");
-  if (p->reserved != 0) return fail(OJBKQ_EINVAL, "reserved must be 0");
+  if (p->scheme != 0 && p->scheme != 1) return fail(OJBKQ_EINVAL, "scheme must be 0 or 1");
+  if (p->scheme == 1 && p->bits < 2) return fail(OJBKQ_EINVAL, "the symmetric scheme needs bits >= 2");
   if (!(p->alpha >= 0.0 && p->alpha <= 1.0)) return fail(OJBKQ_EINVAL, "alpha must be in [0, 1]");
   if (!(p->lambda_rel >= 0.0) || !std::isfinite(p->lambda_rel))
     return fail(OJBKQ_EINVAL, "lambda_rel must be finite and >= 0");
@@ -408,7 +409,8 @@ int ctx_solve(ojbkq_ctx* c, const float* W, double alpha, uint8_t* codes, float*
     stage_end(c, OJBKQ_STAGE_FACTOR, t0);
     t0 = stage_begin(c);
   }
-  OJBKQ_HIP(ojbkq::launch_scale_zero(W, s.n, s.m, s.g, s.G, s.qmax, scales, zeros, st),
+  OJBKQ_HIP(ojbkq::launch_scale_zero(W, s.n, s.m, s.g, s.G, c->p.bits, c->p.scheme == 1, scales,
+                                     zeros, st),
             "scales");
   double* gq = c->at<double>(c->L.gq);
   const bool cross = c->cross_seen && alpha != 1.0;

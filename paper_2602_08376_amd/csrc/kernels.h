@@ -71,8 +71,10 @@ hipError_t cross_from_mixed(double* E, const double* G, int64_t m, hipStream_t s
 hipError_t mixed_from_gram(double* E, const double* G, int64_t m, hipStream_t stream);
 
 // ---- scales and zero points (Alg. 1 step 1) --------------------------------
-hipError_t launch_scale_zero(const float* W, int64_t n, int64_t m, int64_t g, int64_t G, int qmax,
-                             float* S, float* Z, hipStream_t stream);
+// Per (column, group) of W [n, m]: asymmetric min-max, or with `symmetric`
+// the Absmax rule (z = 2^(bits-1), s = max|w| / (2^(bits-1) - 1)).
+hipError_t launch_scale_zero(const float* W, int64_t n, int64_t m, int64_t g, int64_t G, int bits,
+                             bool symmetric, float* S, float* Z, hipStream_t stream);
 
 // ---- damping and factorisation (Alg. 1 step 2) -----------------------------
 // H (lower triangle, row-major, ld = m) += lambda_rel * mean(diag(H)) * I;

@@ -12,10 +12,14 @@ namespace {
 // the range widened to contain 0 (so the grid represents 0 exactly); an
 // all-zero group uses [-1, 1].  The scale is rounded to float32 once and the
 // zero point is taken against that stored value: z = rint(-xmin / s).
+// Symmetric (Absmax): the zero point is the middle of the box, half =
+// 2^(bits-1), and s = max|w| / (half - 1) puts +-max|w| on the grid; an
+// all-zero group uses max|w| = 1.
 __global__ __launch_bounds__(256) void scale_zero_kernel(const float* __restrict__ W, int64_t n,
-                                                         int64_t m, int64_t g, int64_t G, int qmax,
-                                                         float* __restrict__ S,
+                                                         int64_t m, int64_t g, int64_t G, int bits,
+                                                         int symmetric, float* __restrict__ S,
                                                          float* __restrict__ Z) {
+  const int qmax = (1 << bits) - 1;
   const int lane = threadIdx.x & 63;
   const int64_t gid = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
   if (gid >= n * G) return;
@@ -32,7 +36,13 @@ __global__ __launch_bounds__(256) void scale_zero_kernel(const float* __restrict
     mn = fminf(mn, __shfl_xor(mn, off, 64));
     mx = fmaxf(mx, __shfl_xor(mx, off, 64));
   }
-  if (lane == 0) {
+  if (lane == 0 && symmetric) {
+    const int half = 1 << (bits - 1);
+    double a = fmax(-(double)mn, (double)mx);
+    if (a == 0.0) a = 1.0;
+    S[gid] = (float)(a / (double)(half - 1));
+    Z[gid] = (float)half;
+  } else if (lane == 0) {
     double xmin = (double)mn < 0.0 ? (double)mn : 0.0;
     double xmax = (double)mx > 0.0 ? (double)mx : 0.0;
     if (xmax == xmin) {
@@ -112,10 +122,11 @@ unsigned grid_for(int64_t total) {
 
 }  // namespace
 
-hipError_t launch_scale_zero(const float* W, int64_t n, int64_t m, int64_t g, int64_t G, int qmax,
-                             float* S, float* Z, hipStream_t stream) {
+hipError_t launch_scale_zero(const float* W, int64_t n, int64_t m, int64_t g, int64_t G, int bits,
+                             bool symmetric, float* S, float* Z, hipStream_t stream) {
   const int64_t groups = n * G;
-  scale_zero_kernel<<<(unsigned)((groups + 3) / 4), 256, 0, stream>>>(W, n, m, g, G, qmax, S, Z);
+  scale_zero_kernel<<<(unsigned)((groups + 3) / 4), 256, 0, stream>>>(W, n, m, g, G, bits,
+                                                                      symmetric ? 1 : 0, S, Z);
   return hipGetLastError();
 }
 

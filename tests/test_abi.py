@@ -56,11 +56,15 @@ def test_bad_params_rejected(bad):
     assert lib.ojbkq_last_error().decode()
 
 
-def test_reserved_must_be_zero():
+def test_scheme_values():
     lib = ok.library()
-    p = _p()
-    p.reserved = 1
-    assert lib.ojbkq_workspace_bytes(ctypes.byref(p)) == 0
+    for scheme, bits, ok_ in ((0, 4, True), (1, 4, True), (1, 2, True), (1, 1, False),
+                              (0, 1, True), (2, 4, False), (-1, 4, False)):
+        p = _p(bits=bits)
+        p.scheme = scheme
+        assert (lib.ojbkq_workspace_bytes(ctypes.byref(p)) > 0) == ok_, (scheme, bits)
+    with pytest.raises(ValueError):
+        ok._params(128, 64, 4, 128, 4, 0.5, 0.01, 0, "absmax")
 
 
 def test_null_and_shape_errors_before_any_launch():

@@ -328,6 +328,28 @@ def test_large_k_and_k_sweep_invariants():
           f"K=50 {np64(runs[50].residuals).mean():.4e}")
 
 
+@pytest.mark.parametrize("m,n,bits,group,K,mu", [
+    (300, 40, 4, 128, 6, 0.6),    # projected cross term, ragged group
+    (130, 70, 3, 0, 4, 0.5),      # one group per column, mixed-product route
+    (96, 8, 2, 32, 3, 1.0),       # 2-bit box (z = 2, s = max|w|), no cross term
+])
+def test_symmetric_absmax_scales(m, n, bits, group, K, mu):
+    """The symmetric Absmax scales and zero points end to end against the oracle."""
+    cfg = small_cfg(m, n, 4 * m + 17, bits, group, K, 61 + bits)
+    W, Xr, Xq = make_layer(cfg, device=DEV)
+    g = ok.quantize_layer(W, Xr, Xq, mu, bits, group, K, cfg.klein_seed, scheme="sym")
+    torch.cuda.synchronize()
+    o = orc.quantize_layer(np64(W), np64(Xr), np64(Xq), mu, bits, group, K, cfg.klein_seed,
+                           scheme="sym")
+    assert np.all(np64(g.zeros) == 2 ** (bits - 1))
+    assert check_layer(cfg, g, o, mu) >= 0.999
+    s = ok.LayerSolver(m, n, bits, group, K, cfg.klein_seed, device=DEV, scheme="sym")
+    s.accumulate(Xr, Xq)
+    st = s.solve(W, mu)
+    s.close()
+    assert torch.equal(st.codes, g.codes) and torch.equal(st.scales, g.scales)
+
+
 def test_gram_load_paths_agree():
     """The Gram/cross contraction reads 16-byte runs of tokens when rows are
     16-byte aligned and T % 4 == 0, else single tokens; both paths stage the

@@ -86,6 +86,57 @@ def test_scale_zero_properties(bits):
     assert np.array_equal(S1, S2)
 
 
+@pytest.mark.parametrize("bits", [2, 3, 4, 8])
+def test_symmetric_absmax_scale_zero(bits):
+    """Absmax: the box middle is the zero point and +-max|w| lie on the grid;
+    the rule is odd in w (a sign flip keeps s and z) and commutes with
+    power-of-two rescaling."""
+    rng = np.random.default_rng(40 + bits)
+    half = 2 ** (bits - 1)
+    m, group = 200, 128
+    W = (rng.standard_normal((7, m)) * 0.02).astype(np.float32)
+    W[3, :128] = 0.0
+    S, Z = o.scales_zeros(W, bits, group, "sym")
+    assert S.dtype == np.float32 and np.all(Z == half)
+    assert S[3, 0] == np.float32(1.0 / (half - 1))                  # all-zero group: max|w| = 1
+    for j in range(7):
+        for t, (a, b) in enumerate([(0, 128), (128, 200)]):
+            amax = float(np.abs(W[j, a:b]).max())
+            if amax == 0.0:
+                continue
+            s = float(S[j, t])
+            # +max|w| at v = 2 half - 1 and -max|w| at v = 1, to float32 rounding of s
+            assert abs(s * (half - 1) - amax) <= (half - 1) * 2.0 ** -24 * s
+            # every weight rounds onto the box with at most half a step of error
+            v = np.rint(W[j, a:b].astype(np.float64) / s + half)
+            assert v.min() >= 0 and v.max() <= 2 * half - 1
+            assert np.max(np.abs(s * (v - half) - W[j, a:b])) <= 0.5 * s * (1 + 1e-6)
+    Sn, Zn = o.scales_zeros(-W, bits, group, "sym")
+    assert np.array_equal(Sn, S) and np.array_equal(Zn, Z)
+    S4, _ = o.scales_zeros(4 * W, bits, group, "sym")
+    nz = np.abs(W[:, :128]).max(axis=1) > 0
+    assert np.array_equal(S4[nz, 0], 4 * S[nz, 0])
+    with pytest.raises(ValueError):
+        o.scales_zeros(W, 1, group, "sym")
+
+
+def test_symmetric_scales_through_the_layer():
+    """With the problem separated (orthogonal activations, mu = 1) Babai is
+    RTN on the symmetric grid as well, and the optimum."""
+    rng = np.random.default_rng(5)
+    m, n, T = 6, 4, 6
+    Xq = np.diag(np.exp(rng.standard_normal(m))).astype(np.float32) @ np.eye(m, T, dtype=np.float32)
+    W = (rng.standard_normal((n, m)) * 0.3).astype(np.float32)
+    res = o.quantize_layer(W, Xq, Xq, 1.0, 2, 128, 3, 0, lambda_rel=0.0, scheme="sym")
+    assert np.all(res.zeros == 2)
+    rtn = np.clip(np.rint(W / res.scales.astype(np.float64) + 2), 0, 3)
+    assert np.array_equal(res.codes, rtn.astype(np.uint8))
+    for j in range(n):
+        Rb = res.R * o.expand_groups(res.scales[j:j + 1], m, 128)[0][None, :]
+        _, r_opt = brute_force_opt(Rb, res.qbar[j], 3)
+        assert abs(res.residuals[j] - r_opt) <= 1e-9 * max(1, r_opt)
+
+
 # ---------------------------------------------------------------------------
 # Klein temperature: K = (e rho)^(2m / rho)
 # ---------------------------------------------------------------------------
