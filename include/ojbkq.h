@@ -201,6 +201,35 @@ int ojbkq_decode_stage(const ojbkq_params* p, const double* R, const double* qba
  * (greedy rounding); ln K >= 2m: 0 (flat sampling); m < 1: NaN.           */
 double ojbkq_klein_log_rho(int64_t m, int64_t K);
 
+/* The quantized layer in use.  A layer quantized by the calls above is
+ * applied as W_hat = S (Q - Z) (the Q, S, Z data model of Sec. 3.2); when a
+ * model is quantized layer by layer, each layer's X~ (Sec. 3.1) is the
+ * output of the layers already quantized, formed with this product.
+ *
+ * ojbkq_packed_words: 32-bit words per packed row of m codes of `bits` bits
+ *   (0 for m < 1 or bits outside [1, 8]).  Host-only.
+ * ojbkq_pack_codes: codes [n, m] uint8 (device) -> packed [n, words] uint32
+ *   (device, caller-owned): row j is the little-endian bit stream of its codes,
+ *   code i at bits [i bits, (i + 1) bits) counted from bit 0 of word 0, zero
+ *   past the last code.  Only the low `bits` bits of each code are read.
+ *   Asynchronous on `stream`; EINVAL for bad sizes or NULL pointers.
+ * ojbkq_dequant_matmul: Y [n, T] float32 (row stride ldy >= T)
+ *   = W_hat [n, m] X [m, T], with X IEEE binary16 (fp16 bits as uint16_t),
+ *   row stride ldx >= T, and W_hat[j][i] = fp16(fp32(s (q - z))): the
+ *   product s (q - z) rounded to float32, then to fp16, both to nearest even;
+ *   products of fp16 values are exact in float32 and summed in float32.
+ *   scales, zeros: [n, ceil(m / g)] float32 as returned by the quantize calls
+ *   for `group` (g = group, or m when group <= 0 or >= m); needs g % 16 == 0
+ *   or g == m (EINVAL otherwise).  packed as written by ojbkq_pack_codes.
+ *   All pointers device, caller-owned; asynchronous on `stream`; allocates
+ *   nothing.                                                             */
+int64_t ojbkq_packed_words(int64_t m, int32_t bits);
+int ojbkq_pack_codes(const uint8_t* codes, int64_t n, int64_t m, int32_t bits, uint32_t* packed,
+                     void* stream);
+int ojbkq_dequant_matmul(const uint32_t* packed, const float* scales, const float* zeros,
+                         int64_t n, int64_t m, int32_t bits, int32_t group, const uint16_t* X,
+                         int64_t T, int64_t ldx, float* Y, int64_t ldy, void* stream);
+
 /* Message of the last failure on this thread ("" if none). */
 const char* ojbkq_last_error(void);
 

@@ -31,7 +31,8 @@ ABI_FUNCTIONS = (
     "ojbkq_workspace_bytes", "ojbkq_quantize_layer", "ojbkq_create", "ojbkq_accumulate",
     "ojbkq_solve", "ojbkq_destroy", "ojbkq_inspect", "ojbkq_decode_workspace_bytes",
     "ojbkq_decode_stage", "ojbkq_klein_log_rho", "ojbkq_last_error", "ojbkq_set_timing",
-    "ojbkq_stage_times", "ojbkq_set_weights",
+    "ojbkq_stage_times", "ojbkq_set_weights", "ojbkq_packed_words", "ojbkq_pack_codes",
+    "ojbkq_dequant_matmul",
 )
 
 STAGES = ("gram", "factor", "solve", "centres", "decode", "select")
@@ -76,6 +77,10 @@ def library() -> ctypes.CDLL:
                                                 vp, vp, vp, vp, vp]),
         "ojbkq_create": (ctypes.c_int, [P, vp, ctypes.c_size_t, vp, ctypes.POINTER(vp)]),
         "ojbkq_set_weights": (ctypes.c_int, [vp, vp]),
+        "ojbkq_packed_words": (i64, [i64, ctypes.c_int32]),
+        "ojbkq_pack_codes": (ctypes.c_int, [vp, i64, i64, ctypes.c_int32, vp, vp]),
+        "ojbkq_dequant_matmul": (ctypes.c_int, [vp, vp, vp, i64, i64, ctypes.c_int32,
+                                                ctypes.c_int32, vp, i64, i64, vp, i64, vp]),
         "ojbkq_accumulate": (ctypes.c_int, [vp, vp, vp, i64, i64]),
         "ojbkq_solve": (ctypes.c_int, [vp, vp, dp, vp, vp, vp, vp, vp]),
         "ojbkq_destroy": (ctypes.c_int, [vp]),
@@ -341,3 +346,52 @@ def decode_stage(R, qbar, scales, bits, group, K, seed, want_paths=False):
 def klein_log_rho(m: int, K: int) -> float:
     """Host-side ``ojbkq_klein_log_rho`` (no GPU needed)."""
     return float(library().ojbkq_klein_log_rho(int(m), int(K)))
+
+
+# ---------------------------------------------------------------------------
+# the quantized layer in use: packed codes and W_hat X
+# ---------------------------------------------------------------------------
+
+def packed_words(m: int, bits: int) -> int:
+    """32-bit words per packed row (``ojbkq_packed_words``)."""
+    w = library().ojbkq_packed_words(int(m), int(bits))
+    if w <= 0:
+        raise ValueError("need m >= 1 and bits in [1, 8]")
+    return int(w)
+
+
+def pack_codes(codes: torch.Tensor, bits: int) -> torch.Tensor:
+    """``ojbkq_pack_codes``: codes [n, m] uint8 -> [n, words] int32 holding the
+    uint32 bit streams."""
+    _need(codes, "codes", torch.uint8)
+    if codes.dim() != 2 or not codes.is_contiguous():
+        raise ValueError("codes must be a contiguous [n, m] tensor")
+    n, m = codes.shape
+    out = torch.empty(n, packed_words(m, bits), dtype=torch.int32, device=codes.device)
+    _check(library().ojbkq_pack_codes(_ptr(codes), n, m, int(bits), _ptr(out),
+                                      _stream(codes.device)))
+    return out
+
+
+def dequant_matmul(packed: torch.Tensor, scales: torch.Tensor, zeros: torch.Tensor, m: int,
+                   bits: int, group: int, X: torch.Tensor) -> torch.Tensor:
+    """``ojbkq_dequant_matmul``: Y [n, T] float32 = W_hat [n, m] X [m, T] with
+    X float16 (rows contiguous) and W_hat from the packed codes."""
+    dev = packed.device
+    _need(packed, "packed", torch.int32, device=dev)
+    n = packed.shape[0]
+    G = num_groups(m, group)
+    _need(scales, "scales", torch.float32, (n, G), dev)
+    _need(zeros, "zeros", torch.float32, (n, G), dev)
+    _need(X, "X", torch.float16, device=dev)
+    if packed.shape != (n, packed_words(m, bits)) or not packed.is_contiguous():
+        raise ValueError("packed must be [n, packed_words(m, bits)] and contiguous")
+    if not (scales.is_contiguous() and zeros.is_contiguous()):
+        raise ValueError("scales and zeros must be contiguous")
+    T, ld = _rows_view(X, "X", m)
+    Y = torch.empty(n, T, dtype=torch.float32, device=dev)
+    _check(library().ojbkq_dequant_matmul(_ptr(packed), _ptr(scales), _ptr(zeros), n, m,
+                                          int(bits), int(group), _ptr(X), T, ld, _ptr(Y), T,
+                                          _stream(dev)))
+    return Y
+

@@ -20,7 +20,8 @@ INCLUDE = os.path.join(ROOT, "include")
 BUILD_DIR = os.path.join(ROOT, "_build")
 LIB = os.path.join(PKG, "libojbkq.so")
 
-SOURCES = ["api.cpp", "gemm.hip", "gram.hip", "factor.hip", "quant.hip", "decode.hip"]
+SOURCES = ["api.cpp", "gemm.hip", "gram.hip", "factor.hip", "quant.hip", "decode.hip",
+           "infer.hip"]
 
 HIPCC_FLAGS = [
     "-O3", "-std=c++17", "-fPIC", "--offload-arch=gfx950",

@@ -545,6 +545,42 @@ int ojbkq_create(const ojbkq_params* p, void* workspace, size_t workspace_bytes,
   return OJBKQ_OK;
 }
 
+int64_t ojbkq_packed_words(int64_t m, int32_t bits) {
+  if (m < 1 || bits < 1 || bits > 8) return 0;
+  return ojbkq::packed_words(m, bits);
+}
+
+int ojbkq_pack_codes(const uint8_t* codes, int64_t n, int64_t m, int32_t bits, uint32_t* packed,
+                     void* stream) {
+  g_error.clear();
+  if (!codes || !packed) return fail(OJBKQ_EINVAL, "codes and packed are required");
+  if (n < 1 || m < 1 || bits < 1 || bits > 8)
+    return fail(OJBKQ_EINVAL, "need n >= 1, m >= 1 and bits in [1, 8]");
+  if (n > (int64_t)1 << 24 || m > (int64_t)1 << 20) return fail(OJBKQ_EINVAL, "n or m too large");
+  OJBKQ_HIP(ojbkq::launch_pack_codes(codes, n, m, bits, packed, static_cast<hipStream_t>(stream)),
+            "pack codes");
+  return OJBKQ_OK;
+}
+
+int ojbkq_dequant_matmul(const uint32_t* packed, const float* scales, const float* zeros,
+                         int64_t n, int64_t m, int32_t bits, int32_t group, const uint16_t* X,
+                         int64_t T, int64_t ldx, float* Y, int64_t ldy, void* stream) {
+  g_error.clear();
+  if (!packed || !scales || !zeros || !X || !Y)
+    return fail(OJBKQ_EINVAL, "packed, scales, zeros, X and Y are required");
+  if (n < 1 || m < 1 || T < 1 || bits < 1 || bits > 8)
+    return fail(OJBKQ_EINVAL, "need n, m, T >= 1 and bits in [1, 8]");
+  if (n > (int64_t)1 << 24 || m > (int64_t)1 << 20) return fail(OJBKQ_EINVAL, "n or m too large");
+  if (ldx < T || ldy < T) return fail(OJBKQ_EINVAL, "ldx and ldy must be >= T");
+  const int64_t g = (group <= 0 || group >= m) ? m : group;
+  if (g % 16 != 0 && g != m)
+    return fail(OJBKQ_EINVAL, "the group must be a multiple of 16 (or the whole column)");
+  OJBKQ_HIP(ojbkq::launch_dequant_matmul(packed, scales, zeros, n, m, bits, g, X, T, ldx, Y, ldy,
+                                         static_cast<hipStream_t>(stream)),
+            "dequantize and multiply");
+  return OJBKQ_OK;
+}
+
 int ojbkq_set_weights(ojbkq_ctx* ctx, const float* W) {
   g_error.clear();
   if (!ctx) return fail(OJBKQ_EINVAL, "ctx is NULL");

@@ -213,6 +213,20 @@ struct DecodeDesc {
 
 hipError_t launch_decode(const DecodeDesc& d, hipStream_t stream);
 
+// ---- the quantized layer in use (packing, dequantize-and-multiply) ----------
+// Words per packed row of m codes of `bits` bits.
+int64_t packed_words(int64_t m, int bits);
+// P [n, packed_words(m, bits)] uint32: row j is the little-endian bit stream
+// of codes[j][0..m), code i at bits [i bits, (i + 1) bits), zero past the end.
+hipError_t launch_pack_codes(const uint8_t* codes, int64_t n, int64_t m, int bits, uint32_t* P,
+                             hipStream_t stream);
+// Y [n, T] (row stride ldy) = W_hat X, W_hat[j][i] = fp16(fp32(s (q - z)))
+// from P and the [n, ceil(m / g)] scales / zero points; X [m, T] fp16 bits,
+// row stride ldx.  Needs g % 16 == 0 or g == m.
+hipError_t launch_dequant_matmul(const uint32_t* P, const float* S, const float* Z, int64_t n,
+                                 int64_t m, int bits, int64_t g, const uint16_t* X, int64_t T,
+                                 int64_t ldx, float* Y, int64_t ldy, hipStream_t stream);
+
 // First strict minimum over the K + 1 candidates of each column; gathers the
 // winner's codes.  path_codes / path_resid / winner may be null.
 hipError_t launch_select(const uint8_t* pcodes, const double* presid, int64_t n, int64_t m, int K,

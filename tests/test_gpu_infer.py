@@ -1,0 +1,85 @@
+"""GPU parity of the quantized layer in use: packed codes (bit-exact) and the
+dequantize-and-multiply product against the CPU oracle (``oracle/infer.py``),
+through the C ABI."""
+
+import numpy as np
+import pytest
+import torch
+
+import paper_2602_08376_amd as ok
+from oracle import infer as oi
+from oracle import ojbkq as orc
+from parity import np64
+from synth import LayerConfig, make_layer
+
+pytestmark = pytest.mark.gpu
+DEV = "cuda"
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    ok.library()
+
+
+@pytest.mark.parametrize("bits", range(1, 9))
+def test_pack_codes_bit_exact(bits):
+    rng = np.random.default_rng(100 + bits)
+    codes = rng.integers(0, 1 << bits, size=(37, 301), dtype=np.uint8)
+    g = ok.pack_codes(torch.from_numpy(codes).to(DEV), bits)
+    torch.cuda.synchronize()
+    got = g.cpu().numpy().view(np.uint32)
+    assert np.array_equal(got, oi.pack_codes(codes, bits))
+
+
+def _random_quantized(n, m, bits, group, seed):
+    rng = np.random.default_rng(seed)
+    W = (rng.standard_normal((n, m)) * 0.02).astype(np.float32)
+    S, Z = orc.scales_zeros(W, bits, group)
+    codes = rng.integers(0, 1 << bits, size=(n, m), dtype=np.uint8)
+    return codes, S, Z
+
+
+@pytest.mark.parametrize("n,m,T,bits,group", [
+    (300, 200, 257, 4, 32),     # ragged channels, features (one ragged k step) and tokens
+    (130, 512, 300, 3, 128),    # 3-bit fields straddling words
+    (64, 96, 128, 8, 16),       # one tile exactly, 8-bit fields
+    (257, 129, 33, 2, 0),       # one group per column, m not a multiple of 16
+    (16, 4096, 1000, 4, 128),   # a long contraction
+])
+def test_dequant_matmul_matches_oracle(n, m, T, bits, group):
+    codes, S, Z = _random_quantized(n, m, bits, group, n + m + T)
+    rng = np.random.default_rng(7)
+    scale = np.exp(rng.standard_normal((m, 1))).astype(np.float32)
+    X16 = (rng.standard_normal((m, T)).astype(np.float32) * scale).astype(np.float16)
+    P = ok.pack_codes(torch.from_numpy(codes).to(DEV), bits)
+    Y = ok.dequant_matmul(P, torch.from_numpy(S).to(DEV), torch.from_numpy(Z).to(DEV), m, bits,
+                          group, torch.from_numpy(X16).to(DEV))
+    torch.cuda.synchronize()
+    W16 = oi.dequantize_fp16(codes, S, Z, group)
+    ref = oi.dequant_matmul(W16, X16)
+    bound = oi.summation_bound(W16, X16)
+    err = np.abs(Y.cpu().numpy().astype(np.float64) - ref)
+    print(f"[dequant {n}x{m}x{T} b{bits} g{group}] max err / bound {np.max(err / (bound + 1e-300)):.3f}")
+    assert np.all(err <= bound + 1e-30)
+
+
+def test_quantized_layer_forward():
+    """Codes, scales and zeros from the quantize call, packed, applied to X~."""
+    cfg = LayerConfig(key="t", title="t", n=96, m=256, T=640, bits=4, group=128, K=4,
+                      mus=(0.5,), w_std=0.02, kind="heavy", data_seed=71, klein_seed=3, noise=0.02)
+    W, Xr, Xq = make_layer(cfg, device=DEV)
+    q = ok.quantize_layer(W, Xr, Xq, 0.5, cfg.bits, cfg.group, cfg.K, cfg.klein_seed)
+    X16 = Xq.half()
+    P = ok.pack_codes(q.codes, cfg.bits)
+    Y = ok.dequant_matmul(P, q.scales, q.zeros, cfg.m, cfg.bits, cfg.group, X16)
+    torch.cuda.synchronize()
+    W16 = oi.dequantize_fp16(q.codes.cpu().numpy(), np64(q.scales), np64(q.zeros), cfg.group)
+    x16 = X16.cpu().numpy()
+    ref = oi.dequant_matmul(W16, x16)
+    assert np.all(np.abs(Y.cpu().numpy() - ref) <= oi.summation_bound(W16, x16) + 1e-30)
+    ones = torch.ones(cfg.n, ok.num_groups(cfg.m, 40), dtype=torch.float32, device=DEV)
+    with pytest.raises(ok.OjbkqError) as ei:     # groups of 40: not a multiple of 16
+        ok.dequant_matmul(P, ones, ones, cfg.m, cfg.bits, 40, X16)
+    assert ei.value.code == "EINVAL"
