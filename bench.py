@@ -62,6 +62,13 @@ def parse():
     ap.add_argument("--k-values", default="0,1,5,10,25,50", help="K values of --sweep-k")
     ap.add_argument("--scheme", default="asym", choices=("asym", "sym"),
                     help="scales and zero points: asymmetric min-max or symmetric Absmax")
+    ap.add_argument("--mlp-stack", action="store_true",
+                    help="instead of the benchmark line: quantize a synthetic stack of layers in "
+                         "order, each on the activations of the layers already quantized (formed "
+                         "with the packed-code product), and report per-layer output errors")
+    ap.add_argument("--stack-layers", type=int, default=4)
+    ap.add_argument("--stack-dim", type=int, default=4096)
+    ap.add_argument("--stack-tokens", type=int, default=32768)
     return ap.parse_args()
 
 
@@ -217,6 +224,89 @@ def cpu_baseline(cfg, W, Xr, Xq, tokens, columns, scheme="asym"):
     }
 
 
+PEAK_F16_MFMA_TFLOPS = 2500.0   # MI355X dense fp16 matrix peak
+
+
+def mlp_stack(args):
+    """Layer-by-layer quantization of a synthetic stack y = W_l silu(...):
+    layer l is quantized on X = the full-precision activations and X~ = the
+    activations of the stack whose layers 0..l-1 are already quantized (the
+    setting of the paper's JTA target), and X~ of the next layer is formed
+    from the packed codes with the dequantize-and-multiply kernel.  Reports
+    the relative output error of every layer for (alpha, K) in
+    {1, 0.6} x {0, 16}: alpha = 1 drops the cross term (each layer fits its
+    own quantized input), alpha = 0.6 is the paper's setting; and the
+    dequantize-and-multiply kernel against the fp16 MFMA roofline.
+
+    The full-precision forward pass and the SiLU between layers are the
+    synthetic model, computed with torch; every quantization step and the
+    quantized product run in the library."""
+    import torch
+    import paper_2602_08376_amd as ok
+    from synth import LayerConfig
+    from synth.workloads import activation_chunks, make_weights
+
+    dev = torch.device("cuda", 0)
+    torch.cuda.set_device(dev)
+    ok.library()
+    d, L, T, bits, group = args.stack_dim, args.stack_layers, args.stack_tokens, 4, 128
+    base = LayerConfig(key="stack", title="synthetic MLP stack", n=d, m=d, T=T, bits=bits,
+                       group=group, K=16, mus=(0.6,), w_std=0.02, kind="heavy", data_seed=21,
+                       noise=0.0)
+    Ws = [make_weights(dataclass_replace(base, data_seed=21 + l), device=dev) for l in range(L)]
+    (X0, _), = list(activation_chunks(base, device=dev))
+    silu = torch.nn.functional.silu
+
+    def product_ms(fn):
+        st = torch.cuda.current_stream(dev)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(st)
+        out = fn()
+        e1.record(st)
+        e1.synchronize()
+        return out, e0.elapsed_time(e1)
+
+    for mu, K in ((1.0, 0), (1.0, 16), (0.6, 0), (0.6, 16)):
+        X, Xq = X0, X0
+        errs, qtimes, dq = [], [], []
+        for l, W in enumerate(Ws):
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+            s = ok.LayerSolver(d, d, bits, group, K, 0, 0.01, device=dev, scheme=args.scheme)
+            s.set_weights(W)
+            s.accumulate(X, Xq)
+            q = s.solve(W, mu)
+            torch.cuda.synchronize()
+            qtimes.append(time.perf_counter() - t0)
+            s.close()
+            P = ok.pack_codes(q.codes, bits)
+            Xq16 = Xq.half()
+            Yq, ms = product_ms(lambda: ok.dequant_matmul(P, q.scales, q.zeros, d, bits, group,
+                                                          Xq16))
+            dq.append(ms)
+            Y = W @ X                                  # the full-precision stack
+            errs.append(float((Yq - Y).norm() / Y.norm()))
+            X, Xq = silu(Y), silu(Yq)
+            del Y, Yq, P, Xq16
+        flops = 2.0 * d * d * T
+        line = {"mlp_stack": True, "alpha": mu, "K": K, "layers": L, "dim": d, "tokens": T,
+                "bits": bits, "group": group, "scheme": args.scheme,
+                "relative_output_error": errs, "quantize_s": qtimes,
+                "dequant_matmul_ms": dq,
+                "dequant_matmul_roofline": {"bound": "mfma", "unit": "TFLOP/s",
+                                            "achieved": flops / (min(dq) * 1e-3) / 1e12,
+                                            "peak": PEAK_F16_MFMA_TFLOPS,
+                                            "frac": flops / (min(dq) * 1e-3) / 1e12 /
+                                            PEAK_F16_MFMA_TFLOPS}}
+        print(json.dumps(line), flush=True)
+        log(f"stack alpha={mu} K={K}: errors {[round(e, 5) for e in errs]}")
+
+
+def dataclass_replace(cfg, **kw):
+    import dataclasses
+    return dataclasses.replace(cfg, **kw)
+
+
 def main():
     args = parse()
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -227,6 +317,9 @@ def main():
         sys.exit(2)
     if args.sweep_k:
         sweep_k(args)
+        return
+    if args.mlp_stack:
+        mlp_stack(args)
         return
 
     import torch
