@@ -60,6 +60,11 @@ def parse():
                          "layer time and the mean JTA residual, on the Llama-3-8B-shaped layers "
                          "given as a comma list of l3_* keys or 'all'")
     ap.add_argument("--k-values", default="0,1,5,10,25,50", help="K values of --sweep-k")
+    ap.add_argument("--sweep-mu", metavar="SHAPES", default=None,
+                    help="instead of the benchmark line: one JSON line per (layer, alpha) with "
+                         "the output error against the full-precision target and against the "
+                         "quantized input, on one factor per layer (l3_* keys or 'all')")
+    ap.add_argument("--mu-values", default="0,0.2,0.4,0.6,0.8,1", help="alpha values of --sweep-mu")
     ap.add_argument("--scheme", default="asym", choices=("asym", "sym"),
                     help="scales and zero points: asymmetric min-max or symmetric Absmax")
     ap.add_argument("--mlp-stack", action="store_true",
@@ -302,6 +307,56 @@ def mlp_stack(args):
         log(f"stack alpha={mu} K={K}: errors {[round(e, 5) for e in errs]}")
 
 
+def sweep_mu(args):
+    """The JTA knob's trade-off on one layer (the paper's mu ablation): for
+    each alpha the relative output errors ||W_hat X~ - W X|| / ||W X|| (the
+    full-precision target, Eq. obj_mismatch) and ||(W_hat - W) X~|| / ||W X~||
+    (the quantized input, Eq. obj_rt), all alpha values on one factor.  The
+    errors are evaluated with torch in float32 from the dequantized weights;
+    the quantization runs in the library."""
+    import torch
+    import paper_2602_08376_amd as ok
+    from synth import LLAMA3_8B
+    from synth.workloads import activation_chunks, make_weights
+
+    keys = list(LLAMA3_8B) if args.sweep_mu == "all" else args.sweep_mu.split(",")
+    mus = [float(x) for x in args.mu_values.split(",")]
+    dev = torch.device("cuda", 0)
+    torch.cuda.set_device(dev)
+    ok.library()
+    for key in keys:
+        cfg = LLAMA3_8B[key]
+        W = make_weights(cfg, device=dev)
+        (X, Xq), = list(activation_chunks(cfg, device=dev))
+        Y = W @ X
+        Yq = W @ Xq
+        ny, nyq = float(Y.norm()), float(Yq.norm())
+        s = ok.LayerSolver(cfg.m, cfg.n, cfg.bits, cfg.group, cfg.K, cfg.klein_seed,
+                           cfg.lambda_rel, device=dev, scheme=args.scheme)
+        s.set_weights(W)
+        s.accumulate(X, Xq)
+        g = ok.num_groups(cfg.m, cfg.group)
+        gs = cfg.m if cfg.group <= 0 or cfg.group >= cfg.m else cfg.group
+        for mu in mus:
+            q = s.solve(W, mu)
+            Sx = q.scales.repeat_interleave(gs, dim=1)[:, :cfg.m]
+            Zx = q.zeros.repeat_interleave(gs, dim=1)[:, :cfg.m]
+            Wh = Sx * (q.codes.float() - Zx)
+            Yh = Wh @ Xq
+            line = {"sweep": "alpha", "workload": f"{key}: {cfg.title}", "alpha": mu, "K": cfg.K,
+                    "scheme": args.scheme, "groups": g,
+                    "error_vs_full_precision": float((Yh - Y).norm()) / ny,
+                    "error_vs_quantized_input": float((Yh - Yq).norm()) / nyq,
+                    "mean_reduced_residual": float(q.residuals.double().mean())}
+            print(json.dumps(line), flush=True)
+            log(f"sweep {key} alpha={mu}: {line['error_vs_full_precision']:.5f} / "
+                f"{line['error_vs_quantized_input']:.5f}")
+            del Sx, Zx, Wh, Yh
+        s.close()
+        del W, X, Xq, Y, Yq
+        torch.cuda.empty_cache()
+
+
 def dataclass_replace(cfg, **kw):
     import dataclasses
     return dataclasses.replace(cfg, **kw)
@@ -320,6 +375,9 @@ def main():
         return
     if args.mlp_stack:
         mlp_stack(args)
+        return
+    if args.sweep_mu:
+        sweep_mu(args)
         return
 
     import torch
