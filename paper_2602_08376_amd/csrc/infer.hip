@@ -15,7 +15,6 @@ namespace ojbkq {
 namespace {
 
 typedef _Float16 h8 __attribute__((ext_vector_type(8)));
-typedef __attribute__((address_space(1))) const uint16_t gbl_u16;   // global memory
 typedef float f4 __attribute__((ext_vector_type(4)));
 
 // ---- packing ---------------------------------------------------------------
@@ -43,9 +42,10 @@ __global__ __launch_bounds__(256) void pack_codes_kernel(const uint8_t* __restri
 
 // ---- dequantize and multiply -------------------------------------------------
 
-constexpr int kTile = 128;     // output rows (channels) and columns (tokens) per workgroup
-constexpr int kStep = 32;      // k per step: one v_mfma_f32_16x16x32_f16
-constexpr int kLd = kStep + 8; // LDS row in halves: 80 bytes, 16-byte aligned
+constexpr int kTileJ = 128;    // output rows (channels) per workgroup
+constexpr int kTileT = 256;    // output columns (tokens) per workgroup
+constexpr int kStage = 64;     // k per LDS stage: two v_mfma_f32_16x16x32_f16 k-steps
+constexpr int kLd = kStage + 8; // LDS row in halves: 144 bytes, 16-byte aligned
 
 struct DqArgs {
   const uint32_t* P;
@@ -60,9 +60,9 @@ struct DqArgs {
   int64_t tiles_n;
 };
 
-// Codes 16 c0 .. 16 c0 + 15 of the step at k0 for row j: their bits start at
-// (k0 + 16 c0) BITS, a multiple of 16, so the first lies at bit 0 or 16 of a
-// word and each code sits inside one 64-bit window of two words.
+// 16 consecutive codes of row j starting at feature kc (a multiple of 16):
+// their bits start at kc BITS, a multiple of 16, so the first lies at bit 0
+// or 16 of a word and each code sits inside one 64-bit window of two words.
 template <int BITS>
 struct CodeLoader {
   static constexpr int kWords = (16 * BITS + 16 + 31) / 32 + 1;
@@ -81,7 +81,9 @@ struct CodeLoader {
   }
   __device__ __forceinline__ uint32_t code(int c) const {
     const int b = c * BITS;                         // compile-time after unrolling
-    if constexpr (32 % BITS == 0) {                 // sh = 0 and no code straddles a word
+    if constexpr (BITS == 1) {                      // 16 bits from bit sh = 0 or 16 of w[0]
+      return (w[0] >> (sh + b)) & 1u;
+    } else if constexpr (16 % BITS == 0) {          // 2, 4, 8: sh = 0, no code straddles a word
       return (w[b >> 5] >> (b & 31)) & ((1u << BITS) - 1u);
     } else {
       const uint64_t pair = ((uint64_t)w[(b >> 5) + 1] << 32) | w[b >> 5];
@@ -90,55 +92,49 @@ struct CodeLoader {
   }
 };
 
-template <int BITS>
-__global__ __launch_bounds__(256, 2) void dequant_matmul_kernel(DqArgs a) {
-  __shared__ __align__(16) _Float16 sA[kTile * kLd];   // W_hat tile: row j, k contiguous
-  __shared__ __align__(16) _Float16 sB[kTile * kLd];   // X tile transposed: row t, k contiguous
+constexpr int kThreads = 512;  // eight waves: 2 x 4 blocks of 64 channels x 64 tokens
+
+template <int BITS, bool VEC>
+__global__ __launch_bounds__(kThreads, 1) void dequant_matmul_kernel(DqArgs a) {
+  __shared__ __align__(16) _Float16 sA[kTileJ * kLd];   // W_hat tile: row j, k contiguous
+  __shared__ __align__(16) _Float16 sB[kTileT * kLd];   // X tile transposed: row t, k contiguous
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wr = wave >> 1, wc = wave & 1;
+  const int wr = wave >> 2, wc = wave & 3;
   // consecutive workgroups take the channel tiles of one token tile, which
   // then stays in L2 while they read it
   const int64_t tj = (int64_t)blockIdx.x % a.tiles_n, tt = (int64_t)blockIdx.x / a.tiles_n;
-  const int64_t J0 = tj * kTile, T0 = tt * kTile;
+  const int64_t J0 = tj * kTileJ, T0 = tt * kTileT;
 
-  // loader roles: A, thread -> (row tid / 2, codes 16 (tid % 2) ..); B, thread
-  // -> (token tid % 128, k rows 16 (tid / 128) ..), so each k row's 128 tokens
-  // are read by two coalesced wave-wide loads
-  const int ar = tid >> 1, ac = tid & 1;
+  // A loader: thread -> (row tid / 4, codes 16 (tid % 4) .. + 15 of the stage).
+  const int ar = tid >> 2, ac = tid & 3;
   const int64_t aj = J0 + ar;
-  const int bt = tid & 127;
-  const int bk = __builtin_amdgcn_readfirstlane(tid >> 7);   // the same for a whole wave
-  const int64_t btok = T0 + bt;
-  const bool t_in = btok < a.T;
-  const uint32_t xoff = (uint32_t)(t_in ? btok : 0);          // this lane's token
-  // A step is interior when its 32 features and the tile's rows and tokens
-  // all exist (the same for every lane): no clamping or masking then.
-  const bool tile_in = J0 + kTile <= a.n && T0 + kTile <= a.T;
+  // B loader: thread -> (tokens 4 (tid % 64) .. + 3, k rows 8 (tid / 64) ..
+  // + 7 of the stage): one 8-byte load per k row (a wave covers the tile's
+  // 256 tokens of a row), repacked in registers into k-contiguous runs.
+  const int bq = lane, bk = wave;
+  const int64_t btok = T0 + 4 * bq;
+  // The stage is interior when its 64 features and the tile's rows and
+  // tokens all exist (the same for every lane): no clamping or masking then.
+  const bool tile_in = J0 + kTileJ <= a.n && T0 + kTileT <= a.T;
 
   CodeLoader<BITS> cl;
-  uint16_t xr[16];
+  uint2 xv[8];           // VEC interior stages: 4 tokens of each of 8 k rows
   float s_cur = 0.f, z_cur = 0.f;
-  bool step_in = false;   // of the step in flight
+  bool stage_in = false;   // of the stage in flight
+  int64_t kf = 0;
   auto fetch = [&](int64_t k0) {
-    step_in = tile_in && k0 + kStep <= a.m;
+    kf = k0;
+    stage_in = VEC && tile_in && k0 + kStage <= a.m;
     const int64_t kc = k0 + 16 * ac;
     cl.load(a, aj, kc);
     const int64_t grp = (kc < a.m ? kc : a.m - 1) / a.g;
     const int64_t jj = aj < a.n ? aj : a.n - 1;
     s_cur = a.S[jj * a.G + grp];
     z_cur = a.Z[jj * a.G + grp];
-    // wave-uniform row pointers (scalar registers) plus the lane's token offset
-    const int64_t kr = k0 + 16 * bk;
+    if (stage_in) {
+      const uint16_t* base = a.X + (k0 + 8 * bk) * a.ldx + btok;
 #pragma unroll
-    for (int e = 0; e < 16; ++e) {
-      const int64_t k = kr + e < a.m ? kr + e : a.m - 1;
-      // (readfirstlane returns a signed int: each half goes through uint32_t
-      // so that the low word is not sign-extended into the high one)
-      const uint64_t rp = reinterpret_cast<uint64_t>(a.X + k * a.ldx);
-      const uint32_t hi = (uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)(rp >> 32));
-      const uint32_t lo = (uint32_t)__builtin_amdgcn_readfirstlane((uint32_t)rp);
-      const uint64_t ru = ((uint64_t)hi << 32) | (uint64_t)lo;
-      xr[e] = reinterpret_cast<const gbl_u16*>(ru)[xoff];
+      for (int e = 0; e < 8; ++e) xv[e] = *reinterpret_cast<const uint2*>(base + e * a.ldx);
     }
   };
 
@@ -148,49 +144,80 @@ __global__ __launch_bounds__(256, 2) void dequant_matmul_kernel(DqArgs a) {
 #pragma unroll
     for (int y = 0; y < 4; ++y) acc[x][y] = f4{0.f, 0.f, 0.f, 0.f};
 
-  const int64_t nsteps = (a.m + kStep - 1) / kStep;
+  const int64_t nst = (a.m + kStage - 1) / kStage;
   fetch(0);
-  for (int64_t st = 0; st < nsteps; ++st) {
-    const int64_t k0 = st * kStep;
-    __syncthreads();   // every wave is done reading the previous step
+  for (int64_t st = 0; st < nst; ++st) {
+    const int64_t k0 = st * kStage;
+    __syncthreads();   // every wave is done reading the previous stage
     {
-      // W_hat = fp16(fp32(s (q - z))); past the last feature, channel or
-      // token both operands are zero
+      // W_hat = fp16(fp32(s (q - z))), zero past the last feature or channel.
+      // Two roundings: the empty asm pins the float32 product in a register,
+      // so it is not folded into v_fma_mixlo_f16, which rounds once to fp16.
       const int zi = (int)z_cur;
-      h8 v[2], u[2];
 #pragma unroll
-      for (int c = 0; c < 16; ++c)
-        v[c >> 3][c & 7] = (_Float16)(s_cur * (float)((int)cl.code(c) - zi));
+      for (int h = 0; h < 2; ++h) {
+        h8 v;
 #pragma unroll
-      for (int e = 0; e < 16; ++e) u[e >> 3][e & 7] = __builtin_bit_cast(_Float16, xr[e]);
-      if (!step_in) {
+        for (int c = 0; c < 8; ++c) {
+          const int cc = 8 * h + c;
+          float p = s_cur * (float)((int)cl.code(cc) - zi);
+          __asm__("" : "+v"(p));
+          const _Float16 w = (_Float16)p;
+          v[c] = (stage_in || (aj < a.n && k0 + 16 * ac + cc < a.m)) ? w : (_Float16)0.f;
+        }
+        *reinterpret_cast<h8*>(sA + ar * kLd + 16 * ac + 8 * h) = v;
+      }
+      if (stage_in) {
+        // token i of k rows 8 bk + 2 p, + 1 -> one 32-bit word of row
+        // (btok + i): a 16-byte run of 8 features
 #pragma unroll
-        for (int c = 0; c < 16; ++c) {
-          if (!(k0 + 16 * ac + c < a.m && aj < a.n)) v[c >> 3][c & 7] = (_Float16)0.f;
-          if (!(k0 + 16 * bk + c < a.m && t_in)) u[c >> 3][c & 7] = (_Float16)0.f;
+        for (int i = 0; i < 4; ++i) {
+          uint32_t wv[4];
+#pragma unroll
+          for (int p = 0; p < 4; ++p) {
+            const uint32_t lo = (i < 2 ? xv[2 * p].x : xv[2 * p].y) >> (16 * (i & 1));
+            const uint32_t hi = (i < 2 ? xv[2 * p + 1].x : xv[2 * p + 1].y) >> (16 * (i & 1));
+            wv[p] = (lo & 0xffffu) | (hi << 16);
+          }
+          *reinterpret_cast<uint4*>(sB + (4 * bq + i) * kLd + 8 * bk) =
+              make_uint4(wv[0], wv[1], wv[2], wv[3]);
+        }
+      } else {
+        // edge stage: element by element, zero past the last feature or token
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int64_t t = btok + i;
+          h8 u;
+#pragma unroll
+          for (int e = 0; e < 8; ++e) {
+            const int64_t k = kf + 8 * bk + e;
+            uint16_t b = 0;
+            if (t < a.T && k < a.m) b = a.X[k * a.ldx + t];
+            u[e] = __builtin_bit_cast(_Float16, b);
+          }
+          *reinterpret_cast<h8*>(sB + (4 * bq + i) * kLd + 8 * bk) = u;
         }
       }
-      *reinterpret_cast<h8*>(sA + ar * kLd + 16 * ac) = v[0];
-      *reinterpret_cast<h8*>(sA + ar * kLd + 16 * ac + 8) = v[1];
-      *reinterpret_cast<h8*>(sB + bt * kLd + 16 * bk) = u[0];
-      *reinterpret_cast<h8*>(sB + bt * kLd + 16 * bk + 8) = u[1];
     }
     __syncthreads();
-    if (st + 1 < nsteps) fetch(k0 + kStep);
-    h8 fa[4], fb[4];
+    if (st + 1 < nst) fetch(k0 + kStage);
 #pragma unroll
-    for (int x = 0; x < 4; ++x)
-      fa[x] = *reinterpret_cast<const h8*>(sA + (wr * 64 + x * 16 + (lane & 15)) * kLd +
-                                           8 * (lane >> 4));
+    for (int ks = 0; ks < 2; ++ks) {
+      h8 fa[4], fb[4];
 #pragma unroll
-    for (int y = 0; y < 4; ++y)
-      fb[y] = *reinterpret_cast<const h8*>(sB + (wc * 64 + y * 16 + (lane & 15)) * kLd +
-                                           8 * (lane >> 4));
-#pragma unroll
-    for (int x = 0; x < 4; ++x)
+      for (int x = 0; x < 4; ++x)
+        fa[x] = *reinterpret_cast<const h8*>(sA + (wr * 64 + x * 16 + (lane & 15)) * kLd +
+                                             32 * ks + 8 * (lane >> 4));
 #pragma unroll
       for (int y = 0; y < 4; ++y)
-        acc[x][y] = __builtin_amdgcn_mfma_f32_16x16x32_f16(fa[x], fb[y], acc[x][y], 0, 0, 0);
+        fb[y] = *reinterpret_cast<const h8*>(sB + (wc * 64 + y * 16 + (lane & 15)) * kLd +
+                                             32 * ks + 8 * (lane >> 4));
+#pragma unroll
+      for (int x = 0; x < 4; ++x)
+#pragma unroll
+        for (int y = 0; y < 4; ++y)
+          acc[x][y] = __builtin_amdgcn_mfma_f32_16x16x32_f16(fa[x], fb[y], acc[x][y], 0, 0, 0);
+    }
   }
 
   // lane l holds D[4 (l / 16) + r][l % 16] of each 16x16 tile
@@ -208,7 +235,12 @@ __global__ __launch_bounds__(256, 2) void dequant_matmul_kernel(DqArgs a) {
 
 template <int BITS>
 hipError_t launch_dq(const DqArgs& a, int64_t tiles, hipStream_t s) {
-  dequant_matmul_kernel<BITS><<<dim3((unsigned)tiles), dim3(256), 0, s>>>(a);
+  // 8-byte activation loads: rows 8-byte aligned (X 8-byte aligned, ldx % 4 == 0)
+  const bool vec = reinterpret_cast<uintptr_t>(a.X) % 8 == 0 && a.ldx % 4 == 0;
+  if (vec)
+    dequant_matmul_kernel<BITS, true><<<dim3((unsigned)tiles), dim3(kThreads), 0, s>>>(a);
+  else
+    dequant_matmul_kernel<BITS, false><<<dim3((unsigned)tiles), dim3(kThreads), 0, s>>>(a);
   return hipGetLastError();
 }
 
@@ -244,8 +276,8 @@ hipError_t launch_dequant_matmul(const uint32_t* P, const float* S, const float*
   a.ldx = ldx;
   a.Y = Y;
   a.ldy = ldy;
-  a.tiles_n = (n + kTile - 1) / kTile;
-  const int64_t tiles = a.tiles_n * ((T + kTile - 1) / kTile);
+  a.tiles_n = (n + kTileJ - 1) / kTileJ;
+  const int64_t tiles = a.tiles_n * ((T + kTileT - 1) / kTileT);
   if (tiles > 0x7fffffff) return hipErrorInvalidValue;
   switch (bits) {
     case 1: return launch_dq<1>(a, tiles, stream);

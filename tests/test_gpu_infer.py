@@ -44,7 +44,14 @@ def _random_quantized(n, m, bits, group, seed):
 @pytest.mark.parametrize("n,m,T,bits,group", [
     (300, 200, 257, 4, 32),     # ragged channels, features (one ragged k step) and tokens
     (130, 512, 300, 3, 128),    # 3-bit fields straddling words
-    (64, 96, 128, 8, 16),       # one tile exactly, 8-bit fields
+    (64, 96, 128, 8, 32),       # 8-bit fields, a ragged 64-deep stage (and products whose
+                                #   one-step fp16 rounding differs from the two-step one)
+    (64, 96, 128, 8, 16),       # groups of 16
+    (70, 160, 90, 1, 32),       # 1-bit fields: a 16-code run starts at bit 0 or 16
+    (100, 192, 200, 5, 64),     # 5-, 6-, 7-bit fields straddling words
+    (33, 320, 77, 6, 32),
+    (48, 224, 130, 7, 32),
+    (128, 256, 256, 4, 32),     # exactly one tile, interior stages only
     (257, 129, 33, 2, 0),       # one group per column, m not a multiple of 16
     (16, 4096, 1000, 4, 128),   # a long contraction
 ])
