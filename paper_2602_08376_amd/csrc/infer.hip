@@ -66,7 +66,9 @@ struct DqArgs {
 template <int BITS>
 struct CodeLoader {
   static constexpr int kWords = (16 * BITS + 16 + 31) / 32 + 1;
-  uint32_t w[kWords];
+  // a vector, not an array: indexed before unrolling, an array is moved to LDS
+  typedef uint32_t Words __attribute__((ext_vector_type(kWords)));
+  Words w;
   int sh;
   __device__ __forceinline__ void load(const DqArgs& a, int64_t j, int64_t kc) {
     const int64_t bit = kc * BITS;
@@ -96,8 +98,10 @@ constexpr int kThreads = 512;  // eight waves: 2 x 4 blocks of 64 channels x 64 
 
 template <int BITS, bool VEC>
 __global__ __launch_bounds__(kThreads, 1) void dequant_matmul_kernel(DqArgs a) {
-  __shared__ __align__(16) _Float16 sA[kTileJ * kLd];   // W_hat tile: row j, k contiguous
-  __shared__ __align__(16) _Float16 sB[kTileT * kLd];   // X tile transposed: row t, k contiguous
+  // two buffers: the waves dequantize and stage step s + 1 into one while
+  // their MFMAs read step s from the other, with one barrier per step
+  __shared__ __align__(16) _Float16 sA[2][kTileJ * kLd];   // W_hat tile: row j, k contiguous
+  __shared__ __align__(16) _Float16 sB[2][kTileT * kLd];   // X tile transposed: row t, k contiguous
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wr = wave >> 2, wc = wave & 3;
   // consecutive workgroups take the channel tiles of one token tile, which
@@ -137,6 +141,59 @@ __global__ __launch_bounds__(kThreads, 1) void dequant_matmul_kernel(DqArgs a) {
       for (int e = 0; e < 8; ++e) xv[e] = *reinterpret_cast<const uint2*>(base + e * a.ldx);
     }
   };
+  // write the fetched stage (features kf .. kf + 63) into buffer `buf`
+  auto stage = [&](int buf) {
+    _Float16* A = sA[buf];
+    _Float16* B = sB[buf];
+    // W_hat = fp16(fp32(s (q - z))), zero past the last feature or channel.
+    // Two roundings: the empty asm pins the float32 product in a register,
+    // so it is not folded into v_fma_mixlo_f16, which rounds once to fp16.
+    const int zi = (int)z_cur;
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      h8 v;
+#pragma unroll
+      for (int c = 0; c < 8; ++c) {
+        const int cc = 8 * h + c;
+        float p = s_cur * (float)((int)cl.code(cc) - zi);
+        __asm__("" : "+v"(p));
+        const _Float16 w = (_Float16)p;
+        v[c] = (stage_in || (aj < a.n && kf + 16 * ac + cc < a.m)) ? w : (_Float16)0.f;
+      }
+      *reinterpret_cast<h8*>(A + ar * kLd + 16 * ac + 8 * h) = v;
+    }
+    if (stage_in) {
+      // token i of k rows 8 bk + 2 p, + 1 -> one 32-bit word of row
+      // (btok + i): a 16-byte run of 8 features
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        uint32_t wv[4];
+#pragma unroll
+        for (int p = 0; p < 4; ++p) {
+          const uint32_t lo = (i < 2 ? xv[2 * p].x : xv[2 * p].y) >> (16 * (i & 1));
+          const uint32_t hi = (i < 2 ? xv[2 * p + 1].x : xv[2 * p + 1].y) >> (16 * (i & 1));
+          wv[p] = (lo & 0xffffu) | (hi << 16);
+        }
+        *reinterpret_cast<uint4*>(B + (4 * bq + i) * kLd + 8 * bk) =
+            make_uint4(wv[0], wv[1], wv[2], wv[3]);
+      }
+    } else {
+      // edge stage: element by element, zero past the last feature or token
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int64_t t = btok + i;
+        h8 u;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const int64_t k = kf + 8 * bk + e;
+          uint16_t b = 0;
+          if (t < a.T && k < a.m) b = a.X[k * a.ldx + t];
+          u[e] = __builtin_bit_cast(_Float16, b);
+        }
+        *reinterpret_cast<h8*>(B + (4 * bq + i) * kLd + 8 * bk) = u;
+      }
+    }
+  };
 
   f4 acc[4][4];
 #pragma unroll
@@ -146,71 +203,24 @@ __global__ __launch_bounds__(kThreads, 1) void dequant_matmul_kernel(DqArgs a) {
 
   const int64_t nst = (a.m + kStage - 1) / kStage;
   fetch(0);
+  stage(0);
+  __syncthreads();
   for (int64_t st = 0; st < nst; ++st) {
-    const int64_t k0 = st * kStage;
-    __syncthreads();   // every wave is done reading the previous stage
-    {
-      // W_hat = fp16(fp32(s (q - z))), zero past the last feature or channel.
-      // Two roundings: the empty asm pins the float32 product in a register,
-      // so it is not folded into v_fma_mixlo_f16, which rounds once to fp16.
-      const int zi = (int)z_cur;
-#pragma unroll
-      for (int h = 0; h < 2; ++h) {
-        h8 v;
-#pragma unroll
-        for (int c = 0; c < 8; ++c) {
-          const int cc = 8 * h + c;
-          float p = s_cur * (float)((int)cl.code(cc) - zi);
-          __asm__("" : "+v"(p));
-          const _Float16 w = (_Float16)p;
-          v[c] = (stage_in || (aj < a.n && k0 + 16 * ac + cc < a.m)) ? w : (_Float16)0.f;
-        }
-        *reinterpret_cast<h8*>(sA + ar * kLd + 16 * ac + 8 * h) = v;
-      }
-      if (stage_in) {
-        // token i of k rows 8 bk + 2 p, + 1 -> one 32-bit word of row
-        // (btok + i): a 16-byte run of 8 features
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          uint32_t wv[4];
-#pragma unroll
-          for (int p = 0; p < 4; ++p) {
-            const uint32_t lo = (i < 2 ? xv[2 * p].x : xv[2 * p].y) >> (16 * (i & 1));
-            const uint32_t hi = (i < 2 ? xv[2 * p + 1].x : xv[2 * p + 1].y) >> (16 * (i & 1));
-            wv[p] = (lo & 0xffffu) | (hi << 16);
-          }
-          *reinterpret_cast<uint4*>(sB + (4 * bq + i) * kLd + 8 * bk) =
-              make_uint4(wv[0], wv[1], wv[2], wv[3]);
-        }
-      } else {
-        // edge stage: element by element, zero past the last feature or token
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const int64_t t = btok + i;
-          h8 u;
-#pragma unroll
-          for (int e = 0; e < 8; ++e) {
-            const int64_t k = kf + 8 * bk + e;
-            uint16_t b = 0;
-            if (t < a.T && k < a.m) b = a.X[k * a.ldx + t];
-            u[e] = __builtin_bit_cast(_Float16, b);
-          }
-          *reinterpret_cast<h8*>(sB + (4 * bq + i) * kLd + 8 * bk) = u;
-        }
-      }
-    }
-    __syncthreads();
-    if (st + 1 < nst) fetch(k0 + kStage);
+    const int cur = (int)(st & 1);
+    const bool more = st + 1 < nst;
+    if (more) fetch((st + 1) * kStage);
+    const _Float16* A = sA[cur];
+    const _Float16* B = sB[cur];
 #pragma unroll
     for (int ks = 0; ks < 2; ++ks) {
       h8 fa[4], fb[4];
 #pragma unroll
       for (int x = 0; x < 4; ++x)
-        fa[x] = *reinterpret_cast<const h8*>(sA + (wr * 64 + x * 16 + (lane & 15)) * kLd +
+        fa[x] = *reinterpret_cast<const h8*>(A + (wr * 64 + x * 16 + (lane & 15)) * kLd +
                                              32 * ks + 8 * (lane >> 4));
 #pragma unroll
       for (int y = 0; y < 4; ++y)
-        fb[y] = *reinterpret_cast<const h8*>(sB + (wc * 64 + y * 16 + (lane & 15)) * kLd +
+        fb[y] = *reinterpret_cast<const h8*>(B + (wc * 64 + y * 16 + (lane & 15)) * kLd +
                                              32 * ks + 8 * (lane >> 4));
 #pragma unroll
       for (int x = 0; x < 4; ++x)
@@ -218,6 +228,10 @@ __global__ __launch_bounds__(kThreads, 1) void dequant_matmul_kernel(DqArgs a) {
         for (int y = 0; y < 4; ++y)
           acc[x][y] = __builtin_amdgcn_mfma_f32_16x16x32_f16(fa[x], fb[y], acc[x][y], 0, 0, 0);
     }
+    // the other buffer was last read in step st - 1, before the barrier
+    // that ended it
+    if (more) stage(cur ^ 1);
+    __syncthreads();
   }
 
   // lane l holds D[4 (l / 16) + r][l % 16] of each 16x16 tile
