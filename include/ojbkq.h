@@ -98,6 +98,20 @@ typedef struct {
   double alpha;        /* the JTA knob mu of Eq. jta_target, 0 <= alpha <= 1  */
   double lambda_rel;   /* lambda^2 = lambda_rel * mean(diag(X~^T X~)), >= 0   */
   uint64_t seed;       /* Philox key for the Klein draws                      */
+  int32_t act_order;   /* weight permutation (the paper's limitations name it,
+                          as in GPTQ, as future work): 0: features decoded in
+                          their own order (last feature first, Alg. 1);
+                          1: the problem is solved with its input features
+                          reordered so the decoder decides those with the
+                          largest Hessian diagonal first -- position p holds
+                          feature perm[p], features sorted by increasing
+                          diag(X~^T X~), equal values by index -- and scale
+                          groups are runs of `group` positions.  Codes are
+                          still returned in W's order (codes[j][i] is the
+                          code of W[j][i]); scales/zeros [n, G] are per
+                          permuted group, so feature perm[p] uses group
+                          p / g.  perm comes back through the `perm`
+                          argument of the quantize calls.                 */
 } ojbkq_params;
 
 typedef struct ojbkq_ctx ojbkq_ctx;   /* opaque staged-solve state (host)     */
@@ -110,12 +124,14 @@ size_t ojbkq_workspace_bytes(const ojbkq_params* p);
  *   X_ref, X_q: [m, T] with row stride T <= ldx <= 2^27 (elements).  X_ref may be NULL
  *     or equal to X_q, and is not read when alpha == 1: the cross term
  *     X~^T (X - X~) then vanishes (Eq. jta_target with X = X~ or mu = 1).
- *   Outputs: codes, scales, zeros, residuals (required); winner (nullable).
+ *   Outputs: codes, scales, zeros, residuals (required); winner (nullable);
+ *     perm [m] int32 (nullable; written only with p->act_order = 1): the
+ *     decode order, perm[p] = the input feature at position p.
  * Returns OJBKQ_OK, OJBKQ_EINVAL, OJBKQ_ENOSPACE, OJBKQ_ENOTPD or OJBKQ_EHIP. */
 int ojbkq_quantize_layer(const ojbkq_params* p, const float* W, const float* X_ref,
                          const float* X_q, int64_t T, int64_t ldx, void* workspace,
                          size_t workspace_bytes, void* stream, uint8_t* codes, float* scales,
-                         float* zeros, double* residuals, int32_t* winner);
+                         float* zeros, double* residuals, int32_t* winner, int32_t* perm);
 
 /* Staged form of the same path, for calibration sets streamed in token chunks
  * (the Gram and cross term are sums over tokens, Alg. 1 step 2-3) and for
@@ -135,9 +151,10 @@ int ojbkq_quantize_layer(const ojbkq_params* p, const float* W, const float* X_r
  *               ([m, T_c], row stride T_c <= ldx <= 2^27).  X_ref_c NULL or == X_q_c adds no
  *               cross term (that chunk has X_ref = X_q); chunks with and
  *               without one may be mixed.  Not allowed after the first solve (ESTATE).
- *   solve:      damps and factors the accumulated Gram on first use, then runs
- *               the rest of the path for W [n, m] and knob `alpha` (overrides
- *               p->alpha).  Output arguments as in ojbkq_quantize_layer.
+ *   solve:      damps and factors the accumulated Gram on first use (with
+ *               act_order, after reordering the sums), then runs the rest of
+ *               the path for W [n, m] and knob `alpha` (overrides p->alpha).
+ *               Output arguments as in ojbkq_quantize_layer.
  *   destroy:    frees the handle (not the workspace).                       */
 int ojbkq_create(const ojbkq_params* p, void* workspace, size_t workspace_bytes, void* stream,
                  ojbkq_ctx** out);
@@ -145,7 +162,7 @@ int ojbkq_set_weights(ojbkq_ctx* ctx, const float* W);
 int ojbkq_accumulate(ojbkq_ctx* ctx, const float* X_ref_c, const float* X_q_c, int64_t T_c,
                      int64_t ldx);
 int ojbkq_solve(ojbkq_ctx* ctx, const float* W, double alpha, uint8_t* codes, float* scales,
-                float* zeros, double* residuals, int32_t* winner);
+                float* zeros, double* residuals, int32_t* winner, int32_t* perm);
 int ojbkq_destroy(ojbkq_ctx* ctx);
 
 /* Read-only view of an intermediate of the last staged solve (device pointer
@@ -156,6 +173,10 @@ int ojbkq_destroy(ojbkq_ctx* ctx);
  *           2: alpha_j [n] float64 (Klein temperature per column)
  *           3: lambda^2 [1] float64
  *           4: per-candidate residuals [n, K + 1] float64
+ *           5: the decode order perm [m] int32 (act_order = 1 only; EINVAL
+ *              otherwise)
+ * With act_order, 0 and 1 are those of the permuted problem (rows and
+ * columns in decode order).
  * Returns EINVAL for an unknown `which`, ESTATE before the first solve.    */
 int ojbkq_inspect(ojbkq_ctx* ctx, int which, const void** ptr);
 
@@ -189,7 +210,7 @@ int ojbkq_stage_times(ojbkq_ctx* ctx, double* ms_out);
  *   ignored), positive diagonal; qbar [n, m] float64; scales [n, G] float32.
  *   codes/residuals required, winner/path_codes/path_resid nullable:
  *   path_codes [n, K + 1, m] uint8 and path_resid [n, K + 1] float64 receive
- *   every candidate.  p->alpha, p->lambda_rel are not used.              */
+ *   every candidate.  p->alpha, p->lambda_rel, p->act_order are not used. */
 size_t ojbkq_decode_workspace_bytes(const ojbkq_params* p);
 int ojbkq_decode_stage(const ojbkq_params* p, const double* R, const double* qbar,
                        const float* scales, void* workspace, size_t workspace_bytes, void* stream,
@@ -212,6 +233,9 @@ double ojbkq_klein_log_rho(int64_t m, int64_t K);
  *   (device, caller-owned): row j is the little-endian bit stream of its codes,
  *   code i at bits [i bits, (i + 1) bits) counted from bit 0 of word 0, zero
  *   past the last code.  Only the low `bits` bits of each code are read.
+ *   perm (device [m] int32, nullable): pack in that order, position p
+ *   holding codes[j][perm[p]] -- with the perm of an act-order quantize call
+ *   the groups of the scales become runs of g positions again.
  *   Asynchronous on `stream`; EINVAL for bad sizes or NULL pointers.
  * ojbkq_dequant_matmul: Y [n, T] float32 (row stride ldy >= T)
  *   = W_hat [n, m] X [m, T], with X IEEE binary16 (fp16 bits as uint16_t),
@@ -221,14 +245,20 @@ double ojbkq_klein_log_rho(int64_t m, int64_t K);
  *   scales, zeros: [n, ceil(m / g)] float32 as returned by the quantize calls
  *   for `group` (g = group, or m when group <= 0 or >= m); needs g % 16 == 0
  *   or g == m (EINVAL otherwise).  packed as written by ojbkq_pack_codes.
+ *   perm (device [m] int32, nullable): codes packed with this perm; packed
+ *   position k then multiplies row perm[k] of X, so Y is W_hat X in the
+ *   original feature order.  perm must be a permutation of 0 .. m-1 (entries
+ *   outside [0, m) are clamped, so a bad perm gives wrong values, never an
+ *   access outside X or the codes).
  *   All pointers device, caller-owned; asynchronous on `stream`; allocates
  *   nothing.                                                             */
 int64_t ojbkq_packed_words(int64_t m, int32_t bits);
-int ojbkq_pack_codes(const uint8_t* codes, int64_t n, int64_t m, int32_t bits, uint32_t* packed,
-                     void* stream);
+int ojbkq_pack_codes(const uint8_t* codes, int64_t n, int64_t m, int32_t bits,
+                     const int32_t* perm, uint32_t* packed, void* stream);
 int ojbkq_dequant_matmul(const uint32_t* packed, const float* scales, const float* zeros,
                          int64_t n, int64_t m, int32_t bits, int32_t group, const uint16_t* X,
-                         int64_t T, int64_t ldx, float* Y, int64_t ldy, void* stream);
+                         int64_t T, int64_t ldx, const int32_t* perm, float* Y, int64_t ldy,
+                         void* stream);
 
 /* Message of the last failure on this thread ("" if none). */
 const char* ojbkq_last_error(void);

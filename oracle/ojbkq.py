@@ -354,17 +354,74 @@ class LayerResult:
     extra: dict = field(default_factory=dict)
 
 
+def act_order_perm(Gm: np.ndarray) -> np.ndarray:
+    """Decode order of the weight permutation the paper's limitations name as
+    future work (the GPTQ heuristic: treat the input features with the largest
+    Hessian diagonal first).
+
+    Position p of the permuted problem holds input feature perm[p].  The
+    features are sorted by increasing diag(X~^T X~), equal values by index, so
+    that the decoder, which walks positions from m - 1 down to 0 (Alg. 1),
+    decides the largest-diagonal features first and the rest compensate for
+    them.  diag(X~^T X~) and diag(H) give the same order (H adds lambda^2 I).
+    """
+    return np.argsort(np.diag(np.asarray(Gm, dtype=np.float64)), kind="stable")
+
+
+def feature_groups(perm: np.ndarray, group: int) -> np.ndarray:
+    """Scale group of every input feature under the permutation: feature
+    perm[p] belongs to group p // g (groups are runs of g decode positions)."""
+    perm = np.asarray(perm)
+    m = perm.shape[0]
+    g = group_size(m, group)
+    out = np.empty(m, dtype=np.int64)
+    out[perm] = np.arange(m) // g
+    return out
+
+
+def dequantize_by_feature(codes, S, Z, gidx) -> np.ndarray:
+    """W_hat [n, m] = s (q - z) with the group of input feature i given by
+    gidx[i] (codes in the original feature order)."""
+    S = np.asarray(S, dtype=np.float64)
+    Z = np.asarray(Z, dtype=np.float64)
+    return S[:, gidx] * (np.asarray(codes, dtype=np.float64) - Z[:, gidx])
+
+
 def quantize_layer(W, X_ref, X_q, mu: float, bits: int, group: int, K: int, seed: int,
                    lambda_rel: float = 0.01, columns=None, G: Optional[np.ndarray] = None,
-                   scheme: str = "asym") -> LayerResult:
+                   scheme: str = "asym", act_order: bool = False,
+                   perm: Optional[np.ndarray] = None) -> LayerResult:
     """The per-layer path end to end.
 
     ``columns`` restricts the decode (not the scales, Gram or factor) to a
     subset of output channels; ``G`` may pass a Gram the caller already
     formed with :func:`gram` on the same X_q; ``scheme`` picks the scale and
     zero-point rule (see :func:`scales_zeros`).
+
+    ``act_order`` (or an explicit ``perm``) solves the problem with its input
+    features reordered: position p holds feature perm[p] (default order:
+    :func:`act_order_perm`), scale groups are runs of g positions, and the
+    returned codes are put back in the original feature order (codes[j, i]
+    is the code of W[j, i]); scales and zeros are per permuted group, and
+    ``extra["perm"]`` holds the order.  The other fields (G, R, V, qbar,
+    decode) are those of the permuted problem.
     """
     W = np.asarray(W)
+    if act_order or perm is not None:
+        Gm = gram(X_q) if G is None else np.asarray(G)
+        if perm is None:
+            perm = act_order_perm(Gm)
+        perm = np.asarray(perm, dtype=np.int64)
+        if sorted(perm.tolist()) != list(range(W.shape[1])):
+            raise ValueError("perm is not a permutation of the input features")
+        Xr = None if X_ref is None else np.asarray(X_ref)[perm]
+        sub = quantize_layer(W[:, perm], Xr, np.asarray(X_q)[perm], mu, bits, group, K, seed,
+                             lambda_rel, columns, Gm[np.ix_(perm, perm)], scheme)
+        codes = np.empty_like(sub.codes)
+        codes[:, perm] = sub.codes
+        sub.codes = codes
+        sub.extra["perm"] = perm
+        return sub
     S, Z = scales_zeros(W, bits, group, scheme)
     Gm = gram(X_q) if G is None else G
     lam2 = damping(Gm, lambda_rel)

@@ -54,6 +54,7 @@ class Params(ctypes.Structure):
         ("m", ctypes.c_int64), ("n", ctypes.c_int64), ("bits", ctypes.c_int32),
         ("group", ctypes.c_int32), ("K", ctypes.c_int32), ("scheme", ctypes.c_int32),
         ("alpha", ctypes.c_double), ("lambda_rel", ctypes.c_double), ("seed", ctypes.c_uint64),
+        ("act_order", ctypes.c_int32),
     ]
 
 
@@ -74,15 +75,15 @@ def library() -> ctypes.CDLL:
         "ojbkq_workspace_bytes": (ctypes.c_size_t, [P]),
         "ojbkq_decode_workspace_bytes": (ctypes.c_size_t, [P]),
         "ojbkq_quantize_layer": (ctypes.c_int, [P, vp, vp, vp, i64, i64, vp, ctypes.c_size_t, vp,
-                                                vp, vp, vp, vp, vp]),
+                                                vp, vp, vp, vp, vp, vp]),
         "ojbkq_create": (ctypes.c_int, [P, vp, ctypes.c_size_t, vp, ctypes.POINTER(vp)]),
         "ojbkq_set_weights": (ctypes.c_int, [vp, vp]),
         "ojbkq_packed_words": (i64, [i64, ctypes.c_int32]),
-        "ojbkq_pack_codes": (ctypes.c_int, [vp, i64, i64, ctypes.c_int32, vp, vp]),
+        "ojbkq_pack_codes": (ctypes.c_int, [vp, i64, i64, ctypes.c_int32, vp, vp, vp]),
         "ojbkq_dequant_matmul": (ctypes.c_int, [vp, vp, vp, i64, i64, ctypes.c_int32,
-                                                ctypes.c_int32, vp, i64, i64, vp, i64, vp]),
+                                                ctypes.c_int32, vp, i64, i64, vp, vp, i64, vp]),
         "ojbkq_accumulate": (ctypes.c_int, [vp, vp, vp, i64, i64]),
-        "ojbkq_solve": (ctypes.c_int, [vp, vp, dp, vp, vp, vp, vp, vp]),
+        "ojbkq_solve": (ctypes.c_int, [vp, vp, dp, vp, vp, vp, vp, vp, vp]),
         "ojbkq_destroy": (ctypes.c_int, [vp]),
         "ojbkq_inspect": (ctypes.c_int, [vp, ctypes.c_int, ctypes.POINTER(vp)]),
         "ojbkq_decode_stage": (ctypes.c_int, [P, vp, vp, vp, vp, ctypes.c_size_t, vp, vp, vp, vp,
@@ -109,11 +110,12 @@ def _check(rc: int):
 SCHEMES = {"asym": 0, "sym": 1}   # scale / zero-point rule (ojbkq_params.scheme)
 
 
-def _params(m, n, bits, group, K, alpha, lambda_rel, seed, scheme="asym") -> Params:
+def _params(m, n, bits, group, K, alpha, lambda_rel, seed, scheme="asym",
+            act_order=False) -> Params:
     if scheme not in SCHEMES:
         raise ValueError(f"scheme must be one of {sorted(SCHEMES)}")
     return Params(int(m), int(n), int(bits), int(group), int(K), SCHEMES[scheme], float(alpha),
-                  float(lambda_rel), int(seed) & 0xFFFFFFFFFFFFFFFF)
+                  float(lambda_rel), int(seed) & 0xFFFFFFFFFFFFFFFF, 1 if act_order else 0)
 
 
 def _ptr(t: Optional[torch.Tensor]):
@@ -159,8 +161,9 @@ def num_groups(m: int, group: int) -> int:
     return (m + g - 1) // g
 
 
-def workspace_bytes(m, n, bits, group, K, alpha=0.5, lambda_rel=0.01, seed=0) -> int:
-    p = _params(m, n, bits, group, K, alpha, lambda_rel, seed)
+def workspace_bytes(m, n, bits, group, K, alpha=0.5, lambda_rel=0.01, seed=0,
+                    act_order=False) -> int:
+    p = _params(m, n, bits, group, K, alpha, lambda_rel, seed, act_order=act_order)
     nb = library().ojbkq_workspace_bytes(ctypes.byref(p))
     if nb == 0:
         _check(-1)
@@ -187,24 +190,29 @@ class QuantResult:
     zeros: torch.Tensor       # [n, G] float32
     residuals: torch.Tensor   # [n] float64
     winner: torch.Tensor      # [n] int32
+    perm: Optional[torch.Tensor] = None   # [m] int32 decode order (act order only)
 
 
-def _outputs(n, m, G, device):
+def _outputs(n, m, G, device, act_order=False):
     return QuantResult(
         codes=torch.empty(n, m, dtype=torch.uint8, device=device),
         scales=torch.empty(n, G, dtype=torch.float32, device=device),
         zeros=torch.empty(n, G, dtype=torch.float32, device=device),
         residuals=torch.empty(n, dtype=torch.float64, device=device),
         winner=torch.empty(n, dtype=torch.int32, device=device),
+        perm=torch.empty(m, dtype=torch.int32, device=device) if act_order else None,
     )
 
 
 def quantize_layer(W, X_ref, X_q, alpha, bits, group, K, seed, lambda_rel=0.01,
-                   workspace: Optional[torch.Tensor] = None, scheme="asym") -> QuantResult:
+                   workspace: Optional[torch.Tensor] = None, scheme="asym",
+                   act_order=False) -> QuantResult:
     """One-shot ``ojbkq_quantize_layer`` on device tensors.
 
     W [n, m] float32; X_ref, X_q [m, T] float32 (X_ref may be None or X_q);
-    scheme: "asym" (min-max) or "sym" (Absmax) scales and zero points.
+    scheme: "asym" (min-max) or "sym" (Absmax) scales and zero points;
+    act_order: decode the features with the largest Hessian diagonal first
+    (codes stay in W's order, ``perm`` holds the decode order).
     """
     n, m = W.shape
     dev = W.device
@@ -217,17 +225,17 @@ def quantize_layer(W, X_ref, X_q, alpha, bits, group, K, seed, lambda_rel=0.01,
         _need(X_ref, "X_ref", torch.float32, device=dev)
         if tuple(X_ref.shape) != tuple(X_q.shape) or X_ref.stride() != X_q.stride():
             raise ValueError("X_ref must have the shape and strides of X_q")
-    p = _params(m, n, bits, group, K, alpha, lambda_rel, seed, scheme)
+    p = _params(m, n, bits, group, K, alpha, lambda_rel, seed, scheme, act_order)
     lib = library()
     need = lib.ojbkq_workspace_bytes(ctypes.byref(p))
     if need == 0:
         _check(-1)
     ws = workspace if workspace is not None else _workspace(need, dev)
-    out = _outputs(n, m, num_groups(m, group), dev)
+    out = _outputs(n, m, num_groups(m, group), dev, act_order)
     rc = lib.ojbkq_quantize_layer(ctypes.byref(p), _ptr(W), _ptr(X_ref), _ptr(X_q), T, ld,
                                   _ptr(ws), ws.numel(), _stream(dev), _ptr(out.codes),
                                   _ptr(out.scales), _ptr(out.zeros), _ptr(out.residuals),
-                                  _ptr(out.winner))
+                                  _ptr(out.winner), _ptr(out.perm))
     _check(rc)
     return out
 
@@ -236,12 +244,13 @@ class LayerSolver:
     """Staged form: accumulate token chunks, then solve for one or more knobs."""
 
     def __init__(self, m, n, bits, group, K, seed, lambda_rel=0.01, device="cuda",
-                 workspace: Optional[torch.Tensor] = None, scheme="asym"):
+                 workspace: Optional[torch.Tensor] = None, scheme="asym", act_order=False):
         self.m, self.n, self.bits, self.group, self.K = int(m), int(n), bits, group, K
+        self.act_order = bool(act_order)
         self.device = torch.device(device)
         if self.device.index is None:
             self.device = torch.device("cuda", torch.cuda.current_device())
-        self.p = _params(m, n, bits, group, K, 0.5, lambda_rel, seed, scheme)
+        self.p = _params(m, n, bits, group, K, 0.5, lambda_rel, seed, scheme, act_order)
         lib = library()
         need = lib.ojbkq_workspace_bytes(ctypes.byref(self.p))
         if need == 0:
@@ -274,22 +283,25 @@ class LayerSolver:
         _need(W, "W", torch.float32, (self.n, self.m), self.device)
         if not W.is_contiguous():
             raise ValueError("W must be contiguous")
-        out = _outputs(self.n, self.m, num_groups(self.m, self.group), self.device)
+        out = _outputs(self.n, self.m, num_groups(self.m, self.group), self.device,
+                       self.act_order)
         _check(library().ojbkq_solve(self.h, _ptr(W), float(alpha), _ptr(out.codes),
                                      _ptr(out.scales), _ptr(out.zeros), _ptr(out.residuals),
-                                     _ptr(out.winner)))
+                                     _ptr(out.winner), _ptr(out.perm)))
         return out
 
     def inspect(self, which: str) -> torch.Tensor:
         """A copy of an intermediate of the last solve: 'L', 'gq' (rows Rbar_j qbar_j),
-        'alpha', 'lam2', 'path_resid'."""
-        idx = {"L": 0, "gq": 1, "alpha": 2, "lam2": 3, "path_resid": 4}[which]
+        'alpha', 'lam2', 'path_resid', 'perm' (act order)."""
+        idx = {"L": 0, "gq": 1, "alpha": 2, "lam2": 3, "path_resid": 4, "perm": 5}[which]
         ptr = ctypes.c_void_p()
         _check(library().ojbkq_inspect(self.h, idx, ctypes.byref(ptr)))
         shape = {"L": (self.m, self.m), "gq": (self.n, self.m), "alpha": (self.n,),
-                 "lam2": (1,), "path_resid": (self.n, self.K + 1)}[which]
+                 "lam2": (1,), "path_resid": (self.n, self.K + 1), "perm": (self.m,)}[which]
         off = ptr.value - self.ws.data_ptr()
         count = int(math.prod(shape))
+        if which == "perm":
+            return self.ws[off:off + 4 * count].view(torch.int32).clone()
         flat = self.ws[off:off + 8 * count].view(torch.float64)
         return flat.reshape(shape).clone()
 
@@ -360,23 +372,35 @@ def packed_words(m: int, bits: int) -> int:
     return int(w)
 
 
-def pack_codes(codes: torch.Tensor, bits: int) -> torch.Tensor:
+def _perm_arg(perm, m, dev):
+    if perm is None:
+        return None
+    _need(perm, "perm", torch.int32, (m,), dev)
+    if not perm.is_contiguous():
+        raise ValueError("perm must be contiguous")
+    return perm
+
+
+def pack_codes(codes: torch.Tensor, bits: int, perm: Optional[torch.Tensor] = None) -> torch.Tensor:
     """``ojbkq_pack_codes``: codes [n, m] uint8 -> [n, words] int32 holding the
-    uint32 bit streams."""
+    uint32 bit streams (position p holds codes[:, perm[p]] when perm is given)."""
     _need(codes, "codes", torch.uint8)
     if codes.dim() != 2 or not codes.is_contiguous():
         raise ValueError("codes must be a contiguous [n, m] tensor")
     n, m = codes.shape
+    perm = _perm_arg(perm, m, codes.device)
     out = torch.empty(n, packed_words(m, bits), dtype=torch.int32, device=codes.device)
-    _check(library().ojbkq_pack_codes(_ptr(codes), n, m, int(bits), _ptr(out),
+    _check(library().ojbkq_pack_codes(_ptr(codes), n, m, int(bits), _ptr(perm), _ptr(out),
                                       _stream(codes.device)))
     return out
 
 
 def dequant_matmul(packed: torch.Tensor, scales: torch.Tensor, zeros: torch.Tensor, m: int,
-                   bits: int, group: int, X: torch.Tensor) -> torch.Tensor:
+                   bits: int, group: int, X: torch.Tensor,
+                   perm: Optional[torch.Tensor] = None) -> torch.Tensor:
     """``ojbkq_dequant_matmul``: Y [n, T] float32 = W_hat [n, m] X [m, T] with
-    X float16 (rows contiguous) and W_hat from the packed codes."""
+    X float16 (rows contiguous) and W_hat from the packed codes (packed with
+    ``perm`` when one is given)."""
     dev = packed.device
     _need(packed, "packed", torch.int32, device=dev)
     n = packed.shape[0]
@@ -389,9 +413,10 @@ def dequant_matmul(packed: torch.Tensor, scales: torch.Tensor, zeros: torch.Tens
     if not (scales.is_contiguous() and zeros.is_contiguous()):
         raise ValueError("scales and zeros must be contiguous")
     T, ld = _rows_view(X, "X", m)
+    perm = _perm_arg(perm, m, dev)
     Y = torch.empty(n, T, dtype=torch.float32, device=dev)
     _check(library().ojbkq_dequant_matmul(_ptr(packed), _ptr(scales), _ptr(zeros), n, m,
-                                          int(bits), int(group), _ptr(X), T, ld, _ptr(Y), T,
-                                          _stream(dev)))
+                                          int(bits), int(group), _ptr(X), T, ld, _ptr(perm),
+                                          _ptr(Y), T, _stream(dev)))
     return Y
 

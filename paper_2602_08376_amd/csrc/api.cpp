@@ -43,6 +43,7 @@ struct Shape {
   int64_t m, n, g, G, K, paths;
   ojbkq::DecodeGeom geo;
   int qmax;
+  bool act_order;
 };
 
 Shape shape_of(const ojbkq_params& p) {
@@ -55,6 +56,7 @@ Shape shape_of(const ojbkq_params& p) {
   s.paths = p.n * (int64_t)(p.K + 1);
   s.geo = ojbkq::decode_geometry(p.n, p.K);
   s.qmax = (1 << p.bits) - 1;
+  s.act_order = p.act_order != 0;
   return s;
 }
 
@@ -85,7 +87,7 @@ int64_t proj_tokens(const Shape& s) {
 struct Layout {
   size_t status = 0, lam2 = 0, G = 0, E = 0, U = 0, gq = 0, alpha = 0, pcodes = 0,
          presid = 0, gc_scratch = 0, gc_tiles = 0, F = 0, Linv = 0, Q = 0, Lsum = 0, SZ = 0,
-         total = 0;
+         perm = 0, Wp = 0, total = 0;
 };
 
 Layout layout_full(const Shape& s) {
@@ -116,6 +118,10 @@ Layout layout_full(const Shape& s) {
     L.U = take(nm);
   L.Lsum = take((size_t)s.G * (size_t)s.m * sizeof(double));
   L.SZ = take((size_t)s.n * (size_t)s.G * sizeof(double));
+  if (s.act_order) {
+    L.perm = take((size_t)s.m * sizeof(int32_t));
+    L.Wp = take((size_t)s.n * (size_t)s.m * sizeof(float));
+  }
   L.total = off;
   return L;
 }
@@ -159,6 +165,7 @@ int check_params(const ojbkq_params* p) {
   if (p->K < 0 || p->K > (1 << 20)) return fail(OJBKQ_EINVAL, "K must be in [0, 2^20]");
   if (p->scheme != 0 && p->scheme != 1) return fail(OJBKQ_EINVAL, "scheme must be 0 or 1");
   if (p->scheme == 1 && p->bits < 2) return fail(OJBKQ_EINVAL, "the symmetric scheme needs bits >= 2");
+  if (p->act_order != 0 && p->act_order != 1) return fail(OJBKQ_EINVAL, "act_order must be 0 or 1");
   if (!(p->alpha >= 0.0 && p->alpha <= 1.0)) return fail(OJBKQ_EINVAL, "alpha must be in [0, 1]");
   if (!(p->lambda_rel >= 0.0) || !std::isfinite(p->lambda_rel))
     return fail(OJBKQ_EINVAL, "lambda_rel must be finite and >= 0");
@@ -382,7 +389,7 @@ int finish(ojbkq_ctx* c) {
 }
 
 int ctx_solve(ojbkq_ctx* c, const float* W, double alpha, uint8_t* codes, float* scales,
-              float* zeros, double* residuals, int32_t* winner) {
+              float* zeros, double* residuals, int32_t* winner, int32_t* perm_out) {
   if (!c->any_chunk) return fail(OJBKQ_ESTATE, "solve before any accumulate");
   if (!W || !codes || !scales || !zeros || !residuals)
     return fail(OJBKQ_EINVAL, "W, codes, scales, zeros and residuals are required");
@@ -392,9 +399,33 @@ int ctx_solve(ojbkq_ctx* c, const float* W, double alpha, uint8_t* codes, float*
   hipStream_t st = c->stream;
   double* Lf = c->at<double>(c->L.G);
   hipEvent_t t0 = stage_begin(c);
+  int32_t* perm = s.act_order ? c->at<int32_t>(c->L.perm) : nullptr;
   if (!c->factored) {
     if (c->cross_seen && !c->projected)   // mixed product -> cross term, while G is the Gram
       OJBKQ_HIP(ojbkq::cross_from_mixed(c->at<double>(c->L.E), Lf, s.m, st), "cross term");
+    if (perm) {
+      // act order: the permuted problem's P G P^T, P E P^T or U P^T, gathered
+      // through the (not yet used) L^-1 buffer and copied back in place
+      const size_t mm = (size_t)s.m * s.m * sizeof(double);
+      double* tmp = c->at<double>(c->L.Linv);
+      OJBKQ_HIP(ojbkq::launch_act_order_perm(Lf, s.m, perm, st), "act order");
+      OJBKQ_HIP(ojbkq::launch_mirror_lower(Lf, s.m, st), "mirror Gram");
+      OJBKQ_HIP(ojbkq::launch_gather(Lf, s.m, perm, perm, s.m, s.m, tmp, s.m, st), "permute Gram");
+      OJBKQ_HIP(hipMemcpyAsync(Lf, tmp, mm, hipMemcpyDeviceToDevice, st), "copy Gram");
+      if (c->cross_seen && !c->projected) {
+        double* E = c->at<double>(c->L.E);
+        OJBKQ_HIP(ojbkq::launch_gather(E, s.m, perm, perm, s.m, s.m, tmp, s.m, st),
+                  "permute cross term");
+        OJBKQ_HIP(hipMemcpyAsync(E, tmp, mm, hipMemcpyDeviceToDevice, st), "copy cross term");
+      } else if (c->cross_seen) {
+        double* U = c->at<double>(c->L.U);
+        OJBKQ_HIP(ojbkq::launch_gather(U, s.m, nullptr, perm, s.n, s.m, tmp, s.m, st),
+                  "permute projected cross term");
+        OJBKQ_HIP(hipMemcpyAsync(U, tmp, (size_t)s.n * s.m * sizeof(double),
+                                 hipMemcpyDeviceToDevice, st),
+                  "copy projected cross term");
+      }
+    }
     OJBKQ_HIP(ojbkq::launch_damp(Lf, s.m, c->p.lambda_rel, c->at<double>(c->L.lam2), st), "damp");
     OJBKQ_HIP(ojbkq::cholesky_lower(Lf, s.m, c->at<int>(c->L.status), c->at<double>(c->L.Linv), st),
               "cholesky");
@@ -408,6 +439,11 @@ int ctx_solve(ojbkq_ctx* c, const float* W, double alpha, uint8_t* codes, float*
     c->factored = true;
     stage_end(c, OJBKQ_STAGE_FACTOR, t0);
     t0 = stage_begin(c);
+  }
+  if (perm) {   // the permuted problem's weights W P^T
+    float* Wp = c->at<float>(c->L.Wp);
+    OJBKQ_HIP(ojbkq::launch_gather(W, s.m, nullptr, perm, s.n, s.m, Wp, s.m, st), "permute W");
+    W = Wp;
   }
   OJBKQ_HIP(ojbkq::launch_scale_zero(W, s.n, s.m, s.g, s.G, c->p.bits, c->p.scheme == 1, scales,
                                      zeros, st),
@@ -493,8 +529,12 @@ int ctx_solve(ojbkq_ctx* c, const float* W, double alpha, uint8_t* codes, float*
   stage_end(c, OJBKQ_STAGE_DECODE, t0);
   t0 = stage_begin(c);
   OJBKQ_HIP(ojbkq::launch_select(d.pcodes, d.presid, s.n, s.m, (int)s.K, s.geo, codes, residuals,
-                                 winner, nullptr, nullptr, st),
+                                 winner, nullptr, nullptr, perm, st),
             "select");
+  if (perm && perm_out)
+    OJBKQ_HIP(hipMemcpyAsync(perm_out, perm, (size_t)s.m * sizeof(int32_t),
+                             hipMemcpyDeviceToDevice, st),
+              "decode order");
   stage_end(c, OJBKQ_STAGE_SELECT, t0);
   c->solved = true;
   return finish(c);
@@ -512,7 +552,7 @@ size_t ojbkq_workspace_bytes(const ojbkq_params* p) {
 int ojbkq_quantize_layer(const ojbkq_params* p, const float* W, const float* X_ref,
                          const float* X_q, int64_t T, int64_t ldx, void* workspace,
                          size_t workspace_bytes, void* stream, uint8_t* codes, float* scales,
-                         float* zeros, double* residuals, int32_t* winner) {
+                         float* zeros, double* residuals, int32_t* winner, int32_t* perm) {
   g_error.clear();
   int rc = check_params(p);
   if (rc) return rc;
@@ -526,7 +566,7 @@ int ojbkq_quantize_layer(const ojbkq_params* p, const float* W, const float* X_r
   if ((rc = ctx_set_weights(&c, W))) return rc;
   const float* Xr = (p->alpha == 1.0) ? nullptr : X_ref;
   if ((rc = ctx_accumulate(&c, Xr, X_q, T, ldx))) return rc;
-  return ctx_solve(&c, W, p->alpha, codes, scales, zeros, residuals, winner);
+  return ctx_solve(&c, W, p->alpha, codes, scales, zeros, residuals, winner, perm);
 }
 
 int ojbkq_create(const ojbkq_params* p, void* workspace, size_t workspace_bytes, void* stream,
@@ -550,21 +590,23 @@ int64_t ojbkq_packed_words(int64_t m, int32_t bits) {
   return ojbkq::packed_words(m, bits);
 }
 
-int ojbkq_pack_codes(const uint8_t* codes, int64_t n, int64_t m, int32_t bits, uint32_t* packed,
-                     void* stream) {
+int ojbkq_pack_codes(const uint8_t* codes, int64_t n, int64_t m, int32_t bits,
+                     const int32_t* perm, uint32_t* packed, void* stream) {
   g_error.clear();
   if (!codes || !packed) return fail(OJBKQ_EINVAL, "codes and packed are required");
   if (n < 1 || m < 1 || bits < 1 || bits > 8)
     return fail(OJBKQ_EINVAL, "need n >= 1, m >= 1 and bits in [1, 8]");
   if (n > (int64_t)1 << 24 || m > (int64_t)1 << 20) return fail(OJBKQ_EINVAL, "n or m too large");
-  OJBKQ_HIP(ojbkq::launch_pack_codes(codes, n, m, bits, packed, static_cast<hipStream_t>(stream)),
+  OJBKQ_HIP(ojbkq::launch_pack_codes(codes, n, m, bits, perm, packed,
+                                     static_cast<hipStream_t>(stream)),
             "pack codes");
   return OJBKQ_OK;
 }
 
 int ojbkq_dequant_matmul(const uint32_t* packed, const float* scales, const float* zeros,
                          int64_t n, int64_t m, int32_t bits, int32_t group, const uint16_t* X,
-                         int64_t T, int64_t ldx, float* Y, int64_t ldy, void* stream) {
+                         int64_t T, int64_t ldx, const int32_t* perm, float* Y, int64_t ldy,
+                         void* stream) {
   g_error.clear();
   if (!packed || !scales || !zeros || !X || !Y)
     return fail(OJBKQ_EINVAL, "packed, scales, zeros, X and Y are required");
@@ -575,8 +617,8 @@ int ojbkq_dequant_matmul(const uint32_t* packed, const float* scales, const floa
   const int64_t g = (group <= 0 || group >= m) ? m : group;
   if (g % 16 != 0 && g != m)
     return fail(OJBKQ_EINVAL, "the group must be a multiple of 16 (or the whole column)");
-  OJBKQ_HIP(ojbkq::launch_dequant_matmul(packed, scales, zeros, n, m, bits, g, X, T, ldx, Y, ldy,
-                                         static_cast<hipStream_t>(stream)),
+  OJBKQ_HIP(ojbkq::launch_dequant_matmul(packed, scales, zeros, n, m, bits, g, X, T, ldx, perm, Y,
+                                         ldy, static_cast<hipStream_t>(stream)),
             "dequantize and multiply");
   return OJBKQ_OK;
 }
@@ -595,10 +637,10 @@ int ojbkq_accumulate(ojbkq_ctx* ctx, const float* X_ref_c, const float* X_q_c, i
 }
 
 int ojbkq_solve(ojbkq_ctx* ctx, const float* W, double alpha, uint8_t* codes, float* scales,
-                float* zeros, double* residuals, int32_t* winner) {
+                float* zeros, double* residuals, int32_t* winner, int32_t* perm) {
   g_error.clear();
   if (!ctx) return fail(OJBKQ_EINVAL, "ctx is NULL");
-  return ctx_solve(ctx, W, alpha, codes, scales, zeros, residuals, winner);
+  return ctx_solve(ctx, W, alpha, codes, scales, zeros, residuals, winner, perm);
 }
 
 int ojbkq_destroy(ojbkq_ctx* ctx) {
@@ -637,6 +679,10 @@ int ojbkq_inspect(ojbkq_ctx* ctx, int which, const void** ptr) {
     case 2: *ptr = ctx->at<void>(ctx->L.alpha); break;
     case 3: *ptr = ctx->at<void>(ctx->L.lam2); break;
     case 4: *ptr = ctx->at<void>(ctx->L.presid); break;
+    case 5:
+      if (!ctx->s.act_order) return fail(OJBKQ_EINVAL, "no decode order without act_order");
+      *ptr = ctx->at<void>(ctx->L.perm);
+      break;
     default: return fail(OJBKQ_EINVAL, "unknown intermediate");
   }
   return OJBKQ_OK;
@@ -693,7 +739,7 @@ int ojbkq_decode_stage(const ojbkq_params* p, const double* R, const double* qba
   d.presid = reinterpret_cast<double*>(ws + L.presid);
   OJBKQ_HIP(ojbkq::launch_decode(d, st), "decode");
   OJBKQ_HIP(ojbkq::launch_select(d.pcodes, d.presid, s.n, s.m, (int)s.K, s.geo, codes, residuals,
-                                 winner, path_codes, path_resid, st),
+                                 winner, path_codes, path_resid, nullptr, st),
             "select");
   OJBKQ_HIP(hipStreamSynchronize(st), "stream sync");
   return OJBKQ_OK;

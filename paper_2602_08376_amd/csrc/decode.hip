@@ -367,7 +367,8 @@ __global__ __launch_bounds__(256) void select_kernel(const uint8_t* __restrict__
                                                      double* __restrict__ resid,
                                                      int32_t* __restrict__ winner,
                                                      uint8_t* __restrict__ path_codes,
-                                                     double* __restrict__ path_resid) {
+                                                     double* __restrict__ path_resid,
+                                                     const int32_t* __restrict__ perm) {
   __shared__ int kstar;
   const int64_t j = blockIdx.x;
   const int64_t kp1 = (int64_t)K + 1;
@@ -401,7 +402,8 @@ __global__ __launch_bounds__(256) void select_kernel(const uint8_t* __restrict__
   {
     const uint8_t* src = path_base(j * kp1 + kstar);
     for (int64_t i = tid; i < m; i += 256)
-      codes[j * m + i] = src[(i / kBS) * kBlockCodes + seg_byte((int)(i % kBS))];
+      codes[j * m + (perm ? (int64_t)perm[i] : i)] =
+          src[(i / kBS) * kBlockCodes + seg_byte((int)(i % kBS))];
   }
   if (path_resid)
     for (int64_t k = tid; k < kp1; k += 256) path_resid[j * kp1 + k] = presid[j * kp1 + k];
@@ -471,10 +473,11 @@ hipError_t launch_decode(const DecodeDesc& d, hipStream_t stream) {
 
 hipError_t launch_select(const uint8_t* pcodes, const double* presid, int64_t n, int64_t m, int K,
                          const DecodeGeom& geom, uint8_t* codes, double* resid, int32_t* winner,
-                         uint8_t* path_codes, double* path_resid, hipStream_t stream) {
+                         uint8_t* path_codes, double* path_resid, const int32_t* perm,
+                         hipStream_t stream) {
   select_kernel<<<dim3((unsigned)n), dim3(256), 0, stream>>>(
       pcodes, presid, n, m, K, geom.wg_paths, geom.threads, codes, resid, winner, path_codes,
-      path_resid);
+      path_resid, perm);
   return hipGetLastError();
 }
 

@@ -23,6 +23,7 @@ typedef float f4 __attribute__((ext_vector_type(4)));
 // of the row's stream, code i at bits [i bits, (i + 1) bits).
 __global__ __launch_bounds__(256) void pack_codes_kernel(const uint8_t* __restrict__ codes,
                                                          int64_t n, int64_t m, int bits,
+                                                         const int32_t* __restrict__ perm,
                                                          int64_t wpr, uint32_t* __restrict__ P) {
   const int64_t total = n * wpr;
   for (int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x; e < total;
@@ -32,7 +33,12 @@ __global__ __launch_bounds__(256) void pack_codes_kernel(const uint8_t* __restri
     int64_t i = b0 / bits;                           // first code touching it
     uint32_t v = 0;
     for (; i < m && i * bits < b0 + 32; ++i) {
-      const uint64_t q = codes[j * m + i] & ((1u << bits) - 1u);
+      int64_t src = i;
+      if (perm) {
+        src = perm[i];
+        src = src < 0 ? 0 : (src >= m ? m - 1 : src);
+      }
+      const uint64_t q = codes[j * m + src] & ((1u << bits) - 1u);
       const int64_t sh = i * bits - b0;              // may be negative for the first code
       v |= (uint32_t)(sh >= 0 ? (q << sh) : (q >> -sh));
     }
@@ -55,10 +61,18 @@ struct DqArgs {
   int64_t n, m, g, G;
   const uint16_t* X;           // fp16 bits, [m, T] with row stride ldx
   int64_t T, ldx;
+  const int32_t* perm;         // null, or X row of packed position k = perm[k]
   float* Y;
   int64_t ldy;
   int64_t tiles_n;
 };
+
+// Row of X that packed position k (< m) multiplies.
+__device__ __forceinline__ int64_t x_row(const DqArgs& a, int64_t k) {
+  if (!a.perm) return k;
+  const int64_t r = a.perm[k];
+  return r < 0 ? 0 : (r >= a.m ? a.m - 1 : r);
+}
 
 // 16 consecutive codes of row j starting at feature kc (a multiple of 16):
 // their bits start at kc BITS, a multiple of 16, so the first lies at bit 0
@@ -136,9 +150,10 @@ __global__ __launch_bounds__(kThreads, 1) void dequant_matmul_kernel(DqArgs a) {
     s_cur = a.S[jj * a.G + grp];
     z_cur = a.Z[jj * a.G + grp];
     if (stage_in) {
-      const uint16_t* base = a.X + (k0 + 8 * bk) * a.ldx + btok;
+      const uint16_t* base = a.X + btok;
 #pragma unroll
-      for (int e = 0; e < 8; ++e) xv[e] = *reinterpret_cast<const uint2*>(base + e * a.ldx);
+      for (int e = 0; e < 8; ++e)
+        xv[e] = *reinterpret_cast<const uint2*>(base + x_row(a, k0 + 8 * bk + e) * a.ldx);
     }
   };
   // write the fetched stage (features kf .. kf + 63) into buffer `buf`
@@ -187,7 +202,7 @@ __global__ __launch_bounds__(kThreads, 1) void dequant_matmul_kernel(DqArgs a) {
         for (int e = 0; e < 8; ++e) {
           const int64_t k = kf + 8 * bk + e;
           uint16_t b = 0;
-          if (t < a.T && k < a.m) b = a.X[k * a.ldx + t];
+          if (t < a.T && k < a.m) b = a.X[x_row(a, k) * a.ldx + t];
           u[e] = __builtin_bit_cast(_Float16, b);
         }
         *reinterpret_cast<h8*>(B + (4 * bq + i) * kLd + 8 * bk) = u;
@@ -262,19 +277,20 @@ hipError_t launch_dq(const DqArgs& a, int64_t tiles, hipStream_t s) {
 
 int64_t packed_words(int64_t m, int bits) { return (m * bits + 31) / 32; }
 
-hipError_t launch_pack_codes(const uint8_t* codes, int64_t n, int64_t m, int bits, uint32_t* P,
-                             hipStream_t stream) {
+hipError_t launch_pack_codes(const uint8_t* codes, int64_t n, int64_t m, int bits,
+                             const int32_t* perm, uint32_t* P, hipStream_t stream) {
   const int64_t total = n * packed_words(m, bits);
   if (total <= 0) return hipSuccess;
   const int64_t blocks = (total + 255) / 256;
   pack_codes_kernel<<<dim3((unsigned)(blocks < 65536 ? blocks : 65536)), dim3(256), 0, stream>>>(
-      codes, n, m, bits, packed_words(m, bits), P);
+      codes, n, m, bits, perm, packed_words(m, bits), P);
   return hipGetLastError();
 }
 
 hipError_t launch_dequant_matmul(const uint32_t* P, const float* S, const float* Z, int64_t n,
                                  int64_t m, int bits, int64_t g, const uint16_t* X, int64_t T,
-                                 int64_t ldx, float* Y, int64_t ldy, hipStream_t stream) {
+                                 int64_t ldx, const int32_t* perm, float* Y, int64_t ldy,
+                                 hipStream_t stream) {
   if (n <= 0 || T <= 0) return hipSuccess;
   DqArgs a;
   a.P = P;
@@ -288,6 +304,7 @@ hipError_t launch_dequant_matmul(const uint32_t* P, const float* S, const float*
   a.X = X;
   a.T = T;
   a.ldx = ldx;
+  a.perm = perm;
   a.Y = Y;
   a.ldy = ldy;
   a.tiles_n = (n + kTileJ - 1) / kTileJ;

@@ -218,19 +218,40 @@ hipError_t launch_decode(const DecodeDesc& d, hipStream_t stream);
 int64_t packed_words(int64_t m, int bits);
 // P [n, packed_words(m, bits)] uint32: row j is the little-endian bit stream
 // of codes[j][0..m), code i at bits [i bits, (i + 1) bits), zero past the end.
-hipError_t launch_pack_codes(const uint8_t* codes, int64_t n, int64_t m, int bits, uint32_t* P,
-                             hipStream_t stream);
+// With perm (or null), position p of the stream holds codes[j][perm[p]];
+// perm entries are clamped to [0, m).
+hipError_t launch_pack_codes(const uint8_t* codes, int64_t n, int64_t m, int bits,
+                             const int32_t* perm, uint32_t* P, hipStream_t stream);
 // Y [n, T] (row stride ldy) = W_hat X, W_hat[j][i] = fp16(fp32(s (q - z)))
 // from P and the [n, ceil(m / g)] scales / zero points; X [m, T] fp16 bits,
-// row stride ldx.  Needs g % 16 == 0 or g == m.
+// row stride ldx.  Needs g % 16 == 0 or g == m.  With perm (or null), the
+// packed position k multiplies row perm[k] of X (clamped to [0, m)).
 hipError_t launch_dequant_matmul(const uint32_t* P, const float* S, const float* Z, int64_t n,
                                  int64_t m, int bits, int64_t g, const uint16_t* X, int64_t T,
-                                 int64_t ldx, float* Y, int64_t ldy, hipStream_t stream);
+                                 int64_t ldx, const int32_t* perm, float* Y, int64_t ldy,
+                                 hipStream_t stream);
 
 // First strict minimum over the K + 1 candidates of each column; gathers the
-// winner's codes.  path_codes / path_resid / winner may be null.
+// winner's codes.  path_codes / path_resid / winner may be null.  With perm
+// (a permutation of 0 .. m-1, or null), the code at decode position p goes to
+// codes[j][perm[p]] (the original feature order).
 hipError_t launch_select(const uint8_t* pcodes, const double* presid, int64_t n, int64_t m, int K,
                          const DecodeGeom& geom, uint8_t* codes, double* resid, int32_t* winner,
-                         uint8_t* path_codes, double* path_resid, hipStream_t stream);
+                         uint8_t* path_codes, double* path_resid, const int32_t* perm,
+                         hipStream_t stream);
+
+// ---- weight permutation (act order) ----------------------------------------
+// perm[p] = the input feature at decode position p: features by increasing
+// diag(G) (G [m, m] fp64, diagonal read), equal values by index.
+hipError_t launch_act_order_perm(const double* G, int64_t m, int32_t* perm, hipStream_t stream);
+// Copies G's lower triangle onto its upper triangle (G [m, m] fp64).
+hipError_t launch_mirror_lower(double* G, int64_t m, hipStream_t stream);
+// out[r][c] = in[rmap[r]][cmap[c]] for r < rows, c < cols (rmap null:
+// identity); rmap / cmap entries must index inside `in`.
+hipError_t launch_gather(const double* in, int64_t ldi, const int32_t* rmap, const int32_t* cmap,
+                         int64_t rows, int64_t cols, double* out, int64_t ldo,
+                         hipStream_t stream);
+hipError_t launch_gather(const float* in, int64_t ldi, const int32_t* rmap, const int32_t* cmap,
+                         int64_t rows, int64_t cols, float* out, int64_t ldo, hipStream_t stream);
 
 }  // namespace ojbkq

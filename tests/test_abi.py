@@ -51,7 +51,7 @@ def test_bad_params_rejected(bad):
     assert lib.ojbkq_workspace_bytes(ctypes.byref(p)) == 0
     assert lib.ojbkq_decode_workspace_bytes(ctypes.byref(p)) == 0
     rc = lib.ojbkq_quantize_layer(ctypes.byref(p), 1, 1, 1, 10, 10, 256, 1 << 30, None, 1, 1, 1, 1,
-                                  None)
+                                  None, None)
     assert rc == -1
     assert lib.ojbkq_last_error().decode()
 
@@ -67,6 +67,19 @@ def test_scheme_values():
         ok._params(128, 64, 4, 128, 4, 0.5, 0.01, 0, "absmax")
 
 
+def test_act_order_values():
+    """act_order is 0 or 1; 1 adds the decode order and the permuted weights
+    (m int32 + n m float32) to the workspace."""
+    lib = ok.library()
+    for v, ok_ in ((0, True), (1, True), (2, False), (-1, False)):
+        p = _p()
+        p.act_order = v
+        assert (lib.ojbkq_workspace_bytes(ctypes.byref(p)) > 0) == ok_, v
+    plain = ok.workspace_bytes(300, 70, 4, 128, 4)
+    perm = ok.workspace_bytes(300, 70, 4, 128, 4, act_order=True)
+    assert perm >= plain + 300 * 4 + 70 * 300 * 4
+
+
 def test_null_and_shape_errors_before_any_launch():
     lib = ok.library()
     p = _p()
@@ -74,32 +87,32 @@ def test_null_and_shape_errors_before_any_launch():
     assert ws > 0
     # missing outputs / inputs
     assert lib.ojbkq_quantize_layer(ctypes.byref(p), None, None, 1, 10, 10, 256, ws, None, 1, 1, 1,
-                                    1, None) == -1
+                                    1, None, None) == -1
     assert lib.ojbkq_quantize_layer(ctypes.byref(p), 1, None, 1, 10, 10, 256, ws, None, None, 1, 1,
-                                    1, None) == -1
+                                    1, None, None) == -1
     # bad token count / stride
     assert lib.ojbkq_quantize_layer(ctypes.byref(p), 1, None, 1, 0, 10, 256, ws, None, 1, 1, 1, 1,
-                                    None) == -1
+                                    None, None) == -1
     assert lib.ojbkq_quantize_layer(ctypes.byref(p), 1, None, 1, 10, 9, 256, ws, None, 1, 1, 1, 1,
-                                    None) == -1
+                                    None, None) == -1
     assert lib.ojbkq_quantize_layer(ctypes.byref(p), 1, None, 1, 10, (1 << 27) + 1, 256, ws, None,
-                                    1, 1, 1, 1, None) == -1
+                                    1, 1, 1, 1, None, None) == -1
     assert "2^27" in lib.ojbkq_last_error().decode()
     # misaligned or missing workspace
     assert lib.ojbkq_quantize_layer(ctypes.byref(p), 1, None, 1, 10, 10, 0, ws, None, 1, 1, 1, 1,
-                                    None) == -1
+                                    None, None) == -1
     assert lib.ojbkq_quantize_layer(ctypes.byref(p), 1, None, 1, 10, 10, 8, ws, None, 1, 1, 1, 1,
-                                    None) == -1
+                                    None, None) == -1
     # workspace too small
     assert lib.ojbkq_quantize_layer(ctypes.byref(p), 1, None, 1, 10, 10, 256, ws - 1, None, 1, 1,
-                                    1, 1, None) == -2
+                                    1, 1, None, None) == -2
     assert "needs" in lib.ojbkq_last_error().decode()
     # staged calls on a NULL handle
     h = ctypes.c_void_p()
     assert lib.ojbkq_create(ctypes.byref(p), None, ws, None, ctypes.byref(h)) == -1
     assert lib.ojbkq_create(ctypes.byref(p), 256, ws, None, None) == -1
     assert lib.ojbkq_accumulate(None, None, 1, 10, 10) == -1
-    assert lib.ojbkq_solve(None, 1, 0.5, 1, 1, 1, 1, None) == -1
+    assert lib.ojbkq_solve(None, 1, 0.5, 1, 1, 1, 1, None, None) == -1
     ptr = ctypes.c_void_p()
     assert lib.ojbkq_inspect(None, 0, ctypes.byref(ptr)) == -1
     assert lib.ojbkq_destroy(None) == 0
