@@ -65,6 +65,9 @@ def parse():
                          "the output error against the full-precision target and against the "
                          "quantized input, on one factor per layer (l3_* keys or 'all')")
     ap.add_argument("--mu-values", default="0,0.2,0.4,0.6,0.8,1", help="alpha values of --sweep-mu")
+    ap.add_argument("--act-order", action="store_true",
+                    help="weight permutation: decide the features with the largest Hessian "
+                         "diagonal first (every mode)")
     ap.add_argument("--scheme", default="asym", choices=("asym", "sym"),
                     help="scales and zero points: asymmetric min-max or symmetric Absmax")
     ap.add_argument("--mlp-stack", action="store_true",
@@ -100,7 +103,8 @@ def sweep_k(args):
 
         def layer(K):
             s = ok.LayerSolver(cfg.m, cfg.n, cfg.bits, cfg.group, K, cfg.klein_seed,
-                               cfg.lambda_rel, device=dev, scheme=args.scheme)
+                               cfg.lambda_rel, device=dev, scheme=args.scheme,
+                               act_order=args.act_order)
             s.set_timing(True)
             torch.cuda.synchronize()
             t0 = time.perf_counter()
@@ -126,7 +130,7 @@ def sweep_k(args):
                 "sweep": "K", "workload": f"{key}: {cfg.title}", "K": K,
                 "n_out": cfg.n, "m_in": cfg.m, "tokens": cfg.T, "bits": cfg.bits,
                 "group": cfg.group, "alpha": cfg.mu, "scheme": args.scheme,
-                "layer_time_s": t, "time_ratio_vs_first": t / base[0],
+                "act_order": args.act_order, "layer_time_s": t, "time_ratio_vs_first": t / base[0],
                 "decode_ms": stages["decode"],
                 "decode_paths_per_s": cfg.n * (K + 1) / (stages["decode"] * 1e-3),
                 "mean_residual": mean_r, "residual_ratio_vs_first": mean_r / base[1],
@@ -277,17 +281,18 @@ def mlp_stack(args):
         for l, W in enumerate(Ws):
             torch.cuda.synchronize()
             t0 = time.perf_counter()
-            s = ok.LayerSolver(d, d, bits, group, K, 0, 0.01, device=dev, scheme=args.scheme)
+            s = ok.LayerSolver(d, d, bits, group, K, 0, 0.01, device=dev, scheme=args.scheme,
+                               act_order=args.act_order)
             s.set_weights(W)
             s.accumulate(X, Xq)
             q = s.solve(W, mu)
             torch.cuda.synchronize()
             qtimes.append(time.perf_counter() - t0)
             s.close()
-            P = ok.pack_codes(q.codes, bits)
+            P = ok.pack_codes(q.codes, bits, q.perm)     # decode order with act order
             Xq16 = Xq.half()
             Yq, ms = product_ms(lambda: ok.dequant_matmul(P, q.scales, q.zeros, d, bits, group,
-                                                          Xq16))
+                                                          Xq16, q.perm))
             dq.append(ms)
             Y = W @ X                                  # the full-precision stack
             errs.append(float((Yq - Y).norm() / Y.norm()))
@@ -296,7 +301,7 @@ def mlp_stack(args):
         flops = 2.0 * d * d * T
         line = {"mlp_stack": True, "alpha": mu, "K": K, "layers": L, "dim": d, "tokens": T,
                 "bits": bits, "group": group, "scheme": args.scheme,
-                "relative_output_error": errs, "quantize_s": qtimes,
+                "act_order": args.act_order, "relative_output_error": errs, "quantize_s": qtimes,
                 "dequant_matmul_ms": dq,
                 "dequant_matmul_roofline": {"bound": "mfma", "unit": "TFLOP/s",
                                             "achieved": flops / (min(dq) * 1e-3) / 1e12,
@@ -332,19 +337,24 @@ def sweep_mu(args):
         Yq = W @ Xq
         ny, nyq = float(Y.norm()), float(Yq.norm())
         s = ok.LayerSolver(cfg.m, cfg.n, cfg.bits, cfg.group, cfg.K, cfg.klein_seed,
-                           cfg.lambda_rel, device=dev, scheme=args.scheme)
+                           cfg.lambda_rel, device=dev, scheme=args.scheme,
+                           act_order=args.act_order)
         s.set_weights(W)
         s.accumulate(X, Xq)
         g = ok.num_groups(cfg.m, cfg.group)
         gs = cfg.m if cfg.group <= 0 or cfg.group >= cfg.m else cfg.group
         for mu in mus:
             q = s.solve(W, mu)
-            Sx = q.scales.repeat_interleave(gs, dim=1)[:, :cfg.m]
-            Zx = q.zeros.repeat_interleave(gs, dim=1)[:, :cfg.m]
+            # group of every input feature: that of its decode position
+            gidx = torch.arange(cfg.m, device=dev) // gs
+            if q.perm is not None:
+                gidx = torch.empty_like(gidx).index_copy_(0, q.perm.long(), gidx)
+            Sx = q.scales[:, gidx]
+            Zx = q.zeros[:, gidx]
             Wh = Sx * (q.codes.float() - Zx)
             Yh = Wh @ Xq
             line = {"sweep": "alpha", "workload": f"{key}: {cfg.title}", "alpha": mu, "K": cfg.K,
-                    "scheme": args.scheme, "groups": g,
+                    "scheme": args.scheme, "act_order": args.act_order, "groups": g,
                     "error_vs_full_precision": float((Yh - Y).norm()) / ny,
                     "error_vs_quantized_input": float((Yh - Yq).norm()) / nyq,
                     "mean_reduced_residual": float(q.residuals.double().mean())}
@@ -398,14 +408,15 @@ def main():
         f"({sum(x.numel() * 8 for x, _ in chunks) / 2**30:.1f} GiB of activations)")
 
     need = ok.workspace_bytes(cfg.m, cfg.n, cfg.bits, cfg.group, cfg.K, cfg.mu, cfg.lambda_rel,
-                              cfg.klein_seed)
+                              cfg.klein_seed, act_order=args.act_order)
     ws = torch.empty(need, dtype=torch.uint8, device=dev)
     stream = torch.cuda.current_stream(dev)
     log(f"workspace {need / 2**30:.2f} GiB")
 
     def step(record):
         s = ok.LayerSolver(cfg.m, cfg.n, cfg.bits, cfg.group, cfg.K, cfg.klein_seed,
-                           cfg.lambda_rel, device=dev, workspace=ws, scheme=args.scheme)
+                           cfg.lambda_rel, device=dev, workspace=ws, scheme=args.scheme,
+                           act_order=args.act_order)
         s.set_timing(True)                        # per-stage HIP events inside the library
         s.set_weights(W)                          # lets thin layers skip the m x m cross term
         ev = [torch.cuda.Event(enable_timing=True) for _ in range(2 * len(chunks) + 1)]
@@ -467,7 +478,8 @@ def main():
         "vs_baseline": None,
         "dtype": "f64",
         "data": "synthetic (seeded, generated on the GPU; inputs resident in HBM)",
-        "config": {**workload_desc(cfg), **({"scheme": "sym"} if args.scheme == "sym" else {})},
+        "config": {**workload_desc(cfg), **({"scheme": "sym"} if args.scheme == "sym" else {}),
+                   **({"act_order": True} if args.act_order else {})},
         "stages_ms": {"gram_cross_per_launch": gc_avg,
                       "rest_of_path": sum(solve_ms) / len(solve_ms),
                       **{f"library_{k}": v for k, v in stage_ms.items()}},
@@ -496,7 +508,8 @@ def main():
             "paths_per_s": paths / (stage_ms["decode"] * 1e-3),
         },
         "checks": {"codes_max": int(out.codes.max()),
-                   "mean_winner_is_klein": float((out.winner > 0).float().mean())},
+                   "mean_winner_is_klein": float((out.winner > 0).float().mean()),
+                   "mean_residual": float(out.residuals.double().mean())},
     }
     if args.copy_calibration:
         a = torch.empty(1 << 28, dtype=torch.float32, device=dev)

@@ -140,6 +140,18 @@ __global__ __launch_bounds__(kThreads, 1) void dequant_matmul_kernel(DqArgs a) {
   float s_cur = 0.f, z_cur = 0.f;
   bool stage_in = false;   // of the stage in flight
   int64_t kf = 0;
+  // With a permutation, the X rows of the stage the next fetch() loads, read
+  // one stage ahead so that no X address waits on a perm load.
+  int32_t prow[8];
+  auto load_rows = [&](int64_t k0) {
+    if (a.perm) {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const int64_t k = k0 + 8 * bk + e;
+        prow[e] = a.perm[k < a.m ? k : a.m - 1];
+      }
+    }
+  };
   auto fetch = [&](int64_t k0) {
     kf = k0;
     stage_in = VEC && tile_in && k0 + kStage <= a.m;
@@ -152,9 +164,13 @@ __global__ __launch_bounds__(kThreads, 1) void dequant_matmul_kernel(DqArgs a) {
     if (stage_in) {
       const uint16_t* base = a.X + btok;
 #pragma unroll
-      for (int e = 0; e < 8; ++e)
-        xv[e] = *reinterpret_cast<const uint2*>(base + x_row(a, k0 + 8 * bk + e) * a.ldx);
+      for (int e = 0; e < 8; ++e) {
+        int64_t r = k0 + 8 * bk + e;
+        if (a.perm) r = prow[e] < 0 ? 0 : (prow[e] >= a.m ? a.m - 1 : prow[e]);
+        xv[e] = *reinterpret_cast<const uint2*>(base + r * a.ldx);
+      }
     }
+    load_rows(k0 + kStage);
   };
   // write the fetched stage (features kf .. kf + 63) into buffer `buf`
   auto stage = [&](int buf) {
@@ -217,6 +233,7 @@ __global__ __launch_bounds__(kThreads, 1) void dequant_matmul_kernel(DqArgs a) {
     for (int y = 0; y < 4; ++y) acc[x][y] = f4{0.f, 0.f, 0.f, 0.f};
 
   const int64_t nst = (a.m + kStage - 1) / kStage;
+  load_rows(0);
   fetch(0);
   stage(0);
   __syncthreads();
