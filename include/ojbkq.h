@@ -112,6 +112,10 @@ typedef struct {
                           permuted group, so feature perm[p] uses group
                           p / g.  perm comes back through the `perm`
                           argument of the quantize calls.                 */
+  int32_t keep_gram;   /* 1: a staged context keeps a copy of the undamped
+                          Gram (m^2 float64 more workspace) so that
+                          ojbkq_set_knobs can change lambda_rel after a
+                          solve; 0: it cannot.                             */
 } ojbkq_params;
 
 typedef struct ojbkq_ctx ojbkq_ctx;   /* opaque staged-solve state (host)     */
@@ -164,6 +168,21 @@ int ojbkq_accumulate(ojbkq_ctx* ctx, const float* X_ref_c, const float* X_q_c, i
 int ojbkq_solve(ojbkq_ctx* ctx, const float* W, double alpha, uint8_t* codes, float* scales,
                 float* zeros, double* residuals, int32_t* winner, int32_t* perm);
 int ojbkq_destroy(ojbkq_ctx* ctx);
+
+/* Per-layer knobs on a staged context (the paper fixes mu, lambda and K for
+ * all layers and names per-layer choices of them as future work; mu is
+ * already an argument of every solve).  Sets, for the following solves:
+ *   lambda_rel: the damping lambda^2 = lambda_rel * mean(diag(X~^T X~))
+ *     (Alg. 1 step 2).  A value other than the current one re-damps and
+ *     re-factors the kept Gram at the next solve; after the first solve
+ *     that needs params.keep_gram = 1 (ESTATE otherwise).  No new token
+ *     sums are needed: the Gram and cross term do not depend on lambda.
+ *   K: Klein samples, 0 <= K <= params.K (the decoder buffers were carved
+ *     for params.K; EINVAL if this K's geometry would not fit them).  The
+ *     temperature rule and the seed apply as for a context created with
+ *     this K, so the results equal those of such a context.
+ * Returns OJBKQ_OK, EINVAL or ESTATE; enqueues nothing.                  */
+int ojbkq_set_knobs(ojbkq_ctx* ctx, double lambda_rel, int32_t K);
 
 /* Read-only view of an intermediate of the last staged solve (device pointer
  * into the workspace, valid until the next call on ctx):

@@ -32,7 +32,7 @@ ABI_FUNCTIONS = (
     "ojbkq_solve", "ojbkq_destroy", "ojbkq_inspect", "ojbkq_decode_workspace_bytes",
     "ojbkq_decode_stage", "ojbkq_klein_log_rho", "ojbkq_last_error", "ojbkq_set_timing",
     "ojbkq_stage_times", "ojbkq_set_weights", "ojbkq_packed_words", "ojbkq_pack_codes",
-    "ojbkq_dequant_matmul",
+    "ojbkq_dequant_matmul", "ojbkq_set_knobs",
 )
 
 STAGES = ("gram", "factor", "solve", "centres", "decode", "select")
@@ -54,7 +54,7 @@ class Params(ctypes.Structure):
         ("m", ctypes.c_int64), ("n", ctypes.c_int64), ("bits", ctypes.c_int32),
         ("group", ctypes.c_int32), ("K", ctypes.c_int32), ("scheme", ctypes.c_int32),
         ("alpha", ctypes.c_double), ("lambda_rel", ctypes.c_double), ("seed", ctypes.c_uint64),
-        ("act_order", ctypes.c_int32),
+        ("act_order", ctypes.c_int32), ("keep_gram", ctypes.c_int32),
     ]
 
 
@@ -78,6 +78,7 @@ def library() -> ctypes.CDLL:
                                                 vp, vp, vp, vp, vp, vp]),
         "ojbkq_create": (ctypes.c_int, [P, vp, ctypes.c_size_t, vp, ctypes.POINTER(vp)]),
         "ojbkq_set_weights": (ctypes.c_int, [vp, vp]),
+        "ojbkq_set_knobs": (ctypes.c_int, [vp, dp, ctypes.c_int32]),
         "ojbkq_packed_words": (i64, [i64, ctypes.c_int32]),
         "ojbkq_pack_codes": (ctypes.c_int, [vp, i64, i64, ctypes.c_int32, vp, vp, vp]),
         "ojbkq_dequant_matmul": (ctypes.c_int, [vp, vp, vp, i64, i64, ctypes.c_int32,
@@ -111,11 +112,12 @@ SCHEMES = {"asym": 0, "sym": 1}   # scale / zero-point rule (ojbkq_params.scheme
 
 
 def _params(m, n, bits, group, K, alpha, lambda_rel, seed, scheme="asym",
-            act_order=False) -> Params:
+            act_order=False, keep_gram=False) -> Params:
     if scheme not in SCHEMES:
         raise ValueError(f"scheme must be one of {sorted(SCHEMES)}")
     return Params(int(m), int(n), int(bits), int(group), int(K), SCHEMES[scheme], float(alpha),
-                  float(lambda_rel), int(seed) & 0xFFFFFFFFFFFFFFFF, 1 if act_order else 0)
+                  float(lambda_rel), int(seed) & 0xFFFFFFFFFFFFFFFF, 1 if act_order else 0,
+                  1 if keep_gram else 0)
 
 
 def _ptr(t: Optional[torch.Tensor]):
@@ -162,8 +164,9 @@ def num_groups(m: int, group: int) -> int:
 
 
 def workspace_bytes(m, n, bits, group, K, alpha=0.5, lambda_rel=0.01, seed=0,
-                    act_order=False) -> int:
-    p = _params(m, n, bits, group, K, alpha, lambda_rel, seed, act_order=act_order)
+                    act_order=False, keep_gram=False) -> int:
+    p = _params(m, n, bits, group, K, alpha, lambda_rel, seed, act_order=act_order,
+                keep_gram=keep_gram)
     nb = library().ojbkq_workspace_bytes(ctypes.byref(p))
     if nb == 0:
         _check(-1)
@@ -244,13 +247,16 @@ class LayerSolver:
     """Staged form: accumulate token chunks, then solve for one or more knobs."""
 
     def __init__(self, m, n, bits, group, K, seed, lambda_rel=0.01, device="cuda",
-                 workspace: Optional[torch.Tensor] = None, scheme="asym", act_order=False):
+                 workspace: Optional[torch.Tensor] = None, scheme="asym", act_order=False,
+                 keep_gram=False):
         self.m, self.n, self.bits, self.group, self.K = int(m), int(n), bits, group, K
         self.act_order = bool(act_order)
+        self.lambda_rel = float(lambda_rel)
         self.device = torch.device(device)
         if self.device.index is None:
             self.device = torch.device("cuda", torch.cuda.current_device())
-        self.p = _params(m, n, bits, group, K, 0.5, lambda_rel, seed, scheme, act_order)
+        self.p = _params(m, n, bits, group, K, 0.5, lambda_rel, seed, scheme, act_order,
+                         keep_gram)
         lib = library()
         need = lib.ojbkq_workspace_bytes(ctypes.byref(self.p))
         if need == 0:
@@ -269,6 +275,14 @@ class LayerSolver:
             raise ValueError("W must be contiguous")
         _check(library().ojbkq_set_weights(self.h, _ptr(W)))
         self.W = W
+
+    def set_knobs(self, lambda_rel=None, K=None):
+        """``ojbkq_set_knobs``: damping and Klein samples for the next solves
+        (a new lambda_rel after a solve needs keep_gram=True)."""
+        lam = self.lambda_rel if lambda_rel is None else float(lambda_rel)
+        k = self.K if K is None else int(K)
+        _check(library().ojbkq_set_knobs(self.h, lam, k))
+        self.lambda_rel, self.K = lam, k
 
     def accumulate(self, X_ref_c, X_q_c):
         _need(X_q_c, "X_q_c", torch.float32, device=self.device)

@@ -44,6 +44,7 @@ struct Shape {
   ojbkq::DecodeGeom geo;
   int qmax;
   bool act_order;
+  bool keep_gram;
 };
 
 Shape shape_of(const ojbkq_params& p) {
@@ -57,6 +58,7 @@ Shape shape_of(const ojbkq_params& p) {
   s.geo = ojbkq::decode_geometry(p.n, p.K);
   s.qmax = (1 << p.bits) - 1;
   s.act_order = p.act_order != 0;
+  s.keep_gram = p.keep_gram != 0;
   return s;
 }
 
@@ -87,7 +89,7 @@ int64_t proj_tokens(const Shape& s) {
 struct Layout {
   size_t status = 0, lam2 = 0, G = 0, E = 0, U = 0, gq = 0, alpha = 0, pcodes = 0,
          presid = 0, gc_scratch = 0, gc_tiles = 0, F = 0, Linv = 0, Q = 0, Lsum = 0, SZ = 0,
-         perm = 0, Wp = 0, total = 0;
+         perm = 0, Wp = 0, Gsave = 0, total = 0;
 };
 
 Layout layout_full(const Shape& s) {
@@ -122,6 +124,7 @@ Layout layout_full(const Shape& s) {
     L.perm = take((size_t)s.m * sizeof(int32_t));
     L.Wp = take((size_t)s.n * (size_t)s.m * sizeof(float));
   }
+  if (s.keep_gram) L.Gsave = take((size_t)s.m * (size_t)s.m * sizeof(double));
   L.total = off;
   return L;
 }
@@ -166,6 +169,7 @@ int check_params(const ojbkq_params* p) {
   if (p->scheme != 0 && p->scheme != 1) return fail(OJBKQ_EINVAL, "scheme must be 0 or 1");
   if (p->scheme == 1 && p->bits < 2) return fail(OJBKQ_EINVAL, "the symmetric scheme needs bits >= 2");
   if (p->act_order != 0 && p->act_order != 1) return fail(OJBKQ_EINVAL, "act_order must be 0 or 1");
+  if (p->keep_gram != 0 && p->keep_gram != 1) return fail(OJBKQ_EINVAL, "keep_gram must be 0 or 1");
   if (!(p->alpha >= 0.0 && p->alpha <= 1.0)) return fail(OJBKQ_EINVAL, "alpha must be in [0, 1]");
   if (!(p->lambda_rel >= 0.0) || !std::isfinite(p->lambda_rel))
     return fail(OJBKQ_EINVAL, "lambda_rel must be finite and >= 0");
@@ -216,7 +220,10 @@ struct ojbkq_ctx {
   // cross term is accumulated projected, as U = W E^T, and E is never formed
   const float* W = nullptr;
   bool projected = false;
+  bool prepared = false;   // cross term formed and, with act order, the sums permuted
   bool factored = false;
+  double lambda_rel = 0.0; // damping of the next factor (ojbkq_set_knobs may change it)
+  size_t pcodes_cap = 0, presid_cap = 0;   // decoder buffers carved for params.K
   bool solved = false;
   // stage timing: event pairs recorded per stage, folded into ms[] at sync points
   bool timing = false;
@@ -290,6 +297,9 @@ int ctx_init(ojbkq_ctx* c, const ojbkq_params* p, void* ws, size_t bytes, void* 
   c->p = *p;
   c->s = shape_of(*p);
   c->L = layout_full(c->s);
+  c->lambda_rel = p->lambda_rel;
+  c->pcodes_cap = (size_t)ojbkq::decode_code_bytes(c->s.m, c->s.geo);
+  c->presid_cap = (size_t)c->s.paths * sizeof(double);
   if (bytes < c->L.total)
     return fail(OJBKQ_ENOSPACE, "workspace has " + std::to_string(bytes) + " bytes, needs " +
                                     std::to_string(c->L.total));
@@ -367,6 +377,28 @@ int ctx_accumulate(ojbkq_ctx* c, const float* Xr, const float* Xq, int64_t T, in
   return OJBKQ_OK;
 }
 
+int ctx_set_knobs(ojbkq_ctx* c, double lambda_rel, int32_t K) {
+  if (!(lambda_rel >= 0.0) || !std::isfinite(lambda_rel))
+    return fail(OJBKQ_EINVAL, "lambda_rel must be finite and >= 0");
+  if (K < 0 || K > c->p.K)
+    return fail(OJBKQ_EINVAL, "K must be in [0, the K the context was created with]");
+  Shape t = c->s;
+  t.K = K;
+  t.paths = t.n * (int64_t)(K + 1);
+  t.geo = ojbkq::decode_geometry(t.n, K);
+  if ((size_t)ojbkq::decode_code_bytes(t.m, t.geo) > c->pcodes_cap ||
+      (size_t)t.paths * sizeof(double) > c->presid_cap)
+    return fail(OJBKQ_EINVAL, "this K needs more decoder space than the context was created for");
+  if (lambda_rel != c->lambda_rel) {
+    if (c->prepared && !c->s.keep_gram)
+      return fail(OJBKQ_ESTATE, "a new lambda_rel after the first solve needs keep_gram");
+    c->lambda_rel = lambda_rel;
+    c->factored = false;
+  }
+  c->s = t;
+  return OJBKQ_OK;
+}
+
 int ctx_set_weights(ojbkq_ctx* c, const float* W) {
   if (!W) return fail(OJBKQ_EINVAL, "W is NULL");
   if (c->any_chunk) return fail(OJBKQ_ESTATE, "weights must be bound before the first accumulate");
@@ -400,7 +432,13 @@ int ctx_solve(ojbkq_ctx* c, const float* W, double alpha, uint8_t* codes, float*
   double* Lf = c->at<double>(c->L.G);
   hipEvent_t t0 = stage_begin(c);
   int32_t* perm = s.act_order ? c->at<int32_t>(c->L.perm) : nullptr;
-  if (!c->factored) {
+  if (!c->factored && c->prepared) {
+    // a new damping (ojbkq_set_knobs): start again from the kept Gram
+    OJBKQ_HIP(hipMemcpyAsync(Lf, c->at<double>(c->L.Gsave), (size_t)s.m * s.m * sizeof(double),
+                             hipMemcpyDeviceToDevice, st),
+              "restore Gram");
+  }
+  if (!c->prepared) {
     if (c->cross_seen && !c->projected)   // mixed product -> cross term, while G is the Gram
       OJBKQ_HIP(ojbkq::cross_from_mixed(c->at<double>(c->L.E), Lf, s.m, st), "cross term");
     if (perm) {
@@ -426,7 +464,15 @@ int ctx_solve(ojbkq_ctx* c, const float* W, double alpha, uint8_t* codes, float*
                   "copy projected cross term");
       }
     }
-    OJBKQ_HIP(ojbkq::launch_damp(Lf, s.m, c->p.lambda_rel, c->at<double>(c->L.lam2), st), "damp");
+    if (s.keep_gram)
+      OJBKQ_HIP(hipMemcpyAsync(c->at<double>(c->L.Gsave), Lf, (size_t)s.m * s.m * sizeof(double),
+                               hipMemcpyDeviceToDevice, st),
+                "keep Gram");
+    c->prepared = true;
+  }
+  if (!c->factored) {
+    OJBKQ_HIP(hipMemsetAsync(c->at<int>(c->L.status), 0x7f, sizeof(int), st), "status clear");
+    OJBKQ_HIP(ojbkq::launch_damp(Lf, s.m, c->lambda_rel, c->at<double>(c->L.lam2), st), "damp");
     OJBKQ_HIP(ojbkq::cholesky_lower(Lf, s.m, c->at<int>(c->L.status), c->at<double>(c->L.Linv), st),
               "cholesky");
     // L^-1 for the solves; the decoder tiles' buffer is free scratch until
@@ -621,6 +667,12 @@ int ojbkq_dequant_matmul(const uint32_t* packed, const float* scales, const floa
                                          ldy, static_cast<hipStream_t>(stream)),
             "dequantize and multiply");
   return OJBKQ_OK;
+}
+
+int ojbkq_set_knobs(ojbkq_ctx* ctx, double lambda_rel, int32_t K) {
+  g_error.clear();
+  if (!ctx) return fail(OJBKQ_EINVAL, "ctx is NULL");
+  return ctx_set_knobs(ctx, lambda_rel, K);
 }
 
 int ojbkq_set_weights(ojbkq_ctx* ctx, const float* W) {

@@ -29,7 +29,7 @@ def test_library_builds_and_loads():
 
 def test_every_declared_symbol_is_exported():
     names = declared_functions()
-    assert len(names) == 17
+    assert len(names) == 18
     assert sorted(ok.ABI_FUNCTIONS) == names
     lib = ctypes.CDLL(ok.library_path)
     for name in names:
@@ -75,6 +75,11 @@ def test_act_order_values():
         p = _p()
         p.act_order = v
         assert (lib.ojbkq_workspace_bytes(ctypes.byref(p)) > 0) == ok_, v
+        p = _p()
+        p.keep_gram = v
+        assert (lib.ojbkq_workspace_bytes(ctypes.byref(p)) > 0) == ok_, v
+    assert ok.workspace_bytes(300, 70, 4, 128, 4, keep_gram=True) >= \
+        ok.workspace_bytes(300, 70, 4, 128, 4) + 300 * 300 * 8
     plain = ok.workspace_bytes(300, 70, 4, 128, 4)
     perm = ok.workspace_bytes(300, 70, 4, 128, 4, act_order=True)
     assert perm >= plain + 300 * 4 + 70 * 300 * 4
@@ -113,6 +118,7 @@ def test_null_and_shape_errors_before_any_launch():
     assert lib.ojbkq_create(ctypes.byref(p), 256, ws, None, None) == -1
     assert lib.ojbkq_accumulate(None, None, 1, 10, 10) == -1
     assert lib.ojbkq_solve(None, 1, 0.5, 1, 1, 1, 1, None, None) == -1
+    assert lib.ojbkq_set_knobs(None, 0.01, 1) == -1
     ptr = ctypes.c_void_p()
     assert lib.ojbkq_inspect(None, 0, ctypes.byref(ptr)) == -1
     assert lib.ojbkq_destroy(None) == 0
