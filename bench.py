@@ -74,6 +74,8 @@ def parse():
                     help="instead of the benchmark line: quantize a synthetic stack of layers in "
                          "order, each on the activations of the layers already quantized (formed "
                          "with the packed-code product), and report per-layer output errors")
+    ap.add_argument("--adaptive", action="store_true",
+                    help="with --mlp-stack: pick lambda, alpha and K per layer on held-out tokens")
     ap.add_argument("--stack-layers", type=int, default=4)
     ap.add_argument("--stack-dim", type=int, default=4096)
     ap.add_argument("--stack-tokens", type=int, default=32768)
@@ -312,6 +314,104 @@ def mlp_stack(args):
         log(f"stack alpha={mu} K={K}: errors {[round(e, 5) for e in errs]}")
 
 
+def adaptive_stack(args):
+    """Per-layer knobs (the paper fixes mu, lambda and K for every layer and
+    names per-layer choices as future work), on the synthetic stack of
+    --mlp-stack.  The tokens are split 3:1 into a fit set, on which every
+    layer is quantized, and a held-out set.  For each layer: lambda_rel in
+    {0.001, 0.01, 0.1} x alpha in {0, 0.2, .., 1} at K = 0, then K in
+    {0, 4, 16} at the best pair, each candidate scored by the held-out output
+    error ||W_hat X~_v - W X_v|| / ||W X_v|| (the full-precision target the
+    JTA objective serves); one context per layer serves the whole search
+    (one Gram, one factor per lambda).  A second stack runs the fixed knobs
+    (lambda_rel 0.01, alpha 0.6, K 16) on the same fit tokens; each stack
+    feeds its own X~ forward.  Errors are reported on all tokens and on the
+    held-out ones."""
+    import torch
+    import paper_2602_08376_amd as ok
+    from synth import LayerConfig
+    from synth.workloads import activation_chunks, make_weights
+
+    dev = torch.device("cuda", 0)
+    torch.cuda.set_device(dev)
+    ok.library()
+    d, L, T, bits, group = args.stack_dim, args.stack_layers, args.stack_tokens, 4, 128
+    Tf = (3 * T // 4) // 256 * 256
+    base = LayerConfig(key="stack", title="synthetic MLP stack", n=d, m=d, T=T, bits=bits,
+                       group=group, K=16, mus=(0.6,), w_std=0.02, kind="heavy", data_seed=21,
+                       noise=0.0)
+    Ws = [make_weights(dataclass_replace(base, data_seed=21 + l), device=dev) for l in range(L)]
+    (X0, _), = list(activation_chunks(base, device=dev))
+    silu = torch.nn.functional.silu
+    lams, mus, ks = (0.001, 0.01, 0.1), (0.0, 0.2, 0.4, 0.6, 0.8, 1.0), (0, 4, 16)
+
+    def product(q, Xq16):
+        P = ok.pack_codes(q.codes, bits, q.perm)
+        return ok.dequant_matmul(P, q.scales, q.zeros, d, bits, group, Xq16, q.perm)
+
+    def quantize(W, X, Xq, search):
+        s = ok.LayerSolver(d, d, bits, group, max(ks), 0, 0.01, device=dev,
+                           scheme=args.scheme, act_order=args.act_order, keep_gram=True)
+        s.set_weights(W)
+        s.accumulate(X[:, :Tf], Xq[:, :Tf])
+        Yv = W @ X[:, Tf:]
+        nv = float(Yv.norm())
+        Xv16 = Xq[:, Tf:].contiguous().half()
+
+        def held_out(q):
+            return float((product(q, Xv16) - Yv).norm()) / nv
+
+        if not search:
+            s.set_knobs(0.01, 16)
+            q = s.solve(W, 0.6)
+            s.close()
+            return q, (0.01, 0.6, 16), None
+        best, trail = None, []
+        for lam in lams:
+            s.set_knobs(lam, 0)
+            for mu in mus:
+                e = held_out(s.solve(W, mu))
+                trail.append((lam, mu, 0, e))
+                if best is None or e < best[3]:
+                    best = (lam, mu, 0, e)
+        lam, mu = best[0], best[1]
+        for K in ks[1:]:
+            s.set_knobs(lam, K)
+            e = held_out(s.solve(W, mu))
+            trail.append((lam, mu, K, e))
+            if e < best[3]:
+                best = (lam, mu, K, e)
+        s.set_knobs(best[0], best[2])
+        q = s.solve(W, best[1])
+        s.close()
+        return q, best[:3], trail
+
+    for search in (False, True):
+        X, Xq = X0, X0
+        errs, errs_v, knobs, times = [], [], [], []
+        for l, W in enumerate(Ws):
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+            q, kn, _ = quantize(W, X, Xq, search)
+            torch.cuda.synchronize()
+            times.append(time.perf_counter() - t0)
+            Yq = product(q, Xq.half())
+            Y = W @ X
+            errs.append(float((Yq - Y).norm() / Y.norm()))
+            errs_v.append(float((Yq[:, Tf:] - Y[:, Tf:]).norm() / Y[:, Tf:].norm()))
+            knobs.append({"lambda_rel": kn[0], "alpha": kn[1], "K": kn[2]})
+            X, Xq = silu(Y), silu(Yq)
+            del Y, Yq
+        line = {"mlp_stack": True, "knobs": "per-layer search" if search else "fixed",
+                "layers": L, "dim": d, "tokens": T, "fit_tokens": Tf, "bits": bits,
+                "group": group, "scheme": args.scheme, "act_order": args.act_order,
+                "chosen": knobs, "relative_output_error": errs,
+                "relative_output_error_held_out": errs_v, "quantize_and_search_s": times}
+        print(json.dumps(line), flush=True)
+        log(f"stack {'search' if search else 'fixed'}: errors {[round(e, 5) for e in errs]}, "
+            f"knobs {knobs}")
+
+
 def sweep_mu(args):
     """The JTA knob's trade-off on one layer (the paper's mu ablation): for
     each alpha the relative output errors ||W_hat X~ - W X|| / ||W X|| (the
@@ -384,7 +484,7 @@ def main():
         sweep_k(args)
         return
     if args.mlp_stack:
-        mlp_stack(args)
+        (adaptive_stack if args.adaptive else mlp_stack)(args)
         return
     if args.sweep_mu:
         sweep_mu(args)
