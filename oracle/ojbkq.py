@@ -16,6 +16,9 @@ inputs the GPU path receives:
   Klein paths       Eq. klein_prob / Alg. 3, temperature per the alpha rule
                     stated after Eq. klein_prob (K = (e rho)^(2m/rho))
   selection         Alg. 4 over the Babai path and the K Klein paths
+  weight order      optional permutation of the input features (act order),
+                    the extension the paper's limitations name as future
+                    work, read as GPTQ's largest-diagonal-first order
 
 Layout of the arguments is the storage layout shared with the GPU path:
 W is [n, m] (row j = the paper's column w_j), X_ref and X_q are [m, T]
