@@ -113,8 +113,13 @@ def scales_zeros(W: np.ndarray, bits: int, group: int, scheme: str = "asym"):
     return S, Z
 
 
-def expand_groups(A: np.ndarray, m: int, group: int) -> np.ndarray:
-    """[n, groups] -> [n, m] by repeating each group's value over its rows."""
+def expand_groups(A: np.ndarray, m: int, group) -> np.ndarray:
+    """[n, groups] -> [n, m] by repeating each group's value over its rows.
+
+    ``group`` is the group size, or an array giving the group of every row
+    (rows of one group need not be adjacent)."""
+    if np.ndim(group) == 1:
+        return np.asarray(A, dtype=np.float64)[:, np.asarray(group, dtype=np.int64)]
     g = group_size(m, group)
     return np.repeat(np.asarray(A, dtype=np.float64), g, axis=1)[:, :m]
 
@@ -393,7 +398,8 @@ def dequantize_by_feature(codes, S, Z, gidx) -> np.ndarray:
 def quantize_layer(W, X_ref, X_q, mu: float, bits: int, group: int, K: int, seed: int,
                    lambda_rel: float = 0.01, columns=None, G: Optional[np.ndarray] = None,
                    scheme: str = "asym", act_order: bool = False,
-                   perm: Optional[np.ndarray] = None) -> LayerResult:
+                   perm: Optional[np.ndarray] = None, static_groups: bool = False,
+                   scales=None) -> LayerResult:
     """The per-layer path end to end.
 
     ``columns`` restricts the decode (not the scales, Gram or factor) to a
@@ -407,7 +413,13 @@ def quantize_layer(W, X_ref, X_q, mu: float, bits: int, group: int, K: int, seed
     returned codes are put back in the original feature order (codes[j, i]
     is the code of W[j, i]); scales and zeros are per permuted group, and
     ``extra["perm"]`` holds the order.  The other fields (G, R, V, qbar,
-    decode) are those of the permuted problem.
+    decode) are those of the permuted problem.  With ``static_groups`` the
+    groups stay runs of g features in W's order (the scales are those of the
+    unpermuted layer) and only the decode order changes: position p then
+    uses the group of feature perm[p].
+
+    ``scales`` = (S, Z) replaces the scale rule; ``group`` may then also be
+    an array with the group of every row.
     """
     W = np.asarray(W)
     if act_order or perm is not None:
@@ -418,14 +430,21 @@ def quantize_layer(W, X_ref, X_q, mu: float, bits: int, group: int, K: int, seed
         if sorted(perm.tolist()) != list(range(W.shape[1])):
             raise ValueError("perm is not a permutation of the input features")
         Xr = None if X_ref is None else np.asarray(X_ref)[perm]
-        sub = quantize_layer(W[:, perm], Xr, np.asarray(X_q)[perm], mu, bits, group, K, seed,
-                             lambda_rel, columns, Gm[np.ix_(perm, perm)], scheme)
+        if static_groups:
+            S, Z = scales_zeros(W, bits, group, scheme)
+            pos_group = perm // group_size(W.shape[1], group)
+            sub = quantize_layer(W[:, perm], Xr, np.asarray(X_q)[perm], mu, bits, pos_group, K,
+                                 seed, lambda_rel, columns, Gm[np.ix_(perm, perm)], scheme,
+                                 scales=(S, Z))
+        else:
+            sub = quantize_layer(W[:, perm], Xr, np.asarray(X_q)[perm], mu, bits, group, K, seed,
+                                 lambda_rel, columns, Gm[np.ix_(perm, perm)], scheme)
         codes = np.empty_like(sub.codes)
         codes[:, perm] = sub.codes
         sub.codes = codes
         sub.extra["perm"] = perm
         return sub
-    S, Z = scales_zeros(W, bits, group, scheme)
+    S, Z = scales_zeros(W, bits, group, scheme) if scales is None else scales
     Gm = gram(X_q) if G is None else G
     lam2 = damping(Gm, lambda_rel)
     H = Gm + lam2 * np.eye(Gm.shape[0])

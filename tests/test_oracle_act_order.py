@@ -145,3 +145,81 @@ def test_explicit_perm_must_be_a_permutation():
         o.quantize_layer(W, Xr, Xq, 0.5, 4, 0, 1, 0, perm=np.array([0, 1, 1, 3, 4]))
     r = o.quantize_layer(W, Xr, Xq, 0.5, 4, 0, 1, 0, perm=np.array([4, 3, 2, 1, 0]))
     assert r.extra["perm"].tolist() == [4, 3, 2, 1, 0]
+
+
+# ---------------------------------------------------------------------------
+# static groups: only the decode order changes, the groups stay runs of g
+# features in W's order
+# ---------------------------------------------------------------------------
+
+def test_static_groups_keep_the_layer_scales():
+    W, Xr, Xq = layer(7, m=14, n=4, T=50)
+    plain = o.quantize_layer(W, Xr, Xq, 0.5, 3, 4, 4, 1)
+    st = o.quantize_layer(W, Xr, Xq, 0.5, 3, 4, 4, 1, act_order=True, static_groups=True)
+    assert np.array_equal(st.scales, plain.scales) and np.array_equal(st.zeros, plain.zeros)
+    assert st.extra["perm"].tolist() == o.act_order_perm(o.gram(Xq)).tolist()
+
+
+@pytest.mark.parametrize("group", [3, 0])
+def test_static_groups_diagonal_gram_rounds_on_the_original_groups(group):
+    """Diagonal H (orthogonal rows of falling norms, so the order is the
+    reversal): Babai is plain rounding with feature i on group i // g of W's
+    own order."""
+    m, n = 8, 4
+    rng = np.random.default_rng(8)
+    Xq = np.zeros((m, m), dtype=np.float32)
+    for i in range(m):
+        Xq[i, i] = 8.0 - i
+    W = (0.05 * rng.standard_normal((n, m))).astype(np.float32)
+    res = o.quantize_layer(W, Xq, Xq, 0.5, 3, group, 0, 0, lambda_rel=0.0, act_order=True,
+                           static_groups=True)
+    assert res.extra["perm"].tolist() == list(range(m - 1, -1, -1))
+    g = m if group <= 0 else group
+    for j in range(n):
+        for i in range(m):
+            s, z = float(res.scales[j, i // g]), float(res.zeros[j, i // g])
+            assert res.codes[j, i] == min(max(np.rint(float(W[j, i]) / s + z), 0), 7), (j, i)
+
+
+def test_static_groups_score_minus_floor_is_residual():
+    """The JTA score of W_hat dequantized in W's order on W's groups (the
+    plain layout), minus the floor, equals the reported residual."""
+    W, Xr, Xq = layer(9, m=14, n=5, T=60)
+    mu, g = 0.5, 4
+    res = o.quantize_layer(W, Xr, Xq, mu, 3, g, 6, 13, act_order=True, static_groups=True)
+    perm = res.extra["perm"]
+    V = np.zeros(W.shape)
+    V[:, perm] = res.V
+    W_hat = o.dequantize(res.codes, res.scales, res.zeros, g)
+    full = o.jta_score(W, Xr, Xq, W_hat, mu, res.lam2)
+    floor = o.jta_score(W, Xr, Xq, V, mu, res.lam2)
+    assert np.allclose(full - floor, res.residuals, rtol=1e-7, atol=1e-12)
+
+
+def test_static_groups_equivariant_under_group_preserving_relabelling():
+    """Relabel features inside each group and the groups among themselves:
+    scales follow the group relabelling, codes the feature relabelling."""
+    W, Xr, Xq = layer(10, m=16, n=4, T=64)
+    rng = np.random.default_rng(11)
+    gperm = rng.permutation(4)
+    sigma = np.concatenate([4 * gg + rng.permutation(4) for gg in gperm])
+    a = o.quantize_layer(W, Xr, Xq, 0.6, 4, 4, 6, 2, act_order=True, static_groups=True)
+    b = o.quantize_layer(W[:, sigma], Xr[sigma], Xq[sigma], 0.6, 4, 4, 6, 2, act_order=True,
+                         static_groups=True)
+    assert np.array_equal(b.scales, a.scales[:, gperm])
+    assert np.array_equal(b.codes, a.codes[:, sigma])
+    assert np.allclose(b.residuals, a.residuals, rtol=1e-9)
+
+
+def test_static_groups_brute_force_bound():
+    W, Xr, Xq = layer(12, m=6, n=3, T=30)
+    res = o.quantize_layer(W, Xr, Xq, 0.5, 2, 3, 12, 5, act_order=True, static_groups=True)
+    perm = res.extra["perm"]
+    Sx = o.expand_groups(res.scales, 6, 3)           # W's order
+    for j in range(W.shape[0]):
+        Rbar_p = res.R * Sx[j, perm][None, :]
+        best = np.inf
+        for pt in itertools.product(range(4), repeat=6):
+            q = np.array(pt, dtype=np.float64)
+            best = min(best, float(np.sum((Rbar_p @ (q[perm] - res.qbar[j])) ** 2)))
+        assert best * (1 - 1e-12) <= res.residuals[j] <= res.decode.path_resid[j, 0] * (1 + 1e-12)
