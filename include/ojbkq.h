@@ -111,7 +111,12 @@ typedef struct {
                           code of W[j][i]); scales/zeros [n, G] are per
                           permuted group, so feature perm[p] uses group
                           p / g.  perm comes back through the `perm`
-                          argument of the quantize calls.                 */
+                          argument of the quantize calls.
+                          2: the same decode order with static groups: the
+                          scale groups stay runs of `group` features in W's
+                          order (scales/zeros as without act order), so the
+                          codes, scales and zeros have the plain layout and
+                          the product needs no perm.                       */
   int32_t keep_gram;   /* 1: a staged context keeps a copy of the undamped
                           Gram (m^2 float64 more workspace) so that
                           ojbkq_set_knobs can change lambda_rel after a

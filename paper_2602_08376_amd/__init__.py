@@ -111,12 +111,23 @@ def _check(rc: int):
 SCHEMES = {"asym": 0, "sym": 1}   # scale / zero-point rule (ojbkq_params.scheme)
 
 
+ACT_ORDER = {False: 0, True: 1, "static": 2}   # ojbkq_params.act_order
+
+
+def _act_order(v) -> int:
+    if isinstance(v, int) and not isinstance(v, bool) and v in (0, 1, 2):
+        return v
+    if v not in ACT_ORDER:
+        raise ValueError('act_order must be False, True or "static"')
+    return ACT_ORDER[v]
+
+
 def _params(m, n, bits, group, K, alpha, lambda_rel, seed, scheme="asym",
             act_order=False, keep_gram=False) -> Params:
     if scheme not in SCHEMES:
         raise ValueError(f"scheme must be one of {sorted(SCHEMES)}")
     return Params(int(m), int(n), int(bits), int(group), int(K), SCHEMES[scheme], float(alpha),
-                  float(lambda_rel), int(seed) & 0xFFFFFFFFFFFFFFFF, 1 if act_order else 0,
+                  float(lambda_rel), int(seed) & 0xFFFFFFFFFFFFFFFF, _act_order(act_order),
                   1 if keep_gram else 0)
 
 
@@ -215,7 +226,8 @@ def quantize_layer(W, X_ref, X_q, alpha, bits, group, K, seed, lambda_rel=0.01,
     W [n, m] float32; X_ref, X_q [m, T] float32 (X_ref may be None or X_q);
     scheme: "asym" (min-max) or "sym" (Absmax) scales and zero points;
     act_order: decode the features with the largest Hessian diagonal first
-    (codes stay in W's order, ``perm`` holds the decode order).
+    (codes stay in W's order, ``perm`` holds the decode order); True groups
+    the scales by decode position, "static" keeps W's own groups.
     """
     n, m = W.shape
     dev = W.device
@@ -250,7 +262,8 @@ class LayerSolver:
                  workspace: Optional[torch.Tensor] = None, scheme="asym", act_order=False,
                  keep_gram=False):
         self.m, self.n, self.bits, self.group, self.K = int(m), int(n), bits, group, K
-        self.act_order = bool(act_order)
+        _act_order(act_order)
+        self.act_order = act_order
         self.lambda_rel = float(lambda_rel)
         self.device = torch.device(device)
         if self.device.index is None:

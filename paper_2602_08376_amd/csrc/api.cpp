@@ -43,7 +43,8 @@ struct Shape {
   int64_t m, n, g, G, K, paths;
   ojbkq::DecodeGeom geo;
   int qmax;
-  bool act_order;
+  bool act_order;       // any weight permutation
+  bool static_groups;   // act_order 2: scale groups stay runs of g features in W's order
   bool keep_gram;
 };
 
@@ -58,6 +59,7 @@ Shape shape_of(const ojbkq_params& p) {
   s.geo = ojbkq::decode_geometry(p.n, p.K);
   s.qmax = (1 << p.bits) - 1;
   s.act_order = p.act_order != 0;
+  s.static_groups = p.act_order == 2 && s.G > 1;
   s.keep_gram = p.keep_gram != 0;
   return s;
 }
@@ -89,7 +91,7 @@ int64_t proj_tokens(const Shape& s) {
 struct Layout {
   size_t status = 0, lam2 = 0, G = 0, E = 0, U = 0, gq = 0, alpha = 0, pcodes = 0,
          presid = 0, gc_scratch = 0, gc_tiles = 0, F = 0, Linv = 0, Q = 0, Lsum = 0, SZ = 0,
-         perm = 0, Wp = 0, Gsave = 0, total = 0;
+         perm = 0, Wp = 0, invperm = 0, gidx = 0, Gsave = 0, total = 0;
 };
 
 Layout layout_full(const Shape& s) {
@@ -123,6 +125,10 @@ Layout layout_full(const Shape& s) {
   if (s.act_order) {
     L.perm = take((size_t)s.m * sizeof(int32_t));
     L.Wp = take((size_t)s.n * (size_t)s.m * sizeof(float));
+  }
+  if (s.static_groups) {
+    L.invperm = take((size_t)s.m * sizeof(int32_t));
+    L.gidx = take((size_t)s.m * sizeof(int32_t));
   }
   if (s.keep_gram) L.Gsave = take((size_t)s.m * (size_t)s.m * sizeof(double));
   L.total = off;
@@ -168,7 +174,7 @@ int check_params(const ojbkq_params* p) {
   if (p->K < 0 || p->K > (1 << 20)) return fail(OJBKQ_EINVAL, "K must be in [0, 2^20]");
   if (p->scheme != 0 && p->scheme != 1) return fail(OJBKQ_EINVAL, "scheme must be 0 or 1");
   if (p->scheme == 1 && p->bits < 2) return fail(OJBKQ_EINVAL, "the symmetric scheme needs bits >= 2");
-  if (p->act_order != 0 && p->act_order != 1) return fail(OJBKQ_EINVAL, "act_order must be 0 or 1");
+  if (p->act_order < 0 || p->act_order > 2) return fail(OJBKQ_EINVAL, "act_order must be 0, 1 or 2");
   if (p->keep_gram != 0 && p->keep_gram != 1) return fail(OJBKQ_EINVAL, "keep_gram must be 0 or 1");
   if (!(p->alpha >= 0.0 && p->alpha <= 1.0)) return fail(OJBKQ_EINVAL, "alpha must be in [0, 1]");
   if (!(p->lambda_rel >= 0.0) || !std::isfinite(p->lambda_rel))
@@ -447,6 +453,10 @@ int ctx_solve(ojbkq_ctx* c, const float* W, double alpha, uint8_t* codes, float*
       const size_t mm = (size_t)s.m * s.m * sizeof(double);
       double* tmp = c->at<double>(c->L.Linv);
       OJBKQ_HIP(ojbkq::launch_act_order_perm(Lf, s.m, perm, st), "act order");
+      if (s.static_groups)
+        OJBKQ_HIP(ojbkq::launch_position_groups(perm, s.m, s.g, c->at<int32_t>(c->L.invperm),
+                                                c->at<int32_t>(c->L.gidx), st),
+                  "position groups");
       OJBKQ_HIP(ojbkq::launch_mirror_lower(Lf, s.m, st), "mirror Gram");
       OJBKQ_HIP(ojbkq::launch_gather(Lf, s.m, perm, perm, s.m, s.m, tmp, s.m, st), "permute Gram");
       OJBKQ_HIP(hipMemcpyAsync(Lf, tmp, mm, hipMemcpyDeviceToDevice, st), "copy Gram");
@@ -480,20 +490,29 @@ int ctx_solve(ojbkq_ctx* c, const float* W, double alpha, uint8_t* codes, float*
     OJBKQ_HIP(ojbkq::invert_lower(Lf, s.m, c->at<double>(c->L.Linv), c->at<double>(c->L.F), st),
               "factor inverse");
     OJBKQ_HIP(ojbkq::launch_decode_tiles(Lf, s.m, c->at<double>(c->L.F), st), "decoder tiles");
-    OJBKQ_HIP(ojbkq::launch_group_row_sums(Lf, s.m, s.g, s.G, c->at<double>(c->L.Lsum), st),
+    OJBKQ_HIP(ojbkq::launch_group_row_sums(Lf, s.m, s.g, s.G,
+                                           s.static_groups ? c->at<int32_t>(c->L.invperm) : nullptr,
+                                           c->at<double>(c->L.Lsum), st),
               "group sums");
     c->factored = true;
     stage_end(c, OJBKQ_STAGE_FACTOR, t0);
     t0 = stage_begin(c);
   }
+  // scales of W's own groups (static groups), else of the groups of positions
+  if (s.static_groups)
+    OJBKQ_HIP(ojbkq::launch_scale_zero(W, s.n, s.m, s.g, s.G, c->p.bits, c->p.scheme == 1, scales,
+                                       zeros, st),
+              "scales");
   if (perm) {   // the permuted problem's weights W P^T
     float* Wp = c->at<float>(c->L.Wp);
     OJBKQ_HIP(ojbkq::launch_gather(W, s.m, nullptr, perm, s.n, s.m, Wp, s.m, st), "permute W");
     W = Wp;
   }
-  OJBKQ_HIP(ojbkq::launch_scale_zero(W, s.n, s.m, s.g, s.G, c->p.bits, c->p.scheme == 1, scales,
-                                     zeros, st),
-            "scales");
+  if (!s.static_groups)
+    OJBKQ_HIP(ojbkq::launch_scale_zero(W, s.n, s.m, s.g, s.G, c->p.bits, c->p.scheme == 1, scales,
+                                       zeros, st),
+              "scales");
+  const int32_t* gidx = s.static_groups ? c->at<int32_t>(c->L.gidx) : nullptr;
   double* gq = c->at<double>(c->L.gq);
   const bool cross = c->cross_seen && alpha != 1.0;
   if (route_q(s)) {
@@ -560,11 +579,12 @@ int ctx_solve(ojbkq_ctx* c, const float* W, double alpha, uint8_t* codes, float*
     OJBKQ_HIP(ojbkq::gemm_f64(g, st), "Rbar qbar");
   }
   double* al = c->at<double>(c->L.alpha);
-  OJBKQ_HIP(ojbkq::launch_klein_alpha(Lf, scales, s.n, s.m, s.g, s.G, log_rho(s.m, s.K), al, st),
+  OJBKQ_HIP(ojbkq::launch_klein_alpha(Lf, scales, s.n, s.m, s.g, s.G, gidx, log_rho(s.m, s.K), al,
+                                      st),
             "klein alpha");
   stage_end(c, OJBKQ_STAGE_CENTRES, t0);
   ojbkq::DecodeDesc d;
-  d.F = c->at<double>(c->L.F); d.gq = gq; d.S = scales; d.alpha = al;
+  d.F = c->at<double>(c->L.F); d.gq = gq; d.S = scales; d.alpha = al; d.gidx = gidx;
   d.m = s.m; d.n = s.n; d.g = s.g; d.G = s.G; d.K = (int)s.K; d.bits = c->p.bits;
   d.seed = c->p.seed;
   d.wg_paths = s.geo.wg_paths; d.threads = s.geo.threads;
@@ -779,7 +799,8 @@ int ojbkq_decode_stage(const ojbkq_params* p, const double* R, const double* qba
     g.C = gq; g.ldc = s.m;
     OJBKQ_HIP(ojbkq::gemm_f64(g, st), "Rbar qbar");
   }
-  OJBKQ_HIP(ojbkq::launch_klein_alpha(Lf, scales, s.n, s.m, s.g, s.G, log_rho(s.m, s.K), al, st),
+  OJBKQ_HIP(ojbkq::launch_klein_alpha(Lf, scales, s.n, s.m, s.g, s.G, nullptr, log_rho(s.m, s.K),
+                                      al, st),
             "klein alpha");
   OJBKQ_HIP(ojbkq::launch_decode_tiles(Lf, s.m, reinterpret_cast<double*>(ws + L.F), st),
             "decoder tiles");

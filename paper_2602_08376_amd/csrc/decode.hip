@@ -142,7 +142,7 @@ __device__ __forceinline__ void load_b(BOperand<NT, kUniS>& c, const DecodeDesc&
     for (int s = 0; s < 8; ++s) {
       int64_t f = bb * kBS + 4 * s + (lane >> 4);
       f = f < d.m ? f : d.m - 1;
-      const uint32_t grp = (uint32_t)f / (uint32_t)d.g;
+      const uint32_t grp = d.gidx ? (uint32_t)d.gidx[f] : (uint32_t)f / (uint32_t)d.g;
 #pragma unroll
       for (int t = 0; t < NT; ++t) c.sc[t][s] = load_scale(d.S + (so[t] + grp));
     }
@@ -286,7 +286,12 @@ __device__ __forceinline__ void decode_wave(const DecodeDesc& d, int64_t pbase, 
 #pragma unroll
       for (int k = 0; k < kGR; ++k) {
         z[k] = -sG[k * 64 + lane];
-        sr[k] = kUniS ? s_blk : (double)Sj[(uint32_t)(i0 + r0 + k < m ? i0 + r0 + k : m - 1) / (uint32_t)g];
+        if constexpr (kUniS) {
+          sr[k] = s_blk;
+        } else {
+          const uint32_t row = (uint32_t)(i0 + r0 + k < m ? i0 + r0 + k : m - 1);
+          sr[k] = (double)Sj[d.gidx ? (uint32_t)d.gidx[row] : row / (uint32_t)g];
+        }
         rb[k] = sD[(r0 + k) * (kBS + 1)] * sr[k];   // Rbar_ii
         u[k] = (kk != 0) ? klein_uniform(d.seed, (uint32_t)(i0 + r0 + k), (uint32_t)j, kk) : 0.0;
       }
@@ -459,7 +464,7 @@ hipError_t launch_decode(const DecodeDesc& d, hipStream_t stream) {
       d.wg_paths > 4 * (int64_t)d.threads)
     return hipErrorInvalidValue;
   const size_t lds = (size_t)(d.threads / 64) * kWaveLds;
-  const bool uniform_scale = d.G == 1 || d.g % kBS == 0;
+  const bool uniform_scale = !d.gidx && (d.G == 1 || d.g % kBS == 0);
   const void* fn = uniform_scale ? reinterpret_cast<const void*>(&decode_kernel<true>)
                                  : reinterpret_cast<const void*>(&decode_kernel<false>);
   hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);

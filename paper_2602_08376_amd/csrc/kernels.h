@@ -103,18 +103,21 @@ hipError_t invert_lower(const double* L, int64_t m, double* Linv, double* scratc
 // (S Z) [n, G] the products s z per (column, group).  Q does not depend on
 // W, so a mu sweep or a second weight matrix reuses it; the centres qbar are
 // never formed.
-// Lsum[t][i] = sum over rows l of group t of L[l][i].
-hipError_t launch_group_row_sums(const double* L, int64_t m, int64_t g, int64_t G, double* Lsum,
-                                 hipStream_t stream);
+// Lsum[t][i] = sum over rows l of group t of L[l][i]; the rows of group t are
+// t g .. t g + g - 1, or with `rows` (nullable) rows[t g .. t g + g).
+hipError_t launch_group_row_sums(const double* L, int64_t m, int64_t g, int64_t G,
+                                 const int32_t* rows, double* Lsum, hipStream_t stream);
 // SZ[j][t] = S[j][t] * Z[j][t] in fp64 (exact: z is a small integer).
 hipError_t launch_scale_zero_products(const float* S, const float* Z, int64_t n, int64_t G,
                                       double* SZ, hipStream_t stream);
 // Y = s * qbar for given centres (the decoder-only entry point).
 hipError_t launch_scale_centres(const double* qbar, const float* S, int64_t n, int64_t m,
                                 int64_t g, int64_t G, double* Y, hipStream_t stream);
-// alpha_j = log_rho / min_i (L_ii s_j(i))^2.
+// alpha_j = log_rho / min_i (L_ii s_j(i))^2, s_j(i) = S[j][i / g], or
+// S[j][gidx[i]] with gidx (nullable).
 hipError_t launch_klein_alpha(const double* L, const float* S, int64_t n, int64_t m, int64_t g,
-                              int64_t G, double log_rho, double* alpha, hipStream_t stream);
+                              int64_t G, const int32_t* gidx, double log_rho, double* alpha,
+                              hipStream_t stream);
 
 // ---- batched Babai / Klein decode and selection (Alg. 1, 3, 4) -------------
 // Every wave of the decoder owns up to 64 consecutive paths (one per lane),
@@ -202,6 +205,7 @@ struct DecodeDesc {
   const double* gq = nullptr;  // [n, m]: gq_j = Rbar_j qbar_j
   const float* S = nullptr;    // [n, G]
   const double* alpha = nullptr;  // [n]
+  const int32_t* gidx = nullptr;  // [m] scale group of each row, or null: row / g
   int64_t m = 0, n = 0, g = 0, G = 0;
   int K = 0, bits = 0;
   uint64_t seed = 0;
@@ -244,6 +248,9 @@ hipError_t launch_select(const uint8_t* pcodes, const double* presid, int64_t n,
 // perm[p] = the input feature at decode position p: features by increasing
 // diag(G) (G [m, m] fp64, diagonal read), equal values by index.
 hipError_t launch_act_order_perm(const double* G, int64_t m, int32_t* perm, hipStream_t stream);
+// Static groups: invperm[perm[p]] = p and gidx[p] = perm[p] / g.
+hipError_t launch_position_groups(const int32_t* perm, int64_t m, int64_t g, int32_t* invperm,
+                                  int32_t* gidx, hipStream_t stream);
 // Copies G's lower triangle onto its upper triangle (G [m, m] fp64).
 hipError_t launch_mirror_lower(double* G, int64_t m, hipStream_t stream);
 // out[r][c] = in[rmap[r]][cmap[c]] for r < rows, c < cols (rmap null:

@@ -6,7 +6,10 @@
 // positions m - 1 .. 0) meets the largest diagonals first.  The permuted
 // problem is P G P^T, P E P^T (or U P^T for an accumulated W E^T) and W P^T;
 // all of them are gathered once after the token sums, so the Gram kernel and
-// everything after it run unchanged.
+// everything after it run unchanged.  With static groups the scale groups stay
+// runs of g features in W's order, so the rows of one group are scattered over
+// the decode positions: the kernels that read s_j(i) then take the group of
+// each position from gidx.
 #include "kernels.h"
 
 namespace ojbkq {
@@ -81,12 +84,34 @@ __global__ __launch_bounds__(256) void gather_kernel(const T* __restrict__ in, i
   }
 }
 
+// Static groups: invperm[perm[p]] = p, and gidx[p] = perm[p] / g, the scale
+// group (a run of g features in W's order) of decode position p.
+__global__ __launch_bounds__(256) void position_groups_kernel(const int32_t* __restrict__ perm,
+                                                              int64_t m, int64_t g,
+                                                              int32_t* __restrict__ invperm,
+                                                              int32_t* __restrict__ gidx) {
+  for (int64_t p = (int64_t)blockIdx.x * 256 + threadIdx.x; p < m;
+       p += (int64_t)gridDim.x * 256) {
+    const int32_t f = perm[p];
+    invperm[f] = (int32_t)p;
+    gidx[p] = (int32_t)(f / g);
+  }
+}
+
 unsigned rows_grid(int64_t rows) { return (unsigned)(rows < 65535 ? rows : 65535); }
 
 }  // namespace
 
 hipError_t launch_act_order_perm(const double* G, int64_t m, int32_t* perm, hipStream_t stream) {
   act_order_rank_kernel<<<(unsigned)((m + 255) / 256), 256, 0, stream>>>(G, m, perm);
+  return hipGetLastError();
+}
+
+hipError_t launch_position_groups(const int32_t* perm, int64_t m, int64_t g, int32_t* invperm,
+                                  int32_t* gidx, hipStream_t stream) {
+  const int64_t b = (m + 255) / 256;
+  position_groups_kernel<<<(unsigned)(b < 65536 ? b : 65536), 256, 0, stream>>>(perm, m, g,
+                                                                               invperm, gidx);
   return hipGetLastError();
 }
 

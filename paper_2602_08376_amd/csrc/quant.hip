@@ -57,15 +57,22 @@ __global__ __launch_bounds__(256) void scale_zero_kernel(const float* __restrict
 
 // qbar = (w + c * delta) / s + z and Y = s * qbar, elementwise over [n, m].
 // One thread per column i of L and group t: a strided walk down g rows.
+// With `rows` (static groups), the rows of group t are rows[t g .. t g + g)
+// (the decode positions of features t g ..); L's strict upper part is zero.
 __global__ __launch_bounds__(256) void group_row_sums_kernel(const double* __restrict__ L,
                                                              int64_t m, int64_t g, int64_t G,
+                                                             const int32_t* __restrict__ rows,
                                                              double* __restrict__ Lsum) {
   for (int64_t t = blockIdx.y; t < G; t += gridDim.y) {
     const int64_t l0 = t * g, l1 = (l0 + g < m) ? l0 + g : m;
     for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < m;
          i += (int64_t)gridDim.x * 256) {
       double s = 0.0;
-      for (int64_t l = (l0 > i ? l0 : i); l < l1; ++l) s += L[l * m + i];   // L[l][i] = 0 for l < i
+      if (rows) {
+        for (int64_t l = l0; l < l1; ++l) s += L[(int64_t)rows[l] * m + i];
+      } else {
+        for (int64_t l = (l0 > i ? l0 : i); l < l1; ++l) s += L[l * m + i];   // L[l][i] = 0 for l < i
+      }
       Lsum[t * m + i] = s;
     }
   }
@@ -96,6 +103,7 @@ __global__ __launch_bounds__(256) void scale_centres_kernel(const double* __rest
 __global__ __launch_bounds__(256) void klein_alpha_kernel(const double* __restrict__ L,
                                                           const float* __restrict__ S, int64_t n,
                                                           int64_t m, int64_t g, int64_t G,
+                                                          const int32_t* __restrict__ gidx,
                                                           double log_rho,
                                                           double* __restrict__ alpha) {
   const int lane = threadIdx.x & 63;
@@ -103,7 +111,7 @@ __global__ __launch_bounds__(256) void klein_alpha_kernel(const double* __restri
   if (j >= n) return;
   double mn = INFINITY;
   for (int64_t i = lane; i < m; i += 64) {
-    const double rb = L[i * m + i] * (double)S[j * G + i / g];
+    const double rb = L[i * m + i] * (double)S[j * G + (gidx ? (int64_t)gidx[i] : i / g)];
     const double r2 = rb * rb;
     mn = r2 < mn ? r2 : mn;
   }
@@ -130,12 +138,12 @@ hipError_t launch_scale_zero(const float* W, int64_t n, int64_t m, int64_t g, in
   return hipGetLastError();
 }
 
-hipError_t launch_group_row_sums(const double* L, int64_t m, int64_t g, int64_t G, double* Lsum,
-                                 hipStream_t stream) {
+hipError_t launch_group_row_sums(const double* L, int64_t m, int64_t g, int64_t G,
+                                 const int32_t* rows, double* Lsum, hipStream_t stream) {
   const int64_t bx = (m + 255) / 256;
   const int64_t by = G < 65535 ? G : 65535;
   group_row_sums_kernel<<<dim3((unsigned)(bx < 1024 ? bx : 1024), (unsigned)by), 256, 0, stream>>>(
-      L, m, g, G, Lsum);
+      L, m, g, G, rows, Lsum);
   return hipGetLastError();
 }
 
@@ -152,9 +160,10 @@ hipError_t launch_scale_centres(const double* qbar, const float* S, int64_t n, i
 }
 
 hipError_t launch_klein_alpha(const double* L, const float* S, int64_t n, int64_t m, int64_t g,
-                              int64_t G, double log_rho, double* alpha, hipStream_t stream) {
-  klein_alpha_kernel<<<(unsigned)((n + 3) / 4), 256, 0, stream>>>(L, S, n, m, g, G, log_rho,
-                                                                    alpha);
+                              int64_t G, const int32_t* gidx, double log_rho, double* alpha,
+                              hipStream_t stream) {
+  klein_alpha_kernel<<<(unsigned)((n + 3) / 4), 256, 0, stream>>>(L, S, n, m, g, G, gidx,
+                                                                    log_rho, alpha);
   return hipGetLastError();
 }
 

@@ -68,21 +68,30 @@ def test_scheme_values():
 
 
 def test_act_order_values():
-    """act_order is 0 or 1; 1 adds the decode order and the permuted weights
-    (m int32 + n m float32) to the workspace."""
+    """act_order is 0, 1 or 2; 1 adds the decode order and the permuted
+    weights (m int32 + n m float32) to the workspace, 2 also the inverse order
+    and the group of every position; keep_gram is 0 or 1."""
     lib = ok.library()
-    for v, ok_ in ((0, True), (1, True), (2, False), (-1, False)):
+
+    def perm_ws(m, n):
+        return ok.workspace_bytes(m, n, 4, 128, 4, act_order=True)
+
+    for v, ok_ in ((0, True), (1, True), (2, True), (3, False), (-1, False)):
         p = _p()
         p.act_order = v
         assert (lib.ojbkq_workspace_bytes(ctypes.byref(p)) > 0) == ok_, v
+    for v, ok_ in ((0, True), (1, True), (2, False), (-1, False)):
         p = _p()
         p.keep_gram = v
         assert (lib.ojbkq_workspace_bytes(ctypes.byref(p)) > 0) == ok_, v
+    # static groups add the inverse order and the group of every position
+    assert ok.workspace_bytes(300, 70, 4, 128, 4, act_order="static") >= perm_ws(300, 70) + 2 * 300 * 4
+    with pytest.raises(ValueError):
+        ok._params(128, 64, 4, 128, 4, 0.5, 0.01, 0, act_order="desc")
     assert ok.workspace_bytes(300, 70, 4, 128, 4, keep_gram=True) >= \
         ok.workspace_bytes(300, 70, 4, 128, 4) + 300 * 300 * 8
     plain = ok.workspace_bytes(300, 70, 4, 128, 4)
-    perm = ok.workspace_bytes(300, 70, 4, 128, 4, act_order=True)
-    assert perm >= plain + 300 * 4 + 70 * 300 * 4
+    assert perm_ws(300, 70) >= plain + 300 * 4 + 70 * 300 * 4
 
 
 def test_null_and_shape_errors_before_any_launch():

@@ -54,13 +54,14 @@ def check_perm(perm, G_o):
     return len(bad)
 
 
-def check_against_oracle(cfg, g, W, Xr, Xq, mu, G_o=None):
+def check_against_oracle(cfg, g, W, Xr, Xq, mu, G_o=None, static=False):
     perm = np64(g.perm).astype(np.int64)
     Xq_np = np64(Xq)
     G_o = orc.gram(Xq_np) if G_o is None else G_o
     moved = check_perm(perm, G_o)
     o = orc.quantize_layer(np64(W), np64(Xr), Xq_np, mu, cfg.bits, cfg.group, cfg.K,
-                           cfg.klein_seed, lambda_rel=cfg.lambda_rel, G=G_o, perm=perm)
+                           cfg.klein_seed, lambda_rel=cfg.lambda_rel, G=G_o, perm=perm,
+                           static_groups=static)
     S, Z = np64(g.scales), np64(g.zeros)
     assert np.array_equal(S, o.scales), "scales differ"
     assert np.array_equal(Z, o.zeros), "zero points differ"
@@ -69,7 +70,8 @@ def check_against_oracle(cfg, g, W, Xr, Xq, mu, G_o=None):
     assert codes.max() <= (1 << cfg.bits) - 1
     frac = float((codes == o.codes).mean())
     worst, nwin = check_residuals(np64(g.residuals), np64(g.winner), o.residuals, o.winner)
-    print(f"[act order {cfg.key} b{cfg.bits} g{cfg.group} K{cfg.K} mu={mu}] order moved at {moved} "
+    print(f"[act order{' static' if static else ''} {cfg.key} b{cfg.bits} g{cfg.group} K{cfg.K} "
+          f"mu={mu}] order moved at {moved} "
           f"positions, code agreement {frac:.6f}, winner mismatches {nwin}, worst residual rel "
           f"err {worst:.2e}", flush=True)
     assert frac >= 0.999
@@ -169,3 +171,49 @@ def test_packed_product_in_decode_order(n, m, T, bits, group):
     gidx = orc.feature_groups(perm, group)
     W_orig = orc.dequantize_by_feature(codes, np64(q.scales), np64(q.zeros), gidx)
     assert np.array_equal(W_orig.astype(np.float32).astype(np.float16)[:, perm], W16)
+
+
+@pytest.mark.parametrize("m,n,T,bits,group,K,seed,mu", [
+    (200, 150, 700, 4, 64, 6, 71, 0.5),     # Q route, groups of 64 scattered over positions
+    (300, 140, 900, 3, 128, 4, 72, 0.0),    # direct route, ragged last group
+    (300, 40, 900, 4, 32, 5, 73, 0.5),      # projected route
+    (33, 2, 80, 8, 16, 5, 74, 0.25),        # ragged groups of 16
+    (130, 5, 300, 2, 0, 3, 75, 1.0),        # one group: the same as position groups
+])
+def test_static_groups_layer_matches_oracle(m, n, T, bits, group, K, seed, mu):
+    """act_order = "static": the scale groups stay runs of g features in W's
+    order, so the decoder reads each row's scale through the group index of
+    its position, and the scales equal those of the plain call."""
+    cfg = cfg_of(m, n, T, bits, group, K, seed, mu)
+    W, Xr, Xq = make_layer(cfg, device=DEV)
+    g = ok.quantize_layer(W, Xr, Xq, mu, bits, group, K, cfg.klein_seed, cfg.lambda_rel,
+                          act_order="static")
+    plain = ok.quantize_layer(W, Xr, Xq, mu, bits, group, K, cfg.klein_seed, cfg.lambda_rel)
+    torch.cuda.synchronize()
+    assert torch.equal(g.scales, plain.scales) and torch.equal(g.zeros, plain.zeros)
+    check_against_oracle(cfg, g, W, Xr, Xq, mu, static=True)
+
+
+def test_static_groups_staged_and_plain_product():
+    """Static groups through the staged calls (chunks, two knobs on one
+    factor), then the plain packed product (no perm) against the oracle."""
+    cfg = cfg_of(256, 96, 1200, 4, 64, 4, 76)
+    W, Xr, Xq = make_layer(cfg, device=DEV)
+    s = ok.LayerSolver(cfg.m, cfg.n, cfg.bits, cfg.group, cfg.K, cfg.klein_seed, device=DEV,
+                       act_order="static")
+    s.accumulate(Xr[:, :500], Xq[:, :500])
+    s.accumulate(Xr[:, 500:], Xq[:, 500:])
+    G_o = orc.gram(np64(Xq))
+    for mu in (0.5, 0.0):
+        q = s.solve(W, mu)
+        torch.cuda.synchronize()
+        check_against_oracle(cfg, q, W, Xr, Xq, mu, G_o=G_o, static=True)
+    s.close()
+    X16 = Xq.half()
+    P = ok.pack_codes(q.codes, cfg.bits)
+    Y = ok.dequant_matmul(P, q.scales, q.zeros, cfg.m, cfg.bits, cfg.group, X16)
+    torch.cuda.synchronize()
+    W16 = oi.dequantize_fp16(np64(q.codes), np64(q.scales), np64(q.zeros), cfg.group)
+    x16 = X16.cpu().numpy()
+    err = np.abs(Y.cpu().numpy().astype(np.float64) - oi.dequant_matmul(W16, x16))
+    assert np.all(err <= oi.summation_bound(W16, x16) + 1e-30)
