@@ -38,6 +38,17 @@ PEAK_F64_MFMA_TFLOPS = 78.6     # MI355X dense fp64 matrix peak
 PEAK_HBM_GBS = 8000.0
 
 
+def act_order_arg(args):
+    """The binding's act_order value for --act-order."""
+    return {None: False, "positions": True, "static": "static"}[args.act_order]
+
+
+def packing_perm(args, q):
+    """The order to pack codes in: the decode order when the scale groups
+    follow it, else W's own (no act order, or static groups)."""
+    return q.perm if args.act_order == "positions" else None
+
+
 def log(msg):
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
 
@@ -65,9 +76,11 @@ def parse():
                          "the output error against the full-precision target and against the "
                          "quantized input, on one factor per layer (l3_* keys or 'all')")
     ap.add_argument("--mu-values", default="0,0.2,0.4,0.6,0.8,1", help="alpha values of --sweep-mu")
-    ap.add_argument("--act-order", action="store_true",
+    ap.add_argument("--act-order", nargs="?", const="positions", default=None,
+                    choices=("positions", "static"),
                     help="weight permutation: decide the features with the largest Hessian "
-                         "diagonal first (every mode)")
+                         "diagonal first (every mode); scale groups by decode position "
+                         "(default) or kept as W's own groups (static)")
     ap.add_argument("--scheme", default="asym", choices=("asym", "sym"),
                     help="scales and zero points: asymmetric min-max or symmetric Absmax")
     ap.add_argument("--mlp-stack", action="store_true",
@@ -106,7 +119,7 @@ def sweep_k(args):
         def layer(K):
             s = ok.LayerSolver(cfg.m, cfg.n, cfg.bits, cfg.group, K, cfg.klein_seed,
                                cfg.lambda_rel, device=dev, scheme=args.scheme,
-                               act_order=args.act_order)
+                               act_order=act_order_arg(args))
             s.set_timing(True)
             torch.cuda.synchronize()
             t0 = time.perf_counter()
@@ -284,17 +297,18 @@ def mlp_stack(args):
             torch.cuda.synchronize()
             t0 = time.perf_counter()
             s = ok.LayerSolver(d, d, bits, group, K, 0, 0.01, device=dev, scheme=args.scheme,
-                               act_order=args.act_order)
+                               act_order=act_order_arg(args))
             s.set_weights(W)
             s.accumulate(X, Xq)
             q = s.solve(W, mu)
             torch.cuda.synchronize()
             qtimes.append(time.perf_counter() - t0)
             s.close()
-            P = ok.pack_codes(q.codes, bits, q.perm)     # decode order with act order
+            pp = packing_perm(args, q)                   # decode order, position groups
+            P = ok.pack_codes(q.codes, bits, pp)
             Xq16 = Xq.half()
             Yq, ms = product_ms(lambda: ok.dequant_matmul(P, q.scales, q.zeros, d, bits, group,
-                                                          Xq16, q.perm))
+                                                          Xq16, pp))
             dq.append(ms)
             Y = W @ X                                  # the full-precision stack
             errs.append(float((Yq - Y).norm() / Y.norm()))
@@ -346,12 +360,13 @@ def adaptive_stack(args):
     lams, mus, ks = (0.001, 0.01, 0.1), (0.0, 0.2, 0.4, 0.6, 0.8, 1.0), (0, 4, 16)
 
     def product(q, Xq16):
-        P = ok.pack_codes(q.codes, bits, q.perm)
-        return ok.dequant_matmul(P, q.scales, q.zeros, d, bits, group, Xq16, q.perm)
+        pp = packing_perm(args, q)
+        P = ok.pack_codes(q.codes, bits, pp)
+        return ok.dequant_matmul(P, q.scales, q.zeros, d, bits, group, Xq16, pp)
 
     def quantize(W, X, Xq, search):
         s = ok.LayerSolver(d, d, bits, group, max(ks), 0, 0.01, device=dev,
-                           scheme=args.scheme, act_order=args.act_order, keep_gram=True)
+                           scheme=args.scheme, act_order=act_order_arg(args), keep_gram=True)
         s.set_weights(W)
         s.accumulate(X[:, :Tf], Xq[:, :Tf])
         Yv = W @ X[:, Tf:]
@@ -438,7 +453,7 @@ def sweep_mu(args):
         ny, nyq = float(Y.norm()), float(Yq.norm())
         s = ok.LayerSolver(cfg.m, cfg.n, cfg.bits, cfg.group, cfg.K, cfg.klein_seed,
                            cfg.lambda_rel, device=dev, scheme=args.scheme,
-                           act_order=args.act_order)
+                           act_order=act_order_arg(args))
         s.set_weights(W)
         s.accumulate(X, Xq)
         g = ok.num_groups(cfg.m, cfg.group)
@@ -447,7 +462,7 @@ def sweep_mu(args):
             q = s.solve(W, mu)
             # group of every input feature: that of its decode position
             gidx = torch.arange(cfg.m, device=dev) // gs
-            if q.perm is not None:
+            if packing_perm(args, q) is not None:
                 gidx = torch.empty_like(gidx).index_copy_(0, q.perm.long(), gidx)
             Sx = q.scales[:, gidx]
             Zx = q.zeros[:, gidx]
@@ -508,7 +523,7 @@ def main():
         f"({sum(x.numel() * 8 for x, _ in chunks) / 2**30:.1f} GiB of activations)")
 
     need = ok.workspace_bytes(cfg.m, cfg.n, cfg.bits, cfg.group, cfg.K, cfg.mu, cfg.lambda_rel,
-                              cfg.klein_seed, act_order=args.act_order)
+                              cfg.klein_seed, act_order=act_order_arg(args))
     ws = torch.empty(need, dtype=torch.uint8, device=dev)
     stream = torch.cuda.current_stream(dev)
     log(f"workspace {need / 2**30:.2f} GiB")
@@ -516,7 +531,7 @@ def main():
     def step(record):
         s = ok.LayerSolver(cfg.m, cfg.n, cfg.bits, cfg.group, cfg.K, cfg.klein_seed,
                            cfg.lambda_rel, device=dev, workspace=ws, scheme=args.scheme,
-                           act_order=args.act_order)
+                           act_order=act_order_arg(args))
         s.set_timing(True)                        # per-stage HIP events inside the library
         s.set_weights(W)                          # lets thin layers skip the m x m cross term
         ev = [torch.cuda.Event(enable_timing=True) for _ in range(2 * len(chunks) + 1)]
@@ -579,7 +594,7 @@ def main():
         "dtype": "f64",
         "data": "synthetic (seeded, generated on the GPU; inputs resident in HBM)",
         "config": {**workload_desc(cfg), **({"scheme": "sym"} if args.scheme == "sym" else {}),
-                   **({"act_order": True} if args.act_order else {})},
+                   **({"act_order": args.act_order} if args.act_order else {})},
         "stages_ms": {"gram_cross_per_launch": gc_avg,
                       "rest_of_path": sum(solve_ms) / len(solve_ms),
                       **{f"library_{k}": v for k, v in stage_ms.items()}},

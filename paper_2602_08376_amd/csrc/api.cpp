@@ -91,7 +91,7 @@ int64_t proj_tokens(const Shape& s) {
 struct Layout {
   size_t status = 0, lam2 = 0, G = 0, E = 0, U = 0, gq = 0, alpha = 0, pcodes = 0,
          presid = 0, gc_scratch = 0, gc_tiles = 0, F = 0, Linv = 0, Q = 0, Lsum = 0, SZ = 0,
-         perm = 0, Wp = 0, invperm = 0, gidx = 0, Gsave = 0, total = 0;
+         perm = 0, Wp = 0, invperm = 0, gidx = 0, spos = 0, Gsave = 0, total = 0;
 };
 
 Layout layout_full(const Shape& s) {
@@ -129,6 +129,7 @@ Layout layout_full(const Shape& s) {
   if (s.static_groups) {
     L.invperm = take((size_t)s.m * sizeof(int32_t));
     L.gidx = take((size_t)s.m * sizeof(int32_t));
+    L.spos = take((size_t)s.n * (size_t)((s.m + 31) / 32 * 32) * sizeof(float));
   }
   if (s.keep_gram) L.Gsave = take((size_t)s.m * (size_t)s.m * sizeof(double));
   L.total = off;
@@ -585,6 +586,12 @@ int ctx_solve(ojbkq_ctx* c, const float* W, double alpha, uint8_t* codes, float*
   stage_end(c, OJBKQ_STAGE_CENTRES, t0);
   ojbkq::DecodeDesc d;
   d.F = c->at<double>(c->L.F); d.gq = gq; d.S = scales; d.alpha = al; d.gidx = gidx;
+  if (gidx) {   // each row's scale in the decoder's segment order
+    d.spos = c->at<float>(c->L.spos);
+    OJBKQ_HIP(ojbkq::launch_position_scales(scales, gidx, s.n, s.m, s.G, c->at<float>(c->L.spos),
+                                            st),
+              "position scales");
+  }
   d.m = s.m; d.n = s.n; d.g = s.g; d.G = s.G; d.K = (int)s.K; d.bits = c->p.bits;
   d.seed = c->p.seed;
   d.wg_paths = s.geo.wg_paths; d.threads = s.geo.threads;

@@ -129,10 +129,26 @@ struct BOperand {
 
 template <int NT, bool kUniS>
 __device__ __forceinline__ void load_b(BOperand<NT, kUniS>& c, const DecodeDesc& d, int64_t bb,
-                                       const uint8_t* cw, const uint32_t (&so)[NT], int lane) {
+                                       const uint8_t* cw, const uint32_t (&so)[NT],
+                                       const int64_t (&sp)[NT], int lane) {
   const uint8_t* Bt = cw + bb * kBlockCodes + (lane & 15) * kSeg + 8 * (lane >> 4);
 #pragma unroll
   for (int t = 0; t < NT; ++t) c.q[t] = *reinterpret_cast<const uint2*>(Bt + t * 16 * kSeg);
+  if constexpr (!kUniS) {
+    if (d.spos) {
+      // per-row scales in segment order: rows 4 s + h of the block are the
+      // eight floats 8 h .. 8 h + 7, one 32-byte run per lane
+#pragma unroll
+      for (int t = 0; t < NT; ++t) {
+        const float4* src =
+            reinterpret_cast<const float4*>(d.spos + sp[t] + bb * kBS + 8 * (lane >> 4));
+        const float4 lo = src[0], hi = src[1];
+        c.sc[t][0] = lo.x; c.sc[t][1] = lo.y; c.sc[t][2] = lo.z; c.sc[t][3] = lo.w;
+        c.sc[t][4] = hi.x; c.sc[t][5] = hi.y; c.sc[t][6] = hi.z; c.sc[t][7] = hi.w;
+      }
+      return;
+    }
+  }
   if constexpr (kUniS) {
     const uint32_t grp = d.G == 1 ? 0u : (uint32_t)(bb * kBS) / (uint32_t)d.g;
 #pragma unroll
@@ -159,16 +175,16 @@ __device__ __forceinline__ void load_b(BOperand<NT, kUniS>& c, const DecodeDesc&
 template <int NT, bool kUniS>
 __device__ __forceinline__ void lazy_update(const DecodeDesc& d, int64_t nb, int64_t b,
                                             const uint8_t* cw, const uint32_t (&so)[NT],
-                                            d4 (&acc)[2][NT], int lane) {
+                                            const int64_t (&sp)[NT], d4 (&acc)[2][NT], int lane) {
   double2 a[8];   // R[16 a + l % 16][4 s + l / 16], a = 0, 1, for the 4-row steps s = 0..7
   const double* At = d.F + decode_offdiag_tile(nb, b, nb - 1) * kDecodeTile + 2 * lane;
 #pragma unroll
   for (int s = 0; s < 8; ++s) a[s] = *reinterpret_cast<const double2*>(At + s * 128);
   BOperand<NT, kUniS> cur, nxt;
-  load_b(cur, d, nb - 1, cw, so, lane);
+  load_b(cur, d, nb - 1, cw, so, sp, lane);
   for (int64_t bb = nb - 1; bb > b; --bb) {
     const int64_t bn = bb - 1 > b ? bb - 1 : b + 1;
-    load_b(nxt, d, bn, cw, so, lane);
+    load_b(nxt, d, bn, cw, so, sp, lane);
     const double* An = d.F + decode_offdiag_tile(nb, b, bn) * kDecodeTile + 2 * lane;
     // B = code * s, formed exactly as fma(2^52 + code, s, -2^52 s): the first
     // factor is assembled from the code's bits, and code * s needs at most 32
@@ -218,12 +234,15 @@ __device__ __forceinline__ void decode_wave(const DecodeDesc& d, int64_t pbase, 
   // MFMA operand B and result: tile t carries path 16 t + l % 16 of this wave.
   // Scale offsets fit 32 bits (n G < 2^31 is checked on the host).
   uint32_t so[NT], colB[NT];
+  int64_t sp[NT];   // row offsets of the per-row scales (d.spos)
 #pragma unroll
   for (int t = 0; t < NT; ++t) {
     const int loc = 16 * t + (lane & 15);
     colB[t] = (uint32_t)((pbase + (loc < npw ? loc : 0)) / kp1);
     so[t] = colB[t] * (uint32_t)G;
+    sp[t] = (int64_t)colB[t] * (nb * kBS);
   }
+  const float* const Spj = d.spos ? d.spos + j * (nb * kBS) : nullptr;
 
   double* const sG = sZ;            // [4][64]: a group's z or e values by (row, path)
   double* const sD = sZ + kGBuf;    // sD[r * 32 + c] = R[i0 + c][i0 + r], c <= r
@@ -258,7 +277,7 @@ __device__ __forceinline__ void decode_wave(const DecodeDesc& d, int64_t pbase, 
           acc[a][t][r] = (row < bl) ? -gb[row] : 0.0;
         }
     }
-    if (b + 1 < nb) lazy_update<NT, kUniS>(d, nb, b, cw, so, acc, lane);
+    if (b + 1 < nb) lazy_update<NT, kUniS>(d, nb, b, cw, so, sp, acc, lane);
     wave_sync();   // the diagonal tile is in LDS
 
     // ---- serial steps, one path per lane, in groups of four rows from the
@@ -288,6 +307,8 @@ __device__ __forceinline__ void decode_wave(const DecodeDesc& d, int64_t pbase, 
         z[k] = -sG[k * 64 + lane];
         if constexpr (kUniS) {
           sr[k] = s_blk;
+        } else if (Spj) {
+          sr[k] = (double)Spj[i0 + seg_byte(r0 + k)];
         } else {
           const uint32_t row = (uint32_t)(i0 + r0 + k < m ? i0 + r0 + k : m - 1);
           sr[k] = (double)Sj[d.gidx ? (uint32_t)d.gidx[row] : row / (uint32_t)g];
@@ -456,6 +477,31 @@ hipError_t launch_decode_tiles(const double* L, int64_t m, double* F, hipStream_
   return hipGetLastError();
 }
 
+// spos[j][32 b + seg_byte(r)] = S[j][gidx[32 b + r]] (the last row repeated
+// past m): each row's scale, laid out like the code segments.
+__global__ __launch_bounds__(256) void position_scales_kernel(const float* __restrict__ S,
+                                                              const int32_t* __restrict__ gidx,
+                                                              int64_t n, int64_t m, int64_t G,
+                                                              float* __restrict__ spos) {
+  const int64_t mp = (m + kBS - 1) / kBS * kBS;
+  const int64_t total = n * mp;
+  for (int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x; e < total;
+       e += (int64_t)gridDim.x * 256) {
+    const int64_t j = e / mp, i = e % mp;
+    const int64_t row = i < m ? i : m - 1;
+    spos[j * mp + (i / kBS) * kBS + seg_byte((int)(i % kBS))] = S[j * G + gidx[row]];
+  }
+}
+
+hipError_t launch_position_scales(const float* S, const int32_t* gidx, int64_t n, int64_t m,
+                                  int64_t G, float* spos, hipStream_t stream) {
+  const int64_t mp = (m + kBS - 1) / kBS * kBS;
+  const int64_t b = (n * mp + 255) / 256;
+  position_scales_kernel<<<(unsigned)(b < 65536 ? b : 65536), 256, 0, stream>>>(S, gidx, n, m, G,
+                                                                               spos);
+  return hipGetLastError();
+}
+
 hipError_t launch_decode(const DecodeDesc& d, hipStream_t stream) {
   const DecodeGeom geo = decode_geometry(d.n, d.K);
   if (geo.nwg <= 0) return hipSuccess;
@@ -464,7 +510,7 @@ hipError_t launch_decode(const DecodeDesc& d, hipStream_t stream) {
       d.wg_paths > 4 * (int64_t)d.threads)
     return hipErrorInvalidValue;
   const size_t lds = (size_t)(d.threads / 64) * kWaveLds;
-  const bool uniform_scale = !d.gidx && (d.G == 1 || d.g % kBS == 0);
+  const bool uniform_scale = !d.gidx && !d.spos && (d.G == 1 || d.g % kBS == 0);
   const void* fn = uniform_scale ? reinterpret_cast<const void*>(&decode_kernel<true>)
                                  : reinterpret_cast<const void*>(&decode_kernel<false>);
   hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);

@@ -206,6 +206,9 @@ struct DecodeDesc {
   const float* S = nullptr;    // [n, G]
   const double* alpha = nullptr;  // [n]
   const int32_t* gidx = nullptr;  // [m] scale group of each row, or null: row / g
+  // or (preferred when set) each row's scale per column: [n][nb 32] in the
+  // code-segment order of launch_position_scales
+  const float* spos = nullptr;
   int64_t m = 0, n = 0, g = 0, G = 0;
   int K = 0, bits = 0;
   uint64_t seed = 0;
@@ -216,6 +219,10 @@ struct DecodeDesc {
 };
 
 hipError_t launch_decode(const DecodeDesc& d, hipStream_t stream);
+// spos [n][nb 32] fp32: spos[j][32 b + 8 (r % 4) + r / 4] = S[j][gidx[32 b + r]]
+// (rows past m repeat row m - 1), nb = ceil(m / 32).
+hipError_t launch_position_scales(const float* S, const int32_t* gidx, int64_t n, int64_t m,
+                                  int64_t G, float* spos, hipStream_t stream);
 
 // ---- the quantized layer in use (packing, dequantize-and-multiply) ----------
 // Words per packed row of m codes of `bits` bits.
