@@ -106,18 +106,19 @@ def test_attention_projection_full_size():
     assert int(codes_g.max()) <= (1 << cfg.bits) - 1
 
 
-def test_attention_projection_full_size_act_order():
+@pytest.mark.parametrize("mode", ["positions", "static"])
+def test_attention_projection_full_size_act_order(mode):
     """The same layer with the weight permutation: the GPU's decode order
     must sort the oracle's full-size Gram diagonal (ties only within 1e-12
     relative); the oracle then factors the permuted Gram and decodes a sample
     of columns on that order, every candidate, and the codes come back in W's
-    order."""
+    order.  Scale groups by decode position, or W's own (static)."""
     cfg = CONFIGS["c2"]
     dev = torch.device("cuda", 0)
     W = make_weights(cfg, device=dev)
     (Xr, Xq), = list(activation_chunks(cfg, device=dev))
     s = ok.LayerSolver(cfg.m, cfg.n, cfg.bits, cfg.group, cfg.K, cfg.klein_seed, cfg.lambda_rel,
-                       device=dev, act_order=True)
+                       device=dev, act_order=(mode if mode == "static" else True))
     s.set_weights(W)
     s.accumulate(Xr, Xq)
     g = s.solve(W, cfg.mu)
@@ -142,19 +143,25 @@ def test_attention_projection_full_size_act_order():
     del Gp
     Wp, Xqp, Xrp = Wn[:, perm], Xqn[perm], Xrn[perm]
     del Xqn, Xrn
-    S, Z = orc.scales_zeros(Wp, cfg.bits, cfg.group)
+    if mode == "static":   # W's own groups; position p on the group of feature perm[p]
+        S, Z = orc.scales_zeros(Wn, cfg.bits, cfg.group)
+        grp = perm // cfg.group
+    else:
+        S, Z = orc.scales_zeros(Wp, cfg.bits, cfg.group)
+        grp = cfg.group
     assert np.array_equal(np64(g.scales), S) and np.array_equal(np64(g.zeros), Z)
     cols = np.sort(np.random.default_rng(2025).choice(cfg.n, 8, replace=False))
     V = orc.relaxed_solution(Wp[cols], Xrp, Xqp, cfg.mu, lam2, R)
-    qb = orc.centres(V, S[cols], Z[cols], cfg.group)
+    qb = orc.centres(V, S[cols], Z[cols], grp)
     qbar_full = np.zeros((cfg.n, cfg.m))
     qbar_full[cols] = qb
-    print("[full c2 act order] oracle factor and centres done; decoding the sample", flush=True)
-    dec = orc.decode(R, qbar_full, S, cfg.bits, cfg.group, cfg.K, cfg.klein_seed, columns=cols)
+    print(f"[full c2 act order {mode}] oracle factor and centres done; decoding the sample",
+          flush=True)
+    dec = orc.decode(R, qbar_full, S, cfg.bits, grp, cfg.K, cfg.klein_seed, columns=cols)
     codes_o = np.empty_like(dec.codes)
     codes_o[:, perm] = dec.codes                  # back to W's order
     frac = float((codes_g[cols] == codes_o).mean())
-    Sx = orc.expand_groups(S[cols], cfg.m, cfg.group)
+    Sx = orc.expand_groups(S[cols], cfg.m, grp)
     for t, j in enumerate(cols):
         if win_g[j] == dec.winner[t] and not np.array_equal(codes_g[j], codes_o[t]):
             assert first_divergence_is_tie(R, qb[t], Sx[t], cfg.bits, dec.alpha[t],
@@ -163,7 +170,7 @@ def test_attention_projection_full_size_act_order():
     assert frac >= 0.999, frac
     rel = np.abs(pres_g[cols] - dec.path_resid) / np.abs(dec.path_resid)
     worst, nwin = check_residuals(res_g[cols], win_g[cols], dec.residuals, dec.winner)
-    print(f"[full c2 act order] code agreement {frac:.6f}, candidate residual max rel err "
+    print(f"[full c2 act order {mode}] code agreement {frac:.6f}, candidate residual max rel err "
           f"{rel.max():.2e}, winner mismatches {nwin}", flush=True)
     assert float(np.median(rel)) <= 1e-4
     assert np.array_equal(win_g, np.argmin(pres_g, axis=1))
