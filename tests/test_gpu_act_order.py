@@ -217,3 +217,27 @@ def test_static_groups_staged_and_plain_product():
     x16 = X16.cpu().numpy()
     err = np.abs(Y.cpu().numpy().astype(np.float64) - oi.dequant_matmul(W16, x16))
     assert np.all(err <= oi.summation_bound(W16, x16) + 1e-30)
+
+
+@pytest.mark.parametrize("mode", [True, "static"])
+def test_act_order_ties_and_degenerate_channels(mode):
+    """Equal keys and degenerate channels: two duplicated activation rows
+    (equal diagonals, which the GPU may order either way), a dead channel
+    (zero diagonal, decided last), an all-zero weight group, 1-bit codes and
+    K = 0 (Babai only)."""
+    cfg = cfg_of(96, 12, 400, 1, 32, 0, 77)
+    W, Xr, Xq = make_layer(cfg, device=DEV)
+    Xq, Xr, W = Xq.clone(), Xr.clone(), W.clone()
+    Xq[9] = Xq[5]
+    Xr[9] = Xr[5]
+    Xq[40] = 0.0
+    Xr[40] = 0.0
+    W[3, 32:64] = 0.0
+    g = ok.quantize_layer(W, Xr, Xq, 0.5, 1, 32, 0, cfg.klein_seed, cfg.lambda_rel,
+                          act_order=mode)
+    torch.cuda.synchronize()
+    perm = np64(g.perm)
+    assert perm[0] == 40                   # the zero diagonal comes first: decided last
+    assert abs(int(np.nonzero(perm == 5)[0][0]) - int(np.nonzero(perm == 9)[0][0])) == 1
+    assert int(g.winner.max()) == 0
+    check_against_oracle(cfg, g, W, Xr, Xq, 0.5, static=(mode == "static"))
