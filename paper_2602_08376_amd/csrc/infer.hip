@@ -162,12 +162,18 @@ __global__ __launch_bounds__(kThreads, 1) void dequant_matmul_kernel(DqArgs a) {
     s_cur = a.S[jj * a.G + grp];
     z_cur = a.Z[jj * a.G + grp];
     if (stage_in) {
-      const uint16_t* base = a.X + btok;
+      if (a.perm) {
+        const uint16_t* base = a.X + btok;
 #pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        int64_t r = k0 + 8 * bk + e;
-        if (a.perm) r = prow[e] < 0 ? 0 : (prow[e] >= a.m ? a.m - 1 : prow[e]);
-        xv[e] = *reinterpret_cast<const uint2*>(base + r * a.ldx);
+        for (int e = 0; e < 8; ++e) {
+          const int64_t r = prow[e] < 0 ? 0 : (prow[e] >= a.m ? a.m - 1 : prow[e]);
+          xv[e] = *reinterpret_cast<const uint2*>(base + r * a.ldx);
+        }
+      } else {
+        // rows k0 + 8 bk .. + 7: one pointer, rows ldx apart
+        const uint16_t* base = a.X + btok + (k0 + 8 * bk) * a.ldx;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) xv[e] = *reinterpret_cast<const uint2*>(base + e * a.ldx);
       }
     }
     load_rows(k0 + kStage);
@@ -180,18 +186,32 @@ __global__ __launch_bounds__(kThreads, 1) void dequant_matmul_kernel(DqArgs a) {
     // Two roundings: the empty asm pins the float32 product in a register,
     // so it is not folded into v_fma_mixlo_f16, which rounds once to fp16.
     const int zi = (int)z_cur;
+    if (stage_in) {   // interior: no masks
 #pragma unroll
-    for (int h = 0; h < 2; ++h) {
-      h8 v;
+      for (int h = 0; h < 2; ++h) {
+        h8 v;
 #pragma unroll
-      for (int c = 0; c < 8; ++c) {
-        const int cc = 8 * h + c;
-        float p = s_cur * (float)((int)cl.code(cc) - zi);
-        __asm__("" : "+v"(p));
-        const _Float16 w = (_Float16)p;
-        v[c] = (stage_in || (aj < a.n && kf + 16 * ac + cc < a.m)) ? w : (_Float16)0.f;
+        for (int c = 0; c < 8; ++c) {
+          float p = s_cur * (float)((int)cl.code(8 * h + c) - zi);
+          __asm__("" : "+v"(p));
+          v[c] = (_Float16)p;
+        }
+        *reinterpret_cast<h8*>(A + ar * kLd + 16 * ac + 8 * h) = v;
       }
-      *reinterpret_cast<h8*>(A + ar * kLd + 16 * ac + 8 * h) = v;
+    } else {
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        h8 v;
+#pragma unroll
+        for (int c = 0; c < 8; ++c) {
+          const int cc = 8 * h + c;
+          float p = s_cur * (float)((int)cl.code(cc) - zi);
+          __asm__("" : "+v"(p));
+          const _Float16 w = (_Float16)p;
+          v[c] = (aj < a.n && kf + 16 * ac + cc < a.m) ? w : (_Float16)0.f;
+        }
+        *reinterpret_cast<h8*>(A + ar * kLd + 16 * ac + 8 * h) = v;
+      }
     }
     if (stage_in) {
       // token i of k rows 8 bk + 2 p, + 1 -> one 32-bit word of row
