@@ -135,6 +135,10 @@ __global__ __launch_bounds__(kThreads, 1) void dequant_matmul_kernel(DqArgs a) {
   // tokens all exist (the same for every lane): no clamping or masking then.
   const bool tile_in = J0 + kTileJ <= a.n && T0 + kTileT <= a.T;
 
+  // this thread's channel row of the scales and zero points
+  const float* const sz_row[2] = {a.S + (aj < a.n ? aj : a.n - 1) * a.G,
+                                  a.Z + (aj < a.n ? aj : a.n - 1) * a.G};
+
   CodeLoader<BITS> cl;
   uint2 xv[8];           // VEC interior stages: 4 tokens of each of 8 k rows
   float s_cur = 0.f, z_cur = 0.f;
@@ -157,10 +161,10 @@ __global__ __launch_bounds__(kThreads, 1) void dequant_matmul_kernel(DqArgs a) {
     stage_in = VEC && tile_in && k0 + kStage <= a.m;
     const int64_t kc = k0 + 16 * ac;
     cl.load(a, aj, kc);
-    const int64_t grp = (kc < a.m ? kc : a.m - 1) / a.g;
-    const int64_t jj = aj < a.n ? aj : a.n - 1;
-    s_cur = a.S[jj * a.G + grp];
-    z_cur = a.Z[jj * a.G + grp];
+    // m < 2^20: the group index in 32-bit arithmetic
+    const uint32_t grp = (uint32_t)(kc < a.m ? kc : a.m - 1) / (uint32_t)a.g;
+    s_cur = sz_row[0][grp];
+    z_cur = sz_row[1][grp];
     if (stage_in) {
       if (a.perm) {
         const uint16_t* base = a.X + btok;
