@@ -110,6 +110,12 @@ struct CodeLoader {
 
 constexpr int kThreads = 512;  // eight waves: 2 x 4 blocks of 64 channels x 64 tokens
 
+// Offset (in halves) of the 16-byte block `blk` (features 8 blk .. 8 blk + 7
+// of the step) in row `row` of the activation tile: blocks are XOR-swizzled
+// by row / 4, so the eight lanes that stage rows 4 L + i (L = 0..7) of one
+// block write eight different bank groups.
+__device__ __forceinline__ int bswz(int row, int blk) { return 8 * (blk ^ ((row >> 2) & 7)); }
+
 template <int BITS, bool VEC>
 __global__ __launch_bounds__(kThreads, 1) void dequant_matmul_kernel(DqArgs a) {
   // two buffers: the waves dequantize and stage step s + 1 into one while
@@ -229,7 +235,7 @@ __global__ __launch_bounds__(kThreads, 1) void dequant_matmul_kernel(DqArgs a) {
           const uint32_t hi = (i < 2 ? xv[2 * p + 1].x : xv[2 * p + 1].y) >> (16 * (i & 1));
           wv[p] = (lo & 0xffffu) | (hi << 16);
         }
-        *reinterpret_cast<uint4*>(B + (4 * bq + i) * kLd + 8 * bk) =
+        *reinterpret_cast<uint4*>(B + (4 * bq + i) * kLd + bswz(4 * bq + i, bk)) =
             make_uint4(wv[0], wv[1], wv[2], wv[3]);
       }
     } else {
@@ -245,7 +251,7 @@ __global__ __launch_bounds__(kThreads, 1) void dequant_matmul_kernel(DqArgs a) {
           if (t < a.T && k < a.m) b = a.X[x_row(a, k) * a.ldx + t];
           u[e] = __builtin_bit_cast(_Float16, b);
         }
-        *reinterpret_cast<h8*>(B + (4 * bq + i) * kLd + 8 * bk) = u;
+        *reinterpret_cast<h8*>(B + (4 * bq + i) * kLd + bswz(4 * bq + i, bk)) = u;
       }
     }
   };
@@ -275,9 +281,10 @@ __global__ __launch_bounds__(kThreads, 1) void dequant_matmul_kernel(DqArgs a) {
         fa[x] = *reinterpret_cast<const h8*>(A + (wr * 64 + x * 16 + (lane & 15)) * kLd +
                                              32 * ks + 8 * (lane >> 4));
 #pragma unroll
-      for (int y = 0; y < 4; ++y)
-        fb[y] = *reinterpret_cast<const h8*>(B + (wc * 64 + y * 16 + (lane & 15)) * kLd +
-                                             32 * ks + 8 * (lane >> 4));
+      for (int y = 0; y < 4; ++y) {
+        const int row = wc * 64 + y * 16 + (lane & 15);
+        fb[y] = *reinterpret_cast<const h8*>(B + row * kLd + bswz(row, 4 * ks + (lane >> 4)));
+      }
 #pragma unroll
       for (int x = 0; x < 4; ++x)
 #pragma unroll
