@@ -89,6 +89,45 @@ def test_hand_worked_decode(golden):
     assert abs(float(res[0]) - gd["decode_babai_residual"][0]) < 1e-12
 
 
+@pytest.mark.parametrize("tag,mu", [("mu05", 0.5), ("mu0", 0.0)])
+def test_hand_worked_damped_layer(golden, tag, mu):
+    """The 3x3 layer with damping and a cross term, worked by hand: lambda^2,
+    the factor, the codes and the reduced residual."""
+    gd = golden("hand_worked_3x3.txt")
+    W = torch.tensor([gd["layer_W"]], dtype=torch.float32, device=DEV)
+    Xq = torch.tensor(gd["layer_Xq"], dtype=torch.float32, device=DEV).reshape(3, 3)
+    Xr = Xq + gd["damped_delta"][0] * torch.eye(3, dtype=torch.float32, device=DEV)
+    s = ok.LayerSolver(3, 1, 2, 128, 0, 0, lambda_rel=0.01, device=DEV)
+    s.accumulate(Xr, Xq)
+    g = s.solve(W, mu)
+    lam2 = float(s.inspect("lam2")[0])
+    L = np64(s.inspect("L"))
+    s.close()
+    assert abs(lam2 - gd["damped_lam2"][0]) <= 1e-9
+    assert np.allclose(L.T, np.array(gd["damped_R"]).reshape(3, 3), atol=5e-7, rtol=0)
+    assert np64(g.codes)[0].tolist() == [int(v) for v in gd[f"damped_{tag}_codes"]]
+    assert abs(float(g.residuals[0]) - gd[f"damped_{tag}_residual"][0]) < 5e-7
+    one = ok.quantize_layer(W, Xr, Xq, mu, 2, 128, 0, 0, lambda_rel=0.01)
+    assert torch.equal(one.codes, g.codes)
+
+
+def test_exact_residual_tie_keeps_babai(golden):
+    """Alg. 4's strict "<": candidates whose residual equals the Babai one
+    exactly (m = 1, qbar = 1.5) do not replace it."""
+    gd = golden("hand_worked_3x3.txt")
+    R = torch.ones(1, 1, dtype=torch.float64, device=DEV)
+    qbar = torch.full((1, 1), gd["tie_qbar"][0], dtype=torch.float64, device=DEV)
+    S = torch.ones(1, 1, dtype=torch.float32, device=DEV)
+    codes, res, win, pc, pr = ok.decode_stage(R, qbar, S, 2, 128, 8, 5, want_paths=True)
+    pr, pc = np64(pr)[0], np64(pc)[0, :, 0]
+    assert pc[0] == 2 and pr[0] == gd["tie_residual"][0]
+    ties = [k for k in range(1, 9) if pr[k] == pr[0]]
+    assert ties and any(pc[k] == 1 for k in ties)
+    assert int(win[0]) == int(gd["tie_winner"][0]) and float(res[0]) == 0.25
+    dec = orc.decode(np64(R), np64(qbar), np64(S), 2, 128, 8, 5)
+    assert np.array_equal(pc, dec.path_codes[0, :, 0])
+
+
 # ---------------------------------------------------------------------------
 # the decoder alone, on the oracle's own factor and centres
 # ---------------------------------------------------------------------------

@@ -340,6 +340,59 @@ def test_layer_hand_worked(golden):
     assert abs(res.residuals[0] - g["layer_residual"][0]) < 5e-7
 
 
+@pytest.mark.parametrize("tag,mu", [("mu05", 0.5), ("mu0", 0.0)])
+def test_damped_layer_hand_worked(golden, tag, mu):
+    """The 3x3 layer with damping (lambda_rel = 0.01) and a cross term
+    (X_ref = X_q + 0.1 I), worked by hand in the golden file: lambda^2 as
+    lambda_rel times the mean Gram diagonal (Alg. 1 step 2), the factor, the
+    relaxed solution through A^T t (Alg. 1 steps 3-4), the Babai codes and the
+    reduced residual, and the JTA score minus its floor.  A damping taken from
+    the trace, from lambda_rel^2 or from a 1/T-normalised Gram moves lambda^2
+    and the residual far outside these tolerances."""
+    g = golden("hand_worked_3x3.txt")
+    W = np.array([g["layer_W"]], dtype=np.float32)
+    Xq = np.array(g["layer_Xq"], dtype=np.float32).reshape(3, 3)
+    Xr = (Xq + np.float32(g["damped_delta"][0]) * np.eye(3, dtype=np.float32)).astype(np.float32)
+    res = o.quantize_layer(W, Xr, Xq, mu, 2, 128, 0, 0, lambda_rel=0.01)
+    assert abs(res.lam2 - g["damped_lam2"][0]) <= 1e-9
+    assert np.allclose(res.R, np.array(g["damped_R"]).reshape(3, 3), atol=5e-7, rtol=0)
+    assert np.allclose(res.V[0], g[f"damped_{tag}_v"], atol=5e-7, rtol=0)
+    assert np.allclose(res.qbar[0], g[f"damped_{tag}_qbar"], atol=5e-7, rtol=0)
+    assert res.codes[0].tolist() == [int(v) for v in g[f"damped_{tag}_codes"]]
+    assert abs(res.residuals[0] - g[f"damped_{tag}_residual"][0]) < 5e-7
+    What = o.dequantize(res.codes, res.scales, res.zeros, 128)
+    full = o.jta_score(W, Xr, Xq, What, mu, res.lam2)[0]
+    floor = o.jta_score(W, Xr, Xq, res.V, mu, res.lam2)[0]
+    assert abs(full - g[f"damped_{tag}_jta"][0]) < 5e-7
+    assert abs(floor - g[f"damped_{tag}_floor"][0]) < 5e-8
+
+
+def test_select_best_strict_minimum():
+    """Alg. 4 keeps a candidate only when its residual is strictly smaller, so
+    among equal minima the lowest index wins."""
+    assert o.select_best(np.array([0.5, 0.3, 0.3, 0.4])) == 1
+    assert o.select_best(np.array([0.2, 0.2, 0.2])) == 0
+    assert o.select_best(np.array([0.9, 0.4, 0.7, 0.4, 0.1, 0.1])) == 4
+    assert o.select_best(np.array([7.0])) == 0
+
+
+def test_exact_residual_tie_keeps_babai(golden):
+    """m = 1, qbar = 1.5 on the box {0..3}: Babai (half-to-even) gives 2, and
+    every Klein draw of 1 or 2 ties with it exactly at 0.25; the winner is the
+    Babai candidate."""
+    g = golden("hand_worked_3x3.txt")
+    R = np.ones((1, 1))
+    qbar = np.array([[g["tie_qbar"][0]]])
+    dec = o.decode(R, qbar, np.ones((1, 1), np.float32), 2, 128, 8, 5)
+    r = dec.path_resid[0]
+    assert dec.path_codes[0, 0, 0] == 2
+    assert r[0] == g["tie_residual"][0]
+    ties = [k for k in range(1, 9) if r[k] == r[0]]
+    assert ties, "no Klein candidate tied with Babai"
+    assert any(dec.path_codes[0, k, 0] == 1 for k in ties)       # a different point, same residual
+    assert dec.winner[0] == int(g["tie_winner"][0]) and dec.residuals[0] == 0.25
+
+
 @pytest.mark.parametrize("mu", [0.0, 0.3, 1.0])
 def test_relaxed_solution_is_stacked_least_squares(mu):
     """v_j minimises ||[X~; lambda I] v - [y*_j; lambda w_j]|| (Eq. new_obj), via lstsq."""
