@@ -53,7 +53,7 @@ def uniform53(seed: int, i, j, k):
     """Uniform double in [0, 1) for Klein draw (row i, column j, sample k).
 
     The words are pinned by the published known-answer vectors; the mapping
-    of two words to one double (res53) is a convention of this build, since
+    of two words to one double (res53) is a chosen convention, since
     the paper names no generator, and is pinned only by its definition."""
     seed = int(seed)
     i = np.asarray(i, dtype=np.uint64)
