@@ -204,6 +204,16 @@ int ojbkq_set_knobs(ojbkq_ctx* ctx, double lambda_rel, int32_t K);
  * Returns EINVAL for an unknown `which`, ESTATE before the first solve.    */
 int ojbkq_inspect(ojbkq_ctx* ctx, int which, const void** ptr);
 
+/* Every candidate of the last staged solve (Alg. 4 scores K + 1 candidates
+ * per column: the Babai path and K Klein paths), for checking decisions
+ * path by path: path_codes [n, K + 1, m] uint8 (device, caller-owned)
+ * receives candidate k of column j at [j][k][:], in W's feature order (with
+ * act_order the decode positions are mapped back through perm), K being the
+ * one the solve used.  Their residuals are ojbkq_inspect(4).
+ * Synchronises the context's stream.  Returns OJBKQ_OK, EINVAL (NULL
+ * arguments) or ESTATE (no solve yet).                                    */
+int ojbkq_path_codes(ojbkq_ctx* ctx, uint8_t* path_codes);
+
 /* Stage timing of a staged context, for tracing.  With timing enabled, the
  * accumulate and solve calls record HIP events on the context's stream around
  * each stage; ojbkq_stage_times() then returns the device milliseconds spent

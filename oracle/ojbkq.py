@@ -275,6 +275,8 @@ def decode_column(R: np.ndarray, qbar: np.ndarray, s_row: np.ndarray, bits: int,
     P = K + 1
     Q = np.zeros((P, m), dtype=np.int64)
     ks = np.arange(P)
+    # the uniforms of every (row, Klein path) of this column, drawn up front
+    U = uniform53(seed, np.arange(m)[:, None], j, ks[None, 1:]) if K > 0 else None
     for i in range(m - 1, -1, -1):
         # centre of row i from the rows already decided (Alg. 1 step 9)
         diff = qbar[i + 1:][None, :] - Q[:, i + 1:]       # [P, m - i - 1]
@@ -282,8 +284,7 @@ def decode_column(R: np.ndarray, qbar: np.ndarray, s_row: np.ndarray, bits: int,
         q = np.clip(np.rint(c), 0, qmax).astype(np.int64)  # Babai (Alg. 1 step 10)
         if K > 0:
             kappa = np.full(K, alpha * Rbar[i, i] ** 2)
-            u = uniform53(seed, i, j, ks[1:])
-            q[1:] = klein_pick(c[1:], kappa, u, qmax)
+            q[1:] = klein_pick(c[1:], kappa, U[i], qmax)
         Q[:, i] = q
     return Q
 

@@ -32,7 +32,7 @@ ABI_FUNCTIONS = (
     "ojbkq_solve", "ojbkq_destroy", "ojbkq_inspect", "ojbkq_decode_workspace_bytes",
     "ojbkq_decode_stage", "ojbkq_klein_log_rho", "ojbkq_last_error", "ojbkq_set_timing",
     "ojbkq_stage_times", "ojbkq_set_weights", "ojbkq_packed_words", "ojbkq_pack_codes",
-    "ojbkq_dequant_matmul", "ojbkq_set_knobs",
+    "ojbkq_dequant_matmul", "ojbkq_set_knobs", "ojbkq_path_codes",
 )
 
 STAGES = ("gram", "factor", "solve", "centres", "decode", "select")
@@ -87,6 +87,7 @@ def library() -> ctypes.CDLL:
         "ojbkq_solve": (ctypes.c_int, [vp, vp, dp, vp, vp, vp, vp, vp, vp]),
         "ojbkq_destroy": (ctypes.c_int, [vp]),
         "ojbkq_inspect": (ctypes.c_int, [vp, ctypes.c_int, ctypes.POINTER(vp)]),
+        "ojbkq_path_codes": (ctypes.c_int, [vp, vp]),
         "ojbkq_decode_stage": (ctypes.c_int, [P, vp, vp, vp, vp, ctypes.c_size_t, vp, vp, vp, vp,
                                               vp, vp]),
         "ojbkq_klein_log_rho": (ctypes.c_double, [i64, i64]),
@@ -315,6 +316,7 @@ class LayerSolver:
         _check(library().ojbkq_solve(self.h, _ptr(W), float(alpha), _ptr(out.codes),
                                      _ptr(out.scales), _ptr(out.zeros), _ptr(out.residuals),
                                      _ptr(out.winner), _ptr(out.perm)))
+        self._solved_K = self.K
         return out
 
     def inspect(self, which: str) -> torch.Tensor:
@@ -331,6 +333,14 @@ class LayerSolver:
             return self.ws[off:off + 4 * count].view(torch.int32).clone()
         flat = self.ws[off:off + 8 * count].view(torch.float64)
         return flat.reshape(shape).clone()
+
+    def path_codes(self) -> torch.Tensor:
+        """``ojbkq_path_codes``: every candidate of the last solve, [n, K + 1, m]
+        uint8 in W's feature order (K of that solve)."""
+        k = getattr(self, "_solved_K", self.K)
+        out = torch.empty(self.n, k + 1, self.m, dtype=torch.uint8, device=self.device)
+        _check(library().ojbkq_path_codes(self.h, _ptr(out)))
+        return out
 
     def set_timing(self, enable: bool = True):
         """Record per-stage device times from now on (see ojbkq_stage_times)."""

@@ -232,6 +232,7 @@ struct ojbkq_ctx {
   double lambda_rel = 0.0; // damping of the next factor (ojbkq_set_knobs may change it)
   size_t pcodes_cap = 0, presid_cap = 0;   // decoder buffers carved for params.K
   bool solved = false;
+  Shape solved_s;          // shape (K, decoder geometry) of the last solve
   // stage timing: event pairs recorded per stage, folded into ms[] at sync points
   bool timing = false;
   std::vector<std::pair<int, std::pair<hipEvent_t, hipEvent_t>>> pending;
@@ -610,6 +611,7 @@ int ctx_solve(ojbkq_ctx* c, const float* W, double alpha, uint8_t* codes, float*
               "decode order");
   stage_end(c, OJBKQ_STAGE_SELECT, t0);
   c->solved = true;
+  c->solved_s = s;
   return finish(c);
 }
 
@@ -764,6 +766,20 @@ int ojbkq_inspect(ojbkq_ctx* ctx, int which, const void** ptr) {
       break;
     default: return fail(OJBKQ_EINVAL, "unknown intermediate");
   }
+  return OJBKQ_OK;
+}
+
+int ojbkq_path_codes(ojbkq_ctx* ctx, uint8_t* path_codes) {
+  g_error.clear();
+  if (!ctx || !path_codes) return fail(OJBKQ_EINVAL, "ctx and path_codes are required");
+  if (!ctx->solved) return fail(OJBKQ_ESTATE, "path codes before the first solve");
+  const Shape& s = ctx->solved_s;
+  OJBKQ_HIP(ojbkq::launch_select(ctx->at<uint8_t>(ctx->L.pcodes), ctx->at<double>(ctx->L.presid),
+                                 s.n, s.m, (int)s.K, s.geo, nullptr, nullptr, nullptr, path_codes,
+                                 nullptr, s.act_order ? ctx->at<int32_t>(ctx->L.perm) : nullptr,
+                                 ctx->stream),
+            "path codes");
+  OJBKQ_HIP(hipStreamSynchronize(ctx->stream), "stream sync");
   return OJBKQ_OK;
 }
 

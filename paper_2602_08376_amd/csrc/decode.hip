@@ -385,7 +385,7 @@ __global__ __launch_bounds__(kDecodeMaxThreads) void decode_kernel(DecodeDesc d)
 }
 
 // First strict minimum over the K + 1 candidates of column j, then the gather
-// of the winner's codes (and, if asked, of every candidate).
+// of the winner's codes (codes non-null) and, if asked, of every candidate.
 __global__ __launch_bounds__(256) void select_kernel(const uint8_t* __restrict__ pcodes,
                                                      const double* __restrict__ presid, int64_t n,
                                                      int64_t m, int K, int64_t wg_paths,
@@ -411,7 +411,7 @@ __global__ __launch_bounds__(256) void select_kernel(const uint8_t* __restrict__
       }
     }
     kstar = best;
-    resid[j] = br;
+    if (resid) resid[j] = br;
     if (winner) winner[j] = best;
   }
   __syncthreads();
@@ -425,7 +425,7 @@ __global__ __launch_bounds__(256) void select_kernel(const uint8_t* __restrict__
     const int lane = loc - 16 * decode_wave_tiles(tiles, waves, w).first;
     return pcodes + ((wg * waves + w) * nb * 64 + lane) * kSeg;
   };
-  {
+  if (codes) {
     const uint8_t* src = path_base(j * kp1 + kstar);
     for (int64_t i = tid; i < m; i += 256)
       codes[j * m + (perm ? (int64_t)perm[i] : i)] =
@@ -438,7 +438,8 @@ __global__ __launch_bounds__(256) void select_kernel(const uint8_t* __restrict__
       const int64_t ps = j * kp1 + k;
       const uint8_t* src = path_base(ps);
       for (int64_t i = tid; i < m; i += 256)
-        path_codes[ps * m + i] = src[(i / kBS) * kBlockCodes + seg_byte((int)(i % kBS))];
+        path_codes[ps * m + (perm ? (int64_t)perm[i] : i)] =
+            src[(i / kBS) * kBlockCodes + seg_byte((int)(i % kBS))];
     }
   }
 }

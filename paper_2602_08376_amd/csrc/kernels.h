@@ -243,9 +243,10 @@ hipError_t launch_dequant_matmul(const uint32_t* P, const float* S, const float*
                                  hipStream_t stream);
 
 // First strict minimum over the K + 1 candidates of each column; gathers the
-// winner's codes.  path_codes / path_resid / winner may be null.  With perm
-// (a permutation of 0 .. m-1, or null), the code at decode position p goes to
-// codes[j][perm[p]] (the original feature order).
+// winner's codes.  Every output may be null (codes null: no winner gather).
+// With perm (a permutation of 0 .. m-1, or null), the code at decode position
+// p goes to codes[j][perm[p]] and path_codes[j][k][perm[p]] (the original
+// feature order).
 hipError_t launch_select(const uint8_t* pcodes, const double* presid, int64_t n, int64_t m, int K,
                          const DecodeGeom& geom, uint8_t* codes, double* resid, int32_t* winner,
                          uint8_t* path_codes, double* path_resid, const int32_t* perm,

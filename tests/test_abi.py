@@ -29,7 +29,7 @@ def test_library_builds_and_loads():
 
 def test_every_declared_symbol_is_exported():
     names = declared_functions()
-    assert len(names) == 18
+    assert len(names) == 19
     assert sorted(ok.ABI_FUNCTIONS) == names
     lib = ctypes.CDLL(ok.library_path)
     for name in names:
@@ -130,6 +130,7 @@ def test_null_and_shape_errors_before_any_launch():
     assert lib.ojbkq_set_knobs(None, 0.01, 1) == -1
     ptr = ctypes.c_void_p()
     assert lib.ojbkq_inspect(None, 0, ctypes.byref(ptr)) == -1
+    assert lib.ojbkq_path_codes(None, 1) == -1
     assert lib.ojbkq_destroy(None) == 0
     assert lib.ojbkq_set_timing(None, 1) == -1
     ms = (ctypes.c_double * 6)()

@@ -16,7 +16,7 @@ import torch
 import paper_2602_08376_amd as ok
 from oracle import infer as oi
 from oracle import ojbkq as orc
-from parity import SCALE_RTOL, check_residuals, np64
+from parity import SCALE_RTOL, check_layer_strict, np64
 from synth import LayerConfig, make_layer
 
 pytestmark = pytest.mark.gpu
@@ -54,7 +54,26 @@ def check_perm(perm, G_o):
     return len(bad)
 
 
-def check_against_oracle(cfg, g, W, Xr, Xq, mu, G_o=None, static=False):
+def paths_of(s):
+    return np64(s.path_codes()), np64(s.inspect("path_resid"))
+
+
+def staged(cfg, W, Xr, Xq, mu, mode, one_shot):
+    """The solve of a one-shot act-order call through the staged calls (W
+    bound, one chunk): bit-equal results, and every candidate's codes."""
+    s = ok.LayerSolver(cfg.m, cfg.n, cfg.bits, cfg.group, cfg.K, cfg.klein_seed, cfg.lambda_rel,
+                       device=DEV, act_order=mode)
+    s.set_weights(W)
+    s.accumulate(None if mu == 1.0 else Xr, Xq)
+    g = s.solve(W, mu)
+    paths = paths_of(s)
+    s.close()
+    for f in ("codes", "scales", "zeros", "residuals", "winner", "perm"):
+        assert torch.equal(getattr(g, f), getattr(one_shot, f)), f
+    return paths
+
+
+def check_against_oracle(cfg, g, W, Xr, Xq, mu, paths, G_o=None, static=False):
     perm = np64(g.perm).astype(np.int64)
     Xq_np = np64(Xq)
     G_o = orc.gram(Xq_np) if G_o is None else G_o
@@ -68,13 +87,12 @@ def check_against_oracle(cfg, g, W, Xr, Xq, mu, G_o=None, static=False):
     assert np.all(np.abs(S - o.scales) <= SCALE_RTOL * np.abs(o.scales))
     codes = np64(g.codes)
     assert codes.max() <= (1 << cfg.bits) - 1
-    frac = float((codes == o.codes).mean())
-    worst, nwin = check_residuals(np64(g.residuals), np64(g.winner), o.residuals, o.winner)
-    print(f"[act order{' static' if static else ''} {cfg.key} b{cfg.bits} g{cfg.group} K{cfg.K} "
-          f"mu={mu}] order moved at {moved} "
-          f"positions, code agreement {frac:.6f}, winner mismatches {nwin}, worst residual rel "
-          f"err {worst:.2e}", flush=True)
-    assert frac >= 0.999
+    grp = perm // orc.group_size(cfg.m, cfg.group) if static else cfg.group
+    tag = (f"act order{' static' if static else ''} {cfg.key} b{cfg.bits} g{cfg.group} K{cfg.K} "
+           f"mu={mu}, order moved at {moved} positions")
+    st = check_layer_strict(o, g, paths[0], paths[1], cfg.bits, cfg.klein_seed, grp, perm=perm,
+                            tag=tag)
+    assert st["agreement"] >= 0.999
     return o
 
 
@@ -91,8 +109,8 @@ def test_act_order_layer_matches_oracle(m, n, T, bits, group, K, seed, mu):
     W, Xr, Xq = make_layer(cfg, device=DEV)
     g = ok.quantize_layer(W, Xr, Xq, mu, bits, group, K, cfg.klein_seed, cfg.lambda_rel,
                           act_order=True)
-    torch.cuda.synchronize()
-    check_against_oracle(cfg, g, W, Xr, Xq, mu)
+    paths = staged(cfg, W, Xr, Xq, mu, True, g)
+    check_against_oracle(cfg, g, W, Xr, Xq, mu, paths)
 
 
 def test_act_order_heavy_tailed_m1024():
@@ -101,8 +119,8 @@ def test_act_order_heavy_tailed_m1024():
     W, Xr, Xq = make_layer(cfg, device=DEV)
     g = ok.quantize_layer(W, Xr, Xq, 0.5, 4, 128, 16, cfg.klein_seed, cfg.lambda_rel,
                           act_order=True)
-    torch.cuda.synchronize()
-    o = check_against_oracle(cfg, g, W, Xr, Xq, 0.5)
+    paths = staged(cfg, W, Xr, Xq, 0.5, True, g)
+    o = check_against_oracle(cfg, g, W, Xr, Xq, 0.5, paths)
     plain = orc.quantize_layer(np64(W), np64(Xr), np64(Xq), 0.5, 4, 128, 16, cfg.klein_seed,
                                lambda_rel=cfg.lambda_rel)
     print(f"[act order m1024] mean residual {o.residuals.mean():.4e} vs plain order "
@@ -128,7 +146,7 @@ def test_act_order_staged_sweep_and_chunks():
         torch.cuda.synchronize()
         assert torch.equal(s.inspect("perm"), g.perm)
         perms.append(np64(g.perm))
-        check_against_oracle(cfg, g, W, xr, Xq, mu, G_o=G_o)
+        check_against_oracle(cfg, g, W, xr, Xq, mu, paths_of(s), G_o=G_o)
     assert np.array_equal(perms[0], perms[1])
     s.close()
     plain = ok.LayerSolver(cfg.m, cfg.n, cfg.bits, cfg.group, cfg.K, cfg.klein_seed, device=DEV)
@@ -189,9 +207,9 @@ def test_static_groups_layer_matches_oracle(m, n, T, bits, group, K, seed, mu):
     g = ok.quantize_layer(W, Xr, Xq, mu, bits, group, K, cfg.klein_seed, cfg.lambda_rel,
                           act_order="static")
     plain = ok.quantize_layer(W, Xr, Xq, mu, bits, group, K, cfg.klein_seed, cfg.lambda_rel)
-    torch.cuda.synchronize()
+    paths = staged(cfg, W, Xr, Xq, mu, "static", g)
     assert torch.equal(g.scales, plain.scales) and torch.equal(g.zeros, plain.zeros)
-    check_against_oracle(cfg, g, W, Xr, Xq, mu, static=True)
+    check_against_oracle(cfg, g, W, Xr, Xq, mu, paths, static=True)
 
 
 def test_static_groups_staged_and_plain_product():
@@ -207,7 +225,7 @@ def test_static_groups_staged_and_plain_product():
     for mu in (0.5, 0.0):
         q = s.solve(W, mu)
         torch.cuda.synchronize()
-        check_against_oracle(cfg, q, W, Xr, Xq, mu, G_o=G_o, static=True)
+        check_against_oracle(cfg, q, W, Xr, Xq, mu, paths_of(s), G_o=G_o, static=True)
     s.close()
     X16 = Xq.half()
     P = ok.pack_codes(q.codes, cfg.bits)
@@ -235,9 +253,9 @@ def test_act_order_ties_and_degenerate_channels(mode):
     W[3, 32:64] = 0.0
     g = ok.quantize_layer(W, Xr, Xq, 0.5, 1, 32, 0, cfg.klein_seed, cfg.lambda_rel,
                           act_order=mode)
-    torch.cuda.synchronize()
+    paths = staged(cfg, W, Xr, Xq, 0.5, mode, g)
     perm = np64(g.perm)
     assert perm[0] == 40                   # the zero diagonal comes first: decided last
     assert abs(int(np.nonzero(perm == 5)[0][0]) - int(np.nonzero(perm == 9)[0][0])) == 1
     assert int(g.winner.max()) == 0
-    check_against_oracle(cfg, g, W, Xr, Xq, 0.5, static=(mode == "static"))
+    check_against_oracle(cfg, g, W, Xr, Xq, 0.5, paths, static=(mode == "static"))

@@ -9,7 +9,7 @@ import torch
 
 import paper_2602_08376_amd as ok
 from oracle import ojbkq as orc
-from parity import check_residuals, np64
+from parity import check_layer_strict, np64
 from synth import LayerConfig, make_layer
 
 pytestmark = pytest.mark.gpu
@@ -56,16 +56,15 @@ def test_knobs_equal_fresh_calls(m, n, act):
     # the oracle on one of the settings
     s.set_knobs(0.1, 3)
     g = s.solve(W, 0.5)
-    torch.cuda.synchronize()
+    pc, pr = np64(s.path_codes()), np64(s.inspect("path_resid"))
+    assert pc.shape == (n, 4, m) and pr.shape == (n, 4)
     perm = None if not act else np64(g.perm).astype(np.int64)
     o = orc.quantize_layer(np64(W), np64(Xr), np64(Xq), 0.5, cfg.bits, cfg.group, 3,
                            cfg.klein_seed, lambda_rel=0.1, perm=perm)
-    assert np.array_equal(np64(g.scales), o.scales)
-    frac = float((np64(g.codes) == o.codes).mean())
-    worst, nwin = check_residuals(np64(g.residuals), np64(g.winner), o.residuals, o.winner)
-    print(f"[knobs m={m} act={act}] lambda 0.1, K 3: code agreement {frac:.6f}, worst residual "
-          f"rel err {worst:.2e}", flush=True)
-    assert frac >= 0.999
+    assert np.array_equal(np64(g.scales), o.scales) and np.array_equal(np64(g.zeros), o.zeros)
+    st = check_layer_strict(o, g, pc, pr, cfg.bits, cfg.klein_seed, cfg.group, perm=perm,
+                            tag=f"knobs m={m} act={act} lambda 0.1 K 3")
+    assert st["agreement"] >= 0.999
     with pytest.raises(ok.OjbkqError) as ei:
         s.set_knobs(0.1, 9)               # more candidates than the context was carved for
     assert ei.value.code == "EINVAL"

@@ -15,7 +15,7 @@ import torch
 
 import paper_2602_08376_amd as ok
 from oracle import ojbkq as orc
-from parity import (SCALE_RTOL, centres_from_gq, check_paths, check_residuals, np64)
+from parity import (SCALE_RTOL, centres_from_gq, check_layer_strict, check_paths, np64)
 from synth import CONFIGS, LayerConfig, make_layer, make_triangular_problem
 
 pytestmark = pytest.mark.gpu
@@ -38,31 +38,58 @@ def small_cfg(m, n, T, bits, group, K, seed, kind="heavy", sparsity=0.0, mu=0.5)
                        sparsity=sparsity)
 
 
+def paths_of(s):
+    """Every candidate of a staged context's last solve: codes [n, K+1, m] in
+    W's order and residuals [n, K+1]."""
+    return np64(s.path_codes()), np64(s.inspect("path_resid"))
+
+
+def staged(cfg, W, Xr, Xq, mu, lam=None, K=None, **kw):
+    """One staged solve with W bound and all tokens in one chunk (the calls
+    the one-shot entry point makes); returns (result, paths, path residuals)."""
+    s = ok.LayerSolver(cfg.m, cfg.n, cfg.bits, cfg.group, cfg.K if K is None else K,
+                       cfg.klein_seed, cfg.lambda_rel if lam is None else lam, device=DEV, **kw)
+    s.set_weights(W)
+    s.accumulate(None if mu == 1.0 else Xr, Xq)   # the one-shot call reads no X_ref at mu = 1
+    g = s.solve(W, mu)
+    pc, pr = paths_of(s)
+    s.close()
+    return g, pc, pr
+
+
+def same_result(a, b):
+    for f in ("codes", "scales", "zeros", "residuals", "winner"):
+        assert torch.equal(getattr(a, f), getattr(b, f)), f
+
+
 def run_pair(cfg, mu=None, lambda_rel=None):
+    """The one-shot call and the same solve through the staged calls (which
+    must agree bit for bit), and the oracle on the same arrays."""
     mu = cfg.mu if mu is None else mu
     lam = cfg.lambda_rel if lambda_rel is None else lambda_rel
     W, Xr, Xq = make_layer(cfg, device=DEV)
     g = ok.quantize_layer(W, Xr, Xq, mu, cfg.bits, cfg.group, cfg.K, cfg.klein_seed, lam)
+    st, pc, pr = staged(cfg, W, Xr, Xq, mu, lam)
     torch.cuda.synchronize()
+    same_result(g, st)
     o = orc.quantize_layer(np64(W), np64(Xr), np64(Xq), mu, cfg.bits, cfg.group, cfg.K,
                            cfg.klein_seed, lambda_rel=lam)
-    return (W, Xr, Xq), g, o
+    return (W, Xr, Xq), g, o, (pc, pr)
 
 
-def check_layer(cfg, g, o, mu):
+def check_layer(cfg, g, o, mu, paths):
+    """Scales and zero points bit-equal, then the full rule on every
+    candidate of every column (tests/parity.py)."""
     S, Z = np64(g.scales), np64(g.zeros)
     assert np.array_equal(S, o.scales), "scales differ"
     assert np.array_equal(Z, o.zeros), "zero points differ"
     assert np.all(np.abs(S - o.scales) <= SCALE_RTOL * np.abs(o.scales))
     codes = np64(g.codes)
     assert codes.max() <= (1 << cfg.bits) - 1
-    win = np64(g.winner)
-    res = np64(g.residuals)
-    frac = float((codes == o.codes).mean())
-    worst, nwin = check_residuals(res, win, o.residuals, o.winner)
-    print(f"[{cfg.key} mu={mu}] code agreement {frac:.6f}, winner mismatches {nwin}, "
-          f"worst residual rel err {worst:.2e}")
-    return frac
+    pc, pr = paths
+    st = check_layer_strict(o, g, pc, pr, cfg.bits, cfg.klein_seed, cfg.group,
+                            tag=f"{cfg.key} mu={mu}")
+    return st["agreement"]
 
 
 # ---------------------------------------------------------------------------
@@ -189,8 +216,8 @@ def test_decode_brute_force_small():
 
 def test_tiny_config_c1():
     cfg = CONFIGS["c1"]
-    _, g, o = run_pair(cfg)
-    frac = check_layer(cfg, g, o, cfg.mu)
+    _, g, o, paths = run_pair(cfg)
+    frac = check_layer(cfg, g, o, cfg.mu, paths)
     assert frac == 1.0
 
 
@@ -205,16 +232,16 @@ def test_tiny_config_c1():
 ])
 def test_layer_matches_oracle(m, n, T, bits, group, K, seed, mu):
     cfg = small_cfg(m, n, T, bits, group, K, seed)
-    _, g, o = run_pair(cfg, mu=mu)
-    frac = check_layer(cfg, g, o, mu)
+    _, g, o, paths = run_pair(cfg, mu=mu)
+    frac = check_layer(cfg, g, o, mu, paths)
     assert frac >= 0.999
 
 
 def test_heavy_tailed_layer_m1024():
     """A slice of the 4096x4096 attention workload: heavy-tailed channels, 1% outliers x50."""
     cfg = small_cfg(1024, 48, 4096, 4, 128, 16, 21)
-    _, g, o = run_pair(cfg)
-    frac = check_layer(cfg, g, o, cfg.mu)
+    _, g, o, paths = run_pair(cfg)
+    frac = check_layer(cfg, g, o, cfg.mu, paths)
     assert frac >= 0.999
 
 
@@ -227,6 +254,7 @@ def test_wide_layer_two_level_factor():
     s.accumulate(Xr, Xq)
     g = s.solve(W, cfg.mu)
     L = np64(s.inspect("L"))
+    paths = paths_of(s)
     s.close()
     o = orc.quantize_layer(np64(W), np64(Xr), np64(Xq), cfg.mu, cfg.bits, cfg.group, cfg.K,
                            cfg.klein_seed)
@@ -234,14 +262,14 @@ def test_wide_layer_two_level_factor():
     errR = float(np.max(np.abs(L.T - o.R) / colnorm[None, :]))
     print(f"[t6200] R err {errR:.2e}")
     assert errR < 1e-9, errR
-    assert check_layer(cfg, g, o, cfg.mu) >= 0.999
+    assert check_layer(cfg, g, o, cfg.mu, paths) >= 0.999
 
 
 def test_sparse_mlp_layer_3bit():
     """Post-SiLU-like activations (60% near-zero), 3-bit box, as the down_proj workload."""
     cfg = small_cfg(640, 40, 2048, 3, 128, 16, 22, sparsity=0.6)
-    _, g, o = run_pair(cfg)
-    frac = check_layer(cfg, g, o, cfg.mu)
+    _, g, o, paths = run_pair(cfg)
+    frac = check_layer(cfg, g, o, cfg.mu, paths)
     assert frac >= 0.999
 
 
@@ -280,7 +308,7 @@ def test_staged_intermediates_and_chunks():
     pr = np64(s.inspect("path_resid"))
     assert np.allclose(pr, o.decode.path_resid, rtol=1e-9)
     print(f"[staged] R err {errR:.2e}, qbar err {errq:.2e}")
-    check_layer(cfg, g, o, 0.5)
+    check_layer(cfg, g, o, 0.5, paths_of(s))
     # the one-shot call on the whole token set gives the same codes
     one = ok.quantize_layer(W, Xr, Xq, 0.5, cfg.bits, cfg.group, cfg.K, cfg.klein_seed)
     assert torch.equal(one.codes, g.codes)
@@ -328,7 +356,7 @@ def test_mixed_chunks_and_bound_weights(m, n, bind):
         errg = np.max(np.abs(gq - gq_o) / (np.abs(Sx * o.qbar) @ np.abs(o.R.T)))
         print(f"[mixed m={m} n={n} bind={bind} mu={mu}] Rbar qbar rel err {errg:.2e}")
         assert errg < 1e-10, errg
-        assert check_layer(cfg, g, o, mu) >= 0.999
+        assert check_layer(cfg, g, o, mu, paths_of(s)) >= 0.999
     if bind:
         with pytest.raises(ok.OjbkqError) as ei:
             s.solve(W.clone(), 0.5)          # another buffer than the bound one
@@ -354,9 +382,11 @@ def test_large_k_and_k_sweep_invariants():
         torch.cuda.synchronize()
         runs[K] = g
         if K >= 25:
+            st, pc, pr = staged(cfg, W, Xr, Xq, 0.6, K=K)
+            same_result(g, st)
             o = orc.quantize_layer(np64(W), np64(Xr), np64(Xq), 0.6, cfg.bits, cfg.group, K,
                                    cfg.klein_seed)
-            assert check_layer(cfg, g, o, 0.6) >= 0.999
+            assert check_layer(cfg, g, o, 0.6, (pc, pr)) >= 0.999
     r0 = np64(runs[0].residuals)
     assert np.array_equal(np64(runs[1].codes), np64(runs[0].codes))
     assert np.allclose(np64(runs[1].residuals), r0, rtol=1e-13, atol=0)
@@ -381,12 +411,13 @@ def test_symmetric_absmax_scales(m, n, bits, group, K, mu):
     o = orc.quantize_layer(np64(W), np64(Xr), np64(Xq), mu, bits, group, K, cfg.klein_seed,
                            scheme="sym")
     assert np.all(np64(g.zeros) == 2 ** (bits - 1))
-    assert check_layer(cfg, g, o, mu) >= 0.999
     s = ok.LayerSolver(m, n, bits, group, K, cfg.klein_seed, device=DEV, scheme="sym")
     s.accumulate(Xr, Xq)
     st = s.solve(W, mu)
+    paths = paths_of(s)
     s.close()
     assert torch.equal(st.codes, g.codes) and torch.equal(st.scales, g.scales)
+    assert check_layer(cfg, g, o, mu, paths) >= 0.999
 
 
 def test_gram_load_paths_agree():
@@ -430,7 +461,7 @@ def test_alpha_sweep_reuses_factor():
         assert torch.equal(one.codes, g.codes)
         o = orc.quantize_layer(np64(W), np64(Xr), np64(Xq), mu, cfg.bits, cfg.group, cfg.K,
                                cfg.klein_seed)
-        check_layer(cfg, g, o, mu)
+        check_layer(cfg, g, o, mu, paths_of(s))
     with pytest.raises(ok.OjbkqError) as ei:
         s.accumulate(Xr, Xq)
     assert ei.value.code == "ESTATE"
@@ -450,10 +481,12 @@ def test_degenerate_groups_and_channels():
     Xr[5] = 0.0
     Xq[5] = 0.0
     g = ok.quantize_layer(W, Xr, Xq, 0.5, cfg.bits, cfg.group, cfg.K, cfg.klein_seed)
+    st, pc, pr = staged(cfg, W, Xr, Xq, 0.5)
     torch.cuda.synchronize()
+    same_result(g, st)
     o = orc.quantize_layer(np64(W), np64(Xr), np64(Xq), 0.5, cfg.bits, cfg.group, cfg.K,
                            cfg.klein_seed)
-    assert check_layer(cfg, g, o, 0.5) >= 0.999
+    assert check_layer(cfg, g, o, 0.5, (pc, pr)) >= 0.999
     # the degenerate group's grid is [-1, 1]: zero point in the middle of the box
     assert float(g.scales[0, 0]) == float(o.scales[0, 0]) == float(np.float32(2.0 / 15.0))
     assert float(g.zeros[0, 0]) == float(o.zeros[0, 0])
