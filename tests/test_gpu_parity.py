@@ -417,7 +417,7 @@ def test_symmetric_absmax_scales(m, n, bits, group, K, mu):
     paths = paths_of(s)
     s.close()
     assert torch.equal(st.codes, g.codes) and torch.equal(st.scales, g.scales)
-    assert check_layer(cfg, g, o, mu, paths) >= 0.999
+    assert check_layer(cfg, st, o, mu, paths) >= 0.999
 
 
 def test_gram_load_paths_agree():
