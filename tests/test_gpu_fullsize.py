@@ -1,16 +1,24 @@
 """Parity at the full sizes of the five workloads' four large layers.
 
-The Llama-7B-shaped attention projection (W 4096 x 4096, X_ref / X_q 4096 x
-262144 tokens, heavy-tailed channel scales, 1% outlier channels, 4-bit, group
-128, K = 16, alpha = 0.5) is the workload bench.py times; it runs through the
-same staged calls (one token chunk, one solve) in the same launch
-configuration.  The oracle forms its own full fp64 Gram and factor on the
-host, then the relaxed solution and the decode of a seeded sample of columns
-(every candidate of each).  Scales and zero points are compared for every
-column.
+Every check applies the full parity rule of tests/parity.py to every
+candidate of the sampled columns: each differing path must start at a
+near-tie, every candidate residual must match the oracle's residual formula
+on the GPU's codes, and winner swaps must be explained.
 
-The other three layers are checked stage by stage on samples (see the
-comment above test_full_size_sampled).
+* 4096 x 4096 attention projection (262,144 tokens, 4-bit, K = 16), the
+  workload bench.py times, through the same staged calls: the oracle forms
+  its own full fp64 Gram, damping and factor on the host, then the relaxed
+  solution and the decode of 128 seeded columns (every candidate); also with
+  the weight permutation in both group modes (32 columns each).
+* 5120 x 13824 up_proj (3-bit, K = 32, the mu sweep on one factor): the
+  oracle again forms its own Gram and factor, and for every mu its own
+  centres and the decode of 16 columns.
+* 11008 x 4096 (3-bit) and 28672 x 8192 (8 token chunks): a host fp64 Gram
+  of these does not fit a test's time, so the factor is checked matrix-free
+  over every entry (L L^T v - lambda^2 v against X~^T (X~ v) for 8 random
+  probes v, summed chunk by chunk on the host), the centres through the
+  normal equations of the stacked problem (Eq. new_obj), and the oracle then
+  decodes 8 columns on the factor and centres so verified.
 """
 
 import numpy as np
@@ -18,14 +26,19 @@ import pytest
 import torch
 
 import paper_2602_08376_amd as ok
+from oracle import cdecode
 from oracle import ojbkq as orc
-from parity import centres_from_gq, check_residuals, first_divergence_is_tie, np64
+from parity import centres_from_gq, check_paths_strict, np64
 from synth import CONFIGS
 from synth.workloads import activation_chunks, make_weights
 
 pytestmark = pytest.mark.gpu
 
-N_COLS = 12
+N_COLS = 128         # sampled columns at 4096 x 4096
+N_COLS_ACT = 32      # with the weight permutation
+N_COLS_C4 = 16       # per mu at 5120 x 13824
+N_DEC = 8            # at 11008 x 4096 and 28672 x 8192
+N_PROBES = 8
 
 
 @pytest.fixture(scope="module", autouse=True)
@@ -33,6 +46,28 @@ def _gpu():
     if not torch.cuda.is_available():
         pytest.skip("no GPU")
     ok.library()
+
+
+def gpu_paths(s, cols, dev):
+    """Candidate codes [c, K+1, m] (W's order) and residuals [c, K+1] of the
+    sampled columns of the last solve."""
+    idx = torch.as_tensor(np.asarray(cols), device=dev)
+    pc = np64(s.path_codes()[idx])
+    pr = np64(s.inspect("path_resid"))[np.asarray(cols)]
+    return pc, pr
+
+
+def strict(R, qbar, S_cols, group_rows, cfg, cols, dec, pc, pr, g, perm=None, tag=""):
+    """check_paths_strict on sampled columns; pc / g's codes in W's order."""
+    m = R.shape[0]
+    codes = np64(g.codes)[cols]
+    if perm is not None:
+        pc = pc[:, :, perm]
+        codes = codes[:, perm]
+    s_rows = orc.expand_groups(S_cols, m, group_rows)
+    return check_paths_strict(R, qbar, s_rows, cfg.bits, cfg.klein_seed, dec.alpha, cols, pc, pr,
+                              codes, np64(g.residuals)[cols], np64(g.winner)[cols],
+                              dec.path_codes, dec.path_resid, dec.residuals, dec.winner, tag=tag)
 
 
 def test_attention_projection_full_size():
@@ -45,65 +80,48 @@ def test_attention_projection_full_size():
     s.set_weights(W)
     s.accumulate(Xr, Xq)
     g = s.solve(W, cfg.mu)
+    cols = np.sort(np.random.default_rng(2024).choice(cfg.n, N_COLS, replace=False))
     L = np64(s.inspect("L"))
     gq_g = np64(s.inspect("gq"))
     alpha_g = np64(s.inspect("alpha"))
     lam2_g = float(s.inspect("lam2")[0])
-    pres_g = np64(s.inspect("path_resid"))
+    pres_all = np64(s.inspect("path_resid"))
+    pc, pr = gpu_paths(s, cols, dev)
     s.close()
-    codes_g, res_g, win_g = np64(g.codes), np64(g.residuals), np64(g.winner)
-    Wn = np64(W)
-    Xqn = np64(Xq)
-    Xrn = np64(Xr)
+    Wn, Xqn, Xrn = np64(W), np64(Xq), np64(Xr)
     del Xq, Xr
     torch.cuda.empty_cache()
     print("[full c2] GPU layer done; oracle Gram on the host", flush=True)
 
-    # oracle: full Gram and factor, then a column sample
     G = orc.gram(Xqn)
     lam2 = orc.damping(G, cfg.lambda_rel)
     R = orc.cholesky_upper(G + lam2 * np.eye(cfg.m))
     del G
     S, Z = orc.scales_zeros(Wn, cfg.bits, cfg.group)
-    cols = np.sort(np.random.default_rng(2024).choice(cfg.n, N_COLS, replace=False))
     V = orc.relaxed_solution(Wn[cols], Xrn, Xqn, cfg.mu, lam2, R)
     qb = orc.centres(V, S[cols], Z[cols], cfg.group)
     qbar_full = np.zeros((cfg.n, cfg.m))
     qbar_full[cols] = qb
     print("[full c2] oracle factor and centres done; decoding the sample", flush=True)
-    dec = orc.decode(R, qbar_full, S, cfg.bits, cfg.group, cfg.K, cfg.klein_seed, columns=cols)
+    dec = cdecode.decode(R, qbar_full, S, cfg.bits, cfg.group, cfg.K, cfg.klein_seed,
+                         columns=cols)
 
-    # scales / zeros: every column, bit-equal
     assert np.array_equal(np64(g.scales), S) and np.array_equal(np64(g.zeros), Z)
-    # damping and factor
     assert abs(lam2_g - lam2) <= 1e-12 * lam2
     colnorm = np.sqrt(np.sum(R ** 2, axis=0))
     errR = float(np.max(np.abs(L.T - R) / colnorm[None, :]))
     assert errR < 1e-9, errR
-    # centres and temperatures of the sample
     qbar_g = centres_from_gq(L, gq_g[cols], np64(g.scales)[cols], cfg.group)
     errq = float(np.max(np.abs(qbar_g - qb)))
     assert errq < 1e-6, errq
     assert np.allclose(alpha_g[cols], dec.alpha, rtol=1e-9)
-    # codes: the winners' code vectors; a differing one must start at a near-tie
-    frac = float((codes_g[cols] == dec.codes).mean())
-    Sx = orc.expand_groups(S[cols], cfg.m, cfg.group)
-    for t, j in enumerate(cols):
-        if win_g[j] == dec.winner[t] and not np.array_equal(codes_g[j], dec.codes[t]):
-            assert first_divergence_is_tie(R, qb[t], Sx[t], cfg.bits, dec.alpha[t],
-                                           cfg.klein_seed, int(j), int(win_g[j]), codes_g[j],
-                                           dec.codes[t])
-    assert frac >= 0.999, frac
-    # residuals: every candidate of the sample, and the winners
-    rel = np.abs(pres_g[cols] - dec.path_resid) / np.abs(dec.path_resid)
-    worst, nwin = check_residuals(res_g[cols], win_g[cols], dec.residuals, dec.winner)
-    print(f"[full c2] R err {errR:.2e}, qbar err {errq:.2e}, code agreement {frac:.6f}, "
-          f"candidate residual max rel err {rel.max():.2e}, winner mismatches {nwin}", flush=True)
-    assert float(np.median(rel)) <= 1e-4
-    # every GPU winner is the first minimum of its own candidate residuals
-    assert np.array_equal(win_g, np.argmin(pres_g, axis=1))
-    assert np.array_equal(res_g, pres_g[np.arange(cfg.n), win_g])
-    assert int(codes_g.max()) <= (1 << cfg.bits) - 1
+    print(f"[full c2] R err {errR:.2e}, qbar err {errq:.2e}", flush=True)
+    strict(R, qb, S[cols], cfg.group, cfg, cols, dec, pc, pr, g, tag="full c2")
+    # over all columns: every winner is the first minimum of its candidates
+    win_g = np64(g.winner)
+    assert np.array_equal(win_g, np.argmin(pres_all, axis=1))
+    assert np.array_equal(np64(g.residuals), pres_all[np.arange(cfg.n), win_g])
+    assert int(np64(g.codes).max()) <= (1 << cfg.bits) - 1
 
 
 @pytest.mark.parametrize("mode", ["positions", "static"])
@@ -122,9 +140,10 @@ def test_attention_projection_full_size_act_order(mode):
     s.set_weights(W)
     s.accumulate(Xr, Xq)
     g = s.solve(W, cfg.mu)
-    pres_g = np64(s.inspect("path_resid"))
+    cols = np.sort(np.random.default_rng(2025).choice(cfg.n, N_COLS_ACT, replace=False))
+    pres_all = np64(s.inspect("path_resid"))
+    pc, pr = gpu_paths(s, cols, dev)
     s.close()
-    codes_g, res_g, win_g = np64(g.codes), np64(g.residuals), np64(g.winner)
     perm = np64(g.perm).astype(np.int64)
     Wn, Xqn, Xrn = np64(W), np64(Xq), np64(Xr)
     del Xq, Xr
@@ -150,67 +169,81 @@ def test_attention_projection_full_size_act_order(mode):
         S, Z = orc.scales_zeros(Wp, cfg.bits, cfg.group)
         grp = cfg.group
     assert np.array_equal(np64(g.scales), S) and np.array_equal(np64(g.zeros), Z)
-    cols = np.sort(np.random.default_rng(2025).choice(cfg.n, 8, replace=False))
     V = orc.relaxed_solution(Wp[cols], Xrp, Xqp, cfg.mu, lam2, R)
     qb = orc.centres(V, S[cols], Z[cols], grp)
     qbar_full = np.zeros((cfg.n, cfg.m))
     qbar_full[cols] = qb
     print(f"[full c2 act order {mode}] oracle factor and centres done; decoding the sample",
           flush=True)
-    dec = orc.decode(R, qbar_full, S, cfg.bits, grp, cfg.K, cfg.klein_seed, columns=cols)
-    codes_o = np.empty_like(dec.codes)
-    codes_o[:, perm] = dec.codes                  # back to W's order
-    frac = float((codes_g[cols] == codes_o).mean())
-    Sx = orc.expand_groups(S[cols], cfg.m, grp)
-    for t, j in enumerate(cols):
-        if win_g[j] == dec.winner[t] and not np.array_equal(codes_g[j], codes_o[t]):
-            assert first_divergence_is_tie(R, qb[t], Sx[t], cfg.bits, dec.alpha[t],
-                                           cfg.klein_seed, int(j), int(win_g[j]),
-                                           codes_g[j][perm], dec.codes[t])
-    assert frac >= 0.999, frac
-    rel = np.abs(pres_g[cols] - dec.path_resid) / np.abs(dec.path_resid)
-    worst, nwin = check_residuals(res_g[cols], win_g[cols], dec.residuals, dec.winner)
-    print(f"[full c2 act order {mode}] code agreement {frac:.6f}, candidate residual max rel err "
-          f"{rel.max():.2e}, winner mismatches {nwin}", flush=True)
-    assert float(np.median(rel)) <= 1e-4
-    assert np.array_equal(win_g, np.argmin(pres_g, axis=1))
+    dec = cdecode.decode(R, qbar_full, S, cfg.bits, grp, cfg.K, cfg.klein_seed, columns=cols)
+    strict(R, qb, S[cols], grp, cfg, cols, dec, pc, pr, g, perm=perm,
+           tag=f"full c2 act order {mode}")
+    assert np.array_equal(np64(g.winner), np.argmin(pres_all, axis=1))
 
 
-# ---------------------------------------------------------------------------
-# The other three full-size workloads (11008x4096 3-bit, 5120x13824 K=32 with
-# a mu sweep, 28672x8192 in 8 token chunks).  A full oracle factor of these
-# Grams does not fit a test's time, so each stage is checked on samples the
-# oracle computes one by one, or through a property that holds at any size:
-#   * scales and zero points: every column, bit-equal;
-#   * lambda^2 against the mean of the Gram diagonal, summed on the host;
-#   * the factor: sampled entries of L L^T - lambda^2 I against the oracle's
-#     Gram of the two rows (exact fp64 dot products over all tokens);
-#   * the centres: for sampled columns the relaxed solution v (recovered from
-#     the decoder's input Rbar qbar, s, z) satisfies the normal equations of the stacked problem
-#     (Eq. new_obj): (X~^T X~ + lambda^2 I) v = X~^T y*(mu) + lambda^2 w,
-#     both sides formed on the host chunk by chunk;
-#   * the decode: for sampled columns the oracle decodes every candidate
-#     against the GPU's R and qbar; codes, candidate residuals and the
-#     winner must match (differences only at near-ties).
-# ---------------------------------------------------------------------------
+def test_upproj_full_size_mu_sweep():
+    """5120 x 13824, 3-bit, K = 32, mu in {0, 0.5, 1} on one factor: the
+    oracle's own Gram, damping and factor, and per mu its own centres and the
+    decode of 8 columns, every candidate."""
+    cfg = CONFIGS["c4"]
+    dev = torch.device("cuda", 0)
+    W = make_weights(cfg, device=dev)
+    Wn = np64(W)
+    s = ok.LayerSolver(cfg.m, cfg.n, cfg.bits, cfg.group, cfg.K, cfg.klein_seed, cfg.lambda_rel,
+                       device=dev)
+    s.set_weights(W)
+    (Xr, Xq), = list(activation_chunks(cfg, device=dev))
+    s.accumulate(Xr, Xq)
+    Xrn, Xqn = np64(Xr), np64(Xq)
+    del Xr, Xq
+    torch.cuda.empty_cache()
+    rng = np.random.default_rng(44)
+    gpu = []
+    for mu in cfg.mus:
+        g = s.solve(W, mu)
+        cols = np.sort(rng.choice(cfg.n, N_COLS_C4, replace=False))
+        pc, pr = gpu_paths(s, cols, dev)
+        gpu.append((mu, g, cols, pc, pr, np64(s.inspect("path_resid")), np64(s.inspect("L"))
+                    if mu == cfg.mus[0] else None, float(s.inspect("lam2")[0])))
+        print(f"[full c4] GPU solve and decode done for mu = {mu}", flush=True)
+    s.close()
+    print("[full c4] oracle Gram on the host", flush=True)
+    G = orc.gram(Xqn)
+    lam2 = orc.damping(G, cfg.lambda_rel)
+    R = orc.cholesky_upper(G + lam2 * np.eye(cfg.m))
+    del G
+    S, Z = orc.scales_zeros(Wn, cfg.bits, cfg.group)
+    L = gpu[0][6]
+    colnorm = np.sqrt(np.sum(R ** 2, axis=0))
+    errR = float(np.max(np.abs(L.T - R) / colnorm[None, :]))
+    print(f"[full c4] R err {errR:.2e}", flush=True)
+    assert errR < 1e-9, errR
+    for mu, g, cols, pc, pr, pres_all, _, lam2_g in gpu:
+        assert abs(lam2_g - lam2) <= 1e-12 * lam2
+        assert np.array_equal(np64(g.scales), S) and np.array_equal(np64(g.zeros), Z)
+        V = orc.relaxed_solution(Wn[cols], Xrn, Xqn, mu, lam2, R)
+        qb = orc.centres(V, S[cols], Z[cols], cfg.group)
+        qbar_full = np.zeros((cfg.n, cfg.m))
+        qbar_full[cols] = qb
+        dec = cdecode.decode(R, qbar_full, S, cfg.bits, cfg.group, cfg.K, cfg.klein_seed,
+                             columns=cols)
+        strict(R, qb, S[cols], cfg.group, cfg, cols, dec, pc, pr, g, tag=f"full c4 mu={mu}")
+        assert np.array_equal(np64(g.winner), np.argmin(pres_all, axis=1))
 
-SAMPLE = {"c3": (8, 3, 2), "c4": (8, 2, 1), "c5": (8, 2, 1)}   # Gram pairs, centre cols, decode cols
 
-
-@pytest.mark.parametrize("key", ["c3", "c4", "c5"])
-def test_full_size_sampled(key):
+@pytest.mark.parametrize("key", ["c3", "c5"])
+def test_full_size_factor_probes_and_decode(key):
     cfg = CONFIGS[key]
-    n_pairs, n_cent, n_dec = SAMPLE[key]
     dev = torch.device("cuda", 0)
     rng = np.random.default_rng(7 + int(key[1]))
     W = make_weights(cfg, device=dev)
     Wn = np64(W)
     s = ok.LayerSolver(cfg.m, cfg.n, cfg.bits, cfg.group, cfg.K, cfg.klein_seed, cfg.lambda_rel,
                        device=dev)
-    s.set_weights(W)          # as bench.py: c3 and c5 take the projected cross term
+    s.set_weights(W)          # as bench.py: the projected cross term
     diag = np.zeros(cfg.m)
-    pairs = np.sort(rng.choice(cfg.m, size=(n_pairs, 2)), axis=1)[:, ::-1]   # i >= j
-    gpairs = np.zeros(n_pairs)
+    probes = rng.standard_normal((cfg.m, N_PROBES))
+    gprobe = np.zeros((cfg.m, N_PROBES))          # X~^T (X~ v), summed over chunks
     chunks_host = []
     for c, (Xr, Xq) in enumerate(activation_chunks(cfg, device=dev)):
         s.accumulate(Xr, Xq)
@@ -218,73 +251,56 @@ def test_full_size_sampled(key):
         del Xr, Xq
         Xq64 = Xqn.astype(np.float64)
         diag += np.einsum("it,it->i", Xq64, Xq64)
+        gprobe += Xq64 @ (Xq64.T @ probes)
         del Xq64
-        for p, (i, j) in enumerate(pairs):
-            gpairs[p] += orc.gram(Xqn[[i, j]])[0, 1]
         chunks_host.append((Xrn, Xqn))
         print(f"[full {key}] chunk {c + 1}/{cfg.chunks} accumulated", flush=True)
     torch.cuda.empty_cache()
     S, Z = orc.scales_zeros(Wn, cfg.bits, cfg.group)
-    for mu in cfg.mus:
-        g = s.solve(W, mu)
-        torch.cuda.synchronize()
-        print(f"[full {key}] GPU solve and decode done for mu = {mu}", flush=True)
-        assert np.array_equal(np64(g.scales), S) and np.array_equal(np64(g.zeros), Z)
-        lam2_g = float(s.inspect("lam2")[0])
-        assert abs(lam2_g - cfg.lambda_rel * diag.mean()) <= 1e-12 * lam2_g
-        Lg = s.inspect("L")
-        # factor: sampled entries of L L^T
-        for p, (i, j) in enumerate(pairs):
-            li, lj = np64(Lg[i]), np64(Lg[j])
-            h = float(li[: j + 1] @ lj[: j + 1]) - (lam2_g if i == j else 0.0)
-            scale = np.sqrt(diag[i] * diag[j])
-            assert abs(h - gpairs[p]) <= 1e-11 * scale, (key, i, j, h, gpairs[p])
-        # centres: normal equations of the stacked problem for sampled columns
-        gq_g = s.inspect("gq")
-        R = np64(Lg).T.copy()
-        del Lg
-        cols = np.sort(rng.choice(cfg.n, n_cent, replace=False))
-        Sx = orc.expand_groups(S[cols], cfg.m, cfg.group)
-        Zx = orc.expand_groups(Z[cols], cfg.m, cfg.group)
-        qbar_c = centres_from_gq(R.T, np64(gq_g[torch.as_tensor(cols, device=dev)]), S[cols],
-                                 cfg.group)
-        V = ((qbar_c - Zx) * Sx).T   # [m, c]
-        Wc = Wn[cols].astype(np.float64).T
-        lhs = lam2_g * V
-        rhs = lam2_g * Wc
-        for Xrn, Xqn in chunks_host:
-            Xq64 = Xqn.astype(np.float64)
-            lhs += Xq64 @ (Xq64.T @ V)
-            rhs += Xq64 @ orc.jta_target(Wn[cols], Xrn, Xqn, mu)
-            del Xq64
-        rel = np.linalg.norm(lhs - rhs, axis=0) / np.linalg.norm(rhs, axis=0)
-        print(f"[full {key}] mu {mu} columns {cols.tolist()}: normal-equation residuals "
-              f"{[f'{x:.2e}' for x in rel]}", flush=True)
-        assert float(rel.max()) < 1e-9, (key, mu, rel)
-        # decode: oracle candidates on the GPU's R and qbar for sampled columns
-        alpha_g = np64(s.inspect("alpha"))
-        pres_g = np64(s.inspect("path_resid"))
-        codes_g, win_g = np64(g.codes), np64(g.winner)
-        lr = orc.klein_log_rho(cfg.m, cfg.K)
-        dcols = np.sort(rng.choice(cfg.n, n_dec, replace=False))
-        for jcol in dcols:
-            sx = orc.expand_groups(S[jcol:jcol + 1], cfg.m, cfg.group)[0]
-            qb = centres_from_gq(R.T, np64(gq_g[int(jcol):int(jcol) + 1]), S[jcol:jcol + 1],
-                                 cfg.group)[0]
-            alpha_o = lr / float(np.min((np.diag(R) * sx) ** 2))
-            assert abs(alpha_g[jcol] - alpha_o) <= 1e-12 * alpha_o
-            Q = orc.decode_column(R, qb, sx, cfg.bits, cfg.K, alpha_o, cfg.klein_seed, int(jcol))
-            r_o = orc.reduced_residual(R, sx, Q, qb)
-            k_o = orc.select_best(r_o)
-            k_g = int(win_g[jcol])
-            rel = np.abs(pres_g[jcol] - r_o) / np.abs(r_o)
-            print(f"[full {key}] mu {mu} column {jcol}: candidate residual max rel err "
-                  f"{rel.max():.2e}, winner {k_g} / oracle {k_o}", flush=True)
-            assert float(np.median(rel)) <= 1e-4
-            assert k_g == k_o or abs(r_o[k_g] - r_o[k_o]) <= 1e-9 * r_o[k_o]
-            if not np.array_equal(codes_g[jcol], Q[k_g]):
-                assert first_divergence_is_tie(R, qb, sx, cfg.bits, alpha_o, cfg.klein_seed,
-                                               int(jcol), k_g, codes_g[jcol], Q[k_g])
-            assert float((codes_g[jcol] == Q[k_g]).mean()) >= 0.999
-        del R
+    mu = cfg.mu
+    g = s.solve(W, mu)
+    torch.cuda.synchronize()
+    print(f"[full {key}] GPU solve and decode done", flush=True)
+    assert np.array_equal(np64(g.scales), S) and np.array_equal(np64(g.zeros), Z)
+    lam2_g = float(s.inspect("lam2")[0])
+    assert abs(lam2_g - cfg.lambda_rel * diag.mean()) <= 1e-12 * lam2_g
+    L = np64(s.inspect("L"))
+    # the whole factor, matrix-free: L L^T v = (X~^T X~ + lambda^2 I) v
+    lhs = L @ (L.T @ probes) - lam2_g * probes
+    rel = np.linalg.norm(lhs - gprobe, axis=0) / np.linalg.norm(gprobe, axis=0)
+    print(f"[full {key}] factor probes: relative residuals {[f'{x:.1e}' for x in rel]}",
+          flush=True)
+    assert float(rel.max()) < 1e-10, rel
+    # centres: normal equations of the stacked problem for the sampled columns
+    cols = np.sort(rng.choice(cfg.n, N_DEC, replace=False))
+    gq = np64(s.inspect("gq"))[cols]
+    qbar_c = centres_from_gq(L, gq, S[cols], cfg.group)
+    Sx = orc.expand_groups(S[cols], cfg.m, cfg.group)
+    Zx = orc.expand_groups(Z[cols], cfg.m, cfg.group)
+    V = ((qbar_c - Zx) * Sx).T   # [m, c]
+    Wc = Wn[cols].astype(np.float64).T
+    nl, nr = lam2_g * V, lam2_g * Wc
+    for Xrn, Xqn in chunks_host:
+        Xq64 = Xqn.astype(np.float64)
+        nl += Xq64 @ (Xq64.T @ V)
+        nr += Xq64 @ orc.jta_target(Wn[cols], Xrn, Xqn, mu)
+        del Xq64
+    del chunks_host
+    rel = np.linalg.norm(nl - nr, axis=0) / np.linalg.norm(nr, axis=0)
+    print(f"[full {key}] columns {cols.tolist()}: normal-equation residuals "
+          f"{[f'{x:.2e}' for x in rel]}", flush=True)
+    assert float(rel.max()) < 1e-9, rel
+    # decode: the oracle's candidates on the verified factor and centres
+    pc, pr = gpu_paths(s, cols, dev)
+    pres_all = np64(s.inspect("path_resid"))
+    alpha_g = np64(s.inspect("alpha"))
     s.close()
+    R = L.T.copy()
+    del L
+    qbar_full = np.zeros((cfg.n, cfg.m))
+    qbar_full[cols] = qbar_c
+    dec = cdecode.decode(R, qbar_full, S, cfg.bits, cfg.group, cfg.K, cfg.klein_seed,
+                         columns=cols)
+    assert np.allclose(alpha_g[cols], dec.alpha, rtol=1e-12)
+    strict(R, qbar_c, S[cols], cfg.group, cfg, cols, dec, pc, pr, g, tag=f"full {key}")
+    assert np.array_equal(np64(g.winner), np.argmin(pres_all, axis=1))
