@@ -142,6 +142,28 @@ int ojbkq_quantize_layer(const ojbkq_params* p, const float* W, const float* X_r
                          size_t workspace_bytes, void* stream, uint8_t* codes, float* scales,
                          float* zeros, double* residuals, int32_t* winner, int32_t* perm);
 
+/* Bytes of the static device scratch behind ojbkq_quantize_layer_noalloc. */
+#define OJBKQ_NOALLOC_SCRATCH_BYTES (256u * 1024u * 1024u)
+
+/* ojbkq_quantize_layer without a workspace argument, for callers that cannot
+ * allocate device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid hipMalloc).  The workspace is a static device array
+ * of OJBKQ_NOALLOC_SCRATCH_BYTES (256 MiB) inside the library, one per GPU,
+ * held from the first call on that GPU until the process ends; the call
+ * itself allocates no device memory (no hipMalloc, no library allocator).
+ *   Arguments, outputs, errors and results as ojbkq_quantize_layer with
+ *   workspace = that array; the layer must fit it:
+ *   ojbkq_workspace_bytes(p) <= OJBKQ_NOALLOC_SCRATCH_BYTES (about a
+ *   1024 x 1024 layer with K = 16), else OJBKQ_EINVAL before anything is
+ *   enqueued.
+ *   Every call on one GPU shares that GPU's array and leaves its contents
+ *   behind; the path overwrites everything it reads.  Calls that overlap on
+ *   one GPU (other host threads, other streams) race and must not be made. */
+int ojbkq_quantize_layer_noalloc(const ojbkq_params* p, const float* W, const float* X_ref,
+                                 const float* X_q, int64_t T, int64_t ldx, void* stream,
+                                 uint8_t* codes, float* scales, float* zeros, double* residuals,
+                                 int32_t* winner, int32_t* perm);
+
 /* Staged form of the same path, for calibration sets streamed in token chunks
  * (the Gram and cross term are sums over tokens, Alg. 1 step 2-3) and for
  * several JTA knobs on one Gram (R does not depend on mu).

@@ -33,7 +33,10 @@ ABI_FUNCTIONS = (
     "ojbkq_decode_stage", "ojbkq_klein_log_rho", "ojbkq_last_error", "ojbkq_set_timing",
     "ojbkq_stage_times", "ojbkq_set_weights", "ojbkq_packed_words", "ojbkq_pack_codes",
     "ojbkq_dequant_matmul", "ojbkq_set_knobs", "ojbkq_path_codes",
+    "ojbkq_quantize_layer_noalloc",
 )
+
+NOALLOC_SCRATCH_BYTES = 256 * 1024 * 1024   # OJBKQ_NOALLOC_SCRATCH_BYTES
 
 STAGES = ("gram", "factor", "solve", "centres", "decode", "select")
 
@@ -76,6 +79,8 @@ def library() -> ctypes.CDLL:
         "ojbkq_decode_workspace_bytes": (ctypes.c_size_t, [P]),
         "ojbkq_quantize_layer": (ctypes.c_int, [P, vp, vp, vp, i64, i64, vp, ctypes.c_size_t, vp,
                                                 vp, vp, vp, vp, vp, vp]),
+        "ojbkq_quantize_layer_noalloc": (ctypes.c_int, [P, vp, vp, vp, i64, i64, vp, vp, vp,
+                                                        vp, vp, vp, vp]),
         "ojbkq_create": (ctypes.c_int, [P, vp, ctypes.c_size_t, vp, ctypes.POINTER(vp)]),
         "ojbkq_set_weights": (ctypes.c_int, [vp, vp]),
         "ojbkq_set_knobs": (ctypes.c_int, [vp, dp, ctypes.c_int32]),
@@ -252,6 +257,33 @@ def quantize_layer(W, X_ref, X_q, alpha, bits, group, K, seed, lambda_rel=0.01,
                                   _ptr(ws), ws.numel(), _stream(dev), _ptr(out.codes),
                                   _ptr(out.scales), _ptr(out.zeros), _ptr(out.residuals),
                                   _ptr(out.winner), _ptr(out.perm))
+    _check(rc)
+    return out
+
+
+def quantize_layer_noalloc(W, X_ref, X_q, alpha, bits, group, K, seed, lambda_rel=0.01,
+                           scheme="asym", act_order=False,
+                           out: Optional[QuantResult] = None) -> QuantResult:
+    """``ojbkq_quantize_layer_noalloc``: the one-shot call on the library's
+    static scratch (no workspace).  ``out`` may pass preallocated outputs
+    (then nothing at all is allocated on the device for the call)."""
+    n, m = W.shape
+    dev = W.device
+    _need(W, "W", torch.float32, device=dev)
+    if not W.is_contiguous():
+        raise ValueError("W must be contiguous")
+    _need(X_q, "X_q", torch.float32, device=dev)
+    T, ld = _rows_view(X_q, "X_q", m)
+    if X_ref is not None and X_ref is not X_q:
+        _need(X_ref, "X_ref", torch.float32, device=dev)
+        if tuple(X_ref.shape) != tuple(X_q.shape) or X_ref.stride() != X_q.stride():
+            raise ValueError("X_ref must have the shape and strides of X_q")
+    p = _params(m, n, bits, group, K, alpha, lambda_rel, seed, scheme, act_order)
+    if out is None:
+        out = _outputs(n, m, num_groups(m, group), dev, act_order)
+    rc = library().ojbkq_quantize_layer_noalloc(
+        ctypes.byref(p), _ptr(W), _ptr(X_ref), _ptr(X_q), T, ld, _stream(dev), _ptr(out.codes),
+        _ptr(out.scales), _ptr(out.zeros), _ptr(out.residuals), _ptr(out.winner), _ptr(out.perm))
     _check(rc)
     return out
 

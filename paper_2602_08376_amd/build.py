@@ -21,7 +21,7 @@ BUILD_DIR = os.path.join(ROOT, "_build")
 LIB = os.path.join(PKG, "libojbkq.so")
 
 SOURCES = ["api.cpp", "gemm.hip", "gram.hip", "factor.hip", "quant.hip", "decode.hip",
-           "infer.hip", "permute.hip"]
+           "infer.hip", "permute.hip", "noalloc.hip"]
 
 HIPCC_FLAGS = [
     "-O3", "-std=c++17", "-fPIC", "--offload-arch=gfx950",

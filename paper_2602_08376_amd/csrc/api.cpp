@@ -644,6 +644,24 @@ int ojbkq_quantize_layer(const ojbkq_params* p, const float* W, const float* X_r
   return ctx_solve(&c, W, p->alpha, codes, scales, zeros, residuals, winner, perm);
 }
 
+int ojbkq_quantize_layer_noalloc(const ojbkq_params* p, const float* W, const float* X_ref,
+                                 const float* X_q, int64_t T, int64_t ldx, void* stream,
+                                 uint8_t* codes, float* scales, float* zeros, double* residuals,
+                                 int32_t* winner, int32_t* perm) {
+  g_error.clear();
+  int rc = check_params(p);
+  if (rc) return rc;
+  const size_t need = layout_full(shape_of(*p)).total;
+  if (need > (size_t)OJBKQ_NOALLOC_SCRATCH_BYTES)
+    return fail(OJBKQ_EINVAL, "this layer needs " + std::to_string(need) +
+                                  " bytes of workspace; the static scratch holds " +
+                                  std::to_string((size_t)OJBKQ_NOALLOC_SCRATCH_BYTES));
+  void* ws = nullptr;
+  OJBKQ_HIP(ojbkq::noalloc_scratch(&ws), "static scratch address");
+  return ojbkq_quantize_layer(p, W, X_ref, X_q, T, ldx, ws, (size_t)OJBKQ_NOALLOC_SCRATCH_BYTES,
+                              stream, codes, scales, zeros, residuals, winner, perm);
+}
+
 int ojbkq_create(const ojbkq_params* p, void* workspace, size_t workspace_bytes, void* stream,
                  ojbkq_ctx** out) {
   g_error.clear();

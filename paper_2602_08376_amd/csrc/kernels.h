@@ -269,4 +269,9 @@ hipError_t launch_gather(const double* in, int64_t ldi, const int32_t* rmap, con
 hipError_t launch_gather(const float* in, int64_t ldi, const int32_t* rmap, const int32_t* cmap,
                          int64_t rows, int64_t cols, float* out, int64_t ldo, hipStream_t stream);
 
+// ---- static scratch (noalloc.hip) --------------------------------------------
+// Device address of the current device's copy of the library's static
+// scratch array (OJBKQ_NOALLOC_SCRATCH_BYTES), looked up once per device.
+hipError_t noalloc_scratch(void** out);
+
 }  // namespace ojbkq
