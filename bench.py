@@ -35,7 +35,9 @@ if ROOT not in sys.path:
 
 METRIC = "layer quantize time (s) and columns×samples decoded/sec; % MFMA/HBM peak"
 PEAK_F64_MFMA_TFLOPS = 78.6     # MI355X dense fp64 matrix peak
+PEAK_I8_MFMA_TOPS = 5000.0      # MI355X dense int8 matrix peak (5.0 POP/s)
 PEAK_HBM_GBS = 8000.0
+I8_DIGIT_PRODUCTS = 13          # int8 digit products per entry and token (gram_i8.hip)
 
 
 def act_order_arg(args):
@@ -81,6 +83,8 @@ def parse():
                     help="weight permutation: decide the features with the largest Hessian "
                          "diagonal first (every mode); scale groups by decode position "
                          "(default) or kept as W's own groups (static)")
+    ap.add_argument("--gram", default="int8", choices=("int8", "fp64"),
+                    help="arithmetic of the token sums: int8 digit products (default) or fp64")
     ap.add_argument("--scheme", default="asym", choices=("asym", "sym"),
                     help="scales and zero points: asymmetric min-max or symmetric Absmax")
     ap.add_argument("--mlp-stack", action="store_true",
@@ -158,7 +162,13 @@ def sweep_k(args):
         torch.cuda.empty_cache()
 
 
-KERNEL_SOURCES = ("paper_2602_08376_amd/csrc/gram.hip", "paper_2602_08376_amd/csrc/device.h")
+# the sources that decide each measured kernel's traffic (its file, the shared
+# device helpers and the launch constants in kernels.h)
+KERNEL_SOURCES = {
+    "gram_cross_kernel": ("paper_2602_08376_amd/csrc/gram.hip", "paper_2602_08376_amd/csrc/device.h",
+                          "paper_2602_08376_amd/csrc/kernels.h"),
+    "gram_i8": ("paper_2602_08376_amd/csrc/gram_i8.hip", "paper_2602_08376_amd/csrc/kernels.h"),
+}
 
 
 def measured_traffic(kernel, workload):
@@ -170,7 +180,7 @@ def measured_traffic(kernel, workload):
     import glob
     import hashlib
     h = hashlib.sha256()
-    for rel in KERNEL_SOURCES:
+    for rel in KERNEL_SOURCES[kernel]:
         with open(os.path.join(ROOT, rel), "rb") as f:
             h.update(f.read())
     digest = h.hexdigest()[:16]
@@ -523,7 +533,7 @@ def main():
         f"({sum(x.numel() * 8 for x, _ in chunks) / 2**30:.1f} GiB of activations)")
 
     need = ok.workspace_bytes(cfg.m, cfg.n, cfg.bits, cfg.group, cfg.K, cfg.mu, cfg.lambda_rel,
-                              cfg.klein_seed, act_order=act_order_arg(args))
+                              cfg.klein_seed, act_order=act_order_arg(args), gram=args.gram)
     ws = torch.empty(need, dtype=torch.uint8, device=dev)
     stream = torch.cuda.current_stream(dev)
     log(f"workspace {need / 2**30:.2f} GiB")
@@ -531,7 +541,7 @@ def main():
     def step(record):
         s = ok.LayerSolver(cfg.m, cfg.n, cfg.bits, cfg.group, cfg.K, cfg.klein_seed,
                            cfg.lambda_rel, device=dev, workspace=ws, scheme=args.scheme,
-                           act_order=act_order_arg(args))
+                           act_order=act_order_arg(args), gram=args.gram)
         s.set_timing(True)                        # per-stage HIP events inside the library
         s.set_weights(W)                          # lets thin layers skip the m x m cross term
         ev = [torch.cuda.Event(enable_timing=True) for _ in range(2 * len(chunks) + 1)]
@@ -570,12 +580,19 @@ def main():
     gc_avg = sum(gc_ms) / len(gc_ms)
     m, T = cfg.m, cfg.T
     Tc = T // cfg.chunks
-    projected = ok.projects_cross_term(m, cfg.n)
-    # per accumulate call: the Gram's lower half m^2 Tc, plus the cross term:
-    # the mixed product 2 m^2 Tc, or (thin layers, weights bound) W (X - X~)
-    # and its product with X~^T, 4 n m Tc
+    i8 = args.gram == "int8"
+    projected = ok.projects_cross_term(m, cfg.n, gram=args.gram)
+    # per accumulate call, the method's work: the Gram's lower half m^2 Tc,
+    # plus the cross term X~^T (X - X~), 2 m^2 Tc, or (thin layers, weights
+    # bound) W (X - X~) and its product with X~^T, 4 n m Tc
     flops = m * m * Tc + (4.0 * cfg.n * m * Tc if projected else 2.0 * m * m * Tc)
     achieved = flops / (gc_avg * 1e-3) / 1e12
+    # the int8 digit products that carry it: 13 per entry and token, over the
+    # Gram's lower triangle m (m + 1) / 2 and (unless projected) the m^2
+    # cross-term entries, 2 operations per multiply-add
+    i8_ops = (2.0 * I8_DIGIT_PRODUCTS * Tc *
+              (m * (m + 1) / 2 + (0.0 if projected else float(m) * m)))
+    i8_achieved = i8_ops / (gc_avg * 1e-3) / 1e12
     paths = cfg.n * (cfg.K + 1) * len(cfg.mus)
     dec_flops = float(m) * m * paths     # m^2 per candidate path (the strict triangle, 2 FLOP/MAC)
     out = recs[-1][1]
@@ -591,14 +608,30 @@ def main():
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "f64",
+        "dtype": "i8/f64" if i8 else "f64",
         "data": "synthetic (seeded, generated on the GPU; inputs resident in HBM)",
         "config": {**workload_desc(cfg), **({"scheme": "sym"} if args.scheme == "sym" else {}),
                    **({"act_order": args.act_order} if args.act_order else {})},
         "stages_ms": {"gram_cross_per_launch": gc_avg,
                       "rest_of_path": sum(solve_ms) / len(solve_ms),
                       **{f"library_{k}": v for k, v in stage_ms.items()}},
-        "roofline": {
+        "roofline": ({
+            "bound": "mfma",
+            "kernel": ("gram_i8 (row exponents, split, int8 digit contraction, fix-up; "
+                       "one accumulate call)" + (" + fp64 projection GEMMs" if projected else "")),
+            "achieved": i8_achieved,
+            "peak": PEAK_I8_MFMA_TOPS,
+            "unit": "TOP/s",
+            "frac": i8_achieved / PEAK_I8_MFMA_TOPS,
+            "traffic": None if projected else measured_traffic("gram_i8", cfg.key),
+            "algorithmic_ops_per_launch": i8_ops,
+            "method_flops_per_launch": flops,
+            "fp64_equivalent_tflops": achieved,
+            # activations read twice (exponents, split), the digits written and
+            # read once; G and E written
+            "algorithmic_bytes_per_launch": 16.0 * m * Tc + 16.0 * m * Tc + (
+                8.0 * m * m + 20.0 * cfg.n * m if projected else 16.0 * m * m),
+        } if i8 else {
             "bound": "mfma",
             "kernel": ("gram_cross_kernel + projection GEMMs (accumulate call)" if projected
                        else "gram_cross_kernel"),
@@ -611,7 +644,7 @@ def main():
             # activations read once; G (and E) written, or W read and U updated
             "algorithmic_bytes_per_launch": 8.0 * m * Tc + (
                 8.0 * m * m + 20.0 * cfg.n * m if projected else 16.0 * m * m),
-        },
+        }),
         "decode_roofline": {
             "bound": "mfma",
             "kernel": "decode_kernel",

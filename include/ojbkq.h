@@ -121,6 +121,17 @@ typedef struct {
                           Gram (m^2 float64 more workspace) so that
                           ojbkq_set_knobs can change lambda_rel after a
                           solve; 0: it cannot.                             */
+  int32_t gram_fp64;   /* arithmetic of the token sums X~^T X~ and
+                          X~^T (X - X~) (Alg. 1 steps 2-3):
+                          0: every row split into four int8 digits of 7 bits
+                             below its power-of-two maximum (28 bits: every
+                             fp32 value within 2^-5 of the row maximum
+                             exactly), digit products summed exactly in int32
+                             on the int8 matrix cores, ten products per tile,
+                             combined in float64 (the Ozaki scheme); the cross
+                             term is formed from the exact fp64 difference;
+                          1: float64 matrix cores on the widened fp32 values
+                             (exact products, float64 sums).             */
 } ojbkq_params;
 
 typedef struct ojbkq_ctx ojbkq_ctx;   /* opaque staged-solve state (host)     */
@@ -173,9 +184,10 @@ int ojbkq_quantize_layer_noalloc(const ojbkq_params* p, const float* W, const fl
  *               W [n, m] float32 (device, caller-owned, unchanged until the
  *               last solve; NULL: EINVAL).  The cross term enters the path
  *               only as X~^T (X - X~) w_j (Eq. jta_target); when 5 n <= 2 m
- *               the library then accumulates those products chunk by chunk
- *               and never forms the [m, m] cross term, which costs 4 n m
- *               instead of 2 m^2 multiply-adds per token.  Results are the
+ *               (fp64 token sums) or 10 n <= m (int8 token sums) the
+ *               library then accumulates those products chunk by chunk in
+ *               fp64 and never forms the [m, m] cross term, which costs
+ *               4 n m instead of 2 m^2 multiply-adds per token.  Results are the
  *               same either way up to rounding.  Every solve must then pass
  *               this same W pointer (EINVAL otherwise).
  *   accumulate: adds X_q_c X_q_c^T and X_q_c (X_ref_c - X_q_c)^T of one chunk

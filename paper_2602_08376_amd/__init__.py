@@ -58,6 +58,7 @@ class Params(ctypes.Structure):
         ("group", ctypes.c_int32), ("K", ctypes.c_int32), ("scheme", ctypes.c_int32),
         ("alpha", ctypes.c_double), ("lambda_rel", ctypes.c_double), ("seed", ctypes.c_uint64),
         ("act_order", ctypes.c_int32), ("keep_gram", ctypes.c_int32),
+        ("gram_fp64", ctypes.c_int32),
     ]
 
 
@@ -128,13 +129,18 @@ def _act_order(v) -> int:
     return ACT_ORDER[v]
 
 
+GRAMS = {"int8": 0, "fp64": 1}   # arithmetic of the token sums (ojbkq_params.gram_fp64)
+
+
 def _params(m, n, bits, group, K, alpha, lambda_rel, seed, scheme="asym",
-            act_order=False, keep_gram=False) -> Params:
+            act_order=False, keep_gram=False, gram="int8") -> Params:
     if scheme not in SCHEMES:
         raise ValueError(f"scheme must be one of {sorted(SCHEMES)}")
+    if gram not in GRAMS:
+        raise ValueError(f"gram must be one of {sorted(GRAMS)}")
     return Params(int(m), int(n), int(bits), int(group), int(K), SCHEMES[scheme], float(alpha),
                   float(lambda_rel), int(seed) & 0xFFFFFFFFFFFFFFFF, _act_order(act_order),
-                  1 if keep_gram else 0)
+                  1 if keep_gram else 0, GRAMS[gram])
 
 
 def _ptr(t: Optional[torch.Tensor]):
@@ -169,10 +175,10 @@ def _rows_view(X: torch.Tensor, name: str, m: int):
     return T, max(ld, T)
 
 
-def projects_cross_term(m: int, n: int) -> bool:
+def projects_cross_term(m: int, n: int, gram: str = "int8") -> bool:
     """Whether a context with bound weights accumulates the cross term as
     W E^T instead of forming E (the rule stated at ojbkq_set_weights)."""
-    return 5 * n <= 2 * m
+    return 10 * n <= m if gram == "int8" else 5 * n <= 2 * m
 
 
 def num_groups(m: int, group: int) -> int:
@@ -181,9 +187,9 @@ def num_groups(m: int, group: int) -> int:
 
 
 def workspace_bytes(m, n, bits, group, K, alpha=0.5, lambda_rel=0.01, seed=0,
-                    act_order=False, keep_gram=False) -> int:
+                    act_order=False, keep_gram=False, gram="int8") -> int:
     p = _params(m, n, bits, group, K, alpha, lambda_rel, seed, act_order=act_order,
-                keep_gram=keep_gram)
+                keep_gram=keep_gram, gram=gram)
     nb = library().ojbkq_workspace_bytes(ctypes.byref(p))
     if nb == 0:
         _check(-1)
@@ -226,14 +232,15 @@ def _outputs(n, m, G, device, act_order=False):
 
 def quantize_layer(W, X_ref, X_q, alpha, bits, group, K, seed, lambda_rel=0.01,
                    workspace: Optional[torch.Tensor] = None, scheme="asym",
-                   act_order=False) -> QuantResult:
+                   act_order=False, gram="int8") -> QuantResult:
     """One-shot ``ojbkq_quantize_layer`` on device tensors.
 
     W [n, m] float32; X_ref, X_q [m, T] float32 (X_ref may be None or X_q);
     scheme: "asym" (min-max) or "sym" (Absmax) scales and zero points;
     act_order: decode the features with the largest Hessian diagonal first
     (codes stay in W's order, ``perm`` holds the decode order); True groups
-    the scales by decode position, "static" keeps W's own groups.
+    the scales by decode position, "static" keeps W's own groups;
+    gram: "int8" (digit products on the int8 matrix cores) or "fp64".
     """
     n, m = W.shape
     dev = W.device
@@ -246,7 +253,7 @@ def quantize_layer(W, X_ref, X_q, alpha, bits, group, K, seed, lambda_rel=0.01,
         _need(X_ref, "X_ref", torch.float32, device=dev)
         if tuple(X_ref.shape) != tuple(X_q.shape) or X_ref.stride() != X_q.stride():
             raise ValueError("X_ref must have the shape and strides of X_q")
-    p = _params(m, n, bits, group, K, alpha, lambda_rel, seed, scheme, act_order)
+    p = _params(m, n, bits, group, K, alpha, lambda_rel, seed, scheme, act_order, gram=gram)
     lib = library()
     need = lib.ojbkq_workspace_bytes(ctypes.byref(p))
     if need == 0:
@@ -262,7 +269,7 @@ def quantize_layer(W, X_ref, X_q, alpha, bits, group, K, seed, lambda_rel=0.01,
 
 
 def quantize_layer_noalloc(W, X_ref, X_q, alpha, bits, group, K, seed, lambda_rel=0.01,
-                           scheme="asym", act_order=False,
+                           scheme="asym", act_order=False, gram="int8",
                            out: Optional[QuantResult] = None) -> QuantResult:
     """``ojbkq_quantize_layer_noalloc``: the one-shot call on the library's
     static scratch (no workspace).  ``out`` may pass preallocated outputs
@@ -278,7 +285,7 @@ def quantize_layer_noalloc(W, X_ref, X_q, alpha, bits, group, K, seed, lambda_re
         _need(X_ref, "X_ref", torch.float32, device=dev)
         if tuple(X_ref.shape) != tuple(X_q.shape) or X_ref.stride() != X_q.stride():
             raise ValueError("X_ref must have the shape and strides of X_q")
-    p = _params(m, n, bits, group, K, alpha, lambda_rel, seed, scheme, act_order)
+    p = _params(m, n, bits, group, K, alpha, lambda_rel, seed, scheme, act_order, gram=gram)
     if out is None:
         out = _outputs(n, m, num_groups(m, group), dev, act_order)
     rc = library().ojbkq_quantize_layer_noalloc(
@@ -293,7 +300,7 @@ class LayerSolver:
 
     def __init__(self, m, n, bits, group, K, seed, lambda_rel=0.01, device="cuda",
                  workspace: Optional[torch.Tensor] = None, scheme="asym", act_order=False,
-                 keep_gram=False):
+                 keep_gram=False, gram="int8"):
         self.m, self.n, self.bits, self.group, self.K = int(m), int(n), bits, group, K
         _act_order(act_order)
         self.act_order = act_order
@@ -302,7 +309,7 @@ class LayerSolver:
         if self.device.index is None:
             self.device = torch.device("cuda", torch.cuda.current_device())
         self.p = _params(m, n, bits, group, K, 0.5, lambda_rel, seed, scheme, act_order,
-                         keep_gram)
+                         keep_gram, gram)
         lib = library()
         need = lib.ojbkq_workspace_bytes(ctypes.byref(self.p))
         if need == 0:

@@ -46,6 +46,7 @@ struct Shape {
   bool act_order;       // any weight permutation
   bool static_groups;   // act_order 2: scale groups stay runs of g features in W's order
   bool keep_gram;
+  bool gram_i8;         // token sums on the int8 matrix cores (params.gram_fp64 == 0)
 };
 
 Shape shape_of(const ojbkq_params& p) {
@@ -61,6 +62,7 @@ Shape shape_of(const ojbkq_params& p) {
   s.act_order = p.act_order != 0;
   s.static_groups = p.act_order == 2 && s.G > 1;
   s.keep_gram = p.keep_gram != 0;
+  s.gram_i8 = p.gram_fp64 == 0;
   return s;
 }
 
@@ -72,11 +74,15 @@ inline bool route_q(const Shape& s) { return 2 * s.n > s.m; }
 
 // With W known while the activations stream in, the direct route needs the
 // cross term only through U = W E^T = sum over chunks of (W D_c) X~_c^T,
-// D_c = X_c - X~_c: 4 n m multiply-adds per token instead of the mixed
-// product's 2 m^2 (and no W E^T at solve time).  That pays once n is below
-// about 0.4 m (the general GEMM reaches about 0.75 of the MFMA peak, the
-// Gram kernel about 0.89).
-inline bool route_p(const Shape& s) { return 5 * s.n <= 2 * s.m; }
+// D_c = X_c - X~_c: 4 n m fp64 multiply-adds per token instead of the cross
+// term's 2 m^2 (and no W E^T at solve time).  Against the fp64 mixed product
+// that pays once n is below about 0.4 m (the general GEMM reaches about 0.75
+// of the MFMA peak, the Gram kernel about 0.89); against the int8 cross term
+// (ten digit products per entry at about 60 times the fp64 rate) only once n
+// is below about m / 10.
+inline bool route_p(const Shape& s) {
+  return s.gram_i8 ? 10 * s.n <= s.m : 5 * s.n <= 2 * s.m;
+}
 
 // Tokens per projection step: W D_c for this many tokens at a time sits in
 // the cross-term buffer, which the projected route leaves unused (n t <= m^2).
@@ -91,7 +97,7 @@ int64_t proj_tokens(const Shape& s) {
 struct Layout {
   size_t status = 0, lam2 = 0, G = 0, E = 0, U = 0, gq = 0, alpha = 0, pcodes = 0,
          presid = 0, gc_scratch = 0, gc_tiles = 0, F = 0, Linv = 0, Q = 0, Lsum = 0, SZ = 0,
-         perm = 0, Wp = 0, invperm = 0, gidx = 0, spos = 0, Gsave = 0, total = 0;
+         perm = 0, Wp = 0, invperm = 0, gidx = 0, spos = 0, Gsave = 0, split = 0, total = 0;
 };
 
 Layout layout_full(const Shape& s) {
@@ -112,7 +118,8 @@ Layout layout_full(const Shape& s) {
   L.alpha = take((size_t)s.n * sizeof(double));
   L.pcodes = take((size_t)ojbkq::decode_code_bytes(s.m, s.geo));
   L.presid = take((size_t)s.paths * sizeof(double));
-  L.gc_scratch = take(ojbkq::gram_cross_scratch_bytes());
+  L.gc_scratch = take(s.gram_i8 ? ojbkq::gram_i8_scratch_bytes()
+                                 : ojbkq::gram_cross_scratch_bytes());
   L.gc_tiles = take((size_t)ojbkq::gram_tile_count(s.m) * sizeof(uint32_t));
   L.F = take((size_t)ojbkq::decode_tile_count(s.m) * ojbkq::kDecodeTile * sizeof(double));
   L.Linv = take(mm);
@@ -132,18 +139,27 @@ Layout layout_full(const Shape& s) {
     L.spos = take((size_t)s.n * (size_t)((s.m + 31) / 32 * 32) * sizeof(float));
   }
   if (s.keep_gram) L.Gsave = take((size_t)s.m * (size_t)s.m * sizeof(double));
+  if (s.gram_i8) L.split = take(ojbkq::gram_i8_split_bytes(s.m));
   L.total = off;
   return L;
 }
 
-// Resident workgroups of the Gram kernel on the current device: two per CU.
-int gram_shares() {
+// Compute units of the current device (0 if the query fails).
+int device_cus() {
   int dev = 0, cus = 0;
-  if (hipGetDevice(&dev) != hipSuccess) return ojbkq::kGramCrossMaxShares;
+  if (hipGetDevice(&dev) != hipSuccess) return 0;
   if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
       cus <= 0)
-    return ojbkq::kGramCrossMaxShares;
-  return 2 * cus;
+    return 0;
+  return cus;
+}
+
+// Resident workgroups of the Gram kernel on the current device: two per CU
+// for the fp64 kernel, one (128 KB of LDS each) for the int8 kernel.
+int gram_shares(bool i8) {
+  const int cus = device_cus();
+  if (cus <= 0) return i8 ? ojbkq::kGramI8MaxShares : ojbkq::kGramCrossMaxShares;
+  return i8 ? cus : 2 * cus;
 }
 
 Layout layout_decode(const Shape& s) {
@@ -177,6 +193,7 @@ int check_params(const ojbkq_params* p) {
   if (p->scheme == 1 && p->bits < 2) return fail(OJBKQ_EINVAL, "the symmetric scheme needs bits >= 2");
   if (p->act_order < 0 || p->act_order > 2) return fail(OJBKQ_EINVAL, "act_order must be 0, 1 or 2");
   if (p->keep_gram != 0 && p->keep_gram != 1) return fail(OJBKQ_EINVAL, "keep_gram must be 0 or 1");
+  if (p->gram_fp64 != 0 && p->gram_fp64 != 1) return fail(OJBKQ_EINVAL, "gram_fp64 must be 0 or 1");
   if (!(p->alpha >= 0.0 && p->alpha <= 1.0)) return fail(OJBKQ_EINVAL, "alpha must be in [0, 1]");
   if (!(p->lambda_rel >= 0.0) || !std::isfinite(p->lambda_rel))
     return fail(OJBKQ_EINVAL, "lambda_rel must be finite and >= 0");
@@ -342,10 +359,16 @@ int ctx_accumulate(ojbkq_ctx* c, const float* Xr, const float* Xq, int64_t T, in
   double* E = c->at<double>(c->L.E);
   hipEvent_t t0 = stage_begin(c);
   if (c->projected) {
-    OJBKQ_HIP(ojbkq::gram_cross(Xq, nullptr, s.m, T, ldx, G, E, c->any_chunk, false,
-                                c->at<uint32_t>(c->L.gc_tiles), c->at<void>(c->L.gc_scratch),
-                                gram_shares(), c->stream),
-              "gram");
+    if (s.gram_i8)
+      OJBKQ_HIP(ojbkq::gram_i8(Xq, nullptr, s.m, T, ldx, G, E, c->any_chunk, false,
+                               c->at<uint32_t>(c->L.gc_tiles), c->at<void>(c->L.split),
+                               c->at<void>(c->L.gc_scratch), gram_shares(true), c->stream),
+                "gram");
+    else
+      OJBKQ_HIP(ojbkq::gram_cross(Xq, nullptr, s.m, T, ldx, G, E, c->any_chunk, false,
+                                  c->at<uint32_t>(c->L.gc_tiles), c->at<void>(c->L.gc_scratch),
+                                  gram_shares(false), c->stream),
+                "gram");
     if (cross) {
       // U (+)= (W D) X~^T over this chunk, tp tokens at a time; W D in E's buffer
       double* P = E;
@@ -367,6 +390,13 @@ int ctx_accumulate(ojbkq_ctx* c, const float* Xr, const float* Xq, int64_t T, in
         OJBKQ_HIP(ojbkq::gemm_f64(u, c->stream), "projected cross term");
       }
     }
+  } else if (s.gram_i8) {
+    // E is the cross term itself: a chunk without one adds nothing to it
+    OJBKQ_HIP(ojbkq::gram_i8(Xq, cross ? Xr : nullptr, s.m, T, ldx, G, E, c->any_chunk,
+                             c->cross_seen, c->at<uint32_t>(c->L.gc_tiles),
+                             c->at<void>(c->L.split), c->at<void>(c->L.gc_scratch),
+                             gram_shares(true), c->stream),
+              "gram and cross term");
   } else {
     // E holds the mixed product X~ X^T of every chunk; a chunk without a cross
     // term contributes X~ X~^T to it, so that E - G stays the cross term
@@ -376,7 +406,7 @@ int ctx_accumulate(ojbkq_ctx* c, const float* Xr, const float* Xq, int64_t T, in
     OJBKQ_HIP(ojbkq::gram_cross(Xq, mixed ? (cross ? Xr : Xq) : nullptr, s.m, T, ldx, G, E,
                                 c->any_chunk, c->cross_seen || (cross && c->any_chunk),
                                 c->at<uint32_t>(c->L.gc_tiles), c->at<void>(c->L.gc_scratch),
-                                gram_shares(), c->stream),
+                                gram_shares(false), c->stream),
               "gram and cross term");
   }
   stage_end(c, OJBKQ_STAGE_GRAM, t0);
@@ -447,7 +477,7 @@ int ctx_solve(ojbkq_ctx* c, const float* W, double alpha, uint8_t* codes, float*
               "restore Gram");
   }
   if (!c->prepared) {
-    if (c->cross_seen && !c->projected)   // mixed product -> cross term, while G is the Gram
+    if (c->cross_seen && !c->projected && !s.gram_i8)   // mixed product -> cross term
       OJBKQ_HIP(ojbkq::cross_from_mixed(c->at<double>(c->L.E), Lf, s.m, st), "cross term");
     if (perm) {
       // act order: the permuted problem's P G P^T, P E P^T or U P^T, gathered

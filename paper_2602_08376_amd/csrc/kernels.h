@@ -62,6 +62,20 @@ hipError_t gram_cross(const float* Xq, const float* Xr, int64_t m, int64_t T, in
                       double* G, double* E, bool accumulate_g, bool accumulate_e,
                       const uint32_t* tile_list, void* scratch, int max_shares,
                       hipStream_t stream);
+// The same sums on the int8 matrix cores (gram_i8.hip): every row of X_q
+// and of D = X_ref - X_q split into four int8 digits below its power-of-two
+// maximum, digit products summed exactly in int32, combined in fp64.
+//   G (lower triangle by 128-tiles) = [G +] X_q X_q^T
+//   E (all of it, only if Xr != nullptr) = [E +] X_q (X_ref - X_q)^T
+// split: gram_i8_split_bytes(m) of device memory for the digits; scratch:
+// gram_i8_scratch_bytes() for partial tiles; max_shares: workgroups (one per
+// CU is the resident maximum; at most kGramI8MaxShares).
+constexpr int kGramI8MaxShares = 256;
+size_t gram_i8_split_bytes(int64_t m);
+size_t gram_i8_scratch_bytes();
+hipError_t gram_i8(const float* Xq, const float* Xr, int64_t m, int64_t T, int64_t ldx, double* G,
+                   double* E, bool accumulate_g, bool accumulate_e, const uint32_t* tile_list,
+                   void* split, void* scratch, int max_shares, hipStream_t stream);
 // E <- E - G (G read through symmetry): turns the accumulated mixed product
 // X_q X_ref^T into the cross term X_q (X_ref - X_q)^T.  Call before G is
 // factored.

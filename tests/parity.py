@@ -34,6 +34,23 @@ SCALE_RTOL = 1e-6
 TIE_BAND = 1e-5
 U_BAND = 1e-6
 
+# Relative error of the token sums X~^T X~ and X~^T (X - X~), and of what
+# follows from them to first order (lambda^2, the factor, matrix-free probes,
+# the Gram diagonal that orders act-order features), by the arithmetic of the
+# Gram stage (ojbkq_params.gram_fp64):
+#   int8: every value is kept to 28 bits below its row's power-of-two maximum
+#     2^e (error <= 2^(e-28)), so a product x_i x_j loses at most about
+#     2^-27 2^(e_i + e_j) per token, with random signs over the tokens: about
+#     sqrt(T) 2^-27 2^(e_i + e_j) in all, measured 1e-10 to 5e-10 of
+#     sqrt(G_ii G_jj) on these workloads; 1e-8 leaves a 20x margin;
+#   fp64: exact products, float64 sums.
+GRAM_RTOL = {"int8": 1e-8, "fp64": 1e-11}
+# the same for quantities that go through a solve with H (Rbar qbar, whose
+# cross-term part is L^-1 E w, the centres, candidate residuals): the above
+# amplified by at most the conditioning of H, measured up to 2.3e-8 relative
+# for int8
+SOLVE_RTOL = {"int8": 1e-6, "fp64": 1e-9}
+
 
 def np64(t):
     return t.detach().cpu().numpy()

@@ -56,6 +56,19 @@ def test_bad_params_rejected(bad):
     assert lib.ojbkq_last_error().decode()
 
 
+def test_gram_mode_values():
+    lib = ok.library()
+    for v, good in ((0, True), (1, True), (2, False), (-1, False)):
+        p = _p()
+        p.gram_fp64 = v
+        assert (lib.ojbkq_workspace_bytes(ctypes.byref(p)) > 0) == good, v
+    # the int8 token sums carve their split digits (about 64 m^2 bytes) from
+    # the workspace; their partial-tile scratch is half the fp64 kernel's
+    i8 = ok.workspace_bytes(4096, 4096, 4, 128, 16, gram="int8")
+    f64 = ok.workspace_bytes(4096, 4096, 4, 128, 16, gram="fp64")
+    assert i8 - f64 >= 64 * 4096 ** 2 - 64 * 2 ** 20
+
+
 def test_scheme_values():
     lib = ok.library()
     for scheme, bits, ok_ in ((0, 4, True), (1, 4, True), (1, 2, True), (1, 1, False),

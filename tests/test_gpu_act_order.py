@@ -16,12 +16,14 @@ import torch
 import paper_2602_08376_amd as ok
 from oracle import infer as oi
 from oracle import ojbkq as orc
-from parity import SCALE_RTOL, check_layer_strict, np64
+from parity import GRAM_RTOL, SCALE_RTOL, check_layer_strict, np64
 from synth import LayerConfig, make_layer
 
 pytestmark = pytest.mark.gpu
 DEV = "cuda"
-KEY_RTOL = 1e-12     # diagonal entries this close may be ordered either way
+# diagonal entries this close may be ordered either way: the GPU sorts its
+# own Gram diagonal, whose relative error is that of the int8 token sums
+KEY_RTOL = GRAM_RTOL["int8"]
 
 
 @pytest.fixture(scope="module", autouse=True)
