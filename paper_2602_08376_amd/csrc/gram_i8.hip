@@ -293,13 +293,22 @@ __device__ __forceinline__ void i8_segment(const I8Args& a, int64_t tile, int64_
       for (int x = 0; x < 2; ++x)
         fa[p][x] = *reinterpret_cast<const v4i*>(cur + (p * 8 + wr * 2 + x) * kBlockBytes +
                                                  lane * 16);
+    // B fragments one digit ahead: the reads of digit q + 1 fly while the
+    // products of digit q run
+    const uint8_t* bsrc = cur + (kPanelBlocks + wc * 4) * kBlockBytes + lane * 16;
+    v4i fbn[4];
+#pragma unroll
+    for (int y = 0; y < 4; ++y) fbn[y] = *reinterpret_cast<const v4i*>(bsrc + y * kBlockBytes);
 #pragma unroll
     for (int q = 0; q < kDigits; ++q) {
       v4i fb[4];
 #pragma unroll
-      for (int y = 0; y < 4; ++y)
-        fb[y] = *reinterpret_cast<const v4i*>(cur + (kPanelBlocks + q * 8 + wc * 4 + y) *
-                                                        kBlockBytes + lane * 16);
+      for (int y = 0; y < 4; ++y) fb[y] = fbn[y];
+      if (q + 1 < kDigits) {
+#pragma unroll
+        for (int y = 0; y < 4; ++y)
+          fbn[y] = *reinterpret_cast<const v4i*>(bsrc + ((q + 1) * 8 + y) * kBlockBytes);
+      }
 #pragma unroll
       for (int p = 0; p < kDigits; ++p) {
         if (p + q > kDigits) continue;   // digit pairs with p + q <= 6 (1-based)
