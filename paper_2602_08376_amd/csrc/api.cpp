@@ -39,9 +39,20 @@ constexpr int kStatusClear = 0x7f7f7f7f;   // byte-fill value meaning "no bad pi
 
 size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 
+// Compute units of the current device (0 if the query fails).
+int device_cus() {
+  int dev = 0, cus = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return 0;
+  if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+      cus <= 0)
+    return 0;
+  return cus;
+}
+
 struct Shape {
   int64_t m, n, g, G, K, paths;
   ojbkq::DecodeGeom geo;
+  int cus;              // compute units the decoder's geometry is laid out for
   int qmax;
   bool act_order;       // any weight permutation
   bool static_groups;   // act_order 2: scale groups stay runs of g features in W's order
@@ -57,7 +68,8 @@ Shape shape_of(const ojbkq_params& p) {
   s.G = (s.m + s.g - 1) / s.g;
   s.K = p.K;
   s.paths = p.n * (int64_t)(p.K + 1);
-  s.geo = ojbkq::decode_geometry(p.n, p.K);
+  s.cus = device_cus();
+  s.geo = ojbkq::decode_geometry(p.n, p.K, s.cus);
   s.qmax = (1 << p.bits) - 1;
   s.act_order = p.act_order != 0;
   s.static_groups = p.act_order == 2 && s.G > 1;
@@ -142,16 +154,6 @@ Layout layout_full(const Shape& s) {
   if (s.gram_i8) L.split = take(ojbkq::gram_i8_split_bytes(s.m));
   L.total = off;
   return L;
-}
-
-// Compute units of the current device (0 if the query fails).
-int device_cus() {
-  int dev = 0, cus = 0;
-  if (hipGetDevice(&dev) != hipSuccess) return 0;
-  if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
-      cus <= 0)
-    return 0;
-  return cus;
 }
 
 // Resident workgroups of the Gram kernel on the current device: two per CU
@@ -423,7 +425,7 @@ int ctx_set_knobs(ojbkq_ctx* c, double lambda_rel, int32_t K) {
   Shape t = c->s;
   t.K = K;
   t.paths = t.n * (int64_t)(K + 1);
-  t.geo = ojbkq::decode_geometry(t.n, K);
+  t.geo = ojbkq::decode_geometry(t.n, K, t.cus);
   if ((size_t)ojbkq::decode_code_bytes(t.m, t.geo) > c->pcodes_cap ||
       (size_t)t.paths * sizeof(double) > c->presid_cap)
     return fail(OJBKQ_EINVAL, "this K needs more decoder space than the context was created for");
@@ -625,7 +627,7 @@ int ctx_solve(ojbkq_ctx* c, const float* W, double alpha, uint8_t* codes, float*
   }
   d.m = s.m; d.n = s.n; d.g = s.g; d.G = s.G; d.K = (int)s.K; d.bits = c->p.bits;
   d.seed = c->p.seed;
-  d.wg_paths = s.geo.wg_paths; d.threads = s.geo.threads;
+  d.wg_paths = s.geo.wg_paths; d.threads = s.geo.threads; d.nwg = s.geo.nwg;
   d.pcodes = c->at<uint8_t>(c->L.pcodes);
   d.presid = c->at<double>(c->L.presid);
   t0 = stage_begin(c);
@@ -878,7 +880,7 @@ int ojbkq_decode_stage(const ojbkq_params* p, const double* R, const double* qba
   ojbkq::DecodeDesc d;
   d.F = reinterpret_cast<double*>(ws + L.F); d.gq = gq; d.S = scales; d.alpha = al;
   d.m = s.m; d.n = s.n; d.g = s.g; d.G = s.G; d.K = (int)s.K; d.bits = p->bits; d.seed = p->seed;
-  d.wg_paths = s.geo.wg_paths; d.threads = s.geo.threads;
+  d.wg_paths = s.geo.wg_paths; d.threads = s.geo.threads; d.nwg = s.geo.nwg;
   d.pcodes = reinterpret_cast<uint8_t*>(ws + L.pcodes);
   d.presid = reinterpret_cast<double*>(ws + L.presid);
   OJBKQ_HIP(ojbkq::launch_decode(d, st), "decode");

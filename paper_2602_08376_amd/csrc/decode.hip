@@ -504,12 +504,19 @@ hipError_t launch_position_scales(const float* S, const int32_t* gidx, int64_t n
 }
 
 hipError_t launch_decode(const DecodeDesc& d, hipStream_t stream) {
-  const DecodeGeom geo = decode_geometry(d.n, d.K);
-  if (geo.nwg <= 0) return hipSuccess;
-  if (geo.nwg > 0x7fffffff || d.threads != geo.threads || d.wg_paths != geo.wg_paths ||
-      d.threads > kDecodeMaxThreads || d.threads % 64 != 0 || d.wg_paths % 16 != 0 ||
-      d.wg_paths > 4 * (int64_t)d.threads)
+  // the geometry must be one that decode_geometry gives: whole 16-path
+  // tiles, one wave per up to four of them, every path in some workgroup
+  const int64_t P = d.n * ((int64_t)d.K + 1);
+  if (P <= 0) return hipSuccess;
+  if (d.wg_paths < 16 || d.wg_paths % 16 != 0 || d.wg_paths > kDecodeMaxThreads ||
+      d.threads != 64 * (int)(d.wg_paths / 16 < kDecodeMaxWaves ? d.wg_paths / 16
+                                                                  : kDecodeMaxWaves) ||
+      d.nwg != (P + d.wg_paths - 1) / d.wg_paths || d.nwg > 0x7fffffff)
     return hipErrorInvalidValue;
+  DecodeGeom geo;
+  geo.wg_paths = d.wg_paths;
+  geo.threads = d.threads;
+  geo.nwg = d.nwg;
   const size_t lds = (size_t)(d.threads / 64) * kWaveLds;
   const bool uniform_scale = !d.gidx && !d.spos && (d.G == 1 || d.g % kBS == 0);
   const void* fn = uniform_scale ? reinterpret_cast<const void*>(&decode_kernel<true>)

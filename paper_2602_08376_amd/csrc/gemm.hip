@@ -11,9 +11,9 @@
 // Design: 128x128 output tile per 256-thread workgroup, four waves in a 2x2
 // grid, each wave a 64x64 block of 4x4 v_mfma_f64_16x16x4_f64 tiles
 // (64 fp64 accumulators per lane).  Operands are staged through LDS in
-// 16-deep k-chunks, widened to fp64 on the way in (fp32 x fp32 products are
-// exact in fp64), with the next chunk prefetched into registers while the
-// current one feeds the matrix cores.  Tiles are numbered so that each XCD
+// 32-deep k-chunks (loaded in two 16-deep halves), widened to fp64 on the way
+// in (fp32 x fp32 products are exact in fp64), with the next chunk prefetched
+// into registers while the current one feeds the matrix cores.  Tiles are numbered so that each XCD
 // (eight per MI355X, one L2 each) receives a contiguous, row-grouped run of
 // tiles that share A and B panels; with a triangular B, in order of
 // decreasing work instead.

@@ -195,14 +195,15 @@ __global__ __launch_bounds__(kThreads, 1) void dequant_matmul_kernel(DqArgs a) {
     // W_hat = fp16(fp32(s (q - z))), zero past the last feature or channel.
     // Two roundings: the empty asm pins the float32 product in a register,
     // so it is not folded into v_fma_mixlo_f16, which rounds once to fp16.
-    const int zi = (int)z_cur;
+    // q - z in fp32 (exact for the integer zero points a quantize call
+    // gives; a fractional z is honoured as the float it is).
     if (stage_in) {   // interior: no masks
 #pragma unroll
       for (int h = 0; h < 2; ++h) {
         h8 v;
 #pragma unroll
         for (int c = 0; c < 8; ++c) {
-          float p = s_cur * (float)((int)cl.code(8 * h + c) - zi);
+          float p = s_cur * ((float)cl.code(8 * h + c) - z_cur);
           __asm__("" : "+v"(p));
           v[c] = (_Float16)p;
         }
@@ -215,7 +216,7 @@ __global__ __launch_bounds__(kThreads, 1) void dequant_matmul_kernel(DqArgs a) {
 #pragma unroll
         for (int c = 0; c < 8; ++c) {
           const int cc = 8 * h + c;
-          float p = s_cur * (float)((int)cl.code(cc) - zi);
+          float p = s_cur * ((float)cl.code(cc) - z_cur);
           __asm__("" : "+v"(p));
           const _Float16 w = (_Float16)p;
           v[c] = (aj < a.n && kf + 16 * ac + cc < a.m) ? w : (_Float16)0.f;

@@ -141,7 +141,7 @@ hipError_t launch_klein_alpha(const double* L, const float* S, int64_t n, int64_
 // many waves (up to eight) as evenly as possible: with two waves per SIMD one
 // wave's serial steps overlap the other's matrix products.  Waves never wait
 // for each other.
-constexpr int kDecodeCUs = 256;         // compute units of an MI355X
+constexpr int kDecodeCUs = 256;         // compute units assumed when the device cannot be asked
 constexpr int kDecodeMaxThreads = 512;  // paths (one per lane) per workgroup, at most
 constexpr int kDecodeMaxWaves = 8;      // waves per workgroup, at most
 constexpr int kDecodeBlock = 32;        // rows decided per serial block
@@ -153,11 +153,13 @@ struct DecodeGeom {
   int64_t nwg = 0;        // workgroups
 };
 
-inline DecodeGeom decode_geometry(int64_t n, int K) {
+// `cus`: compute units of the device the decoder runs on (<= 0: kDecodeCUs).
+inline DecodeGeom decode_geometry(int64_t n, int K, int cus) {
   const int64_t P = n * (int64_t)(K + 1);
+  const int64_t units = cus > 0 ? cus : kDecodeCUs;
   int64_t per = 16;
   for (int64_t rounds = 1;; ++rounds) {
-    const int64_t slots = (int64_t)kDecodeCUs * rounds;
+    const int64_t slots = units * rounds;
     per = (P + slots - 1) / slots;
     per = (per + 15) / 16 * 16;
     if (per <= kDecodeMaxThreads) break;
@@ -228,6 +230,7 @@ struct DecodeDesc {
   uint64_t seed = 0;
   int64_t wg_paths = 0;        // from decode_geometry
   int threads = 0;
+  int64_t nwg = 0;
   uint8_t* pcodes = nullptr;   // decode_code_bytes(m, geometry) candidate codes
   double* presid = nullptr;    // [n (K + 1)] candidate residuals
 };
