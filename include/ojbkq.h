@@ -125,9 +125,9 @@ typedef struct {
                           X~^T (X - X~) (Alg. 1 steps 2-3):
                           0: every row split into four int8 digits of 7 bits
                              below its power-of-two maximum (28 bits: every
-                             fp32 value within 2^-5 of the row maximum
+                             fp32 value within 2^-4 of the row maximum
                              exactly), digit products summed exactly in int32
-                             on the int8 matrix cores, ten products per tile,
+                             on the int8 matrix cores, thirteen products per tile,
                              combined in float64 (the Ozaki scheme); the cross
                              term is formed from the exact fp64 difference;
                           1: float64 matrix cores on the widened fp32 values

@@ -20,7 +20,7 @@ INCLUDE = os.path.join(ROOT, "include")
 BUILD_DIR = os.path.join(ROOT, "_build")
 LIB = os.path.join(PKG, "libojbkq.so")
 
-SOURCES = ["api.cpp", "gemm.hip", "gram.hip", "gram_i8.hip", "factor.hip", "quant.hip", "decode.hip",
+SOURCES = ["api.cpp", "gemm.hip", "gram.hip", "gram_i8.hip", "factor.hip", "chol_dag.hip", "quant.hip", "decode.hip",
            "infer.hip", "permute.hip", "noalloc.hip"]
 
 HIPCC_FLAGS = [

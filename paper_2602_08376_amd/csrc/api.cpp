@@ -90,10 +90,21 @@ inline bool route_q(const Shape& s) { return 2 * s.n > s.m; }
 // term's 2 m^2 (and no W E^T at solve time).  Against the fp64 mixed product
 // that pays once n is below about 0.4 m (the general GEMM reaches about 0.75
 // of the MFMA peak, the Gram kernel about 0.89); against the int8 cross term
-// (ten digit products per entry at about 60 times the fp64 rate) only once n
+// (thirteen digit products per entry at about 60 times the fp64 rate) only once n
 // is below about m / 10.
 inline bool route_p(const Shape& s) {
   return s.gram_i8 ? 10 * s.n <= s.m : 5 * s.n <= 2 * s.m;
+}
+
+// The factor in one launch of 64x64 tile tasks up to this size; beyond it
+// the blocked factor (64-wide steps, 256-wide outer panels), whose large
+// trailing products run at a higher fraction of the MFMA peak.
+constexpr int64_t kDagMaxM = 12288;
+inline bool use_dag(const Shape& s) { return s.m <= kDagMaxM; }
+// L^-1 for the solves: all of it when Rbar qbar goes through Q, else its
+// diagonal blocks for the triangular solve.
+inline int64_t inv_block(const Shape& s) {
+  return route_q(s) ? (s.m + 63) / 64 * 64 : ojbkq::kTrsmLeaf;
 }
 
 // Tokens per projection step: W D_c for this many tokens at a time sits in
@@ -109,7 +120,8 @@ int64_t proj_tokens(const Shape& s) {
 struct Layout {
   size_t status = 0, lam2 = 0, G = 0, E = 0, U = 0, gq = 0, alpha = 0, pcodes = 0,
          presid = 0, gc_scratch = 0, gc_tiles = 0, F = 0, Linv = 0, Q = 0, Lsum = 0, SZ = 0,
-         perm = 0, Wp = 0, invperm = 0, gidx = 0, spos = 0, Gsave = 0, split = 0, total = 0;
+         perm = 0, Wp = 0, invperm = 0, gidx = 0, spos = 0, Gsave = 0, split = 0, dag = 0,
+         dag_tasks = 0, total = 0;
 };
 
 Layout layout_full(const Shape& s) {
@@ -152,6 +164,10 @@ Layout layout_full(const Shape& s) {
   }
   if (s.keep_gram) L.Gsave = take((size_t)s.m * (size_t)s.m * sizeof(double));
   if (s.gram_i8) L.split = take(ojbkq::gram_i8_split_bytes(s.m));
+  if (use_dag(s)) {
+    L.dag = take(ojbkq::chol_dag_sync_bytes(s.m));
+    L.dag_tasks = take((size_t)ojbkq::chol_dag_task_count(s.m, inv_block(s)) * sizeof(uint32_t));
+  }
   L.total = off;
   return L;
 }
@@ -340,6 +356,16 @@ int ctx_init(ojbkq_ctx* c, const ojbkq_params* p, void* ws, size_t bytes, void* 
     OJBKQ_HIP(hipMemcpyAsync(c->at<uint32_t>(c->L.gc_tiles), tiles.data(),
                              tiles.size() * sizeof(uint32_t), hipMemcpyHostToDevice, c->stream),
               "tile list");
+    if (use_dag(c->s)) {
+      // task order of the tiled factor, also built once per context
+      std::vector<uint32_t> tasks((size_t)ojbkq::chol_dag_task_count(c->s.m, inv_block(c->s)));
+      ojbkq::chol_dag_task_list(c->s.m, inv_block(c->s), tasks.data());
+      OJBKQ_HIP(hipMemcpyAsync(c->at<uint32_t>(c->L.dag_tasks), tasks.data(),
+                               tasks.size() * sizeof(uint32_t), hipMemcpyHostToDevice,
+                               c->stream),
+                "factor task list");
+      OJBKQ_HIP(hipStreamSynchronize(c->stream), "factor task list");
+    }
     OJBKQ_HIP(hipStreamSynchronize(c->stream), "tile list");
   }
   return OJBKQ_OK;
@@ -454,6 +480,8 @@ int finish(ojbkq_ctx* c) {
             "status read");
   OJBKQ_HIP(hipStreamSynchronize(c->stream), "stream sync");
   fold_times(c);
+  if (st < 0)
+    return fail(OJBKQ_EHIP, "the tiled factor launch gave up waiting for a tile");
   if (st != kStatusClear)
     return fail(OJBKQ_ENOTPD, "damped Gram is not positive definite (pivot " + std::to_string(st) +
                                   ")");
@@ -517,12 +545,22 @@ int ctx_solve(ojbkq_ctx* c, const float* W, double alpha, uint8_t* codes, float*
   if (!c->factored) {
     OJBKQ_HIP(hipMemsetAsync(c->at<int>(c->L.status), 0x7f, sizeof(int), st), "status clear");
     OJBKQ_HIP(ojbkq::launch_damp(Lf, s.m, c->lambda_rel, c->at<double>(c->L.lam2), st), "damp");
-    OJBKQ_HIP(ojbkq::cholesky_lower(Lf, s.m, c->at<int>(c->L.status), c->at<double>(c->L.Linv), st),
-              "cholesky");
-    // L^-1 for the solves; the decoder tiles' buffer is free scratch until
-    // they are written
-    OJBKQ_HIP(ojbkq::invert_lower(Lf, s.m, c->at<double>(c->L.Linv), c->at<double>(c->L.F), st),
-              "factor inverse");
+    if (use_dag(s)) {
+      const int cus = s.cus > 0 ? s.cus : 256;   // one resident workgroup per CU
+      OJBKQ_HIP(ojbkq::cholesky_dag(Lf, s.m, c->at<int>(c->L.status), c->at<double>(c->L.Linv),
+                                    c->at<uint32_t>(c->L.dag_tasks),
+                                    ojbkq::chol_dag_task_count(s.m, inv_block(s)),
+                                    c->at<int>(c->L.dag), cus, st),
+                "cholesky");
+    } else {
+      OJBKQ_HIP(ojbkq::cholesky_lower(Lf, s.m, c->at<int>(c->L.status),
+                                      c->at<double>(c->L.Linv), st),
+                "cholesky");
+      // the decoder tiles' buffer is free scratch until they are written
+      OJBKQ_HIP(ojbkq::invert_lower(Lf, s.m, c->at<double>(c->L.Linv), c->at<double>(c->L.F),
+                                    inv_block(s), st),
+                "factor inverse");
+    }
     OJBKQ_HIP(ojbkq::launch_decode_tiles(Lf, s.m, c->at<double>(c->L.F), st), "decoder tiles");
     OJBKQ_HIP(ojbkq::launch_group_row_sums(Lf, s.m, s.g, s.G,
                                            s.static_groups ? c->at<int32_t>(c->L.invperm) : nullptr,
@@ -575,28 +613,29 @@ int ctx_solve(ojbkq_ctx* c, const float* W, double alpha, uint8_t* codes, float*
     OJBKQ_HIP(ojbkq::gemm_f64(g, st), "W Q");
   } else {
     if (cross) {
-      double* U = c->at<double>(c->L.U);
+      // gq = U L^-T, U = W E^T (row j is X~^T (X - X~) w_j): U formed in gq
+      // (or copied there when the projected route accumulated it, so that
+      // it survives for a later solve), then solved in place
       if (!c->projected) {
-        ojbkq::GemmDesc u;   // U = W E^T: row j is X~^T (X - X~) w_j
+        ojbkq::GemmDesc u;
         u.M = s.n; u.N = s.m; u.Kd = s.m;
         u.A = W; u.lda = s.m; u.ta = ojbkq::Elt::F32;
         u.B = c->at<double>(c->L.E); u.ldb = s.m; u.tb = ojbkq::Elt::F64;
-        u.C = U; u.ldc = s.m;
+        u.C = gq; u.ldc = s.m;
         OJBKQ_HIP(ojbkq::gemm_f64(u, st), "target projection");
+      } else {
+        OJBKQ_HIP(hipMemcpyAsync(gq, c->at<double>(c->L.U), (size_t)s.n * s.m * sizeof(double),
+                                 hipMemcpyDeviceToDevice, st),
+                  "projected cross term");
       }
-      ojbkq::GemmDesc y;   // gq = (1 - mu) U L^-T: row j is (1 - mu) L^-1 u_j
-      y.M = s.n; y.N = s.m; y.Kd = s.m;
-      y.A = U; y.lda = s.m; y.ta = ojbkq::Elt::F64;
-      y.B = c->at<double>(c->L.Linv); y.ldb = s.m; y.tb = ojbkq::Elt::F64;
-      y.b_zero_above_col = true;   // Linv[i][k] = 0 for k > i
-      y.C = gq; y.ldc = s.m; y.alpha = 1.0 - alpha;
-      OJBKQ_HIP(ojbkq::gemm_f64(y, st), "solve");
+      OJBKQ_HIP(ojbkq::trsm_right_lower_t(gq, s.m, s.n, Lf, c->at<double>(c->L.Linv), s.m, st),
+                "solve");
     }
-    ojbkq::GemmDesc g;   // gq[j][i] (+)= sum_l W[j][l] L[l][i]
+    ojbkq::GemmDesc g;   // gq[j][i] = (1 - mu) gq[j][i] + sum_l W[j][l] L[l][i]
     g.M = s.n; g.N = s.m; g.Kd = s.m;
     g.A = W; g.lda = s.m; g.ta = ojbkq::Elt::F32;
     g.B = Lf; g.ldb = s.m; g.tb = ojbkq::Elt::F64; g.b_kmajor = true; g.b_zero_below_col = true;
-    g.C = gq; g.ldc = s.m; g.beta = cross ? 1.0 : 0.0;
+    g.C = gq; g.ldc = s.m; g.beta = cross ? 1.0 - alpha : 0.0;
     OJBKQ_HIP(ojbkq::gemm_f64(g, st), "W L");
   }
   stage_end(c, OJBKQ_STAGE_SOLVE, t0);

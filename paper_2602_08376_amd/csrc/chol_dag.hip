@@ -1,0 +1,765 @@
+// Cholesky factor of the damped Gram and the inverse of that factor, tile by
+// tile in one persistent launch (Alg. 1 step 2: H = X~^T X~ + lambda^2 I =
+// L L^T, L = R^T; the relaxed solution of step 3 multiplies by L^-1).
+//
+// The lower triangle is cut into 64 x 64 tiles (the last row and column of
+// tiles ragged).  One task owns one output tile and runs on one 256-thread
+// workgroup, which keeps the tile in registers (wave w holds the 32 x 32
+// quadrant (w / 2, w % 2) as 2 x 2 v_mfma_f64_16x16x4_f64 accumulators):
+//   factor tile (i, j), i >= j:  T = H_ij - sum_{k < j} L_ik L_jk^T, then
+//       i == j: L_jj = chol(T) and Linv_jj = L_jj^-1, both in LDS;
+//       i >  j: L_ij = T Linv_jj^T;
+//   inverse tile (i, j), i > j, inside one block of `span` tiles:
+//       Linv_ij = -Linv_ii sum_{k = j}^{i-1} L_ik Linv_kj.
+// Left-looking: each task pulls the finished tiles it needs, so nothing is
+// written twice and no tile is locked.  The tasks come as a list (built on
+// the host, chol_dag_task_list) in which every task follows each task whose
+// tile it reads, and workgroups take list positions from a counter in order,
+// so a task only ever waits for a task that a running workgroup already
+// holds: the launch cannot deadlock however many workgroups are resident.  Each finished tile is
+// published with a flag (agent-scope release after the stores; readers poll
+// it and acquire).  A wait that outlasts kSpinLimit polls (seconds, far above
+// any real wait) raises a launch-wide error flag, and every workgroup leaves
+// at its next task.
+//
+// The diagonal tile is factored and inverted together by recursive halving
+// (chol_inv below).  The tile just below the diagonal is on the path from one
+// diagonal tile to the next, so the diagonal task forms it too (diag_task).
+#include "kernels.h"
+#include "device.h"
+
+namespace ojbkq {
+namespace {
+
+constexpr int kT = 64;                    // tile edge
+constexpr int kTT = kT * kT;              // doubles per tile
+constexpr int kThreads = 256;             // four waves
+constexpr uint32_t kSpinLimit = 1u << 21; // polls of one flag before the launch gives up
+// LDS: two operand tiles, or the diagonal block and its inverse (pitch
+// kT + 1) and the scratch of the recursive factor
+constexpr int kLdsDoubles = 2 * kT * (kT + 1) + 2 * (32 * 32 + 16 * 16 + 8 * 8);
+static_assert(2 * kTT <= kLdsDoubles, "operand tiles fit");
+
+// Swizzled row-major tile in LDS: element (r, k) at r * 64 + (k ^ 2 (r % 16)).
+// The 32 (row, k) pairs that half a wave reads for an MFMA operand (16 rows,
+// two adjacent k) land in 32 distinct bank pairs, and the two doubles (k, k+1),
+// k even, stay adjacent.
+__device__ __forceinline__ int sw(int r, int k) { return r * kT + (k ^ (2 * (r & 15))); }
+
+// Task kinds of the task list (code: kind << 30 | i << 15 | j).
+enum : int { kTaskDiag = 0, kTaskSub = 1, kTaskOff = 2, kTaskInv = 3 };
+
+struct DagArgs {
+  double* H;      // [m, m] damped Gram in, factor L out (lower; upper set to zero)
+  double* Linv;   // [m, m] inverse tiles out (diagonal tiles; listed inverse tiles)
+  int64_t m;
+  int nt;         // tiles per side
+  const uint32_t* tasks;   // the task list, in an order where every task
+  int64_t ntasks;          // comes after each task whose tile it reads
+  int* status;    // first non-positive pivot (atomic min)
+  int* sync;      // [0] task counter, [1] error, then flags: factor tiles, inverse
+                  // tiles (nt (nt + 1) / 2 each), parked sub-diagonal tiles (nt)
+};
+
+__device__ __forceinline__ int64_t tri(int i, int j) { return (int64_t)i * (i + 1) / 2 + j; }
+
+// Thread 0 polls a flag until it is set, then acquires (one cache
+// invalidation per wait, not per poll), or gives up on the launch-wide error
+// flag / the poll limit.
+__device__ bool wait_flag(const int* flag, int* err) {
+  for (uint32_t it = 0;; ++it) {
+    if (__hip_atomic_load(flag, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0) {
+      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+      return true;
+    }
+    if (__hip_atomic_load(err, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0) return false;
+    if (it >= kSpinLimit) {
+      __hip_atomic_store(err, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      return false;
+    }
+    __builtin_amdgcn_s_sleep(2);
+  }
+}
+
+// Every thread makes its tile stores visible device-wide (agent-scope
+// release fence), the workgroup meets, then thread 0 sets the flag.
+__device__ __forceinline__ void publish(int* flag) {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+  __syncthreads();
+  if (threadIdx.x == 0) __hip_atomic_store(flag, 1, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// Tile (r0, c0) of a row-major [m, m] matrix in the swizzled LDS layout,
+// entries outside the matrix as zero, in two steps so that the loads can be
+// in flight while the matrix cores work: fetch (global -> this thread's
+// registers), then put (registers -> LDS).  transpose: element (r, c) goes
+// to LDS position (c, r).
+constexpr int kPer = kTT / kThreads;   // elements of a tile per thread
+// Thread t holds column t % 64 of rows t / 64 + 4 q, q = 0..15: one base
+// address and a fixed stride of 4 rows.
+__device__ __forceinline__ void fetch(double (&v)[kPer], const double* src, int64_t m, int64_t r0,
+                                      int64_t c0) {
+  const int tid = threadIdx.x, c = tid & 63, rb = tid >> 6;
+  const bool col_in = c0 + c < m;
+  const int64_t rows_left = m - r0 - rb;   // rows rb + 4 q exist while 4 q < rows_left
+  const double* p = src + (r0 + rb) * m + c0 + c;
+  const int64_t step = 4 * m;
+#pragma unroll
+  for (int q = 0; q < kPer; ++q) v[q] = (col_in && 4 * q < rows_left) ? p[q * step] : 0.0;
+}
+__device__ __forceinline__ void put(double* s, const double (&v)[kPer], bool transpose) {
+  const int tid = threadIdx.x, c = tid & 63, rb = tid >> 6;
+#pragma unroll
+  for (int q = 0; q < kPer; ++q) {
+    const int r = rb + 4 * q;
+    s[transpose ? sw(c, r) : sw(r, c)] = v[q];
+  }
+}
+__device__ __forceinline__ void stage(double* s, const double* src, int64_t m, int64_t r0,
+                                      int64_t c0, bool transpose) {
+  double v[kPer];
+  fetch(v, src, m, r0, c0);
+  put(s, v, transpose);
+}
+
+// The wave's quadrant += sign * A B^T over the 64 k of two staged tiles:
+// A(row, k) = sA[sw(row, k)], B(col, k) = sB[sw(col, k)].
+__device__ __forceinline__ void tile_mma(d4 (&acc)[2][2], const double* sA, const double* sB,
+                                         int qa, int qb, double sign) {
+  const int lane = threadIdx.x & 63, l16 = lane & 15, lk = lane >> 4;
+#pragma unroll 4
+  for (int s = 0; s < kT / 4; ++s) {
+    const int k = 4 * s + lk;
+    double a[2], b[2];
+#pragma unroll
+    for (int x = 0; x < 2; ++x) {
+      a[x] = sign * sA[sw(32 * qa + 16 * x + l16, k)];
+      b[x] = sB[sw(32 * qb + 16 * x + l16, k)];
+    }
+#pragma unroll
+    for (int x = 0; x < 2; ++x)
+#pragma unroll
+      for (int y = 0; y < 2; ++y) acc[x][y] = mfma_f64(a[x], b[y], acc[x][y]);
+  }
+}
+
+// (row, col) within the tile of accumulator element q of sub-tile (x, y).
+__device__ __forceinline__ int acc_row(int qa, int x, int q) {
+  return 32 * qa + 16 * x + ((threadIdx.x & 63) >> 4) + 4 * q;
+}
+__device__ __forceinline__ int acc_col(int qb, int y) {
+  return 32 * qb + 16 * y + (threadIdx.x & 15);
+}
+
+__device__ __forceinline__ void store_acc(const d4 (&acc)[2][2], double* dst, int64_t m,
+                                          int64_t r0, int64_t c0, int qa, int qb) {
+#pragma unroll
+  for (int x = 0; x < 2; ++x)
+#pragma unroll
+    for (int y = 0; y < 2; ++y)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int64_t r = r0 + acc_row(qa, x, q), c = c0 + acc_col(qb, y);
+        if (r < m && c < m) dst[r * m + c] = acc[x][y][q];
+      }
+}
+
+__device__ __forceinline__ void zero_tile(double* dst, int64_t m, int64_t r0, int64_t c0) {
+  for (int e = threadIdx.x; e < kTT; e += kThreads) {
+    const int64_t r = r0 + (e >> 6), c = c0 + (e & 63);
+    if (r < m && c < m) dst[r * m + c] = 0.0;
+  }
+}
+
+// 1 / sqrt(d): hardware estimate, then two Newton steps y += y (1 - d y^2) / 2.
+__device__ __forceinline__ double rsqrt_f64(double d) {
+  double y = __builtin_amdgcn_rsq(d);
+#pragma unroll
+  for (int it = 0; it < 2; ++it) {
+    const double e = fma(-d * y, y, 1.0);
+    y = fma(0.5 * y, e, y);
+  }
+  return y;
+}
+
+// ---- Cholesky factor and inverse of one 64 x 64 block, in LDS ----------
+// Recursive halving down to 8 x 8 leaves: for a block [A11 .; A21 A22] of
+// size 2h,
+//   L11, X11 = chol / inverse of A11            (recursion)
+//   S = L21 = A21 X11^T                          (h x h x h)
+//   A22 -= S S^T,  T = S X11                     (together)
+//   L22, X22 = chol / inverse of A22            (recursion)
+//   X21 = -X22 T                                 (h x h x h)
+// The leaves are factored and inverted by every thread redundantly in
+// registers (no exchange on the serial chain); every product runs on MFMA in
+// 16 x 16 tiles dealt to the four waves (an 8 x 8 product is one masked tile).
+// A and X are row-major with pitch kQ; S and T are per-level scratch.
+constexpr int kQ = kT + 1;
+constexpr int kScr = 32 * 32 + 16 * 16 + 8 * 8;   // one scratch set of all levels
+
+// S_h / T_h for half size h (32, 16, 8) inside a scratch set
+__device__ __forceinline__ double* lvl(double* base, int h) {
+  return base + (h == 32 ? 0 : (h == 16 ? 32 * 32 : 32 * 32 + 16 * 16));
+}
+
+// One 16 x 16 tile of sum_k fa(r, k) fb(c, k), k < kd (kd a multiple of 4),
+// on the calling wave; fa, fb return the operand entries (0 outside).
+template <class FA, class FB>
+__device__ __forceinline__ d4 mma16(FA fa, FB fb, int kd) {
+  const int lane = threadIdx.x & 63, l16 = lane & 15, lk = lane >> 4;
+  d4 acc = d4{0.0, 0.0, 0.0, 0.0};
+  for (int k0 = 0; k0 < kd; k0 += 4) acc = mfma_f64(fa(l16, k0 + lk), fb(l16, k0 + lk), acc);
+  return acc;
+}
+
+// leaf: factor and invert the 8 x 8 diagonal block at o (updated in place)
+__device__ __forceinline__ void leaf8(double* A, double* X, int o, int nbk, int64_t k0,
+                                      int* status) {
+  double D[8][8], Xi[8][8], rs[8];
+#pragma unroll
+  for (int a = 0; a < 8; ++a)
+#pragma unroll
+    for (int b = 0; b <= a; ++b) D[a][b] = A[(o + a) * kQ + o + b];
+#pragma unroll
+  for (int a = 0; a < 8; ++a) {
+    const double d = D[a][a];
+    if (threadIdx.x == 0 && o + a < nbk && !(d > 0.0)) atomicMin(status, (int)(k0 + o + a));
+    rs[a] = rsqrt_f64(d);
+    D[a][a] = d * rs[a];
+#pragma unroll
+    for (int b = a + 1; b < 8; ++b) D[b][a] *= rs[a];
+#pragma unroll
+    for (int b = a + 1; b < 8; ++b)
+#pragma unroll
+      for (int c = a + 1; c <= b; ++c) D[b][c] -= D[b][a] * D[c][a];
+  }
+  // Xi = L^-1 by rows: Xi[a][c] = -(1 / L_aa) sum_{c <= k < a} L[a][k] Xi[k][c]
+#pragma unroll
+  for (int a = 0; a < 8; ++a) {
+    Xi[a][a] = rs[a];
+#pragma unroll
+    for (int c = 0; c < a; ++c) {
+      double v = 0.0;
+#pragma unroll
+      for (int k = c; k < a; ++k) v += D[a][k] * Xi[k][c];
+      Xi[a][c] = -rs[a] * v;
+    }
+  }
+  __syncthreads();   // every wave has read the block before it is overwritten
+  if (threadIdx.x == 0) {
+    // one lane stores the 36 + 36 values (the entries above the diagonal
+    // are zero already)
+#pragma unroll
+    for (int a = 0; a < 8; ++a)
+#pragma unroll
+      for (int c = 0; c <= a; ++c) {
+        A[(o + a) * kQ + o + c] = D[a][c];
+        X[(o + a) * kQ + o + c] = Xi[a][c];
+      }
+  }
+  __syncthreads();
+}
+
+// S = A21 X11^T, then A22 -= S S^T (lower), A21 <- S and T = S X11, for the
+// halves of size h of the block at o.
+template <int H>
+__device__ __forceinline__ void split_step(double* A, double* X, double* scr, int o) {
+  constexpr int nt16 = (H + 15) / 16;
+  double* const S = lvl(scr, H);
+  double* const Tm = lvl(scr + kScr, H);
+  const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  for (int t = w; t < nt16 * nt16; t += 4) {
+    const int R = t / nt16, C = t % nt16;
+    const d4 v = mma16(
+        [&](int r, int k) {
+          r += 16 * R;
+          return (r < H && k < H) ? A[(o + H + r) * kQ + o + k] : 0.0;
+        },
+        [&](int c, int k) {
+          c += 16 * C;
+          return (c < H && k < H) ? X[(o + c) * kQ + o + k] : 0.0;
+        },
+        H < 4 ? 4 : H);
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int r = 16 * R + 4 * q + (lane >> 4), c = 16 * C + (lane & 15);
+      if (r < H && c < H) S[r * H + c] = v[q];
+    }
+  }
+  __syncthreads();
+  // update tiles (lower) then T tiles, dealt to the waves together
+  constexpr int nu = nt16 * (nt16 + 1) / 2;
+  for (int t = w; t < nu + nt16 * nt16; t += 4) {
+    if (t < nu) {
+      int R = 0, C = t;
+      while (C > R) C -= ++R;   // t -> (R, C), C <= R
+      const d4 v = mma16(
+          [&](int r, int k) {
+            r += 16 * R;
+            return (r < H && k < H) ? S[r * H + k] : 0.0;
+          },
+          [&](int c, int k) {
+            c += 16 * C;
+            return (c < H && k < H) ? S[c * H + k] : 0.0;
+          },
+          H < 4 ? 4 : H);
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int r = 16 * R + 4 * q + (lane >> 4), c = 16 * C + (lane & 15);
+        if (r < H && c <= r) A[(o + H + r) * kQ + o + H + c] -= v[q];
+      }
+    } else {
+      const int tt = t - nu, R = tt / nt16, C = tt % nt16;
+      const d4 v = mma16(
+          [&](int r, int k) {
+            r += 16 * R;
+            return (r < H && k < H) ? S[r * H + k] : 0.0;
+          },
+          [&](int c, int k) {
+            c += 16 * C;
+            return (c < H && k < H) ? X[(o + k) * kQ + o + c] : 0.0;
+          },
+          H < 4 ? 4 : H);
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int r = 16 * R + 4 * q + (lane >> 4), c = 16 * C + (lane & 15);
+        if (r < H && c < H) Tm[r * H + c] = v[q];
+      }
+    }
+  }
+  for (int e = threadIdx.x; e < H * H; e += kThreads)
+    A[(o + H + e / H) * kQ + o + e % H] = S[e];
+  __syncthreads();
+}
+
+// X21 = -X22 T for the halves of size h of the block at o.
+template <int H>
+__device__ __forceinline__ void finish_inverse(double* X, double* scr, int o) {
+  constexpr int nt16 = (H + 15) / 16;
+  double* const Tm = lvl(scr + kScr, H);
+  const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  for (int t = w; t < nt16 * nt16; t += 4) {
+    const int R = t / nt16, C = t % nt16;
+    const d4 v = mma16(
+        [&](int r, int k) {
+          r += 16 * R;
+          return (r < H && k < H) ? X[(o + H + r) * kQ + o + H + k] : 0.0;
+        },
+        [&](int c, int k) {
+          c += 16 * C;
+          return (c < H && k < H) ? Tm[k * H + c] : 0.0;
+        },
+        H < 4 ? 4 : H);
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int r = 16 * R + 4 * q + (lane >> 4), c = 16 * C + (lane & 15);
+      if (r < H && c < H) X[(o + H + r) * kQ + o + c] = -v[q];
+    }
+  }
+  __syncthreads();
+}
+
+template <int N>
+__device__ __forceinline__ void chol_inv(double* A, double* X, double* scr, int o, int nbk,
+                                         int64_t k0, int* status) {
+  if constexpr (N == 8) {
+    leaf8(A, X, o, nbk, k0, status);
+  } else {
+    constexpr int H = N / 2;
+    chol_inv<H>(A, X, scr, o, nbk, k0, status);
+    split_step<H>(A, X, scr, o);
+    chol_inv<H>(A, X, scr, o + H, nbk, k0, status);
+    finish_inverse<H>(X, scr, o);
+  }
+}
+
+// Tile left-looking update with operand prefetch:
+//   acc -= sum_{k < kend} L_ik L_jk^T  (sym: i == j, B read from the A tile)
+//   acs -= sum_{k < kend} L_ik L_sk^T  (with_s: a second tile row s)
+// Step k + 1's operands are fetched into registers while step k's products
+// run; a step's flags are checked before its fetch.  Returns false if a wait
+// gave up.
+template <bool kSym, bool kWithS>
+__device__ __forceinline__ bool update_tiles(const DagArgs& a, double* lds, int i, int jrow,
+                                             int kend, d4 (&acc)[2][2], d4 (&acs)[2][2],
+                                             bool act, int* sOk) {
+  const int tid = threadIdx.x, w = tid >> 6;
+  const int qa = w >> 1, qb = w & 1;
+  const int64_t m = a.m;
+  int* const err = a.sync + 1;
+  int* const F = a.sync + 2;
+  double* const sA = lds;
+  double* const sB = lds + kTT;
+  const int brow = kWithS ? jrow : (kSym ? i : jrow);   // tile row of the second operand
+  auto ready = [&](int k) {
+    return wait_flag(F + tri(i, k), err) && (kSym && !kWithS ? true : wait_flag(F + tri(brow, k), err));
+  };
+  if (kend <= 0) return true;
+  double va[kPer], vb[kPer];
+  if (tid == 0) *sOk = ready(0);
+  __syncthreads();
+  if (!*sOk) return false;
+  fetch(va, a.H, m, (int64_t)kT * i, 0);
+  if (!kSym || kWithS) fetch(vb, a.H, m, (int64_t)kT * brow, 0);
+  for (int k = 0; k < kend; ++k) {
+    __syncthreads();   // the previous step's operand reads are done
+    put(sA, va, false);
+    if (!kSym || kWithS) put(sB, vb, false);
+    if (tid == 0 && k + 1 < kend) *sOk = ready(k + 1);
+    __syncthreads();
+    if (!*sOk) return false;
+    if (k + 1 < kend) {
+      fetch(va, a.H, m, (int64_t)kT * i, (int64_t)kT * (k + 1));
+      if (!kSym || kWithS) fetch(vb, a.H, m, (int64_t)kT * brow, (int64_t)kT * (k + 1));
+    }
+    if (act) tile_mma(acc, sA, kSym ? sA : sB, qa, qb, -1.0);
+    if (kWithS) tile_mma(acs, sA, sB, qa, qb, -1.0);
+  }
+  __syncthreads();   // operand reads done before LDS is reused
+  return true;
+}
+
+__device__ __forceinline__ void load_acc(d4 (&acc)[2][2], const double* src, int64_t m,
+                                         int64_t r0, int64_t c0) {
+  const int w = threadIdx.x >> 6, qa = w >> 1, qb = w & 1;
+#pragma unroll
+  for (int x = 0; x < 2; ++x)
+#pragma unroll
+    for (int y = 0; y < 2; ++y)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int64_t r = r0 + acc_row(qa, x, q), c = c0 + acc_col(qb, y);
+        acc[x][y][q] = (r < m && c < m) ? src[r * m + c] : 0.0;
+      }
+}
+
+__device__ __forceinline__ void acc_to_lds(const d4 (&acc)[2][2], double* s, bool transpose) {
+  const int w = threadIdx.x >> 6, qa = w >> 1, qb = w & 1;
+#pragma unroll
+  for (int x = 0; x < 2; ++x)
+#pragma unroll
+    for (int y = 0; y < 2; ++y)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int r = acc_row(qa, x, q), c = acc_col(qb, y);
+        s[transpose ? sw(c, r) : sw(r, c)] = acc[x][y][q];
+      }
+}
+
+// Off-diagonal factor tile (i, j), i > j + 1: L_ij = (H_ij - sum_{k<j} L_ik
+// L_jk^T) Linv_jj^T.  Returns false if a wait gave up.  (The three task
+// bodies are calls, each register-allocated on its own.)
+__device__ __noinline__ bool offdiag_task(const DagArgs& a, double* lds, int i, int j, int* sOk) {
+  const int tid = threadIdx.x, w = tid >> 6;
+  const int qa = w >> 1, qb = w & 1;
+  const int64_t m = a.m, r0 = (int64_t)kT * i, c0 = (int64_t)kT * j;
+  int* const err = a.sync + 1;
+  int* const F = a.sync + 2;
+  double* const sA = lds;
+  double* const sB = lds + kTT;
+  d4 acc[2][2], unused[2][2];
+  load_acc(acc, a.H, m, r0, c0);
+  if (!update_tiles<false, false>(a, lds, i, j, j, acc, unused, true, sOk)) return false;
+  // L_ij = T Linv_jj^T: T through LDS as the A operand, Linv_jj as B
+  if (tid == 0) *sOk = wait_flag(F + tri(j, j), err);
+  acc_to_lds(acc, sA, false);
+  __syncthreads();
+  if (!*sOk) return false;
+  stage(sB, a.Linv, m, c0, c0, false);
+  __syncthreads();
+  d4 out[2][2];
+#pragma unroll
+  for (int x = 0; x < 2; ++x)
+#pragma unroll
+    for (int y = 0; y < 2; ++y) out[x][y] = d4{0.0, 0.0, 0.0, 0.0};
+  tile_mma(out, sA, sB, qa, qb, 1.0);
+  store_acc(out, a.H, m, r0, c0, qa, qb);
+  zero_tile(a.H, m, c0, r0);   // the mirrored tile above the diagonal
+  publish(a.sync + 2 + tri(i, j));
+  return true;
+}
+
+// The tile (j, j-1) below a diagonal tile is on the path from one diagonal
+// tile to the next.  Its task only accumulates T = H_j,j-1 - sum_{k<j-1}
+// L_jk L_j-1,k^T and parks T (transposed) in the mirrored tile above the
+// diagonal, publishing it with its own flag; the diagonal task j finishes it
+// (T Linv_j-1,j-1^T) the moment the factor of tile j - 1 appears, and takes
+// its own last update from that product straight from LDS.  Returns false if
+// a wait gave up.
+__device__ __noinline__ bool sub_task(const DagArgs& a, double* lds, int j, int* sOk) {
+  const int64_t m = a.m, c0 = (int64_t)kT * j, p0 = c0 - kT;
+  d4 acc[2][2], unused[2][2];
+  load_acc(acc, a.H, m, c0, p0);
+  if (!update_tiles<false, false>(a, lds, j, j - 1, j - 1, acc, unused, true, sOk)) return false;
+  const int w = threadIdx.x >> 6, qa = w >> 1, qb = w & 1;
+#pragma unroll
+  for (int x = 0; x < 2; ++x)
+#pragma unroll
+    for (int y = 0; y < 2; ++y)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int64_t r = c0 + acc_row(qa, x, q), c = p0 + acc_col(qb, y);
+        if (r < m) a.H[c * m + r] = acc[x][y][q];
+      }
+  publish(a.sync + 2 + (int64_t)a.nt * (a.nt + 1) + j);
+  return true;
+}
+
+// Diagonal tile j: H_jj - sum_{k<j-1} L_jk L_jk^T; then (j > 0) L_j,j-1
+// from the parked T, its update, and L_jj = chol(.) with its inverse by
+// recursive halving.  Returns false if a wait gave up.
+__device__ __noinline__ bool diag_task(const DagArgs& a, double* lds, int j, int* sOk) {
+  const int tid = threadIdx.x, w = tid >> 6;
+  const int qa = w >> 1, qb = w & 1;
+  const int64_t m = a.m, c0 = (int64_t)kT * j, p0 = c0 - kT;
+  int* const err = a.sync + 1;
+  int* const F = a.sync + 2;
+  int* const Pf = a.sync + 2 + (int64_t)a.nt * (a.nt + 1);
+  double* const sA = lds;
+  double* const sB = lds + kTT;
+  const bool act = !(qa < qb);   // the quadrant above the diagonal is not needed
+  d4 acc[2][2], unused[2][2];
+  load_acc(acc, a.H, m, c0, c0);
+  if (j > 0) {
+    if (!update_tiles<true, false>(a, lds, j, j, j - 1, acc, unused, act, sOk)) return false;
+    // L_j,j-1 = T Linv_j-1,j-1^T
+    if (tid == 0) *sOk = wait_flag(Pf + j, err) && wait_flag(F + tri(j - 1, j - 1), err);
+    __syncthreads();
+    if (!*sOk) return false;
+    stage(sA, a.H, m, p0, c0, true);   // A(r, k) = T[r][k], parked at (p0 + k, c0 + r)
+    stage(sB, a.Linv, m, p0, p0, false);
+    __syncthreads();
+    d4 out[2][2];
+#pragma unroll
+    for (int x = 0; x < 2; ++x)
+#pragma unroll
+      for (int y = 0; y < 2; ++y) out[x][y] = d4{0.0, 0.0, 0.0, 0.0};
+    tile_mma(out, sA, sB, qa, qb, 1.0);
+    store_acc(out, a.H, m, c0, p0, qa, qb);
+    zero_tile(a.H, m, p0, c0);   // the parked T: the mirrored tile ends zero
+    __syncthreads();             // operand reads done
+    acc_to_lds(out, sA, false);
+    publish(F + tri(j, j - 1));  // its barrier also completes the LDS writes
+    if (act) tile_mma(acc, sA, sA, qa, qb, -1.0);
+    __syncthreads();
+  }
+  const int nbk = (int)((m - c0) < kT ? (m - c0) : kT);
+  double* const Ab = lds;                   // [64][kQ] the block, then L
+  double* const Xb = lds + kT * kQ;         // [64][kQ] L^-1
+  double* const scr = lds + 2 * kT * kQ;    // scratch of the recursive factor
+  // the updated block (lower triangle; the identity beyond nbk) and X = 0
+  if (act) {
+#pragma unroll
+    for (int x = 0; x < 2; ++x)
+#pragma unroll
+      for (int y = 0; y < 2; ++y)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const int r = acc_row(qa, x, q), c = acc_col(qb, y);
+          Ab[r * kQ + c] = (r < nbk && c < nbk) ? (r >= c ? acc[x][y][q] : 0.0)
+                                                : (r == c ? 1.0 : 0.0);
+        }
+  } else {
+    for (int e = tid - 64; e < 32 * 32; e += 64) Ab[(e >> 5) * kQ + 32 + (e & 31)] = 0.0;
+  }
+  for (int e = tid; e < kTT; e += kThreads) Xb[(e >> 6) * kQ + (e & 63)] = 0.0;
+  __syncthreads();
+  chol_inv<kT>(Ab, Xb, scr, 0, nbk, c0, a.status);
+  // the factor (zeros above the diagonal) and its inverse
+  for (int e = tid; e < kTT; e += kThreads) {
+    const int r = e >> 6, c = e & 63;
+    if (r < nbk && c < nbk) {
+      a.H[(c0 + r) * m + c0 + c] = (c <= r) ? Ab[r * kQ + c] : 0.0;
+      a.Linv[(c0 + r) * m + c0 + c] = (c <= r) ? Xb[r * kQ + c] : 0.0;
+    }
+  }
+  publish(F + tri(j, j));
+  return true;
+}
+
+// Inverse tile (i, j), i > j.
+__device__ __noinline__ bool inverse_task(const DagArgs& a, double* lds, int i, int j, int* sOk) {
+  const int tid = threadIdx.x, w = tid >> 6;
+  const int qa = w >> 1, qb = w & 1;
+  const int64_t m = a.m, nl = (int64_t)a.nt * (a.nt + 1) / 2;
+  int* const err = a.sync + 1;
+  int* const F = a.sync + 2;
+  int* const Gf = a.sync + 2 + nl;
+  double* const sA = lds;
+  double* const sB = lds + kTT;
+  d4 acc[2][2];
+#pragma unroll
+  for (int x = 0; x < 2; ++x)
+#pragma unroll
+    for (int y = 0; y < 2; ++y) acc[x][y] = d4{0.0, 0.0, 0.0, 0.0};
+  // X = sum_{k = j}^{i-1} L_ik Linv_kj: B(col, k') = Linv_kj[k'][col], staged
+  // transposed; step k + 1 fetched during step k's products
+  auto ready = [&](int k) {
+    return wait_flag(F + tri(i, k), err) &&
+           wait_flag(k == j ? F + tri(j, j) : Gf + tri(k, j), err);
+  };
+  double va[kPer], vb[kPer];
+  if (tid == 0) *sOk = ready(j);
+  __syncthreads();
+  if (!*sOk) return false;
+  fetch(va, a.H, m, (int64_t)kT * i, (int64_t)kT * j);
+  fetch(vb, a.Linv, m, (int64_t)kT * j, (int64_t)kT * j);
+  for (int k = j; k < i; ++k) {
+    __syncthreads();
+    put(sA, va, false);
+    put(sB, vb, true);
+    if (tid == 0 && k + 1 < i) *sOk = ready(k + 1);
+    __syncthreads();
+    if (!*sOk) return false;
+    if (k + 1 < i) {
+      fetch(va, a.H, m, (int64_t)kT * i, (int64_t)kT * (k + 1));
+      fetch(vb, a.Linv, m, (int64_t)kT * (k + 1), (int64_t)kT * j);
+    }
+    tile_mma(acc, sA, sB, qa, qb, 1.0);
+  }
+  // Linv_ij = -Linv_ii X: A = Linv_ii, B(col, k') = X[k'][col]
+  if (tid == 0) *sOk = wait_flag(F + tri(i, i), err);
+  __syncthreads();
+  if (!*sOk) return false;
+#pragma unroll
+  for (int x = 0; x < 2; ++x)
+#pragma unroll
+    for (int y = 0; y < 2; ++y)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) sB[sw(acc_col(qb, y), acc_row(qa, x, q))] = acc[x][y][q];
+  stage(sA, a.Linv, m, (int64_t)kT * i, (int64_t)kT * i, false);
+  __syncthreads();
+  d4 out[2][2];
+#pragma unroll
+  for (int x = 0; x < 2; ++x)
+#pragma unroll
+    for (int y = 0; y < 2; ++y) out[x][y] = d4{0.0, 0.0, 0.0, 0.0};
+  tile_mma(out, sA, sB, qa, qb, -1.0);
+  store_acc(out, a.Linv, m, (int64_t)kT * i, (int64_t)kT * j, qa, qb);
+  zero_tile(a.Linv, m, (int64_t)kT * j, (int64_t)kT * i);   // the mirrored tile above the diagonal
+  publish(Gf + tri(i, j));
+  return true;
+}
+
+__global__ __launch_bounds__(kThreads, 1) void chol_dag_kernel(DagArgs a) {
+  __shared__ __align__(16) double lds[kLdsDoubles];
+  __shared__ int sTask, sOk;
+  int* const counter = a.sync;
+  int* const err = a.sync + 1;
+  for (;;) {
+    if (threadIdx.x == 0) {
+      const bool stop = __hip_atomic_load(err, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0;
+      sTask = stop ? (int)a.ntasks : atomicAdd(counter, 1);
+    }
+    __syncthreads();
+    const int64_t t = sTask;
+    __syncthreads();   // sTask read by every thread before thread 0 can write it again
+    if (t >= a.ntasks) {
+      // a launch that gave up reports it through the pivot status (-1)
+      if (threadIdx.x == 0 &&
+          __hip_atomic_load(err, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0)
+        atomicMin(a.status, -1);
+      break;
+    }
+    const uint32_t code = a.tasks[t];
+    const int kind = (int)(code >> 30), i = (int)((code >> 15) & 0x7fffu),
+              j = (int)(code & 0x7fffu);
+    bool ok = true;
+    switch (kind) {
+      case kTaskDiag: ok = diag_task(a, lds, j, &sOk); break;
+      case kTaskSub: ok = sub_task(a, lds, i, &sOk); break;
+      case kTaskOff: ok = offdiag_task(a, lds, i, j, &sOk); break;
+      default: ok = inverse_task(a, lds, i, j, &sOk); break;
+    }
+    if (!ok) continue;
+    __syncthreads();
+  }
+}
+
+__global__ __launch_bounds__(256) void fill_int_kernel(int* __restrict__ p, int64_t count,
+                                                       int value) {
+  for (int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x; e < count;
+       e += (int64_t)gridDim.x * 256)
+    p[e] = value;
+}
+
+}  // namespace
+
+size_t chol_dag_sync_bytes(int64_t m) {
+  const int64_t nt = (m + kT - 1) / kT;
+  return (size_t)(2 + nt * (nt + 1) + nt) * sizeof(int);
+}
+
+// The task order.  A diagonal task j reads the tiles (j, k < j - 1), the
+// parked tile (j, j - 1) and the factor of tile j - 1; the parked tile reads
+// (j, k) and (j - 1, k) for k < j - 1, including (j - 1, j - 2), which the
+// diagonal task j - 1 forms.  So the pair for tile j + 2 can follow the tile
+// (j + 2, j), the first tile of column j it needs: column j's list starts
+// with (j + 2, j), the parked tile (j + 2, j + 1) and the diagonal task j + 2,
+// two columns ahead of where a plain column order would put them, so that the
+// diagonal chain, on which every other task waits, is never short of
+// workgroups.  Then the rest of column j, then the inverse tiles of row j.
+static void dag_tasks(int64_t m, int64_t inv_span, uint32_t* out, int64_t* count) {
+  const int64_t nt = (m + kT - 1) / kT;
+  const int64_t span = inv_span / kT;
+  int64_t n = 0;
+  auto put = [&](int kind, int64_t i, int64_t j) {
+    if (out) out[n] = ((uint32_t)kind << 30) | ((uint32_t)i << 15) | (uint32_t)j;
+    ++n;
+  };
+  put(kTaskDiag, 0, 0);
+  if (nt > 1) {
+    put(kTaskSub, 1, 0);
+    put(kTaskDiag, 1, 1);
+  }
+  for (int64_t g = 0; g < nt; ++g) {
+    if (g + 2 < nt) {
+      put(kTaskOff, g + 2, g);
+      put(kTaskSub, g + 2, g + 1);
+      put(kTaskDiag, g + 2, g + 2);
+    }
+    for (int64_t i = g + 3; i < nt; ++i) put(kTaskOff, i, g);
+    if (span > 0)
+      for (int64_t jj = 0; jj < g; ++jj)
+        if (g / span == jj / span) put(kTaskInv, g, jj);
+  }
+  *count = n;
+}
+
+int64_t chol_dag_task_count(int64_t m, int64_t inv_span) {
+  int64_t n = 0;
+  dag_tasks(m, inv_span, nullptr, &n);
+  return n;
+}
+
+void chol_dag_task_list(int64_t m, int64_t inv_span, uint32_t* out) {
+  int64_t n = 0;
+  dag_tasks(m, inv_span, out, &n);
+}
+
+hipError_t cholesky_dag(double* H, int64_t m, int* status, double* Linv, const uint32_t* tasks,
+                        int64_t ntasks, int* sync, int max_wgs, hipStream_t stream) {
+  if (m <= 0) return hipSuccess;
+  const int64_t nt = (m + kT - 1) / kT;
+  if (nt > 32767) return hipErrorInvalidValue;
+  const int64_t nsync = 2 + nt * (nt + 1) + nt;
+  const int64_t zb = (nsync + 255) / 256;
+  fill_int_kernel<<<dim3((unsigned)(zb < 4096 ? zb : 4096)), dim3(256), 0, stream>>>(sync, nsync,
+                                                                                     0);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  DagArgs a;
+  a.H = H;
+  a.Linv = Linv;
+  a.m = m;
+  a.nt = (int)nt;
+  a.tasks = tasks;
+  a.ntasks = ntasks;
+  a.status = status;
+  a.sync = sync;
+  const int64_t wgs = ntasks < max_wgs ? ntasks : (max_wgs > 0 ? max_wgs : 1);
+  chol_dag_kernel<<<dim3((unsigned)wgs), dim3(kThreads), 0, stream>>>(a);
+  return hipGetLastError();
+}
+
+}  // namespace ojbkq

@@ -1,14 +1,17 @@
-// Damping, blocked Cholesky and the explicit inverse of the factor in fp64
-// (Alg. 1 step 2, H = X~^T X~ + lambda^2 I = R^T R; the solves of step 3 are
-// products with L^-1, R^-1 = L^-T).
+// Damping, blocked Cholesky and the diagonal blocks of the factor's inverse in
+// fp64 (Alg. 1 step 2, H = X~^T X~ + lambda^2 I = R^T R; the solves of step 3
+// multiply by L^-1, R^-1 = L^-T), and the triangular solve that applies L^-T
+// to many right-hand sides.
 //
 // The factor is kept as L = R^T, lower triangular, row-major: row f of L is
 // column f of R, so the decoder's reads of R[i][f] over a block of rows i are
-// contiguous.  Right-looking blocked Cholesky with 64-wide steps (grouped
-// into 256-wide outer panels when m is large): one wave factors and inverts
-// each 64x64 diagonal block, the panel below it is one GEMM with that
-// inverse, and every trailing update is a call of the fp64 MFMA GEMM.  L^-1 is formed once per factor by doubling from the inverted
-// diagonal blocks.
+// contiguous.  This blocked factor serves layers beyond the size the
+// one-launch tiled factor (chol_dag.hip) takes: right-looking with 64-wide
+// steps grouped into 256-wide outer panels, one wave factoring and inverting
+// each 64x64 diagonal block, the panel below it one GEMM with that inverse,
+// every trailing update a call of the fp64 MFMA GEMM.  invert_lower merges
+// the inverted 64x64 blocks by doubling up to the block size the solves need
+// (all of L^-1, or the 128-wide blocks of trsm_right_lower_t).
 #include "kernels.h"
 #include "device.h"
 
@@ -295,10 +298,10 @@ hipError_t launch_upper_to_lower(const double* R, double* L, int64_t m, hipStrea
 //   [A 0; C D]^-1 = [A^-1 0; -D^-1 C A^-1  D^-1],
 // one batched GEMM for T = C A^-1 and one for -D^-1 T per level (plus one
 // pair of calls for a ragged last pair).  scratch holds m^2 / 4 doubles.
-hipError_t invert_lower(const double* L, int64_t m, double* Linv, double* scratch,
+hipError_t invert_lower(const double* L, int64_t m, double* Linv, double* scratch, int64_t block,
                         hipStream_t stream) {
   hipError_t e;
-  for (int64_t s = kNB; s < m; s *= 2) {
+  for (int64_t s = kNB; s < m && 2 * s <= (block < m ? block : 2 * m); s *= 2) {
     const int64_t pitch = 2 * s * m + 2 * s;   // from one pair to the next
     auto merge = [&](int64_t p0, int64_t pairs, int64_t dsize) -> hipError_t {
       const int64_t a0 = 2 * s * p0;           // first row / column of the pair
@@ -328,6 +331,42 @@ hipError_t invert_lower(const double* L, int64_t m, double* Linv, double* scratc
     if (a0 + s < m && (e = merge(full, 1, m - a0 - s)) != hipSuccess) return e;
   }
   return hipSuccess;
+}
+
+namespace {
+
+hipError_t trsm_rec(double* Y, int64_t ldy, int64_t N, const double* L, const double* Linv,
+                    int64_t m, int64_t a, int64_t b, hipStream_t stream) {
+  if (b - a <= kTrsmLeaf) {
+    // Y[:, a:b] <- Y[:, a:b] Linv_blk^T in place: at most 128 output columns,
+    // so each output tile reads its own rows of Y over the whole k range
+    // before it writes them, and no other tile reads those rows
+    GemmDesc g;
+    g.M = N; g.N = b - a; g.Kd = b - a;
+    g.A = Y + a; g.lda = ldy; g.ta = Elt::F64;
+    g.B = Linv + a * m + a; g.ldb = m; g.tb = Elt::F64; g.b_zero_above_col = true;
+    g.C = Y + a; g.ldc = ldy; g.alpha = 1.0; g.beta = 0.0;
+    return gemm_f64(g, stream);
+  }
+  const int64_t half = ((b - a) / 2 + kTrsmLeaf - 1) / kTrsmLeaf * kTrsmLeaf;
+  const int64_t mid = a + half;
+  hipError_t e = trsm_rec(Y, ldy, N, L, Linv, m, a, mid, stream);
+  if (e != hipSuccess) return e;
+  GemmDesc u;   // Y[:, mid:b] -= Z[:, a:mid] L[mid:b, a:mid]^T
+  u.M = N; u.N = b - mid; u.Kd = mid - a;
+  u.A = Y + a; u.lda = ldy; u.ta = Elt::F64;
+  u.B = L + mid * m + a; u.ldb = m; u.tb = Elt::F64;
+  u.C = Y + mid; u.ldc = ldy; u.alpha = -1.0; u.beta = 1.0;
+  if ((e = gemm_f64(u, stream)) != hipSuccess) return e;
+  return trsm_rec(Y, ldy, N, L, Linv, m, mid, b, stream);
+}
+
+}  // namespace
+
+hipError_t trsm_right_lower_t(double* Y, int64_t ldy, int64_t N, const double* L,
+                              const double* Linv, int64_t m, hipStream_t stream) {
+  if (N <= 0 || m <= 0) return hipSuccess;
+  return trsm_rec(Y, ldy, N, L, Linv, m, 0, m, stream);
 }
 
 }  // namespace ojbkq

@@ -102,11 +102,36 @@ hipError_t launch_damp(double* H, int64_t m, double lambda_rel, double* lam2_out
 hipError_t cholesky_lower(double* H, int64_t m, int* status, double* Linv, hipStream_t stream);
 // L = R^T for an upper-triangular R (row-major); strict upper part of L = 0.
 hipError_t launch_upper_to_lower(const double* R, double* L, int64_t m, hipStream_t stream);
-// Linv = L^-1 [m, m] (lower, strict upper part zero) for the lower factor L,
-// given Linv as cholesky_lower leaves it; scratch holds at least m^2 / 4
-// doubles.
-hipError_t invert_lower(const double* L, int64_t m, double* Linv, double* scratch,
+// The diagonal blocks of L^-1 of size `block` (aligned at multiples of it;
+// block >= m: Linv = L^-1 whole), lower with zeros above their diagonal,
+// for the lower factor L, given Linv as cholesky_lower leaves it; scratch
+// holds at least m^2 / 4 doubles.
+hipError_t invert_lower(const double* L, int64_t m, double* Linv, double* scratch, int64_t block,
                         hipStream_t stream);
+
+// The same factor in one persistent launch of 64x64 tile tasks (chol_dag.hip):
+// H = L L^T in place (strict upper part zeroed), *status as above (-1: the
+// launch gave up waiting for a tile), and in Linv the 64x64 diagonal blocks
+// of L^-1 plus, when inv_span > 0 (a multiple of 64), every 64x64 tile of
+// L^-1 inside the diagonal blocks of size inv_span (inv_span >= m: all of
+// L^-1), zero above the diagonal there.  tasks: a device copy of
+// chol_dag_task_list(m, inv_span) (chol_dag_task_count entries); sync:
+// chol_dag_sync_bytes(m) of device memory (cleared by the call); max_wgs:
+// workgroups to launch (one per CU is resident).
+size_t chol_dag_sync_bytes(int64_t m);
+int64_t chol_dag_task_count(int64_t m, int64_t inv_span);
+void chol_dag_task_list(int64_t m, int64_t inv_span, uint32_t* out);   // host-side
+hipError_t cholesky_dag(double* H, int64_t m, int* status, double* Linv, const uint32_t* tasks,
+                        int64_t ntasks, int* sync, int max_wgs, hipStream_t stream);
+
+// Y <- Y L^-T in place for Y [N, m] (row stride ldy): the solution Z of
+// Z L^T = Y by recursive halving (Z_1 = Y_1 L_11^-T, Y_2 -= Z_1 L_21^T,
+// Z_2 = Y_2 L_22^-T), the leaves of kTrsmLeaf columns multiplied by the
+// diagonal blocks of L^-1 of that size (invert_lower / cholesky_dag with
+// block or inv_span = kTrsmLeaf).  N m^2 multiply-adds in all.
+constexpr int64_t kTrsmLeaf = 128;
+hipError_t trsm_right_lower_t(double* Y, int64_t ldy, int64_t N, const double* L,
+                              const double* Linv, int64_t m, hipStream_t stream);
 
 // ---- relaxed solution -> centres (Alg. 1 steps 3-5) ------------------------
 // The decoder's input Rbar_j qbar_j = R (s_j qbar_j) = R (w_j + (1 - mu)

@@ -252,9 +252,78 @@ def test_heavy_tailed_layer_m1024(gram):
     assert frac >= 0.999
 
 
+def gq_error(gq, o, W, m, group):
+    """Largest error of the decoder's input rows Rbar_j qbar_j against the
+    oracle's, each entry relative to the size of the terms summed into it:
+    (|s qbar| + |w| + |s z|) |R^T| (the centre s qbar = w + s z + the
+    cross-term correction can cancel to almost nothing, as in a group of one
+    negative weight)."""
+    Sx = orc.expand_groups(o.scales, m, group)
+    Zx = orc.expand_groups(o.zeros, m, group)
+    scale = (np.abs(Sx * o.qbar) + np.abs(W) + np.abs(Sx * Zx)) @ np.abs(o.R.T)
+    return float(np.max(np.abs(gq - (Sx * o.qbar) @ o.R.T) / scale))
+
+
+@pytest.mark.parametrize("m,n,mu", [
+    (64, 40, 0.5),      # one tile; n > m / 2: the whole L^-1
+    (65, 20, 0.5),      # a ragged second tile of one row; n < m / 2: triangular solve
+    (127, 100, 0.0),
+    (191, 60, 0.5),     # three tiles, the last ragged; solve leaves of 128 and 63
+    (257, 200, 1.0),    # no cross term
+    (700, 120, 0.25),   # eleven tiles (ragged 60), six solve leaves
+    (700, 500, 0.5),
+])
+def test_factor_and_solve_routes(m, n, mu):
+    """The one-launch tiled factor and its inverse tiles (whole, or the
+    128-wide diagonal blocks the triangular solve multiplies by) against the
+    oracle's R and centres, on both routes to Rbar qbar."""
+    cfg = small_cfg(m, n, max(2 * m, 256), 4, 128, 2, 40 + m % 17)
+    W, Xr, Xq = make_layer(cfg, device=DEV)
+    s = ok.LayerSolver(cfg.m, cfg.n, cfg.bits, cfg.group, cfg.K, cfg.klein_seed, device=DEV)
+    s.accumulate(Xr, Xq)
+    g = s.solve(W, mu)
+    o = orc.quantize_layer(np64(W), np64(Xr), np64(Xq), mu, cfg.bits, cfg.group, cfg.K,
+                           cfg.klein_seed)
+    L = np64(s.inspect("L"))
+    assert np.all(np.triu(L, 1) == 0.0), "upper triangle of the factor not cleared"
+    colnorm = np.sqrt(np.sum(o.R ** 2, axis=0))
+    errR = float(np.max(np.abs(L.T - o.R) / colnorm[None, :]))
+    gq = np64(s.inspect("gq"))
+    errg = gq_error(gq, o, np64(W), cfg.m, cfg.group)
+    print(f"[factor m={m} n={n} mu={mu}] R err {errR:.2e}, Rbar qbar err {errg:.2e}")
+    assert errR < GRAM_RTOL["int8"], errR
+    assert errg < SOLVE_RTOL["int8"], errg
+    assert check_layer(cfg, g, o, mu, paths_of(s)) >= 0.999
+    s.close()
+
+
+def test_blocked_factor_beyond_tiled_range():
+    """m = 12300, above the size the one-launch tiled factor takes: the
+    blocked factor (64-wide steps in 256-wide outer panels, ragged last panel
+    of 12 columns), its 128-wide inverse blocks and the triangular solve."""
+    cfg = small_cfg(12300, 6, 1024, 4, 128, 2, 24)
+    W, Xr, Xq = make_layer(cfg, device=DEV)
+    s = ok.LayerSolver(cfg.m, cfg.n, cfg.bits, cfg.group, cfg.K, cfg.klein_seed, device=DEV)
+    s.accumulate(Xr, Xq)
+    g = s.solve(W, cfg.mu)
+    L = np64(s.inspect("L"))
+    gq = np64(s.inspect("gq"))
+    paths = paths_of(s)
+    s.close()
+    o = orc.quantize_layer(np64(W), np64(Xr), np64(Xq), cfg.mu, cfg.bits, cfg.group, cfg.K,
+                           cfg.klein_seed)
+    colnorm = np.sqrt(np.sum(o.R ** 2, axis=0))
+    errR = float(np.max(np.abs(L.T - o.R) / colnorm[None, :]))
+    errg = gq_error(gq, o, np64(W), cfg.m, cfg.group)
+    print(f"[t12300] R err {errR:.2e}, Rbar qbar err {errg:.2e}")
+    assert errR < GRAM_RTOL["int8"], errR
+    assert errg < SOLVE_RTOL["int8"], errg
+    assert check_layer(cfg, g, o, cfg.mu, paths) >= 0.999
+
+
 def test_wide_layer_two_level_factor():
-    """m = 6200: the factor runs in 256-wide outer panels (m >= 6144), with a
-    ragged last outer panel (56 columns) and a ragged last 64-wide step."""
+    """m = 6200 in the one-launch tiled factor: 97 tiles per side, the last
+    of 56 rows."""
     cfg = small_cfg(6200, 6, 8192, 4, 128, 2, 23)
     W, Xr, Xq = make_layer(cfg, device=DEV)
     s = ok.LayerSolver(cfg.m, cfg.n, cfg.bits, cfg.group, cfg.K, cfg.klein_seed, device=DEV)
