@@ -132,6 +132,20 @@ typedef struct {
                              term is formed from the exact fp64 difference;
                           1: float64 matrix cores on the widened fp32 values
                              (exact products, float64 sums).             */
+  int32_t decode_fp64; /* the decoder's lazy update of the centres by the
+                          decided rows (Alg. 1 steps 6-10):
+                          0: on the int8 matrix cores when bits <= 7, the
+                             scales are uniform within 32-row blocks (no
+                             static act-order groups) and the groups are
+                             whole 64-row pairs (group % 64 == 0 or one
+                             group): every row of R split into seven int8
+                             digits below its power-of-two maximum (49 bits,
+                             within 2^-49 of it), the codes themselves the
+                             other operand, digit pairs summed exactly in
+                             int32 per scale group and added in float64;
+                             otherwise as 1;
+                          1: float64 matrix cores on R and the scaled
+                             codes (exact products, float64 sums).       */
 } ojbkq_params;
 
 typedef struct ojbkq_ctx ojbkq_ctx;   /* opaque staged-solve state (host)     */

@@ -58,7 +58,7 @@ class Params(ctypes.Structure):
         ("group", ctypes.c_int32), ("K", ctypes.c_int32), ("scheme", ctypes.c_int32),
         ("alpha", ctypes.c_double), ("lambda_rel", ctypes.c_double), ("seed", ctypes.c_uint64),
         ("act_order", ctypes.c_int32), ("keep_gram", ctypes.c_int32),
-        ("gram_fp64", ctypes.c_int32),
+        ("gram_fp64", ctypes.c_int32), ("decode_fp64", ctypes.c_int32),
     ]
 
 
@@ -129,18 +129,21 @@ def _act_order(v) -> int:
     return ACT_ORDER[v]
 
 
-GRAMS = {"int8": 0, "fp64": 1}   # arithmetic of the token sums (ojbkq_params.gram_fp64)
+GRAMS = {"int8": 0, "fp64": 1}     # arithmetic of the token sums (ojbkq_params.gram_fp64)
+DECODES = {"int8": 0, "fp64": 1}   # the decoder's lazy update (ojbkq_params.decode_fp64)
 
 
 def _params(m, n, bits, group, K, alpha, lambda_rel, seed, scheme="asym",
-            act_order=False, keep_gram=False, gram="int8") -> Params:
+            act_order=False, keep_gram=False, gram="int8", decode="int8") -> Params:
     if scheme not in SCHEMES:
         raise ValueError(f"scheme must be one of {sorted(SCHEMES)}")
     if gram not in GRAMS:
         raise ValueError(f"gram must be one of {sorted(GRAMS)}")
+    if decode not in DECODES:
+        raise ValueError(f"decode must be one of {sorted(DECODES)}")
     return Params(int(m), int(n), int(bits), int(group), int(K), SCHEMES[scheme], float(alpha),
                   float(lambda_rel), int(seed) & 0xFFFFFFFFFFFFFFFF, _act_order(act_order),
-                  1 if keep_gram else 0, GRAMS[gram])
+                  1 if keep_gram else 0, GRAMS[gram], DECODES[decode])
 
 
 def _ptr(t: Optional[torch.Tensor]):
@@ -187,17 +190,17 @@ def num_groups(m: int, group: int) -> int:
 
 
 def workspace_bytes(m, n, bits, group, K, alpha=0.5, lambda_rel=0.01, seed=0,
-                    act_order=False, keep_gram=False, gram="int8") -> int:
+                    act_order=False, keep_gram=False, gram="int8", decode="int8") -> int:
     p = _params(m, n, bits, group, K, alpha, lambda_rel, seed, act_order=act_order,
-                keep_gram=keep_gram, gram=gram)
+                keep_gram=keep_gram, gram=gram, decode=decode)
     nb = library().ojbkq_workspace_bytes(ctypes.byref(p))
     if nb == 0:
         _check(-1)
     return int(nb)
 
 
-def decode_workspace_bytes(m, n, bits, group, K, seed=0) -> int:
-    p = _params(m, n, bits, group, K, 0.5, 0.0, seed)
+def decode_workspace_bytes(m, n, bits, group, K, seed=0, decode="int8") -> int:
+    p = _params(m, n, bits, group, K, 0.5, 0.0, seed, decode=decode)
     nb = library().ojbkq_decode_workspace_bytes(ctypes.byref(p))
     if nb == 0:
         _check(-1)
@@ -232,7 +235,7 @@ def _outputs(n, m, G, device, act_order=False):
 
 def quantize_layer(W, X_ref, X_q, alpha, bits, group, K, seed, lambda_rel=0.01,
                    workspace: Optional[torch.Tensor] = None, scheme="asym",
-                   act_order=False, gram="int8") -> QuantResult:
+                   act_order=False, gram="int8", decode="int8") -> QuantResult:
     """One-shot ``ojbkq_quantize_layer`` on device tensors.
 
     W [n, m] float32; X_ref, X_q [m, T] float32 (X_ref may be None or X_q);
@@ -240,7 +243,10 @@ def quantize_layer(W, X_ref, X_q, alpha, bits, group, K, seed, lambda_rel=0.01,
     act_order: decode the features with the largest Hessian diagonal first
     (codes stay in W's order, ``perm`` holds the decode order); True groups
     the scales by decode position, "static" keeps W's own groups;
-    gram: "int8" (digit products on the int8 matrix cores) or "fp64".
+    gram: "int8" (digit products on the int8 matrix cores) or "fp64";
+    decode: "int8" (the decoder's lazy update on the int8 matrix cores where
+    the codes have at most 7 bits and the scale groups are whole 64-row
+    pairs) or "fp64".
     """
     n, m = W.shape
     dev = W.device
@@ -253,7 +259,8 @@ def quantize_layer(W, X_ref, X_q, alpha, bits, group, K, seed, lambda_rel=0.01,
         _need(X_ref, "X_ref", torch.float32, device=dev)
         if tuple(X_ref.shape) != tuple(X_q.shape) or X_ref.stride() != X_q.stride():
             raise ValueError("X_ref must have the shape and strides of X_q")
-    p = _params(m, n, bits, group, K, alpha, lambda_rel, seed, scheme, act_order, gram=gram)
+    p = _params(m, n, bits, group, K, alpha, lambda_rel, seed, scheme, act_order, gram=gram,
+                decode=decode)
     lib = library()
     need = lib.ojbkq_workspace_bytes(ctypes.byref(p))
     if need == 0:
@@ -269,7 +276,7 @@ def quantize_layer(W, X_ref, X_q, alpha, bits, group, K, seed, lambda_rel=0.01,
 
 
 def quantize_layer_noalloc(W, X_ref, X_q, alpha, bits, group, K, seed, lambda_rel=0.01,
-                           scheme="asym", act_order=False, gram="int8",
+                           scheme="asym", act_order=False, gram="int8", decode="int8",
                            out: Optional[QuantResult] = None) -> QuantResult:
     """``ojbkq_quantize_layer_noalloc``: the one-shot call on the library's
     static scratch (no workspace).  ``out`` may pass preallocated outputs
@@ -285,7 +292,8 @@ def quantize_layer_noalloc(W, X_ref, X_q, alpha, bits, group, K, seed, lambda_re
         _need(X_ref, "X_ref", torch.float32, device=dev)
         if tuple(X_ref.shape) != tuple(X_q.shape) or X_ref.stride() != X_q.stride():
             raise ValueError("X_ref must have the shape and strides of X_q")
-    p = _params(m, n, bits, group, K, alpha, lambda_rel, seed, scheme, act_order, gram=gram)
+    p = _params(m, n, bits, group, K, alpha, lambda_rel, seed, scheme, act_order, gram=gram,
+                decode=decode)
     if out is None:
         out = _outputs(n, m, num_groups(m, group), dev, act_order)
     rc = library().ojbkq_quantize_layer_noalloc(
@@ -300,7 +308,7 @@ class LayerSolver:
 
     def __init__(self, m, n, bits, group, K, seed, lambda_rel=0.01, device="cuda",
                  workspace: Optional[torch.Tensor] = None, scheme="asym", act_order=False,
-                 keep_gram=False, gram="int8"):
+                 keep_gram=False, gram="int8", decode="int8"):
         self.m, self.n, self.bits, self.group, self.K = int(m), int(n), bits, group, K
         _act_order(act_order)
         self.act_order = act_order
@@ -309,7 +317,7 @@ class LayerSolver:
         if self.device.index is None:
             self.device = torch.device("cuda", torch.cuda.current_device())
         self.p = _params(m, n, bits, group, K, 0.5, lambda_rel, seed, scheme, act_order,
-                         keep_gram, gram)
+                         keep_gram, gram, decode)
         lib = library()
         need = lib.ojbkq_workspace_bytes(ctypes.byref(self.p))
         if need == 0:
@@ -403,7 +411,7 @@ class LayerSolver:
             pass
 
 
-def decode_stage(R, qbar, scales, bits, group, K, seed, want_paths=False):
+def decode_stage(R, qbar, scales, bits, group, K, seed, want_paths=False, decode="int8"):
     """``ojbkq_decode_stage``: decode + select on a given upper factor R (float64)."""
     m = R.shape[0]
     n = qbar.shape[0]
@@ -414,7 +422,7 @@ def decode_stage(R, qbar, scales, bits, group, K, seed, want_paths=False):
     for t, nm in ((R, "R"), (qbar, "qbar"), (scales, "scales")):
         if not t.is_contiguous():
             raise ValueError(f"{nm} must be contiguous")
-    p = _params(m, n, bits, group, K, 0.5, 0.0, seed)
+    p = _params(m, n, bits, group, K, 0.5, 0.0, seed, decode=decode)
     lib = library()
     need = lib.ojbkq_decode_workspace_bytes(ctypes.byref(p))
     if need == 0:

@@ -58,6 +58,7 @@ struct Shape {
   bool static_groups;   // act_order 2: scale groups stay runs of g features in W's order
   bool keep_gram;
   bool gram_i8;         // token sums on the int8 matrix cores (params.gram_fp64 == 0)
+  bool dec_i8;          // the decoder's lazy update on the int8 matrix cores
 };
 
 Shape shape_of(const ojbkq_params& p) {
@@ -69,13 +70,60 @@ Shape shape_of(const ojbkq_params& p) {
   s.K = p.K;
   s.paths = p.n * (int64_t)(p.K + 1);
   s.cus = device_cus();
-  s.geo = ojbkq::decode_geometry(p.n, p.K, s.cus);
   s.qmax = (1 << p.bits) - 1;
   s.act_order = p.act_order != 0;
   s.static_groups = p.act_order == 2 && s.G > 1;
   s.keep_gram = p.keep_gram != 0;
   s.gram_i8 = p.gram_fp64 == 0;
+  // codes that fit int8, one scale per 64-row pair of blocks
+  s.dec_i8 = p.decode_fp64 == 0 && p.bits <= 7 && !s.static_groups &&
+             (s.G == 1 || s.g % 64 == 0);
+  s.geo = ojbkq::decode_geometry(p.n, p.K, s.cus, s.dec_i8 ? 3 : 4);
   return s;
+}
+
+// The decoder's copy of the factor: every 32x32 tile in fp64, or (int8 lazy
+// update) the diagonal tiles, the row exponents and the digit tiles -- at
+// least 2 m^2 bytes, the scratch the doubling inverse of the blocked factor
+// borrows from this buffer before the tiles are written.
+struct DecodeParts {
+  size_t rexp = 0, R8 = 0, total = 0;
+};
+DecodeParts decode_parts(const Shape& s) {
+  DecodeParts d;
+  if (!s.dec_i8) {
+    d.total = (size_t)ojbkq::decode_tile_count(s.m) * ojbkq::kDecodeTile * sizeof(double);
+  } else {
+    const size_t nb = (size_t)((s.m + ojbkq::kDecodeBlock - 1) / ojbkq::kDecodeBlock);
+    d.rexp = align_up(nb * ojbkq::kDecodeTile * sizeof(double));
+    d.R8 = d.rexp + align_up((size_t)s.m * sizeof(int32_t));
+    d.total = d.R8 + (size_t)ojbkq::decode_digit_tile_count(s.m) * ojbkq::kDigitTileBytes;
+  }
+  const size_t scratch = (size_t)s.m * (size_t)s.m * 2;
+  if (d.total < scratch) d.total = scratch;
+  return d;
+}
+
+// The decoder's factor from L: the tiles, and the digits if the lazy update
+// runs on int8.
+int build_decoder_factor(const Shape& s, const double* Lf, char* F, hipStream_t st) {
+  const DecodeParts dp = decode_parts(s);
+  OJBKQ_HIP(ojbkq::launch_decode_tiles(Lf, s.m, reinterpret_cast<double*>(F), !s.dec_i8, st),
+            "decoder tiles");
+  if (s.dec_i8)
+    OJBKQ_HIP(ojbkq::launch_decode_digits(Lf, s.m, reinterpret_cast<int32_t*>(F + dp.rexp),
+                                          reinterpret_cast<uint8_t*>(F + dp.R8), st),
+              "decoder digits");
+  return OJBKQ_OK;
+}
+
+void set_decoder_factor(const Shape& s, char* F, ojbkq::DecodeDesc& d) {
+  d.F = reinterpret_cast<const double*>(F);
+  if (s.dec_i8) {
+    const DecodeParts dp = decode_parts(s);
+    d.rexp = reinterpret_cast<const int32_t*>(F + dp.rexp);
+    d.R8 = reinterpret_cast<const uint8_t*>(F + dp.R8);
+  }
 }
 
 // Rbar qbar = W Q + (S Z) Lsum with Q = L + (1 - mu) (L^-1 E)^T costs m^3/2
@@ -145,7 +193,7 @@ Layout layout_full(const Shape& s) {
   L.gc_scratch = take(s.gram_i8 ? ojbkq::gram_i8_scratch_bytes()
                                  : ojbkq::gram_cross_scratch_bytes());
   L.gc_tiles = take((size_t)ojbkq::gram_tile_count(s.m) * sizeof(uint32_t));
-  L.F = take((size_t)ojbkq::decode_tile_count(s.m) * ojbkq::kDecodeTile * sizeof(double));
+  L.F = take(decode_parts(s).total);
   L.Linv = take(mm);
   if (route_q(s))
     L.Q = take(mm);
@@ -196,7 +244,7 @@ Layout layout_decode(const Shape& s) {
   L.alpha = take((size_t)s.n * sizeof(double));
   L.pcodes = take((size_t)ojbkq::decode_code_bytes(s.m, s.geo));
   L.presid = take((size_t)s.paths * sizeof(double));
-  L.F = take((size_t)ojbkq::decode_tile_count(s.m) * ojbkq::kDecodeTile * sizeof(double));
+  L.F = take(decode_parts(s).total);
   L.total = off;
   return L;
 }
@@ -211,6 +259,8 @@ int check_params(const ojbkq_params* p) {
   if (p->scheme == 1 && p->bits < 2) return fail(OJBKQ_EINVAL, "the symmetric scheme needs bits >= 2");
   if (p->act_order < 0 || p->act_order > 2) return fail(OJBKQ_EINVAL, "act_order must be 0, 1 or 2");
   if (p->keep_gram != 0 && p->keep_gram != 1) return fail(OJBKQ_EINVAL, "keep_gram must be 0 or 1");
+  if (p->decode_fp64 != 0 && p->decode_fp64 != 1)
+    return fail(OJBKQ_EINVAL, "decode_fp64 must be 0 or 1");
   if (p->gram_fp64 != 0 && p->gram_fp64 != 1) return fail(OJBKQ_EINVAL, "gram_fp64 must be 0 or 1");
   if (!(p->alpha >= 0.0 && p->alpha <= 1.0)) return fail(OJBKQ_EINVAL, "alpha must be in [0, 1]");
   if (!(p->lambda_rel >= 0.0) || !std::isfinite(p->lambda_rel))
@@ -451,7 +501,7 @@ int ctx_set_knobs(ojbkq_ctx* c, double lambda_rel, int32_t K) {
   Shape t = c->s;
   t.K = K;
   t.paths = t.n * (int64_t)(K + 1);
-  t.geo = ojbkq::decode_geometry(t.n, K, t.cus);
+  t.geo = ojbkq::decode_geometry(t.n, K, t.cus, t.dec_i8 ? 3 : 4);
   if ((size_t)ojbkq::decode_code_bytes(t.m, t.geo) > c->pcodes_cap ||
       (size_t)t.paths * sizeof(double) > c->presid_cap)
     return fail(OJBKQ_EINVAL, "this K needs more decoder space than the context was created for");
@@ -561,7 +611,10 @@ int ctx_solve(ojbkq_ctx* c, const float* W, double alpha, uint8_t* codes, float*
                                     inv_block(s), st),
                 "factor inverse");
     }
-    OJBKQ_HIP(ojbkq::launch_decode_tiles(Lf, s.m, c->at<double>(c->L.F), st), "decoder tiles");
+    {
+      const int rc = build_decoder_factor(s, Lf, c->at<char>(c->L.F), st);
+      if (rc) return rc;
+    }
     OJBKQ_HIP(ojbkq::launch_group_row_sums(Lf, s.m, s.g, s.G,
                                            s.static_groups ? c->at<int32_t>(c->L.invperm) : nullptr,
                                            c->at<double>(c->L.Lsum), st),
@@ -657,7 +710,8 @@ int ctx_solve(ojbkq_ctx* c, const float* W, double alpha, uint8_t* codes, float*
             "klein alpha");
   stage_end(c, OJBKQ_STAGE_CENTRES, t0);
   ojbkq::DecodeDesc d;
-  d.F = c->at<double>(c->L.F); d.gq = gq; d.S = scales; d.alpha = al; d.gidx = gidx;
+  set_decoder_factor(s, c->at<char>(c->L.F), d);
+  d.gq = gq; d.S = scales; d.alpha = al; d.gidx = gidx;
   if (gidx) {   // each row's scale in the decoder's segment order
     d.spos = c->at<float>(c->L.spos);
     OJBKQ_HIP(ojbkq::launch_position_scales(scales, gidx, s.n, s.m, s.G, c->at<float>(c->L.spos),
@@ -914,10 +968,11 @@ int ojbkq_decode_stage(const ojbkq_params* p, const double* R, const double* qba
   OJBKQ_HIP(ojbkq::launch_klein_alpha(Lf, scales, s.n, s.m, s.g, s.G, nullptr, log_rho(s.m, s.K),
                                       al, st),
             "klein alpha");
-  OJBKQ_HIP(ojbkq::launch_decode_tiles(Lf, s.m, reinterpret_cast<double*>(ws + L.F), st),
-            "decoder tiles");
+  rc = build_decoder_factor(s, Lf, ws + L.F, st);
+  if (rc) return rc;
   ojbkq::DecodeDesc d;
-  d.F = reinterpret_cast<double*>(ws + L.F); d.gq = gq; d.S = scales; d.alpha = al;
+  set_decoder_factor(s, ws + L.F, d);
+  d.gq = gq; d.S = scales; d.alpha = al;
   d.m = s.m; d.n = s.n; d.g = s.g; d.G = s.G; d.K = (int)s.K; d.bits = p->bits; d.seed = p->seed;
   d.wg_paths = s.geo.wg_paths; d.threads = s.geo.threads; d.nwg = s.geo.nwg;
   d.pcodes = reinterpret_cast<uint8_t*>(ws + L.pcodes);

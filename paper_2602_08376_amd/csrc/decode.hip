@@ -214,9 +214,147 @@ __device__ __forceinline__ void lazy_update(const DecodeDesc& d, int64_t nb, int
   }
 }
 
+typedef int v4i __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ v4i mfma_i8(v4i a, v4i b, v4i c) {
+  return __builtin_amdgcn_mfma_i32_16x16x64_i8(a, b, c, 0, 0, 0);
+}
+
+// The lazy update of block b on the int8 matrix cores (uniform scales, codes
+// of at most 7 bits): acc += R[block b][later blocks] E, with E = s q and
+// R in seven int8 digits per row (launch_decode_digits).  Per 64-row pair
+// of blocks, one k = 64 product per digit and row half takes the decided
+// codes themselves as the B operand (each lane's 16 bytes of a 32-byte code
+// segment).  The pairs go in units of U (2, or 1 when the scale groups are
+// single pairs) inside one scale group; per unit and digit pair e, digits 2e
+// and 2e + 1 accumulate exactly in int32 (|sum| < 64 * 127 * 128 < 2^21) and
+// are combined exactly as 128 a_2e + a_2e+1 (< 2^28), then added in fp64
+// scaled by s 2^(-13 - 14 e).  The accumulator works in units of 2^rexp of
+// its row meanwhile (an exact rescaling), so the flush needs no per-row
+// exponent.  Operands stream one step ahead: the next step's digits while
+// the current step's products run, the next unit's codes as soon as the last
+// products of a pair have read its current ones.
+template <int NT>
+__device__ __forceinline__ void lazy_update_i8(const DecodeDesc& d, int64_t nb, int64_t b,
+                                               const uint8_t* cw, const uint32_t (&so)[NT],
+                                               d4 (&acc)[2][NT], int lane) {
+  const int64_t nb2 = (nb + 1) / 2;
+  const int64_t c0 = (b + 1) / 2;
+  if (c0 >= nb2) return;
+  // into units of 2^rexp of this lane's rows 32 b + 16 a + lane / 16 + 4 r
+#pragma unroll
+  for (int a = 0; a < 2; ++a)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int64_t row = b * kBS + 16 * a + (lane >> 4) + 4 * r;
+      const int e = row < d.m ? d.rexp[row] : 0;
+#pragma unroll
+      for (int t = 0; t < NT; ++t) acc[a][t][r] = ldexp(acc[a][t][r], -e);
+    }
+  const int U = (d.G == 1 || d.g % 128 == 0) ? 2 : 1;   // pairs per unit
+  const uint8_t* const tbase =
+      d.R8 + decode_digit_tile(nb2, b, c0) * kDigitTileBytes + 16 * lane;
+  // this lane's 16 code bytes of pair c for tile t: block 2c + lane / 32,
+  // path 16 t + lane % 16, bytes 16 ((lane / 16) % 2) ..
+  const uint8_t* const cb =
+      cw + (lane >> 5) * kBlockCodes + (lane & 15) * kSeg + 16 * ((lane >> 4) & 1);
+  auto load_a = [&](int64_t c, int e, v4i (&A)[4]) {
+    const uint8_t* tp = tbase + (c - c0) * kDigitTileBytes + (4 * e) * 1024;
+    A[0] = *reinterpret_cast<const v4i*>(tp);            // digit 2e, half 0
+    A[1] = *reinterpret_cast<const v4i*>(tp + 1024);     // digit 2e, half 1
+    if (2 * e + 1 < kDecodeDigits) {
+      A[2] = *reinterpret_cast<const v4i*>(tp + 2048);   // digit 2e + 1, half 0
+      A[3] = *reinterpret_cast<const v4i*>(tp + 3072);   // digit 2e + 1, half 1
+    } else {
+      A[2] = v4i{0, 0, 0, 0};
+      A[3] = v4i{0, 0, 0, 0};
+    }
+  };
+  auto load_b = [&](int64_t c, v4i (&Bq)[NT]) {
+#pragma unroll
+    for (int t = 0; t < NT; ++t)
+      Bq[t] = *reinterpret_cast<const v4i*>(cb + 2 * c * kBlockCodes + t * 16 * kSeg);
+  };
+  constexpr int kE = (kDecodeDigits + 1) / 2;   // digit pairs
+  v4i Bq[2][NT], An[4];
+  int64_t u = c0 / U * U;
+  {
+    const int64_t pb = u + U < nb2 ? u + U : nb2;
+    for (int64_t c = c0; c < pb; ++c) load_b(c, Bq[c - u]);
+  }
+  load_a(c0, 0, An);
+  for (; u < nb2; u += U) {
+    const int64_t pa = u > c0 ? u : c0, pb = u + U < nb2 ? u + U : nb2;
+    const uint32_t grp = d.G == 1 ? 0u : (uint32_t)((64 * u) / d.g);
+#pragma unroll 1
+    for (int e = 0; e < kE; ++e) {
+      v4i a1[2][NT], a2[2][NT];
+#pragma unroll
+      for (int h = 0; h < 2; ++h)
+#pragma unroll
+        for (int t = 0; t < NT; ++t) {
+          a1[h][t] = v4i{0, 0, 0, 0};
+          a2[h][t] = v4i{0, 0, 0, 0};
+        }
+#pragma unroll
+      for (int slot = 0; slot < 2; ++slot) {   // the unit's pairs c = u + slot in [pa, pb)
+        const int64_t c = u + slot;
+        if (c < pa || c >= pb) continue;
+        v4i A[4] = {An[0], An[1], An[2], An[3]};
+        // the next step's digits
+        if (c + 1 < pb)
+          load_a(c + 1, e, An);
+        else if (e + 1 < kE)
+          load_a(pa, e + 1, An);
+        else if (pb < nb2)
+          load_a(pb, 0, An);
+#pragma unroll
+        for (int h = 0; h < 2; ++h)
+#pragma unroll
+          for (int t = 0; t < NT; ++t) {
+            a1[h][t] = mfma_i8(A[h], Bq[slot][t], a1[h][t]);
+            if (2 * e + 1 < kDecodeDigits) a2[h][t] = mfma_i8(A[2 + h], Bq[slot][t], a2[h][t]);
+          }
+        // the next unit's codes, once these products have read the current ones
+        if (e + 1 == kE && pb < nb2) {
+          const int64_t cn = pb + slot;
+          if (cn < nb2 && cn < pb + U) load_b(cn, Bq[slot]);
+        }
+      }
+#pragma unroll
+      for (int t = 0; t < NT; ++t) {
+        const double mult = ldexp((double)load_scale(d.S + (so[t] + grp)), -13 - 14 * e);
+#pragma unroll
+        for (int h = 0; h < 2; ++h)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const int v = a1[h][t][r] * 128 + a2[h][t][r];
+            acc[h][t][r] = fma(mult, (double)v, acc[h][t][r]);
+          }
+      }
+    }
+    // a slot this unit did not use (a first unit that starts at its second
+    // pair) takes the next unit's codes now
+#pragma unroll
+    for (int slot = 0; slot < 2; ++slot) {
+      const int64_t c = u + slot, cn = u + U + slot;
+      if (slot < U && (c < pa || c >= pb) && cn < nb2) load_b(cn, Bq[slot]);
+    }
+  }
+#pragma unroll
+  for (int a = 0; a < 2; ++a)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int64_t row = b * kBS + 16 * a + (lane >> 4) + 4 * r;
+      const int e = row < d.m ? d.rexp[row] : 0;
+#pragma unroll
+      for (int t = 0; t < NT; ++t) acc[a][t][r] = ldexp(acc[a][t][r], e);
+    }
+}
+
 // One wave's share of the decode: paths pbase .. pbase + npw - 1 (npw <= 64,
 // in NT = ceil(npw / 16) tiles), codes at cw, LDS buffer sZ of kWaveLds bytes.
-template <int NT, bool kUniS>
+template <int NT, bool kUniS, bool kI8>
 __device__ __forceinline__ void decode_wave(const DecodeDesc& d, int64_t pbase, int npw,
                                             uint8_t* cw, double* sZ) {
   const int lane = threadIdx.x & 63;
@@ -277,7 +415,11 @@ __device__ __forceinline__ void decode_wave(const DecodeDesc& d, int64_t pbase, 
           acc[a][t][r] = (row < bl) ? -gb[row] : 0.0;
         }
     }
-    if (b + 1 < nb) lazy_update<NT, kUniS>(d, nb, b, cw, so, sp, acc, lane);
+    if constexpr (kI8) {
+      if (b + 1 < nb) lazy_update_i8<NT>(d, nb, b, cw, so, acc, lane);
+    } else {
+      if (b + 1 < nb) lazy_update<NT, kUniS>(d, nb, b, cw, so, sp, acc, lane);
+    }
     wave_sync();   // the diagonal tile is in LDS
 
     // ---- serial steps, one path per lane, in groups of four rows from the
@@ -360,7 +502,7 @@ __device__ __forceinline__ void decode_wave(const DecodeDesc& d, int64_t pbase, 
   if (valid) d.presid[p] = resid;
 }
 
-template <bool kUniS>
+template <bool kUniS, bool kI8>
 __global__ __launch_bounds__(kDecodeMaxThreads) void decode_kernel(DecodeDesc d) {
   extern __shared__ __align__(16) double lds[];
   const int wave = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
@@ -374,13 +516,19 @@ __global__ __launch_bounds__(kDecodeMaxThreads) void decode_kernel(DecodeDesc d)
   if (pbase >= pend) return;   // waves never synchronise, so idle ones may leave
   const int npw = (int)(pend - pbase);
   const int64_t nb = (d.m + kBS - 1) / kBS;
-  uint8_t* cw = d.pcodes + ((int64_t)blockIdx.x * waves + wave) * nb * kBlockCodes;
+  uint8_t* cw =
+      d.pcodes + ((int64_t)blockIdx.x * waves + wave) * decode_code_blocks(d.m) * kBlockCodes;
   double* sZ = lds + wave * (kWaveLds / (int)sizeof(double));
   switch ((npw + 15) / 16) {
-    case 1: decode_wave<1, kUniS>(d, pbase, npw, cw, sZ); break;
-    case 2: decode_wave<2, kUniS>(d, pbase, npw, cw, sZ); break;
-    case 3: decode_wave<3, kUniS>(d, pbase, npw, cw, sZ); break;
-    default: decode_wave<4, kUniS>(d, pbase, npw, cw, sZ); break;
+    case 1: decode_wave<1, kUniS, kI8>(d, pbase, npw, cw, sZ); break;
+    case 2: decode_wave<2, kUniS, kI8>(d, pbase, npw, cw, sZ); break;
+    case 3: decode_wave<3, kUniS, kI8>(d, pbase, npw, cw, sZ); break;
+    default:   // the int8 update's geometry gives a wave at most three tiles
+      if constexpr (kI8)
+        decode_wave<3, kUniS, kI8>(d, pbase, npw, cw, sZ);
+      else
+        decode_wave<4, kUniS, kI8>(d, pbase, npw, cw, sZ);
+      break;
   }
 }
 
@@ -423,7 +571,7 @@ __global__ __launch_bounds__(256) void select_kernel(const uint8_t* __restrict__
     const int loc = (int)(ps % wg_paths);
     const int w = decode_tile_wave(tiles, waves, loc / 16);
     const int lane = loc - 16 * decode_wave_tiles(tiles, waves, w).first;
-    return pcodes + ((wg * waves + w) * nb * 64 + lane) * kSeg;
+    return pcodes + ((wg * waves + w) * decode_code_blocks(m) * 64 + lane) * kSeg;
   };
   if (codes) {
     const uint8_t* src = path_base(j * kp1 + kstar);
@@ -448,13 +596,13 @@ __global__ __launch_bounds__(256) void select_kernel(const uint8_t* __restrict__
 // decode_tile_count): blockIdx.y = row block b; x runs over the diagonal
 // tile of b followed by the off-diagonal tiles bb = b+1 .. nb-1.
 __global__ __launch_bounds__(256) void decode_tiles_kernel(const double* __restrict__ L, int64_t m,
-                                                           double* __restrict__ F) {
+                                                           double* __restrict__ F, bool all_tiles) {
   const int64_t nb = (m + kBS - 1) / kBS;
   const int64_t b = blockIdx.y;
   const int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x;
   const int64_t tile = e / kDecodeTile;   // 0: diagonal, 1..: bb = b + tile
   const int idx = (int)(e % kDecodeTile);
-  if (tile >= nb - b) return;
+  if (tile >= (all_tiles ? nb - b : 1)) return;
   if (tile == 0) {
     const int r = idx / kBS, c = idx % kBS;
     const int64_t row = b * kBS + r;
@@ -470,11 +618,112 @@ __global__ __launch_bounds__(256) void decode_tiles_kernel(const double* __restr
 
 }  // namespace
 
-hipError_t launch_decode_tiles(const double* L, int64_t m, double* F, hipStream_t stream) {
+hipError_t launch_decode_tiles(const double* L, int64_t m, double* F, bool all_tiles,
+                               hipStream_t stream) {
   const int64_t nb = (m + kBS - 1) / kBS;
   if (nb > 65535) return hipErrorInvalidValue;
-  const int64_t bx = (nb * kDecodeTile + 255) / 256;
-  decode_tiles_kernel<<<dim3((unsigned)bx, (unsigned)nb), dim3(256), 0, stream>>>(L, m, F);
+  const int64_t bx = ((all_tiles ? nb : 1) * kDecodeTile + 255) / 256;
+  decode_tiles_kernel<<<dim3((unsigned)bx, (unsigned)nb), dim3(256), 0, stream>>>(L, m, F,
+                                                                                   all_tiles);
+  return hipGetLastError();
+}
+
+// rexp[i]: the exponent e with max_{l >= 32 (i / 32 + 1)} |R_il| < 2^e (0 for
+// an empty or zero row); R_il = L[l][i], read down a column of L, so the 256
+// threads of a workgroup (256 consecutive rows i) read consecutive addresses.
+// blockIdx.y takes one 512-column slice of l; the slices meet in an atomic
+// max over rexp, which starts at kNoExp.
+constexpr int kNoExp = -100000;
+constexpr int kExpSlice = 512;
+__global__ __launch_bounds__(256) void row_exponent_kernel(const double* __restrict__ L,
+                                                          int64_t m, int32_t* __restrict__ rexp) {
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i >= m) return;
+  const int64_t lo0 = (i / kBS + 1) * kBS, s0 = (int64_t)blockIdx.y * kExpSlice;
+  const int64_t lo = lo0 > s0 ? lo0 : s0;
+  const int64_t hi = s0 + kExpSlice < m ? s0 + kExpSlice : m;
+  double mx = 0.0;
+  for (int64_t l = lo; l < hi; ++l) mx = fmax(mx, fabs(L[l * m + i]));
+  if (mx > 0.0) {
+    int e = 0;
+    frexp(mx, &e);
+    atomicMax(rexp + i, e);
+  }
+}
+
+__global__ __launch_bounds__(256) void exp_fill_kernel(int32_t* __restrict__ rexp, int64_t m,
+                                                       int32_t v) {
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i < m) rexp[i] = v;
+}
+
+// rows with no nonzero entry (still kNoExp) get exponent 0
+__global__ __launch_bounds__(256) void exp_fix_kernel(int32_t* __restrict__ rexp, int64_t m) {
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i < m && rexp[i] == kNoExp) rexp[i] = 0;
+}
+
+// Digit tiles (layout with decode_digit_tile): blockIdx.y = row block b,
+// thread (x) = (pair offset, half, lane); each thread forms its lane's 16
+// entries and writes their seven digits, 16 bytes per plane.
+__global__ __launch_bounds__(256) void digit_tiles_kernel(const double* __restrict__ L, int64_t m,
+                                                          const int32_t* __restrict__ rexp,
+                                                          uint8_t* __restrict__ R8) {
+  const int64_t nb = (m + kBS - 1) / kBS, nb2 = (nb + 1) / 2;
+  const int64_t b = blockIdx.y;
+  const int64_t c0 = (b + 1) / 2;
+  const int64_t gid = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  const int64_t c = c0 + gid / 128;
+  if (c >= nb2) return;
+  const int h = (int)((gid / 64) % 2), lane = (int)(gid % 64);
+  const int rho = lane & 15;
+  const int64_t i = b * kBS + 16 * h + rho / 4 + 4 * (rho % 4);   // row of R
+  const int e = i < m ? rexp[i] : 0;
+  uint32_t words[kDecodeDigits][4];
+#pragma unroll
+  for (int dg = 0; dg < kDecodeDigits; ++dg)
+#pragma unroll
+    for (int w = 0; w < 4; ++w) words[dg][w] = 0u;
+#pragma unroll
+  for (int j = 0; j < 16; ++j) {
+    const int k = 16 * (lane >> 4) + j;
+    const int64_t blk = 2 * c + k / 32;
+    const int beta = k % 32;
+    const int64_t l = blk * kBS + 4 * (beta % 8) + beta / 8;   // column of R
+    const double v = (i < m && l < m && blk > b) ? L[l * m + i] : 0.0;
+    double r = ldexp(v, -e);   // |r| < 1
+    double scale = 64.0;
+#pragma unroll
+    for (int dg = 0; dg < kDecodeDigits; ++dg) {
+      const double t = r * scale;   // exact: a power-of-two scaling
+      const double a = rint(t);
+      r = t - a;                    // exact: |r| <= 1/2
+      scale = 128.0;
+      words[dg][j / 4] |= ((uint32_t)(int)a & 0xffu) << (8 * (j % 4));
+    }
+  }
+  uint8_t* out = R8 + decode_digit_tile(nb2, b, c) * kDigitTileBytes + 16 * lane;
+#pragma unroll
+  for (int dg = 0; dg < kDecodeDigits; ++dg)
+    *reinterpret_cast<uint4*>(out + (dg * 2 + h) * 1024) =
+        make_uint4(words[dg][0], words[dg][1], words[dg][2], words[dg][3]);
+}
+
+hipError_t launch_decode_digits(const double* L, int64_t m, int32_t* rexp, uint8_t* R8,
+                                hipStream_t stream) {
+  const int64_t nb = (m + kBS - 1) / kBS, nb2 = (nb + 1) / 2;
+  if (nb > 65535) return hipErrorInvalidValue;
+  const unsigned rx = (unsigned)((m + 255) / 256);
+  exp_fill_kernel<<<dim3(rx), dim3(256), 0, stream>>>(rexp, m, kNoExp);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  row_exponent_kernel<<<dim3(rx, (unsigned)((m + kExpSlice - 1) / kExpSlice)), dim3(256), 0,
+                        stream>>>(L, m, rexp);
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  exp_fix_kernel<<<dim3(rx), dim3(256), 0, stream>>>(rexp, m);
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  const int64_t bx = (nb2 * 128 + 255) / 256;
+  digit_tiles_kernel<<<dim3((unsigned)bx, (unsigned)nb), dim3(256), 0, stream>>>(L, m, rexp, R8);
   return hipGetLastError();
 }
 
@@ -519,14 +768,22 @@ hipError_t launch_decode(const DecodeDesc& d, hipStream_t stream) {
   geo.nwg = d.nwg;
   const size_t lds = (size_t)(d.threads / 64) * kWaveLds;
   const bool uniform_scale = !d.gidx && !d.spos && (d.G == 1 || d.g % kBS == 0);
-  const void* fn = uniform_scale ? reinterpret_cast<const void*>(&decode_kernel<true>)
-                                 : reinterpret_cast<const void*>(&decode_kernel<false>);
+  const bool i8 = d.R8 != nullptr;
+  if (i8 && (!d.rexp || d.gidx || d.spos || d.bits > 7 || (d.G != 1 && d.g % 64 != 0) ||
+             d.wg_paths > 3 * 16 * (int64_t)(d.threads / 64)))
+    return hipErrorInvalidValue;
+  const void* fn = i8 ? reinterpret_cast<const void*>(&decode_kernel<true, true>)
+                      : uniform_scale ? reinterpret_cast<const void*>(&decode_kernel<true, false>)
+                                      : reinterpret_cast<const void*>(&decode_kernel<false, false>);
   hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
   if (e != hipSuccess) return e;
-  if (uniform_scale)
-    decode_kernel<true><<<dim3((unsigned)geo.nwg), dim3(geo.threads), lds, stream>>>(d);
+  const dim3 grid((unsigned)geo.nwg), block(geo.threads);
+  if (i8)
+    decode_kernel<true, true><<<grid, block, lds, stream>>>(d);
+  else if (uniform_scale)
+    decode_kernel<true, false><<<grid, block, lds, stream>>>(d);
   else
-    decode_kernel<false><<<dim3((unsigned)geo.nwg), dim3(geo.threads), lds, stream>>>(d);
+    decode_kernel<false, false><<<grid, block, lds, stream>>>(d);
   return hipGetLastError();
 }
 

@@ -178,16 +178,19 @@ struct DecodeGeom {
   int64_t nwg = 0;        // workgroups
 };
 
-// `cus`: compute units of the device the decoder runs on (<= 0: kDecodeCUs).
-inline DecodeGeom decode_geometry(int64_t n, int K, int cus) {
+// `cus`: compute units of the device the decoder runs on (<= 0: kDecodeCUs);
+// `wave_tiles`: 16-path tiles a wave may hold (4, or 3 for the int8 lazy
+// update, whose int32 accumulators need the registers of the fourth).
+inline DecodeGeom decode_geometry(int64_t n, int K, int cus, int wave_tiles = 4) {
   const int64_t P = n * (int64_t)(K + 1);
   const int64_t units = cus > 0 ? cus : kDecodeCUs;
+  const int64_t max_per = (int64_t)kDecodeMaxWaves * wave_tiles * 16;
   int64_t per = 16;
   for (int64_t rounds = 1;; ++rounds) {
     const int64_t slots = units * rounds;
     per = (P + slots - 1) / slots;
     per = (per + 15) / 16 * 16;
-    if (per <= kDecodeMaxThreads) break;
+    if (per <= max_per) break;
   }
   if (per < 16) per = 16;
   DecodeGeom g;
@@ -218,11 +221,17 @@ __host__ __device__ inline int decode_tile_wave(int tiles, int waves, int tile) 
   return tile < split ? tile / (base + 1) : extra + (tile - split) / base;
 }
 
+// Row blocks of candidate codes per wave: ceil(m / 32) rounded up to even, so
+// that the int8 lazy update can read whole 64-row pairs (the padding block is
+// never written and only ever meets zero digits).
+__host__ __device__ inline int64_t decode_code_blocks(int64_t m) {
+  const int64_t nb = (m + kDecodeBlock - 1) / kDecodeBlock;
+  return (nb + 1) / 2 * 2;
+}
 // Bytes of candidate codes the decoder writes: per wave, one 32-byte segment
 // per (row block, lane) -- [wave][block][lane][32].
 inline int64_t decode_code_bytes(int64_t m, const DecodeGeom& g) {
-  const int64_t nb = (m + kDecodeBlock - 1) / kDecodeBlock;
-  return g.nwg * (int64_t)g.threads * nb * kDecodeBlock;
+  return g.nwg * (int64_t)g.threads * decode_code_blocks(m) * kDecodeBlock;
 }
 
 // The factor re-laid-out for the decoder, built from L = R^T (lower,
@@ -239,7 +248,36 @@ __host__ __device__ inline int64_t decode_tile_count(int64_t m) {
 __host__ __device__ inline int64_t decode_offdiag_tile(int64_t nb, int64_t b, int64_t bb) {
   return nb + b * (nb - 1) - b * (b - 1) / 2 + (bb - b - 1);
 }
-hipError_t launch_decode_tiles(const double* L, int64_t m, double* F, hipStream_t stream);
+// all_tiles false: only the diagonal tiles (the int8 lazy update reads the
+// digit tiles below instead of the off-diagonal ones).
+hipError_t launch_decode_tiles(const double* L, int64_t m, double* F, bool all_tiles,
+                               hipStream_t stream);
+
+// The int8 form of the factor for the decoder's lazy update (codes of at
+// most 7 bits, one scale per 64-row pair of blocks).  Row i of R, over the
+// columns of the later blocks (l >= 32 (i / 32 + 1)), is written as seven
+// int8 digits below its power-of-two maximum 2^rexp[i]:
+//   R_il = 2^(rexp[i] - 6) sum_{d<7} a_d 128^-d + r,  |a_d| <= 64,
+//   |r| <= 2^(rexp[i] - 49)
+// (each digit the rounded remainder after the one before).  Digit tile
+// (b, c), for row block b and each 64-column pair c >= (b + 1) / 2 of blocks
+// (2c, 2c + 1) (columns of blocks <= b zero), is 7 x 2 planes (digit d, row
+// half h) of 1 KB in v_mfma_i32_16x16x64_i8 A-operand order: lane L holds
+// bytes 16 L .. 16 L + 15, MFMA row rho = L % 16 = row 32 b + 16 h +
+// rho / 4 + 4 (rho % 4) of R (so that a lane's int32 results line up with
+// the rows of its fp64 accumulators), k = 16 (L / 16) + j = column
+// 32 (2c + k / 32) + 4 (k % 8) + (k % 32) / 8 (the code-segment byte order).
+constexpr int kDecodeDigits = 7;
+constexpr int kDigitTileBytes = kDecodeDigits * 2 * 1024;
+__host__ __device__ inline int64_t decode_digit_tile(int64_t nb2, int64_t b, int64_t c) {
+  return b * nb2 - (b * b) / 4 + (c - (b + 1) / 2);
+}
+__host__ __device__ inline int64_t decode_digit_tile_count(int64_t m) {
+  const int64_t nb = (m + kDecodeBlock - 1) / kDecodeBlock, nb2 = (nb + 1) / 2;
+  return nb * nb2 - (nb * nb) / 4;
+}
+hipError_t launch_decode_digits(const double* L, int64_t m, int32_t* rexp, uint8_t* R8,
+                                hipStream_t stream);
 
 struct DecodeDesc {
   const double* F = nullptr;   // decode_tile_count(m) tiles of kDecodeTile doubles
@@ -258,6 +296,11 @@ struct DecodeDesc {
   int64_t nwg = 0;
   uint8_t* pcodes = nullptr;   // decode_code_bytes(m, geometry) candidate codes
   double* presid = nullptr;    // [n (K + 1)] candidate residuals
+  // int8 lazy update (both set, with bits <= 7, no gidx / spos and G == 1 or
+  // g % 64 == 0): launch_decode_digits' output; F then needs only its
+  // diagonal tiles
+  const uint8_t* R8 = nullptr;
+  const int32_t* rexp = nullptr;
 };
 
 hipError_t launch_decode(const DecodeDesc& d, hipStream_t stream);

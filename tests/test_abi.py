@@ -69,6 +69,16 @@ def test_gram_mode_values():
     assert i8 - f64 >= 64 * 4096 ** 2 - 64 * 2 ** 20
 
 
+def test_decode_mode_values():
+    lib = ok.library()
+    for v, good in ((0, True), (1, True), (2, False), (-1, False)):
+        p = _p()
+        p.decode_fp64 = v
+        assert (lib.ojbkq_workspace_bytes(ctypes.byref(p)) > 0) == good, v
+    with pytest.raises(ValueError):
+        ok._params(128, 64, 4, 128, 4, 0.5, 0.01, 0, decode="fp32")
+
+
 def test_scheme_values():
     lib = ok.library()
     for scheme, bits, ok_ in ((0, 4, True), (1, 4, True), (1, 2, True), (1, 1, False),

@@ -164,25 +164,31 @@ def test_exact_residual_tie_keeps_babai(golden):
 # the decoder alone, on the oracle's own factor and centres
 # ---------------------------------------------------------------------------
 
+@pytest.mark.parametrize("decode", ["int8", "fp64"])
 @pytest.mark.parametrize("m,n,bits,group,K,seed", [
     (7, 5, 2, 128, 6, 1),          # tiny, one partial block
-    (100, 23, 3, 40, 9, 2),        # ragged groups and blocks, several workgroups
+    (100, 23, 3, 40, 9, 2),        # ragged groups and blocks, several workgroups (int8: not
+                                   # whole 64-row pairs, so the fp64 update runs)
     (257, 40, 4, 128, 16, 3),      # > 256 paths, 9 blocks, 3 groups (ragged)
     (64, 300, 4, 0, 0, 4),         # Babai only, 2 workgroups
-    (96, 11, 8, 32, 3, 5),         # 8-bit box (256 values)
+    (96, 11, 8, 32, 3, 5),         # 8-bit box (256 values): the fp64 update
+    (990, 17, 7, 64, 5, 6),        # 7-bit box (int8 codes up to 127), one pair per group,
+                                   # 31 blocks (the code segments padded to 32)
+    (1100, 9, 4, 256, 4, 7),       # four pairs per group, ragged last group and block
+    (2900, 3, 3, 0, 2, 8),         # one group: scale flushes every 32 pairs
 ])
-def test_decode_stage_matches_oracle(m, n, bits, group, K, seed):
+def test_decode_stage_matches_oracle(m, n, bits, group, K, seed, decode):
     R, qbar, S = make_triangular_problem(m, n, orc.num_groups(m, group), seed)
-    if bits == 8:
-        qbar = qbar * 16.0
+    if bits >= 7:
+        qbar = qbar * (2.0 ** (bits - 4))
     Rn, qn, Sn = R.numpy(), qbar.numpy(), S.numpy()
     codes, res, win, pc, pr = ok.decode_stage(R.to(DEV), qbar.to(DEV), S.to(DEV), bits, group, K,
-                                              seed, want_paths=True)
+                                              seed, want_paths=True, decode=decode)
     dec = orc.decode(Rn, qn, Sn, bits, group, K, seed)
     frac, ties = check_paths(Rn, qn, Sn, group, bits, K, seed, dec.alpha, np64(pc),
                              dec.path_codes)
     rel = np.abs(np64(pr) - dec.path_resid) / np.abs(dec.path_resid)
-    print(f"[decode m={m} n={n} b={bits} K={K}] agreement {frac:.6f} ties {ties} "
+    print(f"[decode {decode} m={m} n={n} b={bits} K={K}] agreement {frac:.6f} ties {ties} "
           f"max path resid rel err {rel.max():.2e}")
     assert rel.max() <= 1e-9
     assert np.array_equal(np64(win), dec.winner)
