@@ -660,8 +660,11 @@ def main():
                    "mean_residual": float(out.residuals.double().mean())},
     }
     if args.copy_calibration:
-        a = torch.empty(1 << 28, dtype=torch.float32, device=dev)
+        # a written source (a never-written one can read back nothing from
+        # HBM), then one plain copy of it
+        a = torch.empty(1 << 28, dtype=torch.float32, device=dev).uniform_()
         b = torch.empty_like(a)
+        torch.cuda.synchronize()
         b.copy_(a)
         torch.cuda.synchronize()
         result["copy_calibration_bytes"] = a.numel() * 4

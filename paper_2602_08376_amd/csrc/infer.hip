@@ -7,8 +7,10 @@
 //   pack_codes_kernel      codes [n, m] uint8 -> per-row little-endian bit
 //                          streams of `bits`-bit fields in 32-bit words
 //   dequant_matmul_kernel  Y [n, T] fp32 = W_hat [n, m] X [m, T] with X in
-//                          fp16, W_hat dequantized from the packed codes to
-//                          fp16 in LDS, products on v_mfma_f32_16x16x32_f16
+//                          fp16 staged in its own [k][t] layout and read
+//                          k-major by gfx950's transposing LDS read, W_hat
+//                          dequantized from the packed codes to fp16 in
+//                          LDS, products on v_mfma_f32_16x16x32_f16
 #include "kernels.h"
 
 namespace ojbkq {
@@ -110,18 +112,36 @@ struct CodeLoader {
 
 constexpr int kThreads = 512;  // eight waves: 2 x 4 blocks of 64 channels x 64 tokens
 
-// Offset (in halves) of the 16-byte block `blk` (features 8 blk .. 8 blk + 7
-// of the step) in row `row` of the activation tile: blocks are XOR-swizzled
-// by row / 4, so the eight lanes that stage rows 4 L + i (L = 0..7) of one
-// block write eight different bank groups.
-__device__ __forceinline__ int bswz(int row, int blk) { return 8 * (blk ^ ((row >> 2) & 7)); }
+// The activation tile in LDS keeps X's own layout, row k (a feature) with
+// the tile's 256 tokens contiguous, stored as 16-byte runs with no repacking;
+// pitch kLdB halves (544 bytes: rows k and k + 1 start 8 banks apart).  Its
+// 16-token blocks are XOR-swizzled by bit 3 of k, so the 8 rows that half a
+// wave reads in one transposing read (rows 8g .. 8g + 3 for lane groups
+// g = 0, 1, or 2, 3) fall in 64 distinct banks.  Offset (halves) of token t
+// of row k:
+constexpr int kLdB = kTileT + 16;
+__device__ __forceinline__ int xoff(int k, int t) {
+  return k * kLdB + 16 * ((t >> 4) ^ (4 * ((k >> 3) & 1))) + (t & 15);
+}
+
+typedef short s4 __attribute__((ext_vector_type(4)));
+
+// Four features of one token for an MFMA B operand, straight from the
+// activation tile with gfx950's transposing LDS read: lane i of each group of
+// 16 points at row k0 + i / 4, tokens t0 + 4 (i % 4) .. + 3 (t0 a multiple of
+// 16), and receives rows k0 .. k0 + 3 of token t0 + i.
+__device__ __forceinline__ s4 read_tr(const _Float16* B, int k0, int t0, int i) {
+  const _Float16* p = B + xoff(k0 + (i >> 2), t0 + 4 * (i & 3));
+  return __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+      (s4 __attribute__((address_space(3)))*)(const_cast<_Float16*>(p)));
+}
 
 template <int BITS, bool VEC>
 __global__ __launch_bounds__(kThreads, 1) void dequant_matmul_kernel(DqArgs a) {
   // two buffers: the waves dequantize and stage step s + 1 into one while
   // their MFMAs read step s from the other, with one barrier per step
-  __shared__ __align__(16) _Float16 sA[2][kTileJ * kLd];   // W_hat tile: row j, k contiguous
-  __shared__ __align__(16) _Float16 sB[2][kTileT * kLd];   // X tile transposed: row t, k contiguous
+  __shared__ __align__(16) _Float16 sA[2][kTileJ * kLd];      // W_hat tile: row j, k contiguous
+  __shared__ __align__(16) _Float16 sB[2][kStage * kLdB];     // X tile: row k, tokens contiguous
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wr = wave >> 2, wc = wave & 3;
   // consecutive workgroups take the channel tiles of one token tile, which
@@ -132,128 +152,89 @@ __global__ __launch_bounds__(kThreads, 1) void dequant_matmul_kernel(DqArgs a) {
   // A loader: thread -> (row tid / 4, codes 16 (tid % 4) .. + 15 of the stage).
   const int ar = tid >> 2, ac = tid & 3;
   const int64_t aj = J0 + ar;
-  // B loader: thread -> (tokens 4 (tid % 64) .. + 3, k rows 8 (tid / 64) ..
-  // + 7 of the stage): one 8-byte load per k row (a wave covers the tile's
-  // 256 tokens of a row), repacked in registers into k-contiguous runs.
-  const int bq = lane, bk = wave;
-  const int64_t btok = T0 + 4 * bq;
   // The stage is interior when its 64 features and the tile's rows and
   // tokens all exist (the same for every lane): no clamping or masking then.
   const bool tile_in = J0 + kTileJ <= a.n && T0 + kTileT <= a.T;
+  auto interior = [&](int64_t k0) { return VEC && tile_in && k0 + kStage <= a.m; };
 
   // this thread's channel row of the scales and zero points
   const float* const sz_row[2] = {a.S + (aj < a.n ? aj : a.n - 1) * a.G,
                                   a.Z + (aj < a.n ? aj : a.n - 1) * a.G};
 
+  // What the dequantization of one stage reads: this thread's 16 codes and
+  // their group's scale and zero point, loaded a stage ahead.
   CodeLoader<BITS> cl;
-  uint2 xv[8];           // VEC interior stages: 4 tokens of each of 8 k rows
   float s_cur = 0.f, z_cur = 0.f;
-  bool stage_in = false;   // of the stage in flight
-  int64_t kf = 0;
-  // With a permutation, the X rows of the stage the next fetch() loads, read
-  // one stage ahead so that no X address waits on a perm load.
-  int32_t prow[8];
-  auto load_rows = [&](int64_t k0) {
-    if (a.perm) {
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        const int64_t k = k0 + 8 * bk + e;
-        prow[e] = a.perm[k < a.m ? k : a.m - 1];
-      }
-    }
-  };
-  auto fetch = [&](int64_t k0) {
-    kf = k0;
-    stage_in = VEC && tile_in && k0 + kStage <= a.m;
+  auto fetch_codes = [&](int64_t k0) {
     const int64_t kc = k0 + 16 * ac;
     cl.load(a, aj, kc);
     // m < 2^20: the group index in 32-bit arithmetic
     const uint32_t grp = (uint32_t)(kc < a.m ? kc : a.m - 1) / (uint32_t)a.g;
     s_cur = sz_row[0][grp];
     z_cur = sz_row[1][grp];
-    if (stage_in) {
-      if (a.perm) {
-        const uint16_t* base = a.X + btok;
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          const int64_t r = prow[e] < 0 ? 0 : (prow[e] >= a.m ? a.m - 1 : prow[e]);
-          xv[e] = *reinterpret_cast<const uint2*>(base + r * a.ldx);
-        }
-      } else {
-        // rows k0 + 8 bk .. + 7: one pointer, rows ldx apart
-        const uint16_t* base = a.X + btok + (k0 + 8 * bk) * a.ldx;
-#pragma unroll
-        for (int e = 0; e < 8; ++e) xv[e] = *reinterpret_cast<const uint2*>(base + e * a.ldx);
-      }
-    }
-    load_rows(k0 + kStage);
   };
-  // write the fetched stage (features kf .. kf + 63) into buffer `buf`
-  auto stage = [&](int buf) {
-    _Float16* A = sA[buf];
-    _Float16* B = sB[buf];
-    // W_hat = fp16(fp32(s (q - z))), zero past the last feature or channel.
-    // Two roundings: the empty asm pins the float32 product in a register,
-    // so it is not folded into v_fma_mixlo_f16, which rounds once to fp16.
-    // q - z in fp32 (exact for the integer zero points a quantize call
-    // gives; a fractional z is honoured as the float it is).
-    if (stage_in) {   // interior: no masks
+  // an interior stage of X: thread -> tokens 8 (tid % 32) .. + 7 of rows
+  // tid / 32 + 16 q, q = 0..3, one 16-byte load each, held in registers (a
+  // vector, not an array: an array captured by these lambdas is moved to
+  // LDS) while the products run, then stored
+  const int bc = tid & 31, br = tid >> 5;
+  typedef uint32_t Runs __attribute__((ext_vector_type(16)));
+  Runs xv;
+  auto fetch_x = [&](int64_t k0) {
 #pragma unroll
-      for (int h = 0; h < 2; ++h) {
-        h8 v;
-#pragma unroll
-        for (int c = 0; c < 8; ++c) {
-          float p = s_cur * ((float)cl.code(8 * h + c) - z_cur);
-          __asm__("" : "+v"(p));
-          v[c] = (_Float16)p;
-        }
-        *reinterpret_cast<h8*>(A + ar * kLd + 16 * ac + 8 * h) = v;
-      }
-    } else {
-#pragma unroll
-      for (int h = 0; h < 2; ++h) {
-        h8 v;
-#pragma unroll
-        for (int c = 0; c < 8; ++c) {
-          const int cc = 8 * h + c;
-          float p = s_cur * ((float)cl.code(cc) - z_cur);
-          __asm__("" : "+v"(p));
-          const _Float16 w = (_Float16)p;
-          v[c] = (aj < a.n && kf + 16 * ac + cc < a.m) ? w : (_Float16)0.f;
-        }
-        *reinterpret_cast<h8*>(A + ar * kLd + 16 * ac + 8 * h) = v;
-      }
+    for (int q = 0; q < 4; ++q) {
+      const uint4 v = *reinterpret_cast<const uint4*>(a.X + x_row(a, k0 + br + 16 * q) * a.ldx +
+                                                      T0 + 8 * bc);
+      xv[4 * q] = v.x;
+      xv[4 * q + 1] = v.y;
+      xv[4 * q + 2] = v.z;
+      xv[4 * q + 3] = v.w;
     }
-    if (stage_in) {
-      // token i of k rows 8 bk + 2 p, + 1 -> one 32-bit word of row
-      // (btok + i): a 16-byte run of 8 features
+  };
+  auto store_x = [&](_Float16* B) {
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        uint32_t wv[4];
+    for (int q = 0; q < 4; ++q)
+      *reinterpret_cast<uint4*>(B + xoff(br + 16 * q, 8 * bc)) =
+          make_uint4(xv[4 * q], xv[4 * q + 1], xv[4 * q + 2], xv[4 * q + 3]);
+  };
+  // an edge stage of X, element by element, zero past the last feature or token
+  auto stage_x_edge = [&](int64_t k0, _Float16* B) {
 #pragma unroll
-        for (int p = 0; p < 4; ++p) {
-          const uint32_t lo = (i < 2 ? xv[2 * p].x : xv[2 * p].y) >> (16 * (i & 1));
-          const uint32_t hi = (i < 2 ? xv[2 * p + 1].x : xv[2 * p + 1].y) >> (16 * (i & 1));
-          wv[p] = (lo & 0xffffu) | (hi << 16);
-        }
-        *reinterpret_cast<uint4*>(B + (4 * bq + i) * kLd + bswz(4 * bq + i, bk)) =
-            make_uint4(wv[0], wv[1], wv[2], wv[3]);
+    for (int q = 0; q < 4; ++q) {
+      const int r = br + 16 * q;
+      const int64_t k = k0 + r;
+      h8 u;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const int64_t t = T0 + 8 * bc + e;
+        uint16_t b = 0;
+        if (t < a.T && k < a.m) b = a.X[x_row(a, k) * a.ldx + t];
+        u[e] = __builtin_bit_cast(_Float16, b);
       }
-    } else {
-      // edge stage: element by element, zero past the last feature or token
+      *reinterpret_cast<h8*>(B + xoff(r, 8 * bc)) = u;
+    }
+  };
+  // W_hat = fp16(fp32(s (q - z))) of the fetched codes into buffer `buf`,
+  // zero past the last feature or channel.  Two roundings: the empty asm pins
+  // the float32 product in a register, so it is not folded into
+  // v_fma_mixlo_f16, which rounds once to fp16.  q - z in fp32 (exact for the
+  // integer zero points a quantize call gives; a fractional z is honoured as
+  // the float it is).
+  auto dequant = [&](int64_t k0, int buf) {
+    _Float16* A = sA[buf];
+    const bool in = VEC && tile_in && k0 + kStage <= a.m;
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int64_t t = btok + i;
-        h8 u;
+    for (int h = 0; h < 2; ++h) {
+      h8 v;
 #pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          const int64_t k = kf + 8 * bk + e;
-          uint16_t b = 0;
-          if (t < a.T && k < a.m) b = a.X[x_row(a, k) * a.ldx + t];
-          u[e] = __builtin_bit_cast(_Float16, b);
-        }
-        *reinterpret_cast<h8*>(B + (4 * bq + i) * kLd + bswz(4 * bq + i, bk)) = u;
+      for (int c = 0; c < 8; ++c) {
+        const int cc = 8 * h + c;
+        float p = s_cur * ((float)cl.code(cc) - z_cur);
+        __asm__("" : "+v"(p));
+        const _Float16 w = (_Float16)p;
+        v[c] = (in || (aj < a.n && k0 + 16 * ac + cc < a.m)) ? w : (_Float16)0.f;
       }
+      *reinterpret_cast<h8*>(A + ar * kLd + 16 * ac + 8 * h) = v;
     }
   };
 
@@ -263,28 +244,24 @@ __global__ __launch_bounds__(kThreads, 1) void dequant_matmul_kernel(DqArgs a) {
 #pragma unroll
     for (int y = 0; y < 4; ++y) acc[x][y] = f4{0.f, 0.f, 0.f, 0.f};
 
-  const int64_t nst = (a.m + kStage - 1) / kStage;
-  load_rows(0);
-  fetch(0);
-  stage(0);
-  __syncthreads();
-  for (int64_t st = 0; st < nst; ++st) {
-    const int cur = (int)(st & 1);
-    const bool more = st + 1 < nst;
-    if (more) fetch((st + 1) * kStage);
-    const _Float16* A = sA[cur];
-    const _Float16* B = sB[cur];
+  const int g16 = lane >> 4, i16 = lane & 15;
+  // the products of the stage in buffer `buf`
+  auto compute = [&](int buf) {
+    const _Float16* A = sA[buf];
+    const _Float16* B = sB[buf];
 #pragma unroll
     for (int ks = 0; ks < 2; ++ks) {
       h8 fa[4], fb[4];
 #pragma unroll
       for (int x = 0; x < 4; ++x)
-        fa[x] = *reinterpret_cast<const h8*>(A + (wr * 64 + x * 16 + (lane & 15)) * kLd +
-                                             32 * ks + 8 * (lane >> 4));
+        fa[x] = *reinterpret_cast<const h8*>(A + (wr * 64 + x * 16 + i16) * kLd + 32 * ks +
+                                             8 * g16);
 #pragma unroll
       for (int y = 0; y < 4; ++y) {
-        const int row = wc * 64 + y * 16 + (lane & 15);
-        fb[y] = *reinterpret_cast<const h8*>(B + row * kLd + bswz(row, 4 * ks + (lane >> 4)));
+        // features 32 ks + 8 g16 .. + 7 of token wc 64 + 16 y + i16
+        const int k0 = 32 * ks + 8 * g16, t0 = wc * 64 + y * 16;
+        const s4 lo = read_tr(B, k0, t0, i16), hi = read_tr(B, k0 + 4, t0, i16);
+        fb[y] = __builtin_bit_cast(h8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
       }
 #pragma unroll
       for (int x = 0; x < 4; ++x)
@@ -292,9 +269,38 @@ __global__ __launch_bounds__(kThreads, 1) void dequant_matmul_kernel(DqArgs a) {
         for (int y = 0; y < 4; ++y)
           acc[x][y] = __builtin_amdgcn_mfma_f32_16x16x32_f16(fa[x], fb[y], acc[x][y], 0, 0, 0);
     }
-    // the other buffer was last read in step st - 1, before the barrier
-    // that ended it
-    if (more) stage(cur ^ 1);
+  };
+
+  // Stage st computes from buffer st % 2 while the codes and activations of
+  // stage st + 1 stream in (the activations straight into the other buffer)
+  // and are dequantized into it after the products.
+  const int64_t nst = (a.m + kStage - 1) / kStage;
+  fetch_codes(0);
+  if (interior(0)) {
+    fetch_x(0);
+    store_x(sB[0]);
+  } else {
+    stage_x_edge(0, sB[0]);
+  }
+  dequant(0, 0);
+  __syncthreads();
+  for (int64_t st = 0; st < nst; ++st) {
+    const int cur = (int)(st & 1), nxt = cur ^ 1;
+    const int64_t kn = (st + 1) * kStage;
+    const bool more = st + 1 < nst;
+    if (more) {
+      fetch_codes(kn);
+      if (interior(kn)) fetch_x(kn);
+    }
+    compute(cur);
+    // buffer nxt was last read in step st - 1, before the barrier that ended it
+    if (more) {
+      if (interior(kn))
+        store_x(sB[nxt]);
+      else
+        stage_x_edge(kn, sB[nxt]);
+      dequant(kn, nxt);
+    }
     __syncthreads();
   }
 
@@ -313,8 +319,8 @@ __global__ __launch_bounds__(kThreads, 1) void dequant_matmul_kernel(DqArgs a) {
 
 template <int BITS>
 hipError_t launch_dq(const DqArgs& a, int64_t tiles, hipStream_t s) {
-  // 8-byte activation loads: rows 8-byte aligned (X 8-byte aligned, ldx % 4 == 0)
-  const bool vec = reinterpret_cast<uintptr_t>(a.X) % 8 == 0 && a.ldx % 4 == 0;
+  // 16-byte activation loads: rows 16-byte aligned (X 16-byte aligned, ldx % 8 == 0)
+  const bool vec = reinterpret_cast<uintptr_t>(a.X) % 16 == 0 && a.ldx % 8 == 0;
   if (vec)
     dequant_matmul_kernel<BITS, true><<<dim3((unsigned)tiles), dim3(kThreads), 0, s>>>(a);
   else
