@@ -28,6 +28,8 @@
 // lane keeps its 32 decided codes in registers and stores them as one 32-byte
 // segment per block: the operand of later updates and the source of the
 // selection gather.
+#include <type_traits>
+
 #include "kernels.h"
 #include "device.h"
 
@@ -215,6 +217,11 @@ __device__ __forceinline__ void lazy_update(const DecodeDesc& d, int64_t nb, int
 }
 
 typedef int v4i __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) void lds_void;
+typedef __attribute__((address_space(1))) void gbl_void;
+
+// every load of this wave has landed (direct-to-LDS loads included)
+__device__ __forceinline__ void wait_loads() { __builtin_amdgcn_s_waitcnt(0x0f70); }
 
 __device__ __forceinline__ v4i mfma_i8(v4i a, v4i b, v4i c) {
   return __builtin_amdgcn_mfma_i32_16x16x64_i8(a, b, c, 0, 0, 0);
@@ -231,16 +238,26 @@ __device__ __forceinline__ v4i mfma_i8(v4i a, v4i b, v4i c) {
 // are combined exactly as 128 a_2e + a_2e+1 (< 2^28), then added in fp64
 // scaled by s 2^(-13 - 14 e).  The accumulator works in units of 2^rexp of
 // its row meanwhile (an exact rescaling), so the flush needs no per-row
-// exponent.  Operands stream one step ahead: the next step's digits while
-// the current step's products run, the next unit's codes as soon as the last
-// products of a pair have read its current ones.
+// exponent.
+//
+// Every wave of the workgroup walks the same blocks, so a unit's digit tiles
+// (up to 28 KB) are loaded once per workgroup, straight into an LDS ring of
+// two units: the next unit's tiles stream in while the current one's products
+// run, with one barrier per unit.  The ring position `rk` runs on across the
+// blocks, so a block's first unit goes to the slot its predecessor's last
+// unit did not use (every wave finished reading that one before the last
+// barrier).  Digits come from LDS one step ahead; each wave's own codes and
+// scales come from global memory, loaded while the previous unit runs, so no
+// load the products wait on was issued after the ring's.
+constexpr int kUnitBytes = 2 * kDigitTileBytes;   // one LDS ring slot
 template <int NT>
 __device__ __forceinline__ void lazy_update_i8(const DecodeDesc& d, int64_t nb, int64_t b,
                                                const uint8_t* cw, const uint32_t (&so)[NT],
-                                               d4 (&acc)[2][NT], int lane) {
+                                               d4 (&acc)[2][NT], int lane, uint8_t* ring,
+                                               uint32_t& rk) {
   const int64_t nb2 = (nb + 1) / 2;
   const int64_t c0 = (b + 1) / 2;
-  if (c0 >= nb2) return;
+  if (c0 >= nb2) return;   // the same for every wave
   // into units of 2^rexp of this lane's rows 32 b + 16 a + lane / 16 + 4 r
 #pragma unroll
   for (int a = 0; a < 2; ++a)
@@ -252,42 +269,73 @@ __device__ __forceinline__ void lazy_update_i8(const DecodeDesc& d, int64_t nb, 
       for (int t = 0; t < NT; ++t) acc[a][t][r] = ldexp(acc[a][t][r], -e);
     }
   const int U = (d.G == 1 || d.g % 128 == 0) ? 2 : 1;   // pairs per unit
-  const uint8_t* const tbase =
-      d.R8 + decode_digit_tile(nb2, b, c0) * kDigitTileBytes + 16 * lane;
+  const uint8_t* const tile_c0 = d.R8 + decode_digit_tile(nb2, b, c0) * kDigitTileBytes;
+  const int wave = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
+  const int waves = (int)(blockDim.x >> 6);
+  // the digit tiles of unit u's pairs into ring slot `slot`, 1 KB (one
+  // direct-to-LDS load of 16 bytes per lane) at a time, dealt to the waves
+  auto issue = [&](int64_t u, uint32_t slot) {
+    const int64_t pa = u > c0 ? u : c0, pb = u + U < nb2 ? u + U : nb2;
+    const int nblk = (int)(pb - pa) * (kDigitTileBytes / 1024);
+    const uint8_t* src = tile_c0 + (pa - c0) * kDigitTileBytes + 16 * lane;
+    uint8_t* dst = ring + (slot & 1) * kUnitBytes + (pa - u) * kDigitTileBytes;
+    for (int q = wave; q < nblk; q += waves)
+      __builtin_amdgcn_global_load_lds((gbl_void*)(src + q * 1024), (lds_void*)(dst + q * 1024),
+                                       16, 0, 0);
+  };
   // this lane's 16 code bytes of pair c for tile t: block 2c + lane / 32,
   // path 16 t + lane % 16, bytes 16 ((lane / 16) % 2) ..
   const uint8_t* const cb =
       cw + (lane >> 5) * kBlockCodes + (lane & 15) * kSeg + 16 * ((lane >> 4) & 1);
-  auto load_a = [&](int64_t c, int e, v4i (&A)[4]) {
-    const uint8_t* tp = tbase + (c - c0) * kDigitTileBytes + (4 * e) * 1024;
-    A[0] = *reinterpret_cast<const v4i*>(tp);            // digit 2e, half 0
-    A[1] = *reinterpret_cast<const v4i*>(tp + 1024);     // digit 2e, half 1
-    if (2 * e + 1 < kDecodeDigits) {
-      A[2] = *reinterpret_cast<const v4i*>(tp + 2048);   // digit 2e + 1, half 0
-      A[3] = *reinterpret_cast<const v4i*>(tp + 3072);   // digit 2e + 1, half 1
-    } else {
-      A[2] = v4i{0, 0, 0, 0};
-      A[3] = v4i{0, 0, 0, 0};
-    }
-  };
   auto load_b = [&](int64_t c, v4i (&Bq)[NT]) {
 #pragma unroll
     for (int t = 0; t < NT; ++t)
       Bq[t] = *reinterpret_cast<const v4i*>(cb + 2 * c * kBlockCodes + t * 16 * kSeg);
   };
+  // the scales of unit u (one scale group)
+  auto load_s = [&](int64_t u, float (&sc)[NT]) {
+    const uint32_t grp = d.G == 1 ? 0u : (uint32_t)((64 * u) / d.g);
+#pragma unroll
+    for (int t = 0; t < NT; ++t) sc[t] = load_scale(d.S + (so[t] + grp));
+  };
   constexpr int kE = (kDecodeDigits + 1) / 2;   // digit pairs
-  v4i Bq[2][NT], An[4];
+  v4i Bq[2][NT];
+  float scn[NT];
   int64_t u = c0 / U * U;
   {
     const int64_t pb = u + U < nb2 ? u + U : nb2;
     for (int64_t c = c0; c < pb; ++c) load_b(c, Bq[c - u]);
   }
-  load_a(c0, 0, An);
-  for (; u < nb2; u += U) {
+  load_s(u, scn);
+  issue(u, rk);
+  for (; u < nb2; u += U, ++rk) {
     const int64_t pa = u > c0 ? u : c0, pb = u + U < nb2 ? u + U : nb2;
-    const uint32_t grp = d.G == 1 ? 0u : (uint32_t)((64 * u) / d.g);
-#pragma unroll 1
-    for (int e = 0; e < kE; ++e) {
+    float sc[NT];
+#pragma unroll
+    for (int t = 0; t < NT; ++t) sc[t] = scn[t];
+    // this unit's tiles, codes and scales have landed, and every wave is
+    // done with the other slot (the previous unit)
+    wait_loads();
+    __syncthreads();
+    if (pb < nb2) issue(pb, rk + 1);
+    const uint8_t* const slotp = ring + (rk & 1) * kUnitBytes + 16 * lane;
+    // digits 2e and 2e + 1 of pair c, both row halves (for e = kE - 1, whose
+    // second digit does not exist, the first one's again: never used)
+    auto load_a = [&](int64_t c, int e, v4i (&A)[4]) {
+      const uint8_t* tp = slotp + (c - u) * kDigitTileBytes + (4 * e) * 1024;
+      const int o2 = 2 * e + 1 < kDecodeDigits ? 2048 : 0;
+      A[0] = *reinterpret_cast<const v4i*>(tp);
+      A[1] = *reinterpret_cast<const v4i*>(tp + 1024);
+      A[2] = *reinterpret_cast<const v4i*>(tp + o2);
+      A[3] = *reinterpret_cast<const v4i*>(tp + o2 + 1024);
+    };
+    v4i An[4];
+    load_a(pa, 0, An);
+    // digit pair e over the unit's pairs; the last one (a single digit, as
+    // kDecodeDigits is odd) also loads the next unit's codes, and is peeled
+    // off the loop so that no global load sits inside it
+    auto step = [&](int e, auto last_c) {
+      constexpr bool kLast = decltype(last_c)::value;
       v4i a1[2][NT], a2[2][NT];
 #pragma unroll
       for (int h = 0; h < 2; ++h)
@@ -301,29 +349,27 @@ __device__ __forceinline__ void lazy_update_i8(const DecodeDesc& d, int64_t nb, 
         const int64_t c = u + slot;
         if (c < pa || c >= pb) continue;
         v4i A[4] = {An[0], An[1], An[2], An[3]};
-        // the next step's digits
+        // the next step's digits (inside this unit)
         if (c + 1 < pb)
           load_a(c + 1, e, An);
-        else if (e + 1 < kE)
+        else if (!kLast)
           load_a(pa, e + 1, An);
-        else if (pb < nb2)
-          load_a(pb, 0, An);
 #pragma unroll
         for (int h = 0; h < 2; ++h)
 #pragma unroll
           for (int t = 0; t < NT; ++t) {
             a1[h][t] = mfma_i8(A[h], Bq[slot][t], a1[h][t]);
-            if (2 * e + 1 < kDecodeDigits) a2[h][t] = mfma_i8(A[2 + h], Bq[slot][t], a2[h][t]);
+            if (!kLast) a2[h][t] = mfma_i8(A[2 + h], Bq[slot][t], a2[h][t]);
           }
         // the next unit's codes, once these products have read the current ones
-        if (e + 1 == kE && pb < nb2) {
+        if (kLast && pb < nb2) {
           const int64_t cn = pb + slot;
           if (cn < nb2 && cn < pb + U) load_b(cn, Bq[slot]);
         }
       }
 #pragma unroll
       for (int t = 0; t < NT; ++t) {
-        const double mult = ldexp((double)load_scale(d.S + (so[t] + grp)), -13 - 14 * e);
+        const double mult = ldexp((double)sc[t], -13 - 14 * e);
 #pragma unroll
         for (int h = 0; h < 2; ++h)
 #pragma unroll
@@ -332,13 +378,20 @@ __device__ __forceinline__ void lazy_update_i8(const DecodeDesc& d, int64_t nb, 
             acc[h][t][r] = fma(mult, (double)v, acc[h][t][r]);
           }
       }
-    }
-    // a slot this unit did not use (a first unit that starts at its second
-    // pair) takes the next unit's codes now
+    };
+    static_assert(kDecodeDigits % 2 == 1, "the peeled last step takes one digit");
+#pragma unroll 1
+    for (int e = 0; e + 1 < kE; ++e) step(e, std::false_type{});
+    step(kE - 1, std::true_type{});
+    if (pb < nb2) {
+      // a slot this unit did not use (a first unit that starts at its second
+      // pair) takes the next unit's codes now
 #pragma unroll
-    for (int slot = 0; slot < 2; ++slot) {
-      const int64_t c = u + slot, cn = u + U + slot;
-      if (slot < U && (c < pa || c >= pb) && cn < nb2) load_b(cn, Bq[slot]);
+      for (int slot = 0; slot < 2; ++slot) {
+        const int64_t c = u + slot, cn = pb + slot;
+        if (slot < U && (c < pa || c >= pb) && cn < nb2) load_b(cn, Bq[slot]);
+      }
+      load_s(pb, scn);
     }
   }
 #pragma unroll
@@ -353,10 +406,11 @@ __device__ __forceinline__ void lazy_update_i8(const DecodeDesc& d, int64_t nb, 
 }
 
 // One wave's share of the decode: paths pbase .. pbase + npw - 1 (npw <= 64,
-// in NT = ceil(npw / 16) tiles), codes at cw, LDS buffer sZ of kWaveLds bytes.
+// in NT = ceil(npw / 16) tiles), codes at cw, LDS buffer sZ of kWaveLds bytes;
+// with the int8 update, the workgroup's digit ring (2 kUnitBytes) at ring.
 template <int NT, bool kUniS, bool kI8>
 __device__ __forceinline__ void decode_wave(const DecodeDesc& d, int64_t pbase, int npw,
-                                            uint8_t* cw, double* sZ) {
+                                            uint8_t* cw, double* sZ, uint8_t* ring) {
   const int lane = threadIdx.x & 63;
   const int64_t m = d.m, g = d.g, G = d.G;
   const int64_t kp1 = (int64_t)d.K + 1;
@@ -386,6 +440,7 @@ __device__ __forceinline__ void decode_wave(const DecodeDesc& d, int64_t pbase, 
   double* const sD = sZ + kGBuf;    // sD[r * 32 + c] = R[i0 + c][i0 + r], c <= r
 
   double resid = 0.0;
+  uint32_t rk = 0;   // position in the digit ring (int8 update)
   for (int64_t b = nb - 1; b >= 0; --b) {
     const int64_t i0 = b * kBS;
     const int bl = (int)((m - i0) < kBS ? (m - i0) : kBS);
@@ -416,7 +471,7 @@ __device__ __forceinline__ void decode_wave(const DecodeDesc& d, int64_t pbase, 
         }
     }
     if constexpr (kI8) {
-      if (b + 1 < nb) lazy_update_i8<NT>(d, nb, b, cw, so, acc, lane);
+      if (b + 1 < nb) lazy_update_i8<NT>(d, nb, b, cw, so, acc, lane, ring, rk);
     } else {
       if (b + 1 < nb) lazy_update<NT, kUniS>(d, nb, b, cw, so, sp, acc, lane);
     }
@@ -511,23 +566,30 @@ __global__ __launch_bounds__(kDecodeMaxThreads) void decode_kernel(DecodeDesc d)
   const int64_t wg0 = (int64_t)blockIdx.x * d.wg_paths;
   const int64_t wgend = (wg0 + d.wg_paths < P) ? wg0 + d.wg_paths : P;
   const WaveTiles wt = decode_wave_tiles((int)(d.wg_paths / 16), waves, wave);
-  const int64_t pbase = wg0 + 16 * wt.first;
+  int64_t pbase = wg0 + 16 * wt.first;
   const int64_t pend = (pbase + 16 * wt.count < wgend) ? pbase + 16 * wt.count : wgend;
-  if (pbase >= pend) return;   // waves never synchronise, so idle ones may leave
-  const int npw = (int)(pend - pbase);
-  const int64_t nb = (d.m + kBS - 1) / kBS;
+  if (pbase >= pend) {
+    // without the int8 update the waves never synchronise, so idle ones
+    // leave; with it they take their part in loading the digit ring, on a
+    // valid path with no lanes
+    if constexpr (!kI8) return;
+    pbase = P - 1;
+  }
+  const int npw = pbase < pend ? (int)(pend - pbase) : 0;
   uint8_t* cw =
       d.pcodes + ((int64_t)blockIdx.x * waves + wave) * decode_code_blocks(d.m) * kBlockCodes;
   double* sZ = lds + wave * (kWaveLds / (int)sizeof(double));
+  uint8_t* ring = reinterpret_cast<uint8_t*>(lds) + waves * kWaveLds;
   switch ((npw + 15) / 16) {
-    case 1: decode_wave<1, kUniS, kI8>(d, pbase, npw, cw, sZ); break;
-    case 2: decode_wave<2, kUniS, kI8>(d, pbase, npw, cw, sZ); break;
-    case 3: decode_wave<3, kUniS, kI8>(d, pbase, npw, cw, sZ); break;
+    case 0:
+    case 1: decode_wave<1, kUniS, kI8>(d, pbase, npw, cw, sZ, ring); break;
+    case 2: decode_wave<2, kUniS, kI8>(d, pbase, npw, cw, sZ, ring); break;
+    case 3: decode_wave<3, kUniS, kI8>(d, pbase, npw, cw, sZ, ring); break;
     default:   // the int8 update's geometry gives a wave at most three tiles
       if constexpr (kI8)
-        decode_wave<3, kUniS, kI8>(d, pbase, npw, cw, sZ);
+        decode_wave<3, kUniS, kI8>(d, pbase, npw, cw, sZ, ring);
       else
-        decode_wave<4, kUniS, kI8>(d, pbase, npw, cw, sZ);
+        decode_wave<4, kUniS, kI8>(d, pbase, npw, cw, sZ, ring);
       break;
   }
 }
@@ -766,9 +828,9 @@ hipError_t launch_decode(const DecodeDesc& d, hipStream_t stream) {
   geo.wg_paths = d.wg_paths;
   geo.threads = d.threads;
   geo.nwg = d.nwg;
-  const size_t lds = (size_t)(d.threads / 64) * kWaveLds;
   const bool uniform_scale = !d.gidx && !d.spos && (d.G == 1 || d.g % kBS == 0);
   const bool i8 = d.R8 != nullptr;
+  const size_t lds = (size_t)(d.threads / 64) * kWaveLds + (i8 ? 2 * kUnitBytes : 0);
   if (i8 && (!d.rexp || d.gidx || d.spos || d.bits > 7 || (d.G != 1 && d.g % 64 != 0) ||
              d.wg_paths > 3 * 16 * (int64_t)(d.threads / 64)))
     return hipErrorInvalidValue;
