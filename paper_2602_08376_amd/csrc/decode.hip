@@ -218,10 +218,25 @@ __device__ __forceinline__ void lazy_update(const DecodeDesc& d, int64_t nb, int
 
 typedef int v4i __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) void lds_void;
-typedef __attribute__((address_space(1))) void gbl_void;
 
 // every load of this wave has landed (direct-to-LDS loads included)
 __device__ __forceinline__ void wait_loads() { __builtin_amdgcn_s_waitcnt(0x0f70); }
+
+// 16 bytes per lane from global memory straight to LDS: lane i's bytes land
+// at LDS address lds + 16 i.  Issued as its own instruction so that the
+// compiler's wait counting for the LDS reads around it stays exact (it would
+// otherwise treat every LDS read after such a load as possibly out of order
+// and wait for all of them); completion is covered by wait_loads before the
+// barrier that publishes the data.  M0 is set one wait state ahead of the
+// load that reads it.
+__device__ __forceinline__ void load_to_lds16(const void* src, const void* lds) {
+  const uint32_t a = __builtin_amdgcn_readfirstlane(
+      (uint32_t)(uintptr_t)(const lds_void*)lds);
+  asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off"
+               :
+               : "v"(src), "s"(a)
+               : "memory", "m0");
+}
 
 __device__ __forceinline__ v4i mfma_i8(v4i a, v4i b, v4i c) {
   return __builtin_amdgcn_mfma_i32_16x16x64_i8(a, b, c, 0, 0, 0);
@@ -246,18 +261,181 @@ __device__ __forceinline__ v4i mfma_i8(v4i a, v4i b, v4i c) {
 // run, with one barrier per unit.  The ring position `rk` runs on across the
 // blocks, so a block's first unit goes to the slot its predecessor's last
 // unit did not use (every wave finished reading that one before the last
-// barrier).  Digits come from LDS one step ahead; each wave's own codes and
-// scales come from global memory, loaded while the previous unit runs, so no
-// load the products wait on was issued after the ring's.
+// barrier).
+//
+// A unit runs over items (e, h): digit pair e, row half h.  The products of
+// an item are issued one at a time, each followed by one share of the fp64
+// flush of the item before it (the other row half; the first item of a unit
+// flushes the last one of the unit before), so the matrix cores and the
+// vector ALU work side by side; the next item's digits are read from LDS
+// while it runs.  A pair slot outside the unit (the first unit of a block
+// that starts at its second pair, the last one of a block that ends at its
+// first) reads its digits from a tile of zeros and its codes from a decided
+// pair, so no item branches.  Each wave's codes and scales of the next unit
+// are loaded in the last digit pair, whose second digit does not exist, so
+// its int32 sums free the registers.
 constexpr int kUnitBytes = 2 * kDigitTileBytes;   // one LDS ring slot
+constexpr int kRingBytes = 2 * kUnitBytes + kDigitTileBytes;   // two slots and a zero tile
+
+template <int NT, int kU>
+__device__ __forceinline__ void lazy_units_i8(const DecodeDesc& d, int64_t nb2, int64_t b,
+                                              const uint8_t* cw, const uint32_t (&so)[NT],
+                                              d4 (&acc)[2][NT], int lane, uint8_t* ring,
+                                              uint32_t& rk) {
+  const int64_t c0 = (b + 1) / 2;
+  const uint8_t* const tile_c0 = d.R8 + decode_digit_tile(nb2, b, c0) * kDigitTileBytes;
+  const int wave = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
+  const int waves = d.threads >> 6;
+  // the digit tiles of unit u's pairs into ring slot `slot`, 1 KB (one
+  // direct-to-LDS load of 16 bytes per lane) at a time, dealt to the waves
+  auto issue = [&](int64_t u, uint32_t slot) {
+    const int64_t pa = u > c0 ? u : c0, pb = u + kU < nb2 ? u + kU : nb2;
+    const int nblk = (int)(pb - pa) * (kDigitTileBytes / 1024);
+    const uint8_t* src = tile_c0 + (pa - c0) * kDigitTileBytes + 16 * lane;
+    uint8_t* dst = ring + (slot & 1) * kUnitBytes + (pa - u) * kDigitTileBytes;
+    for (int q = wave; q < nblk; q += waves) load_to_lds16(src + q * 1024, dst + q * 1024);
+  };
+  // this lane's 16 code bytes of pair c for tile t (block 2c + lane / 32,
+  // path 16 t + lane % 16, bytes 16 ((lane / 16) % 2) ..), pairs past the
+  // last clamped to it; the scales of the unit's group
+  const uint8_t* const cb =
+      cw + (lane >> 5) * kBlockCodes + (lane & 15) * kSeg + 16 * ((lane >> 4) & 1);
+  auto load_codes = [&](int64_t c, v4i (&Bs)[NT]) {
+    c = c < nb2 ? c : nb2 - 1;
+#pragma unroll
+    for (int t = 0; t < NT; ++t)
+      Bs[t] = *reinterpret_cast<const v4i*>(cb + 2 * c * kBlockCodes + t * 16 * kSeg);
+  };
+  auto load_scales = [&](int64_t u, float (&sc)[NT]) {
+    const int64_t uc = u < nb2 ? u : nb2 - 1;
+    const uint32_t grp = d.G == 1 ? 0u : (uint32_t)((64 * uc) / d.g);
+#pragma unroll
+    for (int t = 0; t < NT; ++t) sc[t] = load_scale(d.S + (so[t] + grp));
+  };
+  constexpr int kE = (kDecodeDigits + 1) / 2;   // digit pairs
+  static_assert(kDecodeDigits % 2 == 1 && kE >= 3, "the last digit pair has one digit");
+  const uint8_t* const zero = ring + 2 * kUnitBytes + 16 * lane;
+
+  v4i a1[2][NT], a2[2][NT];   // int32 sums of digits 2e, 2e + 1 by row half
+  double mult[NT], mprev[NT];   // flush factors s 2^(-13 - 14 e)
+  // nothing pending before the block's first unit
+#pragma unroll
+  for (int t = 0; t < NT; ++t) {
+    a1[1][t] = v4i{0, 0, 0, 0};
+    mprev[t] = 0.0;
+  }
+  // one item: the products of row half h (two digits or one) from digits A
+  // and codes Bq, each followed by its share of the flush of row half hf
+  // with factors m (two digits or one)
+  auto item = [&](int h, const v4i (&A)[kU][2], const v4i (&Bq)[kU][NT], auto two_p, int hf,
+                  const double (&m)[NT], auto two_f) {
+    constexpr bool kTwoP = decltype(two_p)::value, kTwoF = decltype(two_f)::value;
+    constexpr int kDg = kTwoP ? 2 : 1;
+    constexpr int kM = kU * NT * kDg, kF = 4 * NT;   // products, flush elements
+    constexpr int kPer = (kF + kM - 1) / kM;          // flush elements per product
+    auto flush_el = [&](int f) {
+      const int t = f / 4, r = f % 4;
+      const int v = kTwoF ? a1[hf][t][r] * 128 + a2[hf][t][r] : a1[hf][t][r] * 128;
+      acc[hf][t][r] = fma(m[t], (double)v, acc[hf][t][r]);
+    };
+#pragma unroll
+    for (int i = 0; i < kM; ++i) {
+      const int s = i / (NT * kDg), t = (i / kDg) % NT, g = i % kDg;
+      if (g == 0)
+        a1[h][t] = mfma_i8(A[s][0], Bq[s][t], s == 0 ? v4i{0, 0, 0, 0} : a1[h][t]);
+      else
+        a2[h][t] = mfma_i8(A[s][1], Bq[s][t], s == 0 ? v4i{0, 0, 0, 0} : a2[h][t]);
+#pragma unroll
+      for (int f = i * kPer; f < (i + 1) * kPer && f < kF; ++f) flush_el(f);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  };
+  const std::true_type two{};
+  const std::false_type one{};
+
+  int64_t u = c0 / kU * kU;
+  v4i Bq[kU][NT], Bn[kU][NT];
+  float sc[NT], scn[NT];
+#pragma unroll
+  for (int s = 0; s < kU; ++s) load_codes(u + s, Bn[s]);
+  load_scales(u, scn);
+  issue(u, rk);
+  for (; u < nb2; u += kU, ++rk) {
+    const int64_t pa = u > c0 ? u : c0, pb = u + kU < nb2 ? u + kU : nb2;
+    // this unit's tiles, codes and scales have landed, and every wave is
+    // done with the other ring slot
+    wait_loads();
+    __syncthreads();
+#pragma unroll
+    for (int s = 0; s < kU; ++s)
+#pragma unroll
+      for (int t = 0; t < NT; ++t) Bq[s][t] = Bn[s][t];
+#pragma unroll
+    for (int t = 0; t < NT; ++t) sc[t] = scn[t];
+    if (pb < nb2) issue(pb, rk + 1);
+    // lane-relative LDS tiles of the unit's pair slots (zeros outside it)
+    const uint8_t* tile[kU];
+#pragma unroll
+    for (int s = 0; s < kU; ++s)
+      tile[s] = (u + s >= pa && u + s < pb)
+                    ? ring + (rk & 1) * kUnitBytes + s * kDigitTileBytes + 16 * lane
+                    : zero;
+    // digits 2e and 2e + 1 (the first again for the last e) of row half h
+    auto load_a = [&](int e, int h, v4i (&A)[kU][2]) {
+      const int o1 = 2 * e + 1 < kDecodeDigits ? 2048 : 0;
+#pragma unroll
+      for (int s = 0; s < kU; ++s) {
+        const uint8_t* p = tile[s] + (4 * e + h) * 1024;
+        A[s][0] = *reinterpret_cast<const v4i*>(p);
+        A[s][1] = *reinterpret_cast<const v4i*>(p + o1);
+      }
+    };
+    auto set_mult = [&](int e) {
+#pragma unroll
+      for (int t = 0; t < NT; ++t) mult[t] = ldexp((double)sc[t], -13 - 14 * e);
+    };
+    v4i Ac[kU][2], An[kU][2];
+    load_a(0, 0, Ac);
+    // e = 0: half 0 beside the previous unit's last half 1, half 1 beside half 0
+    load_a(0, 1, An);
+    item(0, Ac, Bq, two, 1, mprev, one);
+    set_mult(0);
+    load_a(1, 0, Ac);
+    item(1, An, Bq, two, 0, mult, two);
+#pragma unroll 1
+    for (int e = 1; e + 1 < kE; ++e) {
+      load_a(e, 1, An);
+      item(0, Ac, Bq, two, 1, mult, two);
+      set_mult(e);
+      load_a(e + 1, 0, Ac);
+      item(1, An, Bq, two, 0, mult, two);
+    }
+    // e = kE - 1 (one digit); the next unit's codes and scales meanwhile
+    load_a(kE - 1, 1, An);
+#pragma unroll
+    for (int s = 0; s < kU; ++s) load_codes(u + kU + s, Bn[s]);
+    load_scales(u + kU, scn);
+    item(0, Ac, Bq, one, 1, mult, two);
+    set_mult(kE - 1);
+    item(1, An, Bq, one, 0, mult, one);
+#pragma unroll
+    for (int t = 0; t < NT; ++t) mprev[t] = mult[t];
+  }
+  // the block's last item
+#pragma unroll
+  for (int t = 0; t < NT; ++t)
+#pragma unroll
+    for (int r = 0; r < 4; ++r)
+      acc[1][t][r] = fma(mprev[t], (double)(a1[1][t][r] * 128), acc[1][t][r]);
+}
+
 template <int NT>
 __device__ __forceinline__ void lazy_update_i8(const DecodeDesc& d, int64_t nb, int64_t b,
                                                const uint8_t* cw, const uint32_t (&so)[NT],
                                                d4 (&acc)[2][NT], int lane, uint8_t* ring,
                                                uint32_t& rk) {
   const int64_t nb2 = (nb + 1) / 2;
-  const int64_t c0 = (b + 1) / 2;
-  if (c0 >= nb2) return;   // the same for every wave
+  if ((b + 1) / 2 >= nb2) return;   // the same for every wave
   // into units of 2^rexp of this lane's rows 32 b + 16 a + lane / 16 + 4 r
 #pragma unroll
   for (int a = 0; a < 2; ++a)
@@ -268,132 +446,11 @@ __device__ __forceinline__ void lazy_update_i8(const DecodeDesc& d, int64_t nb, 
 #pragma unroll
       for (int t = 0; t < NT; ++t) acc[a][t][r] = ldexp(acc[a][t][r], -e);
     }
-  const int U = (d.G == 1 || d.g % 128 == 0) ? 2 : 1;   // pairs per unit
-  const uint8_t* const tile_c0 = d.R8 + decode_digit_tile(nb2, b, c0) * kDigitTileBytes;
-  const int wave = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
-  const int waves = (int)(blockDim.x >> 6);
-  // the digit tiles of unit u's pairs into ring slot `slot`, 1 KB (one
-  // direct-to-LDS load of 16 bytes per lane) at a time, dealt to the waves
-  auto issue = [&](int64_t u, uint32_t slot) {
-    const int64_t pa = u > c0 ? u : c0, pb = u + U < nb2 ? u + U : nb2;
-    const int nblk = (int)(pb - pa) * (kDigitTileBytes / 1024);
-    const uint8_t* src = tile_c0 + (pa - c0) * kDigitTileBytes + 16 * lane;
-    uint8_t* dst = ring + (slot & 1) * kUnitBytes + (pa - u) * kDigitTileBytes;
-    for (int q = wave; q < nblk; q += waves)
-      __builtin_amdgcn_global_load_lds((gbl_void*)(src + q * 1024), (lds_void*)(dst + q * 1024),
-                                       16, 0, 0);
-  };
-  // this lane's 16 code bytes of pair c for tile t: block 2c + lane / 32,
-  // path 16 t + lane % 16, bytes 16 ((lane / 16) % 2) ..
-  const uint8_t* const cb =
-      cw + (lane >> 5) * kBlockCodes + (lane & 15) * kSeg + 16 * ((lane >> 4) & 1);
-  auto load_b = [&](int64_t c, v4i (&Bq)[NT]) {
-#pragma unroll
-    for (int t = 0; t < NT; ++t)
-      Bq[t] = *reinterpret_cast<const v4i*>(cb + 2 * c * kBlockCodes + t * 16 * kSeg);
-  };
-  // the scales of unit u (one scale group)
-  auto load_s = [&](int64_t u, float (&sc)[NT]) {
-    const uint32_t grp = d.G == 1 ? 0u : (uint32_t)((64 * u) / d.g);
-#pragma unroll
-    for (int t = 0; t < NT; ++t) sc[t] = load_scale(d.S + (so[t] + grp));
-  };
-  constexpr int kE = (kDecodeDigits + 1) / 2;   // digit pairs
-  v4i Bq[2][NT];
-  float scn[NT];
-  int64_t u = c0 / U * U;
-  {
-    const int64_t pb = u + U < nb2 ? u + U : nb2;
-    for (int64_t c = c0; c < pb; ++c) load_b(c, Bq[c - u]);
-  }
-  load_s(u, scn);
-  issue(u, rk);
-  for (; u < nb2; u += U, ++rk) {
-    const int64_t pa = u > c0 ? u : c0, pb = u + U < nb2 ? u + U : nb2;
-    float sc[NT];
-#pragma unroll
-    for (int t = 0; t < NT; ++t) sc[t] = scn[t];
-    // this unit's tiles, codes and scales have landed, and every wave is
-    // done with the other slot (the previous unit)
-    wait_loads();
-    __syncthreads();
-    if (pb < nb2) issue(pb, rk + 1);
-    const uint8_t* const slotp = ring + (rk & 1) * kUnitBytes + 16 * lane;
-    // digits 2e and 2e + 1 of pair c, both row halves (for e = kE - 1, whose
-    // second digit does not exist, the first one's again: never used)
-    auto load_a = [&](int64_t c, int e, v4i (&A)[4]) {
-      const uint8_t* tp = slotp + (c - u) * kDigitTileBytes + (4 * e) * 1024;
-      const int o2 = 2 * e + 1 < kDecodeDigits ? 2048 : 0;
-      A[0] = *reinterpret_cast<const v4i*>(tp);
-      A[1] = *reinterpret_cast<const v4i*>(tp + 1024);
-      A[2] = *reinterpret_cast<const v4i*>(tp + o2);
-      A[3] = *reinterpret_cast<const v4i*>(tp + o2 + 1024);
-    };
-    v4i An[4];
-    load_a(pa, 0, An);
-    // digit pair e over the unit's pairs; the last one (a single digit, as
-    // kDecodeDigits is odd) also loads the next unit's codes, and is peeled
-    // off the loop so that no global load sits inside it
-    auto step = [&](int e, auto last_c) {
-      constexpr bool kLast = decltype(last_c)::value;
-      v4i a1[2][NT], a2[2][NT];
-#pragma unroll
-      for (int h = 0; h < 2; ++h)
-#pragma unroll
-        for (int t = 0; t < NT; ++t) {
-          a1[h][t] = v4i{0, 0, 0, 0};
-          a2[h][t] = v4i{0, 0, 0, 0};
-        }
-#pragma unroll
-      for (int slot = 0; slot < 2; ++slot) {   // the unit's pairs c = u + slot in [pa, pb)
-        const int64_t c = u + slot;
-        if (c < pa || c >= pb) continue;
-        v4i A[4] = {An[0], An[1], An[2], An[3]};
-        // the next step's digits (inside this unit)
-        if (c + 1 < pb)
-          load_a(c + 1, e, An);
-        else if (!kLast)
-          load_a(pa, e + 1, An);
-#pragma unroll
-        for (int h = 0; h < 2; ++h)
-#pragma unroll
-          for (int t = 0; t < NT; ++t) {
-            a1[h][t] = mfma_i8(A[h], Bq[slot][t], a1[h][t]);
-            if (!kLast) a2[h][t] = mfma_i8(A[2 + h], Bq[slot][t], a2[h][t]);
-          }
-        // the next unit's codes, once these products have read the current ones
-        if (kLast && pb < nb2) {
-          const int64_t cn = pb + slot;
-          if (cn < nb2 && cn < pb + U) load_b(cn, Bq[slot]);
-        }
-      }
-#pragma unroll
-      for (int t = 0; t < NT; ++t) {
-        const double mult = ldexp((double)sc[t], -13 - 14 * e);
-#pragma unroll
-        for (int h = 0; h < 2; ++h)
-#pragma unroll
-          for (int r = 0; r < 4; ++r) {
-            const int v = a1[h][t][r] * 128 + a2[h][t][r];
-            acc[h][t][r] = fma(mult, (double)v, acc[h][t][r]);
-          }
-      }
-    };
-    static_assert(kDecodeDigits % 2 == 1, "the peeled last step takes one digit");
-#pragma unroll 1
-    for (int e = 0; e + 1 < kE; ++e) step(e, std::false_type{});
-    step(kE - 1, std::true_type{});
-    if (pb < nb2) {
-      // a slot this unit did not use (a first unit that starts at its second
-      // pair) takes the next unit's codes now
-#pragma unroll
-      for (int slot = 0; slot < 2; ++slot) {
-        const int64_t c = u + slot, cn = pb + slot;
-        if (slot < U && (c < pa || c >= pb) && cn < nb2) load_b(cn, Bq[slot]);
-      }
-      load_s(pb, scn);
-    }
-  }
+  // two pairs per unit unless a scale group ends after one
+  if (d.G == 1 || d.g % 128 == 0)
+    lazy_units_i8<NT, 2>(d, nb2, b, cw, so, acc, lane, ring, rk);
+  else
+    lazy_units_i8<NT, 1>(d, nb2, b, cw, so, acc, lane, ring, rk);
 #pragma unroll
   for (int a = 0; a < 2; ++a)
 #pragma unroll
@@ -407,7 +464,7 @@ __device__ __forceinline__ void lazy_update_i8(const DecodeDesc& d, int64_t nb, 
 
 // One wave's share of the decode: paths pbase .. pbase + npw - 1 (npw <= 64,
 // in NT = ceil(npw / 16) tiles), codes at cw, LDS buffer sZ of kWaveLds bytes;
-// with the int8 update, the workgroup's digit ring (2 kUnitBytes) at ring.
+// with the int8 update, the workgroup's digit ring (kRingBytes) at ring.
 template <int NT, bool kUniS, bool kI8>
 __device__ __forceinline__ void decode_wave(const DecodeDesc& d, int64_t pbase, int npw,
                                             uint8_t* cw, double* sZ, uint8_t* ring) {
@@ -580,6 +637,11 @@ __global__ __launch_bounds__(kDecodeMaxThreads) void decode_kernel(DecodeDesc d)
       d.pcodes + ((int64_t)blockIdx.x * waves + wave) * decode_code_blocks(d.m) * kBlockCodes;
   double* sZ = lds + wave * (kWaveLds / (int)sizeof(double));
   uint8_t* ring = reinterpret_cast<uint8_t*>(lds) + waves * kWaveLds;
+  if constexpr (kI8) {
+    // the ring's tile of zero digits (read after the first unit's barrier)
+    for (int i = (int)threadIdx.x; i < kDigitTileBytes / 16; i += d.threads)
+      *reinterpret_cast<uint4*>(ring + 2 * kUnitBytes + 16 * i) = make_uint4(0u, 0u, 0u, 0u);
+  }
   switch ((npw + 15) / 16) {
     case 0:
     case 1: decode_wave<1, kUniS, kI8>(d, pbase, npw, cw, sZ, ring); break;
@@ -830,7 +892,7 @@ hipError_t launch_decode(const DecodeDesc& d, hipStream_t stream) {
   geo.nwg = d.nwg;
   const bool uniform_scale = !d.gidx && !d.spos && (d.G == 1 || d.g % kBS == 0);
   const bool i8 = d.R8 != nullptr;
-  const size_t lds = (size_t)(d.threads / 64) * kWaveLds + (i8 ? 2 * kUnitBytes : 0);
+  const size_t lds = (size_t)(d.threads / 64) * kWaveLds + (i8 ? kRingBytes : 0);
   if (i8 && (!d.rexp || d.gidx || d.spos || d.bits > 7 || (d.G != 1 && d.g % 64 != 0) ||
              d.wg_paths > 3 * 16 * (int64_t)(d.threads / 64)))
     return hipErrorInvalidValue;
