@@ -217,26 +217,8 @@ __device__ __forceinline__ void lazy_update(const DecodeDesc& d, int64_t nb, int
 }
 
 typedef int v4i __attribute__((ext_vector_type(4)));
-typedef __attribute__((address_space(3))) void lds_void;
-
 // every load of this wave has landed (direct-to-LDS loads included)
 __device__ __forceinline__ void wait_loads() { __builtin_amdgcn_s_waitcnt(0x0f70); }
-
-// 16 bytes per lane from global memory straight to LDS: lane i's bytes land
-// at LDS address lds + 16 i.  Issued as its own instruction so that the
-// compiler's wait counting for the LDS reads around it stays exact (it would
-// otherwise treat every LDS read after such a load as possibly out of order
-// and wait for all of them); completion is covered by wait_loads before the
-// barrier that publishes the data.  M0 is set one wait state ahead of the
-// load that reads it.
-__device__ __forceinline__ void load_to_lds16(const void* src, const void* lds) {
-  const uint32_t a = __builtin_amdgcn_readfirstlane(
-      (uint32_t)(uintptr_t)(const lds_void*)lds);
-  asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off"
-               :
-               : "v"(src), "s"(a)
-               : "memory", "m0");
-}
 
 __device__ __forceinline__ v4i mfma_i8(v4i a, v4i b, v4i c) {
   return __builtin_amdgcn_mfma_i32_16x16x64_i8(a, b, c, 0, 0, 0);
@@ -291,9 +273,9 @@ __device__ __forceinline__ void lazy_units_i8(const DecodeDesc& d, int64_t nb2, 
   auto issue = [&](int64_t u, uint32_t slot) {
     const int64_t pa = u > c0 ? u : c0, pb = u + kU < nb2 ? u + kU : nb2;
     const int nblk = (int)(pb - pa) * (kDigitTileBytes / 1024);
-    const uint8_t* src = tile_c0 + (pa - c0) * kDigitTileBytes + 16 * lane;
+    const uint8_t* src = tile_c0 + (pa - c0) * kDigitTileBytes;
     uint8_t* dst = ring + (slot & 1) * kUnitBytes + (pa - u) * kDigitTileBytes;
-    for (int q = wave; q < nblk; q += waves) load_to_lds16(src + q * 1024, dst + q * 1024);
+    for (int q = wave; q < nblk; q += waves) load_to_lds16(src + q * 1024, 16 * lane, dst + q * 1024);
   };
   // this lane's 16 code bytes of pair c for tile t (block 2c + lane / 32,
   // path 16 t + lane % 16, bytes 16 ((lane / 16) % 2) ..), pairs past the
@@ -670,7 +652,6 @@ __global__ __launch_bounds__(256) void select_kernel(const uint8_t* __restrict__
   __shared__ int kstar;
   const int64_t j = blockIdx.x;
   const int64_t kp1 = (int64_t)K + 1;
-  const int64_t nb = (m + kBS - 1) / kBS;
   const int tid = threadIdx.x;
   if (tid == 0) {
     int best = 0;

@@ -57,4 +57,21 @@ __device__ __forceinline__ double klein_uniform(uint64_t seed, uint32_t i, uint3
   return (hi * 67108864.0 + lo) * (1.0 / 9007199254740992.0);
 }
 
+typedef __attribute__((address_space(3))) void lds_void;
+
+// 16 bytes per lane from global memory straight to LDS: lane i reads base +
+// off_i (base the same for every lane) and its bytes land at LDS address
+// lds + 16 i.  Issued as its own instruction so that the compiler's wait
+// counting for the LDS reads around it stays exact (it would otherwise treat
+// every LDS read after such a load as possibly out of order and wait for all
+// of them); a vmcnt(0) wait before the barrier that publishes the data covers
+// its completion.  The LDS address goes in M0, set by the compiler; one wait
+// state separates that write from the load reading it.
+__device__ __forceinline__ void load_to_lds16(const void* base, uint32_t off, const void* lds) {
+  const uint32_t a = __builtin_amdgcn_readfirstlane(
+      (uint32_t)(uintptr_t)(const lds_void*)lds);
+  asm volatile("s_nop 0\n\tglobal_load_lds_dwordx4 %0, %1" : : "v"(off), "s"(base), "{m0}"(a)
+               : "memory");
+}
+
 }  // namespace ojbkq

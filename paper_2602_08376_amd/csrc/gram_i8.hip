@@ -49,8 +49,6 @@ constexpr int kStageBytes = 2 * kPanelBlocks * kBlockBytes;   // 64 KB
 constexpr int kSlotElems = kTile * kTile;
 
 typedef int v4i __attribute__((ext_vector_type(4)));
-typedef __attribute__((address_space(3))) void lds_void;
-typedef __attribute__((address_space(1))) void gbl_void;
 
 // ---- split ------------------------------------------------------------------
 
@@ -275,9 +273,7 @@ __device__ __forceinline__ void i8_segment(const I8Args& a, int64_t tile, int64_
   auto issue = [&](int64_t c, uint8_t* dst) {
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
-      gbl_void* g = (gbl_void*)(src[j] + (size_t)c * step_bytes + lane * 16);
-      lds_void* l = (lds_void*)(dst + (uwave * 8 + j) * kBlockBytes);
-      __builtin_amdgcn_global_load_lds(g, l, 16, 0, 0);
+      load_to_lds16(src[j] + (size_t)c * step_bytes, 16 * lane, dst + (uwave * 8 + j) * kBlockBytes);
     }
   };
   issue(c0, sbuf);
@@ -309,6 +305,7 @@ __device__ __forceinline__ void i8_segment(const I8Args& a, int64_t tile, int64_
         for (int y = 0; y < 4; ++y)
           fbn[y] = *reinterpret_cast<const v4i*>(bsrc + ((q + 1) * 8 + y) * kBlockBytes);
       }
+      __builtin_amdgcn_sched_barrier(0);   // the reads go out before the products
 #pragma unroll
       for (int p = 0; p < kDigits; ++p) {
         if (p + q > kDigits) continue;   // digit pairs with p + q <= 6 (1-based)
