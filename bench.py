@@ -67,7 +67,7 @@ def parse():
     ap.add_argument("--cpu-columns", type=int, default=24,
                     help="columns of the oracle's timed solve/decode sample")
     ap.add_argument("--copy-calibration", action="store_true",
-                    help="also run one plain 1 GiB device copy (for scaling HBM counters)")
+                    help="also run one 1 GiB streaming negation (for scaling HBM counters)")
     ap.add_argument("--sweep-k", metavar="SHAPES", default=None,
                     help="instead of the benchmark line: one JSON line per (layer, K) with the "
                          "layer time and the mean JTA residual, on the Llama-3-8B-shaped layers "
@@ -167,7 +167,8 @@ def sweep_k(args):
 KERNEL_SOURCES = {
     "gram_cross_kernel": ("paper_2602_08376_amd/csrc/gram.hip", "paper_2602_08376_amd/csrc/device.h",
                           "paper_2602_08376_amd/csrc/kernels.h"),
-    "gram_i8": ("paper_2602_08376_amd/csrc/gram_i8.hip", "paper_2602_08376_amd/csrc/kernels.h"),
+    "gram_i8": ("paper_2602_08376_amd/csrc/gram_i8.hip", "paper_2602_08376_amd/csrc/device.h",
+                "paper_2602_08376_amd/csrc/kernels.h"),
 }
 
 
@@ -661,11 +662,12 @@ def main():
     }
     if args.copy_calibration:
         # a written source (a never-written one can read back nothing from
-        # HBM), then one plain copy of it
+        # HBM), then one streaming pass over it: a negation, whose kernel no
+        # other step launches, reads 1 GiB and writes 1 GiB
         a = torch.empty(1 << 28, dtype=torch.float32, device=dev).uniform_()
         b = torch.empty_like(a)
         torch.cuda.synchronize()
-        b.copy_(a)
+        torch.neg(a, out=b)
         torch.cuda.synchronize()
         result["copy_calibration_bytes"] = a.numel() * 4
     if not args.no_cpu_baseline:
