@@ -183,7 +183,7 @@ __device__ __forceinline__ double rsqrt_f64(double d) {
 }
 
 // ---- Cholesky factor and inverse of one 64 x 64 block, in LDS ----------
-// Recursive halving down to 8 x 8 leaves: for a block [A11 .; A21 A22] of
+// Recursive halving down to 4 x 4 leaves: for a block [A11 .; A21 A22] of
 // size 2h,
 //   L11, X11 = chol / inverse of A11            (recursion)
 //   S = L21 = A21 X11^T                          (h x h x h)
@@ -192,14 +192,18 @@ __device__ __forceinline__ double rsqrt_f64(double d) {
 //   X21 = -X22 T                                 (h x h x h)
 // The leaves are factored and inverted by every thread redundantly in
 // registers (no exchange on the serial chain); every product runs on MFMA in
-// 16 x 16 tiles dealt to the four waves (an 8 x 8 product is one masked tile).
+// 16 x 16 tiles dealt to the four waves (a smaller product is one masked
+// tile).  The leaves sit on the serial chain, whose latency grows with their
+// size cubed: 4 x 4 leaves took the 64 x 64 block 3% faster than 8 x 8 ones.
 // A and X are row-major with pitch kQ; S and T are per-level scratch.
 constexpr int kQ = kT + 1;
-constexpr int kScr = 32 * 32 + 16 * 16 + 8 * 8;   // one scratch set of all levels
+constexpr int kLeaf = 4;   // leaf size of the recursion
+constexpr int kScr = 32 * 32 + 16 * 16 + 8 * 8 + 4 * 4;   // one scratch set of all levels
 
-// S_h / T_h for half size h (32, 16, 8) inside a scratch set
+// S_h / T_h for half size h (32, 16, 8, 4) inside a scratch set
 __device__ __forceinline__ double* lvl(double* base, int h) {
-  return base + (h == 32 ? 0 : (h == 16 ? 32 * 32 : 32 * 32 + 16 * 16));
+  return base + (h == 32 ? 0
+                         : (h == 16 ? 32 * 32 : (h == 8 ? 32 * 32 + 16 * 16 : 32 * 32 + 16 * 16 + 8 * 8)));
 }
 
 // One 16 x 16 tile of sum_k fa(r, k) fb(c, k), k < kd (kd a multiple of 4),
@@ -212,30 +216,31 @@ __device__ __forceinline__ d4 mma16(FA fa, FB fb, int kd) {
   return acc;
 }
 
-// leaf: factor and invert the 8 x 8 diagonal block at o (updated in place)
-__device__ __forceinline__ void leaf8(double* A, double* X, int o, int nbk, int64_t k0,
-                                      int* status) {
-  double D[8][8], Xi[8][8], rs[8];
+// leaf: factor and invert the NL x NL diagonal block at o (updated in place)
+template <int NL>
+__device__ __forceinline__ void leaf(double* A, double* X, int o, int nbk, int64_t k0,
+                                     int* status) {
+  double D[NL][NL], Xi[NL][NL], rs[NL];
 #pragma unroll
-  for (int a = 0; a < 8; ++a)
+  for (int a = 0; a < NL; ++a)
 #pragma unroll
     for (int b = 0; b <= a; ++b) D[a][b] = A[(o + a) * kQ + o + b];
 #pragma unroll
-  for (int a = 0; a < 8; ++a) {
+  for (int a = 0; a < NL; ++a) {
     const double d = D[a][a];
     if (threadIdx.x == 0 && o + a < nbk && !(d > 0.0)) atomicMin(status, (int)(k0 + o + a));
     rs[a] = rsqrt_f64(d);
     D[a][a] = d * rs[a];
 #pragma unroll
-    for (int b = a + 1; b < 8; ++b) D[b][a] *= rs[a];
+    for (int b = a + 1; b < NL; ++b) D[b][a] *= rs[a];
 #pragma unroll
-    for (int b = a + 1; b < 8; ++b)
+    for (int b = a + 1; b < NL; ++b)
 #pragma unroll
       for (int c = a + 1; c <= b; ++c) D[b][c] -= D[b][a] * D[c][a];
   }
   // Xi = L^-1 by rows: Xi[a][c] = -(1 / L_aa) sum_{c <= k < a} L[a][k] Xi[k][c]
 #pragma unroll
-  for (int a = 0; a < 8; ++a) {
+  for (int a = 0; a < NL; ++a) {
     Xi[a][a] = rs[a];
 #pragma unroll
     for (int c = 0; c < a; ++c) {
@@ -247,10 +252,10 @@ __device__ __forceinline__ void leaf8(double* A, double* X, int o, int nbk, int6
   }
   __syncthreads();   // every wave has read the block before it is overwritten
   if (threadIdx.x == 0) {
-    // one lane stores the 36 + 36 values (the entries above the diagonal
+    // one lane stores the NL (NL + 1) / 2 values of each (the entries above the diagonal
     // are zero already)
 #pragma unroll
-    for (int a = 0; a < 8; ++a)
+    for (int a = 0; a < NL; ++a)
 #pragma unroll
       for (int c = 0; c <= a; ++c) {
         A[(o + a) * kQ + o + c] = D[a][c];
@@ -362,8 +367,8 @@ __device__ __forceinline__ void finish_inverse(double* X, double* scr, int o) {
 template <int N>
 __device__ __forceinline__ void chol_inv(double* A, double* X, double* scr, int o, int nbk,
                                          int64_t k0, int* status) {
-  if constexpr (N == 8) {
-    leaf8(A, X, o, nbk, k0, status);
+  if constexpr (N == kLeaf) {
+    leaf<kLeaf>(A, X, o, nbk, k0, status);
   } else {
     constexpr int H = N / 2;
     chol_inv<H>(A, X, scr, o, nbk, k0, status);
