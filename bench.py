@@ -303,7 +303,7 @@ def mlp_stack(args):
 
     for mu, K in ((1.0, 0), (1.0, 16), (0.6, 0), (0.6, 16)):
         X, Xq = X0, X0
-        errs, qtimes, dq = [], [], []
+        errs, qtimes, dq, dq_tiles = [], [], [], []
         for l, W in enumerate(Ws):
             torch.cuda.synchronize()
             t0 = time.perf_counter()
@@ -318,9 +318,14 @@ def mlp_stack(args):
             pp = packing_perm(args, q)                   # decode order, position groups
             P = ok.pack_codes(q.codes, bits, pp)
             Xq16 = Xq.half()
+            ws = torch.empty(ok.library().ojbkq_dequant_matmul_workspace_bytes(d, d),
+                             dtype=torch.uint8, device=dev)
             Yq, ms = product_ms(lambda: ok.dequant_matmul(P, q.scales, q.zeros, d, bits, group,
-                                                          Xq16, pp))
+                                                          Xq16, pp, workspace=ws))
             dq.append(ms)
+            _, ms_tiles = product_ms(lambda: ok.dequant_matmul(P, q.scales, q.zeros, d, bits,
+                                                               group, Xq16, pp, workspace=False))
+            dq_tiles.append(ms_tiles)
             Y = W @ X                                  # the full-precision stack
             errs.append(float((Yq - Y).norm() / Y.norm()))
             X, Xq = silu(Y), silu(Yq)
@@ -330,6 +335,8 @@ def mlp_stack(args):
                 "bits": bits, "group": group, "scheme": args.scheme,
                 "act_order": args.act_order, "relative_output_error": errs, "quantize_s": qtimes,
                 "dequant_matmul_ms": dq,
+                # the same product without a workspace (dequantized per tile)
+                "dequant_matmul_per_tile_ms": dq_tiles,
                 "dequant_matmul_roofline": {"bound": "mfma", "unit": "TFLOP/s",
                                             "achieved": flops / (min(dq) * 1e-3) / 1e12,
                                             "peak": PEAK_F16_MFMA_TFLOPS,

@@ -342,6 +342,23 @@ int ojbkq_dequant_matmul(const uint32_t* packed, const float* scales, const floa
                          int64_t T, int64_t ldx, const int32_t* perm, float* Y, int64_t ldy,
                          void* stream);
 
+/* ojbkq_dequant_matmul_ws: the same product (identical W_hat, identical
+ *   float32 sums up to their order), with W_hat formed once into a
+ *   caller-owned device workspace of ojbkq_dequant_matmul_workspace_bytes(n,
+ *   m) bytes (16-byte aligned; W_hat as fp16 [n, m rounded up to 64], zeros
+ *   past m) and then multiplied, instead of being dequantized again for
+ *   every tile of tokens: the faster form when T is large.  ENOSPACE for a
+ *   smaller workspace, EINVAL for a NULL or misaligned one and for the
+ *   argument errors of ojbkq_dequant_matmul.  Asynchronous on `stream`; the
+ *   workspace must stay untouched until the product has run.
+ * ojbkq_dequant_matmul_workspace_bytes: that size (0 for n < 1 or m < 1, or
+ *   sizes the product rejects).  Host-only.                              */
+size_t ojbkq_dequant_matmul_workspace_bytes(int64_t n, int64_t m);
+int ojbkq_dequant_matmul_ws(const uint32_t* packed, const float* scales, const float* zeros,
+                            int64_t n, int64_t m, int32_t bits, int32_t group, const uint16_t* X,
+                            int64_t T, int64_t ldx, const int32_t* perm, float* Y, int64_t ldy,
+                            void* workspace, size_t workspace_bytes, void* stream);
+
 /* Message of the last failure on this thread ("" if none). */
 const char* ojbkq_last_error(void);
 

@@ -33,7 +33,8 @@ ABI_FUNCTIONS = (
     "ojbkq_decode_stage", "ojbkq_klein_log_rho", "ojbkq_last_error", "ojbkq_set_timing",
     "ojbkq_stage_times", "ojbkq_set_weights", "ojbkq_packed_words", "ojbkq_pack_codes",
     "ojbkq_dequant_matmul", "ojbkq_set_knobs", "ojbkq_path_codes",
-    "ojbkq_quantize_layer_noalloc",
+    "ojbkq_quantize_layer_noalloc", "ojbkq_dequant_matmul_workspace_bytes",
+    "ojbkq_dequant_matmul_ws",
 )
 
 NOALLOC_SCRATCH_BYTES = 256 * 1024 * 1024   # OJBKQ_NOALLOC_SCRATCH_BYTES
@@ -89,6 +90,10 @@ def library() -> ctypes.CDLL:
         "ojbkq_pack_codes": (ctypes.c_int, [vp, i64, i64, ctypes.c_int32, vp, vp, vp]),
         "ojbkq_dequant_matmul": (ctypes.c_int, [vp, vp, vp, i64, i64, ctypes.c_int32,
                                                 ctypes.c_int32, vp, i64, i64, vp, vp, i64, vp]),
+        "ojbkq_dequant_matmul_workspace_bytes": (ctypes.c_size_t, [i64, i64]),
+        "ojbkq_dequant_matmul_ws": (ctypes.c_int, [vp, vp, vp, i64, i64, ctypes.c_int32,
+                                                   ctypes.c_int32, vp, i64, i64, vp, vp, i64, vp,
+                                                   ctypes.c_size_t, vp]),
         "ojbkq_accumulate": (ctypes.c_int, [vp, vp, vp, i64, i64]),
         "ojbkq_solve": (ctypes.c_int, [vp, vp, dp, vp, vp, vp, vp, vp, vp]),
         "ojbkq_destroy": (ctypes.c_int, [vp]),
@@ -481,10 +486,14 @@ def pack_codes(codes: torch.Tensor, bits: int, perm: Optional[torch.Tensor] = No
 
 def dequant_matmul(packed: torch.Tensor, scales: torch.Tensor, zeros: torch.Tensor, m: int,
                    bits: int, group: int, X: torch.Tensor,
-                   perm: Optional[torch.Tensor] = None) -> torch.Tensor:
-    """``ojbkq_dequant_matmul``: Y [n, T] float32 = W_hat [n, m] X [m, T] with
-    X float16 (rows contiguous) and W_hat from the packed codes (packed with
-    ``perm`` when one is given)."""
+                   perm: Optional[torch.Tensor] = None, workspace=True) -> torch.Tensor:
+    """Y [n, T] float32 = W_hat [n, m] X [m, T] with X float16 (rows
+    contiguous) and W_hat from the packed codes (packed with ``perm`` when one
+    is given).  ``workspace``: True (a device buffer of
+    ``ojbkq_dequant_matmul_workspace_bytes`` is allocated here and W_hat formed
+    there once, ``ojbkq_dequant_matmul_ws``), a uint8 device tensor to use as
+    that buffer, or False (``ojbkq_dequant_matmul``: dequantized per tile, no
+    buffer)."""
     dev = packed.device
     _need(packed, "packed", torch.int32, device=dev)
     n = packed.shape[0]
@@ -499,8 +508,21 @@ def dequant_matmul(packed: torch.Tensor, scales: torch.Tensor, zeros: torch.Tens
     T, ld = _rows_view(X, "X", m)
     perm = _perm_arg(perm, m, dev)
     Y = torch.empty(n, T, dtype=torch.float32, device=dev)
-    _check(library().ojbkq_dequant_matmul(_ptr(packed), _ptr(scales), _ptr(zeros), n, m,
-                                          int(bits), int(group), _ptr(X), T, ld, _ptr(perm),
-                                          _ptr(Y), T, _stream(dev)))
+    if workspace is False:
+        _check(library().ojbkq_dequant_matmul(_ptr(packed), _ptr(scales), _ptr(zeros), n, m,
+                                              int(bits), int(group), _ptr(X), T, ld, _ptr(perm),
+                                              _ptr(Y), T, _stream(dev)))
+        return Y
+    need = int(library().ojbkq_dequant_matmul_workspace_bytes(n, m))
+    if workspace is True:
+        ws = torch.empty(max(need, 1), dtype=torch.uint8, device=dev)
+    else:
+        ws = workspace
+        _need(ws, "workspace", torch.uint8, device=dev)
+        if not ws.is_contiguous():
+            raise ValueError("workspace must be contiguous")
+    _check(library().ojbkq_dequant_matmul_ws(_ptr(packed), _ptr(scales), _ptr(zeros), n, m,
+                                             int(bits), int(group), _ptr(X), T, ld, _ptr(perm),
+                                             _ptr(Y), T, _ptr(ws), ws.numel(), _stream(dev)))
     return Y
 

@@ -821,10 +821,12 @@ int ojbkq_pack_codes(const uint8_t* codes, int64_t n, int64_t m, int32_t bits,
   return OJBKQ_OK;
 }
 
-int ojbkq_dequant_matmul(const uint32_t* packed, const float* scales, const float* zeros,
-                         int64_t n, int64_t m, int32_t bits, int32_t group, const uint16_t* X,
-                         int64_t T, int64_t ldx, const int32_t* perm, float* Y, int64_t ldy,
-                         void* stream) {
+namespace {
+
+int dequant_matmul(const uint32_t* packed, const float* scales, const float* zeros, int64_t n,
+                   int64_t m, int32_t bits, int32_t group, const uint16_t* X, int64_t T,
+                   int64_t ldx, const int32_t* perm, float* Y, int64_t ldy, void* workspace,
+                   size_t workspace_bytes, void* stream) {
   g_error.clear();
   if (!packed || !scales || !zeros || !X || !Y)
     return fail(OJBKQ_EINVAL, "packed, scales, zeros, X and Y are required");
@@ -835,10 +837,43 @@ int ojbkq_dequant_matmul(const uint32_t* packed, const float* scales, const floa
   const int64_t g = (group <= 0 || group >= m) ? m : group;
   if (g % 16 != 0 && g != m)
     return fail(OJBKQ_EINVAL, "the group must be a multiple of 16 (or the whole column)");
+  if (workspace) {
+    if (workspace_bytes < ojbkq::dequant_matmul_workspace_bytes(n, m))
+      return fail(OJBKQ_ENOSPACE, "workspace smaller than ojbkq_dequant_matmul_workspace_bytes");
+    if (reinterpret_cast<uintptr_t>(workspace) % 16 != 0)
+      return fail(OJBKQ_EINVAL, "the workspace must be 16-byte aligned");
+  }
   OJBKQ_HIP(ojbkq::launch_dequant_matmul(packed, scales, zeros, n, m, bits, g, X, T, ldx, perm, Y,
-                                         ldy, static_cast<hipStream_t>(stream)),
+                                         ldy, workspace, static_cast<hipStream_t>(stream)),
             "dequantize and multiply");
   return OJBKQ_OK;
+}
+
+}  // namespace
+
+int ojbkq_dequant_matmul(const uint32_t* packed, const float* scales, const float* zeros,
+                         int64_t n, int64_t m, int32_t bits, int32_t group, const uint16_t* X,
+                         int64_t T, int64_t ldx, const int32_t* perm, float* Y, int64_t ldy,
+                         void* stream) {
+  return dequant_matmul(packed, scales, zeros, n, m, bits, group, X, T, ldx, perm, Y, ldy, nullptr,
+                        0, stream);
+}
+
+size_t ojbkq_dequant_matmul_workspace_bytes(int64_t n, int64_t m) {
+  if (n < 1 || m < 1 || n > (int64_t)1 << 24 || m > (int64_t)1 << 20) return 0;
+  return ojbkq::dequant_matmul_workspace_bytes(n, m);
+}
+
+int ojbkq_dequant_matmul_ws(const uint32_t* packed, const float* scales, const float* zeros,
+                            int64_t n, int64_t m, int32_t bits, int32_t group, const uint16_t* X,
+                            int64_t T, int64_t ldx, const int32_t* perm, float* Y, int64_t ldy,
+                            void* workspace, size_t workspace_bytes, void* stream) {
+  if (!workspace) {
+    g_error.clear();
+    return fail(OJBKQ_EINVAL, "workspace is NULL (ojbkq_dequant_matmul needs none)");
+  }
+  return dequant_matmul(packed, scales, zeros, n, m, bits, group, X, T, ldx, perm, Y, ldy,
+                        workspace, workspace_bytes, stream);
 }
 
 int ojbkq_set_knobs(ojbkq_ctx* ctx, double lambda_rel, int32_t K) {

@@ -50,7 +50,7 @@ __global__ __launch_bounds__(256) void pack_codes_kernel(const uint8_t* __restri
 
 // ---- dequantize and multiply -------------------------------------------------
 
-constexpr int kTileJ = 128;    // output rows (channels) per workgroup
+constexpr int kTileJ = 256;    // output rows (channels) per workgroup
 constexpr int kTileT = 256;    // output columns (tokens) per workgroup
 constexpr int kStage = 64;     // k per LDS stage: two v_mfma_f32_16x16x32_f16 k-steps
 constexpr int kLd = kStage + 8; // LDS row in halves: 144 bytes, 16-byte aligned
@@ -67,6 +67,8 @@ struct DqArgs {
   float* Y;
   int64_t ldy;
   int64_t tiles_n;
+  const _Float16* Wh;          // W_hat [n, mw] fp16 formed beforehand (null: dequantize in the product)
+  int64_t mw;                  // its row stride, m rounded up to a whole stage (zeros past m)
 };
 
 // Row of X that packed position k (< m) multiplies.
@@ -110,7 +112,7 @@ struct CodeLoader {
   }
 };
 
-constexpr int kThreads = 512;  // eight waves: 2 x 4 blocks of 64 channels x 64 tokens
+constexpr int kThreads = 512;  // eight waves: 4 x 2 blocks of 64 channels x 128 tokens
 
 // The activation tile in LDS keeps X's own layout, row k (a feature) with
 // the tile's 256 tokens contiguous, stored as 16-byte runs with no repacking;
@@ -136,21 +138,25 @@ __device__ __forceinline__ s4 read_tr(const _Float16* B, int k0, int t0, int i) 
       (s4 __attribute__((address_space(3)))*)(const_cast<_Float16*>(p)));
 }
 
-template <int BITS, bool VEC>
+// With kPre, W_hat comes ready-made from a.Wh (16-byte loads, staged like the
+// activations) and BITS is unused; every output element then takes the same
+// products in the same order as with the codes, so the two agree bit for bit.
+template <int BITS, bool VEC, bool kPre>
 __global__ __launch_bounds__(kThreads, 1) void dequant_matmul_kernel(DqArgs a) {
   // two buffers: the waves dequantize and stage step s + 1 into one while
   // their MFMAs read step s from the other, with one barrier per step
   __shared__ __align__(16) _Float16 sA[2][kTileJ * kLd];      // W_hat tile: row j, k contiguous
   __shared__ __align__(16) _Float16 sB[2][kStage * kLdB];     // X tile: row k, tokens contiguous
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wr = wave >> 2, wc = wave & 3;
+  const int wr = wave >> 1, wc = wave & 1;
   // consecutive workgroups take the channel tiles of one token tile, which
   // then stays in L2 while they read it
   const int64_t tj = (int64_t)blockIdx.x % a.tiles_n, tt = (int64_t)blockIdx.x / a.tiles_n;
   const int64_t J0 = tj * kTileJ, T0 = tt * kTileT;
 
-  // A loader: thread -> (row tid / 4, codes 16 (tid % 4) .. + 15 of the stage).
-  const int ar = tid >> 2, ac = tid & 3;
+  // A loader: thread -> row tid / 2, two runs of 16 codes of the stage,
+  // 32 (tid % 2) + 16 h .. + 15, h = 0, 1 (each inside one group: g % 16 == 0).
+  const int ar = tid >> 1, ac = tid & 1;
   const int64_t aj = J0 + ar;
   // The stage is interior when its 64 features and the tile's rows and
   // tokens all exist (the same for every lane): no clamping or masking then.
@@ -158,20 +164,27 @@ __global__ __launch_bounds__(kThreads, 1) void dequant_matmul_kernel(DqArgs a) {
   auto interior = [&](int64_t k0) { return VEC && tile_in && k0 + kStage <= a.m; };
 
   // this thread's channel row of the scales and zero points
-  const float* const sz_row[2] = {a.S + (aj < a.n ? aj : a.n - 1) * a.G,
-                                  a.Z + (aj < a.n ? aj : a.n - 1) * a.G};
+  const float* const s_row = a.S + (aj < a.n ? aj : a.n - 1) * a.G;
+  const float* const z_row = a.Z + (aj < a.n ? aj : a.n - 1) * a.G;
 
-  // What the dequantization of one stage reads: this thread's 16 codes and
-  // their group's scale and zero point, loaded a stage ahead.
-  CodeLoader<BITS> cl;
-  float s_cur = 0.f, z_cur = 0.f;
-  auto fetch_codes = [&](int64_t k0) {
-    const int64_t kc = k0 + 16 * ac;
-    cl.load(a, aj, kc);
+  // What the dequantization of one stage reads: this thread's two runs of
+  // codes with their groups' scales and zero points.  The stage being
+  // dequantized holds (c0, c1, s0 .. z1); the one after it is loaded into
+  // (n0, n1, ...) meanwhile, a whole stage ahead of its use.
+  CodeLoader<BITS> c0, c1, n0, n1;
+  float s0 = 0.f, z0 = 0.f, s1 = 0.f, z1 = 0.f, ns0 = 0.f, nz0 = 0.f, ns1 = 0.f, nz1 = 0.f;
+  auto fetch_codes = [&](int64_t k0, CodeLoader<BITS>& l0, CodeLoader<BITS>& l1, float& sa,
+                         float& za, float& sb, float& zb) {
+    const int64_t kc = k0 + 32 * ac;
+    l0.load(a, aj, kc);
+    l1.load(a, aj, kc + 16);
     // m < 2^20: the group index in 32-bit arithmetic
-    const uint32_t grp = (uint32_t)(kc < a.m ? kc : a.m - 1) / (uint32_t)a.g;
-    s_cur = sz_row[0][grp];
-    z_cur = sz_row[1][grp];
+    const uint32_t ga = (uint32_t)(kc < a.m ? kc : a.m - 1) / (uint32_t)a.g;
+    const uint32_t gb = (uint32_t)(kc + 16 < a.m ? kc + 16 : a.m - 1) / (uint32_t)a.g;
+    sa = s_row[ga];
+    za = z_row[ga];
+    sb = s_row[gb];
+    zb = z_row[gb];
   };
   // an interior stage of X: thread -> tokens 8 (tid % 32) .. + 7 of rows
   // tid / 32 + 16 q, q = 0..3, one 16-byte load each, held in registers (a
@@ -190,6 +203,28 @@ __global__ __launch_bounds__(kThreads, 1) void dequant_matmul_kernel(DqArgs a) {
       xv[4 * q + 2] = v.z;
       xv[4 * q + 3] = v.w;
     }
+  };
+  // kPre: this thread's 32 weights of the stage (row aj, features
+  // k0 + 32 (tid % 2) ..), four 16-byte loads, zero for rows past n
+  Runs wv;
+  auto fetch_w = [&](int64_t k0) {
+    const _Float16* row = a.Wh + (aj < a.n ? aj : a.n - 1) * a.mw + k0 + 32 * ac;
+    const bool ok = aj < a.n;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const uint4 v = *reinterpret_cast<const uint4*>(row + 8 * q);
+      wv[4 * q] = ok ? v.x : 0u;
+      wv[4 * q + 1] = ok ? v.y : 0u;
+      wv[4 * q + 2] = ok ? v.z : 0u;
+      wv[4 * q + 3] = ok ? v.w : 0u;
+    }
+  };
+  auto store_w = [&](int buf) {
+    _Float16* A = sA[buf] + ar * kLd + 32 * ac;
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
+      *reinterpret_cast<uint4*>(A + 8 * q) =
+          make_uint4(wv[4 * q], wv[4 * q + 1], wv[4 * q + 2], wv[4 * q + 3]);
   };
   auto store_x = [&](_Float16* B) {
 #pragma unroll
@@ -214,92 +249,143 @@ __global__ __launch_bounds__(kThreads, 1) void dequant_matmul_kernel(DqArgs a) {
       *reinterpret_cast<h8*>(B + xoff(r, 8 * bc)) = u;
     }
   };
-  // W_hat = fp16(fp32(s (q - z))) of the fetched codes into buffer `buf`,
-  // zero past the last feature or channel.  Two roundings: the empty asm pins
-  // the float32 product in a register, so it is not folded into
-  // v_fma_mixlo_f16, which rounds once to fp16.  q - z in fp32 (exact for the
-  // integer zero points a quantize call gives; a fractional z is honoured as
-  // the float it is).
-  auto dequant = [&](int64_t k0, int buf) {
-    _Float16* A = sA[buf];
-    const bool in = VEC && tile_in && k0 + kStage <= a.m;
+  // W_hat = fp16(fp32(s (q - z))) of code c of run h, zero past the last
+  // feature or channel.  Two roundings: the empty asm pins the float32
+  // product in a register, so it is not folded into v_fma_mixlo_f16, which
+  // rounds once to fp16.  q - z in fp32 (exact for the integer zero points a
+  // quantize call gives; a fractional z is honoured as the float it is).
+  auto weight = [&](const CodeLoader<BITS>& l, float sc, float zc, int c, int nvalid) {
+    float p = sc * ((float)l.code(c) - zc);
+    __asm__("" : "+v"(p));
+    const _Float16 w = (_Float16)p;
+    return c < nvalid ? w : (_Float16)0.f;
+  };
+  // how many of the 16 codes of the run at kc exist (all of them on an
+  // interior stage): the masks need no branch
+  auto valid = [&](int64_t kc, bool in) -> int {
+    if (in) return 16;
+    if (aj >= a.n || kc >= a.m) return 0;
+    return a.m - kc < 16 ? (int)(a.m - kc) : 16;
+  };
+  // the whole stage at k0 into buffer `buf` (the first stage)
+  auto dequant_all = [&](int64_t k0, int buf) {
+    _Float16* A = sA[buf] + ar * kLd + 32 * ac;
+    const bool in = interior(k0);
+    const int nv0 = valid(k0 + 32 * ac, in), nv1 = valid(k0 + 32 * ac + 16, in);
 #pragma unroll
-    for (int h = 0; h < 2; ++h) {
-      h8 v;
+    for (int h = 0; h < 2; ++h)
 #pragma unroll
-      for (int c = 0; c < 8; ++c) {
-        const int cc = 8 * h + c;
-        float p = s_cur * ((float)cl.code(cc) - z_cur);
-        __asm__("" : "+v"(p));
-        const _Float16 w = (_Float16)p;
-        v[c] = (in || (aj < a.n && k0 + 16 * ac + cc < a.m)) ? w : (_Float16)0.f;
+      for (int e = 0; e < 2; ++e) {
+        h8 v;
+#pragma unroll
+        for (int c = 0; c < 8; ++c)
+          v[c] = h ? weight(c1, s1, z1, 8 * e + c, nv1) : weight(c0, s0, z0, 8 * e + c, nv0);
+        *reinterpret_cast<h8*>(A + 16 * h + 8 * e) = v;
       }
-      *reinterpret_cast<h8*>(A + ar * kLd + 16 * ac + 8 * h) = v;
-    }
   };
 
-  f4 acc[4][4];
+  f4 acc[4][8];
 #pragma unroll
   for (int x = 0; x < 4; ++x)
 #pragma unroll
-    for (int y = 0; y < 4; ++y) acc[x][y] = f4{0.f, 0.f, 0.f, 0.f};
+    for (int y = 0; y < 8; ++y) acc[x][y] = f4{0.f, 0.f, 0.f, 0.f};
 
   const int g16 = lane >> 4, i16 = lane & 15;
-  // the products of the stage in buffer `buf`
-  auto compute = [&](int buf) {
-    const _Float16* A = sA[buf];
-    const _Float16* B = sB[buf];
+  // The products of the stage in buffer `cur` (two k-steps of 32, each 4 x 8
+  // tiles of v_mfma_f32_16x16x32_f16).  With `dq`, run ks of the next stage
+  // (at kn, into buffer `nxt`) is dequantized beside k-step ks: one weight
+  // after each product, its 16-byte LDS stores as they fill, the order kept
+  // by scheduling barriers so that the vector ALU and the matrix cores work
+  // side by side.
+  auto compute = [&](int cur, int nxt, int64_t kn, bool dq, bool in_n) {
+    const _Float16* A = sA[cur];
+    const _Float16* B = sB[cur];
+    _Float16* An = sA[nxt] + ar * kLd + 32 * ac;
+    const int nv0 = valid(kn + 32 * ac, in_n), nv1 = valid(kn + 32 * ac + 16, in_n);
 #pragma unroll
     for (int ks = 0; ks < 2; ++ks) {
-      h8 fa[4], fb[4];
+      h8 fa[4];
 #pragma unroll
       for (int x = 0; x < 4; ++x)
         fa[x] = *reinterpret_cast<const h8*>(A + (wr * 64 + x * 16 + i16) * kLd + 32 * ks +
                                              8 * g16);
-#pragma unroll
-      for (int y = 0; y < 4; ++y) {
-        // features 32 ks + 8 g16 .. + 7 of token wc 64 + 16 y + i16
-        const int k0 = 32 * ks + 8 * g16, t0 = wc * 64 + y * 16;
+      // features 32 ks + 8 g16 .. + 7 of token wc 128 + 16 y + i16, one
+      // token block ahead of its products
+      auto load_b = [&](int y) {
+        const int k0 = 32 * ks + 8 * g16, t0 = wc * 128 + y * 16;
         const s4 lo = read_tr(B, k0, t0, i16), hi = read_tr(B, k0 + 4, t0, i16);
-        fb[y] = __builtin_bit_cast(h8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+        return __builtin_bit_cast(h8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+      };
+      h8 fb = load_b(0), v;
+#pragma unroll
+      for (int y = 0; y < 8; ++y) {
+        const h8 fbc = fb;
+        if (y + 1 < 8) fb = load_b(y + 1);
+#pragma unroll
+        for (int x = 0; x < 4; ++x) {
+          acc[x][y] = __builtin_amdgcn_mfma_f32_16x16x32_f16(fa[x], fbc, acc[x][y], 0, 0, 0);
+          const int i = 4 * y + x;
+          if (!kPre && (i & 1) == 0) {
+            // (computed on the last stage too, where nothing is stored: no
+            // branch around each weight)
+            const int c = i >> 1;   // code c of run ks
+            v[c & 7] = ks ? weight(c1, s1, z1, c, nv1) : weight(c0, s0, z0, c, nv0);
+            if ((c & 7) == 7 && dq) *reinterpret_cast<h8*>(An + 16 * ks + (c & 8)) = v;
+          }
+          __builtin_amdgcn_sched_barrier(0);
+        }
       }
-#pragma unroll
-      for (int x = 0; x < 4; ++x)
-#pragma unroll
-        for (int y = 0; y < 4; ++y)
-          acc[x][y] = __builtin_amdgcn_mfma_f32_16x16x32_f16(fa[x], fb[y], acc[x][y], 0, 0, 0);
     }
   };
 
   // Stage st computes from buffer st % 2 while the codes and activations of
   // stage st + 1 stream in (the activations straight into the other buffer)
-  // and are dequantized into it after the products.
+  // and are dequantized into it beside the products.
   const int64_t nst = (a.m + kStage - 1) / kStage;
-  fetch_codes(0);
+  if constexpr (kPre) {
+    fetch_w(0);
+    store_w(0);
+  } else {
+    fetch_codes(0, c0, c1, s0, z0, s1, z1);
+  }
   if (interior(0)) {
     fetch_x(0);
     store_x(sB[0]);
   } else {
     stage_x_edge(0, sB[0]);
   }
-  dequant(0, 0);
+  if constexpr (!kPre) {
+    dequant_all(0, 0);
+    if (nst > 1) fetch_codes(kStage, n0, n1, ns0, nz0, ns1, nz1);
+  }
   __syncthreads();
   for (int64_t st = 0; st < nst; ++st) {
     const int cur = (int)(st & 1), nxt = cur ^ 1;
     const int64_t kn = (st + 1) * kStage;
     const bool more = st + 1 < nst;
-    if (more) {
-      fetch_codes(kn);
-      if (interior(kn)) fetch_x(kn);
+    if constexpr (kPre) {
+      if (more) fetch_w(kn);
+    } else {
+      // the next stage's codes (loaded a stage ago) into place, the one
+      // after it on its way
+      c0 = n0;
+      c1 = n1;
+      s0 = ns0;
+      z0 = nz0;
+      s1 = ns1;
+      z1 = nz1;
+      if (st + 2 < nst) fetch_codes(kn + kStage, n0, n1, ns0, nz0, ns1, nz1);
     }
-    compute(cur);
+    const bool in_n = more && interior(kn);
+    if (in_n) fetch_x(kn);
     // buffer nxt was last read in step st - 1, before the barrier that ended it
+    compute(cur, nxt, kn, more, in_n);
     if (more) {
-      if (interior(kn))
+      if constexpr (kPre) store_w(nxt);
+      if (in_n)
         store_x(sB[nxt]);
       else
         stage_x_edge(kn, sB[nxt]);
-      dequant(kn, nxt);
     }
     __syncthreads();
   }
@@ -308,23 +394,69 @@ __global__ __launch_bounds__(kThreads, 1) void dequant_matmul_kernel(DqArgs a) {
 #pragma unroll
   for (int x = 0; x < 4; ++x)
 #pragma unroll
-    for (int y = 0; y < 4; ++y)
+    for (int y = 0; y < 8; ++y)
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         const int64_t j = J0 + wr * 64 + x * 16 + 4 * (lane >> 4) + r;
-        const int64_t t = T0 + wc * 64 + y * 16 + (lane & 15);
+        const int64_t t = T0 + wc * 128 + y * 16 + (lane & 15);
         if (j < a.n && t < a.T) a.Y[j * a.ldy + t] = acc[x][y][r];
       }
 }
+
+// ---- the product with W_hat formed beforehand ----------------------------------
 
 template <int BITS>
 hipError_t launch_dq(const DqArgs& a, int64_t tiles, hipStream_t s) {
   // 16-byte activation loads: rows 16-byte aligned (X 16-byte aligned, ldx % 8 == 0)
   const bool vec = reinterpret_cast<uintptr_t>(a.X) % 16 == 0 && a.ldx % 8 == 0;
-  if (vec)
-    dequant_matmul_kernel<BITS, true><<<dim3((unsigned)tiles), dim3(kThreads), 0, s>>>(a);
-  else
-    dequant_matmul_kernel<BITS, false><<<dim3((unsigned)tiles), dim3(kThreads), 0, s>>>(a);
+  if (a.Wh) {
+    if (vec)
+      dequant_matmul_kernel<1, true, true><<<dim3((unsigned)tiles), dim3(kThreads), 0, s>>>(a);
+    else
+      dequant_matmul_kernel<1, false, true><<<dim3((unsigned)tiles), dim3(kThreads), 0, s>>>(a);
+  } else if (vec) {
+    dequant_matmul_kernel<BITS, true, false><<<dim3((unsigned)tiles), dim3(kThreads), 0, s>>>(a);
+  } else {
+    dequant_matmul_kernel<BITS, false, false><<<dim3((unsigned)tiles), dim3(kThreads), 0, s>>>(a);
+  }
+  return hipGetLastError();
+}
+
+// W_hat [n, mw] fp16 = fp16(fp32(s (q - z))) of the packed codes, zeros for
+// features m .. mw - 1: one thread per 16 weights (one run of 16 codes inside
+// one group, g % 16 == 0), written as two 16-byte stores.
+template <int BITS>
+__global__ __launch_bounds__(256) void dequant_weights_kernel(DqArgs a, _Float16* W) {
+  const int64_t runs = a.mw / 16, total = a.n * runs;
+  for (int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x; e < total;
+       e += (int64_t)gridDim.x * 256) {
+    const int64_t j = e / runs, kc = (e % runs) * 16;
+    CodeLoader<BITS> l;
+    l.load(a, j, kc < a.m ? kc : 0);
+    const uint32_t grp = (uint32_t)(kc < a.m ? kc : a.m - 1) / (uint32_t)a.g;
+    const float sc = a.S[j * a.G + grp], zc = a.Z[j * a.G + grp];
+    const int nv = kc >= a.m ? 0 : (a.m - kc < 16 ? (int)(a.m - kc) : 16);
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      h8 v;
+#pragma unroll
+      for (int c = 0; c < 8; ++c) {
+        // two roundings, as in the product: the asm keeps the float32 product
+        float p = sc * ((float)l.code(8 * h + c) - zc);
+        __asm__("" : "+v"(p));
+        v[c] = 8 * h + c < nv ? (_Float16)p : (_Float16)0.f;
+      }
+      *reinterpret_cast<h8*>(W + j * a.mw + kc + 8 * h) = v;
+    }
+  }
+}
+
+template <int BITS>
+hipError_t launch_dqw(const DqArgs& a, _Float16* W, hipStream_t s) {
+  const int64_t total = a.n * (a.mw / 16);
+  const int64_t blocks = (total + 255) / 256;
+  dequant_weights_kernel<BITS><<<dim3((unsigned)(blocks < 65536 ? blocks : 65536)), dim3(256), 0,
+                                  s>>>(a, W);
   return hipGetLastError();
 }
 
@@ -342,10 +474,15 @@ hipError_t launch_pack_codes(const uint8_t* codes, int64_t n, int64_t m, int bit
   return hipGetLastError();
 }
 
+size_t dequant_matmul_workspace_bytes(int64_t n, int64_t m) {
+  if (n <= 0 || m <= 0) return 0;
+  return (size_t)n * (size_t)((m + kStage - 1) / kStage * kStage) * sizeof(_Float16);
+}
+
 hipError_t launch_dequant_matmul(const uint32_t* P, const float* S, const float* Z, int64_t n,
                                  int64_t m, int bits, int64_t g, const uint16_t* X, int64_t T,
                                  int64_t ldx, const int32_t* perm, float* Y, int64_t ldy,
-                                 hipStream_t stream) {
+                                 void* workspace, hipStream_t stream) {
   if (n <= 0 || T <= 0) return hipSuccess;
   DqArgs a;
   a.P = P;
@@ -363,8 +500,29 @@ hipError_t launch_dequant_matmul(const uint32_t* P, const float* S, const float*
   a.Y = Y;
   a.ldy = ldy;
   a.tiles_n = (n + kTileJ - 1) / kTileJ;
+  a.mw = (m + kStage - 1) / kStage * kStage;
+  a.Wh = nullptr;
   const int64_t tiles = a.tiles_n * ((T + kTileT - 1) / kTileT);
   if (tiles > 0x7fffffff) return hipErrorInvalidValue;
+  if (workspace) {
+    // W_hat once, then the product reads it instead of dequantizing every tile
+    _Float16* W = static_cast<_Float16*>(workspace);
+    hipError_t e = hipSuccess;
+    switch (bits) {
+      case 1: e = launch_dqw<1>(a, W, stream); break;
+      case 2: e = launch_dqw<2>(a, W, stream); break;
+      case 3: e = launch_dqw<3>(a, W, stream); break;
+      case 4: e = launch_dqw<4>(a, W, stream); break;
+      case 5: e = launch_dqw<5>(a, W, stream); break;
+      case 6: e = launch_dqw<6>(a, W, stream); break;
+      case 7: e = launch_dqw<7>(a, W, stream); break;
+      case 8: e = launch_dqw<8>(a, W, stream); break;
+      default: return hipErrorInvalidValue;
+    }
+    if (e != hipSuccess) return e;
+    a.Wh = W;
+    return launch_dq<1>(a, tiles, stream);
+  }
   switch (bits) {
     case 1: return launch_dq<1>(a, tiles, stream);
     case 2: return launch_dq<2>(a, tiles, stream);

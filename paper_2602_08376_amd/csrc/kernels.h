@@ -322,10 +322,14 @@ hipError_t launch_pack_codes(const uint8_t* codes, int64_t n, int64_t m, int bit
 // from P and the [n, ceil(m / g)] scales / zero points; X [m, T] fp16 bits,
 // row stride ldx.  Needs g % 16 == 0 or g == m.  With perm (or null), the
 // packed position k multiplies row perm[k] of X (clamped to [0, m)).
+// workspace: null, or dequant_matmul_workspace_bytes(n, m) bytes: then W_hat
+// is formed there once (fp16, rows padded with zeros to a whole 64-feature
+// stage) and the product reads it instead of dequantizing every tile.
+size_t dequant_matmul_workspace_bytes(int64_t n, int64_t m);
 hipError_t launch_dequant_matmul(const uint32_t* P, const float* S, const float* Z, int64_t n,
                                  int64_t m, int bits, int64_t g, const uint16_t* X, int64_t T,
                                  int64_t ldx, const int32_t* perm, float* Y, int64_t ldy,
-                                 hipStream_t stream);
+                                 void* workspace, hipStream_t stream);
 
 // First strict minimum over the K + 1 candidates of each column; gathers the
 // winner's codes.  Every output may be null (codes null: no winner gather).

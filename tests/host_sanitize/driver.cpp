@@ -268,6 +268,24 @@ int main() {
                                 32, X.as<uint16_t>(), T, T - 1, nullptr, Y.as<float>(), T,
                                 nullptr),
            OJBKQ_EINVAL, "dequant matmul ldx");
+    const size_t wsb = ojbkq_dequant_matmul_workspace_bytes(n, m);
+    Buf ws(wsb + 16);
+    expect(ojbkq_dequant_matmul_ws(packed.as<uint32_t>(), sc.as<float>(), z.as<float>(), n, m,
+                                   bits, 32, X.as<uint16_t>(), T, T, perm.as<int32_t>(),
+                                   Y.as<float>(), T, ws.p, wsb, nullptr),
+           OJBKQ_OK, "dequant matmul with workspace");
+    expect(ojbkq_dequant_matmul_ws(packed.as<uint32_t>(), sc.as<float>(), z.as<float>(), n, m,
+                                   bits, 32, X.as<uint16_t>(), T, T, nullptr, Y.as<float>(), T,
+                                   ws.p, wsb - 1, nullptr),
+           OJBKQ_ENOSPACE, "dequant matmul workspace size");
+    expect(ojbkq_dequant_matmul_ws(packed.as<uint32_t>(), sc.as<float>(), z.as<float>(), n, m,
+                                   bits, 32, X.as<uint16_t>(), T, T, nullptr, Y.as<float>(), T,
+                                   ws.as<char>() + 1, wsb, nullptr),
+           OJBKQ_EINVAL, "dequant matmul workspace alignment");
+    expect(ojbkq_dequant_matmul_ws(packed.as<uint32_t>(), sc.as<float>(), z.as<float>(), n, m,
+                                   bits, 32, X.as<uint16_t>(), T, T, nullptr, Y.as<float>(), T,
+                                   nullptr, wsb, nullptr),
+           OJBKQ_EINVAL, "dequant matmul workspace null");
   }
   expect(ojbkq_pack_codes(nullptr, 3, 3, 4, nullptr, nullptr, nullptr), OJBKQ_EINVAL, "pack null");
   expect(ojbkq_pack_codes(nullptr, 3, 3, 0, nullptr, nullptr, nullptr), OJBKQ_EINVAL, "pack bits");

@@ -51,7 +51,9 @@ def _random_quantized(n, m, bits, group, seed):
     (100, 192, 200, 5, 64),     # 5-, 6-, 7-bit fields straddling words
     (33, 320, 77, 6, 32),
     (48, 224, 130, 7, 32),
-    (128, 256, 256, 4, 32),     # exactly one tile, interior stages only
+    (256, 256, 256, 4, 32),     # exactly one tile, interior stages only
+    (512, 1024, 768, 4, 128),   # several whole tiles in both directions
+    (768, 512, 512, 3, 64),
     (257, 129, 33, 2, 0),       # one group per column, m not a multiple of 16
     (16, 4096, 1000, 4, 128),   # a long contraction
 ])
@@ -61,15 +63,39 @@ def test_dequant_matmul_matches_oracle(n, m, T, bits, group):
     scale = np.exp(rng.standard_normal((m, 1))).astype(np.float32)
     X16 = (rng.standard_normal((m, T)).astype(np.float32) * scale).astype(np.float16)
     P = ok.pack_codes(torch.from_numpy(codes).to(DEV), bits)
-    Y = ok.dequant_matmul(P, torch.from_numpy(S).to(DEV), torch.from_numpy(Z).to(DEV), m, bits,
-                          group, torch.from_numpy(X16).to(DEV))
+    args = (P, torch.from_numpy(S).to(DEV), torch.from_numpy(Z).to(DEV), m, bits, group,
+            torch.from_numpy(X16).to(DEV))
+    # W_hat formed once in a workspace, and dequantized tile by tile: the same
+    # weights and the same sums in the same order, so the same bits
+    Y = ok.dequant_matmul(*args, workspace=True)
+    Y_tiles = ok.dequant_matmul(*args, workspace=False)
     torch.cuda.synchronize()
+    assert torch.equal(Y, Y_tiles)
     W16 = oi.dequantize_fp16(codes, S, Z, group)
     ref = oi.dequant_matmul(W16, X16)
     bound = oi.summation_bound(W16, X16)
     err = np.abs(Y.cpu().numpy().astype(np.float64) - ref)
     print(f"[dequant {n}x{m}x{T} b{bits} g{group}] max err / bound {np.max(err / (bound + 1e-300)):.3f}")
     assert np.all(err <= bound + 1e-30)
+
+
+def test_dequant_matmul_workspace_errors():
+    codes, S, Z = _random_quantized(40, 96, 4, 32, 5)
+    P = ok.pack_codes(torch.from_numpy(codes).to(DEV), 4)
+    X16 = torch.zeros(96, 50, dtype=torch.float16, device=DEV)
+    args = (P, torch.from_numpy(S).to(DEV), torch.from_numpy(Z).to(DEV), 96, 4, 32, X16)
+    need = ok.library().ojbkq_dequant_matmul_workspace_bytes(40, 96)
+    assert need == 40 * 128 * 2                  # rows padded to a whole 64-feature stage
+    small = torch.empty(need - 1, dtype=torch.uint8, device=DEV)
+    with pytest.raises(ok.OjbkqError) as ei:
+        ok.dequant_matmul(*args, workspace=small)
+    assert ei.value.status == -2                  # OJBKQ_ENOSPACE
+    buf = torch.empty(need + 16, dtype=torch.uint8, device=DEV)
+    with pytest.raises(ok.OjbkqError) as ei:
+        ok.dequant_matmul(*args, workspace=buf[1:])   # misaligned
+    assert ei.value.status == -1                  # OJBKQ_EINVAL
+    assert torch.equal(ok.dequant_matmul(*args, workspace=buf[16:]),
+                       ok.dequant_matmul(*args, workspace=False))
 
 
 def test_quantized_layer_forward():
