@@ -292,14 +292,17 @@ def mlp_stack(args):
     (X0, _), = list(activation_chunks(base, device=dev))
     silu = torch.nn.functional.silu
 
-    def product_ms(fn):
+    def product_ms(fn, reps=10):
+        # one call for the output, then the mean of `reps` back-to-back calls
         st = torch.cuda.current_stream(dev)
+        out = fn()
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         e0.record(st)
-        out = fn()
+        for _ in range(reps):
+            fn()
         e1.record(st)
         e1.synchronize()
-        return out, e0.elapsed_time(e1)
+        return out, e0.elapsed_time(e1) / reps
 
     for mu, K in ((1.0, 0), (1.0, 16), (0.6, 0), (0.6, 16)):
         X, Xq = X0, X0

@@ -74,4 +74,11 @@ __device__ __forceinline__ void load_to_lds16(const void* base, uint32_t off, co
                : "memory");
 }
 
+// The same with a full 64-bit global address per lane.
+__device__ __forceinline__ void load_to_lds16_at(const void* src, const void* lds) {
+  const uint32_t a = __builtin_amdgcn_readfirstlane(
+      (uint32_t)(uintptr_t)(const lds_void*)lds);
+  asm volatile("s_nop 0\n\tglobal_load_lds_dwordx4 %0, off" : : "v"(src), "{m0}"(a) : "memory");
+}
+
 }  // namespace ojbkq

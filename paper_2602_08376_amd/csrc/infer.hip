@@ -11,6 +11,7 @@
 //                          k-major by gfx950's transposing LDS read, W_hat
 //                          dequantized from the packed codes to fp16 in
 //                          LDS, products on v_mfma_f32_16x16x32_f16
+#include "device.h"
 #include "kernels.h"
 
 namespace ojbkq {
@@ -53,7 +54,12 @@ __global__ __launch_bounds__(256) void pack_codes_kernel(const uint8_t* __restri
 constexpr int kTileJ = 256;    // output rows (channels) per workgroup
 constexpr int kTileT = 256;    // output columns (tokens) per workgroup
 constexpr int kStage = 64;     // k per LDS stage: two v_mfma_f32_16x16x32_f16 k-steps
-constexpr int kLd = kStage + 8; // LDS row in halves: 144 bytes, 16-byte aligned
+// The W_hat tile in LDS: row j of the stage's 64 features (128 bytes, no
+// padding), its eight 16-byte chunks in the order chunk c at slot c ^ (j % 8).
+// Both the 16-byte stores of a row pair per lane pair and the MFMA reads of
+// 16 rows x 4 chunks then spread over all 64 banks (a padded pitch of 144 or
+// 160 bytes measured a two-way conflict on one or the other).
+__device__ __forceinline__ int aoff(int j, int c) { return j * kStage + 8 * (c ^ (j & 7)); }
 
 struct DqArgs {
   const uint32_t* P;
@@ -112,18 +118,18 @@ struct CodeLoader {
   }
 };
 
-constexpr int kThreads = 512;  // eight waves: 4 x 2 blocks of 64 channels x 128 tokens
+constexpr int kThreads = 512;  // eight waves, each a block of the 256 x 256 output tile
 
 // The activation tile in LDS keeps X's own layout, row k (a feature) with
-// the tile's 256 tokens contiguous, stored as 16-byte runs with no repacking;
-// pitch kLdB halves (544 bytes: rows k and k + 1 start 8 banks apart).  Its
-// 16-token blocks are XOR-swizzled by bit 3 of k, so the 8 rows that half a
-// wave reads in one transposing read (rows 8g .. 8g + 3 for lane groups
-// g = 0, 1, or 2, 3) fall in 64 distinct banks.  Offset (halves) of token t
-// of row k:
-constexpr int kLdB = kTileT + 16;
+// the tile's 256 tokens contiguous (512 bytes, no padding, so that two rows
+// fill the 1 KB that one direct-to-LDS load of a wave writes).  Its 16-token
+// blocks are XOR-swizzled by f(k) = (k % 4) + 4 (bit 3 of k), so the 8 rows
+// that half a wave reads in one transposing read (rows 8g .. 8g + 3 for lane
+// groups g = 0, 1, or 2, 3) fall in 64 distinct banks.  Offset (halves) of
+// token t of row k:
+__device__ __forceinline__ int xswz(int k) { return (k & 3) | (((k >> 3) & 1) << 2); }
 __device__ __forceinline__ int xoff(int k, int t) {
-  return k * kLdB + 16 * ((t >> 4) ^ (4 * ((k >> 3) & 1))) + (t & 15);
+  return k * kTileT + 16 * ((t >> 4) ^ xswz(k)) + (t & 15);
 }
 
 typedef short s4 __attribute__((ext_vector_type(4)));
@@ -138,20 +144,41 @@ __device__ __forceinline__ s4 read_tr(const _Float16* B, int k0, int t0, int i) 
       (s4 __attribute__((address_space(3)))*)(const_cast<_Float16*>(p)));
 }
 
-// With kPre, W_hat comes ready-made from a.Wh (16-byte loads, staged like the
-// activations) and BITS is unused; every output element then takes the same
+// Output tile of this workgroup.  Workgroups are dealt to the eight XCDs
+// round-robin by blockIdx, so the tiles are renumbered to give each XCD a
+// contiguous run, walked in groups of kGroupJ channel tiles with the token
+// tiles outer: the 32 workgroups an XCD runs at once then cover 8 channel
+// tiles x 4 token tiles and share those W_hat and activation panels in its
+// L2.
+constexpr int64_t kGroupJ = 8;
+__device__ __forceinline__ void dq_tile(int64_t tiles_n, int64_t& tj, int64_t& tt) {
+  const int64_t nb = gridDim.x, tiles_t = nb / tiles_n;
+  int64_t t = blockIdx.x;
+  if ((nb & 7) == 0) t = (t & 7) * (nb >> 3) + (t >> 3);
+  const int64_t per = kGroupJ * tiles_t, first = (t / per) * kGroupJ;
+  const int64_t rows = tiles_n - first < kGroupJ ? tiles_n - first : kGroupJ;
+  const int64_t r = t % per;
+  tj = first + r % rows;
+  tt = r / rows;
+}
+
+// With kPre, W_hat comes ready-made from a.Wh (loaded straight into LDS like
+// the activations) and BITS is unused; every output element then takes the same
 // products in the same order as with the codes, so the two agree bit for bit.
 template <int BITS, bool VEC, bool kPre>
 __global__ __launch_bounds__(kThreads, 1) void dequant_matmul_kernel(DqArgs a) {
   // two buffers: the waves dequantize and stage step s + 1 into one while
   // their MFMAs read step s from the other, with one barrier per step
-  __shared__ __align__(16) _Float16 sA[2][kTileJ * kLd];      // W_hat tile: row j, k contiguous
-  __shared__ __align__(16) _Float16 sB[2][kStage * kLdB];     // X tile: row k, tokens contiguous
+  __shared__ __align__(16) _Float16 sA[2][kTileJ * kStage];   // W_hat tile: row j, k contiguous
+  __shared__ __align__(16) _Float16 sB[2][kStage * kTileT];   // X tile: row k, tokens contiguous
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wr = wave >> 1, wc = wave & 1;
-  // consecutive workgroups take the channel tiles of one token tile, which
-  // then stays in L2 while they read it
-  const int64_t tj = (int64_t)blockIdx.x % a.tiles_n, tt = (int64_t)blockIdx.x / a.tiles_n;
+  // each wave's block: NX x NY products of 16 x 16, 2 x 4 blocks of 128
+  // channels x 64 tokens with W_hat ready-made (fewer transposing reads per
+  // product), 4 x 2 blocks of 64 x 128 when dequantizing (fewer registers)
+  constexpr int NX = kPre ? 8 : 4, NY = 32 / NX, kWc = 16 / NY;
+  const int wr = wave / kWc, wc = wave % kWc;
+  int64_t tj, tt;
+  dq_tile(a.tiles_n, tj, tt);
   const int64_t J0 = tj * kTileJ, T0 = tt * kTileT;
 
   // A loader: thread -> row tid / 2, two runs of 16 codes of the stage,
@@ -186,14 +213,28 @@ __global__ __launch_bounds__(kThreads, 1) void dequant_matmul_kernel(DqArgs a) {
     sb = s_row[gb];
     zb = z_row[gb];
   };
-  // an interior stage of X: thread -> tokens 8 (tid % 32) .. + 7 of rows
-  // tid / 32 + 16 q, q = 0..3, one 16-byte load each, held in registers (a
-  // vector, not an array: an array captured by these lambdas is moved to
-  // LDS) while the products run, then stored
+  // kPre: an interior stage of X straight into LDS: wave w's load q covers tile
+  // rows 2 (4 w + q) and + 1 (1 KB); lane l fills 16-byte slot l % 32 of row
+  // l / 32 of it, i.e. the 8 tokens of half (l % 2) of the swizzled block
+  // (l % 32) / 2.
+  auto fetch_x = [&](int64_t k0, int buf) {
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int r0 = 2 * (4 * wave + q), r = r0 + (lane >> 5);
+      const int u = ((lane & 31) >> 1) ^ xswz(r);
+      load_to_lds16_at(a.X + x_row(a, k0 + r) * a.ldx + T0 + 16 * u + 8 * (lane & 1),
+                       sB[buf] + r0 * kTileT);
+    }
+  };
+  // Without kPre (the registers are needed for dequantizing): the same
+  // stage through registers, thread -> tokens 8 (tid % 32) .. + 7 of rows
+  // tid / 32 + 16 q, one 16-byte load each, held (a vector, not an array:
+  // an array captured by these lambdas is moved to LDS) while the products
+  // run, then stored.
   const int bc = tid & 31, br = tid >> 5;
   typedef uint32_t Runs __attribute__((ext_vector_type(16)));
   Runs xv;
-  auto fetch_x = [&](int64_t k0) {
+  auto fetch_xv = [&](int64_t k0) {
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
       const uint4 v = *reinterpret_cast<const uint4*>(a.X + x_row(a, k0 + br + 16 * q) * a.ldx +
@@ -204,35 +245,26 @@ __global__ __launch_bounds__(kThreads, 1) void dequant_matmul_kernel(DqArgs a) {
       xv[4 * q + 3] = v.w;
     }
   };
-  // kPre: this thread's 32 weights of the stage (row aj, features
-  // k0 + 32 (tid % 2) ..), four 16-byte loads, zero for rows past n
-  Runs wv;
-  auto fetch_w = [&](int64_t k0) {
-    const _Float16* row = a.Wh + (aj < a.n ? aj : a.n - 1) * a.mw + k0 + 32 * ac;
-    const bool ok = aj < a.n;
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const uint4 v = *reinterpret_cast<const uint4*>(row + 8 * q);
-      wv[4 * q] = ok ? v.x : 0u;
-      wv[4 * q + 1] = ok ? v.y : 0u;
-      wv[4 * q + 2] = ok ? v.z : 0u;
-      wv[4 * q + 3] = ok ? v.w : 0u;
-    }
-  };
-  auto store_w = [&](int buf) {
-    _Float16* A = sA[buf] + ar * kLd + 32 * ac;
+  auto store_xv = [&](int buf) {
 #pragma unroll
     for (int q = 0; q < 4; ++q)
-      *reinterpret_cast<uint4*>(A + 8 * q) =
-          make_uint4(wv[4 * q], wv[4 * q + 1], wv[4 * q + 2], wv[4 * q + 3]);
-  };
-  auto store_x = [&](_Float16* B) {
-#pragma unroll
-    for (int q = 0; q < 4; ++q)
-      *reinterpret_cast<uint4*>(B + xoff(br + 16 * q, 8 * bc)) =
+      *reinterpret_cast<uint4*>(sB[buf] + xoff(br + 16 * q, 8 * bc)) =
           make_uint4(xv[4 * q], xv[4 * q + 1], xv[4 * q + 2], xv[4 * q + 3]);
   };
-  // an edge stage of X, element by element, zero past the last feature or token
+  // kPre: the stage of W_hat straight into LDS: wave w's load q covers tile
+  // rows 8 (4 w + q) .. + 7 (1 KB); lane l fills slot l % 8 of row l / 8 of
+  // it with chunk (l % 8) ^ (row % 8).  A row past n repeats row n - 1: it
+  // feeds only output rows that are never stored.
+  auto fetch_w = [&](int64_t k0, int buf) {
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int r0 = 8 * (4 * wave + q), r = r0 + (lane >> 3);
+      const int64_t j = J0 + r < a.n ? J0 + r : a.n - 1;
+      load_to_lds16_at(a.Wh + j * a.mw + k0 + 8 * ((lane & 7) ^ (r & 7)), sA[buf] + r0 * kStage);
+    }
+  };
+  // an edge stage of X, element by element, zero past the last feature or
+  // token, with the thread mapping of fetch_xv
   auto stage_x_edge = [&](int64_t k0, _Float16* B) {
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
@@ -269,7 +301,6 @@ __global__ __launch_bounds__(kThreads, 1) void dequant_matmul_kernel(DqArgs a) {
   };
   // the whole stage at k0 into buffer `buf` (the first stage)
   auto dequant_all = [&](int64_t k0, int buf) {
-    _Float16* A = sA[buf] + ar * kLd + 32 * ac;
     const bool in = interior(k0);
     const int nv0 = valid(k0 + 32 * ac, in), nv1 = valid(k0 + 32 * ac + 16, in);
 #pragma unroll
@@ -280,18 +311,18 @@ __global__ __launch_bounds__(kThreads, 1) void dequant_matmul_kernel(DqArgs a) {
 #pragma unroll
         for (int c = 0; c < 8; ++c)
           v[c] = h ? weight(c1, s1, z1, 8 * e + c, nv1) : weight(c0, s0, z0, 8 * e + c, nv0);
-        *reinterpret_cast<h8*>(A + 16 * h + 8 * e) = v;
+        *reinterpret_cast<h8*>(sA[buf] + aoff(ar, 4 * ac + 2 * h + e)) = v;
       }
   };
 
-  f4 acc[4][8];
+  f4 acc[NX][NY];
 #pragma unroll
-  for (int x = 0; x < 4; ++x)
+  for (int x = 0; x < NX; ++x)
 #pragma unroll
-    for (int y = 0; y < 8; ++y) acc[x][y] = f4{0.f, 0.f, 0.f, 0.f};
+    for (int y = 0; y < NY; ++y) acc[x][y] = f4{0.f, 0.f, 0.f, 0.f};
 
   const int g16 = lane >> 4, i16 = lane & 15;
-  // The products of the stage in buffer `cur` (two k-steps of 32, each 4 x 8
+  // The products of the stage in buffer `cur` (two k-steps of 32, each NX x NY
   // tiles of v_mfma_f32_16x16x32_f16).  With `dq`, run ks of the next stage
   // (at kn, into buffer `nxt`) is dequantized beside k-step ks: one weight
   // after each product, its 16-byte LDS stores as they fill, the order kept
@@ -300,37 +331,52 @@ __global__ __launch_bounds__(kThreads, 1) void dequant_matmul_kernel(DqArgs a) {
   auto compute = [&](int cur, int nxt, int64_t kn, bool dq, bool in_n) {
     const _Float16* A = sA[cur];
     const _Float16* B = sB[cur];
-    _Float16* An = sA[nxt] + ar * kLd + 32 * ac;
+    _Float16* An = sA[nxt];
     const int nv0 = valid(kn + 32 * ac, in_n), nv1 = valid(kn + 32 * ac + 16, in_n);
+    // A fragment x of k-step ks: rows 16 (NX wr + x) + i16, features
+    // 32 ks + 8 g16 .. + 7
+    auto load_a = [&](int ks, int x) {
+      return *reinterpret_cast<const h8*>(A + aoff(16 * (NX * wr + x) + i16, 4 * ks + g16));
+    };
+    // B fragment: features 32 ks + 8 g16 .. + 7 of token 16 (NY wc + y) + i16
+    auto load_b = [&](int ks, int y) {
+      const int k0 = 32 * ks + 8 * g16, t0 = 16 * (NY * wc + y);
+      const s4 lo = read_tr(B, k0, t0, i16), hi = read_tr(B, k0 + 4, t0, i16);
+      return __builtin_bit_cast(h8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+    };
+    // B one token block ahead of its products; in the last token block of
+    // k-step 0 each A fragment is reloaded for k-step 1 right after its last
+    // product, and B's first block of k-step 1 follows, so k-step 1 starts
+    // without waiting for LDS
+    h8 fa[NX];
+#pragma unroll
+    for (int x = 0; x < NX; ++x) fa[x] = load_a(0, x);
+    h8 fb = load_b(0, 0), v;
 #pragma unroll
     for (int ks = 0; ks < 2; ++ks) {
-      h8 fa[4];
 #pragma unroll
-      for (int x = 0; x < 4; ++x)
-        fa[x] = *reinterpret_cast<const h8*>(A + (wr * 64 + x * 16 + i16) * kLd + 32 * ks +
-                                             8 * g16);
-      // features 32 ks + 8 g16 .. + 7 of token wc 128 + 16 y + i16, one
-      // token block ahead of its products
-      auto load_b = [&](int y) {
-        const int k0 = 32 * ks + 8 * g16, t0 = wc * 128 + y * 16;
-        const s4 lo = read_tr(B, k0, t0, i16), hi = read_tr(B, k0 + 4, t0, i16);
-        return __builtin_bit_cast(h8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
-      };
-      h8 fb = load_b(0), v;
-#pragma unroll
-      for (int y = 0; y < 8; ++y) {
+      for (int y = 0; y < NY; ++y) {
         const h8 fbc = fb;
-        if (y + 1 < 8) fb = load_b(y + 1);
+        if (y + 1 < NY)
+          fb = load_b(ks, y + 1);
+        else if (ks == 0)
+          fb = load_b(1, 0);
 #pragma unroll
-        for (int x = 0; x < 4; ++x) {
+        for (int x = 0; x < NX; ++x) {
           acc[x][y] = __builtin_amdgcn_mfma_f32_16x16x32_f16(fa[x], fbc, acc[x][y], 0, 0, 0);
-          const int i = 4 * y + x;
+          if (ks == 0 && y + 1 == NY) fa[x] = load_a(1, x);
+          const int i = NX * y + x;
           if (!kPre && (i & 1) == 0) {
             // (computed on the last stage too, where nothing is stored: no
             // branch around each weight)
             const int c = i >> 1;   // code c of run ks
             v[c & 7] = ks ? weight(c1, s1, z1, c, nv1) : weight(c0, s0, z0, c, nv0);
-            if ((c & 7) == 7 && dq) *reinterpret_cast<h8*>(An + 16 * ks + (c & 8)) = v;
+            if ((c & 7) == 7 && dq) {
+              // the slot computed here, not held in a register all along
+              int r = ar;
+              __asm__("" : "+v"(r));
+              *reinterpret_cast<h8*>(An + aoff(r, 4 * ac + 2 * ks + (c >> 3))) = v;
+            }
           }
           __builtin_amdgcn_sched_barrier(0);
         }
@@ -338,33 +384,36 @@ __global__ __launch_bounds__(kThreads, 1) void dequant_matmul_kernel(DqArgs a) {
     }
   };
 
-  // Stage st computes from buffer st % 2 while the codes and activations of
-  // stage st + 1 stream in (the activations straight into the other buffer)
-  // and are dequantized into it beside the products.
+  // Stage st computes from buffer st % 2 while the activations (and W_hat)
+  // of stage st + 1 load straight into the other buffer, or its codes are
+  // dequantized into it beside the products.  vmcnt(0) before each barrier:
+  // the direct loads have landed in LDS.
   const int64_t nst = (a.m + kStage - 1) / kStage;
   if constexpr (kPre) {
-    fetch_w(0);
-    store_w(0);
+    fetch_w(0, 0);
   } else {
     fetch_codes(0, c0, c1, s0, z0, s1, z1);
   }
-  if (interior(0)) {
-    fetch_x(0);
-    store_x(sB[0]);
-  } else {
+  if (!interior(0)) {
     stage_x_edge(0, sB[0]);
+  } else if constexpr (kPre) {
+    fetch_x(0, 0);
+  } else {
+    fetch_xv(0);
+    store_xv(0);
   }
   if constexpr (!kPre) {
     dequant_all(0, 0);
     if (nst > 1) fetch_codes(kStage, n0, n1, ns0, nz0, ns1, nz1);
   }
+  __builtin_amdgcn_s_waitcnt(0x0f70);
   __syncthreads();
   for (int64_t st = 0; st < nst; ++st) {
     const int cur = (int)(st & 1), nxt = cur ^ 1;
     const int64_t kn = (st + 1) * kStage;
     const bool more = st + 1 < nst;
     if constexpr (kPre) {
-      if (more) fetch_w(kn);
+      if (more) fetch_w(kn, nxt);
     } else {
       // the next stage's codes (loaded a stage ago) into place, the one
       // after it on its way
@@ -377,28 +426,35 @@ __global__ __launch_bounds__(kThreads, 1) void dequant_matmul_kernel(DqArgs a) {
       if (st + 2 < nst) fetch_codes(kn + kStage, n0, n1, ns0, nz0, ns1, nz1);
     }
     const bool in_n = more && interior(kn);
-    if (in_n) fetch_x(kn);
     // buffer nxt was last read in step st - 1, before the barrier that ended it
+    if (in_n) {
+      if constexpr (kPre)
+        fetch_x(kn, nxt);
+      else
+        fetch_xv(kn);
+    }
     compute(cur, nxt, kn, more, in_n);
     if (more) {
-      if constexpr (kPre) store_w(nxt);
-      if (in_n)
-        store_x(sB[nxt]);
-      else
+      if (!in_n)
         stage_x_edge(kn, sB[nxt]);
+      else if constexpr (!kPre)
+        store_xv(nxt);
     }
+    // (also keeps the compiler from waiting for this step's code loads at
+    // the top of the next step: it cannot pair their conditions)
+    __builtin_amdgcn_s_waitcnt(0x0f70);
     __syncthreads();
   }
 
   // lane l holds D[4 (l / 16) + r][l % 16] of each 16x16 tile
 #pragma unroll
-  for (int x = 0; x < 4; ++x)
+  for (int x = 0; x < NX; ++x)
 #pragma unroll
-    for (int y = 0; y < 8; ++y)
+    for (int y = 0; y < NY; ++y)
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
-        const int64_t j = J0 + wr * 64 + x * 16 + 4 * (lane >> 4) + r;
-        const int64_t t = T0 + wc * 128 + y * 16 + (lane & 15);
+        const int64_t j = J0 + 16 * (NX * wr + x) + 4 * (lane >> 4) + r;
+        const int64_t t = T0 + 16 * (NY * wc + y) + (lane & 15);
         if (j < a.n && t < a.T) a.Y[j * a.ldy + t] = acc[x][y][r];
       }
 }
