@@ -213,6 +213,25 @@ __global__ __launch_bounds__(kThreads, 1) void dequant_matmul_kernel(DqArgs a) {
     sb = s_row[gb];
     zb = z_row[gb];
   };
+  // kPre: the X row of each of this thread's four loads of a stage (tile
+  // rows 2 (4 w + q) + l / 32: see fetch_x), read right after the loads of
+  // the stage before it are issued, so that with a permutation its entries
+  // arrive a whole step before the rows they address and no activation load
+  // waits on them.  (Without kPre the registers are needed for
+  // dequantizing: fetch_xv reads the entries where it uses them.)
+  // The entries are kept as read and clamped where used (any arithmetic on
+  // them here, or a second definition of the registers on the path without
+  // a permutation, would make the compiler wait for the loads at once).
+  int32_t prow[4] = {0, 0, 0, 0};
+  auto rows_for = [&](int64_t k0) {
+    if (a.perm) {
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int64_t k = k0 + 2 * (4 * wave + q) + (lane >> 5);
+        prow[q] = a.perm[k < a.m ? k : a.m - 1];
+      }
+    }
+  };
   // kPre: an interior stage of X straight into LDS: wave w's load q covers tile
   // rows 2 (4 w + q) and + 1 (1 KB); lane l fills 16-byte slot l % 32 of row
   // l / 32 of it, i.e. the 8 tokens of half (l % 2) of the swizzled block
@@ -222,7 +241,9 @@ __global__ __launch_bounds__(kThreads, 1) void dequant_matmul_kernel(DqArgs a) {
     for (int q = 0; q < 4; ++q) {
       const int r0 = 2 * (4 * wave + q), r = r0 + (lane >> 5);
       const int u = ((lane & 31) >> 1) ^ xswz(r);
-      load_to_lds16_at(a.X + x_row(a, k0 + r) * a.ldx + T0 + 16 * u + 8 * (lane & 1),
+      const int64_t row =
+          !a.perm ? k0 + r : (prow[q] < 0 ? 0 : (prow[q] >= a.m ? a.m - 1 : prow[q]));
+      load_to_lds16_at(a.X + row * a.ldx + T0 + 16 * u + 8 * (lane & 1),
                        sB[buf] + r0 * kTileT);
     }
   };
@@ -394,6 +415,7 @@ __global__ __launch_bounds__(kThreads, 1) void dequant_matmul_kernel(DqArgs a) {
   } else {
     fetch_codes(0, c0, c1, s0, z0, s1, z1);
   }
+  if constexpr (kPre) rows_for(0);
   if (!interior(0)) {
     stage_x_edge(0, sB[0]);
   } else if constexpr (kPre) {
@@ -402,6 +424,7 @@ __global__ __launch_bounds__(kThreads, 1) void dequant_matmul_kernel(DqArgs a) {
     fetch_xv(0);
     store_xv(0);
   }
+  if constexpr (kPre) rows_for(kStage);
   if constexpr (!kPre) {
     dequant_all(0, 0);
     if (nst > 1) fetch_codes(kStage, n0, n1, ns0, nz0, ns1, nz1);
@@ -432,6 +455,9 @@ __global__ __launch_bounds__(kThreads, 1) void dequant_matmul_kernel(DqArgs a) {
         fetch_x(kn, nxt);
       else
         fetch_xv(kn);
+    }
+    if constexpr (kPre) {
+      if (st + 2 < nst) rows_for(kn + kStage);
     }
     compute(cur, nxt, kn, more, in_n);
     if (more) {

@@ -163,6 +163,9 @@ def test_act_order_staged_sweep_and_chunks():
 @pytest.mark.parametrize("n,m,T,bits,group", [
     (96, 256, 300, 4, 128),     # act-order codes of a quantize call
     (70, 200, 133, 3, 32),      # ragged channels, features and tokens, 3-bit fields
+    (256, 512, 512, 4, 128),    # whole 256 x 256 tiles: every stage gathered by the kernels'
+                                #   own loads (rows of the next stage read a step ahead)
+    (320, 640, 300, 3, 64),     # one whole tile beside ragged ones
 ])
 def test_packed_product_in_decode_order(n, m, T, bits, group):
     """Codes packed in decode order (position p holds feature perm[p]) and
@@ -175,7 +178,10 @@ def test_packed_product_in_decode_order(n, m, T, bits, group):
     P = ok.pack_codes(q.codes, bits, q.perm)
     X16 = Xq.half()
     Y = ok.dequant_matmul(P, q.scales, q.zeros, m, bits, group, X16, q.perm)
+    Y_tiles = ok.dequant_matmul(P, q.scales, q.zeros, m, bits, group, X16, q.perm,
+                                workspace=False)
     torch.cuda.synchronize()
+    assert torch.equal(Y, Y_tiles)              # W_hat once or per tile: the same bits
     perm = np64(q.perm).astype(np.int64)
     codes = np64(q.codes)
     assert np.array_equal(P.cpu().numpy().view(np.uint32), oi.pack_codes(codes[:, perm], bits))
