@@ -35,10 +35,6 @@ constexpr int kT = 64;                    // tile edge
 constexpr int kTT = kT * kT;              // doubles per tile
 constexpr int kThreads = 256;             // four waves
 constexpr uint32_t kSpinLimit = 1u << 21; // polls of one flag before the launch gives up
-// LDS: two operand tiles, or the diagonal block and its inverse (pitch
-// kT + 1) and the scratch of the recursive factor
-constexpr int kLdsDoubles = 2 * kT * (kT + 1) + 2 * (32 * 32 + 16 * 16 + 8 * 8);
-static_assert(2 * kTT <= kLdsDoubles, "operand tiles fit");
 
 // Swizzled row-major tile in LDS: element (r, k) at r * 64 + (k ^ 2 (r % 16)).
 // The 32 (row, k) pairs that half a wave reads for an MFMA operand (16 rows,
@@ -81,12 +77,19 @@ __device__ bool wait_flag(const int* flag, int* err) {
   }
 }
 
-// Every thread makes its tile stores visible device-wide (agent-scope
-// release fence), the workgroup meets, then thread 0 sets the flag.
-__device__ __forceinline__ void publish(int* flag) {
+// Every thread completes its tile stores (workgroup-scope release), the
+// workgroup meets, then one thread makes them visible device-wide (an
+// agent-scope release, cumulative over what the barrier ordered before it:
+// the mirror of wait_flag, where one thread acquires and a barrier follows)
+// and sets the flag.  One agent-scope fence per tile instead of one per wave.
+__device__ __forceinline__ void release_flag(int* flag) {
   __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+  __hip_atomic_store(flag, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void publish(int* flag) {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
   __syncthreads();
-  if (threadIdx.x == 0) __hip_atomic_store(flag, 1, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+  if (threadIdx.x == 0) release_flag(flag);
 }
 
 // Tile (r0, c0) of a row-major [m, m] matrix in the swizzled LDS layout,
@@ -195,36 +198,82 @@ __device__ __forceinline__ double rsqrt_f64(double d) {
 // 16 x 16 tiles dealt to the four waves (a smaller product is one masked
 // tile).  The leaves sit on the serial chain, whose latency grows with their
 // size cubed: 4 x 4 leaves took the 64 x 64 block 3% faster than 8 x 8 ones.
-// A and X are row-major with pitch kQ; S and T are per-level scratch.
-constexpr int kQ = kT + 1;
+// Layouts in LDS, chosen so that the MFMA operand reads, 16 rows (or
+// columns) by 4 k per instruction, fall in distinct banks (one double =
+// two of the 64 four-byte banks, so 32 lanes of 8-byte reads fill them):
+// - A and X: row R at R * 64, element C at C ^ g(R), g(R) = 2 (R % 16) with
+//   bit 4 flipped for odd R: conflict-free both for 16 rows x 2 k (the row
+//   operands) and for 2 rows x 16 columns (X read column-wise by T = S X11);
+//   the pitch 65 used before conflicted two- to four-way on both;
+// - S (read by rows): pitch h + 2; T (read by columns): pitch 48 for h = 32,
+//   h below (the pitch 32 conflicted 16-way on the row reads).
 constexpr int kLeaf = 4;   // leaf size of the recursion
-constexpr int kScr = 32 * 32 + 16 * 16 + 8 * 8 + 4 * 4;   // one scratch set of all levels
+__device__ __forceinline__ int bq(int r, int c) {
+  return r * kT + (c ^ (((2 * r) & 31) ^ ((r & 1) << 4)));
+}
+__host__ __device__ constexpr int s_pitch(int h) { return h + 2; }
+__host__ __device__ constexpr int t_pitch(int h) { return h == 32 ? 48 : h; }
+constexpr int kScrS = 32 * s_pitch(32) + 16 * s_pitch(16) + 8 * s_pitch(8) + 4 * s_pitch(4);
+constexpr int kScrT = 32 * t_pitch(32) + 16 * t_pitch(16) + 8 * t_pitch(8) + 4 * t_pitch(4);
+// LDS of a workgroup: two operand tiles, or the diagonal block and its
+// inverse with the S and T scratch of every level of the recursion
+constexpr int kLdsDoubles = 2 * kTT + kScrS + kScrT;
 
-// S_h / T_h for half size h (32, 16, 8, 4) inside a scratch set
-__device__ __forceinline__ double* lvl(double* base, int h) {
+// S_h / T_h for half size h (32, 16, 8, 4) inside the S and T scratch sets
+__device__ __forceinline__ double* lvl_s(double* base, int h) {
   return base + (h == 32 ? 0
-                         : (h == 16 ? 32 * 32 : (h == 8 ? 32 * 32 + 16 * 16 : 32 * 32 + 16 * 16 + 8 * 8)));
+                         : (h == 16 ? 32 * s_pitch(32)
+                                    : (h == 8 ? 32 * s_pitch(32) + 16 * s_pitch(16)
+                                              : 32 * s_pitch(32) + 16 * s_pitch(16) +
+                                                    8 * s_pitch(8))));
+}
+__device__ __forceinline__ double* lvl_t(double* base, int h) {
+  return base + (h == 32 ? 0
+                         : (h == 16 ? 32 * t_pitch(32)
+                                    : (h == 8 ? 32 * t_pitch(32) + 16 * t_pitch(16)
+                                              : 32 * t_pitch(32) + 16 * t_pitch(16) +
+                                                    8 * t_pitch(8))));
 }
 
-// One 16 x 16 tile of sum_k fa(r, k) fb(c, k), k < kd (kd a multiple of 4),
-// on the calling wave; fa, fb return the operand entries (0 outside).
-template <class FA, class FB>
-__device__ __forceinline__ d4 mma16(FA fa, FB fb, int kd) {
+// One 16 x 16 tile of sum_k fa(r, k) fb(c, k), k < KD (a multiple of 4),
+// on the calling wave; fa, fb return the operand entries (0 outside).  All
+// operands are read first, so the chain of MFMAs waits for LDS once.
+template <int KD, class FA, class FB>
+__device__ __forceinline__ d4 mma16(FA fa, FB fb) {
   const int lane = threadIdx.x & 63, l16 = lane & 15, lk = lane >> 4;
+  double av[KD / 4], bv[KD / 4];
+#pragma unroll
+  for (int i = 0; i < KD / 4; ++i) {
+    av[i] = fa(l16, 4 * i + lk);
+    bv[i] = fb(l16, 4 * i + lk);
+  }
   d4 acc = d4{0.0, 0.0, 0.0, 0.0};
-  for (int k0 = 0; k0 < kd; k0 += 4) acc = mfma_f64(fa(l16, k0 + lk), fb(l16, k0 + lk), acc);
+#pragma unroll
+  for (int i = 0; i < KD / 4; ++i) acc = mfma_f64(av[i], bv[i], acc);
   return acc;
 }
 
+// The meeting point between two steps of the recursion: a workgroup barrier
+// when all four waves take part (NW = 4), and for one wave alone (NW = 1) a
+// wait for its own LDS operations (they complete in order for one wave; the
+// memory clobber keeps the compiler from moving LDS accesses across it).
+template <int NW>
+__device__ __forceinline__ void step_sync() {
+  if constexpr (NW == 1)
+    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+  else
+    __syncthreads();
+}
+
 // leaf: factor and invert the NL x NL diagonal block at o (updated in place)
-template <int NL>
+template <int NL, int NW>
 __device__ __forceinline__ void leaf(double* A, double* X, int o, int nbk, int64_t k0,
                                      int* status) {
   double D[NL][NL], Xi[NL][NL], rs[NL];
 #pragma unroll
   for (int a = 0; a < NL; ++a)
 #pragma unroll
-    for (int b = 0; b <= a; ++b) D[a][b] = A[(o + a) * kQ + o + b];
+    for (int b = 0; b <= a; ++b) D[a][b] = A[bq(o + a, o + b)];
 #pragma unroll
   for (int a = 0; a < NL; ++a) {
     const double d = D[a][a];
@@ -250,7 +299,7 @@ __device__ __forceinline__ void leaf(double* A, double* X, int o, int nbk, int64
       Xi[a][c] = -rs[a] * v;
     }
   }
-  __syncthreads();   // every wave has read the block before it is overwritten
+  step_sync<NW>();   // every wave has read the block before it is overwritten
   if (threadIdx.x == 0) {
     // one lane stores the NL (NL + 1) / 2 values of each (the entries above the diagonal
     // are zero already)
@@ -258,123 +307,130 @@ __device__ __forceinline__ void leaf(double* A, double* X, int o, int nbk, int64
     for (int a = 0; a < NL; ++a)
 #pragma unroll
       for (int c = 0; c <= a; ++c) {
-        A[(o + a) * kQ + o + c] = D[a][c];
-        X[(o + a) * kQ + o + c] = Xi[a][c];
+        A[bq(o + a, o + c)] = D[a][c];
+        X[bq(o + a, o + c)] = Xi[a][c];
       }
   }
-  __syncthreads();
+  step_sync<NW>();
 }
 
 // S = A21 X11^T, then A22 -= S S^T (lower), A21 <- S and T = S X11, for the
 // halves of size h of the block at o.
-template <int H>
+template <int H, int NW>
 __device__ __forceinline__ void split_step(double* A, double* X, double* scr, int o) {
   constexpr int nt16 = (H + 15) / 16;
-  double* const S = lvl(scr, H);
-  double* const Tm = lvl(scr + kScr, H);
-  const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  for (int t = w; t < nt16 * nt16; t += 4) {
+  constexpr int SP = s_pitch(H), TP = t_pitch(H);
+  double* const S = lvl_s(scr, H);
+  double* const Tm = lvl_t(scr + kScrS, H);
+  const int w = NW == 1 ? 0 : threadIdx.x >> 6, lane = threadIdx.x & 63;
+  for (int t = w; t < nt16 * nt16; t += NW) {
     const int R = t / nt16, C = t % nt16;
-    const d4 v = mma16(
+    const d4 v = mma16<(H < 4 ? 4 : H)>(
         [&](int r, int k) {
           r += 16 * R;
-          return (r < H && k < H) ? A[(o + H + r) * kQ + o + k] : 0.0;
+          return (r < H && k < H) ? A[bq(o + H + r, o + k)] : 0.0;
         },
         [&](int c, int k) {
           c += 16 * C;
-          return (c < H && k < H) ? X[(o + c) * kQ + o + k] : 0.0;
-        },
-        H < 4 ? 4 : H);
+          return (c < H && k <= c) ? X[bq(o + c, o + k)] : 0.0;   // X11 lower
+        });
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
       const int r = 16 * R + 4 * q + (lane >> 4), c = 16 * C + (lane & 15);
-      if (r < H && c < H) S[r * H + c] = v[q];
+      if (r < H && c < H) S[r * SP + c] = v[q];
     }
   }
-  __syncthreads();
+  step_sync<NW>();
   // update tiles (lower) then T tiles, dealt to the waves together
   constexpr int nu = nt16 * (nt16 + 1) / 2;
-  for (int t = w; t < nu + nt16 * nt16; t += 4) {
+  for (int t = w; t < nu + nt16 * nt16; t += NW) {
     if (t < nu) {
       int R = 0, C = t;
       while (C > R) C -= ++R;   // t -> (R, C), C <= R
-      const d4 v = mma16(
+      const d4 v = mma16<(H < 4 ? 4 : H)>(
           [&](int r, int k) {
             r += 16 * R;
-            return (r < H && k < H) ? S[r * H + k] : 0.0;
+            return (r < H && k < H) ? S[r * SP + k] : 0.0;
           },
           [&](int c, int k) {
             c += 16 * C;
-            return (c < H && k < H) ? S[c * H + k] : 0.0;
-          },
-          H < 4 ? 4 : H);
+            return (c < H && k < H) ? S[c * SP + k] : 0.0;
+          });
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
         const int r = 16 * R + 4 * q + (lane >> 4), c = 16 * C + (lane & 15);
-        if (r < H && c <= r) A[(o + H + r) * kQ + o + H + c] -= v[q];
+        if (r < H && c <= r) A[bq(o + H + r, o + H + c)] -= v[q];
       }
     } else {
       const int tt = t - nu, R = tt / nt16, C = tt % nt16;
-      const d4 v = mma16(
+      const d4 v = mma16<(H < 4 ? 4 : H)>(
           [&](int r, int k) {
             r += 16 * R;
-            return (r < H && k < H) ? S[r * H + k] : 0.0;
+            return (r < H && k < H) ? S[r * SP + k] : 0.0;
           },
           [&](int c, int k) {
             c += 16 * C;
-            return (c < H && k < H) ? X[(o + k) * kQ + o + c] : 0.0;
-          },
-          H < 4 ? 4 : H);
+            return (c <= k && k < H) ? X[bq(o + k, o + c)] : 0.0;   // X11 lower
+          });
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
         const int r = 16 * R + 4 * q + (lane >> 4), c = 16 * C + (lane & 15);
-        if (r < H && c < H) Tm[r * H + c] = v[q];
+        if (r < H && c < H) Tm[r * TP + c] = v[q];
       }
     }
   }
-  for (int e = threadIdx.x; e < H * H; e += kThreads)
-    A[(o + H + e / H) * kQ + o + e % H] = S[e];
-  __syncthreads();
+  for (int e = NW == 1 ? lane : threadIdx.x; e < H * H; e += 64 * NW)
+    A[bq(o + H + e / H, o + e % H)] = S[(e / H) * SP + e % H];
+  step_sync<NW>();
 }
 
 // X21 = -X22 T for the halves of size h of the block at o.
-template <int H>
+template <int H, int NW>
 __device__ __forceinline__ void finish_inverse(double* X, double* scr, int o) {
   constexpr int nt16 = (H + 15) / 16;
-  double* const Tm = lvl(scr + kScr, H);
-  const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  for (int t = w; t < nt16 * nt16; t += 4) {
+  constexpr int TP = t_pitch(H);
+  double* const Tm = lvl_t(scr + kScrS, H);
+  const int w = NW == 1 ? 0 : threadIdx.x >> 6, lane = threadIdx.x & 63;
+  for (int t = w; t < nt16 * nt16; t += NW) {
     const int R = t / nt16, C = t % nt16;
-    const d4 v = mma16(
+    const d4 v = mma16<(H < 4 ? 4 : H)>(
         [&](int r, int k) {
           r += 16 * R;
-          return (r < H && k < H) ? X[(o + H + r) * kQ + o + H + k] : 0.0;
+          return (r < H && k <= r) ? X[bq(o + H + r, o + H + k)] : 0.0;   // X22 lower
         },
         [&](int c, int k) {
           c += 16 * C;
-          return (c < H && k < H) ? Tm[k * H + c] : 0.0;
-        },
-        H < 4 ? 4 : H);
+          return (c < H && k < H) ? Tm[k * TP + c] : 0.0;
+        });
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
       const int r = 16 * R + 4 * q + (lane >> 4), c = 16 * C + (lane & 15);
-      if (r < H && c < H) X[(o + H + r) * kQ + o + c] = -v[q];
+      if (r < H && c < H) X[bq(o + H + r, o + c)] = -v[q];
     }
   }
-  __syncthreads();
+  step_sync<NW>();
 }
 
-template <int N>
+// NW waves take part (the caller's: all four, or wave 0 alone).  Blocks of
+// kWaveN and below are done by wave 0 alone, the other waves waiting at one
+// barrier: at that size the products are small, and the steps, no longer
+// separated by workgroup barriers, follow each other at the pace of one
+// wave's LDS and MFMA latency.
+constexpr int kWaveN = 32;
+template <int N, int NW>
 __device__ __forceinline__ void chol_inv(double* A, double* X, double* scr, int o, int nbk,
                                          int64_t k0, int* status) {
-  if constexpr (N == kLeaf) {
-    leaf<kLeaf>(A, X, o, nbk, k0, status);
+  if constexpr (NW > 1 && N <= kWaveN) {
+    if (threadIdx.x < 64) chol_inv<N, 1>(A, X, scr, o, nbk, k0, status);
+    __syncthreads();
+  } else if constexpr (N == kLeaf) {
+    leaf<kLeaf, NW>(A, X, o, nbk, k0, status);
   } else {
     constexpr int H = N / 2;
-    chol_inv<H>(A, X, scr, o, nbk, k0, status);
-    split_step<H>(A, X, scr, o);
-    chol_inv<H>(A, X, scr, o + H, nbk, k0, status);
-    finish_inverse<H>(X, scr, o);
+    chol_inv<H, NW>(A, X, scr, o, nbk, k0, status);
+    split_step<H, NW>(A, X, scr, o);
+    chol_inv<H, NW>(A, X, scr, o + H, nbk, k0, status);
+    finish_inverse<H, NW>(X, scr, o);
   }
 }
 
@@ -527,11 +583,15 @@ __device__ __noinline__ bool diag_task(const DagArgs& a, double* lds, int j, int
   load_acc(acc, a.H, m, c0, c0);
   if (j > 0) {
     if (!update_tiles<true, false>(a, lds, j, j, j - 1, acc, unused, act, sOk)) return false;
-    // L_j,j-1 = T Linv_j-1,j-1^T
-    if (tid == 0) *sOk = wait_flag(Pf + j, err) && wait_flag(F + tri(j - 1, j - 1), err);
+    // L_j,j-1 = T Linv_j-1,j-1^T: the parked T is staged first (it is ready
+    // long before), then L^-1 of tile j - 1, the link of the chain
+    if (tid == 0) *sOk = wait_flag(Pf + j, err);
     __syncthreads();
     if (!*sOk) return false;
     stage(sA, a.H, m, p0, c0, true);   // A(r, k) = T[r][k], parked at (p0 + k, c0 + r)
+    if (tid == 0) *sOk = wait_flag(F + tri(j - 1, j - 1), err);
+    __syncthreads();
+    if (!*sOk) return false;
     stage(sB, a.Linv, m, p0, p0, false);
     __syncthreads();
     d4 out[2][2];
@@ -540,19 +600,24 @@ __device__ __noinline__ bool diag_task(const DagArgs& a, double* lds, int j, int
 #pragma unroll
       for (int y = 0; y < 2; ++y) out[x][y] = d4{0.0, 0.0, 0.0, 0.0};
     tile_mma(out, sA, sB, qa, qb, 1.0);
+    // L_j,j-1 goes out now and is published after this tile's own update
+    // from it: by then the stores have landed, so the release does not wait
     store_acc(out, a.H, m, c0, p0, qa, qb);
-    zero_tile(a.H, m, p0, c0);   // the parked T: the mirrored tile ends zero
     __syncthreads();             // operand reads done
     acc_to_lds(out, sA, false);
-    publish(F + tri(j, j - 1));  // its barrier also completes the LDS writes
-    if (act) tile_mma(acc, sA, sA, qa, qb, -1.0);
     __syncthreads();
+    if (act) tile_mma(acc, sA, sA, qa, qb, -1.0);
+    // published below, by wave 1 while wave 0 factors the first half
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+    __syncthreads();             // also ends the reads of sA
   }
   const int nbk = (int)((m - c0) < kT ? (m - c0) : kT);
-  double* const Ab = lds;                   // [64][kQ] the block, then L
-  double* const Xb = lds + kT * kQ;         // [64][kQ] L^-1
-  double* const scr = lds + 2 * kT * kQ;    // scratch of the recursive factor
-  // the updated block (lower triangle; the identity beyond nbk) and X = 0
+  double* const Ab = lds;                   // the block, then L (layout bq)
+  double* const Xb = lds + kTT;             // L^-1 (layout bq)
+  double* const scr = lds + 2 * kTT;        // scratch of the recursive factor
+  // the updated block (lower triangle; the identity beyond nbk).  X is not
+  // cleared: the recursion writes its lower triangle and reads nothing above
+  // the diagonal of X.
   if (act) {
 #pragma unroll
     for (int x = 0; x < 2; ++x)
@@ -561,24 +626,38 @@ __device__ __noinline__ bool diag_task(const DagArgs& a, double* lds, int j, int
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
           const int r = acc_row(qa, x, q), c = acc_col(qb, y);
-          Ab[r * kQ + c] = (r < nbk && c < nbk) ? (r >= c ? acc[x][y][q] : 0.0)
+          Ab[bq(r, c)] = (r < nbk && c < nbk) ? (r >= c ? acc[x][y][q] : 0.0)
                                                 : (r == c ? 1.0 : 0.0);
         }
   } else {
-    for (int e = tid - 64; e < 32 * 32; e += 64) Ab[(e >> 5) * kQ + 32 + (e & 31)] = 0.0;
+    for (int e = tid - 64; e < 32 * 32; e += 64) Ab[bq(e >> 5, 32 + (e & 31))] = 0.0;
   }
-  for (int e = tid; e < kTT; e += kThreads) Xb[(e >> 6) * kQ + (e & 63)] = 0.0;
   __syncthreads();
-  chol_inv<kT>(Ab, Xb, scr, 0, nbk, c0, a.status);
-  // the factor (zeros above the diagonal) and its inverse
+  // chol_inv<kT, 4> written out at its top level, so that wave 1 publishes
+  // L_j,j-1 while wave 0 factors the first half alone
+  static_assert(kWaveN == kT / 2, "the top level below assumes halves done by one wave");
+  if (tid < 64)
+    chol_inv<kT / 2, 1>(Ab, Xb, scr, 0, nbk, c0, a.status);
+  else if (tid == 64 && j > 0)
+    release_flag(F + tri(j, j - 1));
+  __syncthreads();
+  split_step<kT / 2, 4>(Ab, Xb, scr, 0);
+  if (tid < 64) chol_inv<kT / 2, 1>(Ab, Xb, scr, kT / 2, nbk, c0, a.status);
+  __syncthreads();
+  finish_inverse<kT / 2, 4>(Xb, scr, 0);
+  // L^-1 first, published at once (the next diagonal tile and the tiles
+  // below wait for it), then the factor tile, which no task reads; both with
+  // zeros above the diagonal
   for (int e = tid; e < kTT; e += kThreads) {
     const int r = e >> 6, c = e & 63;
-    if (r < nbk && c < nbk) {
-      a.H[(c0 + r) * m + c0 + c] = (c <= r) ? Ab[r * kQ + c] : 0.0;
-      a.Linv[(c0 + r) * m + c0 + c] = (c <= r) ? Xb[r * kQ + c] : 0.0;
-    }
+    if (r < nbk && c < nbk) a.Linv[(c0 + r) * m + c0 + c] = (c <= r) ? Xb[bq(r, c)] : 0.0;
   }
   publish(F + tri(j, j));
+  for (int e = tid; e < kTT; e += kThreads) {
+    const int r = e >> 6, c = e & 63;
+    if (r < nbk && c < nbk) a.H[(c0 + r) * m + c0 + c] = (c <= r) ? Ab[bq(r, c)] : 0.0;
+  }
+  if (j > 0) zero_tile(a.H, m, p0, c0);   // the parked T: the mirrored tile ends zero
   return true;
 }
 
