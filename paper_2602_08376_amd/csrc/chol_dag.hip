@@ -16,15 +16,20 @@
 // the host, chol_dag_task_list) in which every task follows each task whose
 // tile it reads, and workgroups take list positions from a counter in order,
 // so a task only ever waits for a task that a running workgroup already
-// holds: the launch cannot deadlock however many workgroups are resident.  Each finished tile is
-// published with a flag (agent-scope release after the stores; readers poll
-// it and acquire).  A wait that outlasts kSpinLimit polls (seconds, far above
+// holds, or for a step of the diagonal chain whose own inputs come earlier in
+// the list: the launch cannot deadlock with two or more workgroups resident.
+// Each finished tile is published with a flag (workgroup-scope release by
+// every thread, then one agent-scope release and the flag; readers poll it
+// and acquire).  A wait that outlasts kSpinLimit polls (seconds, far above
 // any real wait) raises a launch-wide error flag, and every workgroup leaves
 // at its next task.
 //
-// The diagonal tile is factored and inverted together by recursive halving
-// (chol_inv below).  The tile just below the diagonal is on the path from one
-// diagonal tile to the next, so the diagonal task forms it too (diag_task).
+// The diagonal tiles form a chain (each needs L^-1 of the one before), run
+// by one task on one workgroup from start to end (chain_task), which keeps
+// L^-1 of the tile before in LDS; the trailing sums of each diagonal tile
+// (dsum_task) and of the tile below it (sub_task) are formed ahead by other
+// workgroups and parked.  Each diagonal tile is factored and inverted
+// together by recursive halving (chol_inv below).
 #include "kernels.h"
 #include "device.h"
 
@@ -43,7 +48,9 @@ constexpr uint32_t kSpinLimit = 1u << 21; // polls of one flag before the launch
 __device__ __forceinline__ int sw(int r, int k) { return r * kT + (k ^ (2 * (r & 15))); }
 
 // Task kinds of the task list (code: kind << 30 | i << 15 | j).
-enum : int { kTaskDiag = 0, kTaskSub = 1, kTaskOff = 2, kTaskInv = 3 };
+// (An off-diagonal code with i == j is the diagonal sums of tile j; the
+// diagonal code is the chain, once.)
+enum : int { kTaskChain = 0, kTaskSub = 1, kTaskOff = 2, kTaskInv = 3 };
 
 struct DagArgs {
   double* H;      // [m, m] damped Gram in, factor L out (lower; upper set to zero)
@@ -216,8 +223,9 @@ __host__ __device__ constexpr int t_pitch(int h) { return h == 32 ? 48 : h; }
 constexpr int kScrS = 32 * s_pitch(32) + 16 * s_pitch(16) + 8 * s_pitch(8) + 4 * s_pitch(4);
 constexpr int kScrT = 32 * t_pitch(32) + 16 * t_pitch(16) + 8 * t_pitch(8) + 4 * t_pitch(4);
 // LDS of a workgroup: two operand tiles, or the diagonal block and its
-// inverse with the S and T scratch of every level of the recursion
-constexpr int kLdsDoubles = 2 * kTT + kScrS + kScrT;
+// inverse with the S and T scratch of every level of the recursion, and (the
+// chain task) L^-1 of the tile before: 122 KB
+constexpr int kLdsDoubles = 2 * kTT + kScrS + kScrT + kTT;
 
 // S_h / T_h for half size h (32, 16, 8, 4) inside the S and T scratch sets
 __device__ __forceinline__ double* lvl_s(double* base, int h) {
@@ -566,98 +574,119 @@ __device__ __noinline__ bool sub_task(const DagArgs& a, double* lds, int j, int*
   return true;
 }
 
-// Diagonal tile j: H_jj - sum_{k<j-1} L_jk L_jk^T; then (j > 0) L_j,j-1
-// from the parked T, its update, and L_jj = chol(.) with its inverse by
-// recursive halving.  Returns false if a wait gave up.
-__device__ __noinline__ bool diag_task(const DagArgs& a, double* lds, int j, int* sOk) {
-  const int tid = threadIdx.x, w = tid >> 6;
-  const int qa = w >> 1, qb = w & 1;
-  const int64_t m = a.m, c0 = (int64_t)kT * j, p0 = c0 - kT;
-  int* const err = a.sync + 1;
-  int* const F = a.sync + 2;
-  int* const Pf = a.sync + 2 + (int64_t)a.nt * (a.nt + 1);
-  double* const sA = lds;
-  double* const sB = lds + kTT;
+// Diagonal sums of tile j >= 2: S_j = H_jj - sum_{k<j-1} L_jk L_jk^T, parked
+// in place in the diagonal tile (lower triangle) with its own flag; the
+// chain task takes it from there.  Returns false if a wait gave up.
+__device__ __noinline__ bool dsum_task(const DagArgs& a, double* lds, int j, int* sOk) {
+  const int w = threadIdx.x >> 6, qa = w >> 1, qb = w & 1;
+  const int64_t m = a.m, c0 = (int64_t)kT * j;
   const bool act = !(qa < qb);   // the quadrant above the diagonal is not needed
   d4 acc[2][2], unused[2][2];
   load_acc(acc, a.H, m, c0, c0);
-  if (j > 0) {
-    if (!update_tiles<true, false>(a, lds, j, j, j - 1, acc, unused, act, sOk)) return false;
-    // L_j,j-1 = T Linv_j-1,j-1^T: the parked T is staged first (it is ready
-    // long before), then L^-1 of tile j - 1, the link of the chain
-    if (tid == 0) *sOk = wait_flag(Pf + j, err);
-    __syncthreads();
-    if (!*sOk) return false;
-    stage(sA, a.H, m, p0, c0, true);   // A(r, k) = T[r][k], parked at (p0 + k, c0 + r)
-    if (tid == 0) *sOk = wait_flag(F + tri(j - 1, j - 1), err);
-    __syncthreads();
-    if (!*sOk) return false;
-    stage(sB, a.Linv, m, p0, p0, false);
-    __syncthreads();
-    d4 out[2][2];
-#pragma unroll
-    for (int x = 0; x < 2; ++x)
-#pragma unroll
-      for (int y = 0; y < 2; ++y) out[x][y] = d4{0.0, 0.0, 0.0, 0.0};
-    tile_mma(out, sA, sB, qa, qb, 1.0);
-    // L_j,j-1 goes out now and is published after this tile's own update
-    // from it: by then the stores have landed, so the release does not wait
-    store_acc(out, a.H, m, c0, p0, qa, qb);
-    __syncthreads();             // operand reads done
-    acc_to_lds(out, sA, false);
-    __syncthreads();
-    if (act) tile_mma(acc, sA, sA, qa, qb, -1.0);
-    // published below, by wave 1 while wave 0 factors the first half
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
-    __syncthreads();             // also ends the reads of sA
-  }
-  const int nbk = (int)((m - c0) < kT ? (m - c0) : kT);
+  if (!update_tiles<true, false>(a, lds, j, j, j - 1, acc, unused, act, sOk)) return false;
+  if (act) store_acc(acc, a.H, m, c0, c0, qa, qb);
+  publish(a.sync + 2 + (int64_t)a.nt * (a.nt + 1) + a.nt + j);
+  return true;
+}
+
+// The chain of diagonal tiles, all of it on one workgroup, which keeps L^-1
+// of the tile before in LDS.  Step j: S_j (parked by its task; H_jj itself
+// for j < 2) and T_j (parked by the sub-diagonal task), then
+//   L_j,j-1 = T_j Linv_j-1,j-1^T,  L_jj, Linv_jj = chol / inverse of
+//   S_j - L_j,j-1 L_j,j-1^T
+// by recursive halving.  L_j,j-1 is published by wave 1 while wave 0
+// factors the first half, Linv_jj by wave 1 while the next step's inputs
+// load; the factor tile itself is read by no task.  Returns false if a wait
+// gave up.
+__device__ __noinline__ bool chain_task(const DagArgs& a, double* lds, int* sOk) {
+  const int tid = threadIdx.x, w = tid >> 6;
+  const int qa = w >> 1, qb = w & 1;
+  const int64_t m = a.m;
+  int* const err = a.sync + 1;
+  int* const F = a.sync + 2;
+  int* const Pf = a.sync + 2 + (int64_t)a.nt * (a.nt + 1);
+  int* const Df = Pf + a.nt;
+  double* const sA = lds;
   double* const Ab = lds;                   // the block, then L (layout bq)
   double* const Xb = lds + kTT;             // L^-1 (layout bq)
   double* const scr = lds + 2 * kTT;        // scratch of the recursive factor
-  // the updated block (lower triangle; the identity beyond nbk).  X is not
-  // cleared: the recursion writes its lower triangle and reads nothing above
-  // the diagonal of X.
-  if (act) {
+  double* const sL = scr + kScrS + kScrT;   // Linv of the tile before (layout sw)
+  const bool act = !(qa < qb);   // the quadrant above the diagonal is not needed
+  for (int j = 0; j < a.nt; ++j) {
+    const int64_t c0 = (int64_t)kT * j, p0 = c0 - kT;
+    if (tid == 0)
+      *sOk = (j < 2 || wait_flag(Df + j, err)) && (j < 1 || wait_flag(Pf + j, err));
+    __syncthreads();
+    if (!*sOk) return false;
+    d4 acc[2][2];
+    load_acc(acc, a.H, m, c0, c0);
+    if (j > 0) {
+      stage(sA, a.H, m, p0, c0, true);   // A(r, k) = T[r][k], parked at (p0 + k, c0 + r)
+      __syncthreads();
+      d4 out[2][2];
 #pragma unroll
-    for (int x = 0; x < 2; ++x)
+      for (int x = 0; x < 2; ++x)
 #pragma unroll
-      for (int y = 0; y < 2; ++y)
+        for (int y = 0; y < 2; ++y) out[x][y] = d4{0.0, 0.0, 0.0, 0.0};
+      tile_mma(out, sA, sL, qa, qb, 1.0);
+      store_acc(out, a.H, m, c0, p0, qa, qb);   // L_j,j-1, published below
+      __syncthreads();             // operand reads done
+      acc_to_lds(out, sA, false);
+      __syncthreads();
+      if (act) tile_mma(acc, sA, sA, qa, qb, -1.0);
+      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+      __syncthreads();             // also ends the reads of sA
+    }
+    const int nbk = (int)((m - c0) < kT ? (m - c0) : kT);
+    // the updated block (lower triangle; the identity beyond nbk).  X is not
+    // cleared: the recursion writes its lower triangle and reads nothing
+    // above the diagonal of X.
+    if (act) {
 #pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          const int r = acc_row(qa, x, q), c = acc_col(qb, y);
-          Ab[bq(r, c)] = (r < nbk && c < nbk) ? (r >= c ? acc[x][y][q] : 0.0)
-                                                : (r == c ? 1.0 : 0.0);
-        }
-  } else {
-    for (int e = tid - 64; e < 32 * 32; e += 64) Ab[bq(e >> 5, 32 + (e & 31))] = 0.0;
+      for (int x = 0; x < 2; ++x)
+#pragma unroll
+        for (int y = 0; y < 2; ++y)
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            const int r = acc_row(qa, x, q), c = acc_col(qb, y);
+            Ab[bq(r, c)] = (r < nbk && c < nbk) ? (r >= c ? acc[x][y][q] : 0.0)
+                                                  : (r == c ? 1.0 : 0.0);
+          }
+    } else {
+      for (int e = tid - 64; e < 32 * 32; e += 64) Ab[bq(e >> 5, 32 + (e & 31))] = 0.0;
+    }
+    __syncthreads();
+    // chol_inv<kT, 4> written out at its top level, so that wave 1 publishes
+    // L_j,j-1 while wave 0 factors the first half alone
+    static_assert(kWaveN == kT / 2, "the top level below assumes halves done by one wave");
+    if (tid < 64)
+      chol_inv<kT / 2, 1>(Ab, Xb, scr, 0, nbk, c0, a.status);
+    else if (tid == 64 && j > 0)
+      release_flag(F + tri(j, j - 1));
+    __syncthreads();
+    split_step<kT / 2, 4>(Ab, Xb, scr, 0);
+    if (tid < 64) chol_inv<kT / 2, 1>(Ab, Xb, scr, kT / 2, nbk, c0, a.status);
+    __syncthreads();
+    finish_inverse<kT / 2, 4>(Xb, scr, 0);
+    // Linv_jj to memory and, for the next step, into sL; both with zeros
+    // above the diagonal and outside the matrix
+    for (int e = tid; e < kTT; e += kThreads) {
+      const int r = e >> 6, c = e & 63;
+      const double v = (r < nbk && c <= r) ? Xb[bq(r, c)] : 0.0;
+      if (r < nbk && c < nbk) a.Linv[(c0 + r) * m + c0 + c] = v;
+      sL[sw(r, c)] = v;
+    }
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+    __syncthreads();
+    // published by wave 1 while the others go on to the next step's inputs
+    if (tid == 64) release_flag(F + tri(j, j));
+    for (int e = tid; e < kTT; e += kThreads) {
+      const int r = e >> 6, c = e & 63;
+      if (r < nbk && c < nbk) a.H[(c0 + r) * m + c0 + c] = (c <= r) ? Ab[bq(r, c)] : 0.0;
+    }
+    if (j > 0) zero_tile(a.H, m, p0, c0);   // the parked T: the mirrored tile ends zero
+    __syncthreads();   // the block is read out before the next step writes LDS
   }
-  __syncthreads();
-  // chol_inv<kT, 4> written out at its top level, so that wave 1 publishes
-  // L_j,j-1 while wave 0 factors the first half alone
-  static_assert(kWaveN == kT / 2, "the top level below assumes halves done by one wave");
-  if (tid < 64)
-    chol_inv<kT / 2, 1>(Ab, Xb, scr, 0, nbk, c0, a.status);
-  else if (tid == 64 && j > 0)
-    release_flag(F + tri(j, j - 1));
-  __syncthreads();
-  split_step<kT / 2, 4>(Ab, Xb, scr, 0);
-  if (tid < 64) chol_inv<kT / 2, 1>(Ab, Xb, scr, kT / 2, nbk, c0, a.status);
-  __syncthreads();
-  finish_inverse<kT / 2, 4>(Xb, scr, 0);
-  // L^-1 first, published at once (the next diagonal tile and the tiles
-  // below wait for it), then the factor tile, which no task reads; both with
-  // zeros above the diagonal
-  for (int e = tid; e < kTT; e += kThreads) {
-    const int r = e >> 6, c = e & 63;
-    if (r < nbk && c < nbk) a.Linv[(c0 + r) * m + c0 + c] = (c <= r) ? Xb[bq(r, c)] : 0.0;
-  }
-  publish(F + tri(j, j));
-  for (int e = tid; e < kTT; e += kThreads) {
-    const int r = e >> 6, c = e & 63;
-    if (r < nbk && c < nbk) a.H[(c0 + r) * m + c0 + c] = (c <= r) ? Ab[bq(r, c)] : 0.0;
-  }
-  if (j > 0) zero_tile(a.H, m, p0, c0);   // the parked T: the mirrored tile ends zero
   return true;
 }
 
@@ -750,9 +779,9 @@ __global__ __launch_bounds__(kThreads, 1) void chol_dag_kernel(DagArgs a) {
               j = (int)(code & 0x7fffu);
     bool ok = true;
     switch (kind) {
-      case kTaskDiag: ok = diag_task(a, lds, j, &sOk); break;
+      case kTaskChain: ok = chain_task(a, lds, &sOk); break;
       case kTaskSub: ok = sub_task(a, lds, i, &sOk); break;
-      case kTaskOff: ok = offdiag_task(a, lds, i, j, &sOk); break;
+      case kTaskOff: ok = i == j ? dsum_task(a, lds, j, &sOk) : offdiag_task(a, lds, i, j, &sOk); break;
       default: ok = inverse_task(a, lds, i, j, &sOk); break;
     }
     if (!ok) continue;
@@ -771,18 +800,20 @@ __global__ __launch_bounds__(256) void fill_int_kernel(int* __restrict__ p, int6
 
 size_t chol_dag_sync_bytes(int64_t m) {
   const int64_t nt = (m + kT - 1) / kT;
-  return (size_t)(2 + nt * (nt + 1) + nt) * sizeof(int);
+  return (size_t)(2 + nt * (nt + 1) + 2 * nt) * sizeof(int);
 }
 
-// The task order.  A diagonal task j reads the tiles (j, k < j - 1), the
-// parked tile (j, j - 1) and the factor of tile j - 1; the parked tile reads
-// (j, k) and (j - 1, k) for k < j - 1, including (j - 1, j - 2), which the
-// diagonal task j - 1 forms.  So the pair for tile j + 2 can follow the tile
-// (j + 2, j), the first tile of column j it needs: column j's list starts
-// with (j + 2, j), the parked tile (j + 2, j + 1) and the diagonal task j + 2,
-// two columns ahead of where a plain column order would put them, so that the
-// diagonal chain, on which every other task waits, is never short of
-// workgroups.  Then the rest of column j, then the inverse tiles of row j.
+// The task order.  The chain comes first.  Its step j reads the diagonal
+// sums of tile j, which read the tiles (j, k < j - 1), and the parked tile
+// (j, j - 1), which reads (j, k) and (j - 1, k) for k < j - 1, including
+// (j - 1, j - 2), which step j - 1 forms.  So the pair for tile j + 2 can
+// follow the tile (j + 2, j), the first tile of column j it needs: column
+// j's list starts with (j + 2, j), the parked tile (j + 2, j + 1) and the
+// diagonal sums of tile j + 2, two columns ahead of where a plain column
+// order would put them, so that the chain, on which every other task waits,
+// never waits for a task not yet taken while the tasks before it wait for
+// the chain: every task listed before step j's inputs needs only steps
+// before j.  Then the rest of column j, then the inverse tiles of row j.
 static void dag_tasks(int64_t m, int64_t inv_span, uint32_t* out, int64_t* count) {
   const int64_t nt = (m + kT - 1) / kT;
   const int64_t span = inv_span / kT;
@@ -791,16 +822,13 @@ static void dag_tasks(int64_t m, int64_t inv_span, uint32_t* out, int64_t* count
     if (out) out[n] = ((uint32_t)kind << 30) | ((uint32_t)i << 15) | (uint32_t)j;
     ++n;
   };
-  put(kTaskDiag, 0, 0);
-  if (nt > 1) {
-    put(kTaskSub, 1, 0);
-    put(kTaskDiag, 1, 1);
-  }
+  put(kTaskChain, 0, 0);
+  if (nt > 1) put(kTaskSub, 1, 0);
   for (int64_t g = 0; g < nt; ++g) {
     if (g + 2 < nt) {
       put(kTaskOff, g + 2, g);
       put(kTaskSub, g + 2, g + 1);
-      put(kTaskDiag, g + 2, g + 2);
+      put(kTaskOff, g + 2, g + 2);   // the diagonal sums of tile g + 2
     }
     for (int64_t i = g + 3; i < nt; ++i) put(kTaskOff, i, g);
     if (span > 0)
@@ -826,7 +854,7 @@ hipError_t cholesky_dag(double* H, int64_t m, int* status, double* Linv, const u
   if (m <= 0) return hipSuccess;
   const int64_t nt = (m + kT - 1) / kT;
   if (nt > 32767) return hipErrorInvalidValue;
-  const int64_t nsync = 2 + nt * (nt + 1) + nt;
+  const int64_t nsync = 2 + nt * (nt + 1) + 2 * nt;
   const int64_t zb = (nsync + 255) / 256;
   fill_int_kernel<<<dim3((unsigned)(zb < 4096 ? zb : 4096)), dim3(256), 0, stream>>>(sync, nsync,
                                                                                      0);

@@ -736,10 +736,11 @@ hipError_t launch_decode_tiles(const double* L, int64_t m, double* F, bool all_t
 // rexp[i]: the exponent e with max_{l >= 32 (i / 32 + 1)} |R_il| < 2^e (0 for
 // an empty or zero row); R_il = L[l][i], read down a column of L, so the 256
 // threads of a workgroup (256 consecutive rows i) read consecutive addresses.
-// blockIdx.y takes one 512-column slice of l; the slices meet in an atomic
-// max over rexp, which starts at kNoExp.
+// blockIdx.y takes one 64-column slice of l (m / 4 workgroups at m = 4096:
+// enough loads in flight to stream L at HBM speed); the slices meet in an
+// atomic max over rexp, which starts at kNoExp.
 constexpr int kNoExp = -100000;
-constexpr int kExpSlice = 512;
+constexpr int kExpSlice = 64;
 __global__ __launch_bounds__(256) void row_exponent_kernel(const double* __restrict__ L,
                                                           int64_t m, int32_t* __restrict__ rexp) {
   const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
@@ -748,6 +749,7 @@ __global__ __launch_bounds__(256) void row_exponent_kernel(const double* __restr
   const int64_t lo = lo0 > s0 ? lo0 : s0;
   const int64_t hi = s0 + kExpSlice < m ? s0 + kExpSlice : m;
   double mx = 0.0;
+#pragma unroll 8
   for (int64_t l = lo; l < hi; ++l) mx = fmax(mx, fabs(L[l * m + i]));
   if (mx > 0.0) {
     int e = 0;
