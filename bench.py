@@ -513,7 +513,8 @@ def main():
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
         print(f"bench.py measures one GPU only (asked for --gpus {args.gpus}, WORLD_SIZE {world}): "
-              "the path runs on a single GPU; sharding over columns is described in DESIGN.md",
+              "the path runs on a single GPU (it would shard over output columns, each GPU "
+              "decoding its own columns against a replicated factor)",
               file=sys.stderr)
         sys.exit(2)
     if args.sweep_k:
