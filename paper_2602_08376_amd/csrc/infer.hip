@@ -18,6 +18,14 @@ namespace ojbkq {
 namespace {
 
 typedef _Float16 h8 __attribute__((ext_vector_type(8)));
+typedef _Float16 h2 __attribute__((ext_vector_type(2)));
+typedef float f2 __attribute__((ext_vector_type(2)));
+
+// Two float32 weights rounded to fp16 together (one packed convert, round to
+// nearest even as for a single one).
+__device__ __forceinline__ h2 to_f16x2(float lo, float hi) {
+  return __builtin_convertvector(f2{lo, hi}, h2);
+}
 typedef float f4 __attribute__((ext_vector_type(4)));
 
 // ---- packing ---------------------------------------------------------------
@@ -89,7 +97,11 @@ __device__ __forceinline__ int64_t x_row(const DqArgs& a, int64_t k) {
 // or 16 of a word and each code sits inside one 64-bit window of two words.
 template <int BITS>
 struct CodeLoader {
-  static constexpr int kWords = (16 * BITS + 16 + 31) / 32 + 1;
+  // 1, 2, 4, 8 bits: the run fills BITS / 2 whole words (half a word for 1
+  // bit); otherwise it starts at bit 0 or 16 and code() reads a word past
+  // the one its last code ends in
+  static constexpr int kWords =
+      16 % BITS == 0 ? (BITS > 2 ? BITS / 2 : 1) : (16 * BITS + 16 + 31) / 32 + 1;
   // a vector, not an array: indexed before unrolling, an array is moved to LDS
   typedef uint32_t Words __attribute__((ext_vector_type(kWords)));
   Words w;
@@ -114,6 +126,20 @@ struct CodeLoader {
     } else {
       const uint64_t pair = ((uint64_t)w[(b >> 5) + 1] << 32) | w[b >> 5];
       return (uint32_t)(pair >> (sh + (b & 31))) & ((1u << BITS) - 1u);
+    }
+  }
+  // code c as a float.  2-, 4- and 8-bit codes sit at fixed places in their
+  // bytes: one shift and mask of a word isolates a code in each of its four
+  // bytes (shared by the codes at the same place), and the byte-to-float
+  // converts take them from there.
+  __device__ __forceinline__ float codef(int c) const {
+    if constexpr (BITS == 2 || BITS == 4 || BITS == 8) {
+      const int b = c * BITS;
+      constexpr uint32_t kMask = BITS == 8 ? 0xffffffffu : BITS == 4 ? 0x0f0f0f0fu : 0x03030303u;
+      const uint32_t y = (w[b >> 5] >> (b & 7)) & kMask;
+      return (float)((y >> (b & 24)) & 0xffu);
+    } else {
+      return (float)code(c);
     }
   }
 };
@@ -255,11 +281,13 @@ __global__ __launch_bounds__(kThreads, 1) void dequant_matmul_kernel(DqArgs a) {
   const int bc = tid & 31, br = tid >> 5;
   typedef uint32_t Runs __attribute__((ext_vector_type(16)));
   Runs xv;
+  const uint16_t* const xv0 = a.X + (int64_t)br * a.ldx + T0 + 8 * bc;
   auto fetch_xv = [&](int64_t k0) {
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
-      const uint4 v = *reinterpret_cast<const uint4*>(a.X + x_row(a, k0 + br + 16 * q) * a.ldx +
-                                                      T0 + 8 * bc);
+      const uint16_t* src = a.perm ? a.X + x_row(a, k0 + br + 16 * q) * a.ldx + T0 + 8 * bc
+                                   : xv0 + (k0 + 16 * q) * a.ldx;
+      const uint4 v = *reinterpret_cast<const uint4*>(src);
       xv[4 * q] = v.x;
       xv[4 * q + 1] = v.y;
       xv[4 * q + 2] = v.z;
@@ -302,16 +330,17 @@ __global__ __launch_bounds__(kThreads, 1) void dequant_matmul_kernel(DqArgs a) {
       *reinterpret_cast<h8*>(B + xoff(r, 8 * bc)) = u;
     }
   };
-  // W_hat = fp16(fp32(s (q - z))) of code c of run h, zero past the last
-  // feature or channel.  Two roundings: the empty asm pins the float32
-  // product in a register, so it is not folded into v_fma_mixlo_f16, which
-  // rounds once to fp16.  q - z in fp32 (exact for the integer zero points a
-  // quantize call gives; a fractional z is honoured as the float it is).
-  auto weight = [&](const CodeLoader<BITS>& l, float sc, float zc, int c, int nvalid) {
-    float p = sc * ((float)l.code(c) - zc);
+  // W_hat = fp16(fp32(s (q - z))): the float32 weight of code c of a run,
+  // with `mask` zero past the last feature or channel (nvalid codes of the
+  // run exist), rounded to fp16 in pairs by to_f16x2.  Two roundings: the
+  // empty asm pins the float32 product in a register, so it is not folded
+  // into v_fma_mixlo_f16, which rounds once to fp16.  q - z in fp32 (exact
+  // for the integer zero points a quantize call gives; a fractional z is
+  // honoured as the float it is).
+  auto weight = [&](const CodeLoader<BITS>& l, float sc, float zc, int c, int nvalid, bool mask) {
+    float p = sc * (l.codef(c) - zc);
     __asm__("" : "+v"(p));
-    const _Float16 w = (_Float16)p;
-    return c < nvalid ? w : (_Float16)0.f;
+    return mask && c >= nvalid ? 0.f : p;
   };
   // how many of the 16 codes of the run at kc exist (all of them on an
   // interior stage): the masks need no branch
@@ -330,10 +359,39 @@ __global__ __launch_bounds__(kThreads, 1) void dequant_matmul_kernel(DqArgs a) {
       for (int e = 0; e < 2; ++e) {
         h8 v;
 #pragma unroll
-        for (int c = 0; c < 8; ++c)
-          v[c] = h ? weight(c1, s1, z1, 8 * e + c, nv1) : weight(c0, s0, z0, 8 * e + c, nv0);
+        for (int c = 0; c < 8; c += 2) {
+          const int k = 8 * e + c;
+          const h2 w2 = h ? to_f16x2(weight(c1, s1, z1, k, nv1, true),
+                                     weight(c1, s1, z1, k + 1, nv1, true))
+                          : to_f16x2(weight(c0, s0, z0, k, nv0, true),
+                                     weight(c0, s0, z0, k + 1, nv0, true));
+          v[c] = w2.x;
+          v[c + 1] = w2.y;
+        }
         *reinterpret_cast<h8*>(sA[buf] + aoff(ar, 4 * ac + 2 * h + e)) = v;
       }
+  };
+
+  // An edge stage dequantized by compute (unmasked): this thread's weights
+  // past the last feature zeroed in place (the activations there are zero,
+  // but a code past the end, dequantized with the row's last group, need not
+  // give a finite weight).  The thread rereads only its own stores.
+  auto mask_tail = [&](int64_t k0, int buf) {
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const int nv = valid(k0 + 32 * ac + 16 * h, false);
+      if (nv < 16) {
+#pragma unroll
+        for (int e = 0; e < 2; ++e) {
+          h8* p = reinterpret_cast<h8*>(sA[buf] + aoff(ar, 4 * ac + 2 * h + e));
+          h8 v = *p;
+#pragma unroll
+          for (int c = 0; c < 8; ++c)
+            if (8 * e + c >= nv) v[c] = (_Float16)0.f;
+          *p = v;
+        }
+      }
+    }
   };
 
   f4 acc[NX][NY];
@@ -348,12 +406,13 @@ __global__ __launch_bounds__(kThreads, 1) void dequant_matmul_kernel(DqArgs a) {
   // (at kn, into buffer `nxt`) is dequantized beside k-step ks: one weight
   // after each product, its 16-byte LDS stores as they fill, the order kept
   // by scheduling barriers so that the vector ALU and the matrix cores work
-  // side by side.
-  auto compute = [&](int cur, int nxt, int64_t kn, bool dq, bool in_n) {
+  // side by side.  No masks: past the last feature mask_tail zeroes the
+  // weights afterwards, and rows past the last channel feed only output rows
+  // that are never stored.
+  auto compute = [&](int cur, int nxt, int64_t kn, bool dq) {
     const _Float16* A = sA[cur];
     const _Float16* B = sB[cur];
     _Float16* An = sA[nxt];
-    const int nv0 = valid(kn + 32 * ac, in_n), nv1 = valid(kn + 32 * ac + 16, in_n);
     // A fragment x of k-step ks: rows 16 (NX wr + x) + i16, features
     // 32 ks + 8 g16 .. + 7
     auto load_a = [&](int ks, int x) {
@@ -373,6 +432,7 @@ __global__ __launch_bounds__(kThreads, 1) void dequant_matmul_kernel(DqArgs a) {
 #pragma unroll
     for (int x = 0; x < NX; ++x) fa[x] = load_a(0, x);
     h8 fb = load_b(0, 0), v;
+    float pe = 0.f;   // the even weight of a pair
 #pragma unroll
     for (int ks = 0; ks < 2; ++ks) {
 #pragma unroll
@@ -391,7 +451,14 @@ __global__ __launch_bounds__(kThreads, 1) void dequant_matmul_kernel(DqArgs a) {
             // (computed on the last stage too, where nothing is stored: no
             // branch around each weight)
             const int c = i >> 1;   // code c of run ks
-            v[c & 7] = ks ? weight(c1, s1, z1, c, nv1) : weight(c0, s0, z0, c, nv0);
+            const float p = ks ? weight(c1, s1, z1, c, 16, false) : weight(c0, s0, z0, c, 16, false);
+            if ((c & 1) == 0) {
+              pe = p;
+            } else {
+              const h2 w2 = to_f16x2(pe, p);
+              v[(c & 7) - 1] = w2.x;
+              v[c & 7] = w2.y;
+            }
             if ((c & 7) == 7 && dq) {
               // the slot computed here, not held in a register all along
               int r = ar;
@@ -459,10 +526,12 @@ __global__ __launch_bounds__(kThreads, 1) void dequant_matmul_kernel(DqArgs a) {
     if constexpr (kPre) {
       if (st + 2 < nst) rows_for(kn + kStage);
     }
-    compute(cur, nxt, kn, more, in_n);
+    compute(cur, nxt, kn, more);
     if (more) {
-      if (!in_n)
+      if (!in_n) {
         stage_x_edge(kn, sB[nxt]);
+        if constexpr (!kPre) mask_tail(kn, nxt);
+      }
       else if constexpr (!kPre)
         store_xv(nxt);
     }
@@ -522,11 +591,13 @@ __global__ __launch_bounds__(256) void dequant_weights_kernel(DqArgs a, _Float16
     for (int h = 0; h < 2; ++h) {
       h8 v;
 #pragma unroll
-      for (int c = 0; c < 8; ++c) {
-        // two roundings, as in the product: the asm keeps the float32 product
-        float p = sc * ((float)l.code(8 * h + c) - zc);
-        __asm__("" : "+v"(p));
-        v[c] = 8 * h + c < nv ? (_Float16)p : (_Float16)0.f;
+      for (int c = 0; c < 8; c += 2) {
+        // two roundings, as in the product: the asm keeps the float32 products
+        float p0 = sc * (l.codef(8 * h + c) - zc), p1 = sc * (l.codef(8 * h + c + 1) - zc);
+        __asm__("" : "+v"(p0), "+v"(p1));
+        const h2 w2 = to_f16x2(8 * h + c < nv ? p0 : 0.f, 8 * h + c + 1 < nv ? p1 : 0.f);
+        v[c] = w2.x;
+        v[c + 1] = w2.y;
       }
       *reinterpret_cast<h8*>(W + j * a.mw + kc + 8 * h) = v;
     }

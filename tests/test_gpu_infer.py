@@ -79,6 +79,29 @@ def test_dequant_matmul_matches_oracle(n, m, T, bits, group):
     assert np.all(err <= bound + 1e-30)
 
 
+@pytest.mark.parametrize("n,m,bits,group", [
+    (70, 200, 4, 32),    # a ragged last stage: a run cut at m, runs wholly past it
+    (33, 96, 8, 16),
+    (50, 160, 1, 32),
+    (40, 192, 3, 64),
+    (300, 100, 2, 0),    # m not a multiple of 16, channels past one tile
+    (64, 256, 6, 128),
+])
+def test_dequant_matmul_identity_gives_w_hat(n, m, bits, group):
+    # X = I: every output element is one weight times 1 plus zeros, so Y is
+    # W_hat itself and both forms of the product must reproduce the oracle's
+    # fp16(fp32(s (q - z))) bit for bit
+    codes, S, Z = _random_quantized(n, m, bits, group, 3 * n + m + bits)
+    P = ok.pack_codes(torch.from_numpy(codes).to(DEV), bits)
+    X16 = torch.eye(m, dtype=torch.float16, device=DEV)
+    args = (P, torch.from_numpy(S).to(DEV), torch.from_numpy(Z).to(DEV), m, bits, group, X16)
+    want = oi.dequantize_fp16(codes, S, Z, group).astype(np.float32)
+    for ws in (True, False):
+        Y = ok.dequant_matmul(*args, workspace=ws)
+        torch.cuda.synchronize()
+        assert np.array_equal(Y.cpu().numpy(), want), f"workspace={ws}"
+
+
 def test_dequant_matmul_workspace_errors():
     codes, S, Z = _random_quantized(40, 96, 4, 32, 5)
     P = ok.pack_codes(torch.from_numpy(codes).to(DEV), 4)
