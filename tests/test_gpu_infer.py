@@ -102,6 +102,31 @@ def test_dequant_matmul_identity_gives_w_hat(n, m, bits, group):
         assert np.array_equal(Y.cpu().numpy(), want), f"workspace={ws}"
 
 
+def test_dequant_matmul_codes_past_the_end_stay_out():
+    # the last group's grid overflows fp16 at code 0 (5000 (0 - 15) = -75000)
+    # while its real codes 13..15 give finite weights: the packing's zero
+    # bits past m, dequantized with that group, would be -inf, and -inf times
+    # a zero activation is NaN.  Both forms must leave them out.
+    n, m, T, bits, group = 40, 100, 64, 4, 32
+    codes, S, Z = _random_quantized(n, m, bits, group, 17)
+    rng = np.random.default_rng(18)
+    codes[:, 96:] = rng.integers(13, 16, size=(n, 4), dtype=np.uint8)
+    S[:, 3] = 5000.0
+    Z[:, 3] = 15.0
+    X16 = rng.standard_normal((m, T)).astype(np.float16)
+    P = ok.pack_codes(torch.from_numpy(codes).to(DEV), bits)
+    args = (P, torch.from_numpy(S).to(DEV), torch.from_numpy(Z).to(DEV), m, bits, group,
+            torch.from_numpy(X16).to(DEV))
+    W16 = oi.dequantize_fp16(codes, S, Z, group)
+    assert np.all(np.isfinite(W16))
+    ref = oi.dequant_matmul(W16, X16)
+    bound = oi.summation_bound(W16, X16)
+    for ws in (True, False):
+        Y = ok.dequant_matmul(*args, workspace=ws).cpu().numpy()
+        assert np.all(np.isfinite(Y)), f"workspace={ws}"
+        assert np.all(np.abs(Y.astype(np.float64) - ref) <= bound + 1e-30), f"workspace={ws}"
+
+
 def test_dequant_matmul_workspace_errors():
     codes, S, Z = _random_quantized(40, 96, 4, 32, 5)
     P = ok.pack_codes(torch.from_numpy(codes).to(DEV), 4)
