@@ -84,17 +84,22 @@ __device__ bool wait_flag(const int* flag, int* err) {
   }
 }
 
-// Every thread completes its tile stores (workgroup-scope release), the
-// workgroup meets, then one thread makes them visible device-wide (an
-// agent-scope release, cumulative over what the barrier ordered before it:
-// the mirror of wait_flag, where one thread acquires and a barrier follows)
-// and sets the flag.  One agent-scope fence per tile instead of one per wave.
+// Every wave waits until its own tile stores have reached the L2
+// (stores_done: a workgroup-scope release alone does not wait for them, as
+// the waves of a workgroup share the L1), the workgroup meets, then one
+// thread writes the L2 back and sets the flag (an agent-scope release, the
+// mirror of wait_flag, where one thread acquires and a barrier follows).
+// One agent-scope fence per tile instead of one per wave.
+__device__ __forceinline__ void stores_done() {
+  __builtin_amdgcn_s_waitcnt(0x0f70);   // vmcnt(0): loads and stores complete
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+}
 __device__ __forceinline__ void release_flag(int* flag) {
   __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
   __hip_atomic_store(flag, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 __device__ __forceinline__ void publish(int* flag) {
-  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+  stores_done();
   __syncthreads();
   if (threadIdx.x == 0) release_flag(flag);
 }
@@ -634,7 +639,7 @@ __device__ __noinline__ bool chain_task(const DagArgs& a, double* lds, int* sOk)
       acc_to_lds(out, sA, false);
       __syncthreads();
       if (act) tile_mma(acc, sA, sA, qa, qb, -1.0);
-      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+      stores_done();               // L_j,j-1 (released by wave 1 below)
       __syncthreads();             // also ends the reads of sA
     }
     const int nbk = (int)((m - c0) < kT ? (m - c0) : kT);
@@ -676,7 +681,7 @@ __device__ __noinline__ bool chain_task(const DagArgs& a, double* lds, int* sOk)
       if (r < nbk && c < nbk) a.Linv[(c0 + r) * m + c0 + c] = v;
       sL[sw(r, c)] = v;
     }
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+    stores_done();
     __syncthreads();
     // published by wave 1 while the others go on to the next step's inputs
     if (tid == 64) release_flag(F + tri(j, j));
