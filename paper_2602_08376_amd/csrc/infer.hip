@@ -283,11 +283,25 @@ __global__ __launch_bounds__(kThreads, 1) void dequant_matmul_kernel(DqArgs a) {
   Runs xv;
   const uint16_t* const xv0 = a.X + (int64_t)br * a.ldx + T0 + 8 * bc;
   auto fetch_xv = [&](int64_t k0) {
+    const uint16_t* src[4];
+    if (a.perm) {
+      // the four entries first, so that their loads overlap (an entry read
+      // where its row is loaded makes each row wait for its own entry)
+      int32_t pr[4];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) pr[q] = a.perm[k0 + br + 16 * q];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int64_t r = pr[q] < 0 ? 0 : (pr[q] >= a.m ? a.m - 1 : pr[q]);
+        src[q] = a.X + r * a.ldx + T0 + 8 * bc;
+      }
+    } else {
+#pragma unroll
+      for (int q = 0; q < 4; ++q) src[q] = xv0 + (k0 + 16 * q) * a.ldx;
+    }
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
-      const uint16_t* src = a.perm ? a.X + x_row(a, k0 + br + 16 * q) * a.ldx + T0 + 8 * bc
-                                   : xv0 + (k0 + 16 * q) * a.ldx;
-      const uint4 v = *reinterpret_cast<const uint4*>(src);
+      const uint4 v = *reinterpret_cast<const uint4*>(src[q]);
       xv[4 * q] = v.x;
       xv[4 * q + 1] = v.y;
       xv[4 * q + 2] = v.z;
