@@ -244,7 +244,7 @@ __global__ __launch_bounds__(kThreads, 1) void dequant_matmul_kernel(DqArgs a) {
   // the stage before it are issued, so that with a permutation its entries
   // arrive a whole step before the rows they address and no activation load
   // waits on them.  (Without kPre the registers are needed for
-  // dequantizing: fetch_xv reads the entries where it uses them.)
+  // dequantizing: fetch_xv reads a stage's four entries together, then the rows.)
   // The entries are kept as read and clamped where used (any arithmetic on
   // them here, or a second definition of the registers on the path without
   // a permutation, would make the compiler wait for the loads at once).
